@@ -1,0 +1,268 @@
+/*
+ * rtcc.h - C ABI of the release-triggered fork-join detector library.
+ *
+ * The library runs the edge-side DNN of release-triggered communication-
+ * computation coupling (RTCC) on one AMD Instinct MI355X (gfx950):
+ *
+ *   per agent k (branch encoder E_k, independent of the other agents):
+ *     pinned host staging -> H2D copy -> pillar cell ids -> counting sort by
+ *     cell -> point-feature net + dense canvas -> 3x3 conv backbone ->
+ *     upsample + concat into agent slot k
+ *   join (all K encoders finished):
+ *     pose warp to the ego frame -> cross-agent fusion (max or attention)
+ *     -> 1x1 detection head -> threshold + box decode -> D2H
+ *
+ * Paper: "Uplink-Completion-Triggered Edge-GPU Inference for Multi-Agent
+ * Cooperative Perception" (arXiv 2608.08330).
+ *   - completion event e_k = Complete(k, a_k)           Sec. IV-B, eq. completion_event
+ *   - branch state machine WAITING->RELEASED->RUNNING->FINISHED
+ *                                                       Sec. IV-C, eq. branch_state
+ *   - validation, ready order (r_k, k), rejection of duplicate, premature,
+ *     malformed or inconsistent events                  Sec. IV-C
+ *   - release certificate r_k = a_k, release causality  eqs. release_certificate,
+ *                                                       release_causality
+ *   - communication-infeasible frame: fusion withheld   Sec. IV-C, Alg. 1
+ *   - fixed agent-indexed feature slots, post-join subgraph after all K
+ *     encoders are FINISHED                             Sec. IV-D
+ *   - pinned staging, async H2D, event-gated encoder    Sec. IV-F
+ *   - Barrier baseline: all encoders released at A = max_k a_k   Sec. V
+ *   - node service times by event timing after warm-up  Sec. IV-A, Sec. V-A1
+ *
+ * Conventions for every call:
+ *   - Every function returns rtcc_status (RTCC_OK == 0) except
+ *     rtcc_destroy, rtcc_status_str and rtcc_last_error.  No C++ exception
+ *     crosses the ABI.  On error, rtcc_last_error(ctx) describes the cause.
+ *   - Pointers named host_* point to host memory, device_* to device memory
+ *     of the context's HIP device.  The library never frees memory it did
+ *     not allocate; pointers it returns stay owned by the context.
+ *   - Times are seconds, as double.  t0 and "now" are CLOCK_MONOTONIC.
+ *   - One context drives one GPU.  Calls on one context are serialised by an
+ *     internal mutex; release calls for different agents may come from
+ *     different threads.
+ */
+#ifndef RTCC_H
+#define RTCC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Only the functions below are exported; the library is built with hidden
+ * default visibility. */
+#if defined(__GNUC__) || defined(__clang__)
+#define RTCC_API __attribute__((visibility("default")))
+#else
+#define RTCC_API
+#endif
+
+#define RTCC_ABI_VERSION 1
+#define RTCC_MAX_AGENTS 16
+#define RTCC_MAX_STAGES 4
+
+typedef enum rtcc_status {
+    RTCC_OK = 0,
+    RTCC_E_ARG = 1,        /* bad argument, inconsistent descriptor, size mismatch */
+    RTCC_E_STATE = 2,      /* call not valid in the current frame state           */
+    RTCC_E_DUPLICATE = 3,  /* second completion event for one agent in a frame    */
+    RTCC_E_MALFORMED = 4,  /* payload or event fails validation                   */
+    RTCC_E_PREMATURE = 5,  /* event claims an arrival time later than now         */
+    RTCC_E_INFEASIBLE = 6, /* join while a branch is undelivered: no fusion runs  */
+    RTCC_E_NOMEM = 7,      /* host or device allocation failed                    */
+    RTCC_E_HIP = 8,        /* HIP runtime error (message in rtcc_last_error)      */
+    RTCC_E_INTERNAL = 9
+} rtcc_status;
+
+typedef enum rtcc_precision { RTCC_PREC_FP32 = 0, RTCC_PREC_BF16 = 1 } rtcc_precision;
+typedef enum rtcc_fusion { RTCC_FUSE_MAX = 0, RTCC_FUSE_ATTN = 1 } rtcc_fusion;
+
+/* Release rule.  RELEASE (RTCC): r_k = a_k, each branch is dispatched by its
+ * own completion event.  BARRIER: events are validated and recorded; the
+ * K-th valid event dispatches all K encoders in (A, k) = index order. */
+typedef enum rtcc_mode { RTCC_MODE_RELEASE = 0, RTCC_MODE_BARRIER = 1 } rtcc_mode;
+
+/* Executor.  PER_BRANCH_STREAMS: one HIP stream per agent plus a join
+ * stream.  SERIAL: one compute stream for every encoder and the post-join
+ * subgraph (the single-stream model of Sec. III-B), plus a copy stream. */
+typedef enum rtcc_exec { RTCC_EXEC_PER_BRANCH_STREAMS = 0, RTCC_EXEC_SERIAL = 1 } rtcc_exec;
+
+typedef enum rtcc_branch_state {
+    RTCC_WAITING = 0,
+    RTCC_RELEASED = 1,
+    RTCC_RUNNING = 2,
+    RTCC_FINISHED = 3
+} rtcc_branch_state;
+
+typedef struct rtcc_stage {
+    int32_t stride;  /* stride of the stage's first 3x3 conv (1 or 2) */
+    int32_t c_out;   /* output channels of every conv of the stage    */
+    int32_t n_convs; /* number of 3x3 convs in the stage (>= 1)       */
+} rtcc_stage;
+
+/* Network and geometry.  Grid: W = round((x_max - x_min) / pillar_size),
+ * H likewise from y.  A point is kept iff x, y, z, r are finite,
+ * x_min <= x < x_max (same for y, z) and its float32 index
+ * floor((x - x_min) / pillar_size) lies in [0, W) (same for y).
+ * Channel counts must be multiples of 32; c_pfn <= 64 * 8. */
+typedef struct rtcc_model_desc {
+    int32_t abi_version;           /* RTCC_ABI_VERSION                          */
+    int32_t n_agents;              /* K, 1..RTCC_MAX_AGENTS; agent 0 is the ego */
+    int64_t max_points;            /* N_max points per agent and frame          */
+    float x_min, x_max, y_min, y_max, z_min, z_max; /* metres                   */
+    float pillar_size;             /* metres                                    */
+    int32_t max_points_per_pillar; /* points of a pillar fed to the PFN (32)    */
+    int32_t c_pfn;                 /* point-feature channels                    */
+    int32_t precision;             /* rtcc_precision                            */
+    int32_t n_stages;              /* 1..RTCC_MAX_STAGES                        */
+    rtcc_stage stages[RTCC_MAX_STAGES];
+    int32_t up_channels;           /* 0: no upsampling (slot = last stage)      */
+    int32_t fusion;                /* rtcc_fusion                               */
+    int32_t n_anchors;             /* must be 2                                 */
+    float anchor_w, anchor_l, anchor_h, anchor_z;
+    float anchor_yaw[2];
+    float score_logit_threshold;   /* keep anchor iff class logit > threshold   */
+} rtcc_model_desc;
+
+typedef struct rtcc_runtime_opts {
+    int32_t exec;          /* rtcc_exec                                              */
+    int32_t use_graphs;    /* 1: replay each branch and the join as a HIP graph      */
+    int32_t node_timing;   /* 1: record HIP events around every node of every frame  */
+    int32_t device;        /* HIP device ordinal                                     */
+    double premature_tol_s;/* an event with arrival_t > now - t0 + tol is premature  */
+} rtcc_runtime_opts;
+
+typedef struct rtcc_detections {
+    int64_t count;            /* number of kept anchors                                 */
+    const float *boxes;       /* [count][7] x, y, z, w, l, h, yaw (ego frame, m / rad)  */
+    const float *scores;      /* [count] sigmoid of the class logit                     */
+    const int32_t *anchor_idx;/* [count] ascending (row * W2 + col) * 2 + anchor        */
+    double t_head_s;          /* raw head outputs on the GPU, seconds since t0          */
+    double t_det_s;           /* detections on the host, seconds since t0               */
+    int32_t n_agents;
+    double arrival_s[RTCC_MAX_AGENTS];  /* a_k as given in the completion events        */
+    double dispatch_s[RTCC_MAX_AGENTS]; /* host time the branch was enqueued, since t0  */
+} rtcc_detections;
+
+typedef enum rtcc_tensor_id {
+    RTCC_T_PILLAR_CELLS = 0,  /* int32 [P] non-empty cells, ascending             (agent) */
+    RTCC_T_PILLAR_COUNTS = 1, /* int32 [P] points per pillar (before the 32 cap)  (agent) */
+    RTCC_T_CANVAS = 2,        /* [H, W, c_pfn] stored dtype                        (agent) */
+    RTCC_T_SLOT = 3,          /* [H2, W2, C] stored dtype, agent slot               (agent) */
+    RTCC_T_FUSED = 4,         /* [H2, W2, C] stored dtype                                   */
+    RTCC_T_HEAD = 5,          /* float32 [H2, W2, 16]                                       */
+    RTCC_T_STAGE_OUT = 6      /* [Hs, Ws, Cs] stored dtype, last conv of stage `agent>>8`,
+                                 agent `agent & 255`                                        */
+} rtcc_tensor_id;
+
+typedef struct rtcc_ctx rtcc_ctx;
+
+/* Create a context: validate the descriptor, convert and upload the
+ * weights, allocate pinned staging, device slots and activations for every
+ * agent (no memory is shared between agents), create streams and events.
+ *
+ * weights: float32, little endian, tensors back to back in this order
+ * (Sec. IV-A: the trained DNN's parameters, here a seeded network):
+ *   pfn_w [4][c_pfn], pfn_b [c_pfn]
+ *   for each stage s, conv l: w [3][3][C_in][C_out] (HWIO), b [C_out]
+ *   if up_channels: for each stage s: w [u][u][C_s][up] with u = product of
+ *     the strides of stages 1..s, b [up]
+ *   head_w [C][16], head_b [16], C = up_channels * n_stages or the last
+ *     stage's channels; the 16 outputs are 2 anchors x (logit, 7 residuals).
+ * The buffer is borrowed for the call only; weights_bytes must equal the
+ * exact size.  bf16 workloads round weight matrices to bfloat16 (RNE);
+ * biases stay float32.  opts may be NULL (defaults: per-branch streams, no
+ * graphs, no node timing, device 0, tolerance 1e-6 s).
+ * Errors: RTCC_E_ARG, RTCC_E_NOMEM, RTCC_E_HIP. */
+RTCC_API rtcc_status rtcc_create(const rtcc_model_desc *model, const void *weights, size_t weights_bytes,
+                        const rtcc_runtime_opts *opts, rtcc_ctx **out);
+
+/* Release everything the context owns.  NULL is a no-op. */
+RTCC_API void rtcc_destroy(rtcc_ctx *ctx);
+
+/* Select the release rule for the following frames.  RTCC_E_STATE inside
+ * a frame (between rtcc_begin_frame and the end of rtcc_join_and_detect). */
+RTCC_API rtcc_status rtcc_set_mode(rtcc_ctx *ctx, rtcc_mode mode);
+
+/* Pinned host buffer [capacity][4] float32 (x, y, z, r) of one agent, owned
+ * by the context and valid until rtcc_destroy.  Branch inputs stay in
+ * pinned host memory until their arrival (Sec. IV-F): fill it before the
+ * completion event and pass it to rtcc_release_branch to avoid a host copy. */
+RTCC_API rtcc_status rtcc_staging_buffer(rtcc_ctx *ctx, int32_t agent, float **pinned, int64_t *capacity);
+
+/* Start a frame: every branch WAITING, outputs cleared, t0 = uplink start. */
+RTCC_API rtcc_status rtcc_begin_frame(rtcc_ctx *ctx, double t0_monotonic_s);
+
+/* Completion event e_k = Complete(agent, arrival_t) (Sec. IV-B/IV-C).
+ *   host_points: [n][4] float32 in the agent's own frame; if it is the
+ *     agent's staging buffer nothing is copied, otherwise it is copied into
+ *     staging before the call returns (the caller keeps ownership).
+ *   pose: agent-to-ego SE(2) (yaw rad, tx m, ty m): p_ego = R(yaw) p + t.
+ *   arrival_t: a_k in seconds since t0.
+ * Checks, in order: E_STATE (no open frame), E_ARG (agent not in [0, K)),
+ * E_DUPLICATE (branch not WAITING), E_MALFORMED (n < 0, n > max_points,
+ * NULL points with n > 0, non-finite pose or arrival, arrival < 0),
+ * E_PREMATURE (now - t0 < arrival_t - tol).  A rejected event leaves the
+ * branch WAITING.  RELEASE mode: enqueue the H2D copy and encoder E_k on
+ * the branch stream and return without waiting.  BARRIER mode: record;
+ * the K-th valid event enqueues all branches. */
+RTCC_API rtcc_status rtcc_release_branch(rtcc_ctx *ctx, int32_t agent, const float *host_points, int64_t n,
+                                const float pose[3], double arrival_t);
+
+/* Same event for an input that is already resident in device memory (the
+ * resident-input runs of Sec. V-B).  device_points [n][4] float32 must stay
+ * valid and unmodified until rtcc_join_and_detect returns, and any writes
+ * to it must be complete (e.g. the producing stream synchronised) before
+ * the call. */
+RTCC_API rtcc_status rtcc_release_branch_device(rtcc_ctx *ctx, int32_t agent, const float *device_points,
+                                       int64_t n, const float pose[3], double arrival_t);
+
+/* Join and detect.  If any branch is still WAITING the frame is
+ * communication-infeasible: RTCC_E_INFEASIBLE, no fusion kernel is
+ * launched and the frame is closed.  Otherwise wait (on the GPU) for every
+ * encoder, run warp, fusion, head and decode, copy the detections to the
+ * host and block until they are there.  out's arrays belong to the
+ * context and stay valid until the next rtcc_begin_frame. */
+RTCC_API rtcc_status rtcc_join_and_detect(rtcc_ctx *ctx, rtcc_detections *out);
+
+/* State of one branch in the current or last frame. */
+RTCC_API rtcc_status rtcc_get_branch_state(rtcc_ctx *ctx, int32_t agent, int32_t *state);
+
+/* Size in bytes of a tensor of the last completed frame (see
+ * rtcc_tensor_id for which take an agent). */
+RTCC_API rtcc_status rtcc_tensor_bytes(rtcc_ctx *ctx, int32_t id, int32_t agent, size_t *bytes);
+
+/* Copy a tensor of the last completed frame to host memory dst of exactly
+ * rtcc_tensor_bytes bytes (E_ARG otherwise).  Blocks until copied. */
+RTCC_API rtcc_status rtcc_get_tensor(rtcc_ctx *ctx, int32_t id, int32_t agent, void *dst, size_t bytes);
+
+/* Node service times c_v (Sec. IV-A): re-run the last completed frame's
+ * work node by node on one stream, `warmup` untimed passes then `reps`
+ * timed passes, and write the median of each node in ms.  Nodes: E_0 ..
+ * E_{K-1} (encoder without the H2D copy), then the post-join subgraph
+ * (warp + fusion + head + decode).  *n_nodes is K + 1; median_ms must hold
+ * RTCC_MAX_AGENTS + 1 floats. */
+RTCC_API rtcc_status rtcc_profile_nodes(rtcc_ctx *ctx, int32_t warmup, int32_t reps, float *median_ms,
+                               int32_t *n_nodes);
+
+/* Per-kernel-group GPU durations (ms) of the last frame, recorded when
+ * opts.node_timing = 1.  For each agent k, in order: h2d, pillar (cell ids,
+ * counting sort, segment), pfn_canvas, conv[0 .. L-1], up[0 .. S-1] (0 if
+ * no upsampling); then warp_fuse, head, decode.  *n = number written;
+ * ms must hold at least rtcc_node_count() floats. */
+RTCC_API rtcc_status rtcc_node_times(rtcc_ctx *ctx, float *ms, int32_t *n);
+RTCC_API rtcc_status rtcc_node_count(rtcc_ctx *ctx, int32_t *n);
+
+/* Name of a status code. */
+RTCC_API const char *rtcc_status_str(rtcc_status s);
+
+/* Message of the last failed call on ctx; with ctx == NULL, the message of
+ * the last failed rtcc_create on the calling thread. */
+RTCC_API const char *rtcc_last_error(const rtcc_ctx *ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RTCC_H */

@@ -1,0 +1,136 @@
+// extern "C" entry points of include/rtcc.h.  Argument marshalling onto the
+// controller; no computation happens here.
+#include <new>
+#include <string>
+
+#include "controller.hpp"
+
+struct rtcc_ctx {
+    rtcc::Controller ctl;
+    explicit rtcc_ctx(rtcc::Executor *ex) : ctl(ex) {}
+};
+
+namespace {
+// Message of the last failed rtcc_create on this thread (no context exists
+// to hold it); rtcc_last_error(NULL) returns it.
+thread_local std::string t_create_error;
+
+template <class F>
+rtcc_status guarded(F &&f) {
+    try {
+        return f();
+    } catch (const std::bad_alloc &) {
+        return RTCC_E_NOMEM;
+    } catch (...) {
+        return RTCC_E_INTERNAL;
+    }
+}
+}  // namespace
+
+extern "C" {
+
+rtcc_status rtcc_create(const rtcc_model_desc *model, const void *weights, size_t weights_bytes,
+                        const rtcc_runtime_opts *opts, rtcc_ctx **out) {
+    if (!out) return RTCC_E_ARG;
+    *out = nullptr;
+    rtcc_ctx *ctx = nullptr;
+    rtcc_status s = guarded([&] {
+        ctx = new rtcc_ctx(rtcc::make_executor());
+        return ctx->ctl.create(model, weights, weights_bytes, opts);
+    });
+    if (s != RTCC_OK) {
+        if (ctx) t_create_error = ctx->ctl.last_error();
+        delete ctx;
+        return s;
+    }
+    *out = ctx;
+    return RTCC_OK;
+}
+
+void rtcc_destroy(rtcc_ctx *ctx) { delete ctx; }
+
+rtcc_status rtcc_set_mode(rtcc_ctx *ctx, rtcc_mode mode) {
+    if (!ctx) return RTCC_E_ARG;
+    return guarded([&] { return ctx->ctl.set_mode(int(mode)); });
+}
+
+rtcc_status rtcc_staging_buffer(rtcc_ctx *ctx, int32_t agent, float **pinned, int64_t *capacity) {
+    if (!ctx) return RTCC_E_ARG;
+    return guarded([&] { return ctx->ctl.staging(agent, pinned, capacity); });
+}
+
+rtcc_status rtcc_begin_frame(rtcc_ctx *ctx, double t0_monotonic_s) {
+    if (!ctx) return RTCC_E_ARG;
+    return guarded([&] { return ctx->ctl.begin_frame(t0_monotonic_s); });
+}
+
+rtcc_status rtcc_release_branch(rtcc_ctx *ctx, int32_t agent, const float *host_points, int64_t n,
+                                const float pose[3], double arrival_t) {
+    if (!ctx) return RTCC_E_ARG;
+    return guarded([&] { return ctx->ctl.release(agent, host_points, n, pose, arrival_t, false); });
+}
+
+rtcc_status rtcc_release_branch_device(rtcc_ctx *ctx, int32_t agent, const float *device_points,
+                                       int64_t n, const float pose[3], double arrival_t) {
+    if (!ctx) return RTCC_E_ARG;
+    return guarded([&] { return ctx->ctl.release(agent, device_points, n, pose, arrival_t, true); });
+}
+
+rtcc_status rtcc_join_and_detect(rtcc_ctx *ctx, rtcc_detections *out) {
+    if (!ctx) return RTCC_E_ARG;
+    return guarded([&] { return ctx->ctl.join(out); });
+}
+
+rtcc_status rtcc_get_branch_state(rtcc_ctx *ctx, int32_t agent, int32_t *state) {
+    if (!ctx) return RTCC_E_ARG;
+    return guarded([&] { return ctx->ctl.branch_state(agent, state); });
+}
+
+rtcc_status rtcc_tensor_bytes(rtcc_ctx *ctx, int32_t id, int32_t agent, size_t *bytes) {
+    if (!ctx) return RTCC_E_ARG;
+    return guarded([&] { return ctx->ctl.tensor_bytes(id, agent, bytes); });
+}
+
+rtcc_status rtcc_get_tensor(rtcc_ctx *ctx, int32_t id, int32_t agent, void *dst, size_t bytes) {
+    if (!ctx) return RTCC_E_ARG;
+    return guarded([&] { return ctx->ctl.get_tensor(id, agent, dst, bytes); });
+}
+
+rtcc_status rtcc_profile_nodes(rtcc_ctx *ctx, int32_t warmup, int32_t reps, float *median_ms,
+                               int32_t *n_nodes) {
+    if (!ctx) return RTCC_E_ARG;
+    return guarded([&] { return ctx->ctl.profile_nodes(warmup, reps, median_ms, n_nodes); });
+}
+
+rtcc_status rtcc_node_times(rtcc_ctx *ctx, float *ms, int32_t *n) {
+    if (!ctx) return RTCC_E_ARG;
+    return guarded([&] { return ctx->ctl.node_times(ms, n); });
+}
+
+rtcc_status rtcc_node_count(rtcc_ctx *ctx, int32_t *n) {
+    if (!ctx) return RTCC_E_ARG;
+    return guarded([&] { return ctx->ctl.node_count(n); });
+}
+
+const char *rtcc_status_str(rtcc_status s) {
+    switch (s) {
+        case RTCC_OK: return "RTCC_OK";
+        case RTCC_E_ARG: return "RTCC_E_ARG";
+        case RTCC_E_STATE: return "RTCC_E_STATE";
+        case RTCC_E_DUPLICATE: return "RTCC_E_DUPLICATE";
+        case RTCC_E_MALFORMED: return "RTCC_E_MALFORMED";
+        case RTCC_E_PREMATURE: return "RTCC_E_PREMATURE";
+        case RTCC_E_INFEASIBLE: return "RTCC_E_INFEASIBLE";
+        case RTCC_E_NOMEM: return "RTCC_E_NOMEM";
+        case RTCC_E_HIP: return "RTCC_E_HIP";
+        case RTCC_E_INTERNAL: return "RTCC_E_INTERNAL";
+    }
+    return "RTCC_E_UNKNOWN";
+}
+
+const char *rtcc_last_error(const rtcc_ctx *ctx) {
+    if (!ctx) return t_create_error.c_str();
+    return ctx->ctl.last_error();
+}
+
+}  // extern "C"

@@ -1,0 +1,102 @@
+// RTCC release controller (Sec. IV-C) and the executor interface it drives.
+//
+// The controller owns the per-branch state z_k in {WAITING, RELEASED,
+// RUNNING, FINISHED}, validates completion events, applies the release rule
+// (RTCC: dispatch at the event; Barrier: dispatch all K at the K-th event in
+// (A, k) order) and withholds the post-join subgraph of an infeasible frame.
+// It is host-only C++ and is unit-tested against a recording executor.
+#pragma once
+
+#include <array>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/rtcc.h"
+#include "model.hpp"
+
+namespace rtcc {
+
+// What the controller asks of an executor.  All calls come with the
+// controller's mutex held.
+class Executor {
+  public:
+    virtual ~Executor() = default;
+    virtual rtcc_status init(const Plan &p, const HostWeights &w, const rtcc_runtime_opts &o,
+                             std::string &err) = 0;
+    virtual float *staging(int agent) = 0;
+    virtual rtcc_status begin_frame(std::string &err) = 0;
+    // Enqueue H2D (unless device_src) and encoder E_agent.
+    virtual rtcc_status dispatch(int agent, const float *pts, int64_t n, bool device_src,
+                                 std::string &err) = 0;
+    // Wait for all encoders on the device, run the post-join subgraph with
+    // the given per-agent warp affines, copy detections to the host.  Fills
+    // out->count / boxes / scores / anchor_idx / t_head_s (relative to the
+    // host time t_begin at which begin_frame was called).
+    virtual rtcc_status join(const std::vector<std::array<float, 6>> &affine, double t_begin,
+                             rtcc_detections *out, std::string &err) = 0;
+    virtual rtcc_status tensor_bytes(int id, int agent, size_t *bytes, std::string &err) = 0;
+    virtual rtcc_status get_tensor(int id, int agent, void *dst, size_t bytes, std::string &err) = 0;
+    virtual rtcc_status profile_nodes(int warmup, int reps, float *median_ms, int *n_nodes,
+                                      std::string &err) = 0;
+    virtual int node_count() const = 0;
+    virtual rtcc_status node_times(float *ms, int *n, std::string &err) = 0;
+};
+
+// Defined by exactly one executor translation unit of a build.
+Executor *make_executor();
+
+struct Pending {
+    int agent;
+    double arrival;
+    const float *pts;
+    int64_t n;
+    bool device_src;
+};
+
+class Controller {
+  public:
+    explicit Controller(Executor *ex) : ex_(ex) {}
+    ~Controller() { delete ex_; }
+
+    rtcc_status create(const rtcc_model_desc *d, const void *weights, size_t bytes,
+                       const rtcc_runtime_opts *opts);
+    rtcc_status set_mode(int mode);
+    rtcc_status staging(int agent, float **ptr, int64_t *cap);
+    rtcc_status begin_frame(double t0);
+    rtcc_status release(int agent, const float *pts, int64_t n, const float pose[3], double arrival,
+                        bool device_src);
+    rtcc_status join(rtcc_detections *out);
+    rtcc_status branch_state(int agent, int32_t *state);
+    rtcc_status tensor_bytes(int id, int agent, size_t *bytes);
+    rtcc_status get_tensor(int id, int agent, void *dst, size_t bytes);
+    rtcc_status profile_nodes(int warmup, int reps, float *median_ms, int32_t *n_nodes);
+    rtcc_status node_times(float *ms, int32_t *n);
+    rtcc_status node_count(int32_t *n);
+
+    const char *last_error() const { return err_.c_str(); }
+
+  private:
+    rtcc_status fail(rtcc_status s, const std::string &msg) {
+        err_ = msg;
+        return s;
+    }
+    rtcc_status dispatch_locked(int agent, const float *pts, int64_t n, bool device_src);
+
+    std::mutex mu_;
+    Executor *ex_;
+    Plan plan_;
+    rtcc_runtime_opts opts_{};
+    bool created_ = false;
+    int mode_ = RTCC_MODE_RELEASE;
+    bool in_frame_ = false;
+    bool have_output_ = false;
+    double t0_ = 0.0, t_begin_ = 0.0;
+    std::vector<int> z_;
+    std::vector<double> arrival_, dispatch_;
+    std::vector<std::array<float, 6>> affine_;
+    std::vector<Pending> pending_;
+    std::string err_;
+};
+
+}  // namespace rtcc

@@ -1,0 +1,541 @@
+// HIP executor: per-agent device buffers, pinned staging, branch streams and
+// events, the post-join subgraph, tensor readback and node timing.
+//
+// Physical release path (Sec. IV-F): a branch input stays in pinned host
+// memory until its completion event; the event triggers an async H2D copy,
+// and the encoder kernels are ordered after the copy on the GPU (same
+// stream, or in SERIAL mode a copy stream + HIP event + wait on the single
+// compute stream).  Each encoder writes only its own agent-indexed buffers
+// and slot (Sec. IV-D), so branches never share memory and may overlap.  The
+// join waits on every branch's completion event on the GPU (no host wait)
+// before the post-join kernels run.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <array>
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "controller.hpp"
+#include "kernels/kernels.hpp"
+
+namespace rtcc {
+
+namespace {
+
+#define HIP_TRY(expr)                                                                   \
+    do {                                                                                \
+        hipError_t e_ = (expr);                                                         \
+        if (e_ != hipSuccess) {                                                         \
+            err = std::string(#expr) + " failed: " + hipGetErrorString(e_);             \
+            return e_ == hipErrorOutOfMemory ? RTCC_E_NOMEM : RTCC_E_HIP;               \
+        }                                                                               \
+    } while (0)
+
+size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
+
+}  // namespace
+
+class HipExecutor : public Executor {
+  public:
+    ~HipExecutor() override { release_all(); }
+
+    rtcc_status init(const Plan &p, const HostWeights &w, const rtcc_runtime_opts &o,
+                     std::string &err) override {
+        p_ = p;
+        o_ = o;
+        dev_ = o.device;
+        HIP_TRY(hipSetDevice(dev_));
+        // Device arena per agent and for the post-join subgraph.  Nothing is
+        // shared between agents.
+        const size_t n_max = size_t(p.n_max);
+        const size_t n_cells = size_t(p.H) * p.W;
+        const size_t n_tiles = (n_cells + kern::kScanTile - 1) / kern::kScanTile;
+        const size_t over_cap = n_max / size_t(p.d.max_points_per_pillar + 1) + 1;
+        br_.resize(p.K);
+        for (int k = 0; k < p.K; ++k) {
+            Branch &b = br_[k];
+            HIP_TRY(hipHostMalloc(reinterpret_cast<void **>(&b.staging), n_max * 16, hipHostMallocDefault));
+            HIP_TRY(alloc(&b.d_pts, n_max * 16));
+            HIP_TRY(alloc(&b.d_cell, n_max * 4));
+            HIP_TRY(alloc(&b.d_slot, n_max * 4));
+            HIP_TRY(alloc(&b.d_member, n_max * 4));
+            HIP_TRY(alloc(&b.d_pcells, n_max * 4));
+            HIP_TRY(alloc(&b.d_pcounts, n_max * 4));
+            HIP_TRY(alloc(&b.d_overfull, over_cap * 4));
+            HIP_TRY(alloc(&b.d_counts, n_cells * 4));
+            HIP_TRY(alloc(&b.d_offsets, n_cells * 4));
+            HIP_TRY(alloc(&b.d_tiles, n_tiles * 8));
+            HIP_TRY(alloc(&b.d_meta, 64));
+            HIP_TRY(alloc(&b.d_canvas, n_cells * p.c_pfn * p.elt));
+            b.d_act.resize(p.convs.size());
+            for (size_t l = 0; l < p.convs.size(); ++l) {
+                const ConvLayer &c = p.convs[l];
+                HIP_TRY(alloc(&b.d_act[l], size_t(c.Ho) * c.Wo * c.Co * p.elt));
+            }
+            if (!p.ups.empty()) HIP_TRY(alloc(&b.d_slotbuf, size_t(p.H2) * p.W2 * p.c_slot * p.elt));
+            else b.d_slotbuf = b.d_act.back();
+            HIP_TRY(hipStreamCreateWithFlags(&b.stream, hipStreamNonBlocking));
+            HIP_TRY(hipEventCreateWithFlags(&b.done, hipEventDisableTiming));
+            HIP_TRY(hipEventCreateWithFlags(&b.h2d_done, hipEventDisableTiming));
+            b.ev.resize(4 + p.convs.size() + p.ups.size());
+            for (auto &e : b.ev) HIP_TRY(hipEventCreate(&e));
+        }
+        HIP_TRY(alloc(&d_fused, size_t(p.H2) * p.W2 * p.c_slot * p.elt));
+        HIP_TRY(alloc(&d_head, size_t(p.H2) * p.W2 * 16 * 4));
+        n_anchor_ = size_t(p.H2) * p.W2 * 2;
+        const size_t dec_tiles = (n_anchor_ + kern::kDecodeTile - 1) / kern::kDecodeTile;
+        HIP_TRY(alloc(&d_dec_tiles, (dec_tiles + 1) * 4));
+        HIP_TRY(alloc(&d_rec, n_anchor_ * 9 * 4));
+        HIP_TRY(alloc(&d_count, 64));
+        HIP_TRY(hipHostMalloc(reinterpret_cast<void **>(&h_rec), n_anchor_ * 9 * 4, hipHostMallocDefault));
+        HIP_TRY(hipHostMalloc(reinterpret_cast<void **>(&h_small), 64, hipHostMallocDefault));
+        boxes_.resize(n_anchor_ * 7);
+        scores_.resize(n_anchor_);
+        aidx_.resize(n_anchor_);
+        HIP_TRY(hipStreamCreateWithFlags(&join_stream_, hipStreamNonBlocking));
+        HIP_TRY(hipStreamCreateWithFlags(&copy_stream_, hipStreamNonBlocking));
+        HIP_TRY(hipStreamCreateWithFlags(&aux_stream_, hipStreamNonBlocking));
+        HIP_TRY(hipEventCreate(&ev_frame0_));
+        HIP_TRY(hipEventCreate(&ev_head_));
+        for (auto &e : post_ev_) HIP_TRY(hipEventCreate(&e));
+
+        // Weights: matrices in the compute dtype, biases and PFN float32.
+        const size_t mat_bytes = p.mat_elems * p.elt;
+        HIP_TRY(alloc(&d_mat, mat_bytes));
+        HIP_TRY(alloc(&d_bias, p.bias_floats * 4));
+        const void *mat_src = p.bf16 ? static_cast<const void *>(w.mat_bf16.data())
+                                     : static_cast<const void *>(w.mat_f32.data());
+        HIP_TRY(hipMemcpy(d_mat, mat_src, mat_bytes, hipMemcpyHostToDevice));
+        HIP_TRY(hipMemcpy(d_bias, w.bias.data(), p.bias_floats * 4, hipMemcpyHostToDevice));
+        HIP_TRY(hipDeviceSynchronize());
+        return RTCC_OK;
+    }
+
+    float *staging(int agent) override { return br_[agent].staging; }
+
+    rtcc_status begin_frame(std::string &err) override {
+        HIP_TRY(hipSetDevice(dev_));
+        // Work of an abandoned (infeasible) frame may still be running and
+        // reading the staging buffers that the caller is about to refill.
+        for (Branch &b : br_) HIP_TRY(hipStreamSynchronize(b.stream));
+        HIP_TRY(hipStreamSynchronize(copy_stream_));
+        HIP_TRY(hipStreamSynchronize(join_stream_));
+        HIP_TRY(hipEventRecord(ev_frame0_, compute_stream_for_join()));
+        for (Branch &b : br_) b.dispatched = false;
+        return RTCC_OK;
+    }
+
+    rtcc_status dispatch(int agent, const float *pts, int64_t n, bool device_src,
+                         std::string &err) override {
+        HIP_TRY(hipSetDevice(dev_));
+        Branch &b = br_[agent];
+        const bool serial = o_.exec == RTCC_EXEC_SERIAL;
+        hipStream_t cs = serial ? join_stream_ : b.stream;
+        const bool timing = o_.node_timing != 0;
+        if (timing) HIP_TRY(hipEventRecord(b.ev[0], cs));
+        const float *src = pts;
+        if (!device_src) {
+            src = static_cast<const float *>(b.d_pts);
+            if (n > 0) {
+                if (serial) {
+                    // dedicated transfer stream, event, compute stream waits
+                    HIP_TRY(hipMemcpyAsync(b.d_pts, b.staging, size_t(n) * 16, hipMemcpyHostToDevice, copy_stream_));
+                    HIP_TRY(hipEventRecord(b.h2d_done, copy_stream_));
+                    HIP_TRY(hipStreamWaitEvent(cs, b.h2d_done, 0));
+                } else {
+                    HIP_TRY(hipMemcpyAsync(b.d_pts, b.staging, size_t(n) * 16, hipMemcpyHostToDevice, cs));
+                }
+            }
+        }
+        b.src = src;
+        b.n = int32_t(n);
+        b.host_input = !device_src;
+        rtcc_status s = enqueue_encoder(b, cs, timing, 1, err);
+        if (s != RTCC_OK) return s;
+        HIP_TRY(hipEventRecord(b.done, cs));
+        b.dispatched = true;
+        return RTCC_OK;
+    }
+
+    rtcc_status join(const std::vector<std::array<float, 6>> &affine, double t_begin,
+                     rtcc_detections *out, std::string &err) override {
+        HIP_TRY(hipSetDevice(dev_));
+        hipStream_t js = compute_stream_for_join();
+        for (Branch &b : br_) HIP_TRY(hipStreamWaitEvent(js, b.done, 0));
+        const bool timing = o_.node_timing != 0;
+        if (timing) HIP_TRY(hipEventRecord(post_ev_[0], js));
+        rtcc_status s = enqueue_post(affine, js, timing, err);
+        if (s != RTCC_OK) return s;
+        HIP_TRY(hipMemcpyAsync(h_small, d_count, 4, hipMemcpyDeviceToHost, js));
+        HIP_TRY(hipStreamSynchronize(js));
+        const int64_t count = *reinterpret_cast<int32_t *>(h_small);
+        if (count < 0 || size_t(count) > n_anchor_) {
+            err = "decode produced an out-of-range count";
+            return RTCC_E_INTERNAL;
+        }
+        if (count > 0) {
+            HIP_TRY(hipMemcpyAsync(h_rec, d_rec, size_t(count) * 36, hipMemcpyDeviceToHost, js));
+            HIP_TRY(hipStreamSynchronize(js));
+        }
+        for (int64_t i = 0; i < count; ++i) {
+            const float *r = h_rec + i * 9;
+            std::memcpy(&boxes_[i * 7], r, 7 * sizeof(float));
+            scores_[i] = r[7];
+            std::memcpy(&aidx_[i], &r[8], 4);
+        }
+        float ms = 0.f;
+        HIP_TRY(hipEventElapsedTime(&ms, ev_frame0_, ev_head_));
+        out->count = count;
+        out->boxes = boxes_.data();
+        out->scores = scores_.data();
+        out->anchor_idx = aidx_.data();
+        out->t_head_s = t_begin + 1e-3 * double(ms);
+        last_affine_ = affine;
+        return RTCC_OK;
+    }
+
+    rtcc_status tensor_bytes(int id, int agent, size_t *bytes, std::string &err) override {
+        void *ptr = nullptr;
+        return locate(id, agent, &ptr, bytes, err);
+    }
+
+    rtcc_status get_tensor(int id, int agent, void *dst, size_t bytes, std::string &err) override {
+        void *ptr = nullptr;
+        size_t need = 0;
+        rtcc_status s = locate(id, agent, &ptr, &need, err);
+        if (s != RTCC_OK) return s;
+        if (bytes != need) {
+            err = "destination size " + std::to_string(bytes) + " != tensor size " + std::to_string(need);
+            return RTCC_E_ARG;
+        }
+        if (need == 0) return RTCC_OK;
+        HIP_TRY(hipMemcpyAsync(dst, ptr, need, hipMemcpyDeviceToHost, aux_stream_));
+        HIP_TRY(hipStreamSynchronize(aux_stream_));
+        return RTCC_OK;
+    }
+
+    rtcc_status profile_nodes(int warmup, int reps, float *median_ms, int *n_nodes,
+                              std::string &err) override {
+        HIP_TRY(hipSetDevice(dev_));
+        for (const Branch &b : br_)
+            if (!b.host_input) {
+                err = "profiling replays a frame released from host memory";
+                return RTCC_E_STATE;
+            }
+        hipStream_t s = join_stream_;
+        hipEvent_t e0, e1;
+        HIP_TRY(hipEventCreate(&e0));
+        HIP_TRY(hipEventCreate(&e1));
+        std::vector<std::vector<float>> t(p_.K + 1);
+        for (int r = 0; r < warmup + reps; ++r) {
+            for (int k = 0; k <= p_.K; ++k) {
+                HIP_TRY(hipEventRecord(e0, s));
+                rtcc_status st = k < p_.K ? enqueue_encoder(br_[k], s, false, 0, err)
+                                          : enqueue_post(last_affine_, s, false, err);
+                if (st != RTCC_OK) return st;
+                HIP_TRY(hipEventRecord(e1, s));
+                HIP_TRY(hipEventSynchronize(e1));
+                float ms = 0.f;
+                HIP_TRY(hipEventElapsedTime(&ms, e0, e1));
+                if (r >= warmup) t[k].push_back(ms);
+            }
+        }
+        HIP_TRY(hipEventDestroy(e0));
+        HIP_TRY(hipEventDestroy(e1));
+        for (int k = 0; k <= p_.K; ++k) {
+            std::vector<float> &v = t[k];
+            std::sort(v.begin(), v.end());
+            const size_t h = v.size() / 2;
+            median_ms[k] = v.size() % 2 ? v[h] : 0.5f * (v[h - 1] + v[h]);
+        }
+        *n_nodes = p_.K + 1;
+        return RTCC_OK;
+    }
+
+    int node_count() const override {
+        return p_.K * int(3 + p_.convs.size() + (p_.ups.empty() ? 1 : p_.ups.size())) + 3;
+    }
+
+    rtcc_status node_times(float *ms, int *n, std::string &err) override {
+        int q = 0;
+        for (const Branch &b : br_) {
+            for (size_t e = 0; e + 1 < b.ev.size(); ++e) {
+                float v = 0.f;
+                HIP_TRY(hipEventElapsedTime(&v, b.ev[e], b.ev[e + 1]));
+                ms[q++] = v;
+            }
+            if (p_.ups.empty()) ms[q++] = 0.f;
+        }
+        for (int e = 0; e < 3; ++e) {
+            float v = 0.f;
+            HIP_TRY(hipEventElapsedTime(&v, post_ev_[e], post_ev_[e + 1]));
+            ms[q++] = v;
+        }
+        *n = q;
+        return RTCC_OK;
+    }
+
+  private:
+    struct Branch {
+        float *staging = nullptr;
+        void *d_pts = nullptr, *d_cell = nullptr, *d_slot = nullptr, *d_member = nullptr;
+        void *d_pcells = nullptr, *d_pcounts = nullptr, *d_overfull = nullptr;
+        void *d_counts = nullptr, *d_offsets = nullptr, *d_tiles = nullptr, *d_meta = nullptr;
+        void *d_canvas = nullptr, *d_slotbuf = nullptr;
+        std::vector<void *> d_act;
+        hipStream_t stream = nullptr;
+        hipEvent_t done = nullptr, h2d_done = nullptr;
+        std::vector<hipEvent_t> ev;
+        const float *src = nullptr;
+        int32_t n = 0;
+        bool host_input = true;
+        bool dispatched = false;
+    };
+
+    hipStream_t compute_stream_for_join() const { return join_stream_; }
+
+    hipError_t alloc(void **p, size_t bytes) {
+        hipError_t e = hipMalloc(p, align256(bytes ? bytes : 1));
+        if (e == hipSuccess) dev_allocs_.push_back(*p);
+        return e;
+    }
+    template <class T>
+    hipError_t alloc(T **p, size_t bytes) {
+        return alloc(reinterpret_cast<void **>(p), bytes);
+    }
+
+    // Encoder E_k: pillarize, PFN canvas, backbone, upsample into slot k.
+    // `ev_base` is the index of the event recorded after the input copy.
+    rtcc_status enqueue_encoder(Branch &b, hipStream_t s, bool timing, int ev_base, std::string &err) {
+        const Plan &p = p_;
+        const int n_cells = p.H * p.W;
+        const int n_tiles = (n_cells + kern::kScanTile - 1) / kern::kScanTile;
+        const int n = b.n;
+        int32_t *counts = static_cast<int32_t *>(b.d_counts);
+        int32_t *offsets = static_cast<int32_t *>(b.d_offsets);
+        int32_t *tiles = static_cast<int32_t *>(b.d_tiles);
+        int32_t *meta = static_cast<int32_t *>(b.d_meta);
+        int ev = ev_base;
+        if (timing) HIP_TRY(hipEventRecord(b.ev[ev], s));
+        ++ev;
+        kern::PillarGeom g{p.d.x_min, p.d.x_max, p.d.y_min, p.d.y_max, p.d.z_min, p.d.z_max,
+                           p.d.pillar_size, p.H, p.W};
+        HIP_TRY(kern::fill_i32(counts, n_cells, 0, s));
+        HIP_TRY(kern::cell_ids(b.src, n, g, static_cast<int32_t *>(b.d_cell), static_cast<int32_t *>(b.d_slot),
+                               counts, s));
+        HIP_TRY(kern::scan_reduce(counts, n_cells, tiles, s));
+        HIP_TRY(kern::scan_tiles(tiles, n_tiles, meta, s));
+        HIP_TRY(kern::scan_down(counts, n_cells, tiles, p.d.max_points_per_pillar, offsets,
+                                static_cast<int32_t *>(b.d_pcells), static_cast<int32_t *>(b.d_pcounts),
+                                static_cast<int32_t *>(b.d_overfull), meta, s));
+        HIP_TRY(kern::scatter(static_cast<int32_t *>(b.d_cell), static_cast<int32_t *>(b.d_slot), offsets, n,
+                              static_cast<int32_t *>(b.d_member), s));
+        HIP_TRY(kern::overfull_select(static_cast<int32_t *>(b.d_overfull), meta, counts, offsets,
+                                      static_cast<int32_t *>(b.d_member), p.d.max_points_per_pillar, n, s));
+        if (timing) HIP_TRY(hipEventRecord(b.ev[ev], s));
+        ++ev;
+
+        kern::PfnArgs pa{};
+        pa.pts = b.src;
+        pa.counts = counts;
+        pa.offsets = offsets;
+        pa.member = static_cast<int32_t *>(b.d_member);
+        pa.w = static_cast<const float *>(d_bias) + p.pfn_w_off;
+        pa.b = static_cast<const float *>(d_bias) + p.pfn_b_off;
+        pa.canvas = b.d_canvas;
+        pa.n_cells = n_cells;
+        pa.C = p.c_pfn;
+        pa.max_pts = p.d.max_points_per_pillar;
+        pa.inv_hx = float(2.0 / (double(p.d.x_max) - double(p.d.x_min)));
+        pa.inv_hy = float(2.0 / (double(p.d.y_max) - double(p.d.y_min)));
+        pa.z0 = p.d.z_min;
+        pa.inv_dz = float(1.0 / (double(p.d.z_max) - double(p.d.z_min)));
+        HIP_TRY(kern::pfn_canvas(p.bf16, pa, s));
+        if (timing) HIP_TRY(hipEventRecord(b.ev[ev], s));
+        ++ev;
+
+        const void *x = b.d_canvas;
+        for (size_t l = 0; l < p.convs.size(); ++l) {
+            const ConvLayer &c = p.convs[l];
+            kern::GemmArgs ga{};
+            ga.in = x;
+            ga.wt = static_cast<const char *>(d_mat) + c.w_off * p.elt;
+            ga.bias = static_cast<const float *>(d_bias) + c.b_off;
+            ga.out = b.d_act[l];
+            ga.Hi = c.Hi; ga.Wi = c.Wi; ga.Ci = c.Ci;
+            ga.Ho = c.Ho; ga.Wo = c.Wo; ga.N = c.Co;
+            ga.stride = c.stride;
+            ga.u = 1;
+            ga.ldo = c.Co;
+            ga.c_off = 0;
+            HIP_TRY(kern::conv3x3(p.bf16, ga, s));
+            if (timing) HIP_TRY(hipEventRecord(b.ev[ev], s));
+            ++ev;
+            x = b.d_act[l];
+        }
+        for (const UpLayer &u : p.ups) {
+            kern::GemmArgs ga{};
+            ga.in = b.d_act[p.stage_last_conv[u.stage]];
+            ga.wt = static_cast<const char *>(d_mat) + u.w_off * p.elt;
+            ga.bias = static_cast<const float *>(d_bias) + u.b_off;
+            ga.out = b.d_slotbuf;
+            ga.Hi = u.Hi; ga.Wi = u.Wi; ga.Ci = u.Ci;
+            ga.Ho = p.H2; ga.Wo = p.W2; ga.N = u.Co;
+            ga.stride = 1;
+            ga.u = u.u;
+            ga.ldo = p.c_slot;
+            ga.c_off = u.c_off;
+            HIP_TRY(kern::deconv(p.bf16, ga, s));
+            if (timing) HIP_TRY(hipEventRecord(b.ev[ev], s));
+            ++ev;
+        }
+        return RTCC_OK;
+    }
+
+    rtcc_status enqueue_post(const std::vector<std::array<float, 6>> &affine, hipStream_t s, bool timing,
+                             std::string &err) {
+        const Plan &p = p_;
+        kern::WarpArgs wa{};
+        for (int k = 0; k < p.K; ++k) {
+            wa.slots[k] = br_[k].d_slotbuf;
+            for (int e = 0; e < 6; ++e) wa.affine[k][e] = affine[k][e];
+        }
+        wa.fused = d_fused;
+        wa.K = p.K;
+        wa.H2 = p.H2;
+        wa.W2 = p.W2;
+        wa.C = p.c_slot;
+        HIP_TRY(kern::warp_fuse(p.bf16, p.d.fusion == RTCC_FUSE_ATTN, wa, s));
+        if (timing) HIP_TRY(hipEventRecord(post_ev_[1], s));
+        HIP_TRY(kern::head1x1(p.bf16, d_fused, static_cast<const char *>(d_mat) + p.head_w_off * p.elt,
+                              static_cast<const float *>(d_bias) + p.head_b_off, static_cast<float *>(d_head),
+                              p.H2 * p.W2, p.c_slot, s));
+        HIP_TRY(hipEventRecord(ev_head_, s));
+        if (timing) HIP_TRY(hipEventRecord(post_ev_[2], s));
+        kern::DecodeArgs da{};
+        da.head = static_cast<const float *>(d_head);
+        da.H2 = p.H2;
+        da.W2 = p.W2;
+        da.thr = p.d.score_logit_threshold;
+        da.x0 = p.d.x_min;
+        da.y0 = p.d.y_min;
+        da.dx = float((double(p.d.x_max) - double(p.d.x_min)) / p.W2);
+        da.dy = float((double(p.d.y_max) - double(p.d.y_min)) / p.H2);
+        da.aw = p.d.anchor_w;
+        da.al = p.d.anchor_l;
+        da.ah = p.d.anchor_h;
+        da.az = p.d.anchor_z;
+        da.ayaw0 = p.d.anchor_yaw[0];
+        da.ayaw1 = p.d.anchor_yaw[1];
+        da.tile_counts = static_cast<int32_t *>(d_dec_tiles);
+        da.rec = static_cast<float *>(d_rec);
+        da.count = static_cast<int32_t *>(d_count);
+        HIP_TRY(kern::decode(da, s));
+        if (timing) HIP_TRY(hipEventRecord(post_ev_[3], s));
+        return RTCC_OK;
+    }
+
+    rtcc_status locate(int id, int agent, void **ptr, size_t *bytes, std::string &err) {
+        const Plan &p = p_;
+        const bool per_agent = id == RTCC_T_PILLAR_CELLS || id == RTCC_T_PILLAR_COUNTS ||
+                               id == RTCC_T_CANVAS || id == RTCC_T_SLOT;
+        int stage = 0;
+        if (id == RTCC_T_STAGE_OUT) {
+            stage = agent >> 8;
+            agent &= 255;
+            if (stage < 0 || stage >= int(p.stage_last_conv.size())) {
+                err = "stage out of range";
+                return RTCC_E_ARG;
+            }
+        }
+        if ((per_agent || id == RTCC_T_STAGE_OUT) && (agent < 0 || agent >= p.K)) {
+            err = "agent out of range";
+            return RTCC_E_ARG;
+        }
+        switch (id) {
+            case RTCC_T_PILLAR_CELLS:
+            case RTCC_T_PILLAR_COUNTS: {
+                HIP_TRY(hipSetDevice(dev_));
+                HIP_TRY(hipMemcpyAsync(h_small, br_[agent].d_meta, 12, hipMemcpyDeviceToHost, aux_stream_));
+                HIP_TRY(hipStreamSynchronize(aux_stream_));
+                const int32_t P = reinterpret_cast<int32_t *>(h_small)[1];
+                *ptr = id == RTCC_T_PILLAR_CELLS ? br_[agent].d_pcells : br_[agent].d_pcounts;
+                *bytes = size_t(P) * 4;
+                return RTCC_OK;
+            }
+            case RTCC_T_CANVAS:
+                *ptr = br_[agent].d_canvas;
+                *bytes = size_t(p.H) * p.W * p.c_pfn * p.elt;
+                return RTCC_OK;
+            case RTCC_T_SLOT:
+                *ptr = br_[agent].d_slotbuf;
+                *bytes = size_t(p.H2) * p.W2 * p.c_slot * p.elt;
+                return RTCC_OK;
+            case RTCC_T_FUSED:
+                *ptr = d_fused;
+                *bytes = size_t(p.H2) * p.W2 * p.c_slot * p.elt;
+                return RTCC_OK;
+            case RTCC_T_HEAD:
+                *ptr = d_head;
+                *bytes = size_t(p.H2) * p.W2 * 16 * 4;
+                return RTCC_OK;
+            case RTCC_T_STAGE_OUT: {
+                const ConvLayer &c = p.convs[p.stage_last_conv[stage]];
+                *ptr = br_[agent].d_act[p.stage_last_conv[stage]];
+                *bytes = size_t(c.Ho) * c.Wo * c.Co * p.elt;
+                return RTCC_OK;
+            }
+        }
+        err = "unknown tensor id";
+        return RTCC_E_ARG;
+    }
+
+    void release_all() {
+        if (dev_ < 0) return;
+        // Teardown is best effort: errors cannot be reported from a destructor.
+        (void)hipSetDevice(dev_);
+        (void)hipDeviceSynchronize();
+        for (Branch &b : br_) {
+            if (b.staging) (void)hipHostFree(b.staging);
+            if (b.stream) (void)hipStreamDestroy(b.stream);
+            if (b.done) (void)hipEventDestroy(b.done);
+            if (b.h2d_done) (void)hipEventDestroy(b.h2d_done);
+            for (hipEvent_t e : b.ev)
+                if (e) (void)hipEventDestroy(e);
+        }
+        for (void *ptr : dev_allocs_) (void)hipFree(ptr);
+        if (h_rec) (void)hipHostFree(h_rec);
+        if (h_small) (void)hipHostFree(h_small);
+        if (join_stream_) (void)hipStreamDestroy(join_stream_);
+        if (copy_stream_) (void)hipStreamDestroy(copy_stream_);
+        if (aux_stream_) (void)hipStreamDestroy(aux_stream_);
+        if (ev_frame0_) (void)hipEventDestroy(ev_frame0_);
+        if (ev_head_) (void)hipEventDestroy(ev_head_);
+        for (hipEvent_t e : post_ev_)
+            if (e) (void)hipEventDestroy(e);
+    }
+
+    Plan p_;
+    rtcc_runtime_opts o_{};
+    int dev_ = -1;
+    std::vector<Branch> br_;
+    std::vector<void *> dev_allocs_;
+    void *d_mat = nullptr, *d_bias = nullptr;
+    void *d_fused = nullptr, *d_head = nullptr, *d_dec_tiles = nullptr, *d_rec = nullptr, *d_count = nullptr;
+    float *h_rec = nullptr;
+    void *h_small = nullptr;
+    size_t n_anchor_ = 0;
+    std::vector<float> boxes_, scores_;
+    std::vector<int32_t> aidx_;
+    hipStream_t join_stream_ = nullptr, copy_stream_ = nullptr, aux_stream_ = nullptr;
+    hipEvent_t ev_frame0_ = nullptr, ev_head_ = nullptr;
+    hipEvent_t post_ev_[4] = {nullptr, nullptr, nullptr, nullptr};
+    std::vector<std::array<float, 6>> last_affine_;
+};
+
+Executor *make_executor() { return new HipExecutor(); }
+
+}  // namespace rtcc

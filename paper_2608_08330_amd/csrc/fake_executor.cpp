@@ -1,0 +1,97 @@
+// Recording executor for host-only tests of the controller and the C ABI.
+// It allocates no GPU resources and computes nothing: every call appends a
+// line to a log that tests read through rtcc_hosttest_log().  This file is
+// linked only into the host test library, never into the GPU library.
+#include <cstring>
+#include <mutex>
+#include <sstream>
+
+#include "controller.hpp"
+
+namespace rtcc {
+
+namespace {
+std::mutex g_log_mu;
+std::string g_log;
+void log_line(const std::string &s) {
+    std::lock_guard<std::mutex> lk(g_log_mu);
+    g_log += s;
+    g_log += '\n';
+}
+}  // namespace
+
+class FakeExecutor : public Executor {
+  public:
+    rtcc_status init(const Plan &p, const HostWeights &, const rtcc_runtime_opts &o,
+                     std::string &) override {
+        plan_ = p;
+        staging_.assign(p.K, std::vector<float>(size_t(p.n_max) * 4, 0.f));
+        std::ostringstream os;
+        os << "init K=" << p.K << " H=" << p.H << " W=" << p.W << " H2=" << p.H2 << " W2=" << p.W2
+           << " C=" << p.c_slot << " convs=" << p.convs.size() << " ups=" << p.ups.size()
+           << " exec=" << o.exec;
+        log_line(os.str());
+        return RTCC_OK;
+    }
+    float *staging(int agent) override { return staging_[agent].data(); }
+    rtcc_status begin_frame(std::string &) override {
+        log_line("begin_frame");
+        return RTCC_OK;
+    }
+    rtcc_status dispatch(int agent, const float *pts, int64_t n, bool device_src,
+                         std::string &) override {
+        std::ostringstream os;
+        os << "dispatch " << agent << " n=" << n << " src=" << (device_src ? "device" : "staging")
+           << " staged=" << (pts == staging_[agent].data() ? 1 : 0);
+        log_line(os.str());
+        return RTCC_OK;
+    }
+    rtcc_status join(const std::vector<std::array<float, 6>> &affine, double,
+                     rtcc_detections *out, std::string &) override {
+        std::ostringstream os;
+        os << "join";
+        for (const auto &m : affine)
+            os << " [" << m[0] << "," << m[1] << "," << m[2] << "," << m[3] << "," << m[4] << ","
+               << m[5] << "]";
+        log_line(os.str());
+        out->count = 0;
+        return RTCC_OK;
+    }
+    rtcc_status tensor_bytes(int, int, size_t *, std::string &err) override {
+        err = "no tensors in the recording executor";
+        return RTCC_E_STATE;
+    }
+    rtcc_status get_tensor(int, int, void *, size_t, std::string &err) override {
+        err = "no tensors in the recording executor";
+        return RTCC_E_STATE;
+    }
+    rtcc_status profile_nodes(int, int, float *, int *, std::string &err) override {
+        err = "no profiling in the recording executor";
+        return RTCC_E_STATE;
+    }
+    int node_count() const override { return 0; }
+    rtcc_status node_times(float *, int *n, std::string &) override {
+        *n = 0;
+        return RTCC_OK;
+    }
+
+  private:
+    Plan plan_;
+    std::vector<std::vector<float>> staging_;
+};
+
+Executor *make_executor() { return new FakeExecutor(); }
+
+}  // namespace rtcc
+
+extern "C" __attribute__((visibility("default"))) size_t rtcc_hosttest_log(char *buf, size_t cap, int clear) {
+    std::lock_guard<std::mutex> lk(rtcc::g_log_mu);
+    size_t n = rtcc::g_log.size();
+    if (buf && cap) {
+        size_t m = n < cap - 1 ? n : cap - 1;
+        std::memcpy(buf, rtcc::g_log.data(), m);
+        buf[m] = 0;
+    }
+    if (clear) rtcc::g_log.clear();
+    return n;
+}

@@ -1,0 +1,111 @@
+// Host launchers of the gfx950 kernels.  Every launcher checks nothing but
+// enqueues on the given stream and returns hipGetLastError(); the executor
+// validates shapes before calling.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace rtcc {
+namespace kern {
+
+// ------------------------------------------------------------ pillarization
+struct PillarGeom {
+    float x0, x1, y0, y1, z0, z1, v;
+    int H, W;
+};
+
+constexpr int kScanTile = 2048;  // cells per block of the cell scans
+
+hipError_t fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s);
+
+// K1: cell id per point (-1 if dropped); counts[cell] += 1 and the point's
+// rank of arrival in its cell (an arbitrary order) goes to slot[i].
+hipError_t cell_ids(const float *pts, int32_t n, const PillarGeom &g, int32_t *cell, int32_t *slot,
+                    int32_t *counts, hipStream_t s);
+
+// K2a: per tile of kScanTile cells: (points, non-empty cells).
+hipError_t scan_reduce(const int32_t *counts, int32_t n_cells, int32_t *tile_sums, hipStream_t s);
+// K2b: exclusive scan of tile sums in place; meta = {valid points, pillars,
+// overfull count (zeroed)}.
+hipError_t scan_tiles(int32_t *tile_sums, int32_t n_tiles, int32_t *meta, hipStream_t s);
+// K2c: offsets[cell] (exclusive prefix of counts), pillar lists in
+// ascending cell order, list of cells holding more than max_pts points.
+hipError_t scan_down(const int32_t *counts, int32_t n_cells, const int32_t *tile_sums,
+                     int32_t max_pts, int32_t *offsets, int32_t *pcells, int32_t *pcounts,
+                     int32_t *overfull, int32_t *meta, hipStream_t s);
+// K2d: member[offsets[cell] + slot] = point index.
+hipError_t scatter(const int32_t *cell, const int32_t *slot, const int32_t *offsets, int32_t n,
+                   int32_t *member, hipStream_t s);
+// K2e: for every overfull cell, move its max_pts lowest point indices to
+// the front of its member segment.
+hipError_t overfull_select(const int32_t *overfull, const int32_t *meta, const int32_t *counts,
+                           const int32_t *offsets, int32_t *member, int32_t max_pts, int32_t n,
+                           hipStream_t s);
+
+// K3: dense canvas [H*W][C]: per cell, channel max over the first
+// min(count, max_pts) members of ReLU(W^T f + b); zero for empty cells.
+struct PfnArgs {
+    const float *pts;
+    const int32_t *counts;
+    const int32_t *offsets;
+    const int32_t *member;
+    const float *w;  // [4][C]
+    const float *b;  // [C]
+    void *canvas;
+    int32_t n_cells;
+    int32_t C;
+    int32_t max_pts;
+    float inv_hx, inv_hy, z0, inv_dz;
+};
+hipError_t pfn_canvas(bool bf16, const PfnArgs &a, hipStream_t s);
+
+// ------------------------------------------------------------ implicit GEMM
+// conv:   out[m][c_off + n] for m = output pixel, 3x3 taps, pad 1, stride.
+// deconv: A rows are input pixels, phase = blockIdx.z, output pixel
+//         (iy * u + py, ix * u + px), skipped outside Ho x Wo.
+struct GemmArgs {
+    const void *in;    // NHWC, channel stride Ci
+    const void *wt;    // Bt[N][K] (conv) or u*u phases of Bt[N][Ci] (deconv)
+    const float *bias; // [N]
+    void *out;         // NHWC, channel stride ldo
+    int32_t Hi, Wi, Ci;
+    int32_t Ho, Wo;
+    int32_t N;
+    int32_t stride;    // conv only
+    int32_t u;         // deconv only
+    int32_t ldo, c_off;
+};
+hipError_t conv3x3(bool bf16, const GemmArgs &a, hipStream_t s);
+hipError_t deconv(bool bf16, const GemmArgs &a, hipStream_t s);
+
+// ------------------------------------------------------------ post-join
+struct WarpArgs {
+    const void *slots[16];  // per agent [H2*W2][C]
+    float affine[16][6];    // per agent {M00, M01, t0, M10, M11, t1}
+    void *fused;            // [H2*W2][C]
+    int32_t K, H2, W2, C;
+};
+hipError_t warp_fuse(bool bf16, bool attn, const WarpArgs &a, hipStream_t s);
+
+// 1x1 head: out[m][16] float32 = bias + Bt[16][C] . in[m][C].
+hipError_t head1x1(bool bf16, const void *in, const void *wt, const float *bias, float *out,
+                   int32_t M, int32_t C, hipStream_t s);
+
+// Threshold and decode: anchors of [M][16] head outputs (2 anchors x 8).
+struct DecodeArgs {
+    const float *head;
+    int32_t H2, W2;
+    float thr;
+    float x0, y0, dx, dy;
+    float aw, al, ah, az, ayaw0, ayaw1;
+    int32_t *tile_counts;  // [tiles + 1]
+    float *rec;            // [n_anchors][9]: box 7, score, index bits
+    int32_t *count;        // total kept
+};
+constexpr int kDecodeTile = 1024;
+hipError_t decode(const DecodeArgs &a, hipStream_t s);
+
+}  // namespace kern
+}  // namespace rtcc

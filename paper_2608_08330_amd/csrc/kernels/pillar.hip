@@ -1,0 +1,343 @@
+// Pillarization and point-feature canvas for gfx950.
+//
+// Deterministic counting sort by cell (no float atomics, no order-dependent
+// result):
+//   cell_ids        one thread per point: float32 cell index, atomic count
+//                   per cell; the returned old count is the point's rank of
+//                   arrival in its cell
+//   scan_reduce /   exclusive prefix over all H*W cells -> segment offsets,
+//   scan_tiles /    ascending list of non-empty cells (pillars) and their
+//   scan_down       counts, list of cells over the per-pillar point cap
+//   scatter         member[offset[cell] + rank] = point index
+//   overfull_select for the few cells above the cap, one wavefront moves the
+//                   cap lowest point indices (found by bisection on the index
+//                   value) to the front of the segment
+//   pfn_canvas      one lane per (cell, 8 channels): linear 4 -> C, ReLU,
+//                   max over the first min(count, cap) members; empty cells
+//                   are written as zeros, so no separate memset
+// The only order-dependent intermediate is the order of members inside a
+// segment, and every consumer of it is order-independent (max, set
+// selection), so every output is bitwise reproducible.
+#include <climits>
+
+#include "kernels.hpp"
+
+namespace rtcc {
+namespace kern {
+
+namespace {
+
+__device__ inline int2 add2(int2 a, int2 b) { return make_int2(a.x + b.x, a.y + b.y); }
+
+// Inclusive scan across the 64 lanes of a wavefront.
+__device__ inline int2 wave_incl_scan(int2 v) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        int ax = __shfl_up(v.x, d, 64);
+        int ay = __shfl_up(v.y, d, 64);
+        if (lane >= d) {
+            v.x += ax;
+            v.y += ay;
+        }
+    }
+    return v;
+}
+
+// Exclusive scan of one int2 per thread over a 256-thread block.
+__device__ inline int2 block_excl_scan256(int2 v, int2 *total) {
+    __shared__ int2 wsum[4];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    int2 inc = wave_incl_scan(v);
+    if (lane == 63) wsum[w] = inc;
+    __syncthreads();
+    int2 base = make_int2(0, 0), tot = make_int2(0, 0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        if (i < w) base = add2(base, wsum[i]);
+        tot = add2(tot, wsum[i]);
+    }
+    __syncthreads();
+    *total = tot;
+    return make_int2(base.x + inc.x - v.x, base.y + inc.y - v.y);
+}
+
+__global__ __launch_bounds__(256) void k_fill_i32(int32_t *p, int64_t n, int32_t v) {
+    for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < n; i += int64_t(gridDim.x) * 256)
+        p[i] = v;
+}
+
+__global__ __launch_bounds__(256) void k_cell_ids(const float4 *__restrict__ pts, int32_t n,
+                                                  PillarGeom g, int32_t *__restrict__ cell,
+                                                  int32_t *__restrict__ slot,
+                                                  int32_t *__restrict__ counts) {
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    if (i >= n) return;
+    const float4 p = pts[i];
+    int c = -1;
+    if (__builtin_isfinite(p.x) && __builtin_isfinite(p.y) && __builtin_isfinite(p.z) &&
+        __builtin_isfinite(p.w) && p.x >= g.x0 && p.x < g.x1 && p.y >= g.y0 && p.y < g.y1 &&
+        p.z >= g.z0 && p.z < g.z1) {
+        // float32, round-to-nearest subtract and divide, then floor
+        const float fx = floorf(__fdiv_rn(__fsub_rn(p.x, g.x0), g.v));
+        const float fy = floorf(__fdiv_rn(__fsub_rn(p.y, g.y0), g.v));
+        if (fx >= 0.f && fx < float(g.W) && fy >= 0.f && fy < float(g.H)) c = int(fy) * g.W + int(fx);
+    }
+    cell[i] = c;
+    if (c >= 0) slot[i] = atomicAdd(&counts[c], 1);
+}
+
+__global__ __launch_bounds__(256) void k_scan_reduce(const int32_t *__restrict__ counts,
+                                                     int32_t n_cells, int32_t *__restrict__ tile_sums) {
+    const int base = blockIdx.x * kScanTile + threadIdx.x * 8;
+    int s = 0, f = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int c = base + i;
+        if (c < n_cells) {
+            const int v = counts[c];
+            s += v;
+            f += v > 0;
+        }
+    }
+    int2 tot;
+    block_excl_scan256(make_int2(s, f), &tot);
+    if (threadIdx.x == 0) {
+        tile_sums[2 * blockIdx.x] = tot.x;
+        tile_sums[2 * blockIdx.x + 1] = tot.y;
+    }
+}
+
+__global__ __launch_bounds__(256) void k_scan_tiles(int32_t *__restrict__ ts, int32_t n_tiles,
+                                                    int32_t *__restrict__ meta) {
+    int2 carry = make_int2(0, 0);
+    for (int base = 0; base < n_tiles; base += 256) {
+        const int i = base + threadIdx.x;
+        int2 v = make_int2(0, 0);
+        if (i < n_tiles) v = make_int2(ts[2 * i], ts[2 * i + 1]);
+        int2 tot;
+        const int2 ex = block_excl_scan256(v, &tot);
+        if (i < n_tiles) {
+            ts[2 * i] = carry.x + ex.x;
+            ts[2 * i + 1] = carry.y + ex.y;
+        }
+        carry = add2(carry, tot);
+    }
+    if (threadIdx.x == 0) {
+        meta[0] = carry.x;
+        meta[1] = carry.y;
+        meta[2] = 0;
+    }
+}
+
+__global__ __launch_bounds__(256) void k_scan_down(const int32_t *__restrict__ counts, int32_t n_cells,
+                                                   const int32_t *__restrict__ ts, int32_t max_pts,
+                                                   int32_t *__restrict__ offsets,
+                                                   int32_t *__restrict__ pcells,
+                                                   int32_t *__restrict__ pcounts,
+                                                   int32_t *__restrict__ overfull,
+                                                   int32_t *__restrict__ meta) {
+    const int base = blockIdx.x * kScanTile + threadIdx.x * 8;
+    int v[8];
+    int s = 0, f = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int c = base + i;
+        v[i] = c < n_cells ? counts[c] : 0;
+        s += v[i];
+        f += v[i] > 0;
+    }
+    int2 tot;
+    const int2 ex = block_excl_scan256(make_int2(s, f), &tot);
+    int off = ts[2 * blockIdx.x] + ex.x;
+    int p = ts[2 * blockIdx.x + 1] + ex.y;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int c = base + i;
+        if (c < n_cells) {
+            offsets[c] = off;
+            if (v[i] > 0) {
+                pcells[p] = c;
+                pcounts[p] = v[i];
+                ++p;
+                if (v[i] > max_pts) overfull[atomicAdd(&meta[2], 1)] = c;
+            }
+            off += v[i];
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void k_scatter(const int32_t *__restrict__ cell,
+                                                 const int32_t *__restrict__ slot,
+                                                 const int32_t *__restrict__ offsets, int32_t n,
+                                                 int32_t *__restrict__ member) {
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    if (i >= n) return;
+    const int c = cell[i];
+    if (c >= 0) member[offsets[c] + slot[i]] = i;
+}
+
+__global__ __launch_bounds__(256) void k_overfull_select(const int32_t *__restrict__ overfull,
+                                                         const int32_t *__restrict__ meta,
+                                                         const int32_t *__restrict__ counts,
+                                                         const int32_t *__restrict__ offsets,
+                                                         int32_t *__restrict__ member,
+                                                         int32_t max_pts, int32_t n) {
+    const int lane = threadIdx.x & 63;
+    const int wave = (blockIdx.x * 256 + threadIdx.x) >> 6;
+    const int n_waves = (gridDim.x * 256) >> 6;
+    const int n_over = meta[2];
+    for (int w = wave; w < n_over; w += n_waves) {
+        const int c = overfull[w];
+        const int cnt = counts[c];
+        int32_t *seg = member + offsets[c];
+        // Smallest T with #{members < T} >= max_pts.  Members are distinct
+        // point indices in [0, n), so exactly max_pts members lie below T.
+        int lo = 1, hi = n;
+        while (lo < hi) {
+            const int mid = lo + (hi - lo) / 2;
+            int below = 0;
+            for (int j = lane; j < cnt; j += 64) below += seg[j] < mid;
+#pragma unroll
+            for (int d = 32; d >= 1; d >>= 1) below += __shfl_xor(below, d, 64);
+            if (below >= max_pts) hi = mid;
+            else lo = mid + 1;
+        }
+        const int T = lo;
+        // Stable in-place compaction of the selected members to the front:
+        // a chunk is read completely before any of it is overwritten, and
+        // writes never pass the chunk being read.
+        int pos = 0;
+        for (int base = 0; base < cnt && pos < max_pts; base += 64) {
+            const int j = base + lane;
+            const int e = j < cnt ? seg[j] : INT_MAX;
+            const bool sel = j < cnt && e < T;
+            const unsigned long long m = __ballot(sel);
+            const int my = pos + __popcll(m & ((1ull << lane) - 1ull));
+            if (sel) seg[my] = e;
+            pos += __popcll(m);
+        }
+    }
+}
+
+__device__ inline uint32_t pack_bf16x2(float a, float b) {
+    uint32_t ua = __float_as_uint(a), ub = __float_as_uint(b);
+    ua += 0x7fffu + ((ua >> 16) & 1u);
+    ub += 0x7fffu + ((ub >> 16) & 1u);
+    return (ua >> 16) | (ub & 0xffff0000u);
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(256) void k_pfn_canvas(PfnArgs a) {
+    const int lanes_per_cell = a.C >> 3;
+    const int gid = blockIdx.x * 256 + threadIdx.x;
+    const int cell = gid / lanes_per_cell;
+    const int ch = (gid - cell * lanes_per_cell) * 8;
+    if (cell >= a.n_cells) return;
+    float mx[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) mx[i] = 0.f;
+    const int cnt = a.counts[cell];
+    if (cnt > 0) {
+        float w0[8], w1[8], w2[8], w3[8], bb[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            w0[i] = a.w[0 * a.C + ch + i];
+            w1[i] = a.w[1 * a.C + ch + i];
+            w2[i] = a.w[2 * a.C + ch + i];
+            w3[i] = a.w[3 * a.C + ch + i];
+            bb[i] = a.b[ch + i];
+        }
+        const int m = cnt < a.max_pts ? cnt : a.max_pts;
+        const int off = a.offsets[cell];
+        const float4 *pts = reinterpret_cast<const float4 *>(a.pts);
+        for (int t = 0; t < m; ++t) {
+            const float4 p = pts[a.member[off + t]];
+            const float f0 = p.x * a.inv_hx;
+            const float f1 = p.y * a.inv_hy;
+            const float f2 = (p.z - a.z0) * a.inv_dz;
+            const float f3 = p.w;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                float h = bb[i] + w0[i] * f0 + w1[i] * f1 + w2[i] * f2 + w3[i] * f3;
+                h = h > 0.f ? h : 0.f;  // +0 for every non-positive value
+                mx[i] = fmaxf(mx[i], h);
+            }
+        }
+    }
+    if (BF16) {
+        uint4 o;
+        o.x = pack_bf16x2(mx[0], mx[1]);
+        o.y = pack_bf16x2(mx[2], mx[3]);
+        o.z = pack_bf16x2(mx[4], mx[5]);
+        o.w = pack_bf16x2(mx[6], mx[7]);
+        *reinterpret_cast<uint4 *>(static_cast<uint16_t *>(a.canvas) + size_t(cell) * a.C + ch) = o;
+    } else {
+        float4 *dst = reinterpret_cast<float4 *>(static_cast<float *>(a.canvas) + size_t(cell) * a.C + ch);
+        dst[0] = make_float4(mx[0], mx[1], mx[2], mx[3]);
+        dst[1] = make_float4(mx[4], mx[5], mx[6], mx[7]);
+    }
+}
+
+inline unsigned blocks_for(int64_t n, int per) { return unsigned((n + per - 1) / per); }
+
+}  // namespace
+
+hipError_t fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    unsigned g = blocks_for(n, 256);
+    if (g > 4096) g = 4096;
+    k_fill_i32<<<g, 256, 0, s>>>(p, n, v);
+    return hipGetLastError();
+}
+
+hipError_t cell_ids(const float *pts, int32_t n, const PillarGeom &g, int32_t *cell, int32_t *slot,
+                    int32_t *counts, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    k_cell_ids<<<blocks_for(n, 256), 256, 0, s>>>(reinterpret_cast<const float4 *>(pts), n, g, cell,
+                                                   slot, counts);
+    return hipGetLastError();
+}
+
+hipError_t scan_reduce(const int32_t *counts, int32_t n_cells, int32_t *tile_sums, hipStream_t s) {
+    k_scan_reduce<<<blocks_for(n_cells, kScanTile), 256, 0, s>>>(counts, n_cells, tile_sums);
+    return hipGetLastError();
+}
+
+hipError_t scan_tiles(int32_t *tile_sums, int32_t n_tiles, int32_t *meta, hipStream_t s) {
+    k_scan_tiles<<<1, 256, 0, s>>>(tile_sums, n_tiles, meta);
+    return hipGetLastError();
+}
+
+hipError_t scan_down(const int32_t *counts, int32_t n_cells, const int32_t *tile_sums,
+                     int32_t max_pts, int32_t *offsets, int32_t *pcells, int32_t *pcounts,
+                     int32_t *overfull, int32_t *meta, hipStream_t s) {
+    k_scan_down<<<blocks_for(n_cells, kScanTile), 256, 0, s>>>(counts, n_cells, tile_sums, max_pts,
+                                                                offsets, pcells, pcounts, overfull, meta);
+    return hipGetLastError();
+}
+
+hipError_t scatter(const int32_t *cell, const int32_t *slot, const int32_t *offsets, int32_t n,
+                   int32_t *member, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    k_scatter<<<blocks_for(n, 256), 256, 0, s>>>(cell, slot, offsets, n, member);
+    return hipGetLastError();
+}
+
+hipError_t overfull_select(const int32_t *overfull, const int32_t *meta, const int32_t *counts,
+                           const int32_t *offsets, int32_t *member, int32_t max_pts, int32_t n,
+                           hipStream_t s) {
+    if (n <= max_pts) return hipSuccess;  // no cell can exceed the cap
+    k_overfull_select<<<64, 256, 0, s>>>(overfull, meta, counts, offsets, member, max_pts, n);
+    return hipGetLastError();
+}
+
+hipError_t pfn_canvas(bool bf16, const PfnArgs &a, hipStream_t s) {
+    const int64_t threads = int64_t(a.n_cells) * (a.C / 8);
+    if (bf16) k_pfn_canvas<true><<<blocks_for(threads, 256), 256, 0, s>>>(a);
+    else k_pfn_canvas<false><<<blocks_for(threads, 256), 256, 0, s>>>(a);
+    return hipGetLastError();
+}
+
+}  // namespace kern
+}  // namespace rtcc

@@ -1,0 +1,346 @@
+// Post-join subgraph on gfx950: pose warp + cross-agent fusion, 1x1 head,
+// threshold + box decode.
+//
+// warp_fuse: 32 lanes (half a wavefront) per ego cell, VEC = C / 32
+//   channels per lane.  For every agent the lane computes the agent-grid
+//   sample position from the index-space affine, reads the four bilinear
+//   corners of its channel slice (zero outside the grid) and folds the
+//   sample into a running channel max, or into an online softmax over
+//   agents whose scores <X_0, X_k> / sqrt(C) are reduced across the 32 lanes
+//   with butterfly shuffles (fixed order, so deterministic).  Bandwidth
+//   bound: every slot is read about once through L2, the fused map written
+//   once.
+// head1x1: one wavefront per 16 pixels; the 16 outputs of a pixel are one
+//   16 x 16 MFMA tile per 32 (bf16) or 16 (fp32) input channels.
+// decode: tile counts of kept anchors, one-block scan of the tile counts,
+//   then every tile rescans its flags and writes its kept anchors in
+//   ascending anchor order (stable compaction, deterministic).
+#include <cmath>
+
+#include "kernels.hpp"
+
+namespace rtcc {
+namespace kern {
+
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ inline float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ inline float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
+__device__ inline uint32_t rne_bits(float x) {
+    uint32_t u = __float_as_uint(x);
+    return u + 0x7fffu + ((u >> 16) & 1u);
+}
+
+// Load VEC consecutive elements as float.
+template <typename T, int VEC>
+__device__ inline void load_vec(const T *p, float *v);
+template <int VEC>
+__device__ inline void load_vec_bf16(const uint16_t *p, float *v) {
+    if constexpr (VEC % 4 == 0) {
+#pragma unroll
+        for (int q = 0; q < VEC / 4; ++q) {
+            const uint2 u = reinterpret_cast<const uint2 *>(p)[q];
+            v[4 * q + 0] = bf16_lo(u.x);
+            v[4 * q + 1] = bf16_hi(u.x);
+            v[4 * q + 2] = bf16_lo(u.y);
+            v[4 * q + 3] = bf16_hi(u.y);
+        }
+    } else if constexpr (VEC == 2) {
+        const uint32_t u = *reinterpret_cast<const uint32_t *>(p);
+        v[0] = bf16_lo(u);
+        v[1] = bf16_hi(u);
+    } else {
+        v[0] = __uint_as_float(uint32_t(p[0]) << 16);
+    }
+}
+template <int VEC>
+__device__ inline void store_vec_bf16(uint16_t *p, const float *v) {
+    if constexpr (VEC % 4 == 0) {
+#pragma unroll
+        for (int q = 0; q < VEC / 4; ++q) {
+            uint2 u;
+            u.x = (rne_bits(v[4 * q]) >> 16) | (rne_bits(v[4 * q + 1]) & 0xffff0000u);
+            u.y = (rne_bits(v[4 * q + 2]) >> 16) | (rne_bits(v[4 * q + 3]) & 0xffff0000u);
+            reinterpret_cast<uint2 *>(p)[q] = u;
+        }
+    } else if constexpr (VEC == 2) {
+        *reinterpret_cast<uint32_t *>(p) = (rne_bits(v[0]) >> 16) | (rne_bits(v[1]) & 0xffff0000u);
+    } else {
+        p[0] = uint16_t(rne_bits(v[0]) >> 16);
+    }
+}
+
+template <typename T, int VEC, bool ATTN>
+__global__ __launch_bounds__(256) void k_warp_fuse(WarpArgs a) {
+    const int l32 = threadIdx.x & 31;
+    const int cell = (blockIdx.x * 256 + threadIdx.x) >> 5;
+    const int n_cells = a.H2 * a.W2;
+    if (cell >= n_cells) return;  // uniform over the 32 lanes of a cell
+    const int i = cell / a.W2, j = cell - (cell / a.W2) * a.W2;
+    const int c0 = l32 * VEC;
+    const float fj = float(j), fi = float(i);
+
+    float q[VEC], acc[VEC];
+    float run_max = -INFINITY, run_sum = 0.f;
+    const float inv_sqrt_c = 1.0f / sqrtf(float(a.C));
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
+
+    for (int k = 0; k < a.K; ++k) {
+        const float *m = a.affine[k];
+        const float u = m[0] * fj + m[1] * fi + m[2];
+        const float v = m[3] * fj + m[4] * fi + m[5];
+        const float fx0 = floorf(u), fy0 = floorf(v);
+        const float fx = u - fx0, fy = v - fy0;
+        const int x0 = int(fx0), y0 = int(fy0);
+        float x[VEC];
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) x[e] = 0.f;
+        const T *slot = static_cast<const T *>(a.slots[k]);
+#pragma unroll
+        for (int cnr = 0; cnr < 4; ++cnr) {
+            const int yy = y0 + (cnr >> 1), xx = x0 + (cnr & 1);
+            const float wy = (cnr >> 1) ? fy : 1.f - fy;
+            const float wx = (cnr & 1) ? fx : 1.f - fx;
+            if (yy < 0 || yy >= a.H2 || xx < 0 || xx >= a.W2) continue;
+            const float wgt = wx * wy;
+            float val[VEC];
+            const T *p = slot + (size_t(yy) * a.W2 + xx) * a.C + c0;
+            if constexpr (sizeof(T) == 2) {
+                load_vec_bf16<VEC>(reinterpret_cast<const uint16_t *>(p), val);
+            } else {
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) val[e] = reinterpret_cast<const float *>(p)[e];
+            }
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) x[e] += wgt * val[e];
+        }
+        if constexpr (!ATTN) {
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) acc[e] = k == 0 ? x[e] : fmaxf(acc[e], x[e]);
+        } else {
+            if (k == 0) {
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) q[e] = x[e];
+            }
+            float d = 0.f;
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) d += q[e] * x[e];
+#pragma unroll
+            for (int off = 16; off >= 1; off >>= 1) d += __shfl_xor(d, off, 32);
+            const float s = d * inv_sqrt_c;
+            const float nm = fmaxf(run_max, s);
+            const float scale = expf(run_max - nm);
+            const float p = expf(s - nm);
+            run_sum = run_sum * scale + p;
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) acc[e] = acc[e] * scale + p * x[e];
+            run_max = nm;
+        }
+    }
+    if constexpr (ATTN) {
+        const float inv = 1.0f / run_sum;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc[e] *= inv;
+    }
+    T *dst = static_cast<T *>(a.fused) + size_t(cell) * a.C + c0;
+    if constexpr (sizeof(T) == 2) {
+        store_vec_bf16<VEC>(reinterpret_cast<uint16_t *>(dst), acc);
+    } else {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) reinterpret_cast<float *>(dst)[e] = acc[e];
+    }
+}
+
+template <typename T, int VEC>
+hipError_t launch_warp(bool attn, const WarpArgs &a, hipStream_t s) {
+    const int64_t threads = int64_t(a.H2) * a.W2 * 32;
+    const unsigned g = unsigned((threads + 255) / 256);
+    if (attn) k_warp_fuse<T, VEC, true><<<g, 256, 0, s>>>(a);
+    else k_warp_fuse<T, VEC, false><<<g, 256, 0, s>>>(a);
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t warp_dispatch(bool attn, const WarpArgs &a, hipStream_t s) {
+    switch (a.C) {
+        case 32: return launch_warp<T, 1>(attn, a, s);
+        case 64: return launch_warp<T, 2>(attn, a, s);
+        case 128: return launch_warp<T, 4>(attn, a, s);
+        case 256: return launch_warp<T, 8>(attn, a, s);
+        case 384: return launch_warp<T, 12>(attn, a, s);
+        case 512: return launch_warp<T, 16>(attn, a, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+// ------------------------------------------------------------------ head
+
+template <typename T>
+__device__ inline f32x4_t head_mma(uint4 w, uint4 x, f32x4_t c);
+template <>
+__device__ inline f32x4_t head_mma<uint16_t>(uint4 w, uint4 x, f32x4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, w),
+                                                   __builtin_bit_cast(bf16x8_t, x), c, 0, 0, 0);
+}
+template <>
+__device__ inline f32x4_t head_mma<float>(uint4 w, uint4 x, f32x4_t c) {
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(w.x), __uint_as_float(x.x), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(w.y), __uint_as_float(x.y), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(w.z), __uint_as_float(x.z), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(w.w), __uint_as_float(x.w), c, 0, 0, 0);
+    return c;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_head(const T *__restrict__ in, const T *__restrict__ wt,
+                                              const float *__restrict__ bias, float *__restrict__ out,
+                                              int32_t M, int32_t C) {
+    constexpr int EPV = 16 / sizeof(T);
+    constexpr int BK = 4 * EPV;
+    const int lane = threadIdx.x & 63;
+    const int m0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * 16;
+    if (m0 >= M) return;
+    const int fr = lane & 15, fk = lane >> 4;
+    const int m = m0 + fr;
+    const bool ok = m < M;
+    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+    for (int k0 = 0; k0 < C; k0 += BK) {
+        const uint4 w = *reinterpret_cast<const uint4 *>(wt + size_t(fr) * C + k0 + fk * EPV);
+        uint4 x = make_uint4(0, 0, 0, 0);
+        if (ok) x = *reinterpret_cast<const uint4 *>(in + size_t(m) * C + k0 + fk * EPV);
+        acc = head_mma<T>(w, x, acc);
+    }
+    if (ok) {
+        const int n = fk * 4;
+        *reinterpret_cast<float4 *>(out + size_t(m) * 16 + n) =
+            make_float4(acc[0] + bias[n], acc[1] + bias[n + 1], acc[2] + bias[n + 2], acc[3] + bias[n + 3]);
+    }
+}
+
+// ------------------------------------------------------------------ decode
+
+__device__ inline int block_excl_scan256(int v, int *total) {
+    __shared__ int wsum[4];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    int inc = v;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int t = __shfl_up(inc, d, 64);
+        if (lane >= d) inc += t;
+    }
+    if (lane == 63) wsum[w] = inc;
+    __syncthreads();
+    int base = 0, tot = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        if (q < w) base += wsum[q];
+        tot += wsum[q];
+    }
+    __syncthreads();
+    *total = tot;
+    return base + inc - v;
+}
+
+constexpr int kPerThread = kDecodeTile / 256;
+
+__global__ __launch_bounds__(256) void k_decode_count(DecodeArgs a) {
+    const int n_anchor = a.H2 * a.W2 * 2;
+    const int base = blockIdx.x * kDecodeTile + threadIdx.x * kPerThread;
+    int c = 0;
+#pragma unroll
+    for (int q = 0; q < kPerThread; ++q) {
+        const int ai = base + q;
+        if (ai < n_anchor) c += a.head[size_t(ai >> 1) * 16 + (ai & 1) * 8] > a.thr;
+    }
+    int tot;
+    block_excl_scan256(c, &tot);
+    if (threadIdx.x == 0) a.tile_counts[blockIdx.x] = tot;
+}
+
+__global__ __launch_bounds__(256) void k_decode_scan(DecodeArgs a, int32_t n_tiles) {
+    int carry = 0;
+    for (int base = 0; base < n_tiles; base += 256) {
+        const int i = base + threadIdx.x;
+        const int v = i < n_tiles ? a.tile_counts[i] : 0;
+        int tot;
+        const int ex = block_excl_scan256(v, &tot);
+        if (i < n_tiles) a.tile_counts[i] = carry + ex;
+        carry += tot;
+    }
+    if (threadIdx.x == 0) *a.count = carry;
+}
+
+__global__ __launch_bounds__(256) void k_decode_write(DecodeArgs a) {
+    const int n_anchor = a.H2 * a.W2 * 2;
+    const int base = blockIdx.x * kDecodeTile + threadIdx.x * kPerThread;
+    bool keep[kPerThread];
+    int c = 0;
+#pragma unroll
+    for (int q = 0; q < kPerThread; ++q) {
+        const int ai = base + q;
+        keep[q] = ai < n_anchor && a.head[size_t(ai >> 1) * 16 + (ai & 1) * 8] > a.thr;
+        c += keep[q];
+    }
+    int tot;
+    int pos = a.tile_counts[blockIdx.x] + block_excl_scan256(c, &tot);
+    const float diag = sqrtf(a.aw * a.aw + a.al * a.al);
+#pragma unroll
+    for (int q = 0; q < kPerThread; ++q) {
+        if (!keep[q]) continue;
+        const int ai = base + q;
+        const int cell = ai >> 1, an = ai & 1;
+        const int i = cell / a.W2, j = cell - (cell / a.W2) * a.W2;
+        const float *r = a.head + size_t(cell) * 16 + an * 8;
+        const float xa = a.x0 + (float(j) + 0.5f) * a.dx;
+        const float ya = a.y0 + (float(i) + 0.5f) * a.dy;
+        float *o = a.rec + size_t(pos) * 9;
+        o[0] = xa + r[1] * diag;
+        o[1] = ya + r[2] * diag;
+        o[2] = a.az + r[3] * a.ah;
+        o[3] = a.aw * expf(r[4]);
+        o[4] = a.al * expf(r[5]);
+        o[5] = a.ah * expf(r[6]);
+        o[6] = (an ? a.ayaw1 : a.ayaw0) + r[7];
+        o[7] = 1.0f / (1.0f + expf(-r[0]));
+        o[8] = __int_as_float(ai);
+        ++pos;
+    }
+}
+
+}  // namespace
+
+hipError_t warp_fuse(bool bf16, bool attn, const WarpArgs &a, hipStream_t s) {
+    return bf16 ? warp_dispatch<uint16_t>(attn, a, s) : warp_dispatch<float>(attn, a, s);
+}
+
+hipError_t head1x1(bool bf16, const void *in, const void *wt, const float *bias, float *out,
+                   int32_t M, int32_t C, hipStream_t s) {
+    const unsigned g = unsigned((M + 63) / 64);
+    if (bf16)
+        k_head<uint16_t><<<g, 256, 0, s>>>(static_cast<const uint16_t *>(in),
+                                           static_cast<const uint16_t *>(wt), bias, out, M, C);
+    else
+        k_head<float><<<g, 256, 0, s>>>(static_cast<const float *>(in), static_cast<const float *>(wt),
+                                        bias, out, M, C);
+    return hipGetLastError();
+}
+
+hipError_t decode(const DecodeArgs &a, hipStream_t s) {
+    const int n_anchor = a.H2 * a.W2 * 2;
+    const int n_tiles = (n_anchor + kDecodeTile - 1) / kDecodeTile;
+    k_decode_count<<<n_tiles, 256, 0, s>>>(a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    k_decode_scan<<<1, 256, 0, s>>>(a, n_tiles);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    k_decode_write<<<n_tiles, 256, 0, s>>>(a);
+    return hipGetLastError();
+}
+
+}  // namespace kern
+}  // namespace rtcc

@@ -1,0 +1,220 @@
+"""The C ABI: both libraries load and export every function of
+include/rtcc.h; the release controller, driven through the host test
+library (controller + C ABI linked against a recording executor), follows
+the state machine, validation and release rules of Sec. IV-C."""
+
+import ctypes
+import math
+import os
+import re
+import threading
+import time
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import network as N
+from paper_2608_08330_amd import rtcc as R
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _header_functions():
+    text = open(os.path.join(ROOT, "include", "rtcc.h")).read()
+    return sorted(set(re.findall(r"RTCC_API\s+[\w\s\*]+?\b(rtcc_\w+)\s*\(", text)))
+
+
+def test_header_and_binding_agree():
+    assert sorted(R.EXPORTS) == _header_functions()
+
+
+@pytest.mark.parametrize("kind", ["gpu", "host"])
+def test_library_loads_and_exports_every_symbol(kind):
+    lib = R.load(kind)
+    for name in _header_functions():
+        assert hasattr(lib, name), name
+    assert R.load(kind).rtcc_status_str(6) == b"RTCC_E_INFEASIBLE"
+
+
+# --------------------------------------------------------------- controller
+
+def _host_log(clear=True):
+    lib = R.load("host")
+    buf = ctypes.create_string_buffer(1 << 20)
+    lib.rtcc_hosttest_log(buf, len(buf), 1 if clear else 0)
+    return [l for l in buf.value.decode().splitlines() if l]
+
+
+@pytest.fixture
+def host_ctx():
+    cfg = synth.config("t_attn")
+    fr = synth.make_frame(cfg)
+    ctx = R.rtcc_create(R.model_desc(cfg), R.weights_blob(cfg, fr["weights"]), kind="host")
+    _host_log()
+    yield cfg, fr, ctx
+    ctx.close()
+
+
+def _status(fn, *a):
+    try:
+        fn(*a)
+        return R.RTCC_OK
+    except R.RtccError as e:
+        return e.status
+
+
+def test_release_mode_dispatches_each_branch_at_its_event(host_ctx):
+    cfg, fr, ctx = host_ctx
+    R.rtcc_set_mode(ctx, R.RTCC_MODE_RELEASE)
+    R.rtcc_begin_frame(ctx, time.monotonic() - 10)
+    order = [2, 0, 3, 1]
+    for i, k in enumerate(order):
+        assert R.rtcc_get_branch_state(ctx, k) == R.RTCC_WAITING
+        R.rtcc_release_branch(ctx, k, fr["points"][k], fr["poses"][k], 0.1 * i)
+        assert R.rtcc_get_branch_state(ctx, k) == R.RTCC_RUNNING
+        assert _host_log()[-1].startswith("dispatch %d " % k)
+    det = R.rtcc_join_and_detect(ctx)
+    assert all(R.rtcc_get_branch_state(ctx, k) == R.RTCC_FINISHED for k in range(4))
+    np.testing.assert_allclose(det["arrival_s"], [0.1, 0.3, 0.0, 0.2])
+    assert _host_log()[-1].startswith("join")
+
+
+def test_barrier_mode_dispatches_all_at_last_event_in_index_order(host_ctx):
+    cfg, fr, ctx = host_ctx
+    R.rtcc_set_mode(ctx, R.RTCC_MODE_BARRIER)
+    R.rtcc_begin_frame(ctx, time.monotonic() - 10)
+    for i, k in enumerate([3, 1, 2]):
+        R.rtcc_release_branch(ctx, k, fr["points"][k], fr["poses"][k], 0.1 * i)
+        assert R.rtcc_get_branch_state(ctx, k) == R.RTCC_RELEASED
+    assert not any(l.startswith("dispatch") for l in _host_log(clear=False))
+    R.rtcc_release_branch(ctx, 0, fr["points"][0], fr["poses"][0], 0.5)
+    disp = [l.split()[1] for l in _host_log() if l.startswith("dispatch")]
+    assert disp == ["0", "1", "2", "3"]
+    R.rtcc_join_and_detect(ctx)
+
+
+def test_validation_errors_leave_branch_waiting(host_ctx):
+    cfg, fr, ctx = host_ctx
+    pts, pose = fr["points"][0], fr["poses"][0]
+    # no frame open
+    assert _status(R.rtcc_release_branch, ctx, 0, pts, pose, 0.0) == R.RTCC_E_STATE
+    t0 = time.monotonic()
+    R.rtcc_begin_frame(ctx, t0)
+    assert _status(R.rtcc_release_branch, ctx, 7, pts, pose, 0.0) == R.RTCC_E_ARG
+    assert _status(R.rtcc_release_branch, ctx, -1, pts, pose, 0.0) == R.RTCC_E_ARG
+    too_many = np.zeros((cfg["n_points"] + 1, 4), np.float32)
+    assert _status(R.rtcc_release_branch, ctx, 0, too_many, pose, 0.0) == R.RTCC_E_MALFORMED
+    assert _status(R.rtcc_release_branch, ctx, 0, None, pose, 0.0, 5) == R.RTCC_E_MALFORMED
+    assert _status(R.rtcc_release_branch, ctx, 0, pts, (math.nan, 0, 0), 0.0) == R.RTCC_E_MALFORMED
+    assert _status(R.rtcc_release_branch, ctx, 0, pts, pose, math.inf) == R.RTCC_E_MALFORMED
+    assert _status(R.rtcc_release_branch, ctx, 0, pts, pose, -1.0) == R.RTCC_E_MALFORMED
+    # an event claiming an arrival 100 s from now is premature
+    assert _status(R.rtcc_release_branch, ctx, 0, pts, pose, 100.0) == R.RTCC_E_PREMATURE
+    assert R.rtcc_get_branch_state(ctx, 0) == R.RTCC_WAITING
+    assert not any(l.startswith("dispatch") for l in _host_log())
+    # a valid event, then a duplicate
+    R.rtcc_release_branch(ctx, 0, pts, pose, 0.0)
+    assert _status(R.rtcc_release_branch, ctx, 0, pts, pose, 0.0) == R.RTCC_E_DUPLICATE
+    # mode change inside a frame
+    assert _status(R.rtcc_set_mode, ctx, R.RTCC_MODE_BARRIER) == R.RTCC_E_STATE
+    assert _status(R.rtcc_begin_frame, ctx, t0) == R.RTCC_E_STATE
+
+
+def test_infeasible_frame_withholds_fusion(host_ctx):
+    cfg, fr, ctx = host_ctx
+    R.rtcc_begin_frame(ctx, time.monotonic() - 1)
+    for k in (0, 1, 3):
+        R.rtcc_release_branch(ctx, k, fr["points"][k], fr["poses"][k], 0.0)
+    assert _status(R.rtcc_join_and_detect, ctx) == R.RTCC_E_INFEASIBLE
+    assert not any(l.startswith("join") for l in _host_log())
+    # the frame is closed; a new one can start and complete
+    R.rtcc_begin_frame(ctx, time.monotonic() - 1)
+    for k in range(4):
+        R.rtcc_release_branch(ctx, k, fr["points"][k], fr["poses"][k], 0.0)
+    R.rtcc_join_and_detect(ctx)
+
+
+def test_barrier_infeasible_dispatches_nothing(host_ctx):
+    cfg, fr, ctx = host_ctx
+    R.rtcc_set_mode(ctx, R.RTCC_MODE_BARRIER)
+    R.rtcc_begin_frame(ctx, time.monotonic() - 1)
+    for k in (0, 1, 2):
+        R.rtcc_release_branch(ctx, k, fr["points"][k], fr["poses"][k], 0.0)
+    assert _status(R.rtcc_join_and_detect, ctx) == R.RTCC_E_INFEASIBLE
+    assert not any(l.startswith(("dispatch", "join")) for l in _host_log())
+
+
+def test_staging_buffer_is_zero_copy(host_ctx):
+    cfg, fr, ctx = host_ctx
+    stg = R.rtcc_staging_buffer(ctx, 2)
+    assert stg.shape == (cfg["n_points"], 4)
+    n = 100
+    stg[:n] = fr["points"][2][:n]
+    R.rtcc_begin_frame(ctx, time.monotonic() - 1)
+    R.rtcc_release_branch(ctx, 2, stg[:n], fr["poses"][2], 0.0)
+    assert _host_log()[-1] == "dispatch 2 n=100 src=staging staged=1"
+
+
+def test_concurrent_releases_from_threads(host_ctx):
+    cfg, fr, ctx = host_ctx
+    for _ in range(20):
+        R.rtcc_begin_frame(ctx, time.monotonic() - 1)
+        errs = []
+
+        def rel(k):
+            try:
+                R.rtcc_release_branch(ctx, k, fr["points"][k], fr["poses"][k], 0.0)
+            except Exception as e:  # pragma: no cover
+                errs.append(e)
+
+        th = [threading.Thread(target=rel, args=(k,)) for k in range(4)]
+        for t in th:
+            t.start()
+        for t in th:
+            t.join()
+        assert not errs
+        R.rtcc_join_and_detect(ctx)
+        log = _host_log()
+        assert sorted(l.split()[1] for l in log if l.startswith("dispatch")) == ["0", "1", "2", "3"]
+
+
+def test_pose_affines_match_oracle(host_ctx):
+    cfg, fr, ctx = host_ctx
+    R.rtcc_begin_frame(ctx, time.monotonic() - 1)
+    for k in range(4):
+        R.rtcc_release_branch(ctx, k, fr["points"][k], fr["poses"][k], 0.0)
+    R.rtcc_join_and_detect(ctx)
+    line = [l for l in _host_log() if l.startswith("join")][-1]
+    mats = [list(map(float, m.split(","))) for m in re.findall(r"\[([^\]]+)\]", line)]
+    for k in range(4):
+        M, t = N.index_affine(fr["poses"][k], cfg)
+        want = [M[0, 0], M[0, 1], t[0], M[1, 0], M[1, 1], t[1]]
+        np.testing.assert_allclose(mats[k], want, rtol=1e-4, atol=1e-4)
+    assert mats[0] == [1.0, 0.0, 0.0, 0.0, 1.0, 0.0] or mats[0][:3] == [1.0, 0.0, 0.0]
+
+
+@pytest.mark.parametrize("field,value", [
+    ("n_agents", 0), ("n_agents", 17), ("c_pfn", 48), ("pillar_size", 0.0), ("n_anchors", 3),
+    ("precision", 5), ("fusion", 9), ("max_points", 0), ("abi_version", 99),
+])
+def test_bad_descriptor_rejected(field, value):
+    cfg = synth.config("t_max")
+    w = R.weights_blob(cfg, synth.make_weights(cfg))
+    d = R.model_desc(cfg)
+    setattr(d, field, value)
+    with pytest.raises(R.RtccError) as ei:
+        R.rtcc_create(d, w, kind="host")
+    assert ei.value.status == R.RTCC_E_ARG
+
+
+def test_weight_blob_size_and_values_checked():
+    cfg = synth.config("t_max")
+    w = R.weights_blob(cfg, synth.make_weights(cfg))
+    with pytest.raises(R.RtccError) as ei:
+        R.rtcc_create(R.model_desc(cfg), w[:-1], kind="host")
+    assert ei.value.status == R.RTCC_E_ARG
+    bad = w.copy()
+    bad[3] = np.nan
+    with pytest.raises(R.RtccError):
+        R.rtcc_create(R.model_desc(cfg), bad, kind="host")

@@ -1,0 +1,144 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle.
+
+Pillar cells and counts are compared bit for bit; activations by max-norm
+relative error (1e-4 fp32, 2e-2 bf16); detections as sets with a tolerance
+band around the threshold.  RTCC and barrier runs of a frame must give
+bitwise identical outputs."""
+
+import sys
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import network as N
+from paper_2608_08330_amd import rtcc as R
+from tests.helpers import TOL, compare_detections, make_ctx, rel_err, run_frame, tensors
+
+pytestmark = pytest.mark.gpu
+
+_CACHE = {}
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def _oracle(name):
+    if name not in _CACHE:
+        fr = synth.make_frame(name)
+        _CACHE[name] = (fr, N.forward(fr, keep=True))
+    return _CACHE[name]
+
+
+def _check_frame(cfg, fr, ref, got, with_stages=True):
+    tol = TOL[cfg["precision"]]
+    K = cfg["K"]
+    for k in range(K):
+        e = ref["enc"][k]
+        assert np.array_equal(got["cells"][k], e["cells"].astype(np.int32)), "pillar cells, agent %d" % k
+        assert np.array_equal(got["counts"][k], e["counts"].astype(np.int32)), "pillar counts, agent %d" % k
+        err = rel_err(got["canvas"][k], e["canvas"].ravel())
+        assert err <= tol, ("canvas", k, err)
+        if with_stages:
+            for s, so in enumerate(e["stage_out"]):
+                err = rel_err(got["stage"][k][s], so.ravel())
+                assert err <= tol, ("stage", s, k, err)
+        err = rel_err(got["slot"][k], e["slot"].ravel())
+        assert err <= tol, ("slot", k, err)
+    err = rel_err(got["fused"], ref["fused"].ravel())
+    assert err <= tol, ("fused", err)
+    err = rel_err(got["head"], ref["head"].ravel())
+    assert err <= tol, ("head", err)
+
+
+@pytest.mark.parametrize("name", ["t_max", "t_attn", "c1", "c2", "c3"])
+def test_frame_parity_and_mode_identity(name):
+    _say("parity %s" % name)
+    cfg = synth.config(name)
+    fr, ref = _oracle(name)
+    with make_ctx(cfg, fr) as ctx:
+        a = synth.arrival_draws(cfg, 1)[0] * 1e-3 if cfg["arrivals"]["kind"] != "uplink" else None
+        det_r = run_frame(ctx, fr, R.RTCC_MODE_RELEASE, a)
+        got_r = tensors(ctx, cfg)
+        _check_frame(cfg, fr, ref, got_r)
+        compare_detections(det_r, ref["det"], cfg, ref["head"])
+        det_b = run_frame(ctx, fr, R.RTCC_MODE_BARRIER, a)
+        got_b = tensors(ctx, cfg)
+    # RTCC and barrier: bitwise identical outputs and identical box sets
+    for key in ("canvas", "slot"):
+        for k in range(cfg["K"]):
+            assert np.array_equal(got_r[key][k].view(np.uint32), got_b[key][k].view(np.uint32))
+    assert np.array_equal(got_r["fused"].view(np.uint32), got_b["fused"].view(np.uint32))
+    assert np.array_equal(got_r["head"].view(np.uint32), got_b["head"].view(np.uint32))
+    assert np.array_equal(det_r["anchor_idx"], det_b["anchor_idx"])
+    assert np.array_equal(det_r["boxes"].view(np.uint32), det_b["boxes"].view(np.uint32))
+
+
+def test_repeated_frames_are_bitwise_identical():
+    cfg = synth.config("t_attn")
+    fr, _ref = _oracle("t_attn")
+    with make_ctx(cfg, fr) as ctx:
+        outs = []
+        for _ in range(3):
+            run_frame(ctx, fr)
+            outs.append(tensors(ctx, cfg, with_stages=False))
+    for o in outs[1:]:
+        assert np.array_equal(o["fused"].view(np.uint32), outs[0]["fused"].view(np.uint32))
+        assert np.array_equal(o["head"].view(np.uint32), outs[0]["head"].view(np.uint32))
+
+
+def test_serial_executor_matches_per_branch_streams():
+    cfg = synth.config("t_max")
+    fr, _ref = _oracle("t_max")
+    with make_ctx(cfg, fr) as a:
+        run_frame(a, fr)
+        ta = tensors(a, cfg, with_stages=False)
+    with make_ctx(cfg, fr, exec=R.RTCC_EXEC_SERIAL) as b:
+        run_frame(b, fr)
+        tb = tensors(b, cfg, with_stages=False)
+    assert np.array_equal(ta["head"].view(np.uint32), tb["head"].view(np.uint32))
+
+
+def _edge_frame():
+    """t_max frame with adversarial inputs: an empty agent, one cell holding
+    500 points (cap 32), points on cell edges and range limits, NaN/Inf."""
+    cfg = synth.config("t_max")
+    fr = synth.make_frame(cfg)
+    pts = [p.copy() for p in fr["points"]]
+    pts[0] = np.zeros((0, 4), dtype=np.float32)
+    p1 = pts[1]
+    p1[:500, 0] = 0.1
+    p1[:500, 1] = -0.3
+    p1[500:520, 0] = np.float32(cfg["x_range"][1])           # x = xmax: dropped
+    p1[520:540, 0] = np.float32(cfg["x_range"][0])           # x = xmin: kept
+    p1[540:560, 1] = np.float32(-8.8) + np.float32(0.4) * 3  # near a row edge
+    p1[560:570, 2] = np.nan
+    p1[570:580, 3] = np.inf
+    p1[580:590, 2] = np.float32(cfg["z_range"][1])           # z = zmax: dropped
+    fr["points"] = pts
+    return cfg, fr
+
+
+def test_edge_cases_empty_agent_overfull_cell_and_invalid_points():
+    cfg, fr = _edge_frame()
+    ref = N.forward(fr, keep=True)
+    assert ref["enc"][1]["counts"].max() >= 500
+    with make_ctx(cfg, fr, max_points=cfg["n_points"]) as ctx:
+        run_frame(ctx, fr)
+        got = tensors(ctx, cfg)
+    assert got["cells"][0].size == 0 and got["counts"][0].size == 0
+    _check_frame(cfg, fr, ref, got)
+
+
+def test_max_points_exactly_and_ragged_tail():
+    cfg = synth.config("t_attn")
+    fr = synth.make_frame(cfg)
+    # a point count that is not a multiple of any block size
+    fr["points"] = [p[:4999 - 7 * k] for k, p in enumerate(fr["points"])]
+    ref = N.forward(fr, keep=True)
+    with make_ctx(cfg, fr, max_points=4999) as ctx:
+        run_frame(ctx, fr)
+        got = tensors(ctx, cfg)
+    _check_frame(cfg, fr, ref, got)
