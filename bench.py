@@ -1,0 +1,267 @@
+#!/usr/bin/env python
+"""Benchmark of the RTCC fork-join detector path on one MI355X.
+
+One step = one complete frame through the C ABI: K branch encoders
+(pillarize, point-feature net, 3x3 conv backbone, upsample) released on
+device-resident inputs, then the join (warp, fusion, head, decode, D2H).
+
+Output: one JSON line with
+  value       encoder throughput, TFLOP/s = algorithmic encoder FLOPs of the
+              timed frames / wall time of the timed frames
+  roofline    the dominant kernel (3x3 conv implicit GEMM): algorithmic
+              FLOPs / summed HIP-event durations of its launches, against
+              the bf16 dense MFMA peak
+  latency     p50 / p95 complete-detection latency T^det, RTCC vs barrier,
+              over replayed synthetic arrival traces (pinned host inputs,
+              H2D included, as on the release path)
+  cpu_baseline  the fp64 CPU oracle's encoder throughput on a bounded sample
+"""
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "p50/p95 complete-detection latency ms (RTCC vs barrier); encoder TFLOP/s"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3    # MI355X fp32 (vector / MFMA fp32)
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def grid(cfg):
+    W = int(round((cfg["x_range"][1] - cfg["x_range"][0]) / cfg["pillar"]))
+    H = int(round((cfg["y_range"][1] - cfg["y_range"][0]) / cfg["pillar"]))
+    return H, W
+
+
+def layer_work(cfg):
+    """Algorithmic FLOPs / bytes of every node of one agent's encoder and of
+    the post-join subgraph, in node-time order."""
+    H, W = grid(cfg)
+    elt = 2 if cfg["precision"] == "bf16" else 4
+    convs, ups = [], []
+    h, w, c = H, W, cfg["c_pfn"]
+    stage = []
+    for stride, co, n in cfg["stages"]:
+        for l in range(n):
+            s = stride if l == 0 else 1
+            ho, wo = -(-h // s), -(-w // s)
+            convs.append(dict(flops=2.0 * ho * wo * co * 9 * c, M=ho * wo, N=co, K=9 * c,
+                              bytes=(h * w * c + ho * wo * co + 9 * c * co) * elt))
+            h, w, c = ho, wo, co
+        stage.append((h, w, c))
+    H2, W2 = stage[0][0], stage[0][1]
+    if cfg["up_channels"]:
+        for (hs, ws, cs) in stage:
+            ups.append(dict(flops=2.0 * H2 * W2 * cs * cfg["up_channels"],
+                            bytes=(hs * ws * cs + H2 * W2 * cfg["up_channels"]) * elt))
+        C = cfg["up_channels"] * len(cfg["stages"])
+    else:
+        C = stage[-1][2]
+    return dict(H=H, W=W, H2=H2, W2=W2, C=C, elt=elt, convs=convs, ups=ups)
+
+
+def encoder_flops(cfg, lw, n_used):
+    """PFN (linear 4 -> C on every used point) + convs + upsampling."""
+    pfn = 2.0 * 4 * cfg["c_pfn"] * n_used
+    return pfn + sum(c["flops"] for c in lw["convs"]) + sum(u["flops"] for u in lw["ups"])
+
+
+def timed_steps(ctx, cfg, frame, dev_pts, steps, warmup, R, torch):
+    """Warm-up, then exactly `steps` timed frames bracketed by device syncs.
+    Returns wall seconds and the per-node HIP-event times of every step."""
+    K = cfg["K"]
+    n = [len(p) for p in frame["points"]]
+
+    def one():
+        R.rtcc_begin_frame(ctx, time.monotonic() - 1.0)
+        for k in range(K):
+            R.rtcc_release_branch_device(ctx, k, dev_pts[k].data_ptr(), n[k], frame["poses"][k], 0.0)
+        return R.rtcc_join_and_detect(ctx)
+
+    for _ in range(warmup):
+        one()
+    torch.cuda.synchronize()
+    node = []
+    t = time.perf_counter()
+    for _ in range(steps):
+        one()
+        node.append(R.rtcc_node_times(ctx))
+    torch.cuda.synchronize()
+    return time.perf_counter() - t, node
+
+
+def cpu_baseline(cfg, frame, budget_s):
+    """The fp64 oracle (untuned) on one agent's encoder, repeated while the
+    budget lasts.  Reports encoder GFLOP/s on the host cores."""
+    import numpy as np
+    from oracle import network as N
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    pw = N.prepared_weights(cfg, frame["weights"])
+    lw = layer_work(cfg)
+    done, flops = 0, 0.0
+    t = time.perf_counter()
+    while True:
+        k = done % cfg["K"]
+        enc = N.encoder(frame["points"][k], cfg, pw)
+        used = int(np.minimum(enc["counts"], cfg["max_pts"]).sum())
+        flops += encoder_flops(cfg, lw, used)
+        done += 1
+        if time.perf_counter() - t >= budget_s:
+            break
+    dt = time.perf_counter() - t
+    return dict(value=flops / dt / 1e12, unit="TFLOP/s", cores=int(threads), kind="oracle",
+                sample="%d agent encoder(s) of the %s frame (fp64 numpy oracle), %.1f s" % (done, cfg["name"], dt))
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="c5")
+    ap.add_argument("--exec", choices=["serial", "streams"], default="serial")
+    ap.add_argument("--latency-traces", type=int, default=30)
+    ap.add_argument("--latency-reps", type=int, default=3)
+    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    a = ap.parse_args(argv)
+
+    if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the detector path runs on a single MI355X and has no "
+              "multi-GPU mode (--gpus must be 1)", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+    import synth
+    from paper_2608_08330_amd import rtcc as R
+    from paper_2608_08330_amd import replay
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+
+    cfg = synth.config(a.config)
+    frame = synth.make_frame(cfg)
+    lw = layer_work(cfg)
+    K = cfg["K"]
+    o = R.rtcc_runtime_opts()
+    o.exec = R.RTCC_EXEC_SERIAL if a.exec == "serial" else R.RTCC_EXEC_PER_BRANCH_STREAMS
+    o.node_timing = 1
+    o.premature_tol_s = 1e-6
+    ctx = R.rtcc_create(R.model_desc(cfg), R.weights_blob(cfg, frame["weights"]), o)
+    dev_pts = [torch.from_numpy(p).to("cuda") for p in frame["points"]]
+    torch.cuda.synchronize()
+
+    wall, node = timed_steps(ctx, cfg, frame, dev_pts, a.steps, a.warmup, R, torch)
+    ms_per_step = wall / a.steps * 1e3
+
+    # used points per agent (PFN FLOPs), from the library's pillar counts
+    used = []
+    for k in range(K):
+        cnt = R.rtcc_get_tensor(ctx, R.RTCC_T_PILLAR_COUNTS, k, np.int32)
+        used.append(int(np.minimum(cnt, cfg["max_pts"]).sum()))
+    enc_flops = sum(encoder_flops(cfg, lw, u) for u in used)
+    value = enc_flops * a.steps / wall / 1e12
+
+    # node layout per agent: h2d, pillar, pfn, conv[L], up[S or 1]; post: warp_fuse, head, decode
+    L, S = len(lw["convs"]), max(len(lw["ups"]), 1)
+    per_agent = 3 + L + S
+    node = np.array(node)  # [steps, nodes] ms
+    conv_ms = 0.0
+    for k in range(K):
+        base = k * per_agent + 3
+        conv_ms += node[:, base:base + L].sum()
+    conv_flops = sum(c["flops"] for c in lw["convs"]) * K * a.steps
+    conv_launches = L * K * a.steps
+    achieved = conv_flops / (conv_ms * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if cfg["precision"] == "bf16" else PEAK_FP32_TFLOPS
+    pillar_ms = sum(node[:, k * per_agent + 1].sum() + node[:, k * per_agent + 2].sum() for k in range(K))
+    P = [int(R.rtcc_tensor_bytes(ctx, R.RTCC_T_PILLAR_CELLS, k)) // 4 for k in range(K)]
+    pil_bytes = sum(16 * len(frame["points"][k]) + 8 * P[k] + lw["H"] * lw["W"] * cfg["c_pfn"] * lw["elt"]
+                    for k in range(K)) * a.steps
+    post0 = K * per_agent
+    warp_ms = node[:, post0].sum()
+    slot_bytes = lw["H2"] * lw["W2"] * lw["C"] * lw["elt"]
+    warp_bytes = (K + 1) * slot_bytes * a.steps
+
+    layers = []
+    for l, c in enumerate(lw["convs"]):
+        us = float(np.mean([node[:, k * per_agent + 3 + l] for k in range(K)])) * 1e3
+        layers.append({"M": c["M"], "N": c["N"], "K": c["K"], "us": round(us, 2),
+                       "tflops": round(c["flops"] / (us * 1e-6) / 1e12, 1)})
+    out = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if cfg["precision"] == "bf16" else "f32",
+        "data": "synthetic (seeded points, poses, He-normal weights, arrival traces)",
+        "config": {
+            "workload": "%s: %d agents x %d points, %dx%d BEV, %s, %s fusion" % (
+                cfg["name"], K, cfg["n_points"], lw["H"], lw["W"], cfg["precision"], cfg["fusion"]),
+            "agents": K, "executor": a.exec, "inputs": "device-resident",
+        },
+        "roofline": {
+            "bound": "mfma", "kernel": "conv3x3 implicit GEMM (k_igemm)",
+            "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 4), "traffic": None,
+            "launches": conv_launches, "avg_launch_us": round(conv_ms * 1e3 / conv_launches, 3),
+        },
+        "secondary_rooflines": {
+            "pillar_pfn_canvas": {"bound": "hbm", "achieved": round(pil_bytes / (pillar_ms * 1e-3) / 1e9, 1),
+                                  "peak": PEAK_HBM_GBS, "unit": "GB/s"},
+            "warp_fuse": {"bound": "hbm", "achieved": round(warp_bytes / (warp_ms * 1e-3) / 1e9, 1),
+                          "peak": PEAK_HBM_GBS, "unit": "GB/s"},
+        },
+        "conv_layers": layers,
+        "node_ms_mean": {
+            "pillar": round(float(np.mean([node[:, k * per_agent + 1] for k in range(K)])), 4),
+            "pfn_canvas": round(float(np.mean([node[:, k * per_agent + 2] for k in range(K)])), 4),
+            "conv_total_per_agent": round(conv_ms / (K * a.steps), 4),
+            "up_total_per_agent": round(float(np.sum([node[:, k * per_agent + 3 + L:k * per_agent + per_agent]
+                                                      for k in range(K)]) / (K * a.steps)), 4),
+            "warp_fuse": round(float(node[:, post0].mean()), 4),
+            "head": round(float(node[:, post0 + 1].mean()), 4),
+            "decode": round(float(node[:, post0 + 2].mean()), 4),
+        },
+    }
+    print("# throughput done: %.3f ms/step, %.1f TFLOP/s" % (ms_per_step, value), file=sys.stderr, flush=True)
+
+    if a.latency_traces > 0:
+        if cfg["arrivals"]["kind"] == "uplink":
+            raise SystemExit("latency replay of uplink-driven configs runs in the load-sweep report")
+        arr = synth.arrival_draws(cfg, a.latency_traces) * 1e-3
+        rows, identical = replay.replay_traces(ctx, frame["points"], frame["poses"], arr, a.latency_reps)
+        lat = replay.summarize(rows)
+        lat["reps"] = a.latency_reps
+        lat["outputs_identical_rtcc_vs_barrier"] = bool(identical)
+        lat["rtcc_below_barrier_every_trace"] = bool(lat["wins"] == len(rows))
+        out["latency"] = lat
+        print("# latency done", file=sys.stderr, flush=True)
+
+    if not a.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, frame, a.cpu_budget)
+    ctx.close()
+    print(json.dumps(out))
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -54,6 +54,26 @@ class HipExecutor : public Executor {
         const size_t n_cells = size_t(p.H) * p.W;
         const size_t n_tiles = (n_cells + kern::kScanTile - 1) / kern::kScanTile;
         const size_t over_cap = n_max / size_t(p.d.max_points_per_pillar + 1) + 1;
+        // Split-K for convolutions whose tile grid leaves CUs idle: K slices
+        // of >= 8 steps until the grid covers two blocks per CU.
+        int n_cu = 0;
+        HIP_TRY(hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev_));
+        const int target = 2 * (n_cu > 0 ? n_cu : 256);
+        splits_.assign(p.convs.size(), 1);
+        size_t ws_bytes = 0;
+        for (size_t l = 0; l < p.convs.size(); ++l) {
+            const ConvLayer &c = p.convs[l];
+            const int tiles = kern::gemm_tiles(c.Ho * c.Wo, c.Co);
+            const int kt = kern::gemm_k_steps(p.bf16, false, c.Ci);
+            int best = 1;
+            if (tiles < target / 2)
+                for (int sp = 2; sp <= 16 && tiles * best < target; ++sp)
+                    if (kt % sp == 0 && kt / sp >= 8) best = sp;
+            splits_[l] = best;
+            if (best > 1) ws_bytes = std::max(ws_bytes, size_t(best) * c.Ho * c.Wo * c.Co * 4);
+        }
+        HIP_TRY(alloc(&d_zero, 256));
+        HIP_TRY(hipMemset(d_zero, 0, 256));
         br_.resize(p.K);
         for (int k = 0; k < p.K; ++k) {
             Branch &b = br_[k];
@@ -75,6 +95,7 @@ class HipExecutor : public Executor {
                 const ConvLayer &c = p.convs[l];
                 HIP_TRY(alloc(&b.d_act[l], size_t(c.Ho) * c.Wo * c.Co * p.elt));
             }
+            if (ws_bytes) HIP_TRY(alloc(&b.d_ws, ws_bytes));
             if (!p.ups.empty()) HIP_TRY(alloc(&b.d_slotbuf, size_t(p.H2) * p.W2 * p.c_slot * p.elt));
             else b.d_slotbuf = b.d_act.back();
             HIP_TRY(hipStreamCreateWithFlags(&b.stream, hipStreamNonBlocking));
@@ -284,7 +305,7 @@ class HipExecutor : public Executor {
         void *d_pts = nullptr, *d_cell = nullptr, *d_slot = nullptr, *d_member = nullptr;
         void *d_pcells = nullptr, *d_pcounts = nullptr, *d_overfull = nullptr;
         void *d_counts = nullptr, *d_offsets = nullptr, *d_tiles = nullptr, *d_meta = nullptr;
-        void *d_canvas = nullptr, *d_slotbuf = nullptr;
+        void *d_canvas = nullptr, *d_slotbuf = nullptr, *d_ws = nullptr;
         std::vector<void *> d_act;
         hipStream_t stream = nullptr;
         hipEvent_t done = nullptr, h2d_done = nullptr;
@@ -371,6 +392,9 @@ class HipExecutor : public Executor {
             ga.u = 1;
             ga.ldo = c.Co;
             ga.c_off = 0;
+            ga.splits = splits_[l];
+            ga.zero = d_zero;
+            ga.ws = static_cast<float *>(b.d_ws);
             HIP_TRY(kern::conv3x3(p.bf16, ga, s));
             if (timing) HIP_TRY(hipEventRecord(b.ev[ev], s));
             ++ev;
@@ -388,6 +412,9 @@ class HipExecutor : public Executor {
             ga.u = u.u;
             ga.ldo = p.c_slot;
             ga.c_off = u.c_off;
+            ga.splits = 1;
+            ga.zero = d_zero;
+            ga.ws = nullptr;
             HIP_TRY(kern::deconv(p.bf16, ga, s));
             if (timing) HIP_TRY(hipEventRecord(b.ev[ev], s));
             ++ev;
@@ -523,7 +550,8 @@ class HipExecutor : public Executor {
     int dev_ = -1;
     std::vector<Branch> br_;
     std::vector<void *> dev_allocs_;
-    void *d_mat = nullptr, *d_bias = nullptr;
+    void *d_mat = nullptr, *d_bias = nullptr, *d_zero = nullptr;
+    std::vector<int> splits_;
     void *d_fused = nullptr, *d_head = nullptr, *d_dec_tiles = nullptr, *d_rec = nullptr, *d_count = nullptr;
     float *h_rec = nullptr;
     void *h_small = nullptr;

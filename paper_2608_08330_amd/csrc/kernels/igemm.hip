@@ -9,18 +9,28 @@
 //           pixels, N = up channels, K = C_in; row (iy, ix) lands on output
 //           pixel (iy*u + py, ix*u + px) of the concatenated slot, at a
 //           channel offset, and is skipped outside the cropped grid.
-// Epilogue: + bias, ReLU, round to the stored dtype.
+// Epilogue: + bias, ReLU, round to the stored dtype; or, with split-K, a
+// float32 partial tile per K slice that k_splitk_reduce sums in slice order.
 //
-// Tiling: a 256-thread block (4 wavefronts of 64, 2 x 2) computes a BM x BN
-// tile; every wavefront owns (BM/2) x (BN/2) made of 16 x 16 MFMA tiles.
-// Per K step the block stages 64 bytes of every A row and every weight row
-// in LDS (double buffered, rows padded to 80 bytes so the 16 lanes that
-// read one 16-byte column hit 64 distinct banks).  One K step is one
-// v_mfma_f32_16x16x32_bf16 per tile (bf16), or four v_mfma_f32_16x16x4_f32
-// (fp32).  The weight fragment is the MFMA A operand, so each lane's four
-// accumulators are four consecutive output channels of one pixel and the
-// epilogue stores 8 (bf16) or 16 (fp32) contiguous bytes.  The K loop order
-// is fixed, so results do not depend on M, the grid or the stream.
+// Pipeline (per block of WGM x WGN wavefronts, BM x BN tile):
+//   * every K step stages 64 bytes of each of the BM activation rows and BN
+//     weight rows in LDS, straight from global memory with
+//     global_load_lds_dwordx4 (no register staging): one wave instruction
+//     fills 1 KB = 16 rows, lane i writing bytes [16 i, 16 i + 16);
+//   * STAGES LDS buffers form a ring; loads run STAGES - 1 steps ahead of
+//     the MFMAs, and a step waits only for its own loads (vmcnt);
+//   * 16-byte vectors of a row are XOR-swizzled by bits 2..3 of the row
+//     index, so the 16 lanes that read one MFMA fragment column hit 64
+//     distinct banks;
+//   * padding and rows past M / N read a zero line in global memory;
+//   * per step one v_mfma_f32_16x16x32_bf16 per 16 x 16 tile (bf16), or four
+//     v_mfma_f32_16x16x4_f32 (fp32); the weight fragment is the MFMA A
+//     operand, so each lane's four accumulators are four consecutive
+//     output channels of one pixel.
+// Blocks are ordered so that every XCD (block id mod 8) receives contiguous
+// M tiles, which share halo rows in that XCD's L2.  The K loop order and the
+// split-K reduction order are fixed: results do not depend on M, the grid or
+// the stream.
 #include "kernels.hpp"
 
 namespace rtcc {
@@ -30,8 +40,15 @@ namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
 
-constexpr int kRowPitch = 5;  // uint4 per LDS row: 64 data bytes + 16 pad
+constexpr int kRowBytes = 64;  // bytes of one row per K step
+
+// s_waitcnt immediate for gfx9: vmcnt = n, expcnt and lgkmcnt unconstrained.
+template <int N>
+struct VmWait {
+    static constexpr int imm = (N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8);
+};
 
 template <typename T>
 struct Traits;
@@ -72,97 +89,125 @@ struct Traits<float> {
     }
 };
 
-template <typename T, int BM, int BN, bool DECONV>
-__global__ __launch_bounds__(256) void k_igemm(GemmArgs a) {
-    constexpr int EPV = Traits<T>::EPV;
-    constexpr int BK = 4 * EPV;          // elements per row per K step (64 bytes)
-    constexpr int AV = BM / 64;          // A vectors per thread per step
-    constexpr int BV = BN / 64;          // B vectors per thread per step
-    constexpr int WM = BM / 2, WN = BN / 2;
-    constexpr int FM = WM / 16, FN = WN / 16;
+// 16 bytes per lane from global memory into LDS at m0 + 16 * lane.  Issued
+// as inline assembly so that the compiler does not treat the DMA as an
+// unknown LDS write that every later LDS read must wait for; the kernel
+// waits for these loads itself with s_waitcnt vmcnt (they retire in issue
+// order, and all of them are drained before the epilogue).
+__device__ inline void load_lds16(const void *g, uint32_t lds_addr) {
+    // the address is wave-uniform (wave index and stage only)
+    const uint32_t a = __builtin_amdgcn_readfirstlane(lds_addr);
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(a)
+                 : "memory", "m0");
+}
 
-    __shared__ uint4 As[2][BM * kRowPitch];
-    __shared__ uint4 Bs[2][BN * kRowPitch];
+template <typename T, int BM, int BN, int WGM, int WGN, int STAGES, bool DECONV>
+__global__ __launch_bounds__(64 * WGM * WGN) void k_igemm(GemmArgs a) {
+    constexpr int NW = WGM * WGN;                    // wavefronts per block
+    constexpr int EPV = Traits<T>::EPV;
+    constexpr int BK = kRowBytes / int(sizeof(T));  // elements per row per K step
+    constexpr int IA = BM / 16, IB = BN / 16;        // 1-KB load instructions per step
+    static_assert((IA + IB) % NW == 0, "load instructions must split evenly over waves");
+    constexpr int LPS = (IA + IB) / NW;              // loads per wave per step
+    constexpr int WM = BM / WGM, WN = BN / WGN;
+    constexpr int FM = WM / 16, FN = WN / 16;
+    static_assert(FM >= 1 && FN >= 1, "wave tile below one MFMA tile");
+    constexpr int A_BYTES = BM * kRowBytes, B_BYTES = BN * kRowBytes;
+    constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
+
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[STAGES * STAGE_BYTES];
+    const uint32_t lds_base = __builtin_amdgcn_readfirstlane(
+        uint32_t(reinterpret_cast<uintptr_t>((lds_void *)smem)));
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int wm = wave & 1, wn = wave >> 1;
+    const int wm = wave % WGM, wn = wave / WGM;
 
     const int Ci = a.Ci;
     const int M = DECONV ? a.Hi * a.Wi : a.Ho * a.Wo;
     const int N = a.N;
     const int K = DECONV ? Ci : 9 * Ci;
-    const int KT = K / BK;
-    const int m0 = blockIdx.x * BM;
-    const int n0 = blockIdx.y * BN;
+    const int KT_all = K / BK;
+    const int KT = KT_all / a.splits;
+
+    // XCD-aware tile order: block ids are dealt to the 8 XCDs round-robin;
+    // give each XCD a contiguous run of tiles.
+    const int mt = (M + BM - 1) / BM;
+    const int nt = (N + BN - 1) / BN;
+    int bid = blockIdx.x;
+    const int nbx = gridDim.x;
+    if ((nbx & 7) == 0) bid = (bid & 7) * (nbx >> 3) + (bid >> 3);
+    const int m_tile = bid % mt;
+    const int rest = bid / mt;  // n tile, then split
+    const int n_tile = rest % nt;
+    const int split = rest / nt;
     const int phase = DECONV ? int(blockIdx.z) : 0;
+    const int m0 = m_tile * BM;
+    const int n0 = n_tile * BN;
+    const int kt0 = split * KT;
 
     const T *in = static_cast<const T *>(a.in);
     const T *wt = static_cast<const T *>(a.wt) + (DECONV ? size_t(phase) * N * Ci : 0);
+    const char *zero = static_cast<const char *>(a.zero);
 
-    // Per-thread A rows: pixel coordinates fixed for the whole K loop.
-    int a_row[AV], a_kv[AV], a_iy[AV], a_ix[AV];
-    bool a_ok[AV];
+    // Load instruction c of a step covers 16 rows: A rows 16 c .. (c < IA)
+    // or B rows 16 (c - IA) ..; wave w issues c = w, w + NW, ...  Lane i
+    // takes row + (i >> 2) and logical vector (i & 3) ^ ((row >> 2) & 3).
+    int l_iy[LPS], l_ix[LPS], l_vec[LPS], l_row[LPS];
+    bool l_ok[LPS], l_isa[LPS];
 #pragma unroll
-    for (int r = 0; r < AV; ++r) {
-        const int v = tid + 256 * r;
-        a_row[r] = v >> 2;
-        a_kv[r] = v & 3;
-        const int m = m0 + a_row[r];
-        a_ok[r] = m < M;
-        if (DECONV) {
-            a_iy[r] = m;  // flat input pixel
-            a_ix[r] = 0;
+    for (int j = 0; j < LPS; ++j) {
+        const int c = wave + j * NW;
+        const bool isa = c < IA;
+        const int row = 16 * (isa ? c : c - IA) + (lane >> 2);
+        l_isa[j] = isa;
+        l_row[j] = row;
+        l_vec[j] = (lane & 3) ^ ((row >> 2) & 3);
+        if (isa) {
+            const int m = m0 + row;
+            l_ok[j] = m < M;
+            if (DECONV) {
+                l_iy[j] = m;
+                l_ix[j] = 0;
+            } else {
+                const int oy = m / a.Wo, ox = m - (m / a.Wo) * a.Wo;
+                l_iy[j] = oy * a.stride - 1;
+                l_ix[j] = ox * a.stride - 1;
+            }
         } else {
-            const int oy = m / a.Wo, ox = m - (m / a.Wo) * a.Wo;
-            a_iy[r] = oy * a.stride - 1;
-            a_ix[r] = ox * a.stride - 1;
+            l_ok[j] = n0 + row < N;
+            l_iy[j] = 0;
+            l_ix[j] = 0;
         }
     }
-    int b_row[BV], b_kv[BV];
-    bool b_ok[BV];
-#pragma unroll
-    for (int r = 0; r < BV; ++r) {
-        const int v = tid + 256 * r;
-        b_row[r] = v >> 2;
-        b_kv[r] = v & 3;
-        b_ok[r] = n0 + b_row[r] < N;
-    }
 
-    uint4 ra[AV], rb[BV];
-    auto load_global = [&](int kt) {
-        const int k0 = kt * BK;
+    auto issue = [&](int kt, int buf) {
+        const int k0 = (kt0 + kt) * BK;
         int tap = 0, c0 = k0;
         if (!DECONV) {
             tap = k0 / Ci;
             c0 = k0 - tap * Ci;
         }
         const int dy = tap / 3, dx = tap - (tap / 3) * 3;
+        const uint32_t st = lds_base + buf * STAGE_BYTES;
 #pragma unroll
-        for (int r = 0; r < AV; ++r) {
-            uint4 v = make_uint4(0, 0, 0, 0);
-            if (DECONV) {
-                if (a_ok[r]) v = *reinterpret_cast<const uint4 *>(in + size_t(a_iy[r]) * Ci + c0 + a_kv[r] * EPV);
-            } else {
-                const int iy = a_iy[r] + dy, ix = a_ix[r] + dx;
-                if (a_ok[r] && iy >= 0 && iy < a.Hi && ix >= 0 && ix < a.Wi)
-                    v = *reinterpret_cast<const uint4 *>(in + (size_t(iy) * a.Wi + ix) * Ci + c0 + a_kv[r] * EPV);
+        for (int j = 0; j < LPS; ++j) {
+            const int c = wave + j * NW;
+            const void *g = zero;
+            if (l_isa[j]) {
+                if (DECONV) {
+                    if (l_ok[j]) g = in + size_t(l_iy[j]) * Ci + c0 + l_vec[j] * EPV;
+                } else {
+                    const int iy = l_iy[j] + dy, ix = l_ix[j] + dx;
+                    if (l_ok[j] && iy >= 0 && iy < a.Hi && ix >= 0 && ix < a.Wi)
+                        g = in + (size_t(iy) * a.Wi + ix) * Ci + c0 + l_vec[j] * EPV;
+                }
+            } else if (l_ok[j]) {
+                g = wt + size_t(n0 + l_row[j]) * K + k0 + l_vec[j] * EPV;
             }
-            ra[r] = v;
+            load_lds16(g, st + c * 1024);
         }
-#pragma unroll
-        for (int r = 0; r < BV; ++r) {
-            uint4 v = make_uint4(0, 0, 0, 0);
-            if (b_ok[r]) v = *reinterpret_cast<const uint4 *>(wt + size_t(n0 + b_row[r]) * K + k0 + b_kv[r] * EPV);
-            rb[r] = v;
-        }
-    };
-    auto store_lds = [&](int buf) {
-#pragma unroll
-        for (int r = 0; r < AV; ++r) As[buf][a_row[r] * kRowPitch + a_kv[r]] = ra[r];
-#pragma unroll
-        for (int r = 0; r < BV; ++r) Bs[buf][b_row[r] * kRowPitch + b_kv[r]] = rb[r];
     };
 
     f32x4_t acc[FM][FN];
@@ -171,28 +216,62 @@ __global__ __launch_bounds__(256) void k_igemm(GemmArgs a) {
 #pragma unroll
         for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    load_global(0);
-    store_lds(0);
-    __syncthreads();
+#pragma unroll
+    for (int s = 0; s < STAGES - 1; ++s)
+        if (s < KT) issue(s, s);
 
+    // fragment addresses (bytes within a stage): row r, logical vector fk
     const int fr = lane & 15, fk = lane >> 4;
+    int a_off[FM], b_off[FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+        const int r = wm * WM + i * 16 + fr;
+        a_off[i] = r * kRowBytes + ((fk ^ ((r >> 2) & 3)) << 4);
+    }
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+        const int r = wn * WN + j * 16 + fr;
+        b_off[j] = A_BYTES + r * kRowBytes + ((fk ^ ((r >> 2) & 3)) << 4);
+    }
+
     for (int kt = 0; kt < KT; ++kt) {
-        const int buf = kt & 1;
-        if (kt + 1 < KT) load_global(kt + 1);
+        // Loads of steps kt+1 .. kt+STAGES-2 may stay in flight.
+        if (kt + STAGES - 2 < KT) __builtin_amdgcn_s_waitcnt(VmWait<(STAGES - 2) * LPS>::imm);
+        else __builtin_amdgcn_s_waitcnt(VmWait<0>::imm);
+        // No fence: only this step's loads are awaited above, later steps
+        // stay in flight across the barrier.
+        __builtin_amdgcn_s_barrier();  // step kt visible to all waves; step kt-1 consumed
+        asm volatile("" ::: "memory");  // keep LDS reads below the barrier
+        if (kt + STAGES - 1 < KT) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
+        const unsigned char *st = smem + (kt % STAGES) * STAGE_BYTES;
         uint4 af[FM], bfr[FN];
 #pragma unroll
-        for (int i = 0; i < FM; ++i) af[i] = As[buf][(wm * WM + i * 16 + fr) * kRowPitch + fk];
+        for (int i = 0; i < FM; ++i) af[i] = *reinterpret_cast<const uint4 *>(st + a_off[i]);
 #pragma unroll
-        for (int j = 0; j < FN; ++j) bfr[j] = Bs[buf][(wn * WN + j * 16 + fr) * kRowPitch + fk];
+        for (int j = 0; j < FN; ++j) bfr[j] = *reinterpret_cast<const uint4 *>(st + b_off[j]);
 #pragma unroll
         for (int i = 0; i < FM; ++i)
 #pragma unroll
             for (int j = 0; j < FN; ++j) acc[i][j] = Traits<T>::mma(bfr[j], af[i], acc[i][j]);
-        if (kt + 1 < KT) store_lds(buf ^ 1);
-        __syncthreads();
     }
 
     // Epilogue: lane holds channels n .. n+3 of pixel m for every tile.
+    if (a.splits > 1) {
+        float *ws = a.ws + size_t(split) * M * N;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+            const int m = m0 + wm * WM + i * 16 + fr;
+            if (m >= M) continue;
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+                const int n = n0 + wn * WN + j * 16 + fk * 4;
+                if (n >= N) continue;
+                *reinterpret_cast<float4 *>(ws + size_t(m) * N + n) =
+                    make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+            }
+        }
+        return;
+    }
     T *out = static_cast<T *>(a.out);
     const int py = DECONV ? phase / a.u : 0, px = DECONV ? phase - py * a.u : 0;
 #pragma unroll
@@ -221,18 +300,47 @@ __global__ __launch_bounds__(256) void k_igemm(GemmArgs a) {
     }
 }
 
-template <typename T, bool DECONV>
-hipError_t launch(const GemmArgs &a, hipStream_t s) {
+// out[m][n] = ReLU(bias[n] + sum over slices s = 0 .. S-1 of ws[s][m][n]),
+// summed in slice order.  Four channels per thread.
+template <typename T>
+__global__ __launch_bounds__(256) void k_splitk_reduce(GemmArgs a) {
+    const int M = a.Ho * a.Wo;
+    const int N = a.N;
+    const int64_t q = int64_t(blockIdx.x) * 256 + threadIdx.x;
+    const int64_t total = int64_t(M) * (N / 4);
+    if (q >= total) return;
+    const int m = int(q / (N / 4));
+    const int n = int(q - int64_t(m) * (N / 4)) * 4;
+    float4 s = *reinterpret_cast<const float4 *>(a.ws + size_t(m) * N + n);
+    for (int sp = 1; sp < a.splits; ++sp) {
+        const float4 t = *reinterpret_cast<const float4 *>(a.ws + (size_t(sp) * M + m) * N + n);
+        s.x += t.x;
+        s.y += t.y;
+        s.z += t.z;
+        s.w += t.w;
+    }
+    Traits<T>::store4(static_cast<T *>(a.out) + size_t(m) * a.ldo + a.c_off + n,
+                      fmaxf(s.x + a.bias[n], 0.f), fmaxf(s.y + a.bias[n + 1], 0.f),
+                      fmaxf(s.z + a.bias[n + 2], 0.f), fmaxf(s.w + a.bias[n + 3], 0.f));
+}
+
+template <typename T, int BM, int BN, int WGM, int WGN, int STAGES, bool DECONV>
+hipError_t launch_cfg(const GemmArgs &a, hipStream_t s) {
     const int M = DECONV ? a.Hi * a.Wi : a.Ho * a.Wo;
     const unsigned gz = DECONV ? unsigned(a.u * a.u) : 1u;
-    if (a.N % 128 == 0) {
-        dim3 g((M + 127) / 128, a.N / 128, gz);
-        k_igemm<T, 128, 128, DECONV><<<g, 256, 0, s>>>(a);
-    } else {
-        dim3 g((M + 127) / 128, (a.N + 63) / 64, gz);
-        k_igemm<T, 128, 64, DECONV><<<g, 256, 0, s>>>(a);
-    }
+    const unsigned nx = unsigned((M + BM - 1) / BM) * unsigned((a.N + BN - 1) / BN) * unsigned(a.splits);
+    k_igemm<T, BM, BN, WGM, WGN, STAGES, DECONV><<<dim3(nx, 1, gz), 64 * WGM * WGN, 0, s>>>(a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || a.splits == 1) return e;
+    const int64_t total = int64_t(M) * (a.N / 4);
+    k_splitk_reduce<T><<<unsigned((total + 255) / 256), 256, 0, s>>>(a);
     return hipGetLastError();
+}
+
+template <typename T, bool DECONV>
+hipError_t launch(const GemmArgs &a, hipStream_t s) {
+    if (a.N % 128 == 0) return launch_cfg<T, 128, 128, 4, 2, 4, DECONV>(a, s);
+    return launch_cfg<T, 128, 64, 4, 1, 4, DECONV>(a, s);
 }
 
 }  // namespace
@@ -244,6 +352,13 @@ hipError_t conv3x3(bool bf16, const GemmArgs &a, hipStream_t s) {
 hipError_t deconv(bool bf16, const GemmArgs &a, hipStream_t s) {
     return bf16 ? launch<uint16_t, true>(a, s) : launch<float, true>(a, s);
 }
+
+int gemm_k_steps(bool bf16, bool is_deconv, int Ci) {
+    const int bk = bf16 ? 32 : 16;
+    return (is_deconv ? Ci : 9 * Ci) / bk;
+}
+
+int gemm_tiles(int M, int N) { return ((M + 127) / 128) * (N % 128 == 0 ? N / 128 : (N + 63) / 64); }
 
 }  // namespace kern
 }  // namespace rtcc

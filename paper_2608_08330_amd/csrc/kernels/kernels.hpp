@@ -76,9 +76,15 @@ struct GemmArgs {
     int32_t stride;    // conv only
     int32_t u;         // deconv only
     int32_t ldo, c_off;
+    int32_t splits;    // K slices (>= 1); > 1 needs ws and a conv (no deconv)
+    const void *zero;  // >= 16 zero bytes in device memory (padding reads)
+    float *ws;         // split-K partials [splits][M][N] float32
 };
 hipError_t conv3x3(bool bf16, const GemmArgs &a, hipStream_t s);
 hipError_t deconv(bool bf16, const GemmArgs &a, hipStream_t s);
+// K steps of one GEMM (K / elements per 64-byte row chunk) and output tiles.
+int gemm_k_steps(bool bf16, bool is_deconv, int Ci);
+int gemm_tiles(int M, int N);
 
 // ------------------------------------------------------------ post-join
 struct WarpArgs {
