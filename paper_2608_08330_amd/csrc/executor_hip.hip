@@ -54,23 +54,15 @@ class HipExecutor : public Executor {
         const size_t n_cells = size_t(p.H) * p.W;
         const size_t n_tiles = (n_cells + kern::kScanTile - 1) / kern::kScanTile;
         const size_t over_cap = n_max / size_t(p.d.max_points_per_pillar + 1) + 1;
-        // Split-K for convolutions whose tile grid leaves CUs idle: K slices
-        // of >= 8 steps until the grid covers two blocks per CU.
+        // Kernel variant and split-K of every conv layer.
         int n_cu = 0;
         HIP_TRY(hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev_));
-        const int target = 2 * (n_cu > 0 ? n_cu : 256);
-        splits_.assign(p.convs.size(), 1);
+        if (n_cu <= 0) n_cu = 256;
+        plans_.clear();
         size_t ws_bytes = 0;
-        for (size_t l = 0; l < p.convs.size(); ++l) {
-            const ConvLayer &c = p.convs[l];
-            const int tiles = kern::gemm_tiles(c.Ho * c.Wo, c.Co);
-            const int kt = kern::gemm_k_steps(p.bf16, false, c.Ci);
-            int best = 1;
-            if (tiles < target / 2)
-                for (int sp = 2; sp <= 16 && tiles * best < target; ++sp)
-                    if (kt % sp == 0 && kt / sp >= 8) best = sp;
-            splits_[l] = best;
-            if (best > 1) ws_bytes = std::max(ws_bytes, size_t(best) * c.Ho * c.Wo * c.Co * 4);
+        for (const ConvLayer &c : p.convs) {
+            plans_.push_back(kern::conv_plan(p.bf16, c.Hi, c.Wi, c.Ci, c.Ho, c.Wo, c.Co, c.stride, n_cu));
+            ws_bytes = std::max(ws_bytes, plans_.back().ws_bytes);
         }
         HIP_TRY(alloc(&d_zero, 256));
         HIP_TRY(hipMemset(d_zero, 0, 256));
@@ -392,7 +384,8 @@ class HipExecutor : public Executor {
             ga.u = 1;
             ga.ldo = c.Co;
             ga.c_off = 0;
-            ga.splits = splits_[l];
+            ga.splits = plans_[l].splits;
+            ga.variant = plans_[l].variant;
             ga.zero = d_zero;
             ga.ws = static_cast<float *>(b.d_ws);
             HIP_TRY(kern::conv3x3(p.bf16, ga, s));
@@ -413,6 +406,7 @@ class HipExecutor : public Executor {
             ga.ldo = p.c_slot;
             ga.c_off = u.c_off;
             ga.splits = 1;
+            ga.variant = kern::kConvImplicit;
             ga.zero = d_zero;
             ga.ws = nullptr;
             HIP_TRY(kern::deconv(p.bf16, ga, s));
@@ -551,7 +545,7 @@ class HipExecutor : public Executor {
     std::vector<Branch> br_;
     std::vector<void *> dev_allocs_;
     void *d_mat = nullptr, *d_bias = nullptr, *d_zero = nullptr;
-    std::vector<int> splits_;
+    std::vector<kern::ConvPlan> plans_;
     void *d_fused = nullptr, *d_head = nullptr, *d_dec_tiles = nullptr, *d_rec = nullptr, *d_count = nullptr;
     float *h_rec = nullptr;
     void *h_small = nullptr;

@@ -19,9 +19,9 @@
 //     fills 1 KB = 16 rows, lane i writing bytes [16 i, 16 i + 16);
 //   * STAGES LDS buffers form a ring; loads run STAGES - 1 steps ahead of
 //     the MFMAs, and a step waits only for its own loads (vmcnt);
-//   * 16-byte vectors of a row are XOR-swizzled by bits 2..3 of the row
-//     index, so the 16 lanes that read one MFMA fragment column hit 64
-//     distinct banks;
+//   * 16-byte vectors of a row are XOR-swizzled by bits 1..2 of the row
+//     index: ds_read_b128 serves 8 lanes (128 bytes, 32 banks) per cycle,
+//     and any 8 consecutive rows then cover the 32 banks exactly once;
 //   * padding and rows past M / N read a zero line in global memory;
 //   * per step one v_mfma_f32_16x16x32_bf16 per 16 x 16 tile (bf16), or four
 //     v_mfma_f32_16x16x4_f32 (fp32); the weight fragment is the MFMA A
@@ -153,7 +153,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_igemm(GemmArgs a) {
 
     // Load instruction c of a step covers 16 rows: A rows 16 c .. (c < IA)
     // or B rows 16 (c - IA) ..; wave w issues c = w, w + NW, ...  Lane i
-    // takes row + (i >> 2) and logical vector (i & 3) ^ ((row >> 2) & 3).
+    // takes row + (i >> 2) and logical vector (i & 3) ^ ((row >> 1) & 3).
     int l_iy[LPS], l_ix[LPS], l_vec[LPS], l_row[LPS];
     bool l_ok[LPS], l_isa[LPS];
 #pragma unroll
@@ -163,7 +163,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_igemm(GemmArgs a) {
         const int row = 16 * (isa ? c : c - IA) + (lane >> 2);
         l_isa[j] = isa;
         l_row[j] = row;
-        l_vec[j] = (lane & 3) ^ ((row >> 2) & 3);
+        l_vec[j] = (lane & 3) ^ ((row >> 1) & 3);
         if (isa) {
             const int m = m0 + row;
             l_ok[j] = m < M;
@@ -226,12 +226,12 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_igemm(GemmArgs a) {
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
         const int r = wm * WM + i * 16 + fr;
-        a_off[i] = r * kRowBytes + ((fk ^ ((r >> 2) & 3)) << 4);
+        a_off[i] = r * kRowBytes + ((fk ^ ((r >> 1) & 3)) << 4);
     }
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
         const int r = wn * WN + j * 16 + fr;
-        b_off[j] = A_BYTES + r * kRowBytes + ((fk ^ ((r >> 2) & 3)) << 4);
+        b_off[j] = A_BYTES + r * kRowBytes + ((fk ^ ((r >> 1) & 3)) << 4);
     }
 
     for (int kt = 0; kt < KT; ++kt) {
@@ -300,6 +300,178 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_igemm(GemmArgs a) {
     }
 }
 
+// Stride-1 3x3 convolution as a halo-tiled direct convolution.
+//
+// A block owns TH x 16 output pixels and BN output channels.  The K loop runs
+// over input-channel chunks of 64 bytes; per chunk the block stages the
+// (TH + 2) x 18 input patch (halo included, zero outside the grid) in LDS
+// once, and the 9 taps then read their shifted 16-pixel rows from it, so an
+// input element is fetched from L2 once per chunk instead of once per tap.
+// Only the per-tap weight tile (BN rows x 64 bytes) streams through a
+// 3-buffer ring two taps ahead.  Eight wavefronts: 4 along output rows x 2
+// along channels; every wave holds (TH / 4) x (BN / 32) MFMA tiles.  The tap
+// loop is unrolled, so every s_waitcnt vmcnt bound is a constant:
+// after the weights of step s were issued, the loads still allowed in flight
+// are the next step's weights plus, at taps 1 and 2, the next chunk's patch.
+template <typename T, int TH, int BN>
+__global__ __launch_bounds__(512) void k_conv3s1(GemmArgs a) {
+    constexpr int NW = 8;
+    constexpr int EPV = Traits<T>::EPV;
+    constexpr int BK = kRowBytes / int(sizeof(T));
+    constexpr int TW = 16, HW = TW + 2, HH = TH + 2;
+    constexpr int HALO = HH * HW;
+    constexpr int IA = ((HALO + 15) / 16 + NW - 1) / NW * NW;  // 1-KB patch loads, multiple of NW
+    constexpr int LA = IA / NW;
+    constexpr int IB = BN / 16;
+    static_assert(IB % NW == 0, "weight loads must split over the waves");
+    constexpr int LB = IB / NW;
+    constexpr int A_BYTES = IA * 1024, B_BYTES = BN * kRowBytes;
+    constexpr int FM = TH / 4, FN = BN / 32;
+
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * A_BYTES + 3 * B_BYTES];
+    const uint32_t lds_base = __builtin_amdgcn_readfirstlane(
+        uint32_t(reinterpret_cast<uintptr_t>((lds_void *)smem)));
+    const uint32_t lds_b = lds_base + 2 * A_BYTES;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave & 3, wn = wave >> 2;
+
+    const int Ci = a.Ci, N = a.N, Ho = a.Ho, Wo = a.Wo;
+    const int K = 9 * Ci;
+    const int CH = (Ci / BK) / a.splits;  // chunks of this split
+
+    const int tx = (Wo + TW - 1) / TW, ty = (Ho + TH - 1) / TH;
+    const int nt = N / BN;
+    int bid = blockIdx.x;
+    const int nbx = gridDim.x;
+    if ((nbx & 7) == 0) bid = (bid & 7) * (nbx >> 3) + (bid >> 3);
+    const int sp_tile = bid % (tx * ty);
+    const int rest = bid / (tx * ty);
+    const int n_tile = rest % nt;
+    const int split = rest / nt;
+    const int oy0 = (sp_tile / tx) * TH, ox0 = (sp_tile % tx) * TW;
+    const int n0 = n_tile * BN;
+    const int c_begin = split * CH;
+
+    const T *in = static_cast<const T *>(a.in);
+    const T *wt = static_cast<const T *>(a.wt);
+    const char *zero = static_cast<const char *>(a.zero);
+
+    // patch rows this lane loads (halo pixel index, input coordinates)
+    int p_off[LA], p_vec[LA];
+    bool p_ok[LA];
+#pragma unroll
+    for (int j = 0; j < LA; ++j) {
+        const int row = 16 * (wave + j * NW) + (lane >> 2);
+        p_vec[j] = (lane & 3) ^ ((row >> 1) & 3);
+        const int hy = row / HW, hx = row - (row / HW) * HW;
+        const int iy = oy0 - 1 + hy, ix = ox0 - 1 + hx;
+        p_ok[j] = row < HALO && iy >= 0 && iy < a.Hi && ix >= 0 && ix < a.Wi;
+        p_off[j] = p_ok[j] ? (iy * a.Wi + ix) : 0;
+    }
+    int w_row[LB], w_vec[LB];
+#pragma unroll
+    for (int j = 0; j < LB; ++j) {
+        const int row = 16 * (wave + j * NW) + (lane >> 2);
+        w_row[j] = row;
+        w_vec[j] = (lane & 3) ^ ((row >> 1) & 3);
+    }
+
+    auto issue_patch = [&](int chunk) {
+        const int c0 = (c_begin + chunk) * BK;
+        const uint32_t dst = lds_base + (chunk & 1) * A_BYTES;
+#pragma unroll
+        for (int j = 0; j < LA; ++j) {
+            const void *g = zero;
+            if (p_ok[j]) g = in + size_t(p_off[j]) * Ci + c0 + p_vec[j] * EPV;
+            load_lds16(g, dst + (wave + j * NW) * 1024);
+        }
+    };
+    // step s = chunk * 9 + tap: weight rows k = tap * Ci + chunk channels
+    auto issue_w = [&](int s) {
+        const int chunk = s / 9, tap = s - (s / 9) * 9;
+        const int k0 = tap * Ci + (c_begin + chunk) * BK;
+        const uint32_t dst = lds_b + (s % 3) * B_BYTES;
+#pragma unroll
+        for (int j = 0; j < LB; ++j)
+            load_lds16(wt + size_t(n0 + w_row[j]) * K + k0 + w_vec[j] * EPV, dst + (wave + j * NW) * 1024);
+    };
+
+    f32x4_t acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    const int fr = lane & 15, fk = lane >> 4;
+    int b_off[FN];
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+        const int r = wn * (BN / 2) + j * 16 + fr;
+        b_off[j] = r * kRowBytes + ((fk ^ ((r >> 1) & 3)) << 4);
+    }
+
+    issue_patch(0);
+    issue_w(0);
+    issue_w(1);
+    const int S = CH * 9;
+    for (int c = 0; c < CH; ++c) {
+        const bool last = c + 1 == CH;
+        const unsigned char *pa = smem + (c & 1) * A_BYTES;
+#pragma unroll
+        for (int t = 0; t < 9; ++t) {
+            const int s = c * 9 + t;
+            if (!last) {
+                if (t == 1 || t == 2) __builtin_amdgcn_s_waitcnt(VmWait<LB + LA>::imm);
+                else __builtin_amdgcn_s_waitcnt(VmWait<LB>::imm);
+            } else {
+                if (t == 8) __builtin_amdgcn_s_waitcnt(VmWait<0>::imm);
+                else __builtin_amdgcn_s_waitcnt(VmWait<LB>::imm);
+            }
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+            if (s + 2 < S) issue_w(s + 2);
+            if (t == 0 && !last) issue_patch(c + 1);
+            const int dy = t / 3, dx = t % 3;
+            const unsigned char *pb = smem + 2 * A_BYTES + (s % 3) * B_BYTES;
+            uint4 af[FM], bfr[FN];
+#pragma unroll
+            for (int i = 0; i < FM; ++i) {
+                const int r = (wm * FM + i + dy) * HW + dx + fr;
+                af[i] = *reinterpret_cast<const uint4 *>(pa + r * kRowBytes + ((fk ^ ((r >> 1) & 3)) << 4));
+            }
+#pragma unroll
+            for (int j = 0; j < FN; ++j) bfr[j] = *reinterpret_cast<const uint4 *>(pb + b_off[j]);
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j) acc[i][j] = Traits<T>::mma(bfr[j], af[i], acc[i][j]);
+        }
+    }
+
+    const int ox = ox0 + fr;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+        const int oy = oy0 + wm * FM + i;
+        if (oy >= Ho || ox >= Wo) continue;
+        const size_t m = size_t(oy) * Wo + ox;
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+            const int n = n0 + wn * (BN / 2) + j * 16 + fk * 4;
+            if (a.splits > 1) {
+                *reinterpret_cast<float4 *>(a.ws + (size_t(split) * Ho * Wo + m) * N + n) =
+                    make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+            } else {
+                Traits<T>::store4(static_cast<T *>(a.out) + m * a.ldo + a.c_off + n,
+                                  fmaxf(acc[i][j][0] + a.bias[n + 0], 0.f), fmaxf(acc[i][j][1] + a.bias[n + 1], 0.f),
+                                  fmaxf(acc[i][j][2] + a.bias[n + 2], 0.f), fmaxf(acc[i][j][3] + a.bias[n + 3], 0.f));
+            }
+        }
+    }
+}
+
 // out[m][n] = ReLU(bias[n] + sum over slices s = 0 .. S-1 of ws[s][m][n]),
 // summed in slice order.  Four channels per thread.
 template <typename T>
@@ -337,8 +509,22 @@ hipError_t launch_cfg(const GemmArgs &a, hipStream_t s) {
     return hipGetLastError();
 }
 
+template <typename T, int TH>
+hipError_t launch_halo(const GemmArgs &a, hipStream_t s) {
+    const unsigned tiles = unsigned((a.Wo + 15) / 16) * unsigned((a.Ho + TH - 1) / TH);
+    const unsigned nx = tiles * unsigned(a.N / 128) * unsigned(a.splits);
+    k_conv3s1<T, TH, 128><<<dim3(nx), 512, 0, s>>>(a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || a.splits == 1) return e;
+    const int64_t total = int64_t(a.Ho) * a.Wo * (a.N / 4);
+    k_splitk_reduce<T><<<unsigned((total + 255) / 256), 256, 0, s>>>(a);
+    return hipGetLastError();
+}
+
 template <typename T, bool DECONV>
 hipError_t launch(const GemmArgs &a, hipStream_t s) {
+    if (!DECONV && a.variant == kConvHalo16) return launch_halo<T, 16>(a, s);
+    if (!DECONV && a.variant == kConvHalo8) return launch_halo<T, 8>(a, s);
     if (a.N % 128 == 0) return launch_cfg<T, 128, 128, 4, 2, 4, DECONV>(a, s);
     return launch_cfg<T, 128, 64, 4, 1, 4, DECONV>(a, s);
 }
@@ -353,9 +539,34 @@ hipError_t deconv(bool bf16, const GemmArgs &a, hipStream_t s) {
     return bf16 ? launch<uint16_t, true>(a, s) : launch<float, true>(a, s);
 }
 
-int gemm_k_steps(bool bf16, bool is_deconv, int Ci) {
+ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, int stride, int n_cu) {
+    (void)Hi;
+    (void)Wi;
     const int bk = bf16 ? 32 : 16;
-    return (is_deconv ? Ci : 9 * Ci) / bk;
+    ConvPlan p{kConvImplicit, 1, 0};
+    if (stride == 1 && Co % 128 == 0) {
+        const int tx = (Wo + 15) / 16, nt = Co / 128;
+        const int t16 = tx * ((Ho + 15) / 16) * nt, t8 = tx * ((Ho + 7) / 8) * nt;
+        if (t16 >= n_cu) {
+            p.variant = kConvHalo16;
+        } else {
+            p.variant = kConvHalo8;
+            const int chunks = Ci / bk;
+            // a K split costs an f32 partial round trip; split only until
+            // half the CUs have a tile (measured best on 64 x 64 grids)
+            if (t8 < n_cu / 2)
+                for (int sp = 2; sp <= chunks && t8 * p.splits < n_cu / 2; ++sp)
+                    if (chunks % sp == 0) p.splits = sp;
+        }
+    } else {
+        const int tiles = gemm_tiles(Ho * Wo, Co);
+        const int kt = 9 * Ci / bk;
+        if (tiles < n_cu)
+            for (int sp = 2; sp <= 16 && tiles * p.splits < 2 * n_cu; ++sp)
+                if (kt % sp == 0 && kt / sp >= 8) p.splits = sp;
+    }
+    if (p.splits > 1) p.ws_bytes = size_t(p.splits) * Ho * Wo * Co * 4;
+    return p;
 }
 
 int gemm_tiles(int M, int N) { return ((M + 127) / 128) * (N % 128 == 0 ? N / 128 : (N + 63) / 64); }

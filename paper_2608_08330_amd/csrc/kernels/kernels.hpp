@@ -77,13 +77,23 @@ struct GemmArgs {
     int32_t u;         // deconv only
     int32_t ldo, c_off;
     int32_t splits;    // K slices (>= 1); > 1 needs ws and a conv (no deconv)
+    int32_t variant;   // conv kernel: kConvImplicit, kConvHalo16, kConvHalo8
     const void *zero;  // >= 16 zero bytes in device memory (padding reads)
     float *ws;         // split-K partials [splits][M][N] float32
 };
+constexpr int kConvImplicit = 0;  // implicit GEMM (any stride)
+constexpr int kConvHalo16 = 1;    // stride-1 halo tiles of 16 x 16 pixels
+constexpr int kConvHalo8 = 2;     // stride-1 halo tiles of 8 x 16 pixels
+struct ConvPlan {
+    int variant;
+    int splits;
+    size_t ws_bytes;  // split-K workspace needed (0 without split)
+};
+// Kernel variant and K split of one 3x3 conv layer on a GPU with n_cu CUs.
+ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, int stride, int n_cu);
 hipError_t conv3x3(bool bf16, const GemmArgs &a, hipStream_t s);
 hipError_t deconv(bool bf16, const GemmArgs &a, hipStream_t s);
-// K steps of one GEMM (K / elements per 64-byte row chunk) and output tiles.
-int gemm_k_steps(bool bf16, bool is_deconv, int Ci);
+// Output tiles of the implicit GEMM.
 int gemm_tiles(int M, int N);
 
 // ------------------------------------------------------------ post-join
