@@ -308,35 +308,44 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_igemm(GemmArgs a) {
 // once, and the 9 taps then read their shifted 16-pixel rows from it, so an
 // input element is fetched from L2 once per chunk instead of once per tap.
 // Only the per-tap weight tile (BN rows x 64 bytes) streams through a
-// 3-buffer ring two taps ahead.  Eight wavefronts: 4 along output rows x 2
-// along channels; every wave holds (TH / 4) x (BN / 32) MFMA tiles.  The tap
+// 3-buffer ring two taps ahead.  WGM x WGN wavefronts: WGM along output rows,
+// WGN along channels; every wave holds (TH / WGM) x (BN / WGN / 16) MFMA tiles.
+// The tap
 // loop is unrolled, so every s_waitcnt vmcnt bound is a constant:
 // after the weights of step s were issued, the loads still allowed in flight
 // are the next step's weights plus, at taps 1 and 2, the next chunk's patch.
-template <typename T, int TH, int BN>
-__global__ __launch_bounds__(512) void k_conv3s1(GemmArgs a) {
-    constexpr int NW = 8;
+template <typename T, int TH, int BN, int WGM, int WGN, int RB>
+__global__ __launch_bounds__(64 * WGM * WGN) void k_conv3s1(GemmArgs a) {
+    constexpr int NW = WGM * WGN;
     constexpr int EPV = Traits<T>::EPV;
-    constexpr int BK = kRowBytes / int(sizeof(T));
+    constexpr int VPR = RB / 16;                 // 16-byte vectors per row and step
+    constexpr int RPI = 1024 / RB;               // rows per 1-KB load instruction
+    constexpr int KS = RB / 64;                  // MFMA k-substeps per step
+    constexpr int BK = RB / int(sizeof(T));      // channels per step
     constexpr int TW = 16, HW = TW + 2, HH = TH + 2;
     constexpr int HALO = HH * HW;
-    constexpr int IA = ((HALO + 15) / 16 + NW - 1) / NW * NW;  // 1-KB patch loads, multiple of NW
+    constexpr int IA = ((HALO + RPI - 1) / RPI + NW - 1) / NW * NW;  // patch loads, multiple of NW
     constexpr int LA = IA / NW;
-    constexpr int IB = BN / 16;
+    constexpr int IB = BN / RPI;
     static_assert(IB % NW == 0, "weight loads must split over the waves");
     constexpr int LB = IB / NW;
-    constexpr int A_BYTES = IA * 1024, B_BYTES = BN * kRowBytes;
-    constexpr int FM = TH / 4, FN = BN / 32;
+    constexpr int A_BYTES = IA * 1024, B_BYTES = BN * RB;
+    constexpr int FM = TH / WGM, FN = BN / WGN / 16;
+    static_assert(FM * WGM == TH && FN >= 1, "wave layout must tile the block");
 
     __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * A_BYTES + 3 * B_BYTES];
     const uint32_t lds_base = __builtin_amdgcn_readfirstlane(
         uint32_t(reinterpret_cast<uintptr_t>((lds_void *)smem)));
     const uint32_t lds_b = lds_base + 2 * A_BYTES;
 
+    // 16-byte vector v of row r sits at position v ^ swz(r); any 8
+    // consecutive rows then cover the 32 banks once per ds_read_b128 cycle.
+    auto swz = [](int r) { return VPR == 4 ? ((r >> 1) & 3) : (r & 7); };
+
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int wm = wave & 3, wn = wave >> 2;
+    const int wm = wave % WGM, wn = wave / WGM;
 
     const int Ci = a.Ci, N = a.N, Ho = a.Ho, Wo = a.Wo;
     const int K = 9 * Ci;
@@ -359,13 +368,12 @@ __global__ __launch_bounds__(512) void k_conv3s1(GemmArgs a) {
     const T *wt = static_cast<const T *>(a.wt);
     const char *zero = static_cast<const char *>(a.zero);
 
-    // patch rows this lane loads (halo pixel index, input coordinates)
     int p_off[LA], p_vec[LA];
     bool p_ok[LA];
 #pragma unroll
     for (int j = 0; j < LA; ++j) {
-        const int row = 16 * (wave + j * NW) + (lane >> 2);
-        p_vec[j] = (lane & 3) ^ ((row >> 1) & 3);
+        const int row = RPI * (wave + j * NW) + lane / VPR;
+        p_vec[j] = (lane % VPR) ^ swz(row);
         const int hy = row / HW, hx = row - (row / HW) * HW;
         const int iy = oy0 - 1 + hy, ix = ox0 - 1 + hx;
         p_ok[j] = row < HALO && iy >= 0 && iy < a.Hi && ix >= 0 && ix < a.Wi;
@@ -374,9 +382,9 @@ __global__ __launch_bounds__(512) void k_conv3s1(GemmArgs a) {
     int w_row[LB], w_vec[LB];
 #pragma unroll
     for (int j = 0; j < LB; ++j) {
-        const int row = 16 * (wave + j * NW) + (lane >> 2);
+        const int row = RPI * (wave + j * NW) + lane / VPR;
         w_row[j] = row;
-        w_vec[j] = (lane & 3) ^ ((row >> 1) & 3);
+        w_vec[j] = (lane % VPR) ^ swz(row);
     }
 
     auto issue_patch = [&](int chunk) {
@@ -389,7 +397,7 @@ __global__ __launch_bounds__(512) void k_conv3s1(GemmArgs a) {
             load_lds16(g, dst + (wave + j * NW) * 1024);
         }
     };
-    // step s = chunk * 9 + tap: weight rows k = tap * Ci + chunk channels
+    // step s = chunk * 9 + tap: weight columns k = tap * Ci + chunk channels
     auto issue_w = [&](int s) {
         const int chunk = s / 9, tap = s - (s / 9) * 9;
         const int k0 = tap * Ci + (c_begin + chunk) * BK;
@@ -406,12 +414,9 @@ __global__ __launch_bounds__(512) void k_conv3s1(GemmArgs a) {
         for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
     const int fr = lane & 15, fk = lane >> 4;
-    int b_off[FN];
+    int b_row[FN];
 #pragma unroll
-    for (int j = 0; j < FN; ++j) {
-        const int r = wn * (BN / 2) + j * 16 + fr;
-        b_off[j] = r * kRowBytes + ((fk ^ ((r >> 1) & 3)) << 4);
-    }
+    for (int j = 0; j < FN; ++j) b_row[j] = wn * (BN / WGN) + j * 16 + fr;
 
     issue_patch(0);
     issue_w(0);
@@ -423,6 +428,8 @@ __global__ __launch_bounds__(512) void k_conv3s1(GemmArgs a) {
 #pragma unroll
         for (int t = 0; t < 9; ++t) {
             const int s = c * 9 + t;
+            // loads allowed in flight after step s's weights: the next
+            // step's weights, and at taps 1 and 2 the next chunk's patch
             if (!last) {
                 if (t == 1 || t == 2) __builtin_amdgcn_s_waitcnt(VmWait<LB + LA>::imm);
                 else __builtin_amdgcn_s_waitcnt(VmWait<LB>::imm);
@@ -436,18 +443,23 @@ __global__ __launch_bounds__(512) void k_conv3s1(GemmArgs a) {
             if (t == 0 && !last) issue_patch(c + 1);
             const int dy = t / 3, dx = t % 3;
             const unsigned char *pb = smem + 2 * A_BYTES + (s % 3) * B_BYTES;
-            uint4 af[FM], bfr[FN];
 #pragma unroll
-            for (int i = 0; i < FM; ++i) {
-                const int r = (wm * FM + i + dy) * HW + dx + fr;
-                af[i] = *reinterpret_cast<const uint4 *>(pa + r * kRowBytes + ((fk ^ ((r >> 1) & 3)) << 4));
+            for (int ks = 0; ks < KS; ++ks) {
+                const int v = fk + 4 * ks;
+                uint4 af[FM], bfr[FN];
+#pragma unroll
+                for (int i = 0; i < FM; ++i) {
+                    const int r = (wm * FM + i + dy) * HW + dx + fr;
+                    af[i] = *reinterpret_cast<const uint4 *>(pa + r * RB + ((v ^ swz(r)) << 4));
+                }
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+                    bfr[j] = *reinterpret_cast<const uint4 *>(pb + b_row[j] * RB + ((v ^ swz(b_row[j])) << 4));
+#pragma unroll
+                for (int i = 0; i < FM; ++i)
+#pragma unroll
+                    for (int j = 0; j < FN; ++j) acc[i][j] = Traits<T>::mma(bfr[j], af[i], acc[i][j]);
             }
-#pragma unroll
-            for (int j = 0; j < FN; ++j) bfr[j] = *reinterpret_cast<const uint4 *>(pb + b_off[j]);
-#pragma unroll
-            for (int i = 0; i < FM; ++i)
-#pragma unroll
-                for (int j = 0; j < FN; ++j) acc[i][j] = Traits<T>::mma(bfr[j], af[i], acc[i][j]);
         }
     }
 
@@ -459,7 +471,7 @@ __global__ __launch_bounds__(512) void k_conv3s1(GemmArgs a) {
         const size_t m = size_t(oy) * Wo + ox;
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
-            const int n = n0 + wn * (BN / 2) + j * 16 + fk * 4;
+            const int n = n0 + wn * (BN / WGN) + j * 16 + fk * 4;
             if (a.splits > 1) {
                 *reinterpret_cast<float4 *>(a.ws + (size_t(split) * Ho * Wo + m) * N + n) =
                     make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
@@ -509,11 +521,11 @@ hipError_t launch_cfg(const GemmArgs &a, hipStream_t s) {
     return hipGetLastError();
 }
 
-template <typename T, int TH>
+template <typename T, int TH, int BN = 128, int WGM = 4, int WGN = 2, int RB = 64>
 hipError_t launch_halo(const GemmArgs &a, hipStream_t s) {
     const unsigned tiles = unsigned((a.Wo + 15) / 16) * unsigned((a.Ho + TH - 1) / TH);
-    const unsigned nx = tiles * unsigned(a.N / 128) * unsigned(a.splits);
-    k_conv3s1<T, TH, 128><<<dim3(nx), 512, 0, s>>>(a);
+    const unsigned nx = tiles * unsigned(a.N / BN) * unsigned(a.splits);
+    k_conv3s1<T, TH, BN, WGM, WGN, RB><<<dim3(nx), 64 * WGM * WGN, 0, s>>>(a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.splits == 1) return e;
     const int64_t total = int64_t(a.Ho) * a.Wo * (a.N / 4);
@@ -523,8 +535,13 @@ hipError_t launch_halo(const GemmArgs &a, hipStream_t s) {
 
 template <typename T, bool DECONV>
 hipError_t launch(const GemmArgs &a, hipStream_t s) {
-    if (!DECONV && a.variant == kConvHalo16) return launch_halo<T, 16>(a, s);
-    if (!DECONV && a.variant == kConvHalo8) return launch_halo<T, 8>(a, s);
+    if (!DECONV && a.variant != kConvImplicit) {
+        // 128-byte K steps when a chunk of that many channel bytes exists
+        const bool rb128 = (a.Ci * int(sizeof(T))) % 128 == 0;
+        if (a.variant == kConvHalo8)
+            return rb128 ? launch_halo<T, 8, 128, 4, 2, 128>(a, s) : launch_halo<T, 8, 128, 4, 2, 64>(a, s);
+        return rb128 ? launch_halo<T, 4, 128, 2, 2, 128>(a, s) : launch_halo<T, 4, 128, 2, 2, 64>(a, s);
+    }
     if (a.N % 128 == 0) return launch_cfg<T, 128, 128, 4, 2, 4, DECONV>(a, s);
     return launch_cfg<T, 128, 64, 4, 1, 4, DECONV>(a, s);
 }
@@ -542,20 +559,24 @@ hipError_t deconv(bool bf16, const GemmArgs &a, hipStream_t s) {
 ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, int stride, int n_cu) {
     (void)Hi;
     (void)Wi;
-    const int bk = bf16 ? 32 : 16;
+    const int bk = bf16 ? 32 : 16;  // implicit GEMM K step (64 bytes)
     ConvPlan p{kConvImplicit, 1, 0};
     if (stride == 1 && Co % 128 == 0) {
+        // 8 x 16-pixel tiles with 8 wavefronts where the grid fills the
+        // chip; otherwise 4 x 16-pixel tiles with 4 wavefronts, split over
+        // channel chunks until half the CUs hold a tile (an f32 partial
+        // round trip costs more than idle CUs beyond that, measured on
+        // 64 x 64 grids)
         const int tx = (Wo + 15) / 16, nt = Co / 128;
-        const int t16 = tx * ((Ho + 15) / 16) * nt, t8 = tx * ((Ho + 7) / 8) * nt;
-        if (t16 >= n_cu) {
-            p.variant = kConvHalo16;
-        } else {
+        const int t8 = tx * ((Ho + 7) / 8) * nt, t4 = tx * ((Ho + 3) / 4) * nt;
+        const int chunk_bytes = ((Ci * (bf16 ? 2 : 4)) % 128 == 0) ? 128 : 64;
+        const int chunks = Ci * (bf16 ? 2 : 4) / chunk_bytes;
+        if (t8 >= n_cu) {
             p.variant = kConvHalo8;
-            const int chunks = Ci / bk;
-            // a K split costs an f32 partial round trip; split only until
-            // half the CUs have a tile (measured best on 64 x 64 grids)
-            if (t8 < n_cu / 2)
-                for (int sp = 2; sp <= chunks && t8 * p.splits < n_cu / 2; ++sp)
+        } else {
+            p.variant = kConvHalo4;
+            if (t4 < n_cu / 2)
+                for (int sp = 2; sp <= chunks && t4 * p.splits < n_cu / 2; ++sp)
                     if (chunks % sp == 0) p.splits = sp;
         }
     } else {
