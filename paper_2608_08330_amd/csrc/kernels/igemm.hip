@@ -314,7 +314,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_igemm(GemmArgs a) {
 // loop is unrolled, so every s_waitcnt vmcnt bound is a constant:
 // after the weights of step s were issued, the loads still allowed in flight
 // are the next step's weights plus, at taps 1 and 2, the next chunk's patch.
-template <typename T, int TH, int BN, int WGM, int WGN, int RB>
+template <typename T, int TH, int BN, int WGM, int WGN, int RB, int STRIDE>
 __global__ __launch_bounds__(64 * WGM * WGN) void k_conv3s1(GemmArgs a) {
     constexpr int NW = WGM * WGN;
     constexpr int EPV = Traits<T>::EPV;
@@ -322,7 +322,13 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_conv3s1(GemmArgs a) {
     constexpr int RPI = 1024 / RB;               // rows per 1-KB load instruction
     constexpr int KS = RB / 64;                  // MFMA k-substeps per step
     constexpr int BK = RB / int(sizeof(T));      // channels per step
-    constexpr int TW = 16, HW = TW + 2, HH = TH + 2;
+    // input patch of a TH x TW output tile: (STRIDE (TH - 1) + 3) rows of
+    // (STRIDE (TW - 1) + 3) pixels; with stride 2 the even patch columns
+    // are stored first and the odd ones after them, so the 16 pixels a
+    // fragment reads (columns 2 x + dx) are consecutive rows in LDS
+    constexpr int TW = 16;
+    constexpr int HW = STRIDE * (TW - 1) + 3, HH = STRIDE * (TH - 1) + 3;
+    constexpr int EVEN = (HW + 1) / 2;
     constexpr int HALO = HH * HW;
     constexpr int IA = ((HALO + RPI - 1) / RPI + NW - 1) / NW * NW;  // patch loads, multiple of NW
     constexpr int LA = IA / NW;
@@ -374,8 +380,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_conv3s1(GemmArgs a) {
     for (int j = 0; j < LA; ++j) {
         const int row = RPI * (wave + j * NW) + lane / VPR;
         p_vec[j] = (lane % VPR) ^ swz(row);
-        const int hy = row / HW, hx = row - (row / HW) * HW;
-        const int iy = oy0 - 1 + hy, ix = ox0 - 1 + hx;
+        const int hy = row / HW, lc = row - (row / HW) * HW;
+        const int hx = STRIDE == 1 ? lc : (lc < EVEN ? 2 * lc : 2 * (lc - EVEN) + 1);
+        const int iy = STRIDE * oy0 - 1 + hy, ix = STRIDE * ox0 - 1 + hx;
         p_ok[j] = row < HALO && iy >= 0 && iy < a.Hi && ix >= 0 && ix < a.Wi;
         p_off[j] = p_ok[j] ? (iy * a.Wi + ix) : 0;
     }
@@ -449,7 +456,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_conv3s1(GemmArgs a) {
                 uint4 af[FM], bfr[FN];
 #pragma unroll
                 for (int i = 0; i < FM; ++i) {
-                    const int r = (wm * FM + i + dy) * HW + dx + fr;
+                    const int col = STRIDE == 1 ? dx + fr : ((dx & 1) ? EVEN : dx >> 1) + fr;
+                    const int r = (STRIDE * (wm * FM + i) + dy) * HW + col;
                     af[i] = *reinterpret_cast<const uint4 *>(pa + r * RB + ((v ^ swz(r)) << 4));
                 }
 #pragma unroll
@@ -521,11 +529,11 @@ hipError_t launch_cfg(const GemmArgs &a, hipStream_t s) {
     return hipGetLastError();
 }
 
-template <typename T, int TH, int BN = 128, int WGM = 4, int WGN = 2, int RB = 64>
+template <typename T, int TH, int BN = 128, int WGM = 4, int WGN = 2, int RB = 64, int STRIDE = 1>
 hipError_t launch_halo(const GemmArgs &a, hipStream_t s) {
     const unsigned tiles = unsigned((a.Wo + 15) / 16) * unsigned((a.Ho + TH - 1) / TH);
     const unsigned nx = tiles * unsigned(a.N / BN) * unsigned(a.splits);
-    k_conv3s1<T, TH, BN, WGM, WGN, RB><<<dim3(nx), 64 * WGM * WGN, 0, s>>>(a);
+    k_conv3s1<T, TH, BN, WGM, WGN, RB, STRIDE><<<dim3(nx), 64 * WGM * WGN, 0, s>>>(a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.splits == 1) return e;
     const int64_t total = int64_t(a.Ho) * a.Wo * (a.N / 4);
@@ -535,12 +543,18 @@ hipError_t launch_halo(const GemmArgs &a, hipStream_t s) {
 
 template <typename T, bool DECONV>
 hipError_t launch(const GemmArgs &a, hipStream_t s) {
-    if (!DECONV && a.variant != kConvImplicit) {
-        // 128-byte K steps when a chunk of that many channel bytes exists
-        const bool rb128 = (a.Ci * int(sizeof(T))) % 128 == 0;
-        if (a.variant == kConvHalo8)
-            return rb128 ? launch_halo<T, 8, 128, 4, 2, 128>(a, s) : launch_halo<T, 8, 128, 4, 2, 64>(a, s);
-        return rb128 ? launch_halo<T, 4, 128, 2, 2, 128>(a, s) : launch_halo<T, 4, 128, 2, 2, 64>(a, s);
+    if (!DECONV) {
+        // 128-byte K steps pay off from 256 input channels (bf16) on
+        const bool rb128 = (a.Ci * int(sizeof(T))) % 128 == 0 && a.Ci * int(sizeof(T)) >= 512;
+        switch (a.variant) {
+            case kConvHalo8:
+                return rb128 ? launch_halo<T, 8, 128, 4, 2, 128, 1>(a, s) : launch_halo<T, 8, 128, 4, 2, 64, 1>(a, s);
+            case kConvHalo4:
+                return rb128 ? launch_halo<T, 4, 128, 2, 2, 128, 1>(a, s) : launch_halo<T, 4, 128, 2, 2, 64, 1>(a, s);
+            case kConvHalo8S2: return launch_halo<T, 8, 128, 4, 2, 64, 2>(a, s);
+            case kConvHalo4S2: return launch_halo<T, 4, 128, 4, 2, 64, 2>(a, s);
+            default: break;
+        }
     }
     if (a.N % 128 == 0) return launch_cfg<T, 128, 128, 4, 2, 4, DECONV>(a, s);
     return launch_cfg<T, 128, 64, 4, 1, 4, DECONV>(a, s);
@@ -561,6 +575,7 @@ ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, in
     (void)Wi;
     const int bk = bf16 ? 32 : 16;  // implicit GEMM K step (64 bytes)
     ConvPlan p{kConvImplicit, 1, 0};
+    const int elt = bf16 ? 2 : 4;
     if (stride == 1 && Co % 128 == 0) {
         // 8 x 16-pixel tiles with 8 wavefronts where the grid fills the
         // chip; otherwise 4 x 16-pixel tiles with 4 wavefronts, split over
@@ -569,8 +584,8 @@ ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, in
         // 64 x 64 grids)
         const int tx = (Wo + 15) / 16, nt = Co / 128;
         const int t8 = tx * ((Ho + 7) / 8) * nt, t4 = tx * ((Ho + 3) / 4) * nt;
-        const int chunk_bytes = ((Ci * (bf16 ? 2 : 4)) % 128 == 0) ? 128 : 64;
-        const int chunks = Ci * (bf16 ? 2 : 4) / chunk_bytes;
+        const int chunk_bytes = ((Ci * elt) % 128 == 0 && Ci * elt >= 512) ? 128 : 64;
+        const int chunks = Ci * elt / chunk_bytes;
         if (t8 >= n_cu) {
             p.variant = kConvHalo8;
         } else {
@@ -579,6 +594,12 @@ ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, in
                 for (int sp = 2; sp <= chunks && t4 * p.splits < n_cu / 2; ++sp)
                     if (chunks % sp == 0) p.splits = sp;
         }
+    } else if (stride == 2 && Co % 128 == 0 && Ci * elt >= 256) {
+        // stride-2 patches (2 TH + 1 rows of 33 pixels, column-split); at
+        // 64 input channels the implicit GEMM is faster
+        const int tx = (Wo + 15) / 16, nt = Co / 128;
+        const int t8 = tx * ((Ho + 7) / 8) * nt;
+        p.variant = t8 >= n_cu ? kConvHalo8S2 : kConvHalo4S2;
     } else {
         const int tiles = gemm_tiles(Ho * Wo, Co);
         const int kt = 9 * Ci / bk;

@@ -77,13 +77,15 @@ struct GemmArgs {
     int32_t u;         // deconv only
     int32_t ldo, c_off;
     int32_t splits;    // K slices (>= 1); > 1 needs ws and a conv (no deconv)
-    int32_t variant;   // conv kernel: kConvImplicit, kConvHalo8, kConvHalo4
+    int32_t variant;   // conv kernel: kConvImplicit or one of the halo tilings
     const void *zero;  // >= 16 zero bytes in device memory (padding reads)
     float *ws;         // split-K partials [splits][M][N] float32
 };
 constexpr int kConvImplicit = 0;  // implicit GEMM (any stride)
 constexpr int kConvHalo8 = 1;     // stride-1 halo tiles of 8 x 16 pixels, 8 waves
 constexpr int kConvHalo4 = 2;     // stride-1 halo tiles of 4 x 16 pixels, 4 waves
+constexpr int kConvHalo8S2 = 3;   // stride-2 halo tiles of 8 x 16 output pixels, 8 waves
+constexpr int kConvHalo4S2 = 4;   // stride-2 halo tiles of 4 x 16 output pixels, 8 waves
 struct ConvPlan {
     int variant;
     int splits;
