@@ -248,11 +248,12 @@ def main(argv=None):
         if cfg["arrivals"]["kind"] == "uplink":
             raise SystemExit("latency replay of uplink-driven configs runs in the load-sweep report")
         arr = synth.arrival_draws(cfg, a.latency_traces) * 1e-3
-        rows, identical = replay.replay_traces(ctx, frame["points"], frame["poses"], arr, a.latency_reps)
+        staged = replay.stage_inputs(ctx, frame["points"])
+        rows, identical = replay.replay_traces(ctx, staged, frame["poses"], arr, a.latency_reps)
         lat = replay.summarize(rows)
         lat["reps"] = a.latency_reps
         lat["outputs_identical_rtcc_vs_barrier"] = bool(identical)
-        lat["rtcc_below_barrier_every_trace"] = bool(lat["wins"] == len(rows))
+        lat["rtcc_below_barrier_every_trace"] = bool(lat["wins_median"] == len(rows))
         out["latency"] = lat
         print("# latency done", file=sys.stderr, flush=True)
 

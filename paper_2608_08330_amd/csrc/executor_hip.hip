@@ -183,7 +183,7 @@ class HipExecutor : public Executor {
         rtcc_status s = enqueue_post(affine, js, timing, err);
         if (s != RTCC_OK) return s;
         HIP_TRY(hipMemcpyAsync(h_small, d_count, 4, hipMemcpyDeviceToHost, js));
-        HIP_TRY(hipStreamSynchronize(js));
+        HIP_TRY(spin_sync(js));
         const int64_t count = *reinterpret_cast<int32_t *>(h_small);
         if (count < 0 || size_t(count) > n_anchor_) {
             err = "decode produced an out-of-range count";
@@ -191,7 +191,7 @@ class HipExecutor : public Executor {
         }
         if (count > 0) {
             HIP_TRY(hipMemcpyAsync(h_rec, d_rec, size_t(count) * 36, hipMemcpyDeviceToHost, js));
-            HIP_TRY(hipStreamSynchronize(js));
+            HIP_TRY(spin_sync(js));
         }
         for (int64_t i = 0; i < count; ++i) {
             const float *r = h_rec + i * 9;
@@ -309,6 +309,15 @@ class HipExecutor : public Executor {
     };
 
     hipStream_t compute_stream_for_join() const { return join_stream_; }
+
+    // Wait for a stream by polling: T^det is a latency measurement, and a
+    // blocking wait adds the host's wake-up time to it.
+    static hipError_t spin_sync(hipStream_t s) {
+        for (;;) {
+            const hipError_t e = hipStreamQuery(s);
+            if (e != hipErrorNotReady) return e;
+        }
+    }
 
     hipError_t alloc(void **p, size_t bytes) {
         hipError_t e = hipMalloc(p, align256(bytes ? bytes : 1));

@@ -59,13 +59,14 @@ def bootstrap_ci(x, n=10000, seed=0, alpha=0.05):
     return float(np.quantile(means, alpha / 2)), float(np.quantile(means, 1 - alpha / 2))
 
 
-def replay_traces(ctx, points, poses, arrivals_s, reps):
+def replay_traces(ctx, staged, poses, arrivals_s, reps, start=0):
     """Paired RTCC / barrier replay of every trace, alternating which mode
-    runs first per repetition; repetitions are averaged per trace."""
-    staged = stage_inputs(ctx, points)
+    runs first per repetition; repetitions are averaged per trace.
+    ``staged`` are the pinned staging views from :func:`stage_inputs`;
+    ``start`` is the global index of the first trace (order alternation)."""
     rows = []
     identical = True
-    for t, a in enumerate(arrivals_s):
+    for t, a in enumerate(arrivals_s, start):
         tr = {"R": [], "B": []}
         ids = {}
         for r in range(reps):
@@ -79,9 +80,12 @@ def replay_traces(ctx, points, poses, arrivals_s, reps):
                 identical &= np.array_equal(ids[key], res["anchor_idx"])
         identical &= np.array_equal(ids["R"], ids["B"])
         rows.append(dict(
+            a=[float(v) for v in a],
             A=float(np.max(a)), spread=float(np.max(a) - np.min(a)),
             R_det=float(np.mean([x["t_det"] for x in tr["R"]])),
             B_det=float(np.mean([x["t_det"] for x in tr["B"]])),
+            R_det_med=float(np.median([x["t_det"] for x in tr["R"]])),
+            B_det_med=float(np.median([x["t_det"] for x in tr["B"]])),
             R_head=float(np.mean([x["t_head"] for x in tr["R"]])),
             B_head=float(np.mean([x["t_head"] for x in tr["B"]])),
             lateness=[l for x in tr["R"] for l in x["lateness"]],
@@ -105,6 +109,7 @@ def summarize(rows):
         rtcc_head_p50_ms=float(np.percentile(Rh, 50)), barrier_head_p50_ms=float(np.percentile(Bh, 50)),
         mean_gain_ms=float(gain.mean()), gain_ci95_ms=[lo, hi],
         wins=int(np.sum(gain > 0)),
+        wins_median=int(sum(r["R_det_med"] < r["B_det_med"] for r in rows)),
         dispatch_lateness_p50_ms=float(np.percentile(late, 50)) if late.size else None,
         dispatch_lateness_p95_ms=float(np.percentile(late, 95)) if late.size else None,
     )

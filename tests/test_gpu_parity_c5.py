@@ -1,0 +1,82 @@
+"""Full-size parity on the c5 frame (8 agents x 100,000 points, 512 x 512 BEV,
+bf16, attention fusion), in the launch configuration bench.py times: single
+compute stream, device-resident inputs.
+
+Pillar lists and the canvas are compared in full against the oracle,
+recomputed here; slots, the fused map and the head are compared at sampled
+cells against tests/golden/c5_oracle_samples.npz (written by
+tests/golden/make_c5_samples.py from the oracle); detections as sets with a
+tolerance band around the threshold.  RTCC and barrier runs are bitwise
+identical."""
+
+import os
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import network as N
+from paper_2608_08330_amd import rtcc as R
+from tests.helpers import TOL, as_f32, compare_detections, make_ctx
+
+pytestmark = pytest.mark.gpu
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden", "c5_oracle_samples.npz")
+
+
+def _run(ctx, cfg, fr, dev, mode):
+    import time
+    R.rtcc_set_mode(ctx, mode)
+    R.rtcc_begin_frame(ctx, time.monotonic() - 1.0)
+    for k in range(cfg["K"]):
+        R.rtcc_release_branch_device(ctx, k, dev[k].data_ptr(), len(fr["points"][k]), fr["poses"][k], 0.0)
+    return R.rtcc_join_and_detect(ctx)
+
+
+def test_c5_full_size_parity_and_mode_identity():
+    import torch
+    print("parity c5 full size", flush=True)
+    cfg = synth.config("c5")
+    fr = synth.make_frame(cfg)
+    ref = np.load(GOLD)
+    tol = TOL["bf16"]
+    H2, W2 = N.feature_grid(cfg)
+    dev = [torch.from_numpy(p).to("cuda") for p in fr["points"]]
+    torch.cuda.synchronize()
+    with make_ctx(cfg, fr, exec=R.RTCC_EXEC_SERIAL) as ctx:
+        det = _run(ctx, cfg, fr, dev, R.RTCC_MODE_RELEASE)
+        pw = N.prepared_weights(cfg, fr["weights"])
+        for k in range(cfg["K"]):
+            cell = N.cell_ids(fr["points"][k], cfg)
+            pil = N.pillars(cell, cfg["max_pts"])
+            got_cells = R.rtcc_get_tensor(ctx, R.RTCC_T_PILLAR_CELLS, k, np.int32)
+            got_counts = R.rtcc_get_tensor(ctx, R.RTCC_T_PILLAR_COUNTS, k, np.int32)
+            assert np.array_equal(got_cells, pil["cells"].astype(np.int32)), k
+            assert np.array_equal(got_counts, pil["counts"].astype(np.int32)), k
+            canvas = N.pfn_canvas(fr["points"][k], pil, pw["pfn_w"], pw["pfn_b"], cfg)
+            got = as_f32(R.rtcc_get_tensor(ctx, R.RTCC_T_CANVAS, k), cfg)
+            err = float(np.max(np.abs(got - canvas.ravel())) / np.max(np.abs(canvas)))
+            assert err <= tol, ("canvas", k, err)
+            slot = as_f32(R.rtcc_get_tensor(ctx, R.RTCC_T_SLOT, k), cfg).reshape(H2 * W2, -1)
+            cells = ref["slot_cells_%d" % k]
+            want = R.bf16_bits_to_f32(ref["slot_%d" % k])
+            err = float(np.max(np.abs(slot[cells] - want)) / ref["slot_absmax_%d" % k])
+            assert err <= tol, ("slot", k, err)
+        fused = as_f32(R.rtcc_get_tensor(ctx, R.RTCC_T_FUSED), cfg).reshape(H2 * W2, -1)
+        head = R.rtcc_get_tensor(ctx, R.RTCC_T_HEAD, 0, np.float32).reshape(H2 * W2, 16)
+        err = float(np.max(np.abs(fused[ref["fused_cells"]] - R.bf16_bits_to_f32(ref["fused"]))) / ref["fused_absmax"])
+        assert err <= tol, ("fused", err)
+        err = float(np.max(np.abs(head[ref["head_cells"]] - ref["head"])) / ref["head_absmax"])
+        assert err <= tol, ("head", err)
+        oref = dict(anchor_idx=ref["det_anchor_idx"], boxes=ref["det_boxes"], scores=ref["det_scores"],
+                    logits=ref["logits"].astype(np.float64))
+        common, ambiguous = compare_detections(det, oref, cfg, np.array([ref["head_absmax"]]))
+        print("c5 detections: gpu %d, oracle %d, common %d, band %d" % (
+            det["count"], len(ref["det_anchor_idx"]), common, ambiguous), flush=True)
+
+        det_b = _run(ctx, cfg, fr, dev, R.RTCC_MODE_BARRIER)
+        head_b = R.rtcc_get_tensor(ctx, R.RTCC_T_HEAD, 0, np.float32).reshape(H2 * W2, 16)
+        fused_b = as_f32(R.rtcc_get_tensor(ctx, R.RTCC_T_FUSED), cfg).reshape(H2 * W2, -1)
+    assert np.array_equal(head.view(np.uint32), head_b.view(np.uint32))
+    assert np.array_equal(fused.view(np.uint32), fused_b.view(np.uint32))
+    assert np.array_equal(det["anchor_idx"], det_b["anchor_idx"])
