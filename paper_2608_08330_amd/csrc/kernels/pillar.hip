@@ -229,6 +229,10 @@ __device__ inline uint32_t pack_bf16x2(float a, float b) {
 
 template <bool BF16>
 __global__ __launch_bounds__(256) void k_pfn_canvas(PfnArgs a) {
+    // PFN weights and bias, read once per block into LDS (C <= 512)
+    __shared__ float sw[5 * 512];
+    for (int q = threadIdx.x; q < 5 * a.C; q += 256) sw[q] = q < 4 * a.C ? a.w[q] : a.b[q - 4 * a.C];
+    __syncthreads();
     const int lanes_per_cell = a.C >> 3;
     const int gid = blockIdx.x * 256 + threadIdx.x;
     const int cell = gid / lanes_per_cell;
@@ -242,11 +246,11 @@ __global__ __launch_bounds__(256) void k_pfn_canvas(PfnArgs a) {
         float w0[8], w1[8], w2[8], w3[8], bb[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-            w0[i] = a.w[0 * a.C + ch + i];
-            w1[i] = a.w[1 * a.C + ch + i];
-            w2[i] = a.w[2 * a.C + ch + i];
-            w3[i] = a.w[3 * a.C + ch + i];
-            bb[i] = a.b[ch + i];
+            w0[i] = sw[0 * a.C + ch + i];
+            w1[i] = sw[1 * a.C + ch + i];
+            w2[i] = sw[2 * a.C + ch + i];
+            w3[i] = sw[3 * a.C + ch + i];
+            bb[i] = sw[4 * a.C + ch + i];
         }
         const int m = cnt < a.max_pts ? cnt : a.max_pts;
         const int off = a.offsets[cell];

@@ -73,10 +73,49 @@ __device__ inline void store_vec_bf16(uint16_t *p, const float *v) {
     }
 }
 
+// Bilinear sample of one agent's slot at the ego cell (i, j): VEC channels
+// starting at c0, zero outside the grid.
+template <typename T, int VEC>
+__device__ inline void warp_sample(const WarpArgs &a, int k, float fi, float fj, int c0, float *x) {
+    const float *m = a.affine[k];
+    const float u = m[0] * fj + m[1] * fi + m[2];
+    const float v = m[3] * fj + m[4] * fi + m[5];
+    const float fx0 = floorf(u), fy0 = floorf(v);
+    const float fx = u - fx0, fy = v - fy0;
+    const int x0 = int(fx0), y0 = int(fy0);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) x[e] = 0.f;
+    const T *slot = static_cast<const T *>(a.slots[k]);
+#pragma unroll
+    for (int cnr = 0; cnr < 4; ++cnr) {
+        const int yy = y0 + (cnr >> 1), xx = x0 + (cnr & 1);
+        const float wy = (cnr >> 1) ? fy : 1.f - fy;
+        const float wx = (cnr & 1) ? fx : 1.f - fx;
+        if (yy < 0 || yy >= a.H2 || xx < 0 || xx >= a.W2) continue;
+        const float wgt = wx * wy;
+        float val[VEC];
+        const T *p = slot + (size_t(yy) * a.W2 + xx) * a.C + c0;
+        if constexpr (sizeof(T) == 2) {
+            load_vec_bf16<VEC>(reinterpret_cast<const uint16_t *>(p), val);
+        } else {
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) val[e] = reinterpret_cast<const float *>(p)[e];
+        }
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) x[e] += wgt * val[e];
+    }
+}
+
 template <typename T, int VEC, bool ATTN>
 __global__ __launch_bounds__(256) void k_warp_fuse(WarpArgs a) {
     const int l32 = threadIdx.x & 31;
-    const int cell = (blockIdx.x * 256 + threadIdx.x) >> 5;
+    // XCD-aware order: block ids go to the 8 XCDs round-robin; give each
+    // XCD a contiguous band of cells, so bilinear corners shared by
+    // neighbouring cells are reused from that XCD's L2.
+    int bid = blockIdx.x;
+    const int nb = gridDim.x;
+    if ((nb & 7) == 0) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
+    const int cell = (bid * 256 + int(threadIdx.x)) >> 5;
     const int n_cells = a.H2 * a.W2;
     if (cell >= n_cells) return;  // uniform over the 32 lanes of a cell
     const int i = cell / a.W2, j = cell - (cell / a.W2) * a.W2;
@@ -89,35 +128,7 @@ __global__ __launch_bounds__(256) void k_warp_fuse(WarpArgs a) {
 #pragma unroll
     for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
 
-    for (int k = 0; k < a.K; ++k) {
-        const float *m = a.affine[k];
-        const float u = m[0] * fj + m[1] * fi + m[2];
-        const float v = m[3] * fj + m[4] * fi + m[5];
-        const float fx0 = floorf(u), fy0 = floorf(v);
-        const float fx = u - fx0, fy = v - fy0;
-        const int x0 = int(fx0), y0 = int(fy0);
-        float x[VEC];
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) x[e] = 0.f;
-        const T *slot = static_cast<const T *>(a.slots[k]);
-#pragma unroll
-        for (int cnr = 0; cnr < 4; ++cnr) {
-            const int yy = y0 + (cnr >> 1), xx = x0 + (cnr & 1);
-            const float wy = (cnr >> 1) ? fy : 1.f - fy;
-            const float wx = (cnr & 1) ? fx : 1.f - fx;
-            if (yy < 0 || yy >= a.H2 || xx < 0 || xx >= a.W2) continue;
-            const float wgt = wx * wy;
-            float val[VEC];
-            const T *p = slot + (size_t(yy) * a.W2 + xx) * a.C + c0;
-            if constexpr (sizeof(T) == 2) {
-                load_vec_bf16<VEC>(reinterpret_cast<const uint16_t *>(p), val);
-            } else {
-#pragma unroll
-                for (int e = 0; e < VEC; ++e) val[e] = reinterpret_cast<const float *>(p)[e];
-            }
-#pragma unroll
-            for (int e = 0; e < VEC; ++e) x[e] += wgt * val[e];
-        }
+    auto fold = [&](int k, const float *x) {
         if constexpr (!ATTN) {
 #pragma unroll
             for (int e = 0; e < VEC; ++e) acc[e] = k == 0 ? x[e] : fmaxf(acc[e], x[e]);
@@ -140,6 +151,21 @@ __global__ __launch_bounds__(256) void k_warp_fuse(WarpArgs a) {
             for (int e = 0; e < VEC; ++e) acc[e] = acc[e] * scale + p * x[e];
             run_max = nm;
         }
+    };
+
+    // two agents per iteration: the loads of both are in flight together
+    int k = 0;
+    for (; k + 1 < a.K; k += 2) {
+        float x0[VEC], x1[VEC];
+        warp_sample<T, VEC>(a, k, fi, fj, c0, x0);
+        warp_sample<T, VEC>(a, k + 1, fi, fj, c0, x1);
+        fold(k, x0);
+        fold(k + 1, x1);
+    }
+    if (k < a.K) {
+        float x0[VEC];
+        warp_sample<T, VEC>(a, k, fi, fj, c0, x0);
+        fold(k, x0);
     }
     if constexpr (ATTN) {
         const float inv = 1.0f / run_sum;
