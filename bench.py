@@ -37,10 +37,10 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 # commands in profiles/traffic_c5_bench.md).  Each figure holds only for the
 # kernel source it was taken on; after a change it reads null until re-taken.
 MEASURED_TRAFFIC = {
-    "conv": dict(src="paper_2608_08330_amd/csrc/kernels/igemm.hip", bytes=28.43e6,
-                 sha256="3c6ad0950c9d5ae8c60290a95a6439b0c2819289ab1be656e88c062c4531cb4b"),
-    "warp_fuse": dict(src="paper_2608_08330_amd/csrc/kernels/post.hip", bytes=488.91e6,
-                      sha256="11185b3af6bc304d3c795be2fe7a42b5a26f74f56300caa58d40a6d6ec2a030d"),
+    "conv": dict(src="paper_2608_08330_amd/csrc/kernels/igemm.hip", bytes=30.04e6,
+                 sha256="53927807097a3fd3877f52576bf6d7a21b7885a35f577a2a2f83d64f3e047233"),
+    "warp_fuse": dict(src="paper_2608_08330_amd/csrc/kernels/post.hip", bytes=493.70e6,
+                      sha256="2bd8e6aa825c827403e7c4578e180b00136c895a7db997c87a5fb36d8ebb8e95"),
 }
 
 

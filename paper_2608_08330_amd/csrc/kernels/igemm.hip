@@ -49,6 +49,13 @@ template <int N>
 struct VmWait {
     static constexpr int imm = (N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8);
 };
+// s_waitcnt vmcnt(n) for n <= NMAX; n must fold to a constant after
+// unrolling, so that the chain collapses to the one instruction.
+template <int NMAX>
+__device__ inline void vm_wait(int n) {
+    if (n == NMAX) __builtin_amdgcn_s_waitcnt(VmWait<NMAX>::imm);
+    else if constexpr (NMAX > 0) vm_wait<NMAX - 1>(n);
+}
 
 template <typename T>
 struct Traits;
@@ -307,16 +314,21 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_igemm(GemmArgs a) {
 // (TH + 2) x 18 input patch (halo included, zero outside the grid) in LDS
 // once, and the 9 taps then read their shifted 16-pixel rows from it, so an
 // input element is fetched from L2 once per chunk instead of once per tap.
-// Only the per-tap weight tile (BN rows x 64 bytes) streams through a
-// 3-buffer ring two taps ahead.  WGM x WGN wavefronts: WGM along output rows,
+// Only the per-tap weight tile (BN rows x RB bytes) streams through an
+// R-buffer ring, R - 1 taps ahead.  WGM x WGN wavefronts: WGM along output rows,
 // WGN along channels; every wave holds (TH / WGM) x (BN / WGN / 16) MFMA tiles.
-// The tap
+// With KG > 1 the block holds KG such groups of wavefronts over the same
+// output tile: group g takes the channel chunks g, g + KG, ... with its own
+// patch and weight buffers, and at the end groups 1 .. KG-1 hand their
+// accumulators to group 0 through LDS, which adds them in group order
+// (fixed, so the result does not depend on timing).  The tap
 // loop is unrolled, so every s_waitcnt vmcnt bound is a constant:
-// after the weights of step s were issued, the loads still allowed in flight
-// are the next step's weights plus, at taps 1 and 2, the next chunk's patch.
-template <typename T, int TH, int BN, int WGM, int WGN, int RB, int STRIDE>
-__global__ __launch_bounds__(64 * WGM * WGN) void k_conv3s1(GemmArgs a) {
-    constexpr int NW = WGM * WGN;
+// once step s's weights have landed, the loads still allowed in flight are
+// the weights of the next R - 2 steps plus, at taps 1 .. R - 1, the next
+// chunk's patch (issued at tap 0 after the weights of step s + R - 1).
+template <typename T, int TH, int BN, int WGM, int WGN, int RB, int STRIDE, int KG, int R>
+__global__ __launch_bounds__(64 * WGM * WGN * KG) void k_conv3s1(GemmArgs a) {
+    constexpr int NW = WGM * WGN;  // wavefronts per group
     constexpr int EPV = Traits<T>::EPV;
     constexpr int VPR = RB / 16;                 // 16-byte vectors per row and step
     constexpr int RPI = 1024 / RB;               // rows per 1-KB load instruction
@@ -339,10 +351,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_conv3s1(GemmArgs a) {
     constexpr int FM = TH / WGM, FN = BN / WGN / 16;
     static_assert(FM * WGM == TH && FN >= 1, "wave layout must tile the block");
 
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[2 * A_BYTES + 3 * B_BYTES];
-    const uint32_t lds_base = __builtin_amdgcn_readfirstlane(
-        uint32_t(reinterpret_cast<uintptr_t>((lds_void *)smem)));
-    const uint32_t lds_b = lds_base + 2 * A_BYTES;
+    static_assert(R >= 3 && R <= 9, "weight ring depth");
+    constexpr int G_BYTES = 2 * A_BYTES + R * B_BYTES;  // LDS of one group
+    static_assert((KG - 1) * NW * 64 * FM * FN * 16 <= KG * G_BYTES, "group reduction must fit in LDS");
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[KG * G_BYTES];
 
     // 16-byte vector v of row r sits at position v ^ swz(r); any 8
     // consecutive rows then cover the 32 banks once per ds_read_b128 cycle.
@@ -350,12 +362,17 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_conv3s1(GemmArgs a) {
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int grp = (tid >> 6) / NW;   // wave group: channel chunks grp, grp + KG, ...
+    const int wave = (tid >> 6) % NW;  // wavefront within its group
     const int wm = wave % WGM, wn = wave / WGM;
+    unsigned char *gsmem = smem + grp * G_BYTES;
+    const uint32_t lds_base = __builtin_amdgcn_readfirstlane(
+        uint32_t(reinterpret_cast<uintptr_t>((lds_void *)gsmem)));
+    const uint32_t lds_b = lds_base + 2 * A_BYTES;
 
     const int Ci = a.Ci, N = a.N, Ho = a.Ho, Wo = a.Wo;
     const int K = 9 * Ci;
-    const int CH = (Ci / BK) / a.splits;  // chunks of this split
+    const int CH = (Ci / BK) / a.splits / KG;  // chunks of this split and group
 
     const int tx = (Wo + TW - 1) / TW, ty = (Ho + TH - 1) / TH;
     const int nt = N / BN;
@@ -394,8 +411,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_conv3s1(GemmArgs a) {
         w_vec[j] = (lane % VPR) ^ swz(row);
     }
 
+    // local chunk i of this group is chunk c_begin + grp + KG i of the layer
     auto issue_patch = [&](int chunk) {
-        const int c0 = (c_begin + chunk) * BK;
+        const int c0 = (c_begin + grp + KG * chunk) * BK;
         const uint32_t dst = lds_base + (chunk & 1) * A_BYTES;
 #pragma unroll
         for (int j = 0; j < LA; ++j) {
@@ -407,8 +425,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_conv3s1(GemmArgs a) {
     // step s = chunk * 9 + tap: weight columns k = tap * Ci + chunk channels
     auto issue_w = [&](int s) {
         const int chunk = s / 9, tap = s - (s / 9) * 9;
-        const int k0 = tap * Ci + (c_begin + chunk) * BK;
-        const uint32_t dst = lds_b + (s % 3) * B_BYTES;
+        const int k0 = tap * Ci + (c_begin + grp + KG * chunk) * BK;
+        const uint32_t dst = lds_b + (s % R) * B_BYTES;
 #pragma unroll
         for (int j = 0; j < LB; ++j)
             load_lds16(wt + size_t(n0 + w_row[j]) * K + k0 + w_vec[j] * EPV, dst + (wave + j * NW) * 1024);
@@ -425,31 +443,28 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_conv3s1(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) b_row[j] = wn * (BN / WGN) + j * 16 + fr;
 
-    issue_patch(0);
-    issue_w(0);
-    issue_w(1);
     const int S = CH * 9;
+    issue_patch(0);
+#pragma unroll
+    for (int q = 0; q + 1 < R; ++q)
+        if (q < S) issue_w(q);
     for (int c = 0; c < CH; ++c) {
         const bool last = c + 1 == CH;
-        const unsigned char *pa = smem + (c & 1) * A_BYTES;
+        const unsigned char *pa = gsmem + (c & 1) * A_BYTES;
 #pragma unroll
         for (int t = 0; t < 9; ++t) {
             const int s = c * 9 + t;
-            // loads allowed in flight after step s's weights: the next
-            // step's weights, and at taps 1 and 2 the next chunk's patch
-            if (!last) {
-                if (t == 1 || t == 2) __builtin_amdgcn_s_waitcnt(VmWait<LB + LA>::imm);
-                else __builtin_amdgcn_s_waitcnt(VmWait<LB>::imm);
-            } else {
-                if (t == 8) __builtin_amdgcn_s_waitcnt(VmWait<0>::imm);
-                else __builtin_amdgcn_s_waitcnt(VmWait<LB>::imm);
-            }
+            // loads allowed in flight once step s's weights are in: the
+            // weights of the next R - 2 steps (fewer near the end) and, at
+            // taps 1 .. R - 1, the next chunk's patch
+            if (!last) vm_wait<(R - 2) * LB + LA>((R - 2) * LB + (t >= 1 && t <= R - 1 ? LA : 0));
+            else vm_wait<(R - 2) * LB>((8 - t < R - 2 ? 8 - t : R - 2) * LB);
             __builtin_amdgcn_s_barrier();
             asm volatile("" ::: "memory");
-            if (s + 2 < S) issue_w(s + 2);
+            if (s + R - 1 < S) issue_w(s + R - 1);
             if (t == 0 && !last) issue_patch(c + 1);
             const int dy = t / 3, dx = t % 3;
-            const unsigned char *pb = smem + 2 * A_BYTES + (s % 3) * B_BYTES;
+            const unsigned char *pb = gsmem + 2 * A_BYTES + (s % R) * B_BYTES;
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
                 const int v = fk + 4 * ks;
@@ -468,6 +483,34 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_conv3s1(GemmArgs a) {
 #pragma unroll
                     for (int j = 0; j < FN; ++j) acc[i][j] = Traits<T>::mma(bfr[j], af[i], acc[i][j]);
             }
+        }
+    }
+
+    if constexpr (KG > 1) {
+        // every wave has read its last LDS operands and every DMA load has
+        // landed (vmcnt(0) at the last step) before the buffers are reused
+        __syncthreads();
+        float *red = reinterpret_cast<float *>(smem);
+        constexpr int E = FM * FN * 4;  // accumulators per lane
+        if (grp > 0) {
+            float *dst = red + ((grp - 1) * NW + wave) * 64 * E;
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) dst[((i * FN + j) * 4 + q) * 64 + lane] = acc[i][j][q];
+        }
+        __syncthreads();
+        if (grp > 0) return;
+        for (int g = 1; g < KG; ++g) {
+            const float *src = red + ((g - 1) * NW + wave) * 64 * E;
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) acc[i][j][q] += src[((i * FN + j) * 4 + q) * 64 + lane];
         }
     }
 
@@ -529,11 +572,12 @@ hipError_t launch_cfg(const GemmArgs &a, hipStream_t s) {
     return hipGetLastError();
 }
 
-template <typename T, int TH, int BN = 128, int WGM = 4, int WGN = 2, int RB = 64, int STRIDE = 1>
+template <typename T, int TH, int BN = 128, int WGM = 4, int WGN = 2, int RB = 64, int STRIDE = 1, int KG = 1,
+          int R = 3>
 hipError_t launch_halo(const GemmArgs &a, hipStream_t s) {
     const unsigned tiles = unsigned((a.Wo + 15) / 16) * unsigned((a.Ho + TH - 1) / TH);
     const unsigned nx = tiles * unsigned(a.N / BN) * unsigned(a.splits);
-    k_conv3s1<T, TH, BN, WGM, WGN, RB, STRIDE><<<dim3(nx), 64 * WGM * WGN, 0, s>>>(a);
+    k_conv3s1<T, TH, BN, WGM, WGN, RB, STRIDE, KG, R><<<dim3(nx), 64 * WGM * WGN * KG, 0, s>>>(a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.splits == 1) return e;
     const int64_t total = int64_t(a.Ho) * a.Wo * (a.N / 4);
@@ -547,12 +591,17 @@ hipError_t launch(const GemmArgs &a, hipStream_t s) {
         // 128-byte K steps pay off from 256 input channels (bf16) on
         const bool rb128 = (a.Ci * int(sizeof(T))) % 128 == 0 && a.Ci * int(sizeof(T)) >= 512;
         switch (a.variant) {
+            // weight ring depth R: 4 where it measured faster at the c5 shapes
             case kConvHalo8:
-                return rb128 ? launch_halo<T, 8, 128, 4, 2, 128, 1>(a, s) : launch_halo<T, 8, 128, 4, 2, 64, 1>(a, s);
+                return rb128 ? launch_halo<T, 8, 128, 4, 2, 128, 1, 1, 4>(a, s)
+                             : launch_halo<T, 8, 128, 4, 2, 64, 1, 1, 4>(a, s);
             case kConvHalo4:
                 return rb128 ? launch_halo<T, 4, 128, 2, 2, 128, 1>(a, s) : launch_halo<T, 4, 128, 2, 2, 64, 1>(a, s);
-            case kConvHalo8S2: return launch_halo<T, 8, 128, 4, 2, 64, 2>(a, s);
+            case kConvHalo8S2: return launch_halo<T, 8, 128, 4, 2, 64, 2, 1, 4>(a, s);
             case kConvHalo4S2: return launch_halo<T, 4, 128, 4, 2, 64, 2>(a, s);
+            case kConvHalo4N64K2:
+                return rb128 ? launch_halo<T, 4, 64, 2, 2, 128, 1, 2>(a, s) : launch_halo<T, 4, 64, 2, 2, 64, 1, 2>(a, s);
+            case kConvHalo4S2N64K2: return launch_halo<T, 4, 64, 2, 2, 64, 2, 2, 4>(a, s);
             default: break;
         }
     }
@@ -586,8 +635,13 @@ ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, in
         const int t8 = tx * ((Ho + 7) / 8) * nt, t4 = tx * ((Ho + 3) / 4) * nt;
         const int chunk_bytes = ((Ci * elt) % 128 == 0 && Ci * elt >= 512) ? 128 : 64;
         const int chunks = Ci * elt / chunk_bytes;
+        const int t64 = tx * ((Ho + 3) / 4) * (Co / 64);
         if (t8 >= n_cu) {
             p.variant = kConvHalo8;
+        } else if (t64 >= n_cu && chunks % 2 == 0) {
+            // 64-channel tiles fill the chip; two wave groups split the
+            // channel chunks so every CU runs 8 wavefronts
+            p.variant = kConvHalo4N64K2;
         } else {
             p.variant = kConvHalo4;
             if (t4 < n_cu / 2)
@@ -599,7 +653,11 @@ ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, in
         // 64 input channels the implicit GEMM is faster
         const int tx = (Wo + 15) / 16, nt = Co / 128;
         const int t8 = tx * ((Ho + 7) / 8) * nt;
-        p.variant = t8 >= n_cu ? kConvHalo8S2 : kConvHalo4S2;
+        const int t64 = tx * ((Ho + 3) / 4) * (Co / 64);
+        const int chunks = Ci * elt / 64;
+        if (t8 >= n_cu) p.variant = kConvHalo8S2;
+        else if (t64 >= n_cu && chunks % 2 == 0) p.variant = kConvHalo4S2N64K2;
+        else p.variant = kConvHalo4S2;
     } else {
         const int tiles = gemm_tiles(Ho * Wo, Co);
         const int kt = 9 * Ci / bk;

@@ -86,6 +86,8 @@ constexpr int kConvHalo8 = 1;     // stride-1 halo tiles of 8 x 16 pixels, 8 wav
 constexpr int kConvHalo4 = 2;     // stride-1 halo tiles of 4 x 16 pixels, 4 waves
 constexpr int kConvHalo8S2 = 3;   // stride-2 halo tiles of 8 x 16 output pixels, 8 waves
 constexpr int kConvHalo4S2 = 4;   // stride-2 halo tiles of 4 x 16 output pixels, 8 waves
+constexpr int kConvHalo4N64K2 = 5;    // stride-1 4 x 16 pixels x 64 channels, 2 groups of 4 waves
+constexpr int kConvHalo4S2N64K2 = 6;  // stride-2 4 x 16 pixels x 64 channels, 2 groups of 4 waves
 struct ConvPlan {
     int variant;
     int splits;

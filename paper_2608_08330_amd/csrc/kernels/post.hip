@@ -74,7 +74,10 @@ __device__ inline void store_vec_bf16(uint16_t *p, const float *v) {
 }
 
 // Bilinear sample of one agent's slot at the ego cell (i, j): VEC channels
-// starting at c0, zero outside the grid.
+// starting at c0, zero outside the grid.  Branch-free: a corner outside the
+// grid loads cell (0, 0) instead and its value is replaced by 0, so the four
+// corner loads of this agent (and of the agent sampled next to it) are all in
+// flight before the first is consumed.
 template <typename T, int VEC>
 __device__ inline void warp_sample(const WarpArgs &a, int k, float fi, float fj, int c0, float *x) {
     const float *m = a.affine[k];
@@ -83,30 +86,35 @@ __device__ inline void warp_sample(const WarpArgs &a, int k, float fi, float fj,
     const float fx0 = floorf(u), fy0 = floorf(v);
     const float fx = u - fx0, fy = v - fy0;
     const int x0 = int(fx0), y0 = int(fy0);
-#pragma unroll
-    for (int e = 0; e < VEC; ++e) x[e] = 0.f;
     const T *slot = static_cast<const T *>(a.slots[k]);
+    float val[4][VEC];
+    bool in[4];
 #pragma unroll
     for (int cnr = 0; cnr < 4; ++cnr) {
         const int yy = y0 + (cnr >> 1), xx = x0 + (cnr & 1);
-        const float wy = (cnr >> 1) ? fy : 1.f - fy;
-        const float wx = (cnr & 1) ? fx : 1.f - fx;
-        if (yy < 0 || yy >= a.H2 || xx < 0 || xx >= a.W2) continue;
-        const float wgt = wx * wy;
-        float val[VEC];
-        const T *p = slot + (size_t(yy) * a.W2 + xx) * a.C + c0;
+        in[cnr] = unsigned(yy) < unsigned(a.H2) && unsigned(xx) < unsigned(a.W2);
+        const size_t cell = in[cnr] ? size_t(yy) * a.W2 + xx : 0;
+        const T *p = slot + cell * a.C + c0;
         if constexpr (sizeof(T) == 2) {
-            load_vec_bf16<VEC>(reinterpret_cast<const uint16_t *>(p), val);
+            load_vec_bf16<VEC>(reinterpret_cast<const uint16_t *>(p), val[cnr]);
         } else {
 #pragma unroll
-            for (int e = 0; e < VEC; ++e) val[e] = reinterpret_cast<const float *>(p)[e];
+            for (int e = 0; e < VEC; ++e) val[cnr][e] = reinterpret_cast<const float *>(p)[e];
         }
+    }
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) x[e] += wgt * val[e];
+    for (int e = 0; e < VEC; ++e) x[e] = 0.f;
+#pragma unroll
+    for (int cnr = 0; cnr < 4; ++cnr) {
+        const float wy = (cnr >> 1) ? fy : 1.f - fy;
+        const float wx = (cnr & 1) ? fx : 1.f - fx;
+        const float wgt = wx * wy;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) x[e] += in[cnr] ? wgt * val[cnr][e] : 0.f;
     }
 }
 
-template <typename T, int VEC, bool ATTN>
+template <typename T, int VEC, bool ATTN, int G = 1>
 __global__ __launch_bounds__(256) void k_warp_fuse(WarpArgs a) {
     const int l32 = threadIdx.x & 31;
     // XCD-aware order: block ids go to the 8 XCDs round-robin; give each
@@ -153,16 +161,18 @@ __global__ __launch_bounds__(256) void k_warp_fuse(WarpArgs a) {
         }
     };
 
-    // two agents per iteration: the loads of both are in flight together
+    // G agents per iteration (the corner loads of all G in flight together);
+    // with branch-free sampling G = 1 already keeps 8 loads per lane in
+    // flight and measured fastest at c5 size
     int k = 0;
-    for (; k + 1 < a.K; k += 2) {
-        float x0[VEC], x1[VEC];
-        warp_sample<T, VEC>(a, k, fi, fj, c0, x0);
-        warp_sample<T, VEC>(a, k + 1, fi, fj, c0, x1);
-        fold(k, x0);
-        fold(k + 1, x1);
+    for (; k + G <= a.K; k += G) {
+        float xs[G][VEC];
+#pragma unroll
+        for (int g = 0; g < G; ++g) warp_sample<T, VEC>(a, k + g, fi, fj, c0, xs[g]);
+#pragma unroll
+        for (int g = 0; g < G; ++g) fold(k + g, xs[g]);
     }
-    if (k < a.K) {
+    for (; k < a.K; ++k) {
         float x0[VEC];
         warp_sample<T, VEC>(a, k, fi, fj, c0, x0);
         fold(k, x0);
