@@ -379,10 +379,13 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void k_conv3s1(GemmArgs a) {
     int bid = blockIdx.x;
     const int nbx = gridDim.x;
     if ((nbx & 7) == 0) bid = (bid & 7) * (nbx >> 3) + (bid >> 3);
-    const int sp_tile = bid % (tx * ty);
-    const int rest = bid / (tx * ty);
-    const int n_tile = rest % nt;
-    const int split = rest / nt;
+    // channel tile fastest: the nt blocks that read the same input patch
+    // are neighbours in the remapped order and so run on the same XCD,
+    // where the patch is fetched from HBM once and then hits in L2
+    const int n_tile = bid % nt;
+    const int rest = bid / nt;
+    const int sp_tile = rest % (tx * ty);
+    const int split = rest / (tx * ty);
     const int oy0 = (sp_tile / tx) * TH, ox0 = (sp_tile % tx) * TW;
     const int n0 = n_tile * BN;
     const int c_begin = split * CH;
