@@ -11,6 +11,7 @@ Modules
             is bf16)
   schedule  single-stream release-aware execution model, RTCC and barrier
   uplink    slot-level uplink emulation producing branch arrival times
+  nms       rotated bird's-eye-view IoU and greedy non-maximum suppression
 
 Parity status: every function is pinned by tests under ``tests/`` against
 closed forms, brute force or library routines, except the composition of the
