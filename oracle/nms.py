@@ -17,11 +17,11 @@ DESIGN.md):
     overlaps nothing (IoU 0 with every box);
   * the kept boxes are reported in ascending anchor index.
 
-The intersection area is computed from its plain definition: the
-intersection of two convex polygons is the convex polygon whose vertices are
-the corners of either rectangle lying inside (or on) the other one plus the
-crossing points of their edges; those points are ordered by angle around
-their mean and the shoelace formula gives the area.
+The intersection area is computed from its plain definition: the footprint
+of one box is intersected with the four half-planes bounded by the edges of
+the other (textbook polygon clipping, one half-plane at a time; every
+crossing point is computed once, so the clipped polygon is always closed),
+and the shoelace formula gives the area of the result.
 """
 
 import math
@@ -49,24 +49,19 @@ def _cross(o, a, b):
     return (a[0] - o[0]) * (b[1] - o[1]) - (a[1] - o[1]) * (b[0] - o[0])
 
 
-def _inside(p, poly):
-    """p inside or on the counter-clockwise convex polygon."""
+def clip_halfplane(poly, e0, e1):
+    """Part of the polygon on the left of (or on) the directed line e0 -> e1."""
+    out = []
     n = len(poly)
-    return all(_cross(poly[i], poly[(i + 1) % n], p) >= 0.0 for i in range(n))
-
-
-def _segment_crossing(p1, p2, q1, q2):
-    """Crossing point of segments p1p2 and q1q2, or None (parallel / apart)."""
-    d1 = (p2[0] - p1[0], p2[1] - p1[1])
-    d2 = (q2[0] - q1[0], q2[1] - q1[1])
-    den = d1[0] * d2[1] - d1[1] * d2[0]
-    if den == 0.0:
-        return None
-    t = ((q1[0] - p1[0]) * d2[1] - (q1[1] - p1[1]) * d2[0]) / den
-    u = ((q1[0] - p1[0]) * d1[1] - (q1[1] - p1[1]) * d1[0]) / den
-    if 0.0 <= t <= 1.0 and 0.0 <= u <= 1.0:
-        return (p1[0] + t * d1[0], p1[1] + t * d1[1])
-    return None
+    for i in range(n):
+        p, q = poly[i], poly[(i + 1) % n]
+        fp, fq = _cross(e0, e1, p), _cross(e0, e1, q)
+        if fp >= 0.0:
+            out.append(p)
+        if (fp >= 0.0) != (fq >= 0.0):
+            t = fp / (fp - fq)
+            out.append((p[0] + t * (q[0] - p[0]), p[1] + t * (q[1] - p[1])))
+    return out
 
 
 def polygon_area(pts):
@@ -82,18 +77,12 @@ def polygon_area(pts):
 
 def intersection_area(A, B):
     """Area of the intersection of two convex counter-clockwise polygons."""
-    pts = [p for p in A if _inside(p, B)] + [p for p in B if _inside(p, A)]
-    for i in range(len(A)):
-        for j in range(len(B)):
-            q = _segment_crossing(A[i], A[(i + 1) % len(A)], B[j], B[(j + 1) % len(B)])
-            if q is not None:
-                pts.append(q)
-    if len(pts) < 3:
-        return 0.0
-    cx = sum(p[0] for p in pts) / len(pts)
-    cy = sum(p[1] for p in pts) / len(pts)
-    pts.sort(key=lambda p: math.atan2(p[1] - cy, p[0] - cx))
-    return polygon_area(pts)
+    poly = list(A)
+    for j in range(len(B)):
+        poly = clip_halfplane(poly, B[j], B[(j + 1) % len(B)])
+        if len(poly) < 3:
+            return 0.0
+    return polygon_area(poly)
 
 
 def iou(a, b):

@@ -66,6 +66,23 @@ def test_axis_aligned_closed_form():
         assert O.iou(a, b) == pytest.approx(aligned_overlap(a, b), abs=1e-12)
 
 
+def test_shared_edges_closed_form():
+    # integer positions and sizes with yaw a multiple of pi/2: edges of the
+    # two footprints often lie on the same line (coincident up to the
+    # rounding of cos / sin), the degenerate case of the clipping
+    rng = np.random.default_rng(8)
+    for _ in range(3000):
+        a = box(*rng.integers(-3, 3, 2).astype(float), *rng.integers(1, 4, 2).astype(float),
+                rng.integers(0, 4) * math.pi / 2)
+        b = box(*rng.integers(-3, 3, 2).astype(float), *rng.integers(1, 4, 2).astype(float),
+                rng.integers(0, 4) * math.pi / 2)
+        assert O.iou(a, b) == pytest.approx(aligned_overlap(a, b), abs=1e-12)
+    # contained with three shared sides
+    a = box(1.0, 1.0, 2.0, 1.0, 3 * math.pi / 2)
+    b = box(1.0, 0.0, 3.0, 2.0, math.pi)
+    assert O.iou(a, b) == pytest.approx(1.0 / 3.0, abs=1e-12)
+
+
 def test_square_rotated_45_degrees_is_an_octagon():
     # same centre, side s: the intersection is a regular octagon of inradius
     # s / 2, area 8 (s/2)^2 tan(pi/8) = 2 (sqrt 2 - 1) s^2
