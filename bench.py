@@ -275,6 +275,7 @@ def main(argv=None):
             "warp_fuse": round(float(node[:, post0].mean()), 4),
             "head": round(float(node[:, post0 + 1].mean()), 4),
             "decode": round(float(node[:, post0 + 2].mean()), 4),
+            "nms": round(float(node[:, post0 + 3].mean()), 4),
         },
     }
     print("# throughput done: %.3f ms/step, %.1f TFLOP/s" % (ms_per_step, value), file=sys.stderr, flush=True)

@@ -58,7 +58,7 @@ extern "C" {
 #define RTCC_API
 #endif
 
-#define RTCC_ABI_VERSION 1
+#define RTCC_ABI_VERSION 2
 #define RTCC_MAX_AGENTS 16
 #define RTCC_MAX_STAGES 4
 
@@ -123,6 +123,15 @@ typedef struct rtcc_model_desc {
     float anchor_w, anchor_l, anchor_h, anchor_z;
     float anchor_yaw[2];
     float score_logit_threshold;   /* keep anchor iff class logit > threshold   */
+    /* Rotated NMS after decoding (part of T^det, Sec. V-A3): 0 = off; else the
+     * first nms_max_candidates decoded boxes by score (descending, ties by
+     * ascending anchor index), 1 .. 16384, take part.  A candidate is kept
+     * iff its bird's-eye-view IoU (float64) with every box kept before it is
+     * <= nms_iou_threshold (in [0, 1]).  Footprint of (x, y, z, w, l, h, yaw):
+     * the rectangle centred at (x, y), side l along the heading, w across;
+     * a box with a non-finite footprint or w, l <= 0 overlaps nothing. */
+    int32_t nms_max_candidates;
+    float nms_iou_threshold;
 } rtcc_model_desc;
 
 typedef struct rtcc_runtime_opts {
@@ -134,7 +143,8 @@ typedef struct rtcc_runtime_opts {
 } rtcc_runtime_opts;
 
 typedef struct rtcc_detections {
-    int64_t count;            /* number of kept anchors                                 */
+    int64_t count;            /* number of detections (after NMS when it is on)         */
+    int64_t count_decoded;    /* anchors above the score threshold, before NMS          */
     const float *boxes;       /* [count][7] x, y, z, w, l, h, yaw (ego frame, m / rad)  */
     const float *scores;      /* [count] sigmoid of the class logit                     */
     const int32_t *anchor_idx;/* [count] ascending (row * W2 + col) * 2 + anchor        */
@@ -152,8 +162,10 @@ typedef enum rtcc_tensor_id {
     RTCC_T_SLOT = 3,          /* [H2, W2, C] stored dtype, agent slot               (agent) */
     RTCC_T_FUSED = 4,         /* [H2, W2, C] stored dtype                                   */
     RTCC_T_HEAD = 5,          /* float32 [H2, W2, 16]                                       */
-    RTCC_T_STAGE_OUT = 6      /* [Hs, Ws, Cs] stored dtype, last conv of stage `agent>>8`,
+    RTCC_T_STAGE_OUT = 6,     /* [Hs, Ws, Cs] stored dtype, last conv of stage `agent>>8`,
                                  agent `agent & 255`                                        */
+    RTCC_T_DECODED = 7        /* float32 [count_decoded][9] before NMS: x, y, z, w, l, h,
+                                 yaw, score, anchor index (int32 bits); ascending anchor    */
 } rtcc_tensor_id;
 
 typedef struct rtcc_ctx rtcc_ctx;
@@ -221,8 +233,8 @@ RTCC_API rtcc_status rtcc_release_branch_device(rtcc_ctx *ctx, int32_t agent, co
 /* Join and detect.  If any branch is still WAITING the frame is
  * communication-infeasible: RTCC_E_INFEASIBLE, no fusion kernel is
  * launched and the frame is closed.  Otherwise wait (on the GPU) for every
- * encoder, run warp, fusion, head and decode, copy the detections to the
- * host and block until they are there.  out's arrays belong to the
+ * encoder, run warp, fusion, head, decode and (if enabled) rotated NMS, copy
+ * the detections to the host and block until they are there.  out's arrays belong to the
  * context and stay valid until the next rtcc_begin_frame. */
 RTCC_API rtcc_status rtcc_join_and_detect(rtcc_ctx *ctx, rtcc_detections *out);
 
@@ -254,11 +266,29 @@ RTCC_API rtcc_status rtcc_profile_nodes(rtcc_ctx *ctx, int32_t warmup, int32_t r
 RTCC_API rtcc_status rtcc_node_times(rtcc_ctx *ctx, float *ms, int32_t *n);
 RTCC_API rtcc_status rtcc_node_count(rtcc_ctx *ctx, int32_t *n);
 
+/* Rotated NMS of caller-provided decoded boxes, the same kernels that end
+ * rtcc_join_and_detect (Sec. V-A3: decoding, score thresholding and rotated
+ * NMS end T^det).  On the current HIP device, synchronous.
+ *   device_records: [n][9] float32 x, y, z, w, l, h, yaw, score, anchor
+ *     index (int32 bit pattern), in ascending anchor index (ties in score
+ *     rank by it);
+ *   max_candidates, iou_threshold: as nms_max_candidates / nms_iou_threshold
+ *     of rtcc_model_desc (1 .. 16384, [0, 1]);
+ *   device_out: [min(n, max_candidates)][9] float32, receives the kept
+ *     records in ascending anchor index; *kept their number.
+ * n = 0 keeps nothing.  E_ARG for NULL pointers with n > 0, n < 0,
+ * n > 2^31 - 1 or parameters out of range; E_NOMEM / E_HIP for device
+ * errors.  Scratch memory is allocated and freed inside the call.  The
+ * message of a failure is rtcc_last_error(NULL). */
+RTCC_API rtcc_status rtcc_rotated_nms(const float *device_records, int64_t n, int32_t max_candidates,
+                                      float iou_threshold, float *device_out, int64_t *kept);
+
 /* Name of a status code. */
 RTCC_API const char *rtcc_status_str(rtcc_status s);
 
 /* Message of the last failed call on ctx; with ctx == NULL, the message of
- * the last failed rtcc_create on the calling thread. */
+ * the last failed context-free call (rtcc_create, rtcc_rotated_nms) on the
+ * calling thread. */
 RTCC_API const char *rtcc_last_error(const rtcc_ctx *ctx);
 
 #ifdef __cplusplus

@@ -31,6 +31,8 @@ HIP_SOURCES = [
     "kernels/pillar.hip",
     "kernels/igemm.hip",
     "kernels/post.hip",
+    "kernels/nms.hip",
+    "nms_api.hip",
 ]
 
 # Packed fp32 instructions are disabled for every device compile.

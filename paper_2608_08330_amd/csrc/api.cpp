@@ -11,8 +11,8 @@ struct rtcc_ctx {
 };
 
 namespace {
-// Message of the last failed rtcc_create on this thread (no context exists
-// to hold it); rtcc_last_error(NULL) returns it.
+// Message of the last failed context-free call (rtcc_create,
+// rtcc_rotated_nms) on this thread; rtcc_last_error(NULL) returns it.
 thread_local std::string t_create_error;
 
 template <class F>
@@ -26,6 +26,10 @@ rtcc_status guarded(F &&f) {
     }
 }
 }  // namespace
+
+namespace rtcc {
+void set_thread_error(const std::string &msg) { t_create_error = msg; }
+}  // namespace rtcc
 
 extern "C" {
 

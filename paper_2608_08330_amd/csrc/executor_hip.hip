@@ -103,6 +103,19 @@ class HipExecutor : public Executor {
         HIP_TRY(alloc(&d_dec_tiles, (dec_tiles + 1) * 4));
         HIP_TRY(alloc(&d_rec, n_anchor_ * 9 * 4));
         HIP_TRY(alloc(&d_count, 64));
+        nms_max_ = p.d.nms_max_candidates;
+        if (nms_max_ > 0) {
+            const size_t words = size_t(nms_max_ + 63) / 64;
+            HIP_TRY(alloc(&d_nms_rank, n_anchor_ * 4));
+            HIP_TRY(alloc(&d_nms_flag, n_anchor_ * 4));
+            HIP_TRY(alloc(&d_nms_order, size_t(nms_max_) * 4));
+            HIP_TRY(alloc(&d_nms_foot, size_t(nms_max_) * kern::kNmsFootDoubles * 8));
+            HIP_TRY(alloc(&d_nms_mask, size_t(nms_max_) * words * 8));
+            HIP_TRY(alloc(&d_nms_out, size_t(nms_max_) * 9 * 4));
+            HIP_TRY(alloc(&d_nms_count, 64));
+            HIP_TRY(alloc(&d_nms_mask_t, size_t(nms_max_) * 8));
+            HIP_TRY(alloc(&d_nms_partial, size_t(kern::kNmsRankSplits) * n_anchor_ * 4));
+        }
         HIP_TRY(hipHostMalloc(reinterpret_cast<void **>(&h_rec), n_anchor_ * 9 * 4, hipHostMallocDefault));
         HIP_TRY(hipHostMalloc(reinterpret_cast<void **>(&h_small), 64, hipHostMallocDefault));
         boxes_.resize(n_anchor_ * 7);
@@ -182,15 +195,20 @@ class HipExecutor : public Executor {
         if (timing) HIP_TRY(hipEventRecord(post_ev_[0], js));
         rtcc_status s = enqueue_post(affine, js, timing, err);
         if (s != RTCC_OK) return s;
-        HIP_TRY(hipMemcpyAsync(h_small, d_count, 4, hipMemcpyDeviceToHost, js));
+        int32_t *hs = reinterpret_cast<int32_t *>(h_small);
+        HIP_TRY(hipMemcpyAsync(hs, d_count, 4, hipMemcpyDeviceToHost, js));
+        if (nms_max_ > 0) HIP_TRY(hipMemcpyAsync(hs + 1, d_nms_count, 4, hipMemcpyDeviceToHost, js));
         HIP_TRY(spin_sync(js));
-        const int64_t count = *reinterpret_cast<int32_t *>(h_small);
-        if (count < 0 || size_t(count) > n_anchor_) {
-            err = "decode produced an out-of-range count";
+        const int64_t decoded = hs[0];
+        const int64_t count = nms_max_ > 0 ? hs[1] : decoded;
+        if (decoded < 0 || size_t(decoded) > n_anchor_ || count < 0 || count > decoded ||
+            (nms_max_ > 0 && count > nms_max_)) {
+            err = "decode or NMS produced an out-of-range count";
             return RTCC_E_INTERNAL;
         }
         if (count > 0) {
-            HIP_TRY(hipMemcpyAsync(h_rec, d_rec, size_t(count) * 36, hipMemcpyDeviceToHost, js));
+            HIP_TRY(hipMemcpyAsync(h_rec, nms_max_ > 0 ? d_nms_out : d_rec, size_t(count) * 36,
+                                   hipMemcpyDeviceToHost, js));
             HIP_TRY(spin_sync(js));
         }
         for (int64_t i = 0; i < count; ++i) {
@@ -202,6 +220,7 @@ class HipExecutor : public Executor {
         float ms = 0.f;
         HIP_TRY(hipEventElapsedTime(&ms, ev_frame0_, ev_head_));
         out->count = count;
+        out->count_decoded = decoded;
         out->boxes = boxes_.data();
         out->scores = scores_.data();
         out->anchor_idx = aidx_.data();
@@ -269,7 +288,7 @@ class HipExecutor : public Executor {
     }
 
     int node_count() const override {
-        return p_.K * int(3 + p_.convs.size() + (p_.ups.empty() ? 1 : p_.ups.size())) + 3;
+        return p_.K * int(3 + p_.convs.size() + (p_.ups.empty() ? 1 : p_.ups.size())) + 4;
     }
 
     rtcc_status node_times(float *ms, int *n, std::string &err) override {
@@ -282,7 +301,7 @@ class HipExecutor : public Executor {
             }
             if (p_.ups.empty()) ms[q++] = 0.f;
         }
-        for (int e = 0; e < 3; ++e) {
+        for (int e = 0; e < 4; ++e) {
             float v = 0.f;
             HIP_TRY(hipEventElapsedTime(&v, post_ev_[e], post_ev_[e + 1]));
             ms[q++] = v;
@@ -465,6 +484,24 @@ class HipExecutor : public Executor {
         da.count = static_cast<int32_t *>(d_count);
         HIP_TRY(kern::decode(da, s));
         if (timing) HIP_TRY(hipEventRecord(post_ev_[3], s));
+        if (nms_max_ > 0) {
+            kern::NmsArgs na{};
+            na.rec = static_cast<const float *>(d_rec);
+            na.count = static_cast<const int32_t *>(d_count);
+            na.rank = static_cast<int32_t *>(d_nms_rank);
+            na.flag = static_cast<int32_t *>(d_nms_flag);
+            na.order = static_cast<int32_t *>(d_nms_order);
+            na.foot = static_cast<double *>(d_nms_foot);
+            na.mask = static_cast<unsigned long long *>(d_nms_mask);
+            na.mask_t = static_cast<unsigned long long *>(d_nms_mask_t);
+            na.partial = static_cast<int32_t *>(d_nms_partial);
+            na.out = static_cast<float *>(d_nms_out);
+            na.out_count = static_cast<int32_t *>(d_nms_count);
+            na.iou_threshold = double(p.d.nms_iou_threshold);
+            na.max_candidates = nms_max_;
+            HIP_TRY(kern::rotated_nms(na, int64_t(n_anchor_), s));
+        }
+        if (timing) HIP_TRY(hipEventRecord(post_ev_[4], s));
         return RTCC_OK;
     }
 
@@ -518,6 +555,19 @@ class HipExecutor : public Executor {
                 *bytes = size_t(c.Ho) * c.Wo * c.Co * p.elt;
                 return RTCC_OK;
             }
+            case RTCC_T_DECODED: {
+                HIP_TRY(hipSetDevice(dev_));
+                HIP_TRY(hipMemcpyAsync(h_small, d_count, 4, hipMemcpyDeviceToHost, aux_stream_));
+                HIP_TRY(hipStreamSynchronize(aux_stream_));
+                const int32_t n = reinterpret_cast<int32_t *>(h_small)[0];
+                if (n < 0 || size_t(n) > n_anchor_) {
+                    err = "decoded count out of range";
+                    return RTCC_E_INTERNAL;
+                }
+                *ptr = d_rec;
+                *bytes = size_t(n) * 9 * 4;
+                return RTCC_OK;
+            }
         }
         err = "unknown tensor id";
         return RTCC_E_ARG;
@@ -556,6 +606,10 @@ class HipExecutor : public Executor {
     void *d_mat = nullptr, *d_bias = nullptr, *d_zero = nullptr;
     std::vector<kern::ConvPlan> plans_;
     void *d_fused = nullptr, *d_head = nullptr, *d_dec_tiles = nullptr, *d_rec = nullptr, *d_count = nullptr;
+    int nms_max_ = 0;  // 0: no NMS
+    void *d_nms_rank = nullptr, *d_nms_flag = nullptr, *d_nms_order = nullptr, *d_nms_foot = nullptr;
+    void *d_nms_mask = nullptr, *d_nms_out = nullptr, *d_nms_count = nullptr;
+    void *d_nms_mask_t = nullptr, *d_nms_partial = nullptr;
     float *h_rec = nullptr;
     void *h_small = nullptr;
     size_t n_anchor_ = 0;
@@ -563,7 +617,7 @@ class HipExecutor : public Executor {
     std::vector<int32_t> aidx_;
     hipStream_t join_stream_ = nullptr, copy_stream_ = nullptr, aux_stream_ = nullptr;
     hipEvent_t ev_frame0_ = nullptr, ev_head_ = nullptr;
-    hipEvent_t post_ev_[4] = {nullptr, nullptr, nullptr, nullptr};
+    hipEvent_t post_ev_[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
     std::vector<std::array<float, 6>> last_affine_;
 };
 

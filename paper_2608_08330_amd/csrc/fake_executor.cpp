@@ -55,6 +55,7 @@ class FakeExecutor : public Executor {
                << m[5] << "]";
         log_line(os.str());
         out->count = 0;
+        out->count_decoded = 0;
         return RTCC_OK;
     }
     rtcc_status tensor_bytes(int, int, size_t *, std::string &err) override {
@@ -94,4 +95,17 @@ extern "C" __attribute__((visibility("default"))) size_t rtcc_hosttest_log(char 
     }
     if (clear) rtcc::g_log.clear();
     return n;
+}
+
+namespace rtcc {
+void set_thread_error(const std::string &msg);
+}
+
+// The recording library has no GPU: the context-free NMS entry point only
+// reports that.
+extern "C" __attribute__((visibility("default"))) rtcc_status rtcc_rotated_nms(const float *, int64_t, int32_t,
+                                                                              float, float *, int64_t *kept) {
+    if (kept) *kept = 0;
+    rtcc::set_thread_error("rtcc_rotated_nms needs the GPU library");
+    return RTCC_E_STATE;
 }

@@ -127,5 +127,27 @@ struct DecodeArgs {
 constexpr int kDecodeTile = 1024;
 hipError_t decode(const DecodeArgs &a, hipStream_t s);
 
+// Rotated NMS of the decoded records (see nms.hip).
+constexpr int kNmsMaxCandidates = 16384;
+constexpr int kNmsFootDoubles = 8;
+constexpr int kNmsRankSplits = 16;  // per candidate: x, y, w, l, cos yaw, sin yaw, valid, pad
+struct NmsArgs {
+    const float *rec;             // [n][9] decoded records, ascending anchor index
+    const int32_t *count;         // n, on the device
+    int32_t *rank;                // [max_records]
+    int32_t *flag;                // [max_records]
+    int32_t *order;               // [max_candidates]
+    double *foot;                 // [max_candidates][kNmsFootDoubles]
+    unsigned long long *mask;     // [max_candidates][max_candidates / 64] (rounded up)
+    unsigned long long *mask_t;   // [max_candidates]: earlier rows of its own 64-row chunk that suppress it
+    int32_t *partial;             // [kNmsRankSplits][max_records] partial rank counts
+    float *out;                   // [max_candidates][9] kept records, ascending anchor index
+    int32_t *out_count;           // kept, on the device
+    double iou_threshold;         // suppress iff IoU > threshold
+    int32_t max_candidates;       // 1 .. kNmsMaxCandidates
+};
+// max_records bounds n (the grid of the per-record kernels).
+hipError_t rotated_nms(const NmsArgs &a, int64_t max_records, hipStream_t s);
+
 }  // namespace kern
 }  // namespace rtcc

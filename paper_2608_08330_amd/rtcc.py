@@ -20,7 +20,7 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_DIR = os.path.join(HERE, "lib")
 
-RTCC_ABI_VERSION = 1
+RTCC_ABI_VERSION = 2
 RTCC_MAX_AGENTS = 16
 RTCC_MAX_STAGES = 4
 
@@ -37,7 +37,7 @@ RTCC_MODE_RELEASE, RTCC_MODE_BARRIER = 0, 1
 RTCC_EXEC_PER_BRANCH_STREAMS, RTCC_EXEC_SERIAL = 0, 1
 RTCC_WAITING, RTCC_RELEASED, RTCC_RUNNING, RTCC_FINISHED = 0, 1, 2, 3
 (RTCC_T_PILLAR_CELLS, RTCC_T_PILLAR_COUNTS, RTCC_T_CANVAS, RTCC_T_SLOT, RTCC_T_FUSED,
- RTCC_T_HEAD, RTCC_T_STAGE_OUT) = range(7)
+ RTCC_T_HEAD, RTCC_T_STAGE_OUT, RTCC_T_DECODED) = range(8)
 
 
 class rtcc_stage(ctypes.Structure):
@@ -65,6 +65,8 @@ class rtcc_model_desc(ctypes.Structure):
         ("anchor_h", ctypes.c_float), ("anchor_z", ctypes.c_float),
         ("anchor_yaw", ctypes.c_float * 2),
         ("score_logit_threshold", ctypes.c_float),
+        ("nms_max_candidates", ctypes.c_int32),
+        ("nms_iou_threshold", ctypes.c_float),
     ]
 
 
@@ -81,6 +83,7 @@ class rtcc_runtime_opts(ctypes.Structure):
 class rtcc_detections(ctypes.Structure):
     _fields_ = [
         ("count", ctypes.c_int64),
+        ("count_decoded", ctypes.c_int64),
         ("boxes", ctypes.POINTER(ctypes.c_float)),
         ("scores", ctypes.POINTER(ctypes.c_float)),
         ("anchor_idx", ctypes.POINTER(ctypes.c_int32)),
@@ -96,7 +99,7 @@ EXPORTS = (
     "rtcc_create", "rtcc_destroy", "rtcc_set_mode", "rtcc_staging_buffer", "rtcc_begin_frame",
     "rtcc_release_branch", "rtcc_release_branch_device", "rtcc_join_and_detect",
     "rtcc_get_branch_state", "rtcc_tensor_bytes", "rtcc_get_tensor", "rtcc_profile_nodes",
-    "rtcc_node_times", "rtcc_node_count", "rtcc_status_str", "rtcc_last_error",
+    "rtcc_node_times", "rtcc_node_count", "rtcc_rotated_nms", "rtcc_status_str", "rtcc_last_error",
 )
 
 
@@ -128,6 +131,8 @@ def _declare(lib):
         "rtcc_profile_nodes": (S, [_P, ctypes.c_int32, ctypes.c_int32, _F, ctypes.POINTER(ctypes.c_int32)]),
         "rtcc_node_times": (S, [_P, _F, ctypes.POINTER(ctypes.c_int32)]),
         "rtcc_node_count": (S, [_P, ctypes.POINTER(ctypes.c_int32)]),
+        "rtcc_rotated_nms": (S, [_P, ctypes.c_int64, ctypes.c_int32, ctypes.c_float, _P,
+                                 ctypes.POINTER(ctypes.c_int64)]),
         "rtcc_status_str": (ctypes.c_char_p, [ctypes.c_int]),
         "rtcc_last_error": (ctypes.c_char_p, [_P]),
     }
@@ -192,6 +197,8 @@ def model_desc(cfg, max_points=None):
         cfg["anchor_w"], cfg["anchor_l"], cfg["anchor_h"], cfg["anchor_z"])
     d.anchor_yaw[0], d.anchor_yaw[1] = cfg["anchor_yaws"]
     d.score_logit_threshold = cfg["logit_threshold"]
+    d.nms_max_candidates = cfg.get("nms_max_candidates", 0)
+    d.nms_iou_threshold = cfg.get("nms_iou_threshold", 0.0)
     return d
 
 
@@ -315,8 +322,29 @@ def rtcc_join_and_detect(ctx):
     scores = np.ctypeslib.as_array(d.scores, shape=(n,)).copy() if n else np.zeros(0, np.float32)
     aidx = np.ctypeslib.as_array(d.anchor_idx, shape=(n,)).copy() if n else np.zeros(0, np.int32)
     K = d.n_agents
-    return dict(count=n, boxes=boxes, scores=scores, anchor_idx=aidx, t_head_s=d.t_head_s,
+    return dict(count=n, count_decoded=d.count_decoded, boxes=boxes, scores=scores, anchor_idx=aidx,
+                t_head_s=d.t_head_s,
                 t_det_s=d.t_det_s, arrival_s=list(d.arrival_s[:K]), dispatch_s=list(d.dispatch_s[:K]))
+
+
+def decoded_records(ctx):
+    """Decoded anchors of the last frame before NMS (RTCC_T_DECODED) as a
+    dict of boxes [n][7] float32, scores [n] float32, anchor_idx [n] int32."""
+    raw = rtcc_get_tensor(ctx, RTCC_T_DECODED, 0, np.float32).reshape(-1, 9)
+    return dict(boxes=raw[:, :7].copy(), scores=raw[:, 7].copy(),
+                anchor_idx=raw[:, 8].copy().view(np.int32))
+
+
+def rtcc_rotated_nms(device_records, n, max_candidates, iou_threshold, device_out, kind="gpu"):
+    """Rotated NMS of [n][9] device records into device_out; returns the
+    number kept.  Pointers are integers (e.g. torch ``data_ptr()``)."""
+    lib = load(kind)
+    kept = ctypes.c_int64()
+    st = lib.rtcc_rotated_nms(_P(device_records), n, max_candidates, iou_threshold, _P(device_out),
+                              ctypes.byref(kept))
+    if st != 0:
+        raise RtccError(st, (lib.rtcc_last_error(None) or b"").decode())
+    return kept.value
 
 
 def rtcc_get_branch_state(ctx, agent):

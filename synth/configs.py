@@ -26,6 +26,13 @@ _ANCHORS = dict(
     anchor_yaws=(0.0, math.pi / 2.0),
 )
 
+# Rotated NMS after decoding: bird's-eye-view IoU threshold and the number of
+# top-scoring decoded boxes that take part.
+_NMS = dict(
+    nms_iou_threshold=0.15,
+    nms_max_candidates=4096,
+)
+
 _MIXTURE = dict(
     ground_frac=0.7,
     ground_z_mean=-1.7,
@@ -216,6 +223,7 @@ def config(name):
         cfg["data_from"] = name
     cfg["name"] = name
     cfg.update(copy.deepcopy(_ANCHORS))
+    cfg.update(copy.deepcopy(_NMS))
     if cfg.get("dist") == "mixture":
         cfg["mixture"] = dict(_MIXTURE)
     return cfg

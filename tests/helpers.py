@@ -5,6 +5,7 @@ import time
 
 import numpy as np
 
+from oracle import nms as ONMS
 from paper_2608_08330_amd import rtcc as R
 
 # Tolerances of the parity bar: max-norm relative error ||x - r||_inf / ||r||_inf
@@ -105,3 +106,61 @@ def compare_detections(det, ref, cfg, head_ref):
         os_ = ref["scores"][[oi[a] for a in common]]
         assert np.max(np.abs(gs - os_)) <= 5 * tol
     return len(common), len(ambiguous)
+
+
+def nms_threshold(cfg):
+    """The IoU threshold as the library stores it (float32), in float64."""
+    return float(np.float32(cfg["nms_iou_threshold"]))
+
+
+def ambiguous_pairs(boxes, thr, eps=1e-9):
+    """Candidate pairs whose oracle IoU lies within eps of the threshold:
+    float64 rounding of two different IoU algorithms may decide these
+    either way."""
+    b = np.asarray(boxes, dtype=np.float64)
+    out = []
+    for i in range(len(b)):
+        for j in np.nonzero(ONMS._may_touch(b[i], b[i + 1:]))[0] + i + 1:
+            if abs(ONMS.iou(b[i], b[j]) - thr) < eps:
+                out.append((i, int(j)))
+    return out
+
+
+def check_nms(kept_idx, boxes, scores, anchor_idx, thr, max_candidates):
+    """GPU NMS result (indices into the candidate records) against the
+    oracle on the same float32 records: identical kept set; if the two
+    differ, only pairs within rounding of the threshold may explain it and
+    the GPU result must still be a valid greedy suppression."""
+    b64 = np.asarray(boxes, dtype=np.float64)
+    want = ONMS.nms(b64, scores, anchor_idx, thr, max_candidates)
+    if list(kept_idx) == list(want):
+        return len(want)
+    amb = ambiguous_pairs(b64, thr)
+    assert amb, ("NMS differs from the oracle", sorted(set(kept_idx) ^ set(want))[:10])
+    order = ONMS.ranking(scores, anchor_idx, max_candidates)
+    rank = {i: r for r, i in enumerate(order)}
+    kept = set(kept_idx)
+    assert kept <= set(order)
+    for i in kept:
+        for j in kept:
+            if i < j:
+                assert ONMS.iou(b64[i], b64[j]) <= thr + 1e-9
+    for i in order:
+        if i not in kept:
+            assert any(rank[k] < rank[i] and ONMS.iou(b64[i], b64[k]) > thr - 1e-9 for k in kept)
+    return len(kept)
+
+
+def check_frame_nms(ctx, det, cfg):
+    """The detections of the last frame are the oracle's NMS of the GPU's
+    own decoded records (bit-identical records, identical kept set).
+    Returns the decoded records for the decode-stage comparison."""
+    dec = R.decoded_records(ctx)
+    assert det["count_decoded"] == len(dec["anchor_idx"])
+    assert list(dec["anchor_idx"]) == sorted(dec["anchor_idx"])
+    pos = {int(a): i for i, a in enumerate(dec["anchor_idx"])}
+    kept = [pos[int(a)] for a in det["anchor_idx"]]
+    check_nms(kept, dec["boxes"], dec["scores"], dec["anchor_idx"], nms_threshold(cfg), cfg["nms_max_candidates"])
+    assert np.array_equal(det["boxes"].view(np.uint32), dec["boxes"][kept].view(np.uint32))
+    assert np.array_equal(det["scores"].view(np.uint32), dec["scores"][kept].view(np.uint32))
+    return dec

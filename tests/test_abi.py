@@ -197,6 +197,8 @@ def test_pose_affines_match_oracle(host_ctx):
 @pytest.mark.parametrize("field,value", [
     ("n_agents", 0), ("n_agents", 17), ("c_pfn", 48), ("pillar_size", 0.0), ("n_anchors", 3),
     ("precision", 5), ("fusion", 9), ("max_points", 0), ("abi_version", 99),
+    ("nms_max_candidates", -1), ("nms_max_candidates", 16385), ("nms_iou_threshold", 1.5),
+    ("nms_iou_threshold", -0.5), ("nms_iou_threshold", float("nan")),
 ])
 def test_bad_descriptor_rejected(field, value):
     cfg = synth.config("t_max")
@@ -218,3 +220,19 @@ def test_weight_blob_size_and_values_checked():
     bad[3] = np.nan
     with pytest.raises(R.RtccError):
         R.rtcc_create(R.model_desc(cfg), bad, kind="host")
+
+
+def test_nms_off_and_threshold_edges_accepted():
+    cfg = synth.config("t_max")
+    w = R.weights_blob(cfg, synth.make_weights(cfg))
+    for cap, thr in ((0, 7.0), (1, 0.0), (16384, 1.0)):
+        d = R.model_desc(cfg)
+        d.nms_max_candidates, d.nms_iou_threshold = cap, thr
+        R.rtcc_create(d, w, kind="host").close()
+
+
+def test_host_library_nms_entry_reports_no_gpu():
+    lib = R.load("host")
+    kept = ctypes.c_int64(5)
+    assert lib.rtcc_rotated_nms(None, 0, 16, 0.15, None, ctypes.byref(kept)) == R.RTCC_E_STATE
+    assert kept.value == 0 and b"GPU" in lib.rtcc_last_error(None)

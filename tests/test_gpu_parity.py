@@ -2,8 +2,9 @@
 
 Pillar cells and counts are compared bit for bit; activations by max-norm
 relative error (1e-4 fp32, 2e-2 bf16); detections as sets with a tolerance
-band around the threshold.  RTCC and barrier runs of a frame must give
-bitwise identical outputs."""
+band around the threshold, before NMS; the NMS output exactly against the
+oracle's NMS of the same decoded records.  RTCC and barrier runs of a frame
+must give bitwise identical outputs."""
 
 import sys
 
@@ -13,7 +14,7 @@ import pytest
 import synth
 from oracle import network as N
 from paper_2608_08330_amd import rtcc as R
-from tests.helpers import TOL, compare_detections, make_ctx, rel_err, run_frame, tensors
+from tests.helpers import TOL, check_frame_nms, compare_detections, make_ctx, rel_err, run_frame, tensors
 
 pytestmark = pytest.mark.gpu
 
@@ -63,9 +64,12 @@ def test_frame_parity_and_mode_identity(name):
         det_r = run_frame(ctx, fr, R.RTCC_MODE_RELEASE, a)
         got_r = tensors(ctx, cfg)
         _check_frame(cfg, fr, ref, got_r)
-        compare_detections(det_r, ref["det"], cfg, ref["head"])
+        dec_r = check_frame_nms(ctx, det_r, cfg)
+        compare_detections(dec_r, ref["det"], cfg, ref["head"])
+        _say("  %s: %d decoded, %d after NMS" % (name, det_r["count_decoded"], det_r["count"]))
         det_b = run_frame(ctx, fr, R.RTCC_MODE_BARRIER, a)
         got_b = tensors(ctx, cfg)
+        dec_b = R.decoded_records(ctx)
     # RTCC and barrier: bitwise identical outputs and identical box sets
     for key in ("canvas", "slot"):
         for k in range(cfg["K"]):
@@ -74,6 +78,8 @@ def test_frame_parity_and_mode_identity(name):
     assert np.array_equal(got_r["head"].view(np.uint32), got_b["head"].view(np.uint32))
     assert np.array_equal(det_r["anchor_idx"], det_b["anchor_idx"])
     assert np.array_equal(det_r["boxes"].view(np.uint32), det_b["boxes"].view(np.uint32))
+    assert np.array_equal(dec_r["anchor_idx"], dec_b["anchor_idx"])
+    assert np.array_equal(dec_r["boxes"].view(np.uint32), dec_b["boxes"].view(np.uint32))
 
 
 def test_repeated_frames_are_bitwise_identical():

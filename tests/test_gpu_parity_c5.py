@@ -17,7 +17,7 @@ import pytest
 import synth
 from oracle import network as N
 from paper_2608_08330_amd import rtcc as R
-from tests.helpers import TOL, as_f32, compare_detections, make_ctx
+from tests.helpers import TOL, as_f32, check_frame_nms, compare_detections, make_ctx
 
 pytestmark = pytest.mark.gpu
 
@@ -70,9 +70,10 @@ def test_c5_full_size_parity_and_mode_identity():
         assert err <= tol, ("head", err)
         oref = dict(anchor_idx=ref["det_anchor_idx"], boxes=ref["det_boxes"], scores=ref["det_scores"],
                     logits=ref["logits"].astype(np.float64))
-        common, ambiguous = compare_detections(det, oref, cfg, np.array([ref["head_absmax"]]))
-        print("c5 detections: gpu %d, oracle %d, common %d, band %d" % (
-            det["count"], len(ref["det_anchor_idx"]), common, ambiguous), flush=True)
+        dec = check_frame_nms(ctx, det, cfg)
+        common, ambiguous = compare_detections(dec, oref, cfg, np.array([ref["head_absmax"]]))
+        print("c5 detections: gpu %d, oracle %d, common %d, band %d; %d after NMS" % (
+            det["count_decoded"], len(ref["det_anchor_idx"]), common, ambiguous, det["count"]), flush=True)
 
         det_b = _run(ctx, cfg, fr, dev, R.RTCC_MODE_BARRIER)
         head_b = R.rtcc_get_tensor(ctx, R.RTCC_T_HEAD, 0, np.float32).reshape(H2 * W2, 16)
