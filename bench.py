@@ -7,10 +7,12 @@ device-resident inputs, then the join (warp, fusion, head, decode, D2H).
 
 Output: one JSON line with
   value       encoder throughput, TFLOP/s = algorithmic encoder FLOPs of the
-              timed frames / wall time of the timed frames
-  roofline    the dominant kernel (3x3 conv implicit GEMM): algorithmic
-              FLOPs / summed HIP-event durations of its launches, against
-              the bf16 dense MFMA peak
+              timed frames / wall time of the timed frames, with the library's
+              default executor (per-branch streams)
+  roofline    the dominant kernel (3x3 convolution): algorithmic FLOPs /
+              summed kernel durations of its launches (HIP events that
+              bracket the kernels, one compute stream), against the bf16
+              dense MFMA peak
   latency     p50 / p95 complete-detection latency T^det, RTCC vs barrier,
               over replayed synthetic arrival traces (pinned host inputs,
               H2D included, as on the release path)
@@ -38,7 +40,7 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 # kernel source it was taken on; after a change it reads null until re-taken.
 MEASURED_TRAFFIC = {
     "conv": dict(src="paper_2608_08330_amd/csrc/kernels/igemm.hip", bytes=26.77e6,
-                 sha256="e31ef1d53cac4675e11dccf192aefcc9951bc4e2bdcb837e037f8b951d6d886c"),
+                 sha256="c344b6046ed2bdf9191513bbc9f4229dfac31992b8be9a50b15e9f7851d1aef1"),
     "warp_fuse": dict(src="paper_2608_08330_amd/csrc/kernels/post.hip", bytes=493.70e6,
                       sha256="2bd8e6aa825c827403e7c4578e180b00136c895a7db997c87a5fb36d8ebb8e95"),
 }
@@ -94,9 +96,10 @@ def encoder_flops(cfg, lw, n_used):
     return pfn + sum(c["flops"] for c in lw["convs"]) + sum(u["flops"] for u in lw["ups"])
 
 
-def timed_steps(ctx, cfg, frame, dev_pts, steps, warmup, R, torch):
+def timed_steps(ctx, cfg, frame, dev_pts, steps, warmup, R, torch, record_nodes=True):
     """Warm-up, then exactly `steps` timed frames bracketed by device syncs.
-    Returns wall seconds and the per-node HIP-event times of every step."""
+    Returns wall seconds and (with record_nodes) the per-node HIP-event times
+    of every step."""
     K = cfg["K"]
     n = [len(p) for p in frame["points"]]
 
@@ -113,7 +116,8 @@ def timed_steps(ctx, cfg, frame, dev_pts, steps, warmup, R, torch):
     t = time.perf_counter()
     for _ in range(steps):
         one()
-        node.append(R.rtcc_node_times(ctx))
+        if record_nodes:
+            node.append(R.rtcc_node_times(ctx))
     torch.cuda.synchronize()
     return time.perf_counter() - t, node
 
@@ -151,7 +155,10 @@ def main(argv=None):
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="c5")
-    ap.add_argument("--exec", choices=["serial", "streams"], default="serial")
+    ap.add_argument("--exec", choices=["serial", "streams"], default="streams",
+                    help="executor of the throughput pass (the library's default: per-branch streams)")
+    ap.add_argument("--roofline-steps", type=int, default=10,
+                    help="frames of the serial, node-timed pass behind roofline and per-layer tables")
     ap.add_argument("--latency-traces", type=int, default=30)
     ap.add_argument("--latency-reps", type=int, default=3)
     ap.add_argument("--cpu-budget", type=float, default=15.0)
@@ -190,16 +197,27 @@ def main(argv=None):
     frame = synth.make_frame(cfg)
     lw = layer_work(cfg)
     K = cfg["K"]
-    o = R.rtcc_runtime_opts()
-    o.exec = R.RTCC_EXEC_SERIAL if a.exec == "serial" else R.RTCC_EXEC_PER_BRANCH_STREAMS
-    o.node_timing = 1
-    o.premature_tol_s = 1e-6
-    ctx = R.rtcc_create(R.model_desc(cfg), R.weights_blob(cfg, frame["weights"]), o)
+
+    def make_ctx(exec_kind, timing):
+        o = R.rtcc_runtime_opts()
+        o.exec = R.RTCC_EXEC_SERIAL if exec_kind == "serial" else R.RTCC_EXEC_PER_BRANCH_STREAMS
+        o.node_timing = 1 if timing else 0
+        o.premature_tol_s = 1e-6
+        return R.rtcc_create(R.model_desc(cfg), R.weights_blob(cfg, frame["weights"]), o)
+
     dev_pts = [torch.from_numpy(p).to("cuda") for p in frame["points"]]
     torch.cuda.synchronize()
 
-    wall, node = timed_steps(ctx, cfg, frame, dev_pts, a.steps, a.warmup, R, torch)
+    # throughput: the library's executor, no node events
+    ctx_t = make_ctx(a.exec, False)
+    wall, _ = timed_steps(ctx_t, cfg, frame, dev_pts, a.steps, a.warmup, R, torch, record_nodes=False)
     ms_per_step = wall / a.steps * 1e3
+    # roofline and per-node tables: one compute stream (the paper's execution
+    # model), so that node durations do not overlap; conv nodes are timed by
+    # events that bracket their kernels
+    ctx = make_ctx("serial", True)
+    wall_s, node = timed_steps(ctx, cfg, frame, dev_pts, a.roofline_steps, a.warmup, R, torch)
+    rsteps = a.roofline_steps
 
     # used points per agent (PFN FLOPs), from the library's pillar counts
     used = []
@@ -217,18 +235,18 @@ def main(argv=None):
     for k in range(K):
         base = k * per_agent + 3
         conv_ms += node[:, base:base + L].sum()
-    conv_flops = sum(c["flops"] for c in lw["convs"]) * K * a.steps
-    conv_launches = L * K * a.steps
+    conv_flops = sum(c["flops"] for c in lw["convs"]) * K * rsteps
+    conv_launches = L * K * rsteps
     achieved = conv_flops / (conv_ms * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if cfg["precision"] == "bf16" else PEAK_FP32_TFLOPS
     pillar_ms = sum(node[:, k * per_agent + 1].sum() + node[:, k * per_agent + 2].sum() for k in range(K))
     P = [int(R.rtcc_tensor_bytes(ctx, R.RTCC_T_PILLAR_CELLS, k)) // 4 for k in range(K)]
     pil_bytes = sum(16 * len(frame["points"][k]) + 8 * P[k] + lw["H"] * lw["W"] * cfg["c_pfn"] * lw["elt"]
-                    for k in range(K)) * a.steps
+                    for k in range(K)) * rsteps
     post0 = K * per_agent
     warp_ms = node[:, post0].sum()
     slot_bytes = lw["H2"] * lw["W2"] * lw["C"] * lw["elt"]
-    warp_bytes = (K + 1) * slot_bytes * a.steps
+    warp_bytes = (K + 1) * slot_bytes * rsteps
 
     layers = []
     for l, c in enumerate(lw["convs"]):
@@ -251,8 +269,10 @@ def main(argv=None):
         "config": {
             "workload": "%s: %d agents x %d points, %dx%d BEV, %s, %s fusion" % (
                 cfg["name"], K, cfg["n_points"], lw["H"], lw["W"], cfg["precision"], cfg["fusion"]),
-            "agents": K, "executor": a.exec, "inputs": "device-resident",
+            "agents": K, "inputs": "device-resident",
+            "executor": "per-branch streams" if a.exec == "streams" else "serial",
         },
+        "serial_ms_per_step": round(wall_s / rsteps * 1e3, 4),
         "roofline": {
             "bound": "mfma", "kernel": "3x3 conv: halo-tiled k_conv3s1 + implicit-GEMM k_igemm",
             "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
@@ -269,9 +289,9 @@ def main(argv=None):
         "node_ms_mean": {
             "pillar": round(float(np.mean([node[:, k * per_agent + 1] for k in range(K)])), 4),
             "pfn_canvas": round(float(np.mean([node[:, k * per_agent + 2] for k in range(K)])), 4),
-            "conv_total_per_agent": round(conv_ms / (K * a.steps), 4),
+            "conv_total_per_agent": round(conv_ms / (K * rsteps), 4),
             "up_total_per_agent": round(float(np.sum([node[:, k * per_agent + 3 + L:k * per_agent + per_agent]
-                                                      for k in range(K)]) / (K * a.steps)), 4),
+                                                      for k in range(K)]) / (K * rsteps)), 4),
             "warp_fuse": round(float(node[:, post0].mean()), 4),
             "head": round(float(node[:, post0 + 1].mean()), 4),
             "decode": round(float(node[:, post0 + 2].mean()), 4),
@@ -284,18 +304,23 @@ def main(argv=None):
         if cfg["arrivals"]["kind"] == "uplink":
             raise SystemExit("latency replay of uplink-driven configs runs in the load-sweep report")
         arr = synth.arrival_draws(cfg, a.latency_traces) * 1e-3
-        staged = replay.stage_inputs(ctx, frame["points"])
-        rows, identical = replay.replay_traces(ctx, staged, frame["poses"], arr, a.latency_reps)
-        lat = replay.summarize(rows)
-        lat["reps"] = a.latency_reps
-        lat["outputs_identical_rtcc_vs_barrier"] = bool(identical)
-        lat["rtcc_below_barrier_every_trace"] = bool(lat["wins_median"] == len(rows))
-        out["latency"] = lat
-        print("# latency done", file=sys.stderr, flush=True)
+        # primary: one compute stream, as the paper's latency model; then the
+        # per-branch-stream executor on the same traces
+        for key, c in (("latency", ctx), ("latency_streams", ctx_t)):
+            staged = replay.stage_inputs(c, frame["points"])
+            rows, identical = replay.replay_traces(c, staged, frame["poses"], arr, a.latency_reps)
+            lat = replay.summarize(rows)
+            lat["reps"] = a.latency_reps
+            lat["executor"] = "serial" if c is ctx else "per-branch streams"
+            lat["outputs_identical_rtcc_vs_barrier"] = bool(identical)
+            lat["rtcc_below_barrier_every_trace"] = bool(lat["wins_median"] == len(rows))
+            out[key] = lat
+            print("# %s done" % key, file=sys.stderr, flush=True)
 
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, frame, a.cpu_budget)
     ctx.close()
+    ctx_t.close()
     print(json.dumps(out))
     return 0
 

@@ -261,8 +261,11 @@ RTCC_API rtcc_status rtcc_profile_nodes(rtcc_ctx *ctx, int32_t warmup, int32_t r
 /* Per-kernel-group GPU durations (ms) of the last frame, recorded when
  * opts.node_timing = 1.  For each agent k, in order: h2d, pillar (cell ids,
  * counting sort, segment), pfn_canvas, conv[0 .. L-1], up[0 .. S-1] (0 if
- * no upsampling); then warp_fuse, head, decode.  *n = number written;
- * ms must hold at least rtcc_node_count() floats. */
+ * no upsampling); then warp_fuse, head, decode, nms (0 if off).  Conv nodes
+ * are the execution time of their kernels (events that bracket the kernels
+ * themselves); the other nodes span the stream between events recorded
+ * around them, dispatch gaps included.  *n = number written; ms must hold
+ * at least rtcc_node_count() floats. */
 RTCC_API rtcc_status rtcc_node_times(rtcc_ctx *ctx, float *ms, int32_t *n);
 RTCC_API rtcc_status rtcc_node_count(rtcc_ctx *ctx, int32_t *n);
 

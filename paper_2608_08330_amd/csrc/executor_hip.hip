@@ -95,6 +95,8 @@ class HipExecutor : public Executor {
             HIP_TRY(hipEventCreateWithFlags(&b.h2d_done, hipEventDisableTiming));
             b.ev.resize(4 + p.convs.size() + p.ups.size());
             for (auto &e : b.ev) HIP_TRY(hipEventCreate(&e));
+            b.kev.resize(2 * p.convs.size());
+            for (auto &e : b.kev) HIP_TRY(hipEventCreate(&e));
         }
         HIP_TRY(alloc(&d_fused, size_t(p.H2) * p.W2 * p.c_slot * p.elt));
         HIP_TRY(alloc(&d_head, size_t(p.H2) * p.W2 * 16 * 4));
@@ -296,7 +298,11 @@ class HipExecutor : public Executor {
         for (const Branch &b : br_) {
             for (size_t e = 0; e + 1 < b.ev.size(); ++e) {
                 float v = 0.f;
-                HIP_TRY(hipEventElapsedTime(&v, b.ev[e], b.ev[e + 1]));
+                const size_t l = e - 3;  // node e >= 3 and < 3 + L is conv layer e - 3
+                if (e >= 3 && l < p_.convs.size())
+                    HIP_TRY(hipEventElapsedTime(&v, b.kev[2 * l], b.kev[2 * l + 1]));
+                else
+                    HIP_TRY(hipEventElapsedTime(&v, b.ev[e], b.ev[e + 1]));
                 ms[q++] = v;
             }
             if (p_.ups.empty()) ms[q++] = 0.f;
@@ -321,6 +327,7 @@ class HipExecutor : public Executor {
         hipStream_t stream = nullptr;
         hipEvent_t done = nullptr, h2d_done = nullptr;
         std::vector<hipEvent_t> ev;
+        std::vector<hipEvent_t> kev;  // per conv layer: start / stop of its kernels
         const float *src = nullptr;
         int32_t n = 0;
         bool host_input = true;
@@ -416,7 +423,10 @@ class HipExecutor : public Executor {
             ga.variant = plans_[l].variant;
             ga.zero = d_zero;
             ga.ws = static_cast<float *>(b.d_ws);
-            HIP_TRY(kern::conv3x3(p.bf16, ga, s));
+            // with timing, conv nodes are timed by events bracketing their
+            // kernels' execution (no dispatch gap)
+            HIP_TRY(kern::conv3x3(p.bf16, ga, s, timing ? b.kev[2 * l] : nullptr,
+                                  timing ? b.kev[2 * l + 1] : nullptr));
             if (timing) HIP_TRY(hipEventRecord(b.ev[ev], s));
             ++ev;
             x = b.d_act[l];
@@ -584,6 +594,8 @@ class HipExecutor : public Executor {
             if (b.done) (void)hipEventDestroy(b.done);
             if (b.h2d_done) (void)hipEventDestroy(b.h2d_done);
             for (hipEvent_t e : b.ev)
+                if (e) (void)hipEventDestroy(e);
+            for (hipEvent_t e : b.kev)
                 if (e) (void)hipEventDestroy(e);
         }
         for (void *ptr : dev_allocs_) (void)hipFree(ptr);

@@ -33,6 +33,8 @@
 // the stream.
 #include "kernels.hpp"
 
+#include <hip/hip_ext.h>
+
 namespace rtcc {
 namespace kern {
 
@@ -49,6 +51,14 @@ template <int N>
 struct VmWait {
     static constexpr int imm = (N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8);
 };
+// Before a barrier after which another wave may refill an LDS buffer that
+// this wave read in the previous step: wait until this wave's LDS reads
+// have returned.  The compiler places its own lgkmcnt waits just before the
+// MFMAs that use the data and may sink those MFMAs (and the waits) below the
+// barrier, leaving reads in flight while the refill lands.  Inline assembly
+// with a memory clobber: no LDS access moves across it.
+__device__ inline void lds_reads_done() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
 // s_waitcnt vmcnt(n) for n <= NMAX; n must fold to a constant after
 // unrolling, so that the chain collapses to the one instruction.
 template <int NMAX>
@@ -245,6 +255,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_igemm(GemmArgs a) {
         // Loads of steps kt+1 .. kt+STAGES-2 may stay in flight.
         if (kt + STAGES - 2 < KT) __builtin_amdgcn_s_waitcnt(VmWait<(STAGES - 2) * LPS>::imm);
         else __builtin_amdgcn_s_waitcnt(VmWait<0>::imm);
+        lds_reads_done();  // step kt-1's buffer is refilled right after the barrier
         // No fence: only this step's loads are awaited above, later steps
         // stay in flight across the barrier.
         __builtin_amdgcn_s_barrier();  // step kt visible to all waves; step kt-1 consumed
@@ -462,6 +473,9 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void k_conv3s1(GemmArgs a) {
             // taps 1 .. R - 1, the next chunk's patch
             if (!last) vm_wait<(R - 2) * LB + LA>((R - 2) * LB + (t >= 1 && t <= R - 1 ? LA : 0));
             else vm_wait<(R - 2) * LB>((8 - t < R - 2 ? 8 - t : R - 2) * LB);
+            // the weight buffer of step s - 1 (and at tap 0 the patch buffer
+            // of chunk c - 1) is refilled right after this barrier
+            lds_reads_done();
             __builtin_amdgcn_s_barrier();
             asm volatile("" ::: "memory");
             if (s + R - 1 < S) issue_w(s + R - 1);
@@ -562,60 +576,70 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(GemmArgs a) {
                       fmaxf(s.z + a.bias[n + 2], 0.f), fmaxf(s.w + a.bias[n + 3], 0.f));
 }
 
+// Launch on stream s; with events, through hipExtLaunchKernelGGL so that they
+// bracket the kernel's own execution.
+template <typename F>
+hipError_t launch_kernel(F kernel, dim3 grid, dim3 block, hipStream_t s, hipEvent_t e0, hipEvent_t e1,
+                         const GemmArgs &a) {
+    if (e0 || e1) hipExtLaunchKernelGGL(kernel, grid, block, 0, s, e0, e1, 0, a);
+    else kernel<<<grid, block, 0, s>>>(a);
+    return hipGetLastError();
+}
+
 template <typename T, int BM, int BN, int WGM, int WGN, int STAGES, bool DECONV>
-hipError_t launch_cfg(const GemmArgs &a, hipStream_t s) {
+hipError_t launch_cfg(const GemmArgs &a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr) {
     const int M = DECONV ? a.Hi * a.Wi : a.Ho * a.Wo;
     const unsigned gz = DECONV ? unsigned(a.u * a.u) : 1u;
     const unsigned nx = unsigned((M + BM - 1) / BM) * unsigned((a.N + BN - 1) / BN) * unsigned(a.splits);
-    k_igemm<T, BM, BN, WGM, WGN, STAGES, DECONV><<<dim3(nx, 1, gz), 64 * WGM * WGN, 0, s>>>(a);
-    hipError_t e = hipGetLastError();
+    hipError_t e = launch_kernel(k_igemm<T, BM, BN, WGM, WGN, STAGES, DECONV>, dim3(nx, 1, gz),
+                                 dim3(64 * WGM * WGN), s, e0, a.splits == 1 ? e1 : nullptr, a);
     if (e != hipSuccess || a.splits == 1) return e;
     const int64_t total = int64_t(M) * (a.N / 4);
-    k_splitk_reduce<T><<<unsigned((total + 255) / 256), 256, 0, s>>>(a);
-    return hipGetLastError();
+    return launch_kernel(k_splitk_reduce<T>, dim3(unsigned((total + 255) / 256)), dim3(256), s, nullptr, e1, a);
 }
 
 template <typename T, int TH, int BN = 128, int WGM = 4, int WGN = 2, int RB = 64, int STRIDE = 1, int KG = 1,
           int R = 3>
-hipError_t launch_halo(const GemmArgs &a, hipStream_t s) {
+hipError_t launch_halo(const GemmArgs &a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr) {
     const unsigned tiles = unsigned((a.Wo + 15) / 16) * unsigned((a.Ho + TH - 1) / TH);
     const unsigned nx = tiles * unsigned(a.N / BN) * unsigned(a.splits);
-    k_conv3s1<T, TH, BN, WGM, WGN, RB, STRIDE, KG, R><<<dim3(nx), 64 * WGM * WGN * KG, 0, s>>>(a);
-    hipError_t e = hipGetLastError();
+    hipError_t e = launch_kernel(k_conv3s1<T, TH, BN, WGM, WGN, RB, STRIDE, KG, R>, dim3(nx),
+                                 dim3(64 * WGM * WGN * KG), s, e0, a.splits == 1 ? e1 : nullptr, a);
     if (e != hipSuccess || a.splits == 1) return e;
     const int64_t total = int64_t(a.Ho) * a.Wo * (a.N / 4);
-    k_splitk_reduce<T><<<unsigned((total + 255) / 256), 256, 0, s>>>(a);
-    return hipGetLastError();
+    return launch_kernel(k_splitk_reduce<T>, dim3(unsigned((total + 255) / 256)), dim3(256), s, nullptr, e1, a);
 }
 
 template <typename T, bool DECONV>
-hipError_t launch(const GemmArgs &a, hipStream_t s) {
+hipError_t launch(const GemmArgs &a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr) {
     if (!DECONV) {
         // 128-byte K steps pay off from 256 input channels (bf16) on
         const bool rb128 = (a.Ci * int(sizeof(T))) % 128 == 0 && a.Ci * int(sizeof(T)) >= 512;
         switch (a.variant) {
             // weight ring depth R: 4 where it measured faster at the c5 shapes
             case kConvHalo8:
-                return rb128 ? launch_halo<T, 8, 128, 4, 2, 128, 1, 1, 4>(a, s)
-                             : launch_halo<T, 8, 128, 4, 2, 64, 1, 1, 4>(a, s);
+                return rb128 ? launch_halo<T, 8, 128, 4, 2, 128, 1, 1, 4>(a, s, e0, e1)
+                             : launch_halo<T, 8, 128, 4, 2, 64, 1, 1, 4>(a, s, e0, e1);
             case kConvHalo4:
-                return rb128 ? launch_halo<T, 4, 128, 2, 2, 128, 1>(a, s) : launch_halo<T, 4, 128, 2, 2, 64, 1>(a, s);
-            case kConvHalo8S2: return launch_halo<T, 8, 128, 4, 2, 64, 2, 1, 4>(a, s);
-            case kConvHalo4S2: return launch_halo<T, 4, 128, 4, 2, 64, 2>(a, s);
+                return rb128 ? launch_halo<T, 4, 128, 2, 2, 128, 1>(a, s, e0, e1)
+                             : launch_halo<T, 4, 128, 2, 2, 64, 1>(a, s, e0, e1);
+            case kConvHalo8S2: return launch_halo<T, 8, 128, 4, 2, 64, 2, 1, 4>(a, s, e0, e1);
+            case kConvHalo4S2: return launch_halo<T, 4, 128, 4, 2, 64, 2>(a, s, e0, e1);
             case kConvHalo4N64K2:
-                return rb128 ? launch_halo<T, 4, 64, 2, 2, 128, 1, 2>(a, s) : launch_halo<T, 4, 64, 2, 2, 64, 1, 2>(a, s);
-            case kConvHalo4S2N64K2: return launch_halo<T, 4, 64, 2, 2, 64, 2, 2, 4>(a, s);
+                return rb128 ? launch_halo<T, 4, 64, 2, 2, 128, 1, 2>(a, s, e0, e1)
+                             : launch_halo<T, 4, 64, 2, 2, 64, 1, 2>(a, s, e0, e1);
+            case kConvHalo4S2N64K2: return launch_halo<T, 4, 64, 2, 2, 64, 2, 2, 4>(a, s, e0, e1);
             default: break;
         }
     }
-    if (a.N % 128 == 0) return launch_cfg<T, 128, 128, 4, 2, 4, DECONV>(a, s);
-    return launch_cfg<T, 128, 64, 4, 1, 4, DECONV>(a, s);
+    if (a.N % 128 == 0) return launch_cfg<T, 128, 128, 4, 2, 4, DECONV>(a, s, e0, e1);
+    return launch_cfg<T, 128, 64, 4, 1, 4, DECONV>(a, s, e0, e1);
 }
 
 }  // namespace
 
-hipError_t conv3x3(bool bf16, const GemmArgs &a, hipStream_t s) {
-    return bf16 ? launch<uint16_t, false>(a, s) : launch<float, false>(a, s);
+hipError_t conv3x3(bool bf16, const GemmArgs &a, hipStream_t s, hipEvent_t start, hipEvent_t stop) {
+    return bf16 ? launch<uint16_t, false>(a, s, start, stop) : launch<float, false>(a, s, start, stop);
 }
 
 hipError_t deconv(bool bf16, const GemmArgs &a, hipStream_t s) {

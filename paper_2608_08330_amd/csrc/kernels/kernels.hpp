@@ -95,7 +95,11 @@ struct ConvPlan {
 };
 // Kernel variant and K split of one 3x3 conv layer on a GPU with n_cu CUs.
 ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, int stride, int n_cu);
-hipError_t conv3x3(bool bf16, const GemmArgs &a, hipStream_t s);
+// With start / stop events, the first kernel of the convolution records
+// `start` when it begins executing and the last one `stop` when it ends
+// (kernel execution time, without the dispatch gap before it).
+hipError_t conv3x3(bool bf16, const GemmArgs &a, hipStream_t s, hipEvent_t start = nullptr,
+                   hipEvent_t stop = nullptr);
 hipError_t deconv(bool bf16, const GemmArgs &a, hipStream_t s);
 // Output tiles of the implicit GEMM.
 int gemm_tiles(int M, int N);
