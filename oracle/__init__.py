@@ -10,7 +10,12 @@ Modules
             warp, fusion, head and box decode (fp64 unless a storage point
             is bf16)
   schedule  single-stream release-aware execution model, RTCC and barrier
-  uplink    slot-level uplink emulation producing branch arrival times
+  uplink    slot-level uplink emulation producing branch arrival times,
+            with round robin, proportional fair and the five causal
+            evaluation schedulers
+  ofdma     the evaluation's OFDMA channel (mobility, path loss,
+            blockage, fading), DAG upward rank and the paired
+            measured-DAG trial in integer nanoseconds
   nms       rotated bird's-eye-view IoU and greedy non-maximum suppression
 
 Parity status: every function is pinned by tests under ``tests/`` against

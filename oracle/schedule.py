@@ -80,3 +80,32 @@ def w_pre(a, c_enc, c_post=()):
 def overlap_window(a):
     """Usable overlap window: time between the first and the last arrival."""
     return float(np.max(a) - np.min(a))
+
+
+def execute_int(release, c_enc, c_post):
+    """The same single-stream model on integer times (e.g. nanoseconds), in
+    Python integers, so that every start, finish and latency is exact.
+    Returns dict(order, start, finish, T, g) as :func:`execute`."""
+    r = [int(v) for v in release]
+    c = [int(v) for v in c_enc]
+    K = len(r)
+    order = sorted(range(K), key=lambda k: (r[k], k))
+    start = [0] * K
+    finish = [0] * K
+    g = 0
+    for k in order:
+        start[k] = max(r[k], g)
+        finish[k] = start[k] + c[k]
+        g = finish[k]
+    return dict(order=order, start=start, finish=finish, T=g + sum(int(v) for v in c_post), g=g)
+
+
+def paired_int(a, c_enc, c_post):
+    """RTCC and barrier on the same integer arrival vector: returns (T_R,
+    T_B, W_pre) with W_pre the RTCC encoder work inside [0, A)."""
+    a = [int(v) for v in a]
+    A = max(a)
+    r = execute_int(a, c_enc, c_post)
+    b = execute_int([A] * len(a), c_enc, c_post)
+    w = sum(max(0, min(f, A) - s) for s, f in zip(r["start"], r["finish"]))
+    return r["T"], b["T"], w

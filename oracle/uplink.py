@@ -17,7 +17,22 @@ generation of Sec. IV-B, written out slot by slot:
     a_k = +inf and the frame is infeasible (Sec. IV-C).
 
 Rates: R_{k,f}[t] = bandwidth * log2(1 + snr * g_{k,f}[t]) with
-g ~ Exp(1) (Rayleigh fading power) drawn by ``synth.fading_draws``.
+g ~ Exp(1) (Rayleigh fading power) drawn by ``synth.fading_draws`` (the
+single-RB workloads), or the OFDMA channel of ``oracle.ofdma``.
+
+Policies: round robin and proportional fair (single-RB workloads), and the
+five causal evaluation schedulers of eqs. evaluation_schedulers and
+evaluation_scores: RB f goes to the eligible agent with the largest score
+s_{k,f}[t], ties to the smallest agent index, where s is
+  MaxRate           R_{k,f}[t]
+  MaxWeight         Q_k[t] R_{k,f}[t]
+  EarliestRelease   -Q_k[t] / b_{k,f}[t],  b = Delta R_{k,f}[t] (the payload
+                    RB f can deliver in slot t; -inf where it is 0)
+  DAGRank           omega_k R_{k,f}[t]  (omega: normalised upward rank)
+  TW-MaxRate        q_k R_{k,f}[t]      (q: fixed task weights)
+Every RB of a slot is assigned from the slot-start state Q[t] (the causal
+history of eq. causal_history holds Q[1:t], not the effect of the RBs of
+the same slot), so one agent may receive several RBs of a slot.
 """
 
 import math
@@ -90,10 +105,10 @@ class ScoreArgmax:
         self.score = score
 
     def pick(self, t, f, eligible, R, Q):
-        best, best_v = None, -np.inf
+        best, best_v = None, None
         for k in sorted(eligible):
             v = self.score(k, f, R, Q)
-            if v > best_v:
+            if best is None or v > best_v:
                 best, best_v = k, v
         return best
 
@@ -125,7 +140,15 @@ def emulate(rates, B_bits, slot_s, policy, ell=None):
             for f in range(F):
                 k = policy.pick(t, f, eligible, R[ti], Q)
                 x[k, f] = 1
-        d = slot_s * np.sum(x * R[ti], axis=1)
+        # eq. slot_payload: the rates of the RBs an agent holds, summed in
+        # ascending RB order, times the slot length
+        d = np.zeros(K)
+        for k in range(K):
+            acc = 0.0
+            for f in range(F):
+                if x[k, f]:
+                    acc += R[ti, k, f]
+            d[k] = slot_s * acc
         Qn = np.maximum(0.0, Q - d)
         for k in range(K):
             if Q[k] > 0 and Qn[k] == 0:
@@ -142,13 +165,29 @@ def emulate(rates, B_bits, slot_s, policy, ell=None):
     return dict(a=a, tau=tau, d=d_all, x=x_all, feasible=bool(np.all(np.isfinite(a))))
 
 
-def make_policy(name, K, snr_db=None, bandwidth_hz=None, window=100):
+def _earliest_release(slot_s):
+    def score(k, f, R, Q):
+        b = slot_s * R[k, f]
+        return -Q[k] / b if b > 0.0 else -math.inf
+    return score
+
+
+def make_policy(name, K, snr_db=None, bandwidth_hz=None, window=100, slot_s=None, weights=None):
+    """Policy by name: rr, pf, maxrate, maxweight, earliest_release (needs
+    slot_s), dagrank and tw_maxrate (need the per-agent weights)."""
     if name == "rr":
         return RoundRobin(K)
     if name == "pf":
         return ProportionalFair(K, window, ergodic_rate(snr_db, bandwidth_hz))
     if name == "maxrate":
         return ScoreArgmax(lambda k, f, R, Q: R[k, f])
+    if name == "maxweight":
+        return ScoreArgmax(lambda k, f, R, Q: Q[k] * R[k, f])
+    if name == "earliest_release":
+        return ScoreArgmax(_earliest_release(float(slot_s)))
+    if name in ("dagrank", "tw_maxrate"):
+        w = [float(v) for v in weights]
+        return ScoreArgmax(lambda k, f, R, Q: w[k] * R[k, f])
     raise ValueError(name)
 
 

@@ -14,6 +14,8 @@ from .inputs import (
     make_frame,
     arrival_draws,
     fading_draws,
+    ofdma_draws,
+    points_per_agent,
     seed_children,
 )
 
@@ -28,5 +30,7 @@ __all__ = [
     "make_frame",
     "arrival_draws",
     "fading_draws",
+    "ofdma_draws",
+    "points_per_agent",
     "seed_children",
 ]

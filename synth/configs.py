@@ -42,6 +42,38 @@ _MIXTURE = dict(
     blob_zc=(-1.7, 0.0),
 )
 
+# Slot-level OFDMA uplink of the evaluation (Sec. V-A2, Table of simulation
+# parameters): K = 6 mobile agents in an 80 x 50 m area with the edge server
+# at its centre, F = 8 resource blocks, 1 ms slots, a 900-slot horizon and a
+# 400 ms service deadline.  Reference rate of each agent-RB pair uniform in
+# [250, 4500] kbit/s, scaled by distance attenuation (path-loss exponent
+# 2.15), agent-specific blockage and per-slot, per-RB small-scale fading.
+# Payloads scale by gamma, rates by beta; nominal point (1.0, 0.8).  The
+# values the paper does not give (reference distance, speeds, blockage
+# statistics, fading law) are this workload's own choices.
+_OFDMA = dict(
+    kind="ofdma",
+    n_rb=8,
+    slot_s=1e-3,
+    t_max_slots=900,
+    deadline_s=0.4,
+    area_m=(80.0, 50.0),
+    server_m=(40.0, 25.0),
+    path_loss_exp=2.15,
+    ref_distance_m=30.0,
+    ref_rate_bps=(250e3, 4500e3),
+    speed_mps=(5.0, 15.0),
+    blockage_fraction=0.2,
+    blockage_dwell_slots=200.0,
+    blockage_loss_db=4.0,
+    gammas=(0.5, 1.0, 1.5, 2.0),
+    betas=(0.6, 0.8, 1.0, 1.2, 1.4),
+    nominal=(1.0, 0.8),
+    schedulers=("maxrate", "maxweight", "earliest_release", "dagrank", "tw_maxrate"),
+    task_weights=(1.00, 0.80, 1.20, 0.70, 1.05, 0.60),
+    bytes_per_point=16,
+)
+
 _PP_BACKBONE_64 = ((2, 64, 3), (2, 128, 5), (2, 256, 5))
 _PP_BACKBONE_128 = ((2, 128, 3), (2, 256, 5), (2, 256, 5))
 
@@ -204,7 +236,22 @@ _CONFIGS = {
     ),
 }
 
-CONFIG_NAMES = ("c1", "c2", "c3", "c4", "c5", "t_max", "t_attn")
+# Six-agent measured-DAG instance: the config-3 network (bf16, attention
+# fusion, 352 x 100 grid) with six agents whose branch inputs are 60.6 to
+# 65.2 KiB of float32 points (16 bytes each; Sec. V-A1), sent over the OFDMA
+# uplink above.
+_CONFIGS["s6"] = dict(
+    _CONFIGS["c3"],
+    K=6,
+    points_per_agent=(3878, 3937, 3996, 4055, 4114, 4173),
+    n_points=4173,
+    arrivals=_OFDMA,
+    traces=30,
+    reps=3,
+    seed_index=7,
+)
+
+CONFIG_NAMES = ("c1", "c2", "c3", "c4", "c5", "t_max", "t_attn", "s6")
 
 ROOT_SEED = 20260830
 

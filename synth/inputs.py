@@ -77,15 +77,22 @@ def _mixture_cloud(rng, n, cfg):
     return pts[rng.permutation(n)]
 
 
+def points_per_agent(cfg):
+    """Point count of every agent's cloud (``points_per_agent`` if the
+    workload lists one per agent, else ``n_points`` each)."""
+    n = cfg.get("points_per_agent")
+    return [int(v) for v in n] if n is not None else [int(cfg["n_points"])] * cfg["K"]
+
+
 def make_points(cfg):
-    """List of K float32 arrays [n, 4] = (x, y, z, intensity), agent frame."""
+    """List of K float32 arrays [n_k, 4] = (x, y, z, intensity), agent frame."""
     out = []
-    for k in range(cfg["K"]):
+    for k, n in enumerate(points_per_agent(cfg)):
         rng = _rng(cfg, "points", k)
         if cfg["dist"] == "uniform":
-            pts = _uniform_cloud(rng, cfg["n_points"], cfg)
+            pts = _uniform_cloud(rng, n, cfg)
         elif cfg["dist"] == "mixture":
-            pts = _mixture_cloud(rng, cfg["n_points"], cfg)
+            pts = _mixture_cloud(rng, n, cfg)
         else:
             raise ValueError(cfg["dist"])
         out.append(np.ascontiguousarray(pts.astype(np.float32)))
@@ -169,3 +176,32 @@ def fading_draws(cfg, trace, n_slots=None):
     n_slots = arr["t_max_slots"] if n_slots is None else n_slots
     rng = _rng(cfg, "traces", trace)
     return rng.exponential(1.0, (n_slots, cfg["K"], arr["n_rb"]))
+
+
+def ofdma_draws(cfg, trace):
+    """Random draws of one OFDMA channel trace (T = t_max_slots slots, K
+    agents, F = n_rb RBs), independent of the payload and bandwidth scales
+    and of the scheduler, so that every (gamma, beta, scheduler) cell of a
+    trace sees the same channel realisation:
+
+      ref_rate_bps [K, F]  reference rate of each agent-RB pair, uniform
+                           in ref_rate_bps
+      pos0_m       [K, 2]  start position, uniform over the area
+      heading      [K]     direction of travel, uniform in [-pi, pi)
+      speed_mps    [K]     speed, uniform in speed_mps
+      block_u0     [K]     uniform [0, 1): initial blockage draw
+      block_u      [T, K]  uniform [0, 1): per-slot blockage transition draws
+      fading       [T, K, F] small-scale power gains, Exp(1) i.i.d.
+    """
+    arr = cfg["arrivals"]
+    T, K, F = arr["t_max_slots"], cfg["K"], arr["n_rb"]
+    rng = _rng(cfg, "traces", trace)
+    lo, hi = arr["ref_rate_bps"]
+    out = dict(ref_rate_bps=rng.uniform(lo, hi, (K, F)))
+    out["pos0_m"] = np.stack([rng.uniform(0.0, arr["area_m"][0], K), rng.uniform(0.0, arr["area_m"][1], K)], axis=1)
+    out["heading"] = rng.uniform(-math.pi, math.pi, K)
+    out["speed_mps"] = rng.uniform(arr["speed_mps"][0], arr["speed_mps"][1], K)
+    out["block_u0"] = rng.uniform(0.0, 1.0, K)
+    out["block_u"] = rng.uniform(0.0, 1.0, (T, K))
+    out["fading"] = rng.exponential(1.0, (T, K, F))
+    return out

@@ -11,8 +11,8 @@ def test_generators_are_deterministic_and_shaped():
         a = synth.make_frame(name)
         b = synth.make_frame(name)
         assert len(a["points"]) == cfg["K"]
-        for pa, pb in zip(a["points"], b["points"]):
-            assert pa.dtype == np.float32 and pa.shape == (cfg["n_points"], 4)
+        for pa, pb, n in zip(a["points"], b["points"], synth.points_per_agent(cfg)):
+            assert pa.dtype == np.float32 and pa.shape == (n, 4) and n <= cfg["n_points"]
             assert np.array_equal(pa, pb)
         assert np.array_equal(a["poses"][0], [0.0, 0.0, 0.0])
         for n, arr in a["weights"].items():
@@ -37,3 +37,21 @@ def test_arrival_draws():
     assert 10 < np.median(c5) < 40
     g = synth.fading_draws(synth.config("c4"), 0, n_slots=100)
     assert g.shape == (100, 5, 1)
+
+
+def test_ofdma_draws_are_deterministic_and_independent_per_trace():
+    cfg = synth.config("s6")
+    arr = cfg["arrivals"]
+    a, b, c = synth.ofdma_draws(cfg, 0), synth.ofdma_draws(cfg, 0), synth.ofdma_draws(cfg, 1)
+    T, K, F = arr["t_max_slots"], cfg["K"], arr["n_rb"]
+    assert a["fading"].shape == (T, K, F) and a["ref_rate_bps"].shape == (K, F)
+    assert a["block_u"].shape == (T, K) and a["pos0_m"].shape == (K, 2)
+    for key in a:
+        assert np.array_equal(a[key], b[key])
+        assert not np.array_equal(a[key], c[key])
+    assert np.all((a["pos0_m"] >= 0) & (a["pos0_m"] <= np.array(arr["area_m"])))
+    lo, hi = arr["speed_mps"]
+    assert np.all((a["speed_mps"] >= lo) & (a["speed_mps"] < hi))
+    # branch inputs of 60.6 to 65.2 KiB of 16-byte points
+    kib = np.array(synth.points_per_agent(cfg)) * arr["bytes_per_point"] / 1024
+    assert abs(kib.min() - 60.6) < 0.01 and abs(kib.max() - 65.2) < 0.01
