@@ -253,8 +253,8 @@ RTCC_API rtcc_status rtcc_get_tensor(rtcc_ctx *ctx, int32_t id, int32_t agent, v
  * work node by node on one stream, `warmup` untimed passes then `reps`
  * timed passes, and write the median of each node in ms.  Nodes: E_0 ..
  * E_{K-1} (encoder without the H2D copy), then the post-join subgraph
- * (warp + fusion + head + decode).  *n_nodes is K + 1; median_ms must hold
- * RTCC_MAX_AGENTS + 1 floats. */
+ * (warp + fusion + head + decode + rotated NMS when it is on).  *n_nodes
+ * is K + 1; median_ms must hold RTCC_MAX_AGENTS + 1 floats. */
 RTCC_API rtcc_status rtcc_profile_nodes(rtcc_ctx *ctx, int32_t warmup, int32_t reps, float *median_ms,
                                int32_t *n_nodes);
 
@@ -286,11 +286,100 @@ RTCC_API rtcc_status rtcc_node_count(rtcc_ctx *ctx, int32_t *n);
 RTCC_API rtcc_status rtcc_rotated_nms(const float *device_records, int64_t n, int32_t max_candidates,
                                       float iou_threshold, float *device_out, int64_t *kept);
 
+/* ------------------------------------------------------------------------
+ * Host-side models of the communication and of the profiled DAG.  They run
+ * on the host only (no GPU work, no context), are deterministic, and report
+ * failures through rtcc_last_error(NULL).
+ * ------------------------------------------------------------------------ */
+
+/* Causal RB-allocation policies (Sec. III-A eq. pluggable_scheduler; Sec.
+ * V-A2 eqs. evaluation_schedulers, evaluation_scores).  In slot t each RB
+ * f goes to the eligible agent with the largest score, ties to the smallest
+ * agent index:
+ *   MAXRATE           s = R_{k,f}[t]
+ *   MAXWEIGHT         s = Q_k[t] R_{k,f}[t]
+ *   EARLIEST_RELEASE  s = -Q_k[t] / (Delta R_{k,f}[t]), -inf where R = 0
+ *   WEIGHTED_RATE     s = w_k R_{k,f}[t]: DAGRank with w = the normalised
+ *                     upward rank omega, Task-Weighted MaxRate with w = q
+ *   ROUND_ROBIN       the first eligible agent after the last one served,
+ *                     cycling in index order (the first RB of slot 1 from
+ *                     agent 0)
+ *   PROPORTIONAL_FAIR s = R_{k,f}[t] / Rbar_k, Rbar_k <- (1 - 1/W) Rbar_k +
+ *                     (1/W) (rate served to k in the slot) after every slot
+ * Q_k[t] is the slot-start backlog for every RB of the slot. */
+typedef enum rtcc_sched {
+    RTCC_SCHED_MAXRATE = 0,
+    RTCC_SCHED_MAXWEIGHT = 1,
+    RTCC_SCHED_EARLIEST_RELEASE = 2,
+    RTCC_SCHED_WEIGHTED_RATE = 3,
+    RTCC_SCHED_ROUND_ROBIN = 4,
+    RTCC_SCHED_PROPORTIONAL_FAIR = 5
+} rtcc_sched;
+
+typedef struct rtcc_uplink_desc {
+    int32_t slots;              /* T: slots emulated (the horizon T_max), >= 1          */
+    int32_t agents;             /* K, >= 1                                               */
+    int32_t rbs;                /* F, >= 1                                               */
+    int32_t policy;             /* rtcc_sched                                            */
+    double slot_s;              /* Delta, seconds, > 0                                   */
+    const double *agent_weight; /* [K] w_k for WEIGHTED_RATE (finite); else unused       */
+    double pf_window;           /* PROPORTIONAL_FAIR: W in slots, >= 1                   */
+    double pf_init_rate;        /* PROPORTIONAL_FAIR: Rbar_k before slot 1, bit/s, > 0   */
+} rtcc_uplink_desc;
+
+/* Slot-level uplink emulation (Sec. III-A eqs. rb_orthogonality,
+ * local_ready_constraint, slot_payload, queue_evolution, branch_arrival;
+ * Sec. IV-B eq. eligible_set, completion_event).  Q_k[1] = B_k; in slot t
+ * the agents with Q_k[t] > 0 and t >= l_k are eligible and every RB goes to
+ * one of them by the policy; d_k[t] = Delta * (sum of the rates of the RBs
+ * k holds, in ascending RB order); Q_k[t+1] = max(0, Q_k[t] - d_k[t]).
+ *   rates:           host [T][K][F] bit/s, finite and >= 0
+ *   payload_bits:    host [K] B_k, finite and > 0
+ *   avail_slot:      host [K] l_k >= 1, or NULL for l_k = 1
+ *   completion_slot: host [K] out: the slot in which Q_k reaches zero
+ *                    (a_k = slot * Delta), 0 if still undelivered after T
+ *                    slots (a_k = +inf: the frame is infeasible)
+ *   rb_agent:        host [T][F] out or NULL: agent given each RB, -1 idle
+ * Returns RTCC_E_ARG for invalid arguments (nothing written). */
+RTCC_API rtcc_status rtcc_uplink_emulate(const rtcc_uplink_desc *desc, const double *rates,
+                                         const double *payload_bits, const int32_t *avail_slot,
+                                         int32_t *completion_slot, int32_t *rb_agent);
+
+/* Single-stream latency of the profiled DAG for one arrival vector (Sec.
+ * III-B eq. encoder_release, dag_precedence; Sec. III-C eq. full_latency;
+ * Sec. IV-C eqs. rtcc_encoder_start, rtcc_encoder_finish,
+ * rtcc_gpu_availability): encoders run one at a time in (r_k, k) order,
+ * each from max(r_k, stream free) for encoder_ns[k]; the post-join subgraph
+ * then takes post_ns.  mode RELEASE: r_k = a_k; BARRIER: r_k = A = max a_k.
+ * Integer nanoseconds, so every result is exact.
+ *   arrival_ns, encoder_ns: host [agents], in [0, 2^60); post_ns likewise
+ *   latency_ns:     out: finish of the post-join subgraph (T)
+ *   pre_arrival_ns: out or NULL: encoder time spent before A, the sum over
+ *                   k of |[s_k, f_k) intersected with [0, A)| (W_pre under
+ *                   RELEASE; 0 under BARRIER)
+ *   start_ns:       out [agents] or NULL: encoder start times s_k
+ * Returns RTCC_E_ARG for invalid arguments. */
+RTCC_API rtcc_status rtcc_schedule_model(int32_t agents, const int64_t *arrival_ns, const int64_t *encoder_ns,
+                                         int64_t post_ns, int32_t mode, int64_t *latency_ns,
+                                         int64_t *pre_arrival_ns, int64_t *start_ns);
+
+/* Upward rank of every node of a DAG (the DAGRank priority of Sec. V-A2):
+ * rank(v) = cost(v) + max over successors w of rank(w), 0 without
+ * successors, i.e. the longest path from v to an exit node, v included.
+ *   cost_ns:   host [nodes], in [0, 2^60), summing to less than 2^60
+ *   edge_list: host [edges][2] (u, v): v depends on u; NULL if edges == 0
+ *   rank_ns:   host [nodes] out
+ * Returns RTCC_E_ARG for invalid arguments, an endpoint out of range, a
+ * self loop or a cycle. */
+RTCC_API rtcc_status rtcc_upward_rank(int32_t nodes, const int64_t *cost_ns, int32_t edges,
+                                      const int32_t *edge_list, int64_t *rank_ns);
+
 /* Name of a status code. */
 RTCC_API const char *rtcc_status_str(rtcc_status s);
 
 /* Message of the last failed call on ctx; with ctx == NULL, the message of
- * the last failed context-free call (rtcc_create, rtcc_rotated_nms) on the
+ * the last failed context-free call (rtcc_create, rtcc_rotated_nms,
+ * rtcc_uplink_emulate, rtcc_schedule_model, rtcc_upward_rank) on the
  * calling thread. */
 RTCC_API const char *rtcc_last_error(const rtcc_ctx *ctx);
 

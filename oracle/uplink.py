@@ -93,8 +93,13 @@ class ProportionalFair:
         return best
 
     def end_slot(self, x, R):
-        served = np.sum(x * R, axis=1)
-        self.avg = (1.0 - 1.0 / self.W) * self.avg + served / self.W
+        K, F = x.shape
+        for k in range(K):
+            served = 0.0
+            for f in range(F):
+                if x[k, f]:
+                    served += R[k, f]
+            self.avg[k] = (1.0 - 1.0 / self.W) * self.avg[k] + served / self.W
 
 
 class ScoreArgmax:

@@ -25,7 +25,7 @@ ARCH = "gfx950"
 HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
 CXX = shutil.which("g++") or "g++"
 
-HOST_SOURCES = ["api.cpp", "controller.cpp", "model.cpp"]
+HOST_SOURCES = ["api.cpp", "controller.cpp", "model.cpp", "uplink.cpp"]
 HIP_SOURCES = [
     "executor_hip.hip",
     "kernels/pillar.hip",
@@ -41,7 +41,10 @@ HIP_FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-result", "-fvisibility=hidden", "-I" + INCLUDE,
 ]
-HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-Wextra", "-fvisibility=hidden", "-I" + INCLUDE]
+# Host code never contracts a * b + c into an FMA, so its floating point
+# follows the written order of operations.
+HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-Wextra", "-ffp-contract=off", "-fvisibility=hidden",
+              "-I" + INCLUDE]
 
 
 def _run(cmd):

@@ -26,9 +26,12 @@ def stage_inputs(ctx, points):
     return views
 
 
-def replay_frame(ctx, staged, poses, a, mode):
+def replay_frame(ctx, staged, poses, a, mode, resident=False):
     """Run one frame; returns dict with T^head, T^det (s since the uplink
-    start), dispatch lateness per agent and the detections count."""
+    start), dispatch lateness per agent and the detections count.
+    ``staged`` holds the pinned staging views, or with ``resident`` the
+    (device pointer, point count) of every agent's device-resident input
+    (the resident-input runs of Sec. V-C)."""
     a = np.asarray(a, dtype=np.float64)
     shift = float(a.min())
     rel = a - shift
@@ -40,7 +43,10 @@ def replay_frame(ctx, staged, poses, a, mode):
         target = t0 + rel[k]
         while time.monotonic() < target:
             pass
-        R.rtcc_release_branch(ctx, k, staged[k], poses[k], float(rel[k]))
+        if resident:
+            R.rtcc_release_branch_device(ctx, k, staged[k][0], staged[k][1], poses[k], float(rel[k]))
+        else:
+            R.rtcc_release_branch(ctx, k, staged[k], poses[k], float(rel[k]))
     det = R.rtcc_join_and_detect(ctx)
     lateness = [det["dispatch_s"][k] - rel[k] for k in range(len(a))]
     return dict(t_head=det["t_head_s"] + shift, t_det=det["t_det_s"] + shift,
@@ -59,7 +65,7 @@ def bootstrap_ci(x, n=10000, seed=0, alpha=0.05):
     return float(np.quantile(means, alpha / 2)), float(np.quantile(means, 1 - alpha / 2))
 
 
-def replay_traces(ctx, staged, poses, arrivals_s, reps, start=0):
+def replay_traces(ctx, staged, poses, arrivals_s, reps, start=0, resident=False):
     """Paired RTCC / barrier replay of every trace, alternating which mode
     runs first per repetition; repetitions are averaged per trace.
     ``staged`` are the pinned staging views from :func:`stage_inputs`;
@@ -74,7 +80,7 @@ def replay_traces(ctx, staged, poses, arrivals_s, reps, start=0):
             if (t + r) % 2:
                 modes = modes[::-1]
             for key, mode in modes:
-                res = replay_frame(ctx, staged, poses, a, mode)
+                res = replay_frame(ctx, staged, poses, a, mode, resident)
                 tr[key].append(res)
                 ids.setdefault(key, res["anchor_idx"])
                 identical &= np.array_equal(ids[key], res["anchor_idx"])

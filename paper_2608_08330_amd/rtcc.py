@@ -38,6 +38,8 @@ RTCC_EXEC_PER_BRANCH_STREAMS, RTCC_EXEC_SERIAL = 0, 1
 RTCC_WAITING, RTCC_RELEASED, RTCC_RUNNING, RTCC_FINISHED = 0, 1, 2, 3
 (RTCC_T_PILLAR_CELLS, RTCC_T_PILLAR_COUNTS, RTCC_T_CANVAS, RTCC_T_SLOT, RTCC_T_FUSED,
  RTCC_T_HEAD, RTCC_T_STAGE_OUT, RTCC_T_DECODED) = range(8)
+(RTCC_SCHED_MAXRATE, RTCC_SCHED_MAXWEIGHT, RTCC_SCHED_EARLIEST_RELEASE, RTCC_SCHED_WEIGHTED_RATE,
+ RTCC_SCHED_ROUND_ROBIN, RTCC_SCHED_PROPORTIONAL_FAIR) = range(6)
 
 
 class rtcc_stage(ctypes.Structure):
@@ -80,6 +82,19 @@ class rtcc_runtime_opts(ctypes.Structure):
     ]
 
 
+class rtcc_uplink_desc(ctypes.Structure):
+    _fields_ = [
+        ("slots", ctypes.c_int32),
+        ("agents", ctypes.c_int32),
+        ("rbs", ctypes.c_int32),
+        ("policy", ctypes.c_int32),
+        ("slot_s", ctypes.c_double),
+        ("agent_weight", ctypes.POINTER(ctypes.c_double)),
+        ("pf_window", ctypes.c_double),
+        ("pf_init_rate", ctypes.c_double),
+    ]
+
+
 class rtcc_detections(ctypes.Structure):
     _fields_ = [
         ("count", ctypes.c_int64),
@@ -99,7 +114,8 @@ EXPORTS = (
     "rtcc_create", "rtcc_destroy", "rtcc_set_mode", "rtcc_staging_buffer", "rtcc_begin_frame",
     "rtcc_release_branch", "rtcc_release_branch_device", "rtcc_join_and_detect",
     "rtcc_get_branch_state", "rtcc_tensor_bytes", "rtcc_get_tensor", "rtcc_profile_nodes",
-    "rtcc_node_times", "rtcc_node_count", "rtcc_rotated_nms", "rtcc_status_str", "rtcc_last_error",
+    "rtcc_node_times", "rtcc_node_count", "rtcc_rotated_nms", "rtcc_uplink_emulate", "rtcc_schedule_model",
+    "rtcc_upward_rank", "rtcc_status_str", "rtcc_last_error",
 )
 
 
@@ -111,6 +127,7 @@ class RtccError(RuntimeError):
 
 _P = ctypes.c_void_p
 _F = ctypes.POINTER(ctypes.c_float)
+_I64P = ctypes.POINTER(ctypes.c_int64)
 
 
 def _declare(lib):
@@ -133,6 +150,9 @@ def _declare(lib):
         "rtcc_node_count": (S, [_P, ctypes.POINTER(ctypes.c_int32)]),
         "rtcc_rotated_nms": (S, [_P, ctypes.c_int64, ctypes.c_int32, ctypes.c_float, _P,
                                  ctypes.POINTER(ctypes.c_int64)]),
+        "rtcc_uplink_emulate": (S, [ctypes.POINTER(rtcc_uplink_desc), _P, _P, _P, _P, _P]),
+        "rtcc_schedule_model": (S, [ctypes.c_int32, _P, _P, ctypes.c_int64, ctypes.c_int32, _I64P, _I64P, _P]),
+        "rtcc_upward_rank": (S, [ctypes.c_int32, _P, ctypes.c_int32, _P, _P]),
         "rtcc_status_str": (ctypes.c_char_p, [ctypes.c_int]),
         "rtcc_last_error": (ctypes.c_char_p, [_P]),
     }
@@ -345,6 +365,70 @@ def rtcc_rotated_nms(device_records, n, max_candidates, iou_threshold, device_ou
     if st != 0:
         raise RtccError(st, (lib.rtcc_last_error(None) or b"").decode())
     return kept.value
+
+
+def _free_call(lib, st):
+    if st != 0:
+        raise RtccError(st, (lib.rtcc_last_error(None) or b"").decode())
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(_P)
+
+
+def rtcc_uplink_emulate(rates, payload_bits, policy, slot_s, agent_weight=None, avail_slot=None,
+                        pf_window=100.0, pf_init_rate=1.0, want_alloc=False, kind="gpu"):
+    """Slot-level uplink emulation.  rates [T, K, F] bit/s, payload_bits [K].
+    Returns the completion slot per agent (int32, 0 = undelivered) and, with
+    want_alloc, the [T, F] agent given each RB (-1 idle)."""
+    lib = load(kind)
+    R = np.ascontiguousarray(rates, dtype=np.float64)
+    if R.ndim != 3:
+        raise ValueError("rates must be [T, K, F]")
+    T, K, F = R.shape
+    B = np.ascontiguousarray(payload_bits, dtype=np.float64)
+    if B.shape != (K,):
+        raise ValueError("payload_bits must be [K]")
+    d = rtcc_uplink_desc(T, K, F, int(policy), float(slot_s), None, float(pf_window), float(pf_init_rate))
+    w = None
+    if agent_weight is not None:
+        w = np.ascontiguousarray(agent_weight, dtype=np.float64)
+        if w.shape != (K,):
+            raise ValueError("agent_weight must be [K]")
+        d.agent_weight = w.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+    ell = None if avail_slot is None else np.ascontiguousarray(avail_slot, dtype=np.int32)
+    if ell is not None and ell.shape != (K,):
+        raise ValueError("avail_slot must be [K]")
+    done = np.zeros(K, dtype=np.int32)
+    alloc = np.empty((T, F), dtype=np.int32) if want_alloc else None
+    _free_call(lib, lib.rtcc_uplink_emulate(ctypes.byref(d), _ptr(R), _ptr(B), _ptr(ell), _ptr(done), _ptr(alloc)))
+    return (done, alloc) if want_alloc else done
+
+
+def rtcc_schedule_model(arrival_ns, encoder_ns, post_ns, mode, kind="gpu"):
+    """Single-stream latency of one arrival vector (integer ns).  Returns
+    (latency_ns, pre_arrival_ns, start_ns[K])."""
+    lib = load(kind)
+    a = np.ascontiguousarray(arrival_ns, dtype=np.int64)
+    c = np.ascontiguousarray(encoder_ns, dtype=np.int64)
+    if a.ndim != 1 or c.shape != a.shape:
+        raise ValueError("arrival_ns and encoder_ns must be [K]")
+    lat, pre = ctypes.c_int64(), ctypes.c_int64()
+    start = np.zeros(len(a), dtype=np.int64)
+    _free_call(lib, lib.rtcc_schedule_model(len(a), _ptr(a), _ptr(c), int(post_ns), int(mode), ctypes.byref(lat),
+                                            ctypes.byref(pre), _ptr(start)))
+    return lat.value, pre.value, start
+
+
+def rtcc_upward_rank(cost_ns, edges, kind="gpu"):
+    """Upward rank (ns) of every node; edges is a sequence of (u, v) pairs,
+    v depending on u."""
+    lib = load(kind)
+    c = np.ascontiguousarray(cost_ns, dtype=np.int64)
+    e = np.ascontiguousarray(np.asarray(edges, dtype=np.int32).reshape(-1, 2))
+    out = np.zeros(len(c), dtype=np.int64)
+    _free_call(lib, lib.rtcc_upward_rank(len(c), _ptr(c), len(e), _ptr(e) if len(e) else None, _ptr(out)))
+    return out
 
 
 def rtcc_get_branch_state(ctx, agent):

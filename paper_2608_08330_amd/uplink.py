@@ -10,15 +10,19 @@ which the backlog reaches zero is the completion slot, and a_k = slot *
 slot duration (eqs. branch_arrival, completion_event).  Undelivered at the
 horizon -> infeasible frame.
 
-Policies: round robin over the eligible agents (next after the last served)
-and proportional fair (argmax of instantaneous rate over an exponentially
-weighted average rate with window W, ties to the smallest index, average
-initialised at the ergodic rate of the Rayleigh channel).
+The slot loop itself runs in the library (rtcc_uplink_emulate): round
+robin, proportional fair (average initialised at the ergodic rate of the
+Rayleigh channel), and the five causal evaluation schedulers (MaxRate,
+MaxWeight, EarliestRelease, DAGRank, Task-Weighted MaxRate; eqs.
+evaluation_schedulers, evaluation_scores).  This module computes the rates
+and the ergodic-rate closed form.
 """
 
 import math
 
 import numpy as np
+
+from . import rtcc as R
 
 
 def _expint_e1(x):
@@ -59,41 +63,30 @@ def mean_rate(snr_db, bandwidth_hz):
     return bandwidth_hz * math.log2(math.e) * math.exp(1.0 / snr) * _expint_e1(1.0 / snr)
 
 
-def completion_times(gains, payload_bits, snr_db, bandwidth_hz, slot_s, scheduler, pf_window=100):
+SCHEDULERS = {
+    "rr": R.RTCC_SCHED_ROUND_ROBIN,
+    "pf": R.RTCC_SCHED_PROPORTIONAL_FAIR,
+    "maxrate": R.RTCC_SCHED_MAXRATE,
+    "maxweight": R.RTCC_SCHED_MAXWEIGHT,
+    "earliest_release": R.RTCC_SCHED_EARLIEST_RELEASE,
+    "dagrank": R.RTCC_SCHED_WEIGHTED_RATE,
+    "tw_maxrate": R.RTCC_SCHED_WEIGHTED_RATE,
+}
+
+
+def completion_slots(rates, payload_bits, slot_s, scheduler, agent_weight=None, pf_window=100.0,
+                     pf_init_rate=1.0, kind="gpu"):
+    """Completion slot per agent (0 = undelivered) of the native slot-level
+    emulation (rtcc_uplink_emulate) for a [slots, K, RBs] rate array."""
+    return R.rtcc_uplink_emulate(rates, payload_bits, SCHEDULERS[scheduler], slot_s, agent_weight=agent_weight,
+                                 pf_window=pf_window, pf_init_rate=pf_init_rate, kind=kind)
+
+
+def completion_times(gains, payload_bits, snr_db, bandwidth_hz, slot_s, scheduler, pf_window=100, kind="gpu"):
     """Arrival time per agent (s), inf if undelivered within the slots of
-    ``gains`` ([slots, K, RBs] power gains)."""
+    ``gains`` ([slots, K, RBs] power gains), for the Shannon-rate channel."""
     g = np.asarray(gains, dtype=np.float64)
-    T, K, F = g.shape
     rate = bandwidth_hz * np.log2(1.0 + (10.0 ** (snr_db / 10.0)) * g)
-    backlog = np.asarray(payload_bits, dtype=np.float64).copy()
-    arrival = np.full(K, np.inf)
-    last = -1
-    avg = np.full(K, mean_rate(snr_db, bandwidth_hz))
-    for t in range(T):
-        active = backlog > 0
-        if not active.any():
-            break
-        served_rate = np.zeros(K)
-        for f in range(F):
-            if scheduler == "rr":
-                k = -1
-                for step in range(1, K + 1):
-                    c = (last + step) % K
-                    if active[c]:
-                        k = c
-                        break
-                last = k
-            elif scheduler == "pf":
-                score = np.where(active, rate[t, :, f] / avg, -np.inf)
-                k = int(np.argmax(score))
-            else:
-                raise ValueError(scheduler)
-            served_rate[k] += rate[t, k, f]
-        sent = served_rate * slot_s
-        new = np.maximum(0.0, backlog - sent)
-        done = active & (new == 0.0)
-        arrival[done] = (t + 1) * slot_s
-        backlog = new
-        if scheduler == "pf":
-            avg = (1.0 - 1.0 / pf_window) * avg + served_rate / pf_window
-    return arrival
+    slots = completion_slots(rate, payload_bits, slot_s, scheduler, pf_window=float(pf_window),
+                             pf_init_rate=mean_rate(snr_db, bandwidth_hz), kind=kind)
+    return np.where(slots > 0, slots * slot_s, np.inf)

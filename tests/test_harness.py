@@ -1,6 +1,7 @@
 """Host-side harness logic against the oracle: the product's uplink
-emulation and DAG gain model reproduce the oracle's, and the ergodic-rate
-closed form agrees with scipy."""
+emulation (the library's rtcc_uplink_emulate, through the host-test build of
+the same source) and DAG gain model reproduce the oracle's, and the
+ergodic-rate closed form agrees with scipy."""
 
 import math
 
@@ -26,7 +27,7 @@ def test_uplink_completion_times_match_oracle(sched):
         g = synth.fading_draws(cfg, t, n_slots=8000)
         B = rng.uniform(1e6, 2.5e7, 5)
         for snr in (0.0, 10.0, 20.0):
-            a = uplink.completion_times(g, B, snr, 20e6, 1e-3, sched, 100)
+            a = uplink.completion_times(g, B, snr, 20e6, 1e-3, sched, 100, kind="host")
             ref = U.trace_arrivals(cfg, g, B / 8.0, snr, sched)["a"]
             assert np.array_equal(np.isfinite(a), np.isfinite(ref))
             fin = np.isfinite(a)
