@@ -422,12 +422,21 @@ def forward(frame, keep=False, agents=None):
     same for every arrival and release vector, which is the output
     invariance RTCC preserves (Sec. IV-D: fixed agent-indexed feature
     storage, post-join subgraph in topological order).
+
+    With ``cfg['warp_in_branch']`` the pose warp moves out of the shared
+    subgraph into each branch (a dependency-preserving move: the warp of
+    agent k needs only E_k's slot and k's pose), which then stores its
+    ego-frame map; the join fuses the K stored maps.
     """
     cfg = frame["cfg"]
     pw = prepared_weights(cfg, frame["weights"])
     K = cfg["K"]
     enc = [encoder(frame["points"][k], cfg, pw, keep=keep) for k in range(K)]
     warped = [warp(enc[k]["slot"], frame["poses"][k], cfg) for k in range(K)]
+    if cfg.get("warp_in_branch"):
+        # the warp is the last node of each branch, which stores its
+        # ego-frame map: a storage point (rounded for bf16 workloads)
+        warped = [_store(cfg, w) for w in warped]
     if cfg["fusion"] == "max":
         fused = fuse_max(warped)
     elif cfg["fusion"] == "attn":

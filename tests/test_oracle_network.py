@@ -9,6 +9,7 @@ import pytest
 
 import synth
 from oracle import network as N
+from oracle.bf16 import round_bf16
 
 
 # ---------------------------------------------------------------- PFN
@@ -265,3 +266,48 @@ def test_forward_output_does_not_depend_on_agent_slot_order():
     warped = [N.warp(rev[k], fr["poses"][k], cfg) for k in range(cfg["K"])]
     fused = N._store(cfg, N.fuse_attn(warped))
     assert np.array_equal(fused, out["fused"])
+
+
+def _prewarp(cfg, on=True):
+    c = dict(cfg)
+    c["warp_in_branch"] = on
+    return c
+
+
+@pytest.mark.parametrize("name", ["t_max", "c1"])
+def test_prewarp_max_fusion_equals_post_join_warp(name):
+    """Rounding to bfloat16 is monotone, so the maximum of the rounded
+    ego-frame maps is the rounded maximum: with max fusion, storing each
+    branch's warped map changes nothing (c1 is float32: no rounding)."""
+    fr = synth.make_frame(name)
+    base = N.forward(fr)
+    fr2 = dict(fr, cfg=_prewarp(fr["cfg"]))
+    pre = N.forward(fr2, keep=True)
+    assert np.array_equal(pre["fused"], base["fused"])
+    assert np.array_equal(pre["head"], base["head"])
+    if fr["cfg"]["precision"] == "bf16":
+        for w in pre["warped"]:
+            assert np.array_equal(w, round_bf16(w))
+
+
+def test_prewarp_attention_identity_poses_and_single_agent():
+    cfg = synth.config("t_attn")
+    fr = synth.make_frame(cfg)
+    # identity poses: every warp is the identity on bf16 slots, so the stored
+    # maps equal the slots and both placements fuse the same values
+    ident = dict(fr, poses=np.zeros_like(fr["poses"]))
+    a = N.forward(ident)
+    b = N.forward(dict(ident, cfg=_prewarp(cfg)))
+    assert np.array_equal(a["fused"], b["fused"])
+    # one agent: attention returns its (stored) warped map
+    one = dict(cfg, K=1, warp_in_branch=True)
+    fr1 = dict(fr, cfg=one, points=fr["points"][:1], poses=fr["poses"][:1])
+    out = N.forward(fr1, keep=True)
+    assert np.array_equal(out["fused"], N._store(one, out["warped"][0]))
+    # random poses: the two placements differ only by the rounding of the
+    # warped maps (relative 2^-8 per element before fusion)
+    c = N.forward(fr)
+    d = N.forward(dict(fr, cfg=_prewarp(cfg)))
+    scale = np.abs(c["fused"]).max()
+    assert np.abs(c["fused"] - d["fused"]).max() <= 2 ** -7 * scale
+    assert not np.array_equal(c["fused"], d["fused"])
