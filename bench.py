@@ -3,7 +3,8 @@
 
 One step = one complete frame through the C ABI: K branch encoders
 (pillarize, point-feature net, 3x3 conv backbone, upsample) released on
-device-resident inputs, then the join (warp, fusion, head, decode, D2H).
+device-resident inputs, then the join (warp, fusion, head, decode, NMS,
+D2H).  --warp-in-branch moves the pose warp into the branches.
 
 Output: one JSON line with
   value       encoder throughput, TFLOP/s = algorithmic encoder FLOPs of the
@@ -163,6 +164,8 @@ def main(argv=None):
     ap.add_argument("--latency-reps", type=int, default=3)
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--warp-in-branch", action="store_true",
+                    help="place the pose warp as the last node of every branch (the join only fuses)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB, 5 times "
                          "(reference for the FETCH_SIZE / WRITE_SIZE counters)")
@@ -194,6 +197,7 @@ def main(argv=None):
         return 0
 
     cfg = synth.config(a.config)
+    cfg["warp_in_branch"] = bool(a.warp_in_branch)
     frame = synth.make_frame(cfg)
     lw = layer_work(cfg)
     K = cfg["K"]
@@ -227,9 +231,10 @@ def main(argv=None):
     enc_flops = sum(encoder_flops(cfg, lw, u) for u in used)
     value = enc_flops * a.steps / wall / 1e12
 
-    # node layout per agent: h2d, pillar, pfn, conv[L], up[S or 1]; post: warp_fuse, head, decode
+    # node layout per agent: h2d, pillar, pfn, conv[L], up[S or 1], warp (0 unless in the branch);
+    # post: warp_fuse (or fuse), head, decode, nms
     L, S = len(lw["convs"]), max(len(lw["ups"]), 1)
-    per_agent = 3 + L + S
+    per_agent = 3 + L + S + 1
     node = np.array(node)  # [steps, nodes] ms
     conv_ms = 0.0
     for k in range(K):
@@ -246,7 +251,11 @@ def main(argv=None):
     post0 = K * per_agent
     warp_ms = node[:, post0].sum()
     slot_bytes = lw["H2"] * lw["W2"] * lw["C"] * lw["elt"]
+    # warp + fusion, or fusion of the stored maps: K maps read, one written
     warp_bytes = (K + 1) * slot_bytes * rsteps
+    # branch warps (agents with a non-identity pose): one slot read, one map written
+    bw_ms = sum(node[:, k * per_agent + per_agent - 1].sum() for k in range(K))
+    bw_launches = sum(1 for k in range(K) if node[:, k * per_agent + per_agent - 1].sum() > 0) * rsteps
 
     layers = []
     for l, c in enumerate(lw["convs"]):
@@ -267,8 +276,9 @@ def main(argv=None):
         "dtype": "bf16" if cfg["precision"] == "bf16" else "f32",
         "data": "synthetic (seeded points, poses, He-normal weights, arrival traces)",
         "config": {
-            "workload": "%s: %d agents x %d points, %dx%d BEV, %s, %s fusion" % (
-                cfg["name"], K, cfg["n_points"], lw["H"], lw["W"], cfg["precision"], cfg["fusion"]),
+            "workload": "%s: %d agents x %d points, %dx%d BEV, %s, %s fusion%s" % (
+                cfg["name"], K, cfg["n_points"], lw["H"], lw["W"], cfg["precision"], cfg["fusion"],
+                ", warp in the branches" if cfg["warp_in_branch"] else ""),
             "agents": K, "inputs": "device-resident",
             "executor": "per-branch streams" if a.exec == "streams" else "serial",
         },
@@ -282,8 +292,10 @@ def main(argv=None):
         "secondary_rooflines": {
             "pillar_pfn_canvas": {"bound": "hbm", "achieved": round(pil_bytes / (pillar_ms * 1e-3) / 1e9, 1),
                                   "peak": PEAK_HBM_GBS, "unit": "GB/s"},
-            "warp_fuse": {"bound": "hbm", "achieved": round(warp_bytes / (warp_ms * 1e-3) / 1e9, 1),
-                          "peak": PEAK_HBM_GBS, "unit": "GB/s", "traffic": measured_traffic("warp_fuse")},
+            ("fuse" if cfg["warp_in_branch"] else "warp_fuse"): {
+                "bound": "hbm", "achieved": round(warp_bytes / (warp_ms * 1e-3) / 1e9, 1),
+                "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "traffic": None if cfg["warp_in_branch"] else measured_traffic("warp_fuse")},
         },
         "conv_layers": layers,
         "node_ms_mean": {
@@ -292,12 +304,17 @@ def main(argv=None):
             "conv_total_per_agent": round(conv_ms / (K * rsteps), 4),
             "up_total_per_agent": round(float(np.sum([node[:, k * per_agent + 3 + L:k * per_agent + per_agent]
                                                       for k in range(K)]) / (K * rsteps)), 4),
-            "warp_fuse": round(float(node[:, post0].mean()), 4),
+            "branch_warp_per_agent": round(bw_ms / (K * rsteps), 4),
+            ("fuse" if cfg["warp_in_branch"] else "warp_fuse"): round(float(node[:, post0].mean()), 4),
             "head": round(float(node[:, post0 + 1].mean()), 4),
             "decode": round(float(node[:, post0 + 2].mean()), 4),
             "nms": round(float(node[:, post0 + 3].mean()), 4),
         },
     }
+    if cfg["warp_in_branch"] and bw_launches:
+        out["secondary_rooflines"]["branch_warp"] = {
+            "bound": "hbm", "achieved": round(2 * slot_bytes * bw_launches / (bw_ms * 1e-3) / 1e9, 1),
+            "peak": PEAK_HBM_GBS, "unit": "GB/s"}
     print("# throughput done: %.3f ms/step, %.1f TFLOP/s" % (ms_per_step, value), file=sys.stderr, flush=True)
 
     if a.latency_traces > 0:

@@ -58,7 +58,7 @@ extern "C" {
 #define RTCC_API
 #endif
 
-#define RTCC_ABI_VERSION 2
+#define RTCC_ABI_VERSION 3
 #define RTCC_MAX_AGENTS 16
 #define RTCC_MAX_STAGES 4
 
@@ -132,6 +132,15 @@ typedef struct rtcc_model_desc {
      * a box with a non-finite footprint or w, l <= 0 overlaps nothing. */
     int32_t nms_max_candidates;
     float nms_iou_threshold;
+    /* Placement of the pose warp.  0: in the post-join subgraph, fused with
+     * the cross-agent fusion.  1: as the last node of every branch, which
+     * resamples its slot on the ego grid and stores the ego-frame map in the
+     * activation dtype (RTCC_T_WARPED); the join then only fuses the K maps.
+     * The warp of agent k needs only E_k's slot and k's pose, so both
+     * placements keep the DAG's dependencies (Sec. III-B); with max fusion
+     * they give identical outputs, with attention they differ by the rounding
+     * of the stored maps (bf16). */
+    int32_t warp_in_branch;
 } rtcc_model_desc;
 
 typedef struct rtcc_runtime_opts {
@@ -164,8 +173,10 @@ typedef enum rtcc_tensor_id {
     RTCC_T_HEAD = 5,          /* float32 [H2, W2, 16]                                       */
     RTCC_T_STAGE_OUT = 6,     /* [Hs, Ws, Cs] stored dtype, last conv of stage `agent>>8`,
                                  agent `agent & 255`                                        */
-    RTCC_T_DECODED = 7        /* float32 [count_decoded][9] before NMS: x, y, z, w, l, h,
+    RTCC_T_DECODED = 7,       /* float32 [count_decoded][9] before NMS: x, y, z, w, l, h,
                                  yaw, score, anchor index (int32 bits); ascending anchor    */
+    RTCC_T_WARPED = 8         /* [H2, W2, C] stored dtype, the agent's ego-frame map when
+                                 warp_in_branch = 1 (E_ARG otherwise)               (agent) */
 } rtcc_tensor_id;
 
 typedef struct rtcc_ctx rtcc_ctx;
@@ -252,16 +263,19 @@ RTCC_API rtcc_status rtcc_get_tensor(rtcc_ctx *ctx, int32_t id, int32_t agent, v
 /* Node service times c_v (Sec. IV-A): re-run the last completed frame's
  * work node by node on one stream, `warmup` untimed passes then `reps`
  * timed passes, and write the median of each node in ms.  Nodes: E_0 ..
- * E_{K-1} (encoder without the H2D copy), then the post-join subgraph
- * (warp + fusion + head + decode + rotated NMS when it is on).  *n_nodes
- * is K + 1; median_ms must hold RTCC_MAX_AGENTS + 1 floats. */
+ * E_{K-1} (encoder without the H2D copy, with the warp when
+ * warp_in_branch = 1), then the post-join subgraph (warp + fusion, or
+ * fusion alone, + head + decode + rotated NMS when it is on).  *n_nodes is
+ * K + 1; median_ms must hold RTCC_MAX_AGENTS + 1 floats. */
 RTCC_API rtcc_status rtcc_profile_nodes(rtcc_ctx *ctx, int32_t warmup, int32_t reps, float *median_ms,
                                int32_t *n_nodes);
 
 /* Per-kernel-group GPU durations (ms) of the last frame, recorded when
  * opts.node_timing = 1.  For each agent k, in order: h2d, pillar (cell ids,
  * counting sort, segment), pfn_canvas, conv[0 .. L-1], up[0 .. S-1] (0 if
- * no upsampling); then warp_fuse, head, decode, nms (0 if off).  Conv nodes
+ * no upsampling), warp (0 unless warp_in_branch = 1 and the agent's pose
+ * is not the identity, which needs no resampling); then warp_fuse (or
+ * fuse), head, decode, nms (0 if off).  Conv nodes
  * are the execution time of their kernels (events that bracket the kernels
  * themselves); the other nodes span the stream between events recorded
  * around them, dispatch gaps included.  *n = number written; ms must hold

@@ -76,7 +76,7 @@ rtcc_status Controller::begin_frame(double t0) {
 rtcc_status Controller::dispatch_locked(int agent, const float *pts, int64_t n, bool device_src) {
     dispatch_[agent] = now_s() - t0_;
     std::string err;
-    rtcc_status s = ex_->dispatch(agent, pts, n, device_src, err);
+    rtcc_status s = ex_->dispatch(agent, pts, n, device_src, affine_[agent].data(), err);
     if (s != RTCC_OK) return fail(s, err);
     z_[agent] = RTCC_RUNNING;
     return RTCC_OK;

@@ -26,8 +26,10 @@ class Executor {
                              std::string &err) = 0;
     virtual float *staging(int agent) = 0;
     virtual rtcc_status begin_frame(std::string &err) = 0;
-    // Enqueue H2D (unless device_src) and encoder E_agent.
-    virtual rtcc_status dispatch(int agent, const float *pts, int64_t n, bool device_src,
+    // Enqueue H2D (unless device_src) and encoder E_agent; `affine` is the
+    // agent's pose warp (index space), used by the branch when the warp is
+    // its last node.
+    virtual rtcc_status dispatch(int agent, const float *pts, int64_t n, bool device_src, const float affine[6],
                                  std::string &err) = 0;
     // Wait for all encoders on the device, run the post-join subgraph with
     // the given per-agent warp affines, copy detections to the host.  Fills

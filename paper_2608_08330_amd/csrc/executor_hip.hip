@@ -90,10 +90,12 @@ class HipExecutor : public Executor {
             if (ws_bytes) HIP_TRY(alloc(&b.d_ws, ws_bytes));
             if (!p.ups.empty()) HIP_TRY(alloc(&b.d_slotbuf, size_t(p.H2) * p.W2 * p.c_slot * p.elt));
             else b.d_slotbuf = b.d_act.back();
+            if (p.d.warp_in_branch) HIP_TRY(alloc(&b.d_warped, size_t(p.H2) * p.W2 * p.c_slot * p.elt));
+            b.ego_map = b.d_slotbuf;
             HIP_TRY(hipStreamCreateWithFlags(&b.stream, hipStreamNonBlocking));
             HIP_TRY(hipEventCreateWithFlags(&b.done, hipEventDisableTiming));
             HIP_TRY(hipEventCreateWithFlags(&b.h2d_done, hipEventDisableTiming));
-            b.ev.resize(4 + p.convs.size() + p.ups.size());
+            b.ev.resize(5 + p.convs.size() + p.ups.size());
             for (auto &e : b.ev) HIP_TRY(hipEventCreate(&e));
             b.kev.resize(2 * p.convs.size());
             for (auto &e : b.kev) HIP_TRY(hipEventCreate(&e));
@@ -156,10 +158,11 @@ class HipExecutor : public Executor {
         return RTCC_OK;
     }
 
-    rtcc_status dispatch(int agent, const float *pts, int64_t n, bool device_src,
+    rtcc_status dispatch(int agent, const float *pts, int64_t n, bool device_src, const float affine[6],
                          std::string &err) override {
         HIP_TRY(hipSetDevice(dev_));
         Branch &b = br_[agent];
+        for (int e = 0; e < 6; ++e) b.affine[e] = affine[e];
         const bool serial = o_.exec == RTCC_EXEC_SERIAL;
         hipStream_t cs = serial ? join_stream_ : b.stream;
         const bool timing = o_.node_timing != 0;
@@ -290,22 +293,34 @@ class HipExecutor : public Executor {
     }
 
     int node_count() const override {
-        return p_.K * int(3 + p_.convs.size() + (p_.ups.empty() ? 1 : p_.ups.size())) + 4;
+        return p_.K * int(3 + p_.convs.size() + (p_.ups.empty() ? 1 : p_.ups.size()) + 1) + 4;
     }
 
+    // Events of a branch: ev[0] dispatch, ev[1] after the H2D copy, ev[2]
+    // after the pillar stage, ev[3] after the PFN canvas, ev[4 + l] after
+    // conv l, ev[4 + L + s] after upsampling s, ev[4 + L + S] after the warp.
     rtcc_status node_times(float *ms, int *n, std::string &err) override {
         int q = 0;
+        const int L = int(p_.convs.size()), S = int(p_.ups.size());
         for (const Branch &b : br_) {
-            for (size_t e = 0; e + 1 < b.ev.size(); ++e) {
-                float v = 0.f;
-                const size_t l = e - 3;  // node e >= 3 and < 3 + L is conv layer e - 3
-                if (e >= 3 && l < p_.convs.size())
-                    HIP_TRY(hipEventElapsedTime(&v, b.kev[2 * l], b.kev[2 * l + 1]));
-                else
-                    HIP_TRY(hipEventElapsedTime(&v, b.ev[e], b.ev[e + 1]));
+            float v = 0.f;
+            for (int e = 0; e < 3; ++e) {
+                HIP_TRY(hipEventElapsedTime(&v, b.ev[e], b.ev[e + 1]));
                 ms[q++] = v;
             }
-            if (p_.ups.empty()) ms[q++] = 0.f;
+            for (int l = 0; l < L; ++l) {
+                HIP_TRY(hipEventElapsedTime(&v, b.kev[2 * l], b.kev[2 * l + 1]));
+                ms[q++] = v;
+            }
+            for (int u = 0; u < S; ++u) {
+                HIP_TRY(hipEventElapsedTime(&v, b.ev[3 + L + u], b.ev[4 + L + u]));
+                ms[q++] = v;
+            }
+            if (S == 0) ms[q++] = 0.f;
+            v = 0.f;
+            if (p_.d.warp_in_branch && b.warp_ran)
+                HIP_TRY(hipEventElapsedTime(&v, b.ev[3 + L + S], b.ev[4 + L + S]));
+            ms[q++] = v;
         }
         for (int e = 0; e < 4; ++e) {
             float v = 0.f;
@@ -323,6 +338,10 @@ class HipExecutor : public Executor {
         void *d_pcells = nullptr, *d_pcounts = nullptr, *d_overfull = nullptr;
         void *d_counts = nullptr, *d_offsets = nullptr, *d_tiles = nullptr, *d_meta = nullptr;
         void *d_canvas = nullptr, *d_slotbuf = nullptr, *d_ws = nullptr;
+        void *d_warped = nullptr;        // ego-frame map (warp in the branch)
+        const void *ego_map = nullptr;   // what the fusion reads when the warp is in the branch
+        float affine[6] = {1, 0, 0, 0, 1, 0};
+        bool warp_ran = false;           // the last frame ran a branch warp kernel
         std::vector<void *> d_act;
         hipStream_t stream = nullptr;
         hipEvent_t done = nullptr, h2d_done = nullptr;
@@ -451,23 +470,56 @@ class HipExecutor : public Executor {
             if (timing) HIP_TRY(hipEventRecord(b.ev[ev], s));
             ++ev;
         }
+        if (p.d.warp_in_branch) {
+            // The identity pose (the ego agent) samples every cell exactly at
+            // itself with weight 1, a copy: the fusion then reads the slot.
+            // (Compared by value: the identity's off-diagonal terms may be -0.)
+            static const float kIdentity[6] = {1, 0, 0, 0, 1, 0};
+            b.warp_ran = false;
+            for (int e = 0; e < 6; ++e) b.warp_ran |= b.affine[e] != kIdentity[e];
+            if (!b.warp_ran) {
+                b.ego_map = b.d_slotbuf;
+            } else {
+                kern::WarpSlotArgs wa{};
+                wa.slot = b.d_slotbuf;
+                for (int e = 0; e < 6; ++e) wa.affine[e] = b.affine[e];
+                wa.out = b.d_warped;
+                wa.H2 = p.H2;
+                wa.W2 = p.W2;
+                wa.C = p.c_slot;
+                HIP_TRY(kern::warp_slot(p.bf16, wa, s));
+                b.ego_map = b.d_warped;
+            }
+            if (timing) HIP_TRY(hipEventRecord(b.ev[ev], s));
+            ++ev;
+        }
         return RTCC_OK;
     }
 
     rtcc_status enqueue_post(const std::vector<std::array<float, 6>> &affine, hipStream_t s, bool timing,
                              std::string &err) {
         const Plan &p = p_;
-        kern::WarpArgs wa{};
-        for (int k = 0; k < p.K; ++k) {
-            wa.slots[k] = br_[k].d_slotbuf;
-            for (int e = 0; e < 6; ++e) wa.affine[k][e] = affine[k][e];
+        if (p.d.warp_in_branch) {
+            kern::FuseArgs fa{};
+            for (int k = 0; k < p.K; ++k) fa.maps[k] = br_[k].ego_map;
+            fa.fused = d_fused;
+            fa.K = p.K;
+            fa.cells = p.H2 * p.W2;
+            fa.C = p.c_slot;
+            HIP_TRY(kern::fuse(p.bf16, p.d.fusion == RTCC_FUSE_ATTN, fa, s));
+        } else {
+            kern::WarpArgs wa{};
+            for (int k = 0; k < p.K; ++k) {
+                wa.slots[k] = br_[k].d_slotbuf;
+                for (int e = 0; e < 6; ++e) wa.affine[k][e] = affine[k][e];
+            }
+            wa.fused = d_fused;
+            wa.K = p.K;
+            wa.H2 = p.H2;
+            wa.W2 = p.W2;
+            wa.C = p.c_slot;
+            HIP_TRY(kern::warp_fuse(p.bf16, p.d.fusion == RTCC_FUSE_ATTN, wa, s));
         }
-        wa.fused = d_fused;
-        wa.K = p.K;
-        wa.H2 = p.H2;
-        wa.W2 = p.W2;
-        wa.C = p.c_slot;
-        HIP_TRY(kern::warp_fuse(p.bf16, p.d.fusion == RTCC_FUSE_ATTN, wa, s));
         if (timing) HIP_TRY(hipEventRecord(post_ev_[1], s));
         HIP_TRY(kern::head1x1(p.bf16, d_fused, static_cast<const char *>(d_mat) + p.head_w_off * p.elt,
                               static_cast<const float *>(d_bias) + p.head_b_off, static_cast<float *>(d_head),
@@ -518,7 +570,7 @@ class HipExecutor : public Executor {
     rtcc_status locate(int id, int agent, void **ptr, size_t *bytes, std::string &err) {
         const Plan &p = p_;
         const bool per_agent = id == RTCC_T_PILLAR_CELLS || id == RTCC_T_PILLAR_COUNTS ||
-                               id == RTCC_T_CANVAS || id == RTCC_T_SLOT;
+                               id == RTCC_T_CANVAS || id == RTCC_T_SLOT || id == RTCC_T_WARPED;
         int stage = 0;
         if (id == RTCC_T_STAGE_OUT) {
             stage = agent >> 8;
@@ -549,6 +601,14 @@ class HipExecutor : public Executor {
                 return RTCC_OK;
             case RTCC_T_SLOT:
                 *ptr = br_[agent].d_slotbuf;
+                *bytes = size_t(p.H2) * p.W2 * p.c_slot * p.elt;
+                return RTCC_OK;
+            case RTCC_T_WARPED:
+                if (!p.d.warp_in_branch) {
+                    err = "no ego-frame maps: the warp is not in the branches";
+                    return RTCC_E_ARG;
+                }
+                *ptr = const_cast<void *>(br_[agent].ego_map);
                 *bytes = size_t(p.H2) * p.W2 * p.c_slot * p.elt;
                 return RTCC_OK;
             case RTCC_T_FUSED:

@@ -38,11 +38,12 @@ class FakeExecutor : public Executor {
         log_line("begin_frame");
         return RTCC_OK;
     }
-    rtcc_status dispatch(int agent, const float *pts, int64_t n, bool device_src,
+    rtcc_status dispatch(int agent, const float *pts, int64_t n, bool device_src, const float affine[6],
                          std::string &) override {
         std::ostringstream os;
         os << "dispatch " << agent << " n=" << n << " src=" << (device_src ? "device" : "staging")
-           << " staged=" << (pts == staging_[agent].data() ? 1 : 0);
+           << " staged=" << (pts == staging_[agent].data() ? 1 : 0) << " affine=[" << affine[0] << ","
+           << affine[1] << "," << affine[2] << "," << affine[3] << "," << affine[4] << "," << affine[5] << "]";
         log_line(os.str());
         return RTCC_OK;
     }

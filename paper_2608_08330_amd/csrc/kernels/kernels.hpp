@@ -113,6 +113,24 @@ struct WarpArgs {
 };
 hipError_t warp_fuse(bool bf16, bool attn, const WarpArgs &a, hipStream_t s);
 
+// Warp as the last node of a branch: one agent's slot resampled on the ego
+// grid (the sampling of warp_fuse) and stored in the activation dtype.
+struct WarpSlotArgs {
+    const void *slot;  // [H2*W2][C]
+    float affine[6];   // {M00, M01, t0, M10, M11, t1}
+    void *out;         // [H2*W2][C]
+    int32_t H2, W2, C;
+};
+hipError_t warp_slot(bool bf16, const WarpSlotArgs &a, hipStream_t s);
+
+// Fusion (the fold of warp_fuse) of K stored ego-frame maps.
+struct FuseArgs {
+    const void *maps[16];  // per agent [cells][C]
+    void *fused;           // [cells][C]
+    int32_t K, cells, C;
+};
+hipError_t fuse(bool bf16, bool attn, const FuseArgs &a, hipStream_t s);
+
 // 1x1 head: out[m][16] float32 = bias + Bt[16][C] . in[m][C].
 hipError_t head1x1(bool bf16, const void *in, const void *wt, const float *bias, float *out,
                    int32_t M, int32_t C, hipStream_t s);

@@ -10,6 +10,10 @@
 //   with butterfly shuffles (fixed order, so deterministic).  Bandwidth
 //   bound: every slot is read about once through L2, the fused map written
 //   once.
+// warp_slot + fuse: the same two steps split at the join when the warp is
+//   the last node of each branch: warp_slot resamples one agent's slot on
+//   the ego grid and stores it; fuse folds the K stored maps (sequential
+//   reads) with the same arithmetic.
 // head1x1: one wavefront per 16 pixels; the 16 outputs of a pixel are one
 //   16 x 16 MFMA tile per 32 (bf16) or 16 (fp32) input channels.
 // decode: tile counts of kept anchors, one-block scan of the tile counts,
@@ -34,9 +38,6 @@ __device__ inline uint32_t rne_bits(float x) {
     return u + 0x7fffu + ((u >> 16) & 1u);
 }
 
-// Load VEC consecutive elements as float.
-template <typename T, int VEC>
-__device__ inline void load_vec(const T *p, float *v);
 template <int VEC>
 __device__ inline void load_vec_bf16(const uint16_t *p, float *v) {
     if constexpr (VEC % 4 == 0) {
@@ -56,6 +57,16 @@ __device__ inline void load_vec_bf16(const uint16_t *p, float *v) {
         v[0] = __uint_as_float(uint32_t(p[0]) << 16);
     }
 }
+// Load VEC consecutive elements as float.
+template <typename T, int VEC>
+__device__ inline void load_vec(const T *p, float *v) {
+    if constexpr (sizeof(T) == 2) {
+        load_vec_bf16<VEC>(reinterpret_cast<const uint16_t *>(p), v);
+    } else {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) v[e] = reinterpret_cast<const float *>(p)[e];
+    }
+}
 template <int VEC>
 __device__ inline void store_vec_bf16(uint16_t *p, const float *v) {
     if constexpr (VEC % 4 == 0) {
@@ -73,34 +84,79 @@ __device__ inline void store_vec_bf16(uint16_t *p, const float *v) {
     }
 }
 
-// Bilinear sample of one agent's slot at the ego cell (i, j): VEC channels
-// starting at c0, zero outside the grid.  Branch-free: a corner outside the
-// grid loads cell (0, 0) instead and its value is replaced by 0, so the four
-// corner loads of this agent (and of the agent sampled next to it) are all in
-// flight before the first is consumed.
 template <typename T, int VEC>
-__device__ inline void warp_sample(const WarpArgs &a, int k, float fi, float fj, int c0, float *x) {
-    const float *m = a.affine[k];
+__device__ inline void store_vec(T *p, const float *v) {
+    if constexpr (sizeof(T) == 2) {
+        store_vec_bf16<VEC>(reinterpret_cast<uint16_t *>(p), v);
+    } else {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) reinterpret_cast<float *>(p)[e] = v[e];
+    }
+}
+
+// Channel slice of lane l (0 .. 31) of a cell.  Contiguous: channels
+// [VEC l, VEC l + VEC).  Split (bf16, 384 channels): [8 l, 8 l + 8) and
+// [256 + 4 l, 256 + 4 l + 4), so that the 32 lanes read one 512-byte and one
+// 256-byte run with 16- and 8-byte loads instead of three 8-byte loads at a
+// 24-byte stride.  The arithmetic of a channel does not depend on the lane
+// that holds it.
+template <typename T, int VEC>
+constexpr bool kSplitSlice = sizeof(T) == 2 && VEC == 12;
+
+template <typename T, int VEC, bool SPLIT>
+__device__ inline void load_slice(const T *cell, int l, float *v) {
+    if constexpr (SPLIT) {
+        const uint4 a = reinterpret_cast<const uint4 *>(cell)[l];
+        const uint2 b = reinterpret_cast<const uint2 *>(cell + 256)[l];
+        const uint32_t w[6] = {a.x, a.y, a.z, a.w, b.x, b.y};
+#pragma unroll
+        for (int q = 0; q < 6; ++q) {
+            v[2 * q] = bf16_lo(w[q]);
+            v[2 * q + 1] = bf16_hi(w[q]);
+        }
+    } else {
+        load_vec<T, VEC>(cell + l * VEC, v);
+    }
+}
+
+template <typename T, int VEC, bool SPLIT>
+__device__ inline void store_slice(T *cell, int l, const float *v) {
+    if constexpr (SPLIT) {
+        uint32_t w[6];
+#pragma unroll
+        for (int q = 0; q < 6; ++q) w[q] = (rne_bits(v[2 * q]) >> 16) | (rne_bits(v[2 * q + 1]) & 0xffff0000u);
+        reinterpret_cast<uint4 *>(cell)[l] = make_uint4(w[0], w[1], w[2], w[3]);
+        reinterpret_cast<uint2 *>(cell + 256)[l] = make_uint2(w[4], w[5]);
+    } else {
+        store_vec<T, VEC>(cell + l * VEC, v);
+    }
+}
+
+// Bilinear sample of one agent's slot (affine m = {M00, M01, t0, M10, M11,
+// t1}) at the ego cell (i, j): VEC channels starting at c0, zero outside the
+// grid.  Branch-free: a corner outside the grid loads cell (0, 0) instead and
+// its value is replaced by 0, so the four corner loads of this agent (and of
+// the agent sampled next to it) are all in flight before the first is
+// consumed.  No contraction into FMAs: the sample is the same sequence of
+// IEEE operations in every kernel it is inlined into (warp + fusion, branch
+// warp), so both placements of the warp sample identical values.
+template <typename T, int VEC, bool SPLIT>
+__device__ inline void warp_sample(const T *slot, const float *m, int H2, int W2, int C, float fi, float fj,
+                                   int l, float *x) {
+#pragma clang fp contract(off)
     const float u = m[0] * fj + m[1] * fi + m[2];
     const float v = m[3] * fj + m[4] * fi + m[5];
     const float fx0 = floorf(u), fy0 = floorf(v);
     const float fx = u - fx0, fy = v - fy0;
     const int x0 = int(fx0), y0 = int(fy0);
-    const T *slot = static_cast<const T *>(a.slots[k]);
     float val[4][VEC];
     bool in[4];
 #pragma unroll
     for (int cnr = 0; cnr < 4; ++cnr) {
         const int yy = y0 + (cnr >> 1), xx = x0 + (cnr & 1);
-        in[cnr] = unsigned(yy) < unsigned(a.H2) && unsigned(xx) < unsigned(a.W2);
-        const size_t cell = in[cnr] ? size_t(yy) * a.W2 + xx : 0;
-        const T *p = slot + cell * a.C + c0;
-        if constexpr (sizeof(T) == 2) {
-            load_vec_bf16<VEC>(reinterpret_cast<const uint16_t *>(p), val[cnr]);
-        } else {
-#pragma unroll
-            for (int e = 0; e < VEC; ++e) val[cnr][e] = reinterpret_cast<const float *>(p)[e];
-        }
+        in[cnr] = unsigned(yy) < unsigned(H2) && unsigned(xx) < unsigned(W2);
+        const size_t cell = in[cnr] ? size_t(yy) * W2 + xx : 0;
+        load_slice<T, VEC, SPLIT>(slot + cell * C, l, val[cnr]);
     }
 #pragma unroll
     for (int e = 0; e < VEC; ++e) x[e] = 0.f;
@@ -114,29 +170,19 @@ __device__ inline void warp_sample(const WarpArgs &a, int k, float fi, float fj,
     }
 }
 
-template <typename T, int VEC, bool ATTN, int G = 1>
-__global__ __launch_bounds__(256) void k_warp_fuse(WarpArgs a) {
-    const int l32 = threadIdx.x & 31;
-    // XCD-aware order: block ids go to the 8 XCDs round-robin; give each
-    // XCD a contiguous band of cells, so bilinear corners shared by
-    // neighbouring cells are reused from that XCD's L2.
-    int bid = blockIdx.x;
-    const int nb = gridDim.x;
-    if ((nb & 7) == 0) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
-    const int cell = (bid * 256 + int(threadIdx.x)) >> 5;
-    const int n_cells = a.H2 * a.W2;
-    if (cell >= n_cells) return;  // uniform over the 32 lanes of a cell
-    const int i = cell / a.W2, j = cell - (cell / a.W2) * a.W2;
-    const int c0 = l32 * VEC;
-    const float fj = float(j), fi = float(i);
-
+// Cross-agent fusion of one cell's VEC-channel slice, agents folded in index
+// order: a running channel max, or an online softmax whose scores
+// <X_0, X_k> / sqrt(C) are reduced over the 32 lanes of the cell with
+// butterfly shuffles (fixed order, so deterministic).
+template <int VEC, bool ATTN>
+struct Fold {
     float q[VEC], acc[VEC];
-    float run_max = -INFINITY, run_sum = 0.f;
-    const float inv_sqrt_c = 1.0f / sqrtf(float(a.C));
+    float run_max = -INFINITY, run_sum = 0.f, inv_sqrt_c;
+    __device__ explicit Fold(int C) : inv_sqrt_c(1.0f / sqrtf(float(C))) {
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
-
-    auto fold = [&](int k, const float *x) {
+        for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
+    }
+    __device__ void add(int k, const float *x) {
         if constexpr (!ATTN) {
 #pragma unroll
             for (int e = 0; e < VEC; ++e) acc[e] = k == 0 ? x[e] : fmaxf(acc[e], x[e]);
@@ -150,65 +196,117 @@ __global__ __launch_bounds__(256) void k_warp_fuse(WarpArgs a) {
             for (int e = 0; e < VEC; ++e) d += q[e] * x[e];
 #pragma unroll
             for (int off = 16; off >= 1; off >>= 1) d += __shfl_xor(d, off, 32);
-            const float s = d * inv_sqrt_c;
-            const float nm = fmaxf(run_max, s);
+            const float sc = d * inv_sqrt_c;
+            const float nm = fmaxf(run_max, sc);
             const float scale = expf(run_max - nm);
-            const float p = expf(s - nm);
+            const float p = expf(sc - nm);
             run_sum = run_sum * scale + p;
 #pragma unroll
             for (int e = 0; e < VEC; ++e) acc[e] = acc[e] * scale + p * x[e];
             run_max = nm;
         }
-    };
+    }
+    __device__ void finish() {
+        if constexpr (ATTN) {
+            const float inv = 1.0f / run_sum;
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) acc[e] *= inv;
+        }
+    }
+};
 
-    // G agents per iteration (the corner loads of all G in flight together);
-    // with branch-free sampling G = 1 already keeps 8 loads per lane in
-    // flight and measured fastest at c5 size
-    int k = 0;
-    for (; k + G <= a.K; k += G) {
-        float xs[G][VEC];
-#pragma unroll
-        for (int g = 0; g < G; ++g) warp_sample<T, VEC>(a, k + g, fi, fj, c0, xs[g]);
-#pragma unroll
-        for (int g = 0; g < G; ++g) fold(k + g, xs[g]);
+// Cell of this half wavefront.  XCD-aware order: block ids go to the 8 XCDs
+// round-robin; give each XCD a contiguous band of cells, so bilinear corners
+// shared by neighbouring cells are reused from that XCD's L2 (and the fused
+// maps are read in long runs).
+__device__ inline int cell_of_thread() {
+    int bid = blockIdx.x;
+    const int nb = gridDim.x;
+    if ((nb & 7) == 0) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
+    return (bid * 256 + int(threadIdx.x)) >> 5;
+}
+
+template <typename T, int VEC, bool ATTN>
+__global__ __launch_bounds__(256) void k_warp_fuse(WarpArgs a) {
+    const int cell = cell_of_thread();
+    if (cell >= a.H2 * a.W2) return;  // uniform over the 32 lanes of a cell
+    const int i = cell / a.W2, j = cell - (cell / a.W2) * a.W2;
+    const int l = threadIdx.x & 31;
+    const float fj = float(j), fi = float(i);
+    Fold<VEC, ATTN> f(a.C);
+    // with branch-free sampling one agent at a time already keeps 8 loads
+    // per lane in flight; that measured fastest at the 8-agent size
+    for (int k = 0; k < a.K; ++k) {
+        float x[VEC];
+        warp_sample<T, VEC, false>(static_cast<const T *>(a.slots[k]), a.affine[k], a.H2, a.W2, a.C, fi, fj, l, x);
+        f.add(k, x);
     }
-    for (; k < a.K; ++k) {
-        float x0[VEC];
-        warp_sample<T, VEC>(a, k, fi, fj, c0, x0);
-        fold(k, x0);
+    f.finish();
+    store_slice<T, VEC, false>(static_cast<T *>(a.fused) + size_t(cell) * a.C, l, f.acc);
+}
+
+// Branch-side warp: agent k's slot resampled on the ego grid and stored in
+// the activation dtype.
+template <typename T, int VEC>
+__global__ __launch_bounds__(256) void k_warp_slot(WarpSlotArgs a) {
+    const int cell = cell_of_thread();
+    if (cell >= a.H2 * a.W2) return;
+    const int i = cell / a.W2, j = cell - (cell / a.W2) * a.W2;
+    constexpr bool SPLIT = kSplitSlice<T, VEC>;
+    const int l = threadIdx.x & 31;
+    float x[VEC];
+    warp_sample<T, VEC, SPLIT>(static_cast<const T *>(a.slot), a.affine, a.H2, a.W2, a.C, float(i), float(j), l, x);
+    store_slice<T, VEC, SPLIT>(static_cast<T *>(a.out) + size_t(cell) * a.C, l, x);
+}
+
+// Fusion of K ego-frame maps: the same fold as k_warp_fuse over stored
+// maps, read as K sequential streams; the next agent's slice is loaded
+// before the current one is folded.
+template <typename T, int VEC, bool ATTN>
+__global__ __launch_bounds__(256) void k_fuse(FuseArgs a) {
+    const int cell = cell_of_thread();
+    if (cell >= a.cells) return;
+    constexpr bool SPLIT = kSplitSlice<T, VEC>;
+    const size_t off = size_t(cell) * a.C;
+    const int l = threadIdx.x & 31;
+    Fold<VEC, ATTN> f(a.C);
+    float x[2][VEC];
+    load_slice<T, VEC, SPLIT>(static_cast<const T *>(a.maps[0]) + off, l, x[0]);
+    for (int k = 0; k < a.K; ++k) {
+        if (k + 1 < a.K) load_slice<T, VEC, SPLIT>(static_cast<const T *>(a.maps[k + 1]) + off, l, x[(k + 1) & 1]);
+        f.add(k, x[k & 1]);
     }
-    if constexpr (ATTN) {
-        const float inv = 1.0f / run_sum;
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) acc[e] *= inv;
-    }
-    T *dst = static_cast<T *>(a.fused) + size_t(cell) * a.C + c0;
-    if constexpr (sizeof(T) == 2) {
-        store_vec_bf16<VEC>(reinterpret_cast<uint16_t *>(dst), acc);
-    } else {
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) reinterpret_cast<float *>(dst)[e] = acc[e];
-    }
+    f.finish();
+    store_slice<T, VEC, SPLIT>(static_cast<T *>(a.fused) + off, l, f.acc);
 }
 
 template <typename T, int VEC>
-hipError_t launch_warp(bool attn, const WarpArgs &a, hipStream_t s) {
-    const int64_t threads = int64_t(a.H2) * a.W2 * 32;
-    const unsigned g = unsigned((threads + 255) / 256);
-    if (attn) k_warp_fuse<T, VEC, true><<<g, 256, 0, s>>>(a);
-    else k_warp_fuse<T, VEC, false><<<g, 256, 0, s>>>(a);
+hipError_t launch_warp(int kind, bool attn, const void *args, int64_t cells, hipStream_t s) {
+    const unsigned g = unsigned((cells * 32 + 255) / 256);
+    if (kind == 0) {
+        const WarpArgs &a = *static_cast<const WarpArgs *>(args);
+        if (attn) k_warp_fuse<T, VEC, true><<<g, 256, 0, s>>>(a);
+        else k_warp_fuse<T, VEC, false><<<g, 256, 0, s>>>(a);
+    } else if (kind == 1) {
+        k_warp_slot<T, VEC><<<g, 256, 0, s>>>(*static_cast<const WarpSlotArgs *>(args));
+    } else {
+        const FuseArgs &a = *static_cast<const FuseArgs *>(args);
+        if (attn) k_fuse<T, VEC, true><<<g, 256, 0, s>>>(a);
+        else k_fuse<T, VEC, false><<<g, 256, 0, s>>>(a);
+    }
     return hipGetLastError();
 }
 
+// kind 0: warp + fusion, 1: branch warp, 2: fusion of stored maps
 template <typename T>
-hipError_t warp_dispatch(bool attn, const WarpArgs &a, hipStream_t s) {
-    switch (a.C) {
-        case 32: return launch_warp<T, 1>(attn, a, s);
-        case 64: return launch_warp<T, 2>(attn, a, s);
-        case 128: return launch_warp<T, 4>(attn, a, s);
-        case 256: return launch_warp<T, 8>(attn, a, s);
-        case 384: return launch_warp<T, 12>(attn, a, s);
-        case 512: return launch_warp<T, 16>(attn, a, s);
+hipError_t warp_dispatch(int kind, bool attn, const void *args, int C, int64_t cells, hipStream_t s) {
+    switch (C) {
+        case 32: return launch_warp<T, 1>(kind, attn, args, cells, s);
+        case 64: return launch_warp<T, 2>(kind, attn, args, cells, s);
+        case 128: return launch_warp<T, 4>(kind, attn, args, cells, s);
+        case 256: return launch_warp<T, 8>(kind, attn, args, cells, s);
+        case 384: return launch_warp<T, 12>(kind, attn, args, cells, s);
+        case 512: return launch_warp<T, 16>(kind, attn, args, cells, s);
     }
     return hipErrorInvalidValue;
 }
@@ -350,7 +448,20 @@ __global__ __launch_bounds__(256) void k_decode_write(DecodeArgs a) {
 }  // namespace
 
 hipError_t warp_fuse(bool bf16, bool attn, const WarpArgs &a, hipStream_t s) {
-    return bf16 ? warp_dispatch<uint16_t>(attn, a, s) : warp_dispatch<float>(attn, a, s);
+    const int64_t cells = int64_t(a.H2) * a.W2;
+    return bf16 ? warp_dispatch<uint16_t>(0, attn, &a, a.C, cells, s)
+                : warp_dispatch<float>(0, attn, &a, a.C, cells, s);
+}
+
+hipError_t warp_slot(bool bf16, const WarpSlotArgs &a, hipStream_t s) {
+    const int64_t cells = int64_t(a.H2) * a.W2;
+    return bf16 ? warp_dispatch<uint16_t>(1, false, &a, a.C, cells, s)
+                : warp_dispatch<float>(1, false, &a, a.C, cells, s);
+}
+
+hipError_t fuse(bool bf16, bool attn, const FuseArgs &a, hipStream_t s) {
+    return bf16 ? warp_dispatch<uint16_t>(2, attn, &a, a.C, a.cells, s)
+                : warp_dispatch<float>(2, attn, &a, a.C, a.cells, s);
 }
 
 hipError_t head1x1(bool bf16, const void *in, const void *wt, const float *bias, float *out,

@@ -71,6 +71,7 @@ bool make_plan(const rtcc_model_desc &d, Plan &p, std::string &err) {
     if (d.nms_max_candidates > 0 && !(d.nms_iou_threshold >= 0.f && d.nms_iou_threshold <= 1.f)) {
         err = "nms_iou_threshold must be in [0, 1]"; return false;
     }
+    if (d.warp_in_branch != 0 && d.warp_in_branch != 1) { err = "warp_in_branch must be 0 or 1"; return false; }
 
     size_t blob = 0, mat = 0, bias = 0;
     p.pfn_w_off = bias; bias += size_t(4) * d.c_pfn; blob += size_t(4) * d.c_pfn;

@@ -153,7 +153,7 @@ def test_staging_buffer_is_zero_copy(host_ctx):
     stg[:n] = fr["points"][2][:n]
     R.rtcc_begin_frame(ctx, time.monotonic() - 1)
     R.rtcc_release_branch(ctx, 2, stg[:n], fr["poses"][2], 0.0)
-    assert _host_log()[-1] == "dispatch 2 n=100 src=staging staged=1"
+    assert _host_log()[-1].startswith("dispatch 2 n=100 src=staging staged=1 affine=[")
 
 
 def test_concurrent_releases_from_threads(host_ctx):
@@ -194,11 +194,29 @@ def test_pose_affines_match_oracle(host_ctx):
     assert mats[0] == [1.0, 0.0, 0.0, 0.0, 1.0, 0.0] or mats[0][:3] == [1.0, 0.0, 0.0]
 
 
+def test_dispatch_carries_the_agents_pose_warp(host_ctx):
+    """The branch receives its own warp at dispatch (for a warp placed in
+    the branch), the same affine the join receives."""
+    cfg, fr, ctx = host_ctx
+    R.rtcc_set_mode(ctx, R.RTCC_MODE_RELEASE)
+    _host_log()
+    R.rtcc_begin_frame(ctx, time.monotonic())
+    for k in range(cfg["K"]):
+        R.rtcc_release_branch(ctx, k, fr["points"][k], fr["poses"][k], 0.0)
+    R.rtcc_join_and_detect(ctx)
+    log = _host_log()
+    disp = {int(l.split()[1]): l.split("affine=")[1] for l in log if l.startswith("dispatch")}
+    join = [l for l in log if l.startswith("join")][-1]
+    mats = join.split(" ", 1)[1].split(" ")
+    assert [disp[k] for k in range(cfg["K"])] == mats
+
+
 @pytest.mark.parametrize("field,value", [
     ("n_agents", 0), ("n_agents", 17), ("c_pfn", 48), ("pillar_size", 0.0), ("n_anchors", 3),
     ("precision", 5), ("fusion", 9), ("max_points", 0), ("abi_version", 99),
     ("nms_max_candidates", -1), ("nms_max_candidates", 16385), ("nms_iou_threshold", 1.5),
-    ("nms_iou_threshold", -0.5), ("nms_iou_threshold", float("nan")),
+    ("nms_iou_threshold", -0.5), ("nms_iou_threshold", float("nan")), ("warp_in_branch", 2),
+    ("warp_in_branch", -1),
 ])
 def test_bad_descriptor_rejected(field, value):
     cfg = synth.config("t_max")
