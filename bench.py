@@ -42,8 +42,12 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 MEASURED_TRAFFIC = {
     "conv": dict(src="paper_2608_08330_amd/csrc/kernels/igemm.hip", bytes=26.77e6,
                  sha256="c344b6046ed2bdf9191513bbc9f4229dfac31992b8be9a50b15e9f7851d1aef1"),
-    "warp_fuse": dict(src="paper_2608_08330_amd/csrc/kernels/post.hip", bytes=493.70e6,
-                      sha256="2bd8e6aa825c827403e7c4578e180b00136c895a7db997c87a5fb36d8ebb8e95"),
+    "warp_fuse": dict(src="paper_2608_08330_amd/csrc/kernels/post.hip", bytes=489.17e6,
+                      sha256="dcae4db170e631d98f45d4e55720a1be7d842c47ca1613bef3f36b13702ebabe"),
+    "fuse": dict(src="paper_2608_08330_amd/csrc/kernels/post.hip", bytes=453.03e6,
+                 sha256="dcae4db170e631d98f45d4e55720a1be7d842c47ca1613bef3f36b13702ebabe"),
+    "warp_slot": dict(src="paper_2608_08330_amd/csrc/kernels/post.hip", bytes=96.24e6,
+                      sha256="dcae4db170e631d98f45d4e55720a1be7d842c47ca1613bef3f36b13702ebabe"),
 }
 
 
@@ -291,11 +295,11 @@ def main(argv=None):
         },
         "secondary_rooflines": {
             "pillar_pfn_canvas": {"bound": "hbm", "achieved": round(pil_bytes / (pillar_ms * 1e-3) / 1e9, 1),
-                                  "peak": PEAK_HBM_GBS, "unit": "GB/s"},
+                                  "peak": PEAK_HBM_GBS, "unit": "GB/s", "traffic": measured_traffic("warp_slot")},
             ("fuse" if cfg["warp_in_branch"] else "warp_fuse"): {
                 "bound": "hbm", "achieved": round(warp_bytes / (warp_ms * 1e-3) / 1e9, 1),
                 "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "traffic": None if cfg["warp_in_branch"] else measured_traffic("warp_fuse")},
+                "traffic": measured_traffic("fuse" if cfg["warp_in_branch"] else "warp_fuse")},
         },
         "conv_layers": layers,
         "node_ms_mean": {
@@ -314,7 +318,7 @@ def main(argv=None):
     if cfg["warp_in_branch"] and bw_launches:
         out["secondary_rooflines"]["branch_warp"] = {
             "bound": "hbm", "achieved": round(2 * slot_bytes * bw_launches / (bw_ms * 1e-3) / 1e9, 1),
-            "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+            "peak": PEAK_HBM_GBS, "unit": "GB/s", "traffic": measured_traffic("warp_slot")}
     print("# throughput done: %.3f ms/step, %.1f TFLOP/s" % (ms_per_step, value), file=sys.stderr, flush=True)
 
     if a.latency_traces > 0:
