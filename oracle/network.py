@@ -244,14 +244,16 @@ def encoder(points, cfg, pw, keep=False):
 # O7: pose warp
 # ----------------------------------------------------------------------------
 
-def cell_pitch(cfg):
-    H2, W2 = feature_grid(cfg)
+def cell_pitch(cfg, grid=None):
+    """Cell size of a map of ``grid`` = (H, W) cells covering the BEV region
+    (default: the feature grid)."""
+    H2, W2 = feature_grid(cfg) if grid is None else grid
     dx = (cfg["x_range"][1] - cfg["x_range"][0]) / W2
     dy = (cfg["y_range"][1] - cfg["y_range"][0]) / H2
     return dx, dy
 
 
-def sample_coords_metric(pose, cfg):
+def sample_coords_metric(pose, cfg, grid=None):
     """Continuous agent-grid index (u = column, v = row) sampled by every
     ego cell, evaluated through metric coordinates.
 
@@ -261,8 +263,8 @@ def sample_coords_metric(pose, cfg):
     R(yaw)^T (p - t), whose index on the agent's grid (cell centres at
     integer indices) is u = (p_agent.x - xmin) / dx - 1/2, likewise v.
     """
-    H2, W2 = feature_grid(cfg)
-    dx, dy = cell_pitch(cfg)
+    H2, W2 = feature_grid(cfg) if grid is None else grid
+    dx, dy = cell_pitch(cfg, grid)
     yaw, tx, ty = (float(v) for v in pose)
     c, s = math.cos(yaw), math.sin(yaw)
     jj, ii = np.meshgrid(np.arange(W2, dtype=np.float64), np.arange(H2, dtype=np.float64))
@@ -275,7 +277,7 @@ def sample_coords_metric(pose, cfg):
     return u, v
 
 
-def index_affine(pose, cfg):
+def index_affine(pose, cfg, grid=None):
     """The same map written in index space: (u, v) = M (j, i) + t.
 
     With D = diag(dx, dy) and o the centre of cell (0, 0):
@@ -283,7 +285,7 @@ def index_affine(pose, cfg):
       t = D^-1 (R^T (o - t_pose) - o)
     The identity pose gives M = I and t = 0 exactly.
     """
-    dx, dy = cell_pitch(cfg)
+    dx, dy = cell_pitch(cfg, grid)
     yaw, tx, ty = (float(v) for v in pose)
     c, s = math.cos(yaw), math.sin(yaw)
     ox = cfg["x_range"][0] + 0.5 * dx
@@ -296,9 +298,9 @@ def index_affine(pose, cfg):
     return M, t
 
 
-def sample_coords(pose, cfg):
-    H2, W2 = feature_grid(cfg)
-    M, t = index_affine(pose, cfg)
+def sample_coords(pose, cfg, grid=None):
+    H2, W2 = feature_grid(cfg) if grid is None else grid
+    M, t = index_affine(pose, cfg, grid)
     jj, ii = np.meshgrid(np.arange(W2, dtype=np.float64), np.arange(H2, dtype=np.float64))
     u = M[0, 0] * jj + M[0, 1] * ii + t[0]
     v = M[1, 0] * jj + M[1, 1] * ii + t[1]
@@ -326,8 +328,10 @@ def bilinear(X, u, v):
     return out
 
 
-def warp(slot, pose, cfg):
-    u, v = sample_coords(pose, cfg)
+def warp(slot, pose, cfg, grid=None):
+    """Resample an agent's map [H, W, C] on the ego grid of the same size
+    (``grid`` = (H, W); default the feature grid)."""
+    u, v = sample_coords(pose, cfg, grid)
     return bilinear(slot, u, v)
 
 
@@ -423,6 +427,9 @@ def forward(frame, keep=False, agents=None):
     invariance RTCC preserves (Sec. IV-D: fixed agent-indexed feature
     storage, post-join subgraph in topological order).
 
+    With ``cfg['multiscale']`` the agents are fused at every backbone scale
+    before upsampling (see :func:`_forward_multiscale`).
+
     With ``cfg['warp_in_branch']`` the pose warp moves out of the shared
     subgraph into each branch (a dependency-preserving move: the warp of
     agent k needs only E_k's slot and k's pose), which then stores its
@@ -431,6 +438,8 @@ def forward(frame, keep=False, agents=None):
     cfg = frame["cfg"]
     pw = prepared_weights(cfg, frame["weights"])
     K = cfg["K"]
+    if cfg.get("multiscale"):
+        return _forward_multiscale(frame, pw, keep)
     enc = [encoder(frame["points"][k], cfg, pw, keep=keep) for k in range(K)]
     warped = [warp(enc[k]["slot"], frame["poses"][k], cfg) for k in range(K)]
     if cfg.get("warp_in_branch"):
@@ -449,4 +458,48 @@ def forward(frame, keep=False, agents=None):
     out = dict(enc=enc, fused=fused, head=Z, det=det)
     if keep:
         out["warped"] = warped
+    return out
+
+
+def _fuse(cfg, warped):
+    if cfg["fusion"] == "max":
+        return fuse_max(warped)
+    if cfg["fusion"] == "attn":
+        return fuse_attn(warped)
+    raise ValueError(cfg["fusion"])
+
+
+def _forward_multiscale(frame, pw, keep):
+    """Multi-scale fusion: the branch E_k ends at its backbone stage outputs;
+    the shared subgraph warps every agent's stage-s map onto the ego grid of
+    stage s (H_s x W_s cells covering the BEV region, cell-centre
+    convention), fuses the K maps of each scale, upsamples every fused map
+    to the feature grid (transposed convolution, kernel = stride =
+    2^s, bias, ReLU, crop), concatenates the scales and runs the head.
+    Storage points (bf16 workloads): the fused map of each scale and each
+    upsampled map."""
+    cfg = frame["cfg"]
+    K = cfg["K"]
+    if not cfg["up_channels"]:
+        raise ValueError("multi-scale fusion needs the upsampling stages")
+    enc = [encoder(frame["points"][k], cfg, pw, keep=True) for k in range(K)]
+    grids = stage_grids(cfg)
+    H2, W2 = feature_grid(cfg)
+    fused_s, parts, warped_s = [], [], []
+    rel = 1
+    for s, (stride, _c, _n) in enumerate(cfg["stages"]):
+        if s > 0:
+            rel *= stride
+        warped = [warp(enc[k]["stage_out"][s], frame["poses"][k], cfg, grids[s]) for k in range(K)]
+        f = _store(cfg, _fuse(cfg, warped))
+        fused_s.append(f)
+        parts.append(_store(cfg, deconv(f, pw["up%d_w" % s], pw["up%d_b" % s], rel, H2, W2)))
+        if keep:
+            warped_s.append(warped)
+    fused = np.concatenate(parts, axis=2)
+    Z = head(fused, pw["head_w"], pw["head_b"])
+    det = decode(Z, cfg)
+    out = dict(enc=enc, fused=fused, fused_stages=fused_s, head=Z, det=det)
+    if keep:
+        out["warped_stages"] = warped_s
     return out

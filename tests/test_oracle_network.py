@@ -311,3 +311,78 @@ def test_prewarp_attention_identity_poses_and_single_agent():
     scale = np.abs(c["fused"]).max()
     assert np.abs(c["fused"] - d["fused"]).max() <= 2 ** -7 * scale
     assert not np.array_equal(c["fused"], d["fused"])
+
+
+def _multiscale(cfg):
+    c = dict(cfg)
+    c["multiscale"] = True
+    return c
+
+
+def test_stage_grid_warp_identity_and_metric_consistency():
+    cfg = synth.config("c3")  # ragged stage grids: 50 x 176, 25 x 88, 13 x 44
+    for g in N.stage_grids(cfg):
+        M, t = N.index_affine((0.0, 0.0, 0.0), cfg, g)
+        assert np.array_equal(M, np.eye(2)) and np.array_equal(t, np.zeros(2))
+        pose = (0.7, 2.3, -1.9)
+        u1, v1 = N.sample_coords(pose, cfg, g)
+        u2, v2 = N.sample_coords_metric(pose, cfg, g)
+        np.testing.assert_allclose(u1, u2, atol=1e-9)
+        np.testing.assert_allclose(v1, v2, atol=1e-9)
+
+
+def test_stage_grid_whole_cell_translation():
+    cfg = synth.config("t_attn")
+    g = N.stage_grids(cfg)[1]
+    dx, dy = N.cell_pitch(cfg, g)
+    rng = np.random.default_rng(2)
+    X = rng.uniform(0, 1, g + (5,))
+    # the agent lies 2 cells to the right and 1 cell up of the ego: the ego
+    # cell (i, j) pulls the agent cell (i - 1, j - 2)
+    out = N.warp(X, (0.0, 2 * dx, 1 * dy), cfg, g)
+    want = np.zeros_like(X)
+    want[1:, 2:] = X[:-1, :-2]
+    np.testing.assert_allclose(out, want, atol=1e-12)
+
+
+@pytest.mark.parametrize("name", ["t_attn", "t_max"])
+def test_multiscale_one_agent_equals_single_scale(name):
+    """One agent at the identity pose: fusing before or after upsampling is
+    the same (fusion of one map returns it), so both shapes give exactly
+    the same fused map and head output."""
+    cfg = dict(synth.config(name), K=1)
+    fr = synth.make_frame(name)
+    fr1 = dict(fr, cfg=cfg, points=fr["points"][:1], poses=np.zeros((1, 3)))
+    a = N.forward(fr1)
+    b = N.forward(dict(fr1, cfg=_multiscale(cfg)))
+    assert np.array_equal(a["fused"], b["fused"])
+    assert np.array_equal(a["head"], b["head"])
+
+
+def test_multiscale_max_of_identical_agents_is_one_agent():
+    cfg = synth.config("t_max")
+    fr = synth.make_frame(cfg)
+    one = dict(cfg, K=1, multiscale=True)
+    three = dict(cfg, K=3, multiscale=True)
+    p0 = fr["points"][0]
+    a = N.forward(dict(fr, cfg=one, points=[p0], poses=np.zeros((1, 3))))
+    b = N.forward(dict(fr, cfg=three, points=[p0, p0, p0], poses=np.zeros((3, 3))))
+    assert np.array_equal(a["fused"], b["fused"])
+    for s in range(3):
+        assert np.array_equal(a["fused_stages"][s], b["fused_stages"][s])
+
+
+def test_multiscale_fuses_at_every_scale():
+    """The scales are fused independently: the stage-s fused map is the
+    fusion of the agents' warped stage-s maps, and the head reads the
+    upsampled fused maps; with poses, fusing before upsampling differs
+    from the single-scale shape (upsampling is not linear through ReLU)."""
+    cfg = synth.config("t_attn")
+    fr = synth.make_frame(cfg)
+    ms = N.forward(dict(fr, cfg=_multiscale(cfg)), keep=True)
+    for s, f in enumerate(ms["fused_stages"]):
+        want = N._store(cfg, N.fuse_attn(ms["warped_stages"][s]))
+        assert np.array_equal(f, want)
+        assert f.shape[:2] == N.stage_grids(cfg)[s]
+    assert ms["fused"].shape == N.forward(fr)["fused"].shape
+    assert not np.array_equal(ms["fused"], N.forward(fr)["fused"])
