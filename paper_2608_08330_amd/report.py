@@ -92,10 +92,9 @@ def main(argv=None):
             r, same = replay.replay_traces(ctx, staged, fr["poses"], arr[t:t + 1], reps, start=t)
             rows += r
             identical &= same
-            if t % 10 == 0:
-                print("# %s setting %d trace %d/%d A=%.3f s gain=%.3f ms (%.0f s)" % (
-                    a.config, i, t, len(arr), r[0]["A"], (r[0]["B_det"] - r[0]["R_det"]) * 1e3,
-                    time.time() - t0), flush=True)
+            print("# %s setting %d trace %d/%d A=%.3f s gain=%.3f ms (%.0f s)" % (
+                a.config, i, t, len(arr), r[0]["A"], (r[0]["B_det"] - r[0]["R_det"]) * 1e3,
+                time.time() - t0), flush=True)
         summ = replay.summarize(rows)
         pred = np.array([dag.predicted_gain(x, c_enc, c_post) for x in arr]) * 1e3
         meas = np.array([(r["B_head"] - r["R_head"]) * 1e3 for r in rows])
