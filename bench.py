@@ -98,7 +98,9 @@ def layer_work(cfg):
 def encoder_flops(cfg, lw, n_used):
     """PFN (linear 4 -> C on every used point) + convs + upsampling."""
     pfn = 2.0 * 4 * cfg["c_pfn"] * n_used
-    return pfn + sum(c["flops"] for c in lw["convs"]) + sum(u["flops"] for u in lw["ups"])
+    # multi-scale fusion upsamples the fused maps once, after the join
+    ups = 0.0 if cfg.get("multiscale") else sum(u["flops"] for u in lw["ups"])
+    return pfn + sum(c["flops"] for c in lw["convs"]) + ups
 
 
 def timed_steps(ctx, cfg, frame, dev_pts, steps, warmup, R, torch, record_nodes=True):
@@ -170,6 +172,8 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--warp-in-branch", action="store_true",
                     help="place the pose warp as the last node of every branch (the join only fuses)")
+    ap.add_argument("--multiscale", action="store_true",
+                    help="fuse the agents at every backbone scale before upsampling")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB, 5 times "
                          "(reference for the FETCH_SIZE / WRITE_SIZE counters)")
@@ -202,6 +206,7 @@ def main(argv=None):
 
     cfg = synth.config(a.config)
     cfg["warp_in_branch"] = bool(a.warp_in_branch)
+    cfg["multiscale"] = bool(a.multiscale)
     frame = synth.make_frame(cfg)
     lw = layer_work(cfg)
     K = cfg["K"]
@@ -282,7 +287,8 @@ def main(argv=None):
         "config": {
             "workload": "%s: %d agents x %d points, %dx%d BEV, %s, %s fusion%s" % (
                 cfg["name"], K, cfg["n_points"], lw["H"], lw["W"], cfg["precision"], cfg["fusion"],
-                ", warp in the branches" if cfg["warp_in_branch"] else ""),
+                (", warp in the branches" if cfg["warp_in_branch"] else "")
+                + (", multi-scale fusion" if cfg["multiscale"] else "")),
             "agents": K, "inputs": "device-resident",
             "executor": "per-branch streams" if a.exec == "streams" else "serial",
         },
@@ -296,10 +302,6 @@ def main(argv=None):
         "secondary_rooflines": {
             "pillar_pfn_canvas": {"bound": "hbm", "achieved": round(pil_bytes / (pillar_ms * 1e-3) / 1e9, 1),
                                   "peak": PEAK_HBM_GBS, "unit": "GB/s", "traffic": measured_traffic("warp_slot")},
-            ("fuse" if cfg["warp_in_branch"] else "warp_fuse"): {
-                "bound": "hbm", "achieved": round(warp_bytes / (warp_ms * 1e-3) / 1e9, 1),
-                "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "traffic": measured_traffic("fuse" if cfg["warp_in_branch"] else "warp_fuse")},
         },
         "conv_layers": layers,
         "node_ms_mean": {
@@ -309,12 +311,18 @@ def main(argv=None):
             "up_total_per_agent": round(float(np.sum([node[:, k * per_agent + 3 + L:k * per_agent + per_agent]
                                                       for k in range(K)]) / (K * rsteps)), 4),
             "branch_warp_per_agent": round(bw_ms / (K * rsteps), 4),
-            ("fuse" if cfg["warp_in_branch"] else "warp_fuse"): round(float(node[:, post0].mean()), 4),
+            ("multiscale_fusion_upsample" if cfg["multiscale"] else "fuse" if cfg["warp_in_branch"]
+             else "warp_fuse"): round(float(node[:, post0].mean()), 4),
             "head": round(float(node[:, post0 + 1].mean()), 4),
             "decode": round(float(node[:, post0 + 2].mean()), 4),
             "nms": round(float(node[:, post0 + 3].mean()), 4),
         },
     }
+    if not cfg["multiscale"]:
+        out["secondary_rooflines"]["fuse" if cfg["warp_in_branch"] else "warp_fuse"] = {
+            "bound": "hbm", "achieved": round(warp_bytes / (warp_ms * 1e-3) / 1e9, 1),
+            "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "traffic": measured_traffic("fuse" if cfg["warp_in_branch"] else "warp_fuse")}
     if cfg["warp_in_branch"] and bw_launches:
         out["secondary_rooflines"]["branch_warp"] = {
             "bound": "hbm", "achieved": round(2 * slot_bytes * bw_launches / (bw_ms * 1e-3) / 1e9, 1),

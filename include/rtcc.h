@@ -58,7 +58,7 @@ extern "C" {
 #define RTCC_API
 #endif
 
-#define RTCC_ABI_VERSION 3
+#define RTCC_ABI_VERSION 4
 #define RTCC_MAX_AGENTS 16
 #define RTCC_MAX_STAGES 4
 
@@ -141,6 +141,16 @@ typedef struct rtcc_model_desc {
      * they give identical outputs, with attention they differ by the rounding
      * of the stored maps (bf16). */
     int32_t warp_in_branch;
+    /* Fusion shape.  0: each branch upsamples and concatenates its stage
+     * outputs into its slot; the join fuses the K slots.  1 (multi-scale, the
+     * paper's post-join subgraph of multi-scale fusion, upsampling,
+     * concatenation and heads, Sec. III-B): each branch ends at its stage
+     * outputs; the join warps every agent's stage-s map onto the stage-s ego
+     * grid (H_s x W_s cells covering the BEV region), fuses the K maps of
+     * each scale (RTCC_T_FUSED_STAGE), upsamples each fused map once into the
+     * concatenated feature map (RTCC_T_FUSED) and runs the head.  Needs
+     * up_channels > 0 and warp_in_branch = 0. */
+    int32_t multiscale;
 } rtcc_model_desc;
 
 typedef struct rtcc_runtime_opts {
@@ -168,15 +178,18 @@ typedef enum rtcc_tensor_id {
     RTCC_T_PILLAR_CELLS = 0,  /* int32 [P] non-empty cells, ascending             (agent) */
     RTCC_T_PILLAR_COUNTS = 1, /* int32 [P] points per pillar (before the 32 cap)  (agent) */
     RTCC_T_CANVAS = 2,        /* [H, W, c_pfn] stored dtype                        (agent) */
-    RTCC_T_SLOT = 3,          /* [H2, W2, C] stored dtype, agent slot               (agent) */
-    RTCC_T_FUSED = 4,         /* [H2, W2, C] stored dtype                                   */
+    RTCC_T_SLOT = 3,          /* [H2, W2, C] stored dtype, agent slot (E_ARG when
+                                 multiscale = 1: the branch ends at its stages)      (agent) */
+    RTCC_T_FUSED = 4,         /* [H2, W2, C] stored dtype, the head's input                 */
     RTCC_T_HEAD = 5,          /* float32 [H2, W2, 16]                                       */
     RTCC_T_STAGE_OUT = 6,     /* [Hs, Ws, Cs] stored dtype, last conv of stage `agent>>8`,
                                  agent `agent & 255`                                        */
     RTCC_T_DECODED = 7,       /* float32 [count_decoded][9] before NMS: x, y, z, w, l, h,
                                  yaw, score, anchor index (int32 bits); ascending anchor    */
-    RTCC_T_WARPED = 8         /* [H2, W2, C] stored dtype, the agent's ego-frame map when
+    RTCC_T_WARPED = 8,        /* [H2, W2, C] stored dtype, the agent's ego-frame map when
                                  warp_in_branch = 1 (E_ARG otherwise)               (agent) */
+    RTCC_T_FUSED_STAGE = 9    /* [Hs, Ws, Cs] stored dtype, fused map of stage `agent` when
+                                 multiscale = 1 (E_ARG otherwise)                           */
 } rtcc_tensor_id;
 
 typedef struct rtcc_ctx rtcc_ctx;
@@ -273,9 +286,11 @@ RTCC_API rtcc_status rtcc_profile_nodes(rtcc_ctx *ctx, int32_t warmup, int32_t r
 /* Per-kernel-group GPU durations (ms) of the last frame, recorded when
  * opts.node_timing = 1.  For each agent k, in order: h2d, pillar (cell ids,
  * counting sort, segment), pfn_canvas, conv[0 .. L-1], up[0 .. S-1] (0 if
- * no upsampling), warp (0 unless warp_in_branch = 1 and the agent's pose
- * is not the identity, which needs no resampling); then warp_fuse (or
- * fuse), head, decode, nms (0 if off).  Conv nodes
+ * no upsampling; 0 each when multiscale = 1), warp (0 unless warp_in_branch
+ * = 1 and the agent's pose is not the identity, which needs no
+ * resampling); then warp_fuse (or fuse; with multiscale = 1 the warp and
+ * fusion of every scale and the upsampling of the fused maps), head,
+ * decode, nms (0 if off).  Conv nodes
  * are the execution time of their kernels (events that bracket the kernels
  * themselves); the other nodes span the stream between events recorded
  * around them, dispatch gaps included.  *n = number written; ms must hold

@@ -34,6 +34,7 @@ rtcc_status Controller::create(const rtcc_model_desc *d, const void *weights, si
     arrival_.assign(plan_.K, 0.0);
     dispatch_.assign(plan_.K, 0.0);
     affine_.assign(plan_.K, std::array<float, 6>{1, 0, 0, 0, 1, 0});
+    pose_.assign(plan_.K, std::array<float, 3>{0, 0, 0});
     created_ = true;
     return RTCC_OK;
 }
@@ -105,6 +106,7 @@ rtcc_status Controller::release(int agent, const float *pts, int64_t n, const fl
         pts = stg;
     }
     pose_affine(plan_, pose, affine_[agent].data());
+    pose_[agent] = {pose[0], pose[1], pose[2]};
     z_[agent] = RTCC_RELEASED;
     arrival_[agent] = arrival;
 
@@ -138,7 +140,7 @@ rtcc_status Controller::join(rtcc_detections *out) {
     }
     std::memset(out, 0, sizeof(*out));
     std::string err;
-    rtcc_status s = ex_->join(affine_, t_begin_ - t0_, out, err);
+    rtcc_status s = ex_->join(affine_, pose_, t_begin_ - t0_, out, err);
     in_frame_ = false;
     if (s != RTCC_OK) return fail(s, err);
     for (int k = 0; k < plan_.K; ++k) z_[k] = RTCC_FINISHED;

@@ -32,10 +32,12 @@ class Executor {
     virtual rtcc_status dispatch(int agent, const float *pts, int64_t n, bool device_src, const float affine[6],
                                  std::string &err) = 0;
     // Wait for all encoders on the device, run the post-join subgraph with
-    // the given per-agent warp affines, copy detections to the host.  Fills
+    // the given per-agent warp affines (feature grid) and poses (for the
+    // stage grids of multi-scale fusion), copy detections to the host.  Fills
     // out->count / boxes / scores / anchor_idx / t_head_s (relative to the
     // host time t_begin at which begin_frame was called).
-    virtual rtcc_status join(const std::vector<std::array<float, 6>> &affine, double t_begin,
+    virtual rtcc_status join(const std::vector<std::array<float, 6>> &affine,
+                             const std::vector<std::array<float, 3>> &poses, double t_begin,
                              rtcc_detections *out, std::string &err) = 0;
     virtual rtcc_status tensor_bytes(int id, int agent, size_t *bytes, std::string &err) = 0;
     virtual rtcc_status get_tensor(int id, int agent, void *dst, size_t bytes, std::string &err) = 0;
@@ -97,6 +99,7 @@ class Controller {
     std::vector<int> z_;
     std::vector<double> arrival_, dispatch_;
     std::vector<std::array<float, 6>> affine_;
+    std::vector<std::array<float, 3>> pose_;
     std::vector<Pending> pending_;
     std::string err_;
 };

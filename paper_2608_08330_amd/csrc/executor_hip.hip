@@ -88,7 +88,8 @@ class HipExecutor : public Executor {
                 HIP_TRY(alloc(&b.d_act[l], size_t(c.Ho) * c.Wo * c.Co * p.elt));
             }
             if (ws_bytes) HIP_TRY(alloc(&b.d_ws, ws_bytes));
-            if (!p.ups.empty()) HIP_TRY(alloc(&b.d_slotbuf, size_t(p.H2) * p.W2 * p.c_slot * p.elt));
+            if (p.d.multiscale) b.d_slotbuf = nullptr;  // the branch ends at its stage outputs
+            else if (!p.ups.empty()) HIP_TRY(alloc(&b.d_slotbuf, size_t(p.H2) * p.W2 * p.c_slot * p.elt));
             else b.d_slotbuf = b.d_act.back();
             if (p.d.warp_in_branch) HIP_TRY(alloc(&b.d_warped, size_t(p.H2) * p.W2 * p.c_slot * p.elt));
             b.ego_map = b.d_slotbuf;
@@ -101,6 +102,10 @@ class HipExecutor : public Executor {
             for (auto &e : b.kev) HIP_TRY(hipEventCreate(&e));
         }
         HIP_TRY(alloc(&d_fused, size_t(p.H2) * p.W2 * p.c_slot * p.elt));
+        d_fused_stage_.assign(p.ups.size(), nullptr);
+        if (p.d.multiscale)
+            for (const UpLayer &u : p.ups)
+                HIP_TRY(alloc(&d_fused_stage_[u.stage], size_t(u.Hi) * u.Wi * u.Ci * p.elt));
         HIP_TRY(alloc(&d_head, size_t(p.H2) * p.W2 * 16 * 4));
         n_anchor_ = size_t(p.H2) * p.W2 * 2;
         const size_t dec_tiles = (n_anchor_ + kern::kDecodeTile - 1) / kern::kDecodeTile;
@@ -191,14 +196,15 @@ class HipExecutor : public Executor {
         return RTCC_OK;
     }
 
-    rtcc_status join(const std::vector<std::array<float, 6>> &affine, double t_begin,
-                     rtcc_detections *out, std::string &err) override {
+    rtcc_status join(const std::vector<std::array<float, 6>> &affine,
+                     const std::vector<std::array<float, 3>> &poses, double t_begin, rtcc_detections *out,
+                     std::string &err) override {
         HIP_TRY(hipSetDevice(dev_));
         hipStream_t js = compute_stream_for_join();
         for (Branch &b : br_) HIP_TRY(hipStreamWaitEvent(js, b.done, 0));
         const bool timing = o_.node_timing != 0;
         if (timing) HIP_TRY(hipEventRecord(post_ev_[0], js));
-        rtcc_status s = enqueue_post(affine, js, timing, err);
+        rtcc_status s = enqueue_post(affine, poses, js, timing, err);
         if (s != RTCC_OK) return s;
         int32_t *hs = reinterpret_cast<int32_t *>(h_small);
         HIP_TRY(hipMemcpyAsync(hs, d_count, 4, hipMemcpyDeviceToHost, js));
@@ -231,6 +237,7 @@ class HipExecutor : public Executor {
         out->anchor_idx = aidx_.data();
         out->t_head_s = t_begin + 1e-3 * double(ms);
         last_affine_ = affine;
+        last_poses_ = poses;
         return RTCC_OK;
     }
 
@@ -271,7 +278,7 @@ class HipExecutor : public Executor {
             for (int k = 0; k <= p_.K; ++k) {
                 HIP_TRY(hipEventRecord(e0, s));
                 rtcc_status st = k < p_.K ? enqueue_encoder(br_[k], s, false, 0, err)
-                                          : enqueue_post(last_affine_, s, false, err);
+                                          : enqueue_post(last_affine_, last_poses_, s, false, err);
                 if (st != RTCC_OK) return st;
                 HIP_TRY(hipEventRecord(e1, s));
                 HIP_TRY(hipEventSynchronize(e1));
@@ -313,7 +320,8 @@ class HipExecutor : public Executor {
                 ms[q++] = v;
             }
             for (int u = 0; u < S; ++u) {
-                HIP_TRY(hipEventElapsedTime(&v, b.ev[3 + L + u], b.ev[4 + L + u]));
+                v = 0.f;
+                if (!p_.d.multiscale) HIP_TRY(hipEventElapsedTime(&v, b.ev[3 + L + u], b.ev[4 + L + u]));
                 ms[q++] = v;
             }
             if (S == 0) ms[q++] = 0.f;
@@ -451,22 +459,8 @@ class HipExecutor : public Executor {
             x = b.d_act[l];
         }
         for (const UpLayer &u : p.ups) {
-            kern::GemmArgs ga{};
-            ga.in = b.d_act[p.stage_last_conv[u.stage]];
-            ga.wt = static_cast<const char *>(d_mat) + u.w_off * p.elt;
-            ga.bias = static_cast<const float *>(d_bias) + u.b_off;
-            ga.out = b.d_slotbuf;
-            ga.Hi = u.Hi; ga.Wi = u.Wi; ga.Ci = u.Ci;
-            ga.Ho = p.H2; ga.Wo = p.W2; ga.N = u.Co;
-            ga.stride = 1;
-            ga.u = u.u;
-            ga.ldo = p.c_slot;
-            ga.c_off = u.c_off;
-            ga.splits = 1;
-            ga.variant = kern::kConvImplicit;
-            ga.zero = d_zero;
-            ga.ws = nullptr;
-            HIP_TRY(kern::deconv(p.bf16, ga, s));
+            if (p.d.multiscale) break;  // upsampling runs once, on the fused maps
+            HIP_TRY(upsample(u, b.d_act[p.stage_last_conv[u.stage]], b.d_slotbuf, s));
             if (timing) HIP_TRY(hipEventRecord(b.ev[ev], s));
             ++ev;
         }
@@ -496,10 +490,50 @@ class HipExecutor : public Executor {
         return RTCC_OK;
     }
 
-    rtcc_status enqueue_post(const std::vector<std::array<float, 6>> &affine, hipStream_t s, bool timing,
+    // Upsampling u of the map `in` into channels [c_off, c_off + Co) of `out`
+    // ([H2][W2][c_slot]).
+    hipError_t upsample(const UpLayer &u, const void *in, void *out, hipStream_t s) {
+        const Plan &p = p_;
+        kern::GemmArgs ga{};
+        ga.in = in;
+        ga.wt = static_cast<const char *>(d_mat) + u.w_off * p.elt;
+        ga.bias = static_cast<const float *>(d_bias) + u.b_off;
+        ga.out = out;
+        ga.Hi = u.Hi; ga.Wi = u.Wi; ga.Ci = u.Ci;
+        ga.Ho = p.H2; ga.Wo = p.W2; ga.N = u.Co;
+        ga.stride = 1;
+        ga.u = u.u;
+        ga.ldo = p.c_slot;
+        ga.c_off = u.c_off;
+        ga.splits = 1;
+        ga.variant = kern::kConvImplicit;
+        ga.zero = d_zero;
+        ga.ws = nullptr;
+        return kern::deconv(p.bf16, ga, s);
+    }
+
+    rtcc_status enqueue_post(const std::vector<std::array<float, 6>> &affine,
+                             const std::vector<std::array<float, 3>> &poses, hipStream_t s, bool timing,
                              std::string &err) {
         const Plan &p = p_;
-        if (p.d.warp_in_branch) {
+        if (p.d.multiscale) {
+            // every scale: warp the K stage maps onto the stage's ego grid and
+            // fuse them, then upsample the fused map into the head's input
+            for (const UpLayer &u : p.ups) {
+                kern::WarpArgs wa{};
+                for (int k = 0; k < p.K; ++k) {
+                    wa.slots[k] = br_[k].d_act[p.stage_last_conv[u.stage]];
+                    pose_affine_grid(p, poses[k].data(), u.Hi, u.Wi, wa.affine[k]);
+                }
+                wa.fused = d_fused_stage_[u.stage];
+                wa.K = p.K;
+                wa.H2 = u.Hi;
+                wa.W2 = u.Wi;
+                wa.C = u.Ci;
+                HIP_TRY(kern::warp_fuse(p.bf16, p.d.fusion == RTCC_FUSE_ATTN, wa, s));
+                HIP_TRY(upsample(u, d_fused_stage_[u.stage], d_fused, s));
+            }
+        } else if (p.d.warp_in_branch) {
             kern::FuseArgs fa{};
             for (int k = 0; k < p.K; ++k) fa.maps[k] = br_[k].ego_map;
             fa.fused = d_fused;
@@ -600,6 +634,10 @@ class HipExecutor : public Executor {
                 *bytes = size_t(p.H) * p.W * p.c_pfn * p.elt;
                 return RTCC_OK;
             case RTCC_T_SLOT:
+                if (p.d.multiscale) {
+                    err = "multi-scale fusion: the branch ends at its stage outputs (no slot)";
+                    return RTCC_E_ARG;
+                }
                 *ptr = br_[agent].d_slotbuf;
                 *bytes = size_t(p.H2) * p.W2 * p.c_slot * p.elt;
                 return RTCC_OK;
@@ -611,6 +649,16 @@ class HipExecutor : public Executor {
                 *ptr = const_cast<void *>(br_[agent].ego_map);
                 *bytes = size_t(p.H2) * p.W2 * p.c_slot * p.elt;
                 return RTCC_OK;
+            case RTCC_T_FUSED_STAGE: {
+                if (!p.d.multiscale || agent < 0 || agent >= int(p.ups.size())) {
+                    err = "no fused stage map (needs multiscale = 1 and a stage index)";
+                    return RTCC_E_ARG;
+                }
+                const UpLayer &u = p.ups[agent];
+                *ptr = d_fused_stage_[u.stage];
+                *bytes = size_t(u.Hi) * u.Wi * u.Ci * p.elt;
+                return RTCC_OK;
+            }
             case RTCC_T_FUSED:
                 *ptr = d_fused;
                 *bytes = size_t(p.H2) * p.W2 * p.c_slot * p.elt;
@@ -691,6 +739,8 @@ class HipExecutor : public Executor {
     hipEvent_t ev_frame0_ = nullptr, ev_head_ = nullptr;
     hipEvent_t post_ev_[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
     std::vector<std::array<float, 6>> last_affine_;
+    std::vector<std::array<float, 3>> last_poses_;
+    std::vector<void *> d_fused_stage_;  // multi-scale: fused map of every stage
 };
 
 Executor *make_executor() { return new HipExecutor(); }

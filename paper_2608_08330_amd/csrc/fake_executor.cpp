@@ -47,8 +47,8 @@ class FakeExecutor : public Executor {
         log_line(os.str());
         return RTCC_OK;
     }
-    rtcc_status join(const std::vector<std::array<float, 6>> &affine, double,
-                     rtcc_detections *out, std::string &) override {
+    rtcc_status join(const std::vector<std::array<float, 6>> &affine, const std::vector<std::array<float, 3>> &,
+                     double, rtcc_detections *out, std::string &) override {
         std::ostringstream os;
         os << "join";
         for (const auto &m : affine)

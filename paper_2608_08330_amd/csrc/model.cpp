@@ -72,6 +72,10 @@ bool make_plan(const rtcc_model_desc &d, Plan &p, std::string &err) {
         err = "nms_iou_threshold must be in [0, 1]"; return false;
     }
     if (d.warp_in_branch != 0 && d.warp_in_branch != 1) { err = "warp_in_branch must be 0 or 1"; return false; }
+    if (d.multiscale != 0 && d.multiscale != 1) { err = "multiscale must be 0 or 1"; return false; }
+    if (d.multiscale && (d.up_channels == 0 || d.warp_in_branch)) {
+        err = "multiscale needs up_channels > 0 and warp_in_branch = 0"; return false;
+    }
 
     size_t blob = 0, mat = 0, bias = 0;
     p.pfn_w_off = bias; bias += size_t(4) * d.c_pfn; blob += size_t(4) * d.c_pfn;
@@ -191,9 +195,11 @@ bool prepare_weights(const Plan &p, const float *blob, size_t n_floats, HostWeig
     return true;
 }
 
-void pose_affine(const Plan &p, const float pose[3], float m[6]) {
-    const double dx = (double(p.d.x_max) - double(p.d.x_min)) / p.W2;
-    const double dy = (double(p.d.y_max) - double(p.d.y_min)) / p.H2;
+void pose_affine(const Plan &p, const float pose[3], float m[6]) { pose_affine_grid(p, pose, p.H2, p.W2, m); }
+
+void pose_affine_grid(const Plan &p, const float pose[3], int H, int W, float m[6]) {
+    const double dx = (double(p.d.x_max) - double(p.d.x_min)) / W;
+    const double dy = (double(p.d.y_max) - double(p.d.y_min)) / H;
     const double c = std::cos(double(pose[0])), s = std::sin(double(pose[0]));
     const double ox = double(p.d.x_min) + 0.5 * dx, oy = double(p.d.y_min) + 0.5 * dy;
     // ego cell centre o + D (j, i) pulls the agent point R^T (o + D (j, i) - t):

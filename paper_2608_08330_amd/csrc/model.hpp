@@ -75,6 +75,8 @@ float bf16_to_f32(uint16_t h);
 // of ego cell (i, j) is (u, v) = M (j, i) + t.  Output m = {M00, M01, t0,
 // M10, M11, t1}.  Identity pose -> exactly {1, 0, 0, 0, 1, 0}.
 void pose_affine(const Plan &p, const float pose[3], float m[6]);
+// The same for a map of H x W cells covering the BEV region (a stage grid).
+void pose_affine_grid(const Plan &p, const float pose[3], int H, int W, float m[6]);
 
 double now_s();
 

@@ -20,7 +20,7 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_DIR = os.path.join(HERE, "lib")
 
-RTCC_ABI_VERSION = 3
+RTCC_ABI_VERSION = 4
 RTCC_MAX_AGENTS = 16
 RTCC_MAX_STAGES = 4
 
@@ -37,7 +37,7 @@ RTCC_MODE_RELEASE, RTCC_MODE_BARRIER = 0, 1
 RTCC_EXEC_PER_BRANCH_STREAMS, RTCC_EXEC_SERIAL = 0, 1
 RTCC_WAITING, RTCC_RELEASED, RTCC_RUNNING, RTCC_FINISHED = 0, 1, 2, 3
 (RTCC_T_PILLAR_CELLS, RTCC_T_PILLAR_COUNTS, RTCC_T_CANVAS, RTCC_T_SLOT, RTCC_T_FUSED,
- RTCC_T_HEAD, RTCC_T_STAGE_OUT, RTCC_T_DECODED, RTCC_T_WARPED) = range(9)
+ RTCC_T_HEAD, RTCC_T_STAGE_OUT, RTCC_T_DECODED, RTCC_T_WARPED, RTCC_T_FUSED_STAGE) = range(10)
 (RTCC_SCHED_MAXRATE, RTCC_SCHED_MAXWEIGHT, RTCC_SCHED_EARLIEST_RELEASE, RTCC_SCHED_WEIGHTED_RATE,
  RTCC_SCHED_ROUND_ROBIN, RTCC_SCHED_PROPORTIONAL_FAIR) = range(6)
 
@@ -70,6 +70,7 @@ class rtcc_model_desc(ctypes.Structure):
         ("nms_max_candidates", ctypes.c_int32),
         ("nms_iou_threshold", ctypes.c_float),
         ("warp_in_branch", ctypes.c_int32),
+        ("multiscale", ctypes.c_int32),
     ]
 
 
@@ -221,6 +222,7 @@ def model_desc(cfg, max_points=None):
     d.nms_max_candidates = cfg.get("nms_max_candidates", 0)
     d.nms_iou_threshold = cfg.get("nms_iou_threshold", 0.0)
     d.warp_in_branch = int(bool(cfg.get("warp_in_branch", False)))
+    d.multiscale = int(bool(cfg.get("multiscale", False)))
     return d
 
 

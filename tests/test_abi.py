@@ -216,7 +216,7 @@ def test_dispatch_carries_the_agents_pose_warp(host_ctx):
     ("precision", 5), ("fusion", 9), ("max_points", 0), ("abi_version", 99),
     ("nms_max_candidates", -1), ("nms_max_candidates", 16385), ("nms_iou_threshold", 1.5),
     ("nms_iou_threshold", -0.5), ("nms_iou_threshold", float("nan")), ("warp_in_branch", 2),
-    ("warp_in_branch", -1),
+    ("warp_in_branch", -1), ("multiscale", 2),
 ])
 def test_bad_descriptor_rejected(field, value):
     cfg = synth.config("t_max")
@@ -254,3 +254,15 @@ def test_host_library_nms_entry_reports_no_gpu():
     kept = ctypes.c_int64(5)
     assert lib.rtcc_rotated_nms(None, 0, 16, 0.15, None, ctypes.byref(kept)) == R.RTCC_E_STATE
     assert kept.value == 0 and b"GPU" in lib.rtcc_last_error(None)
+
+
+def test_multiscale_needs_upsampling_and_a_post_join_warp():
+    for name, extra in (("c1", {}), ("t_attn", {"warp_in_branch": True})):
+        cfg = dict(synth.config(name), multiscale=True, **extra)
+        fr = synth.make_frame(name)
+        with pytest.raises(R.RtccError) as e:
+            R.rtcc_create(R.model_desc(cfg), R.weights_blob(cfg, fr["weights"]), kind="host")
+        assert e.value.status == R.RTCC_E_ARG
+    cfg = dict(synth.config("t_attn"), multiscale=True)
+    fr = synth.make_frame("t_attn")
+    R.rtcc_create(R.model_desc(cfg), R.weights_blob(cfg, fr["weights"]), kind="host").close()
