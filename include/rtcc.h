@@ -290,10 +290,10 @@ RTCC_API rtcc_status rtcc_profile_nodes(rtcc_ctx *ctx, int32_t warmup, int32_t r
  * = 1 and the agent's pose is not the identity, which needs no
  * resampling); then warp_fuse (or fuse; with multiscale = 1 the warp and
  * fusion of every scale and the upsampling of the fused maps), head,
- * decode, nms (0 if off).  Conv nodes
- * are the execution time of their kernels (events that bracket the kernels
- * themselves); the other nodes span the stream between events recorded
- * around them, dispatch gaps included.  *n = number written; ms must hold
+ * decode, nms (0 if off).  Conv nodes, the branch warp and a one-kernel
+ * warp_fuse / fuse node are the execution time of their kernels (events
+ * that bracket the kernels themselves); the other nodes span the stream
+ * between events recorded around them, dispatch gaps included.  *n = number written; ms must hold
  * at least rtcc_node_count() floats. */
 RTCC_API rtcc_status rtcc_node_times(rtcc_ctx *ctx, float *ms, int32_t *n);
 RTCC_API rtcc_status rtcc_node_count(rtcc_ctx *ctx, int32_t *n);

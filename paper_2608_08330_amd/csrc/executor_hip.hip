@@ -100,6 +100,8 @@ class HipExecutor : public Executor {
             for (auto &e : b.ev) HIP_TRY(hipEventCreate(&e));
             b.kev.resize(2 * p.convs.size());
             for (auto &e : b.kev) HIP_TRY(hipEventCreate(&e));
+            if (p.d.warp_in_branch)
+                for (auto &e : b.wev) HIP_TRY(hipEventCreate(&e));
         }
         HIP_TRY(alloc(&d_fused, size_t(p.H2) * p.W2 * p.c_slot * p.elt));
         d_fused_stage_.assign(p.ups.size(), nullptr);
@@ -203,7 +205,8 @@ class HipExecutor : public Executor {
         hipStream_t js = compute_stream_for_join();
         for (Branch &b : br_) HIP_TRY(hipStreamWaitEvent(js, b.done, 0));
         const bool timing = o_.node_timing != 0;
-        if (timing) HIP_TRY(hipEventRecord(post_ev_[0], js));
+        // one-kernel fusion nodes are timed by events bracketing the kernel
+        if (timing && p_.d.multiscale) HIP_TRY(hipEventRecord(post_ev_[0], js));
         rtcc_status s = enqueue_post(affine, poses, js, timing, err);
         if (s != RTCC_OK) return s;
         int32_t *hs = reinterpret_cast<int32_t *>(h_small);
@@ -326,8 +329,7 @@ class HipExecutor : public Executor {
             }
             if (S == 0) ms[q++] = 0.f;
             v = 0.f;
-            if (p_.d.warp_in_branch && b.warp_ran)
-                HIP_TRY(hipEventElapsedTime(&v, b.ev[3 + L + S], b.ev[4 + L + S]));
+            if (p_.d.warp_in_branch && b.warp_ran) HIP_TRY(hipEventElapsedTime(&v, b.wev[0], b.wev[1]));
             ms[q++] = v;
         }
         for (int e = 0; e < 4; ++e) {
@@ -350,6 +352,7 @@ class HipExecutor : public Executor {
         const void *ego_map = nullptr;   // what the fusion reads when the warp is in the branch
         float affine[6] = {1, 0, 0, 0, 1, 0};
         bool warp_ran = false;           // the last frame ran a branch warp kernel
+        hipEvent_t wev[2] = {nullptr, nullptr};  // bracket the branch warp kernel
         std::vector<void *> d_act;
         hipStream_t stream = nullptr;
         hipEvent_t done = nullptr, h2d_done = nullptr;
@@ -481,7 +484,7 @@ class HipExecutor : public Executor {
                 wa.H2 = p.H2;
                 wa.W2 = p.W2;
                 wa.C = p.c_slot;
-                HIP_TRY(kern::warp_slot(p.bf16, wa, s));
+                HIP_TRY(kern::warp_slot(p.bf16, wa, s, timing ? b.wev[0] : nullptr, timing ? b.wev[1] : nullptr));
                 b.ego_map = b.d_warped;
             }
             if (timing) HIP_TRY(hipEventRecord(b.ev[ev], s));
@@ -540,7 +543,8 @@ class HipExecutor : public Executor {
             fa.K = p.K;
             fa.cells = p.H2 * p.W2;
             fa.C = p.c_slot;
-            HIP_TRY(kern::fuse(p.bf16, p.d.fusion == RTCC_FUSE_ATTN, fa, s));
+            HIP_TRY(kern::fuse(p.bf16, p.d.fusion == RTCC_FUSE_ATTN, fa, s, timing ? post_ev_[0] : nullptr,
+                               timing ? post_ev_[1] : nullptr));
         } else {
             kern::WarpArgs wa{};
             for (int k = 0; k < p.K; ++k) {
@@ -552,9 +556,10 @@ class HipExecutor : public Executor {
             wa.H2 = p.H2;
             wa.W2 = p.W2;
             wa.C = p.c_slot;
-            HIP_TRY(kern::warp_fuse(p.bf16, p.d.fusion == RTCC_FUSE_ATTN, wa, s));
+            HIP_TRY(kern::warp_fuse(p.bf16, p.d.fusion == RTCC_FUSE_ATTN, wa, s, timing ? post_ev_[0] : nullptr,
+                                    timing ? post_ev_[1] : nullptr));
         }
-        if (timing) HIP_TRY(hipEventRecord(post_ev_[1], s));
+        if (timing && p.d.multiscale) HIP_TRY(hipEventRecord(post_ev_[1], s));
         HIP_TRY(kern::head1x1(p.bf16, d_fused, static_cast<const char *>(d_mat) + p.head_w_off * p.elt,
                               static_cast<const float *>(d_bias) + p.head_b_off, static_cast<float *>(d_head),
                               p.H2 * p.W2, p.c_slot, s));
@@ -704,6 +709,8 @@ class HipExecutor : public Executor {
             for (hipEvent_t e : b.ev)
                 if (e) (void)hipEventDestroy(e);
             for (hipEvent_t e : b.kev)
+                if (e) (void)hipEventDestroy(e);
+            for (hipEvent_t e : b.wev)
                 if (e) (void)hipEventDestroy(e);
         }
         for (void *ptr : dev_allocs_) (void)hipFree(ptr);

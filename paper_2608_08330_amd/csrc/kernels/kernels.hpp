@@ -111,7 +111,10 @@ struct WarpArgs {
     void *fused;            // [H2*W2][C]
     int32_t K, H2, W2, C;
 };
-hipError_t warp_fuse(bool bf16, bool attn, const WarpArgs &a, hipStream_t s);
+// With start / stop events the launch records them around the kernel's own
+// execution (hipExtLaunchKernelGGL).
+hipError_t warp_fuse(bool bf16, bool attn, const WarpArgs &a, hipStream_t s, hipEvent_t start = nullptr,
+                     hipEvent_t stop = nullptr);
 
 // Warp as the last node of a branch: one agent's slot resampled on the ego
 // grid (the sampling of warp_fuse) and stored in the activation dtype.
@@ -121,7 +124,8 @@ struct WarpSlotArgs {
     void *out;         // [H2*W2][C]
     int32_t H2, W2, C;
 };
-hipError_t warp_slot(bool bf16, const WarpSlotArgs &a, hipStream_t s);
+hipError_t warp_slot(bool bf16, const WarpSlotArgs &a, hipStream_t s, hipEvent_t start = nullptr,
+                     hipEvent_t stop = nullptr);
 
 // Fusion (the fold of warp_fuse) of K stored ego-frame maps.
 struct FuseArgs {
@@ -129,7 +133,8 @@ struct FuseArgs {
     void *fused;           // [cells][C]
     int32_t K, cells, C;
 };
-hipError_t fuse(bool bf16, bool attn, const FuseArgs &a, hipStream_t s);
+hipError_t fuse(bool bf16, bool attn, const FuseArgs &a, hipStream_t s, hipEvent_t start = nullptr,
+                hipEvent_t stop = nullptr);
 
 // 1x1 head: out[m][16] float32 = bias + Bt[16][C] . in[m][C].
 hipError_t head1x1(bool bf16, const void *in, const void *wt, const float *bias, float *out,

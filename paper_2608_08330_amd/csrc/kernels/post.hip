@@ -19,6 +19,8 @@
 // decode: tile counts of kept anchors, one-block scan of the tile counts,
 //   then every tile rescans its flags and writes its kept anchors in
 //   ascending anchor order (stable compaction, deterministic).
+#include <hip/hip_ext.h>
+
 #include <cmath>
 
 #include "kernels.hpp"
@@ -280,33 +282,43 @@ __global__ __launch_bounds__(256) void k_fuse(FuseArgs a) {
     store_slice<T, VEC, SPLIT>(static_cast<T *>(a.fused) + off, l, f.acc);
 }
 
+// Launch on stream s; with events, through hipExtLaunchKernelGGL so that they
+// bracket the kernel's own execution.
+template <typename F, typename A>
+void launch_timed(F kernel, unsigned g, hipStream_t s, hipEvent_t e0, hipEvent_t e1, const A &a) {
+    if (e0 || e1) hipExtLaunchKernelGGL(kernel, dim3(g), dim3(256), 0, s, e0, e1, 0, a);
+    else kernel<<<g, 256, 0, s>>>(a);
+}
+
 template <typename T, int VEC>
-hipError_t launch_warp(int kind, bool attn, const void *args, int64_t cells, hipStream_t s) {
+hipError_t launch_warp(int kind, bool attn, const void *args, int64_t cells, hipStream_t s, hipEvent_t e0,
+                       hipEvent_t e1) {
     const unsigned g = unsigned((cells * 32 + 255) / 256);
     if (kind == 0) {
         const WarpArgs &a = *static_cast<const WarpArgs *>(args);
-        if (attn) k_warp_fuse<T, VEC, true><<<g, 256, 0, s>>>(a);
-        else k_warp_fuse<T, VEC, false><<<g, 256, 0, s>>>(a);
+        if (attn) launch_timed(k_warp_fuse<T, VEC, true>, g, s, e0, e1, a);
+        else launch_timed(k_warp_fuse<T, VEC, false>, g, s, e0, e1, a);
     } else if (kind == 1) {
-        k_warp_slot<T, VEC><<<g, 256, 0, s>>>(*static_cast<const WarpSlotArgs *>(args));
+        launch_timed(k_warp_slot<T, VEC>, g, s, e0, e1, *static_cast<const WarpSlotArgs *>(args));
     } else {
         const FuseArgs &a = *static_cast<const FuseArgs *>(args);
-        if (attn) k_fuse<T, VEC, true><<<g, 256, 0, s>>>(a);
-        else k_fuse<T, VEC, false><<<g, 256, 0, s>>>(a);
+        if (attn) launch_timed(k_fuse<T, VEC, true>, g, s, e0, e1, a);
+        else launch_timed(k_fuse<T, VEC, false>, g, s, e0, e1, a);
     }
     return hipGetLastError();
 }
 
 // kind 0: warp + fusion, 1: branch warp, 2: fusion of stored maps
 template <typename T>
-hipError_t warp_dispatch(int kind, bool attn, const void *args, int C, int64_t cells, hipStream_t s) {
+hipError_t warp_dispatch(int kind, bool attn, const void *args, int C, int64_t cells, hipStream_t s,
+                         hipEvent_t e0, hipEvent_t e1) {
     switch (C) {
-        case 32: return launch_warp<T, 1>(kind, attn, args, cells, s);
-        case 64: return launch_warp<T, 2>(kind, attn, args, cells, s);
-        case 128: return launch_warp<T, 4>(kind, attn, args, cells, s);
-        case 256: return launch_warp<T, 8>(kind, attn, args, cells, s);
-        case 384: return launch_warp<T, 12>(kind, attn, args, cells, s);
-        case 512: return launch_warp<T, 16>(kind, attn, args, cells, s);
+        case 32: return launch_warp<T, 1>(kind, attn, args, cells, s, e0, e1);
+        case 64: return launch_warp<T, 2>(kind, attn, args, cells, s, e0, e1);
+        case 128: return launch_warp<T, 4>(kind, attn, args, cells, s, e0, e1);
+        case 256: return launch_warp<T, 8>(kind, attn, args, cells, s, e0, e1);
+        case 384: return launch_warp<T, 12>(kind, attn, args, cells, s, e0, e1);
+        case 512: return launch_warp<T, 16>(kind, attn, args, cells, s, e0, e1);
     }
     return hipErrorInvalidValue;
 }
@@ -447,21 +459,21 @@ __global__ __launch_bounds__(256) void k_decode_write(DecodeArgs a) {
 
 }  // namespace
 
-hipError_t warp_fuse(bool bf16, bool attn, const WarpArgs &a, hipStream_t s) {
+hipError_t warp_fuse(bool bf16, bool attn, const WarpArgs &a, hipStream_t s, hipEvent_t start, hipEvent_t stop) {
     const int64_t cells = int64_t(a.H2) * a.W2;
-    return bf16 ? warp_dispatch<uint16_t>(0, attn, &a, a.C, cells, s)
-                : warp_dispatch<float>(0, attn, &a, a.C, cells, s);
+    return bf16 ? warp_dispatch<uint16_t>(0, attn, &a, a.C, cells, s, start, stop)
+                : warp_dispatch<float>(0, attn, &a, a.C, cells, s, start, stop);
 }
 
-hipError_t warp_slot(bool bf16, const WarpSlotArgs &a, hipStream_t s) {
+hipError_t warp_slot(bool bf16, const WarpSlotArgs &a, hipStream_t s, hipEvent_t start, hipEvent_t stop) {
     const int64_t cells = int64_t(a.H2) * a.W2;
-    return bf16 ? warp_dispatch<uint16_t>(1, false, &a, a.C, cells, s)
-                : warp_dispatch<float>(1, false, &a, a.C, cells, s);
+    return bf16 ? warp_dispatch<uint16_t>(1, false, &a, a.C, cells, s, start, stop)
+                : warp_dispatch<float>(1, false, &a, a.C, cells, s, start, stop);
 }
 
-hipError_t fuse(bool bf16, bool attn, const FuseArgs &a, hipStream_t s) {
-    return bf16 ? warp_dispatch<uint16_t>(2, attn, &a, a.C, a.cells, s)
-                : warp_dispatch<float>(2, attn, &a, a.C, a.cells, s);
+hipError_t fuse(bool bf16, bool attn, const FuseArgs &a, hipStream_t s, hipEvent_t start, hipEvent_t stop) {
+    return bf16 ? warp_dispatch<uint16_t>(2, attn, &a, a.C, a.cells, s, start, stop)
+                : warp_dispatch<float>(2, attn, &a, a.C, a.cells, s, start, stop);
 }
 
 hipError_t head1x1(bool bf16, const void *in, const void *wt, const float *bias, float *out,
