@@ -16,7 +16,8 @@ Output: one JSON line with
               dense MFMA peak
   latency     p50 / p95 complete-detection latency T^det, RTCC vs barrier,
               over replayed synthetic arrival traces (pinned host inputs,
-              H2D included, as on the release path)
+              H2D included, as on the release path; contexts without node
+              events)
   cpu_baseline  the fp64 CPU oracle's encoder throughput on a bounded sample
 """
 
@@ -334,17 +335,21 @@ def main(argv=None):
             raise SystemExit("latency replay of uplink-driven configs runs in the load-sweep report")
         arr = synth.arrival_draws(cfg, a.latency_traces) * 1e-3
         # primary: one compute stream, as the paper's latency model; then the
-        # per-branch-stream executor on the same traces
-        for key, c in (("latency", ctx), ("latency_streams", ctx_t)):
+        # per-branch-stream executor on the same traces.  Both without node
+        # events, which would add their own overhead to every launch (and far
+        # more of it to the barrier, which runs every branch after A).
+        ctx_l = make_ctx("serial", False)
+        for key, c in (("latency", ctx_l), ("latency_streams", ctx_t)):
             staged = replay.stage_inputs(c, frame["points"])
             rows, identical = replay.replay_traces(c, staged, frame["poses"], arr, a.latency_reps)
             lat = replay.summarize(rows)
             lat["reps"] = a.latency_reps
-            lat["executor"] = "serial" if c is ctx else "per-branch streams"
+            lat["executor"] = "serial" if c is ctx_l else "per-branch streams"
             lat["outputs_identical_rtcc_vs_barrier"] = bool(identical)
             lat["rtcc_below_barrier_every_trace"] = bool(lat["wins_median"] == len(rows))
             out[key] = lat
             print("# %s done" % key, file=sys.stderr, flush=True)
+        ctx_l.close()
 
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, frame, a.cpu_budget)
