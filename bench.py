@@ -175,6 +175,10 @@ def main(argv=None):
                     help="place the pose warp as the last node of every branch (the join only fuses)")
     ap.add_argument("--multiscale", action="store_true",
                     help="fuse the agents at every backbone scale before upsampling")
+    ap.add_argument("--no-graphs", action="store_true",
+                    help="launch kernels one by one on the per-branch-stream executor too (by default it "
+                         "replays each branch and the join as HIP graphs; the serial executor is eager, "
+                         "graph launches on one stream being slower there)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB, 5 times "
                          "(reference for the FETCH_SIZE / WRITE_SIZE counters)")
@@ -216,6 +220,7 @@ def main(argv=None):
         o = R.rtcc_runtime_opts()
         o.exec = R.RTCC_EXEC_SERIAL if exec_kind == "serial" else R.RTCC_EXEC_PER_BRANCH_STREAMS
         o.node_timing = 1 if timing else 0
+        o.use_graphs = 1 if exec_kind == "streams" and not a.no_graphs and not timing else 0
         o.premature_tol_s = 1e-6
         return R.rtcc_create(R.model_desc(cfg), R.weights_blob(cfg, frame["weights"]), o)
 
@@ -292,6 +297,7 @@ def main(argv=None):
                 + (", multi-scale fusion" if cfg["multiscale"] else "")),
             "agents": K, "inputs": "device-resident",
             "executor": "per-branch streams" if a.exec == "streams" else "serial",
+            "hip_graphs": bool(a.exec == "streams" and not a.no_graphs),
         },
         "serial_ms_per_step": round(wall_s / rsteps * 1e3, 4),
         "roofline": {
@@ -328,6 +334,8 @@ def main(argv=None):
         out["secondary_rooflines"]["branch_warp"] = {
             "bound": "hbm", "achieved": round(2 * slot_bytes * bw_launches / (bw_ms * 1e-3) / 1e9, 1),
             "peak": PEAK_HBM_GBS, "unit": "GB/s", "traffic": measured_traffic("warp_slot")}
+    if a.exec == "streams" and not a.no_graphs:
+        out["graph_stats"] = dict(zip(("instantiated", "updates", "launches"), R.rtcc_graph_stats(ctx_t)))
     print("# throughput done: %.3f ms/step, %.1f TFLOP/s" % (ms_per_step, value), file=sys.stderr, flush=True)
 
     if a.latency_traces > 0:

@@ -58,7 +58,7 @@ extern "C" {
 #define RTCC_API
 #endif
 
-#define RTCC_ABI_VERSION 4
+#define RTCC_ABI_VERSION 5
 #define RTCC_MAX_AGENTS 16
 #define RTCC_MAX_STAGES 4
 
@@ -155,7 +155,11 @@ typedef struct rtcc_model_desc {
 
 typedef struct rtcc_runtime_opts {
     int32_t exec;          /* rtcc_exec                                              */
-    int32_t use_graphs;    /* 1: replay each branch and the join as a HIP graph      */
+    int32_t use_graphs;    /* 1: each branch's encoder (after the input copy) and the
+                              post-join subgraph (split at T^head) run as HIP graphs,
+                              captured on first use and updated in place when a
+                              branch's point count, input pointer or pose, or the
+                              join's poses, change; not while node_timing = 1          */
     int32_t node_timing;   /* 1: record HIP events around every node of every frame  */
     int32_t device;        /* HIP device ordinal                                     */
     double premature_tol_s;/* an event with arrival_t > now - t0 + tol is premature  */
@@ -297,6 +301,14 @@ RTCC_API rtcc_status rtcc_profile_nodes(rtcc_ctx *ctx, int32_t warmup, int32_t r
  * at least rtcc_node_count() floats. */
 RTCC_API rtcc_status rtcc_node_times(rtcc_ctx *ctx, float *ms, int32_t *n);
 RTCC_API rtcc_status rtcc_node_count(rtcc_ctx *ctx, int32_t *n);
+
+/* With opts.use_graphs = 1: counts[0] = HIP graphs instantiated, counts[1] =
+ * in-place updates attempted (a branch or the join whose arguments changed
+ * since its graph was captured is captured again and the executable graph
+ * updated; a failed update instantiates anew), counts[2] = graph launches,
+ * all since rtcc_create (zeros without graphs).  counts: caller-owned
+ * int64_t[3].  Errors: RTCC_E_ARG (NULL ctx or counts). */
+RTCC_API rtcc_status rtcc_graph_stats(rtcc_ctx *ctx, int64_t *counts);
 
 /* Rotated NMS of caller-provided decoded boxes, the same kernels that end
  * rtcc_join_and_detect (Sec. V-A3: decoding, score thresholding and rotated

@@ -116,6 +116,11 @@ rtcc_status rtcc_node_count(rtcc_ctx *ctx, int32_t *n) {
     return guarded([&] { return ctx->ctl.node_count(n); });
 }
 
+rtcc_status rtcc_graph_stats(rtcc_ctx *ctx, int64_t *counts) {
+    if (!ctx) return RTCC_E_ARG;
+    return guarded([&] { return ctx->ctl.graph_stats(counts); });
+}
+
 const char *rtcc_status_str(rtcc_status s) {
     switch (s) {
         case RTCC_OK: return "RTCC_OK";

@@ -24,6 +24,8 @@ rtcc_status Controller::create(const rtcc_model_desc *d, const void *weights, si
         return fail(RTCC_E_ARG, "bad exec option");
     if (!(o.premature_tol_s >= 0.0) || !std::isfinite(o.premature_tol_s))
         return fail(RTCC_E_ARG, "premature_tol_s must be finite and >= 0");
+    if ((o.use_graphs != 0 && o.use_graphs != 1) || (o.node_timing != 0 && o.node_timing != 1))
+        return fail(RTCC_E_ARG, "use_graphs and node_timing must be 0 or 1");
     opts_ = o;
     HostWeights hw;
     if (!prepare_weights(plan_, static_cast<const float *>(weights), bytes / 4, hw, err))
@@ -208,6 +210,13 @@ rtcc_status Controller::node_count(int32_t *n) {
     std::lock_guard<std::mutex> lk(mu_);
     if (!n) return fail(RTCC_E_ARG, "NULL output");
     *n = ex_->node_count();
+    return RTCC_OK;
+}
+
+rtcc_status Controller::graph_stats(int64_t out[3]) {
+    std::lock_guard<std::mutex> lk(mu_);
+    if (!out) return fail(RTCC_E_ARG, "NULL output");
+    ex_->graph_stats(out);
     return RTCC_OK;
 }
 

@@ -45,6 +45,8 @@ class Executor {
                                       std::string &err) = 0;
     virtual int node_count() const = 0;
     virtual rtcc_status node_times(float *ms, int *n, std::string &err) = 0;
+    // HIP graph instantiations, in-place update attempts and launches so far.
+    virtual void graph_stats(int64_t out[3]) const { out[0] = out[1] = out[2] = 0; }
 };
 
 // Defined by exactly one executor translation unit of a build.
@@ -77,6 +79,7 @@ class Controller {
     rtcc_status profile_nodes(int warmup, int reps, float *median_ms, int32_t *n_nodes);
     rtcc_status node_times(float *ms, int32_t *n);
     rtcc_status node_count(int32_t *n);
+    rtcc_status graph_stats(int64_t out[3]);
 
     const char *last_error() const { return err_.c_str(); }
 

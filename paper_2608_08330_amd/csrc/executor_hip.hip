@@ -135,6 +135,7 @@ class HipExecutor : public Executor {
         HIP_TRY(hipStreamCreateWithFlags(&join_stream_, hipStreamNonBlocking));
         HIP_TRY(hipStreamCreateWithFlags(&copy_stream_, hipStreamNonBlocking));
         HIP_TRY(hipStreamCreateWithFlags(&aux_stream_, hipStreamNonBlocking));
+        HIP_TRY(hipStreamCreateWithFlags(&cap_stream_, hipStreamNonBlocking));
         HIP_TRY(hipEventCreate(&ev_frame0_));
         HIP_TRY(hipEventCreate(&ev_head_));
         for (auto &e : post_ev_) HIP_TRY(hipEventCreate(&e));
@@ -191,7 +192,16 @@ class HipExecutor : public Executor {
         b.src = src;
         b.n = int32_t(n);
         b.host_input = !device_src;
-        rtcc_status s = enqueue_encoder(b, cs, timing, 1, err);
+        rtcc_status s;
+        if (o_.use_graphs && !timing) {
+            std::vector<unsigned char> key;
+            put(key, b.src);
+            put(key, b.n);
+            for (int e = 0; e < 6; ++e) put(key, b.affine[e]);
+            s = run_graph(b.graph, key, cs, [&](hipStream_t c) { return enqueue_encoder(b, c, false, 1, err); }, err);
+        } else {
+            s = enqueue_encoder(b, cs, timing, 1, err);
+        }
         if (s != RTCC_OK) return s;
         HIP_TRY(hipEventRecord(b.done, cs));
         b.dispatched = true;
@@ -207,7 +217,23 @@ class HipExecutor : public Executor {
         const bool timing = o_.node_timing != 0;
         // one-kernel fusion nodes are timed by events bracketing the kernel
         if (timing && p_.d.multiscale) HIP_TRY(hipEventRecord(post_ev_[0], js));
-        rtcc_status s = enqueue_post(affine, poses, js, timing, err);
+        rtcc_status s;
+        if (o_.use_graphs && !timing) {
+            std::vector<unsigned char> key;
+            for (int k = 0; k < p_.K; ++k) {
+                put(key, br_[k].ego_map);
+                for (int e = 0; e < 6; ++e) put(key, affine[k][e]);
+                for (int e = 0; e < 3; ++e) put(key, poses[k][e]);
+            }
+            s = run_graph(post_graph_[0], key, js,
+                          [&](hipStream_t c) { return enqueue_post_head(affine, poses, c, false, err); }, err);
+            if (s != RTCC_OK) return s;
+            HIP_TRY(hipEventRecord(ev_head_, js));
+            s = run_graph(post_graph_[1], {}, js, [&](hipStream_t c) { return enqueue_post_detect(c, false, err); },
+                          err);
+        } else {
+            s = enqueue_post(affine, poses, js, timing, err);
+        }
         if (s != RTCC_OK) return s;
         int32_t *hs = reinterpret_cast<int32_t *>(h_small);
         HIP_TRY(hipMemcpyAsync(hs, d_count, 4, hipMemcpyDeviceToHost, js));
@@ -341,7 +367,73 @@ class HipExecutor : public Executor {
         return RTCC_OK;
     }
 
+    void graph_stats(int64_t out[3]) const override {
+        for (int i = 0; i < 3; ++i) out[i] = graph_stats_[i];
+    }
+
   private:
+    // A captured sequence of kernel launches and the key (the arguments that
+    // vary between frames) it was captured with.
+    struct Graph {
+        hipGraph_t g = nullptr;
+        hipGraphExec_t x = nullptr;
+        std::vector<unsigned char> key;
+    };
+    static void drop(Graph &gr) {
+        if (gr.x) (void)hipGraphExecDestroy(gr.x);
+        if (gr.g) (void)hipGraphDestroy(gr.g);
+        gr.x = nullptr;
+        gr.g = nullptr;
+        gr.key.clear();
+    }
+    template <class T>
+    static void put(std::vector<unsigned char> &key, const T &v) {
+        const unsigned char *b = reinterpret_cast<const unsigned char *>(&v);
+        key.insert(key.end(), b, b + sizeof(T));
+    }
+    // Launch `gr` on stream s.  If it was captured for another key, capture
+    // the launches again on the capture stream and update the executable
+    // graph in place (the same kernels with other arguments or grids); a
+    // graph of another shape, or the first one, is instantiated.
+    // `enqueue(stream)` issues kernel launches only (no memset, copy or wait).
+    template <class F>
+    rtcc_status run_graph(Graph &gr, const std::vector<unsigned char> &key, hipStream_t s, F &&enqueue,
+                          std::string &err) {
+        if (!gr.x || gr.key != key) {
+            HIP_TRY(hipStreamBeginCapture(cap_stream_, hipStreamCaptureModeRelaxed));
+            const rtcc_status st = enqueue(cap_stream_);
+            hipGraph_t g = nullptr;
+            const hipError_t e = hipStreamEndCapture(cap_stream_, &g);
+            if (st != RTCC_OK || e != hipSuccess) {
+                if (g) (void)hipGraphDestroy(g);
+                drop(gr);
+                if (st != RTCC_OK) return st;
+                HIP_TRY(e);
+            }
+            bool updated = false;
+            if (gr.x) {
+                hipGraphNode_t bad = nullptr;
+                hipGraphExecUpdateResult res = hipGraphExecUpdateError;
+                updated = hipGraphExecUpdate(gr.x, g, &bad, &res) == hipSuccess && res == hipGraphExecUpdateSuccess;
+                (void)hipGetLastError();
+                ++graph_stats_[1];
+            }
+            if (updated) {
+                (void)hipGraphDestroy(gr.g);
+                gr.g = g;
+            } else {
+                drop(gr);
+                gr.g = g;
+                HIP_TRY(hipGraphInstantiate(&gr.x, g, nullptr, nullptr, 0));
+                ++graph_stats_[0];
+            }
+            gr.key = key;
+        }
+        HIP_TRY(hipGraphLaunch(gr.x, s));
+        ++graph_stats_[2];
+        return RTCC_OK;
+    }
+
     struct Branch {
         float *staging = nullptr;
         void *d_pts = nullptr, *d_cell = nullptr, *d_slot = nullptr, *d_member = nullptr;
@@ -353,6 +445,7 @@ class HipExecutor : public Executor {
         float affine[6] = {1, 0, 0, 0, 1, 0};
         bool warp_ran = false;           // the last frame ran a branch warp kernel
         hipEvent_t wev[2] = {nullptr, nullptr};  // bracket the branch warp kernel
+        Graph graph;                     // the encoder as a HIP graph (use_graphs)
         std::vector<void *> d_act;
         hipStream_t stream = nullptr;
         hipEvent_t done = nullptr, h2d_done = nullptr;
@@ -515,9 +608,19 @@ class HipExecutor : public Executor {
         return kern::deconv(p.bf16, ga, s);
     }
 
+    // Post-join subgraph: warp + fusion and head, T^head, then decode and NMS.
     rtcc_status enqueue_post(const std::vector<std::array<float, 6>> &affine,
                              const std::vector<std::array<float, 3>> &poses, hipStream_t s, bool timing,
                              std::string &err) {
+        rtcc_status st = enqueue_post_head(affine, poses, s, timing, err);
+        if (st != RTCC_OK) return st;
+        HIP_TRY(hipEventRecord(ev_head_, s));
+        return enqueue_post_detect(s, timing, err);
+    }
+
+    rtcc_status enqueue_post_head(const std::vector<std::array<float, 6>> &affine,
+                                  const std::vector<std::array<float, 3>> &poses, hipStream_t s, bool timing,
+                                  std::string &err) {
         const Plan &p = p_;
         if (p.d.multiscale) {
             // every scale: warp the K stage maps onto the stage's ego grid and
@@ -563,8 +666,12 @@ class HipExecutor : public Executor {
         HIP_TRY(kern::head1x1(p.bf16, d_fused, static_cast<const char *>(d_mat) + p.head_w_off * p.elt,
                               static_cast<const float *>(d_bias) + p.head_b_off, static_cast<float *>(d_head),
                               p.H2 * p.W2, p.c_slot, s));
-        HIP_TRY(hipEventRecord(ev_head_, s));
         if (timing) HIP_TRY(hipEventRecord(post_ev_[2], s));
+        return RTCC_OK;
+    }
+
+    rtcc_status enqueue_post_detect(hipStream_t s, bool timing, std::string &err) {
+        const Plan &p = p_;
         kern::DecodeArgs da{};
         da.head = static_cast<const float *>(d_head);
         da.H2 = p.H2;
@@ -712,6 +819,7 @@ class HipExecutor : public Executor {
                 if (e) (void)hipEventDestroy(e);
             for (hipEvent_t e : b.wev)
                 if (e) (void)hipEventDestroy(e);
+            drop(b.graph);
         }
         for (void *ptr : dev_allocs_) (void)hipFree(ptr);
         if (h_rec) (void)hipHostFree(h_rec);
@@ -719,6 +827,8 @@ class HipExecutor : public Executor {
         if (join_stream_) (void)hipStreamDestroy(join_stream_);
         if (copy_stream_) (void)hipStreamDestroy(copy_stream_);
         if (aux_stream_) (void)hipStreamDestroy(aux_stream_);
+        for (Graph &g : post_graph_) drop(g);
+        if (cap_stream_) (void)hipStreamDestroy(cap_stream_);
         if (ev_frame0_) (void)hipEventDestroy(ev_frame0_);
         if (ev_head_) (void)hipEventDestroy(ev_head_);
         for (hipEvent_t e : post_ev_)
@@ -748,6 +858,9 @@ class HipExecutor : public Executor {
     std::vector<std::array<float, 6>> last_affine_;
     std::vector<std::array<float, 3>> last_poses_;
     std::vector<void *> d_fused_stage_;  // multi-scale: fused map of every stage
+    hipStream_t cap_stream_ = nullptr;   // where graphs are captured (use_graphs)
+    Graph post_graph_[2];                // post-join: up to T^head, then decode and NMS
+    int64_t graph_stats_[3] = {0, 0, 0}; // instantiations, update attempts, launches
 };
 
 Executor *make_executor() { return new HipExecutor(); }

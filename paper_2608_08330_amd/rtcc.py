@@ -20,7 +20,7 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_DIR = os.path.join(HERE, "lib")
 
-RTCC_ABI_VERSION = 4
+RTCC_ABI_VERSION = 5
 RTCC_MAX_AGENTS = 16
 RTCC_MAX_STAGES = 4
 
@@ -116,7 +116,7 @@ EXPORTS = (
     "rtcc_create", "rtcc_destroy", "rtcc_set_mode", "rtcc_staging_buffer", "rtcc_begin_frame",
     "rtcc_release_branch", "rtcc_release_branch_device", "rtcc_join_and_detect",
     "rtcc_get_branch_state", "rtcc_tensor_bytes", "rtcc_get_tensor", "rtcc_profile_nodes",
-    "rtcc_node_times", "rtcc_node_count", "rtcc_rotated_nms", "rtcc_uplink_emulate", "rtcc_schedule_model",
+    "rtcc_node_times", "rtcc_node_count", "rtcc_graph_stats", "rtcc_rotated_nms", "rtcc_uplink_emulate", "rtcc_schedule_model",
     "rtcc_upward_rank", "rtcc_status_str", "rtcc_last_error",
 )
 
@@ -150,6 +150,7 @@ def _declare(lib):
         "rtcc_profile_nodes": (S, [_P, ctypes.c_int32, ctypes.c_int32, _F, ctypes.POINTER(ctypes.c_int32)]),
         "rtcc_node_times": (S, [_P, _F, ctypes.POINTER(ctypes.c_int32)]),
         "rtcc_node_count": (S, [_P, ctypes.POINTER(ctypes.c_int32)]),
+        "rtcc_graph_stats": (S, [_P, ctypes.POINTER(ctypes.c_int64)]),
         "rtcc_rotated_nms": (S, [_P, ctypes.c_int64, ctypes.c_int32, ctypes.c_float, _P,
                                  ctypes.POINTER(ctypes.c_int64)]),
         "rtcc_uplink_emulate": (S, [ctypes.POINTER(rtcc_uplink_desc), _P, _P, _P, _P, _P]),
@@ -465,6 +466,13 @@ def rtcc_node_count(ctx):
     n = ctypes.c_int32()
     ctx.check(ctx.lib.rtcc_node_count(ctx.handle, ctypes.byref(n)))
     return n.value
+
+
+def rtcc_graph_stats(ctx):
+    """(instantiated, update attempts, launches) of the context's HIP graphs."""
+    out = (ctypes.c_int64 * 3)()
+    ctx.check(ctx.lib.rtcc_graph_stats(ctx.handle, out))
+    return tuple(out)
 
 
 def rtcc_node_times(ctx):

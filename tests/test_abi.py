@@ -266,3 +266,20 @@ def test_multiscale_needs_upsampling_and_a_post_join_warp():
     cfg = dict(synth.config("t_attn"), multiscale=True)
     fr = synth.make_frame("t_attn")
     R.rtcc_create(R.model_desc(cfg), R.weights_blob(cfg, fr["weights"]), kind="host").close()
+
+
+@pytest.mark.parametrize("field,value", [("use_graphs", 2), ("use_graphs", -1), ("node_timing", 3)])
+def test_bad_runtime_opts_rejected(field, value):
+    cfg = synth.config("t_max")
+    w = R.weights_blob(cfg, synth.make_weights(cfg))
+    o = R.rtcc_runtime_opts()
+    o.exec = R.RTCC_EXEC_PER_BRANCH_STREAMS
+    o.premature_tol_s = 1e-6
+    setattr(o, field, value)
+    with pytest.raises(R.RtccError) as ei:
+        R.rtcc_create(R.model_desc(cfg), w, o, kind="host")
+    assert ei.value.status == R.RTCC_E_ARG
+    o.use_graphs, o.node_timing = 1, 0
+    ctx = R.rtcc_create(R.model_desc(cfg), w, o, kind="host")
+    assert R.rtcc_graph_stats(ctx) == (0, 0, 0)   # the recording executor runs no graphs
+    ctx.close()
