@@ -35,6 +35,8 @@
 
 #include <hip/hip_ext.h>
 
+#include <type_traits>
+
 namespace rtcc {
 namespace kern {
 
@@ -71,7 +73,8 @@ template <typename T>
 struct Traits;
 template <>
 struct Traits<uint16_t> {
-    static constexpr int EPV = 8;  // elements per 16-byte vector
+    static constexpr int EPV = 8;    // elements per 16-byte vector
+    static constexpr int MFMAS = 1;  // MFMA instructions per mma()
     __device__ static inline f32x4_t mma(uint4 a, uint4 b, f32x4_t c) {
         return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
                                                        __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
@@ -92,6 +95,7 @@ struct Traits<uint16_t> {
 template <>
 struct Traits<float> {
     static constexpr int EPV = 4;
+    static constexpr int MFMAS = 4;
     __device__ static inline f32x4_t mma(uint4 a, uint4 b, f32x4_t c) {
         // lane group g holds k = 4g .. 4g+3 of both operands; the four
         // MFMAs sum k = e, 4 + e, 8 + e, 12 + e for e = 0..3
@@ -116,6 +120,67 @@ __device__ inline void load_lds16(const void *g, uint32_t lds_addr) {
     const uint32_t a = __builtin_amdgcn_readfirstlane(lds_addr);
     asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(a)
                  : "memory", "m0");
+}
+
+// Scheduling hint for the scheduler of the step that follows: NR LDS reads
+// spread evenly between NM MFMAs (MFMAs first), so that neither the LDS
+// queue nor the matrix pipe idles behind the other in issue order.
+template <int NR, int NM, int I = 0>
+__device__ inline void interleave_reads() {
+    if constexpr (I < NR) {
+        constexpr int q = (NM * (I + 1)) / NR - (NM * I) / NR;
+        if constexpr (q > 0) __builtin_amdgcn_sched_group_barrier(0x008, q, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                        // LDS read
+        interleave_reads<NR, NM, I + 1>();
+    }
+}
+
+// 16 bytes to global memory with the non-temporal hint: outputs are read
+// by the next kernel, not by this one, and stream past the L2.
+__device__ inline void store16_nt(void *p, uint4 v) {
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    __builtin_nontemporal_store(u32x4{v.x, v.y, v.z, v.w}, static_cast<u32x4 *>(p));
+}
+
+// Epilogue through LDS.  Every lane first writes its ReLU(acc + bias)
+// values (four consecutive channels of one pixel) into a [pixels][BN] tile
+// in `stage` (rows padded by 16 bytes), then the block writes the tile out
+// as whole 16-byte vectors of each pixel's BN-channel row: every pixel's
+// row is one contiguous run of BN * elt bytes in global memory.  `pix(p)`
+// gives the global element offset of tile pixel p's channel n0, or -1 to
+// skip it.  Called by every thread of the block (it holds two barriers);
+// `holds` is false for threads that hold no accumulators.
+template <typename T, int NPIX, int BN, int NT, int FM, int FN, typename PixF, typename RowF, typename ChF>
+__device__ inline void staged_store(unsigned char *stage, const f32x4_t (&acc)[FM][FN], bool holds, const float *bias,
+                                    int n0, T *out, PixF pix, RowF row_of, ChF ch_of, int tid) {
+    constexpr int RS = BN * int(sizeof(T)) + 16;
+    __syncthreads();  // every wave is done with the LDS it staged operands in
+    if (holds) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+                const int p = row_of(i), ch = ch_of(j);
+                const int n = n0 + ch;
+                Traits<T>::store4(reinterpret_cast<T *>(stage + p * RS) + ch, fmaxf(acc[i][j][0] + bias[n + 0], 0.f),
+                                  fmaxf(acc[i][j][1] + bias[n + 1], 0.f), fmaxf(acc[i][j][2] + bias[n + 2], 0.f),
+                                  fmaxf(acc[i][j][3] + bias[n + 3], 0.f));
+            }
+        }
+    }
+    __syncthreads();
+    constexpr int VPP = BN * int(sizeof(T)) / 16;  // 16-byte vectors per pixel row
+    constexpr int NV = NPIX * VPP;
+#pragma unroll
+    for (int q = 0; q < (NV + NT - 1) / NT; ++q) {
+        const int v = tid + q * NT;
+        if (v >= NV) break;
+        const int p = v / VPP, part = v - (v / VPP) * VPP;
+        const int64_t off = pix(p);
+        if (off < 0) continue;
+        store16_nt(reinterpret_cast<uint4 *>(out + off) + part,
+                   *reinterpret_cast<const uint4 *>(stage + p * RS + part * 16));
+    }
 }
 
 template <typename T, int BM, int BN, int WGM, int WGN, int STAGES, bool DECONV>
@@ -292,28 +357,43 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_igemm(GemmArgs a) {
     }
     T *out = static_cast<T *>(a.out);
     const int py = DECONV ? phase / a.u : 0, px = DECONV ? phase - py * a.u : 0;
-#pragma unroll
-    for (int i = 0; i < FM; ++i) {
-        const int m = m0 + wm * WM + i * 16 + fr;
-        if (m >= M) continue;
-        size_t pix;
+    // global element offset of tile row p (channel n0), -1 outside the output
+    auto pix = [&](int p) -> int64_t {
+        const int m = m0 + p;
+        if (m >= M) return -1;
+        size_t q;
         if (DECONV) {
             const int iy = m / a.Wi, ix = m - (m / a.Wi) * a.Wi;
             const int oy = iy * a.u + py, ox = ix * a.u + px;
-            if (oy >= a.Ho || ox >= a.Wo) continue;
-            pix = size_t(oy) * a.Wo + ox;
+            if (oy >= a.Ho || ox >= a.Wo) return -1;
+            q = size_t(oy) * a.Wo + ox;
         } else {
-            pix = size_t(m);
+            q = size_t(m);
         }
+        return int64_t(q * a.ldo + a.c_off + n0);
+    };
+    constexpr int RS = BN * int(sizeof(T)) + 16;
+    if constexpr (BM * RS <= STAGES * STAGE_BYTES) {
+        if (n0 + BN <= N) {
+            staged_store<T, BM, BN, 64 * NW, FM, FN>(
+                smem, acc, true, a.bias, n0, out, pix, [&](int i) { return wm * WM + i * 16 + fr; },
+                [&](int j) { return wn * WN + j * 16 + fk * 4; }, tid);
+            return;
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+        const int64_t off = pix(wm * WM + i * 16 + fr);
+        if (off < 0) continue;
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
-            const int n = n0 + wn * WN + j * 16 + fk * 4;
+            const int ch = wn * WN + j * 16 + fk * 4, n = n0 + ch;
             if (n >= N) continue;
             const float v0 = fmaxf(acc[i][j][0] + a.bias[n + 0], 0.f);
             const float v1 = fmaxf(acc[i][j][1] + a.bias[n + 1], 0.f);
             const float v2 = fmaxf(acc[i][j][2] + a.bias[n + 2], 0.f);
             const float v3 = fmaxf(acc[i][j][3] + a.bias[n + 3], 0.f);
-            Traits<T>::store4(out + pix * a.ldo + a.c_off + n, v0, v1, v2, v3);
+            Traits<T>::store4(out + off + ch, v0, v1, v2, v3);
         }
     }
 }
@@ -337,7 +417,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_igemm(GemmArgs a) {
 // once step s's weights have landed, the loads still allowed in flight are
 // the weights of the next R - 2 steps plus, at taps 1 .. R - 1, the next
 // chunk's patch (issued at tap 0 after the weights of step s + R - 1).
-template <typename T, int TH, int BN, int WGM, int WGN, int RB, int STRIDE, int KG, int R>
+template <typename T, int TH, int BN, int WGM, int WGN, int RB, int STRIDE, int KG, int R, bool ILV>
 __global__ __launch_bounds__(64 * WGM * WGN * KG) void k_conv3s1(GemmArgs a) {
     constexpr int NW = WGM * WGN;  // wavefronts per group
     constexpr int EPV = Traits<T>::EPV;
@@ -457,51 +537,90 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void k_conv3s1(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) b_row[j] = wn * (BN / WGN) + j * 16 + fr;
 
+    // MFMA operands of one step, read from LDS a step ahead of their use
+    struct Frag {
+        uint4 a[KS][FM], b[KS][FN];
+    };
+    // step (chunk c, tap t): patch buffer c & 1, weight buffer s % R
+    auto read_frags = [&](Frag &f, int c, int t, int s) {
+        const unsigned char *pa = gsmem + (c & 1) * A_BYTES;
+        const unsigned char *pb = gsmem + 2 * A_BYTES + (s % R) * B_BYTES;
+        const int dy = t / 3, dx = t % 3;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            const int v = fk + 4 * ks;
+#pragma unroll
+            for (int i = 0; i < FM; ++i) {
+                const int col = STRIDE == 1 ? dx + fr : ((dx & 1) ? EVEN : dx >> 1) + fr;
+                const int r = (STRIDE * (wm * FM + i) + dy) * HW + col;
+                f.a[ks][i] = *reinterpret_cast<const uint4 *>(pa + r * RB + ((v ^ swz(r)) << 4));
+            }
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+                f.b[ks][j] = *reinterpret_cast<const uint4 *>(pb + b_row[j] * RB + ((v ^ swz(b_row[j])) << 4));
+        }
+    };
+
+    // Prologue: the first patch and the weights of steps 0 .. R-1; once the
+    // patch and step 0's weights have landed, step 0's operands are read.
     const int S = CH * 9;
     issue_patch(0);
 #pragma unroll
-    for (int q = 0; q + 1 < R; ++q)
+    for (int q = 0; q < R; ++q)
         if (q < S) issue_w(q);
-    for (int c = 0; c < CH; ++c) {
-        const bool last = c + 1 == CH;
-        const unsigned char *pa = gsmem + (c & 1) * A_BYTES;
-#pragma unroll
-        for (int t = 0; t < 9; ++t) {
-            const int s = c * 9 + t;
-            // loads allowed in flight once step s's weights are in: the
-            // weights of the next R - 2 steps (fewer near the end) and, at
-            // taps 1 .. R - 1, the next chunk's patch
-            if (!last) vm_wait<(R - 2) * LB + LA>((R - 2) * LB + (t >= 1 && t <= R - 1 ? LA : 0));
-            else vm_wait<(R - 2) * LB>((8 - t < R - 2 ? 8 - t : R - 2) * LB);
-            // the weight buffer of step s - 1 (and at tap 0 the patch buffer
-            // of chunk c - 1) is refilled right after this barrier
+    vm_wait<(R - 1) * LB>((S - 1 < R - 1 ? S - 1 : R - 1) * LB);
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    Frag cur, nxt;
+    read_frags(cur, 0, 0, 0);
+    // Step s = 9 c + t (chunk c, tap t; LAST: c is the group's last chunk):
+    // wait for step s + 1's operands to land, barrier, refill the weight
+    // buffer of step s (whose operands every wave has read) with step
+    // s + R, at tap 0 also the other patch buffer with chunk c + 1, read
+    // step s + 1's operands and run step s's MFMAs on the operands read
+    // during the previous step.
+    auto step = [&](auto tc, auto lastc, int c) {
+        constexpr int t = decltype(tc)::value;
+        constexpr bool last = decltype(lastc)::value;
+        constexpr bool more = !(last && t == 8);
+        const int s = c * 9 + t;
+        if constexpr (more) {
+            // still in flight once step s + 1's weights (and at tap 8 the
+            // next patch, issued before them) have landed: the weights of
+            // steps s + 2 .. s + R - 1 (fewer near the end) and, at taps
+            // 1 .. R - 2, the next chunk's patch
+            if constexpr (!last) vm_wait<(R - 2) * LB + LA>((R - 2) * LB + (t >= 1 && t <= R - 2 ? LA : 0));
+            else vm_wait<(R - 2) * LB>((7 - t < R - 2 ? 7 - t : R - 2) * LB);
             lds_reads_done();
             __builtin_amdgcn_s_barrier();
             asm volatile("" ::: "memory");
-            if (s + R - 1 < S) issue_w(s + R - 1);
-            if (t == 0 && !last) issue_patch(c + 1);
-            const int dy = t / 3, dx = t % 3;
-            const unsigned char *pb = gsmem + 2 * A_BYTES + (s % R) * B_BYTES;
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                const int v = fk + 4 * ks;
-                uint4 af[FM], bfr[FN];
-#pragma unroll
-                for (int i = 0; i < FM; ++i) {
-                    const int col = STRIDE == 1 ? dx + fr : ((dx & 1) ? EVEN : dx >> 1) + fr;
-                    const int r = (STRIDE * (wm * FM + i) + dy) * HW + col;
-                    af[i] = *reinterpret_cast<const uint4 *>(pa + r * RB + ((v ^ swz(r)) << 4));
-                }
-#pragma unroll
-                for (int j = 0; j < FN; ++j)
-                    bfr[j] = *reinterpret_cast<const uint4 *>(pb + b_row[j] * RB + ((v ^ swz(b_row[j])) << 4));
-#pragma unroll
-                for (int i = 0; i < FM; ++i)
-#pragma unroll
-                    for (int j = 0; j < FN; ++j) acc[i][j] = Traits<T>::mma(bfr[j], af[i], acc[i][j]);
-            }
+            if constexpr (!last || t + R < 9) issue_w(s + R);
+            if constexpr (t == 0 && !last) issue_patch(c + 1);
+            if constexpr (t < 8) read_frags(nxt, c, t + 1, s + 1);
+            else read_frags(nxt, c + 1, 0, s + 1);
         }
-    }
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j) acc[i][j] = Traits<T>::mma(cur.b[ks][j], cur.a[ks][i], acc[i][j]);
+        if constexpr (more && ILV) interleave_reads<KS * (FM + FN), KS * FM * FN * Traits<T>::MFMAS>();
+        cur = nxt;
+    };
+    auto chunk = [&](auto lastc, int c) {
+        step(std::integral_constant<int, 0>{}, lastc, c);
+        step(std::integral_constant<int, 1>{}, lastc, c);
+        step(std::integral_constant<int, 2>{}, lastc, c);
+        step(std::integral_constant<int, 3>{}, lastc, c);
+        step(std::integral_constant<int, 4>{}, lastc, c);
+        step(std::integral_constant<int, 5>{}, lastc, c);
+        step(std::integral_constant<int, 6>{}, lastc, c);
+        step(std::integral_constant<int, 7>{}, lastc, c);
+        step(std::integral_constant<int, 8>{}, lastc, c);
+    };
+    for (int c = 0; c + 1 < CH; ++c) chunk(std::false_type{}, c);
+    chunk(std::true_type{}, CH - 1);
 
     if constexpr (KG > 1) {
         // every wave has read its last LDS operands and every DMA load has
@@ -519,18 +638,38 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void k_conv3s1(GemmArgs a) {
                     for (int q = 0; q < 4; ++q) dst[((i * FN + j) * 4 + q) * 64 + lane] = acc[i][j][q];
         }
         __syncthreads();
-        if (grp > 0) return;
-        for (int g = 1; g < KG; ++g) {
-            const float *src = red + ((g - 1) * NW + wave) * 64 * E;
+        if (grp == 0) {
+            for (int g = 1; g < KG; ++g) {
+                const float *src = red + ((g - 1) * NW + wave) * 64 * E;
 #pragma unroll
-            for (int i = 0; i < FM; ++i)
+                for (int i = 0; i < FM; ++i)
 #pragma unroll
-                for (int j = 0; j < FN; ++j)
+                    for (int j = 0; j < FN; ++j)
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) acc[i][j][q] += src[((i * FN + j) * 4 + q) * 64 + lane];
+                        for (int q = 0; q < 4; ++q) acc[i][j][q] += src[((i * FN + j) * 4 + q) * 64 + lane];
+            }
         }
     }
 
+    // Group 0 holds the block's accumulators.
+    constexpr int RS = BN * int(sizeof(T)) + 16;
+    if constexpr (TH * TW * RS <= KG * G_BYTES) {
+        if (a.splits == 1) {
+            // the staging tile overwrites the reduction area: staged_store
+            // starts with a barrier, after group 0 has read it
+            staged_store<T, TH * TW, BN, 64 * NW * KG, FM, FN>(
+                smem, acc, grp == 0, a.bias, n0, static_cast<T *>(a.out),
+                [&](int p) -> int64_t {
+                    const int oy = oy0 + p / TW, ox = ox0 + p % TW;
+                    if (oy >= Ho || ox >= Wo) return -1;
+                    return int64_t((size_t(oy) * Wo + ox) * a.ldo + a.c_off + n0);
+                },
+                [&](int i) { return (wm * FM + i) * TW + fr; },
+                [&](int j) { return wn * (BN / WGN) + j * 16 + fk * 4; }, tid);
+            return;
+        }
+    }
+    if (grp > 0) return;
     const int ox = ox0 + fr;
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
@@ -598,12 +737,11 @@ hipError_t launch_cfg(const GemmArgs &a, hipStream_t s, hipEvent_t e0 = nullptr,
     return launch_kernel(k_splitk_reduce<T>, dim3(unsigned((total + 255) / 256)), dim3(256), s, nullptr, e1, a);
 }
 
-template <typename T, int TH, int BN = 128, int WGM = 4, int WGN = 2, int RB = 64, int STRIDE = 1, int KG = 1,
-          int R = 3>
+template <typename T, int TH, int BN, int WGM, int WGN, int RB, int STRIDE, int KG, int R, bool ILV>
 hipError_t launch_halo(const GemmArgs &a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr) {
     const unsigned tiles = unsigned((a.Wo + 15) / 16) * unsigned((a.Ho + TH - 1) / TH);
     const unsigned nx = tiles * unsigned(a.N / BN) * unsigned(a.splits);
-    hipError_t e = launch_kernel(k_conv3s1<T, TH, BN, WGM, WGN, RB, STRIDE, KG, R>, dim3(nx),
+    hipError_t e = launch_kernel(k_conv3s1<T, TH, BN, WGM, WGN, RB, STRIDE, KG, R, ILV>, dim3(nx),
                                  dim3(64 * WGM * WGN * KG), s, e0, a.splits == 1 ? e1 : nullptr, a);
     if (e != hipSuccess || a.splits == 1) return e;
     const int64_t total = int64_t(a.Ho) * a.Wo * (a.N / 4);
@@ -615,20 +753,22 @@ hipError_t launch(const GemmArgs &a, hipStream_t s, hipEvent_t e0 = nullptr, hip
     if (!DECONV) {
         // 128-byte K steps pay off from 256 input channels (bf16) on
         const bool rb128 = (a.Ci * int(sizeof(T))) % 128 == 0 && a.Ci * int(sizeof(T)) >= 512;
+        // template arguments: TH, BN, WGM, WGN, RB, STRIDE, KG, weight ring
+        // depth R, interleaved LDS reads; R and the interleaving as they
+        // measured fastest at the c5 shapes
         switch (a.variant) {
-            // weight ring depth R: 4 where it measured faster at the c5 shapes
             case kConvHalo8:
-                return rb128 ? launch_halo<T, 8, 128, 4, 2, 128, 1, 1, 4>(a, s, e0, e1)
-                             : launch_halo<T, 8, 128, 4, 2, 64, 1, 1, 4>(a, s, e0, e1);
+                return rb128 ? launch_halo<T, 8, 128, 4, 2, 128, 1, 1, 4, true>(a, s, e0, e1)
+                             : launch_halo<T, 8, 128, 4, 2, 64, 1, 1, 4, false>(a, s, e0, e1);
             case kConvHalo4:
-                return rb128 ? launch_halo<T, 4, 128, 2, 2, 128, 1>(a, s, e0, e1)
-                             : launch_halo<T, 4, 128, 2, 2, 64, 1>(a, s, e0, e1);
-            case kConvHalo8S2: return launch_halo<T, 8, 128, 4, 2, 64, 2, 1, 4>(a, s, e0, e1);
-            case kConvHalo4S2: return launch_halo<T, 4, 128, 4, 2, 64, 2>(a, s, e0, e1);
+                return rb128 ? launch_halo<T, 4, 128, 2, 2, 128, 1, 1, 3, true>(a, s, e0, e1)
+                             : launch_halo<T, 4, 128, 2, 2, 64, 1, 1, 3, true>(a, s, e0, e1);
+            case kConvHalo8S2: return launch_halo<T, 8, 128, 4, 2, 64, 2, 1, 4, true>(a, s, e0, e1);
+            case kConvHalo4S2: return launch_halo<T, 4, 128, 4, 2, 64, 2, 1, 3, true>(a, s, e0, e1);
             case kConvHalo4N64K2:
-                return rb128 ? launch_halo<T, 4, 64, 2, 2, 128, 1, 2>(a, s, e0, e1)
-                             : launch_halo<T, 4, 64, 2, 2, 64, 1, 2>(a, s, e0, e1);
-            case kConvHalo4S2N64K2: return launch_halo<T, 4, 64, 2, 2, 64, 2, 2, 4>(a, s, e0, e1);
+                return rb128 ? launch_halo<T, 4, 64, 2, 2, 128, 1, 2, 4, true>(a, s, e0, e1)
+                             : launch_halo<T, 4, 64, 2, 2, 64, 1, 2, 3, true>(a, s, e0, e1);
+            case kConvHalo4S2N64K2: return launch_halo<T, 4, 64, 2, 2, 64, 2, 2, 4, false>(a, s, e0, e1);
             default: break;
         }
     }
