@@ -220,6 +220,13 @@ __global__ __launch_bounds__(256) void k_overfull_select(const int32_t *__restri
     }
 }
 
+// 16 bytes with the non-temporal hint: the canvas is read by the backbone,
+// not by this kernel.
+__device__ inline void nt_store16(void *p, uint4 v) {
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    __builtin_nontemporal_store(u32x4{v.x, v.y, v.z, v.w}, static_cast<u32x4 *>(p));
+}
+
 __device__ inline uint32_t pack_bf16x2(float a, float b) {
     uint32_t ua = __float_as_uint(a), ub = __float_as_uint(b);
     ua += 0x7fffu + ((ua >> 16) & 1u);
@@ -275,11 +282,13 @@ __global__ __launch_bounds__(256) void k_pfn_canvas(PfnArgs a) {
         o.y = pack_bf16x2(mx[2], mx[3]);
         o.z = pack_bf16x2(mx[4], mx[5]);
         o.w = pack_bf16x2(mx[6], mx[7]);
-        *reinterpret_cast<uint4 *>(static_cast<uint16_t *>(a.canvas) + size_t(cell) * a.C + ch) = o;
+        nt_store16(static_cast<uint16_t *>(a.canvas) + size_t(cell) * a.C + ch, o);
     } else {
-        float4 *dst = reinterpret_cast<float4 *>(static_cast<float *>(a.canvas) + size_t(cell) * a.C + ch);
-        dst[0] = make_float4(mx[0], mx[1], mx[2], mx[3]);
-        dst[1] = make_float4(mx[4], mx[5], mx[6], mx[7]);
+        float *dst = static_cast<float *>(a.canvas) + size_t(cell) * a.C + ch;
+        nt_store16(dst, make_uint4(__float_as_uint(mx[0]), __float_as_uint(mx[1]), __float_as_uint(mx[2]),
+                                   __float_as_uint(mx[3])));
+        nt_store16(dst + 4, make_uint4(__float_as_uint(mx[4]), __float_as_uint(mx[5]), __float_as_uint(mx[6]),
+                                       __float_as_uint(mx[7])));
     }
 }
 
