@@ -41,9 +41,9 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 # commands in profiles/traffic_c5_bench.md).  Each figure holds only for the
 # kernel source it was taken on; after a change it reads null until re-taken.
 MEASURED_TRAFFIC = {
-    "conv": dict(src="paper_2608_08330_amd/csrc/kernels/igemm.hip", bytes=26.77e6,
-                 sha256="c344b6046ed2bdf9191513bbc9f4229dfac31992b8be9a50b15e9f7851d1aef1"),
-    "warp_fuse": dict(src="paper_2608_08330_amd/csrc/kernels/post.hip", bytes=488.83e6,
+    "conv": dict(src="paper_2608_08330_amd/csrc/kernels/igemm.hip", bytes=26.73e6,
+                 sha256="90a6cec7ffbd0011ebff14ca9359e122b8c5e344f748a4d9bd13a4c0845ad1f9"),
+    "warp_fuse": dict(src="paper_2608_08330_amd/csrc/kernels/post.hip", bytes=486.12e6,
                       sha256="d9e47ed29b6c1248a27c5f4d72953ae5f87db05b42e23cc2f803da37fb5acbc7"),
     "fuse": dict(src="paper_2608_08330_amd/csrc/kernels/post.hip", bytes=453.03e6,
                  sha256="d9e47ed29b6c1248a27c5f4d72953ae5f87db05b42e23cc2f803da37fb5acbc7"),
@@ -130,6 +130,31 @@ def timed_steps(ctx, cfg, frame, dev_pts, steps, warmup, R, torch, record_nodes=
     return time.perf_counter() - t, node
 
 
+def gemm_reference(layers, torch, iters=50):
+    """The vendor library's dense GEMM (torch.matmul -> hipBLASLt, bf16, fp32
+    accumulation) on each conv layer's GEMM shape: the cost of the same
+    FLOPs as a plain GEMM whose im2col operand is already in memory."""
+    rows = []
+    for l in layers:
+        M, N, K = l["M"], l["N"], l["K"]
+        x = torch.randn(M, K, device="cuda", dtype=torch.bfloat16)
+        w = torch.randn(K, N, device="cuda", dtype=torch.bfloat16)
+        for _ in range(5):
+            torch.matmul(x, w)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(iters):
+            torch.matmul(x, w)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / iters * 1e3
+        rows.append({"M": M, "N": N, "K": K, "hipblaslt_us": round(us, 2),
+                     "hipblaslt_tflops": round(2.0 * M * N * K / (us * 1e-6) / 1e12, 1), "conv_us": l["us"]})
+        del x, w
+    return rows
+
+
 def cpu_baseline(cfg, frame, budget_s):
     """The fp64 oracle (untuned) on one agent's encoder, repeated while the
     budget lasts.  Reports encoder GFLOP/s on the host cores."""
@@ -179,6 +204,9 @@ def main(argv=None):
                     help="launch kernels one by one on the per-branch-stream executor too (by default it "
                          "replays each branch and the join as HIP graphs; the serial executor is eager, "
                          "graph launches on one stream being slower there)")
+    ap.add_argument("--gemm-reference", action="store_true",
+                    help="also time the vendor GEMM (torch.matmul, hipBLASLt) on every conv layer's GEMM shape "
+                         "(M x K times K x N, bf16) next to the conv kernel")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB, 5 times "
                          "(reference for the FETCH_SIZE / WRITE_SIZE counters)")
@@ -334,6 +362,8 @@ def main(argv=None):
         out["secondary_rooflines"]["branch_warp"] = {
             "bound": "hbm", "achieved": round(2 * slot_bytes * bw_launches / (bw_ms * 1e-3) / 1e9, 1),
             "peak": PEAK_HBM_GBS, "unit": "GB/s", "traffic": measured_traffic("warp_slot")}
+    if a.gemm_reference:
+        out["gemm_reference"] = gemm_reference(layers, torch)
     if a.exec == "streams" and not a.no_graphs:
         out["graph_stats"] = dict(zip(("instantiated", "updates", "launches"), R.rtcc_graph_stats(ctx_t)))
     print("# throughput done: %.3f ms/step, %.1f TFLOP/s" % (ms_per_step, value), file=sys.stderr, flush=True)
