@@ -74,8 +74,10 @@ class HipExecutor : public Executor {
             HIP_TRY(alloc(&b.d_cell, n_max * 4));
             HIP_TRY(alloc(&b.d_slot, n_max * 4));
             HIP_TRY(alloc(&b.d_member, n_max * 4));
+            HIP_TRY(alloc(&b.d_sorted, n_max * 16));
             HIP_TRY(alloc(&b.d_pcells, n_max * 4));
             HIP_TRY(alloc(&b.d_pcounts, n_max * 4));
+            HIP_TRY(alloc(&b.d_poffs, n_max * 4));
             HIP_TRY(alloc(&b.d_overfull, over_cap * 4));
             HIP_TRY(alloc(&b.d_counts, n_cells * 4));
             HIP_TRY(alloc(&b.d_offsets, n_cells * 4));
@@ -437,7 +439,8 @@ class HipExecutor : public Executor {
     struct Branch {
         float *staging = nullptr;
         void *d_pts = nullptr, *d_cell = nullptr, *d_slot = nullptr, *d_member = nullptr;
-        void *d_pcells = nullptr, *d_pcounts = nullptr, *d_overfull = nullptr;
+        void *d_sorted = nullptr;  // points in segment (pillar) order
+        void *d_pcells = nullptr, *d_pcounts = nullptr, *d_poffs = nullptr, *d_overfull = nullptr;
         void *d_counts = nullptr, *d_offsets = nullptr, *d_tiles = nullptr, *d_meta = nullptr;
         void *d_canvas = nullptr, *d_slotbuf = nullptr, *d_ws = nullptr;
         void *d_warped = nullptr;        // ego-frame map (warp in the branch)
@@ -501,19 +504,22 @@ class HipExecutor : public Executor {
         HIP_TRY(kern::scan_tiles(tiles, n_tiles, meta, s));
         HIP_TRY(kern::scan_down(counts, n_cells, tiles, p.d.max_points_per_pillar, offsets,
                                 static_cast<int32_t *>(b.d_pcells), static_cast<int32_t *>(b.d_pcounts),
-                                static_cast<int32_t *>(b.d_overfull), meta, s));
+                                static_cast<int32_t *>(b.d_poffs), static_cast<int32_t *>(b.d_overfull), meta, s));
         HIP_TRY(kern::scatter(static_cast<int32_t *>(b.d_cell), static_cast<int32_t *>(b.d_slot), offsets, n,
-                              static_cast<int32_t *>(b.d_member), s));
-        HIP_TRY(kern::overfull_select(static_cast<int32_t *>(b.d_overfull), meta, counts, offsets,
-                                      static_cast<int32_t *>(b.d_member), p.d.max_points_per_pillar, n, s));
+                              b.src, static_cast<int32_t *>(b.d_member), static_cast<float *>(b.d_sorted), s));
+        HIP_TRY(kern::overfull_select(static_cast<int32_t *>(b.d_overfull), meta, counts, offsets, b.src,
+                                      static_cast<int32_t *>(b.d_member), static_cast<float *>(b.d_sorted),
+                                      p.d.max_points_per_pillar, n, s));
         if (timing) HIP_TRY(hipEventRecord(b.ev[ev], s));
         ++ev;
 
         kern::PfnArgs pa{};
-        pa.pts = b.src;
+        pa.sorted = static_cast<const float4 *>(b.d_sorted);
         pa.counts = counts;
-        pa.offsets = offsets;
-        pa.member = static_cast<int32_t *>(b.d_member);
+        pa.pcells = static_cast<const int32_t *>(b.d_pcells);
+        pa.pcounts = static_cast<const int32_t *>(b.d_pcounts);
+        pa.poffs = static_cast<const int32_t *>(b.d_poffs);
+        pa.meta = meta;
         pa.w = static_cast<const float *>(d_bias) + p.pfn_w_off;
         pa.b = static_cast<const float *>(d_bias) + p.pfn_b_off;
         pa.canvas = b.d_canvas;
@@ -524,7 +530,7 @@ class HipExecutor : public Executor {
         pa.inv_hy = float(2.0 / (double(p.d.y_max) - double(p.d.y_min)));
         pa.z0 = p.d.z_min;
         pa.inv_dz = float(1.0 / (double(p.d.z_max) - double(p.d.z_min)));
-        HIP_TRY(kern::pfn_canvas(p.bf16, pa, s));
+        HIP_TRY(kern::pfn_canvas(p.bf16, pa, n < n_cells ? n : n_cells, s));
         if (timing) HIP_TRY(hipEventRecord(b.ev[ev], s));
         ++ev;
 

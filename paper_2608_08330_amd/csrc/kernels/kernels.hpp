@@ -33,24 +33,24 @@ hipError_t scan_tiles(int32_t *tile_sums, int32_t n_tiles, int32_t *meta, hipStr
 // K2c: offsets[cell] (exclusive prefix of counts), pillar lists in
 // ascending cell order, list of cells holding more than max_pts points.
 hipError_t scan_down(const int32_t *counts, int32_t n_cells, const int32_t *tile_sums,
-                     int32_t max_pts, int32_t *offsets, int32_t *pcells, int32_t *pcounts,
+                     int32_t max_pts, int32_t *offsets, int32_t *pcells, int32_t *pcounts, int32_t *poffs,
                      int32_t *overfull, int32_t *meta, hipStream_t s);
 // K2d: member[offsets[cell] + slot] = point index.
 hipError_t scatter(const int32_t *cell, const int32_t *slot, const int32_t *offsets, int32_t n,
-                   int32_t *member, hipStream_t s);
+                   const float *pts, int32_t *member, float *sorted, hipStream_t s);
 // K2e: for every overfull cell, move its max_pts lowest point indices to
 // the front of its member segment.
 hipError_t overfull_select(const int32_t *overfull, const int32_t *meta, const int32_t *counts,
-                           const int32_t *offsets, int32_t *member, int32_t max_pts, int32_t n,
-                           hipStream_t s);
+                           const int32_t *offsets, const float *pts, int32_t *member, float *sorted,
+                           int32_t max_pts, int32_t n, hipStream_t s);
 
 // K3: dense canvas [H*W][C]: per cell, channel max over the first
 // min(count, max_pts) members of ReLU(W^T f + b); zero for empty cells.
 struct PfnArgs {
-    const float *pts;
-    const int32_t *counts;
-    const int32_t *offsets;
-    const int32_t *member;
+    const float4 *sorted;  // points in segment order; each segment's first min(count, max_pts) are used
+    const int32_t *counts; // per cell (0: empty)
+    const int32_t *pcells, *pcounts, *poffs;  // per pillar: cell, count, segment offset
+    const int32_t *meta;   // meta[1] = number of pillars
     const float *w;  // [4][C]
     const float *b;  // [C]
     void *canvas;
@@ -59,7 +59,8 @@ struct PfnArgs {
     int32_t max_pts;
     float inv_hx, inv_hy, z0, inv_dz;
 };
-hipError_t pfn_canvas(bool bf16, const PfnArgs &a, hipStream_t s);
+// max_pillars bounds meta[1] (at most min(cells, points)).
+hipError_t pfn_canvas(bool bf16, const PfnArgs &a, int32_t max_pillars, hipStream_t s);
 
 // ------------------------------------------------------------ implicit GEMM
 // conv:   out[m][c_off + n] for m = output pixel, 3x3 taps, pad 1, stride.

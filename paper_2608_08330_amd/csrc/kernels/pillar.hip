@@ -135,6 +135,7 @@ __global__ __launch_bounds__(256) void k_scan_down(const int32_t *__restrict__ c
                                                    int32_t *__restrict__ offsets,
                                                    int32_t *__restrict__ pcells,
                                                    int32_t *__restrict__ pcounts,
+                                                   int32_t *__restrict__ poffs,
                                                    int32_t *__restrict__ overfull,
                                                    int32_t *__restrict__ meta) {
     const int base = blockIdx.x * kScanTile + threadIdx.x * 8;
@@ -159,6 +160,7 @@ __global__ __launch_bounds__(256) void k_scan_down(const int32_t *__restrict__ c
             if (v[i] > 0) {
                 pcells[p] = c;
                 pcounts[p] = v[i];
+                poffs[p] = off;
                 ++p;
                 if (v[i] > max_pts) overfull[atomicAdd(&meta[2], 1)] = c;
             }
@@ -170,18 +172,25 @@ __global__ __launch_bounds__(256) void k_scan_down(const int32_t *__restrict__ c
 __global__ __launch_bounds__(256) void k_scatter(const int32_t *__restrict__ cell,
                                                  const int32_t *__restrict__ slot,
                                                  const int32_t *__restrict__ offsets, int32_t n,
-                                                 int32_t *__restrict__ member) {
+                                                 const float4 *__restrict__ pts,
+                                                 int32_t *__restrict__ member, float4 *__restrict__ sorted) {
     const int i = blockIdx.x * 256 + threadIdx.x;
     if (i >= n) return;
     const int c = cell[i];
-    if (c >= 0) member[offsets[c] + slot[i]] = i;
+    if (c >= 0) {
+        const int d = offsets[c] + slot[i];
+        member[d] = i;
+        sorted[d] = pts[i];
+    }
 }
 
 __global__ __launch_bounds__(256) void k_overfull_select(const int32_t *__restrict__ overfull,
                                                          const int32_t *__restrict__ meta,
                                                          const int32_t *__restrict__ counts,
                                                          const int32_t *__restrict__ offsets,
+                                                         const float4 *__restrict__ pts,
                                                          int32_t *__restrict__ member,
+                                                         float4 *__restrict__ sorted,
                                                          int32_t max_pts, int32_t n) {
     const int lane = threadIdx.x & 63;
     const int wave = (blockIdx.x * 256 + threadIdx.x) >> 6;
@@ -191,6 +200,7 @@ __global__ __launch_bounds__(256) void k_overfull_select(const int32_t *__restri
         const int c = overfull[w];
         const int cnt = counts[c];
         int32_t *seg = member + offsets[c];
+        float4 *sseg = sorted + offsets[c];
         // Smallest T with #{members < T} >= max_pts.  Members are distinct
         // point indices in [0, n), so exactly max_pts members lie below T.
         int lo = 1, hi = n;
@@ -214,7 +224,10 @@ __global__ __launch_bounds__(256) void k_overfull_select(const int32_t *__restri
             const bool sel = j < cnt && e < T;
             const unsigned long long m = __ballot(sel);
             const int my = pos + __popcll(m & ((1ull << lane) - 1ull));
-            if (sel) seg[my] = e;
+            if (sel) {
+                seg[my] = e;
+                sseg[my] = pts[e];
+            }
             pos += __popcll(m);
         }
     }
@@ -234,47 +247,74 @@ __device__ inline uint32_t pack_bf16x2(float a, float b) {
     return (ua >> 16) | (ub & 0xffff0000u);
 }
 
+// Two kinds of blocks.  The first cover the canvas, a lane per (cell, 8
+// channels), and write zeros into the empty cells; the others take the
+// pillars (the ascending list from the scan), a lane per (pillar, 8
+// channels), and write ReLU(W^T f + b) maxed over the pillar's first
+// min(count, max_pts) points, read in segment order from `sorted`.  Every
+// cell is written exactly once, and the pillar lanes read their cell,
+// count and segment offset together instead of through the cell grid.
 template <bool BF16>
 __global__ __launch_bounds__(256) void k_pfn_canvas(PfnArgs a) {
+    const int lanes_per_cell = a.C >> 3;
+    const int64_t zero_threads = int64_t(a.n_cells) * lanes_per_cell;
+    const int zero_blocks = int((zero_threads + 255) / 256);
+    if (int(blockIdx.x) < zero_blocks) {
+        const int64_t gid = int64_t(blockIdx.x) * 256 + threadIdx.x;
+        if (gid >= zero_threads) return;
+        const int cell = int(gid / lanes_per_cell);
+        const int ch = int(gid - int64_t(cell) * lanes_per_cell) * 8;
+        if (a.counts[cell] != 0) return;
+        if (BF16) {
+            nt_store16(static_cast<uint16_t *>(a.canvas) + size_t(cell) * a.C + ch, make_uint4(0u, 0u, 0u, 0u));
+        } else {
+            float *dst = static_cast<float *>(a.canvas) + size_t(cell) * a.C + ch;
+            nt_store16(dst, make_uint4(0u, 0u, 0u, 0u));
+            nt_store16(dst + 4, make_uint4(0u, 0u, 0u, 0u));
+        }
+        return;
+    }
     // PFN weights and bias, read once per block into LDS (C <= 512)
     __shared__ float sw[5 * 512];
     for (int q = threadIdx.x; q < 5 * a.C; q += 256) sw[q] = q < 4 * a.C ? a.w[q] : a.b[q - 4 * a.C];
     __syncthreads();
-    const int lanes_per_cell = a.C >> 3;
-    const int gid = blockIdx.x * 256 + threadIdx.x;
-    const int cell = gid / lanes_per_cell;
-    const int ch = (gid - cell * lanes_per_cell) * 8;
-    if (cell >= a.n_cells) return;
-    float mx[8];
+    const int gid = (int(blockIdx.x) - zero_blocks) * 256 + int(threadIdx.x);
+    const int p = gid / lanes_per_cell;
+    const int ch = (gid - p * lanes_per_cell) * 8;
+    if (p >= a.meta[1]) return;
+    const int cell = a.pcells[p];
+    const int cnt = a.pcounts[p];
+    const int off = a.poffs[p];
+    const int m = cnt < a.max_pts ? cnt : a.max_pts;
+    float w0[8], w1[8], w2[8], w3[8], bb[8], mx[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) mx[i] = 0.f;
-    const int cnt = a.counts[cell];
-    if (cnt > 0) {
-        float w0[8], w1[8], w2[8], w3[8], bb[8];
+    for (int i = 0; i < 8; ++i) {
+        w0[i] = sw[0 * a.C + ch + i];
+        w1[i] = sw[1 * a.C + ch + i];
+        w2[i] = sw[2 * a.C + ch + i];
+        w3[i] = sw[3 * a.C + ch + i];
+        bb[i] = sw[4 * a.C + ch + i];
+        mx[i] = 0.f;
+    }
+    auto add = [&](const float4 pt) {
+        const float f0 = pt.x * a.inv_hx;
+        const float f1 = pt.y * a.inv_hy;
+        const float f2 = (pt.z - a.z0) * a.inv_dz;
+        const float f3 = pt.w;
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-            w0[i] = sw[0 * a.C + ch + i];
-            w1[i] = sw[1 * a.C + ch + i];
-            w2[i] = sw[2 * a.C + ch + i];
-            w3[i] = sw[3 * a.C + ch + i];
-            bb[i] = sw[4 * a.C + ch + i];
+            float h = bb[i] + w0[i] * f0 + w1[i] * f1 + w2[i] * f2 + w3[i] * f3;
+            h = h > 0.f ? h : 0.f;  // +0 for every non-positive value
+            mx[i] = fmaxf(mx[i], h);
         }
-        const int m = cnt < a.max_pts ? cnt : a.max_pts;
-        const int off = a.offsets[cell];
-        const float4 *pts = reinterpret_cast<const float4 *>(a.pts);
-        for (int t = 0; t < m; ++t) {
-            const float4 p = pts[a.member[off + t]];
-            const float f0 = p.x * a.inv_hx;
-            const float f1 = p.y * a.inv_hy;
-            const float f2 = (p.z - a.z0) * a.inv_dz;
-            const float f3 = p.w;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                float h = bb[i] + w0[i] * f0 + w1[i] * f1 + w2[i] * f2 + w3[i] * f3;
-                h = h > 0.f ? h : 0.f;  // +0 for every non-positive value
-                mx[i] = fmaxf(mx[i], h);
-            }
-        }
+    };
+    // two points per step, both loads in flight (max is order-free)
+    for (int t = 0; t < m; t += 2) {
+        const float4 p0 = a.sorted[off + t];
+        const bool two = t + 1 < m;
+        const float4 p1 = a.sorted[off + (two ? t + 1 : t)];
+        add(p0);
+        if (two) add(p1);
     }
     if (BF16) {
         uint4 o;
@@ -323,32 +363,35 @@ hipError_t scan_tiles(int32_t *tile_sums, int32_t n_tiles, int32_t *meta, hipStr
 }
 
 hipError_t scan_down(const int32_t *counts, int32_t n_cells, const int32_t *tile_sums,
-                     int32_t max_pts, int32_t *offsets, int32_t *pcells, int32_t *pcounts,
+                     int32_t max_pts, int32_t *offsets, int32_t *pcells, int32_t *pcounts, int32_t *poffs,
                      int32_t *overfull, int32_t *meta, hipStream_t s) {
     k_scan_down<<<blocks_for(n_cells, kScanTile), 256, 0, s>>>(counts, n_cells, tile_sums, max_pts,
-                                                                offsets, pcells, pcounts, overfull, meta);
+                                                                offsets, pcells, pcounts, poffs, overfull, meta);
     return hipGetLastError();
 }
 
 hipError_t scatter(const int32_t *cell, const int32_t *slot, const int32_t *offsets, int32_t n,
-                   int32_t *member, hipStream_t s) {
+                   const float *pts, int32_t *member, float *sorted, hipStream_t s) {
     if (n <= 0) return hipSuccess;
-    k_scatter<<<blocks_for(n, 256), 256, 0, s>>>(cell, slot, offsets, n, member);
+    k_scatter<<<blocks_for(n, 256), 256, 0, s>>>(cell, slot, offsets, n, reinterpret_cast<const float4 *>(pts),
+                                                 member, reinterpret_cast<float4 *>(sorted));
     return hipGetLastError();
 }
 
 hipError_t overfull_select(const int32_t *overfull, const int32_t *meta, const int32_t *counts,
-                           const int32_t *offsets, int32_t *member, int32_t max_pts, int32_t n,
-                           hipStream_t s) {
+                           const int32_t *offsets, const float *pts, int32_t *member, float *sorted,
+                           int32_t max_pts, int32_t n, hipStream_t s) {
     if (n <= max_pts) return hipSuccess;  // no cell can exceed the cap
-    k_overfull_select<<<64, 256, 0, s>>>(overfull, meta, counts, offsets, member, max_pts, n);
+    k_overfull_select<<<64, 256, 0, s>>>(overfull, meta, counts, offsets, reinterpret_cast<const float4 *>(pts),
+                                         member, reinterpret_cast<float4 *>(sorted), max_pts, n);
     return hipGetLastError();
 }
 
-hipError_t pfn_canvas(bool bf16, const PfnArgs &a, hipStream_t s) {
-    const int64_t threads = int64_t(a.n_cells) * (a.C / 8);
-    if (bf16) k_pfn_canvas<true><<<blocks_for(threads, 256), 256, 0, s>>>(a);
-    else k_pfn_canvas<false><<<blocks_for(threads, 256), 256, 0, s>>>(a);
+hipError_t pfn_canvas(bool bf16, const PfnArgs &a, int32_t max_pillars, hipStream_t s) {
+    const int lanes = a.C / 8;
+    const unsigned blocks = blocks_for(int64_t(a.n_cells) * lanes, 256) + blocks_for(int64_t(max_pillars) * lanes, 256);
+    if (bf16) k_pfn_canvas<true><<<blocks, 256, 0, s>>>(a);
+    else k_pfn_canvas<false><<<blocks, 256, 0, s>>>(a);
     return hipGetLastError();
 }
 
