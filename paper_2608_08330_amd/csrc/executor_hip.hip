@@ -128,6 +128,8 @@ class HipExecutor : public Executor {
             HIP_TRY(alloc(&d_nms_count, 64));
             HIP_TRY(alloc(&d_nms_mask_t, size_t(nms_max_) * 8));
             HIP_TRY(alloc(&d_nms_partial, size_t(kern::kNmsRankSplits) * n_anchor_ * 4));
+            HIP_TRY(alloc(&d_nms_colrows, kern::nms_colrows(nms_max_) * 4));
+            HIP_TRY(alloc(&d_nms_colcount, words * 4));
         }
         HIP_TRY(hipHostMalloc(reinterpret_cast<void **>(&h_rec), n_anchor_ * 9 * 4, hipHostMallocDefault));
         HIP_TRY(hipHostMalloc(reinterpret_cast<void **>(&h_small), 64, hipHostMallocDefault));
@@ -709,6 +711,8 @@ class HipExecutor : public Executor {
             na.mask = static_cast<unsigned long long *>(d_nms_mask);
             na.mask_t = static_cast<unsigned long long *>(d_nms_mask_t);
             na.partial = static_cast<int32_t *>(d_nms_partial);
+            na.colrows = static_cast<int32_t *>(d_nms_colrows);
+            na.colcount = static_cast<int32_t *>(d_nms_colcount);
             na.out = static_cast<float *>(d_nms_out);
             na.out_count = static_cast<int32_t *>(d_nms_count);
             na.iou_threshold = double(p.d.nms_iou_threshold);
@@ -852,7 +856,7 @@ class HipExecutor : public Executor {
     int nms_max_ = 0;  // 0: no NMS
     void *d_nms_rank = nullptr, *d_nms_flag = nullptr, *d_nms_order = nullptr, *d_nms_foot = nullptr;
     void *d_nms_mask = nullptr, *d_nms_out = nullptr, *d_nms_count = nullptr;
-    void *d_nms_mask_t = nullptr, *d_nms_partial = nullptr;
+    void *d_nms_mask_t = nullptr, *d_nms_partial = nullptr, *d_nms_colrows = nullptr, *d_nms_colcount = nullptr;
     float *h_rec = nullptr;
     void *h_small = nullptr;
     size_t n_anchor_ = 0;

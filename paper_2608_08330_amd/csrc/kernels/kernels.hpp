@@ -169,6 +169,8 @@ struct NmsArgs {
     unsigned long long *mask;     // [max_candidates][max_candidates / 64] (rounded up)
     unsigned long long *mask_t;   // [max_candidates]: earlier rows of its own 64-row chunk that suppress it
     int32_t *partial;             // [kNmsRankSplits][max_records] partial rank counts
+    int32_t *colrows;             // [64 W (W - 1) / 2], W = words per mask row: listed rows per column chunk
+    int32_t *colcount;            // [W] rows listed per column chunk
     float *out;                   // [max_candidates][9] kept records, ascending anchor index
     int32_t *out_count;           // kept, on the device
     double iou_threshold;         // suppress iff IoU > threshold
@@ -176,6 +178,11 @@ struct NmsArgs {
 };
 // max_records bounds n (the grid of the per-record kernels).
 hipError_t rotated_nms(const NmsArgs &a, int64_t max_records, hipStream_t s);
+// Elements of NmsArgs::colrows for a candidate cap.
+inline size_t nms_colrows(int32_t max_candidates) {
+    const size_t w = size_t(max_candidates + 63) / 64;
+    return 64 * w * (w > 0 ? w - 1 : 0) / 2 + 1;
+}
 
 }  // namespace kern
 }  // namespace rtcc

@@ -15,9 +15,11 @@
 //                  order[rank] = record, footprint (x, y, w, l, cos yaw,
 //                  sin yaw, valid) as f64.
 //   k_nms_mask     bit b of word (a, b / 64) is set iff b > a and the BEV
-//                  IoU of candidates a and b exceeds the threshold; four
-//                  lanes per (row a, 16 columns), storing a 16-bit part of
-//                  the word.  IoU in float64: the intersection area is the
+//                  IoU of candidates a and b exceeds the threshold; one
+//                  block per 64 x 64 tile, which lists the pairs whose
+//                  circumcircles meet in LDS and then evaluates that list
+//                  densely; the rows with a nonzero word in a later chunk
+//                  are listed per column chunk.  IoU in float64: the intersection area is the
 //                  shoelace sum over the edge pieces of each rectangle
 //                  inside the other (Cyrus-Beck clipped, crossing points
 //                  shared by the two pieces that meet there); pairs whose
@@ -25,14 +27,12 @@
 //                  circumradii are disjoint and skip the clipping.  A box
 //                  with a non-finite parameter or w <= 0 or l <= 0 overlaps
 //                  nothing.
-//   k_nms_select   one block: the greedy walk over the ranking, 64 rows at a
-//                  time: wave 0 resolves the rows of a chunk against each
-//                  other with the chunk's diagonal mask words (scalar loop;
-//                  the words were prefetched during the previous chunk),
-//                  then every thread takes (kept row, later word) pairs and
-//                  ORs the mask word into the LDS removed set (one load per
-//                  pair, all in flight together).  The kept records are then
-//                  compacted in ascending record (anchor) order.
+//   k_nms_select   one wavefront walks the ranking 64 rows at a time: the
+//                  rows removed by earlier chunks are the OR of the listed
+//                  words of the kept rows (copied into LDS first), then the
+//                  chunk resolves itself from its in-chunk suppressors.  The
+//                  kept records are then compacted in ascending record
+//                  (anchor) order.
 // Everything is integer or float64 except the scores, which are compared as
 // stored: the decisions do not depend on the grid or the timing.
 #include "kernels.hpp"
@@ -101,6 +101,8 @@ __device__ inline void gather_one(const NmsArgs &a, int i, int r) {
 }
 
 __global__ __launch_bounds__(256) void k_nms_gather(NmsArgs a) {
+    if (blockIdx.x == 0)  // the mask kernel counts the listed rows per column chunk from zero
+        for (int c = threadIdx.x; c < (a.max_candidates + 63) / 64; c += 256) a.colcount[c] = 0;
     const int n = *a.count;
     const int T = (n + 255) / 256;
     const int S = T < kNmsRankSplits ? T : kNmsRankSplits;
@@ -278,6 +280,17 @@ __device__ __forceinline__ R foot_iou(const Foot<R> &A, const Foot<R> &B) {
     return uni > R(0) ? inter / uni : R(0);
 }
 
+// Whether the footprints' circumcircles meet in float32 or in float64, the
+// same comparisons foot_iou makes before clipping: a pair for which both
+// fail has IoU 0 in both precisions.
+__device__ __forceinline__ bool circles_meet(const double *A, const double *B) {
+#pragma clang fp contract(off)
+    const float dxf = float(A[0]) - float(B[0]), dyf = float(A[1]) - float(B[1]);
+    const float rf = float(A[7]) + float(B[7]);
+    const double dx = A[0] - B[0], dy = A[1] - B[1], rd = A[7] + B[7];
+    return !(dxf * dxf + dyf * dyf > rf * rf) || !(dx * dx + dy * dy > rd * rd);
+}
+
 // The decision IoU > threshold, taken in float64.  The float32 evaluation
 // of the same formula decides first whenever it lies more than kFilter from
 // the threshold: its rounding error, for footprints whose coordinates
@@ -292,86 +305,82 @@ __device__ __forceinline__ bool suppresses(const double *fa, const double *fb, d
     return foot_iou(load_foot<double>(fa), load_foot<double>(fb)) > thr;
 }
 
-__device__ __forceinline__ void mask_piece(const NmsArgs &a, int m, int rb, int cb, int piece, double *cf) {
-    const int c0 = cb * 64 + piece * 16;
-    if (c0 >= m) return;  // uniform over the block
-    for (int q = threadIdx.x; q < 16 * kFoot; q += 256) {
-        const int b = c0 + q / kFoot;
-        cf[q] = b < m ? a.foot[size_t(c0) * kFoot + q] : 0.0;
-    }
-    __syncthreads();
-    const int row = rb * 64 + int(threadIdx.x >> 2);
-    const int sub = threadIdx.x & 3;  // columns c0 + 4 sub .. c0 + 4 sub + 3
-    unsigned bits = 0u;
-    if (row < m) {
-        const double *fa = a.foot + size_t(row) * kFoot;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int q = 4 * sub + k, col = c0 + q;
-            if (col >= m || col <= row) continue;
-            if (suppresses(fa, cf + q * kFoot, a.iou_threshold)) bits |= 1u << q;
-        }
-    }
-    if (cb == rb) {
-        // diagonal block: also the transposed words, column q of this piece
-        // <- the rows of the chunk that suppress it
-        __shared__ unsigned long long tq[16];
-        if (threadIdx.x < 16) tq[threadIdx.x] = 0ull;
-        __syncthreads();
-        if (bits) {
-            unsigned rest = bits;
-            while (rest) {
-                const int q = __builtin_ctz(rest);
-                rest &= rest - 1u;
-                atomicOr(&tq[q], 1ull << (row & 63));
-            }
-        }
-        __syncthreads();
-        if (threadIdx.x < 16 && c0 + int(threadIdx.x) < m) a.mask_t[c0 + threadIdx.x] = tq[threadIdx.x];
-    }
-    bits |= __shfl_xor(bits, 1, 64);
-    bits |= __shfl_xor(bits, 2, 64);
-    if (row < m && sub == 0) {
-        const int words = (a.max_candidates + 63) / 64;
-        reinterpret_cast<unsigned short *>(a.mask + size_t(row) * words + cb)[piece] =
-            static_cast<unsigned short>(bits);
-    }
-}
+// Column chunk c of the mask: the rows of earlier chunks that have a
+// nonzero word there are listed from colrows[col_base(c)], at most 64 c.
+__host__ __device__ inline int64_t col_base(int c) { return int64_t(64) * c * (c - 1) / 2; }
 
+// One 64 x 64 tile (row chunk rb, column chunk cb >= rb) of the suppression
+// matrix.  The pairs whose footprints' circumcircles meet (in float32 or
+// float64: the two tests that can let `suppresses` return true) are first
+// compacted into an LDS list, then the block evaluates that list, so the
+// clipping runs on dense lanes instead of the few close pairs scattered
+// over the tile.  Writes every word (row, cb) of the tile (no zeroing
+// needed), lists the rows with a nonzero off-diagonal word, and on the
+// diagonal tile the transposed words: for every column, the earlier rows
+// of its own chunk that suppress it.
 __global__ __launch_bounds__(256) void k_nms_mask(NmsArgs a) {
+    __shared__ double fr[64 * kFoot], fc[64 * kFoot];
+    __shared__ unsigned short list[64 * 64];
+    __shared__ unsigned long long rowbits[64], tq[64];
+    __shared__ int nlist;
     const int n = *a.count;
     const int m = n < a.max_candidates ? n : a.max_candidates;
     const int T = (m + 63) / 64;
-    const int items = 4 * (T * (T + 1) / 2);
-    __shared__ double cf[16 * kFoot];
-    for (int item = blockIdx.x; item < items; item += gridDim.x) {
-        // item -> (row chunk rb, column chunk cb >= rb, 16-column piece)
-        int tri = item >> 2, rb = 0;
+    const int words = (a.max_candidates + 63) / 64;
+    const int tid = threadIdx.x;
+    for (int item = blockIdx.x; item < T * (T + 1) / 2; item += gridDim.x) {  // uniform over the block
+        int tri = item, rb = 0;
         while (tri >= T - rb) {
             tri -= T - rb;
             ++rb;
         }
-        mask_piece(a, m, rb, rb + tri, item & 3, cf);
+        const int cb = rb + tri;
+        const int r0 = rb * 64, c0 = cb * 64;
+        for (int q = tid; q < 64 * kFoot; q += 256) {
+            const int k = q / kFoot;
+            fr[q] = r0 + k < m ? a.foot[size_t(r0) * kFoot + q] : 0.0;
+            fc[q] = c0 + k < m ? a.foot[size_t(c0) * kFoot + q] : 0.0;
+        }
+        if (tid < 64) {
+            rowbits[tid] = 0ull;
+            tq[tid] = 0ull;
+        }
+        if (tid == 0) nlist = 0;
         __syncthreads();
+        // close pairs (row i, column j), j > i on the diagonal tile
+        const int i = tid >> 2;
+        for (int k = 0; k < 16; ++k) {
+            const int j = (tid & 3) * 16 + k;
+            bool close = false;
+            if (r0 + i < m && c0 + j < m && (cb > rb || j > i)) {
+                const double *A = fr + i * kFoot, *B = fc + j * kFoot;
+                if (A[6] != 0.0 && B[6] != 0.0) close = circles_meet(A, B);
+            }
+            if (close) list[atomicAdd(&nlist, 1)] = static_cast<unsigned short>((i << 6) | j);
+        }
+        __syncthreads();
+        const int nl = nlist;
+        for (int q = tid; q < nl; q += 256) {
+            const int ii = list[q] >> 6, jj = list[q] & 63;
+            if (suppresses(fr + ii * kFoot, fc + jj * kFoot, a.iou_threshold)) {
+                atomicOr(&rowbits[ii], 1ull << jj);
+                if (cb == rb) atomicOr(&tq[jj], 1ull << ii);
+            }
+        }
+        __syncthreads();
+        if (tid < 64 && r0 + tid < m) {
+            const unsigned long long w = rowbits[tid];
+            a.mask[size_t(r0 + tid) * words + cb] = w;
+            if (cb != rb && w) a.colrows[col_base(cb) + atomicAdd(&a.colcount[cb], 1)] = r0 + tid;
+        }
+        if (cb == rb && tid < 64 && c0 + tid < m) a.mask_t[c0 + tid] = tq[tid];
+        __syncthreads();  // the tile's LDS is reused by the next item
     }
 }
 
 __device__ inline unsigned long long uniform64(unsigned long long v) {
     const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(v));
     const uint32_t hi = __builtin_amdgcn_readfirstlane(uint32_t(v >> 32));
-    return (static_cast<unsigned long long>(hi) << 32) | lo;
-}
-
-// Greedy resolution of one chunk of 64 ranked rows (one wavefront): `rem`
-// are the rows already removed by earlier chunks, lane r holds the
-// diagonal word of row r (bits of later rows of the chunk it suppresses).
-// Visits only the rows still standing, in rank order; all loop state is
-// wave-uniform (scalar registers).  Returns the kept rows.
-__device__ inline unsigned long long resolve_chunk(unsigned long long rem, unsigned long long diag, int rows);
-
-__device__ inline unsigned long long readlane64(unsigned long long v, int lane) {
-    const uint32_t lo = __builtin_amdgcn_readlane(uint32_t(v), lane);
-    const uint32_t hi = __builtin_amdgcn_readlane(uint32_t(v >> 32), lane);
     return (static_cast<unsigned long long>(hi) << 32) | lo;
 }
 
@@ -407,21 +416,6 @@ __device__ inline unsigned long long resolve_chunk_parallel(unsigned long long r
         kept = next;
     }
     return kept;
-}
-
-__device__ inline unsigned long long resolve_chunk(unsigned long long rem, unsigned long long diag, int rows) {
-    const unsigned long long rowmask = rows >= 64 ? ~0ull : (1ull << rows) - 1ull;
-    rem = uniform64(rem);
-    unsigned long long kb = 0ull, done = 0ull;
-    for (;;) {
-        const unsigned long long avail = ~rem & rowmask & ~done;
-        if (!avail) break;
-        const int r = __builtin_ctzll(avail);
-        kb |= 1ull << r;
-        rem |= readlane64(diag, r);
-        done = r == 63 ? ~0ull : (2ull << r) - 1ull;
-    }
-    return kb;
 }
 
 constexpr int kSelectThreads = 1024;
@@ -477,122 +471,71 @@ __device__ void compact_kept(const NmsArgs &a, const unsigned long long *keep, i
     if (tid == 0) *a.out_count = base_sh;
 }
 
+// The greedy walk over the ranking, 64 rows (one chunk) at a time, by one
+// wavefront: the rows of chunk c removed by earlier chunks are the OR of
+// the words (r, c) of the kept rows r listed for column chunk c; the rows
+// of the chunk then resolve among themselves from their in-chunk
+// suppressors (resolve_chunk_parallel).  The listed rows and their words
+// are first copied into LDS by the whole block when they fit (the lists
+// are short: suppression is local), else the walk reads them from global
+// memory.  The kept records are then compacted in ascending record order.
+constexpr int kSelCap = 5120;  // listed words held in LDS
+
 __global__ __launch_bounds__(kSelectThreads) void k_nms_select(NmsArgs a) {
-    __shared__ unsigned long long removed[kMaxWords];
     __shared__ unsigned long long keep[kMaxWords];
-    __shared__ int klist[64];
-    __shared__ int kcnt;
+    __shared__ unsigned long long eword[kSelCap];
+    __shared__ unsigned short erow[kSelCap];
+    __shared__ int coff[kMaxWords + 1];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int n = *a.count;
     const int m = n < a.max_candidates ? n : a.max_candidates;
-    const int nw = (m + 63) / 64;
+    const int T = (m + 63) / 64;
     const int words = (a.max_candidates + 63) / 64;
-    for (int w = tid; w < nw; w += kSelectThreads) removed[w] = 0ull;
     if (n > kFlagBits)
         for (int i = tid; i < n; i += kSelectThreads) a.flag[i] = 0;
-    unsigned long long diag_next = 0ull;
-    if (wave == 0 && lane < m) diag_next = a.mask[size_t(lane) * words];
-    __syncthreads();
-
-    for (int c = 0; c < nw; ++c) {
-        if (wave == 0) {
-            const unsigned long long diag = diag_next;
-            const unsigned long long kb = resolve_chunk(removed[c], diag, m - c * 64);
-            if ((kb >> lane) & 1ull) klist[__popcll(kb & ((1ull << lane) - 1ull))] = lane;
-            if (lane == 0) {
-                keep[c] = kb;
-                kcnt = __popcll(kb);
-            }
+    if (tid == 0) {
+        int o = 0;
+        for (int c = 0; c < T; ++c) {
+            coff[c] = o;
+            o += a.colcount[c];
         }
-        __syncthreads();
-        // (kept row, later word) pairs: every load of this chunk in flight at once
-        const int kc = kcnt;
-        const int total = kc * (nw - c - 1);
-        for (int q = tid; q < total; q += kSelectThreads) {
-            const int r = klist[q % kc], w = c + 1 + q / kc;
-            const unsigned long long v = a.mask[size_t(c * 64 + r) * words + w];
-            if (v) atomicOr(&removed[w], v);
-        }
-        if (wave == 0 && c + 1 < nw) {
-            const int row = (c + 1) * 64 + lane;
-            diag_next = row < m ? a.mask[size_t(row) * words + c + 1] : 0ull;
-        }
-        __syncthreads();
+        coff[T] = o;
     }
-
-    compact_kept(a, keep, m, n);
-}
-
-
-// Pull form of the greedy walk for max_candidates <= kPullMax: the removed
-// bits of chunk c are the OR, over the kept rows of the earlier chunks, of
-// their word c (column c of the mask).  Columns are read two chunks ahead
-// (registers, then LDS), so the walk itself only touches LDS.
-constexpr int kPullMax = 4096;
-
-__global__ __launch_bounds__(kSelectThreads) void k_nms_select_pull(NmsArgs a) {
-    __shared__ unsigned long long col[2][kPullMax];
-    __shared__ unsigned long long keep[kPullMax / 64];
-    __shared__ unsigned long long part[kSelectThreads / 64];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int n = *a.count;
-    const int m = n < a.max_candidates ? n : a.max_candidates;
-    const int nw = (m + 63) / 64;
-    const int words = (a.max_candidates + 63) / 64;
-    constexpr int PER = kPullMax / kSelectThreads;
-    // column w of the rows that have a word there: rows < min(64 (w + 1), m)
-    auto load_col = [&](int w, unsigned long long *dst) {
-        const int rows = (w + 1) * 64 < m ? (w + 1) * 64 : m;
-#pragma unroll
-        for (int k = 0; k < PER; ++k) {
-            const int r = tid + k * kSelectThreads;
-            dst[k] = (w < nw && r < rows) ? a.mask[size_t(r) * words + w] : 0ull;
-        }
-    };
-    if (n > kFlagBits)
-        for (int i = tid; i < n; i += kSelectThreads) a.flag[i] = 0;
-    for (int r = tid; r < 64 && r < m; r += kSelectThreads) col[0][r] = a.mask[size_t(r) * words];
-    // two columns ahead in registers: column c + 1 was issued during chunk
-    // c - 1 and lands in LDS at the end of chunk c
-    unsigned long long pre1[PER], pre2[PER];
-    load_col(1, pre1);
-    // wave 0 lane r: the in-chunk suppressors of row r of the current chunk
-    // (read one chunk ahead)
-    unsigned long long sup_cur = (wave == 0 && lane < m) ? a.mask_t[lane] : 0ull;
     __syncthreads();
-    for (int c = 0; c < nw; ++c) {
-        const int buf = c & 1;
-        load_col(c + 2, pre2);
-        const int next_row = (c + 1) * 64 + lane;
-        const unsigned long long sup_next = (wave == 0 && next_row < m) ? a.mask_t[next_row] : 0ull;
-        const int rows_next = (c + 2) * 64 < m ? (c + 2) * 64 : m;
-        // removed bits of chunk c: word c of every kept row before the chunk
-        unsigned long long acc = 0ull;
-#pragma unroll
-        for (int k = 0; k < PER; ++k) {
-            const int r = tid + k * kSelectThreads;
-            if (r < c * 64 && ((keep[r >> 6] >> (r & 63)) & 1ull)) acc |= col[buf][r];
+    const bool fits = coff[T] <= kSelCap;
+    if (fits) {
+        for (int e = tid; e < coff[T]; e += kSelectThreads) {
+            int lo = 0, hi = T - 1;  // the chunk c with coff[c] <= e < coff[c + 1]
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (coff[mid] <= e) lo = mid;
+                else hi = mid - 1;
+            }
+            const int r = a.colrows[col_base(lo) + (e - coff[lo])];
+            erow[e] = static_cast<unsigned short>(r);
+            eword[e] = a.mask[size_t(r) * words + lo];
         }
-        acc = wave_or64(acc);
-        if (lane == 0) part[wave] = acc;
-        __syncthreads();
-        if (wave == 0) {
-            const int rows = m - c * 64 < 64 ? m - c * 64 : 64;
-            unsigned long long rem = lane < kSelectThreads / 64 ? part[lane] : 0ull;
+    }
+    __syncthreads();
+    if (wave == 0) {
+        unsigned long long sup_next = lane < m ? a.mask_t[lane] : 0ull;
+        for (int c = 0; c < T; ++c) {
+            const unsigned long long sup = sup_next;
+            const int nxt = (c + 1) * 64 + lane;
+            sup_next = nxt < m ? a.mask_t[nxt] : 0ull;
+            unsigned long long rem = 0ull;
+            for (int k = coff[c] + lane; k < coff[c + 1]; k += 64) {
+                const int r = fits ? int(erow[k]) : a.colrows[col_base(c) + (k - coff[c])];
+                const unsigned long long w = fits ? eword[k] : a.mask[size_t(r) * words + c];
+                if ((keep[r >> 6] >> (r & 63)) & 1ull) rem |= w;
+            }
             rem = wave_or64(rem);
-            const unsigned long long sup = lane < rows ? sup_cur : 0ull;
-            const unsigned long long kb = resolve_chunk_parallel(rem, sup, rows);
+            const int rows = m - c * 64 < 64 ? m - c * 64 : 64;
+            const unsigned long long kb = resolve_chunk_parallel(rem, lane < rows ? sup : 0ull, rows);
             if (lane == 0) keep[c] = kb;
         }
-#pragma unroll
-        for (int k = 0; k < PER; ++k) {
-            const int r = tid + k * kSelectThreads;
-            if (r < rows_next) col[buf ^ 1][r] = pre1[k];
-            pre1[k] = pre2[k];
-        }
-        sup_cur = sup_next;
-        __syncthreads();
     }
+    __syncthreads();
     compact_kept(a, keep, m, n);
 }
 
@@ -608,10 +551,9 @@ hipError_t rotated_nms(const NmsArgs &a, int64_t max_records, hipStream_t s) {
     k_nms_rank<<<blocks < 1024u ? blocks : 1024u, 256, 0, s>>>(a);
     k_nms_gather<<<small, 256, 0, s>>>(a);
     const unsigned chunks = unsigned((a.max_candidates + 63) / 64);
-    const unsigned items = 4u * chunks * (chunks + 1u) / 2u;
-    k_nms_mask<<<items < 2048u ? items : 2048u, 256, 0, s>>>(a);
-    if (a.max_candidates <= kPullMax) k_nms_select_pull<<<1, kSelectThreads, 0, s>>>(a);
-    else k_nms_select<<<1, kSelectThreads, 0, s>>>(a);
+    const unsigned tiles = chunks * (chunks + 1u) / 2u;
+    k_nms_mask<<<tiles < 2048u ? tiles : 2048u, 256, 0, s>>>(a);
+    k_nms_select<<<1, kSelectThreads, 0, s>>>(a);
     return hipGetLastError();
 }
 

@@ -15,7 +15,7 @@ void set_thread_error(const std::string &msg);
 namespace {
 
 struct Scratch {
-    void *p[8] = {};
+    void *p[10] = {};
     ~Scratch() {
         for (void *q : p)
             if (q) (void)hipFree(q);
@@ -48,9 +48,10 @@ extern "C" RTCC_API rtcc_status rtcc_rotated_nms(const float *device_records, in
     const size_t m = size_t(max_candidates);
     const size_t words = (m + 63) / 64;
     Scratch sc;
-    const size_t sizes[8] = {size_t(n) * 4, size_t(n) * 4, m * 4, m * rtcc::kern::kNmsFootDoubles * 8, m * words * 8, 64,
-                             m * 8, size_t(rtcc::kern::kNmsRankSplits) * size_t(n) * 4};
-    for (int i = 0; i < 8; ++i) {
+    const size_t sizes[10] = {size_t(n) * 4, size_t(n) * 4, m * 4, m * rtcc::kern::kNmsFootDoubles * 8, m * words * 8, 64,
+                              m * 8, size_t(rtcc::kern::kNmsRankSplits) * size_t(n) * 4,
+                              rtcc::kern::nms_colrows(max_candidates) * 4, words * 4};
+    for (int i = 0; i < 10; ++i) {
         hipError_t e = hipMalloc(&sc.p[i], sizes[i]);
         if (e != hipSuccess) return hip_fail(e, "hipMalloc");
     }
@@ -70,6 +71,8 @@ extern "C" RTCC_API rtcc_status rtcc_rotated_nms(const float *device_records, in
     a.mask = static_cast<unsigned long long *>(sc.p[4]);
     a.mask_t = static_cast<unsigned long long *>(sc.p[6]);
     a.partial = static_cast<int32_t *>(sc.p[7]);
+    a.colrows = static_cast<int32_t *>(sc.p[8]);
+    a.colcount = static_cast<int32_t *>(sc.p[9]);
     a.out = device_out;
     a.out_count = count + 1;
     a.iou_threshold = double(iou_threshold);
