@@ -479,13 +479,15 @@ __device__ void compact_kept(const NmsArgs &a, const unsigned long long *keep, i
 // are first copied into LDS by the whole block when they fit (the lists
 // are short: suppression is local), else the walk reads them from global
 // memory.  The kept records are then compacted in ascending record order.
-constexpr int kSelCap = 5120;  // listed words held in LDS
+constexpr int kSelCap = 5120;   // listed words held in LDS
+constexpr int kSupLds = 4096;   // candidates whose in-chunk suppressors are held in LDS
 
 __global__ __launch_bounds__(kSelectThreads) void k_nms_select(NmsArgs a) {
     __shared__ unsigned long long keep[kMaxWords];
     __shared__ unsigned long long eword[kSelCap];
     __shared__ unsigned short erow[kSelCap];
     __shared__ int coff[kMaxWords + 1];
+    __shared__ unsigned long long supl[kSupLds];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int n = *a.count;
     const int m = n < a.max_candidates ? n : a.max_candidates;
@@ -493,16 +495,24 @@ __global__ __launch_bounds__(kSelectThreads) void k_nms_select(NmsArgs a) {
     const int words = (a.max_candidates + 63) / 64;
     if (n > kFlagBits)
         for (int i = tid; i < n; i += kSelectThreads) a.flag[i] = 0;
+    // exclusive prefix of the per-chunk list lengths: read in parallel, then
+    // summed from LDS (one global load latency, not T)
+    for (int c = tid; c < T; c += kSelectThreads) coff[c + 1] = a.colcount[c];
+    __syncthreads();
     if (tid == 0) {
         int o = 0;
         for (int c = 0; c < T; ++c) {
+            const int k = coff[c + 1];
             coff[c] = o;
-            o += a.colcount[c];
+            o += k;
         }
         coff[T] = o;
     }
     __syncthreads();
     const bool fits = coff[T] <= kSelCap;
+    const bool sup_lds = m <= kSupLds;
+    if (sup_lds)
+        for (int q = tid; q < m; q += kSelectThreads) supl[q] = a.mask_t[q];
     if (fits) {
         for (int e = tid; e < coff[T]; e += kSelectThreads) {
             int lo = 0, hi = T - 1;  // the chunk c with coff[c] <= e < coff[c + 1]
@@ -518,11 +528,17 @@ __global__ __launch_bounds__(kSelectThreads) void k_nms_select(NmsArgs a) {
     }
     __syncthreads();
     if (wave == 0) {
-        unsigned long long sup_next = lane < m ? a.mask_t[lane] : 0ull;
+        // in-chunk suppressors from LDS, or prefetched a chunk ahead
+        unsigned long long sup_next = !sup_lds && lane < m ? a.mask_t[lane] : 0ull;
         for (int c = 0; c < T; ++c) {
-            const unsigned long long sup = sup_next;
-            const int nxt = (c + 1) * 64 + lane;
-            sup_next = nxt < m ? a.mask_t[nxt] : 0ull;
+            const int row = c * 64 + lane, nxt = row + 64;
+            unsigned long long sup;
+            if (sup_lds) {
+                sup = row < m ? supl[row] : 0ull;
+            } else {
+                sup = sup_next;
+                sup_next = nxt < m ? a.mask_t[nxt] : 0ull;
+            }
             unsigned long long rem = 0ull;
             for (int k = coff[c] + lane; k < coff[c + 1]; k += 64) {
                 const int r = fits ? int(erow[k]) : a.colrows[col_base(c) + (k - coff[c])];
