@@ -69,6 +69,7 @@ def _check(boxes, scores, anchors, max_cand, thr, label):
     (3, 700, 15.0, 0, 4096, 0.0),      # any overlap suppresses
     (4, 700, 15.0, 0, 4096, 0.5),
     (5, 129, 5.0, 0, 64, 0.15),        # ragged: cap and count not multiples of 64
+    (6, 4096, 6.0, 0, 4096, 0.15),     # dense: more listed mask words than the walk holds in LDS
 ])
 def test_random_scenes(seed, n, spread, clusters, cap, thr):
     rng = np.random.default_rng(seed)
