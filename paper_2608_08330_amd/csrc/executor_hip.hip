@@ -488,7 +488,6 @@ class HipExecutor : public Executor {
     rtcc_status enqueue_encoder(Branch &b, hipStream_t s, bool timing, int ev_base, std::string &err) {
         const Plan &p = p_;
         const int n_cells = p.H * p.W;
-        const int n_tiles = (n_cells + kern::kScanTile - 1) / kern::kScanTile;
         const int n = b.n;
         int32_t *counts = static_cast<int32_t *>(b.d_counts);
         int32_t *offsets = static_cast<int32_t *>(b.d_offsets);
@@ -502,8 +501,7 @@ class HipExecutor : public Executor {
         HIP_TRY(kern::fill_i32(counts, n_cells, 0, s));
         HIP_TRY(kern::cell_ids(b.src, n, g, static_cast<int32_t *>(b.d_cell), static_cast<int32_t *>(b.d_slot),
                                counts, s));
-        HIP_TRY(kern::scan_reduce(counts, n_cells, tiles, s));
-        HIP_TRY(kern::scan_tiles(tiles, n_tiles, meta, s));
+        HIP_TRY(kern::scan_reduce(counts, n_cells, tiles, meta, s));
         HIP_TRY(kern::scan_down(counts, n_cells, tiles, p.d.max_points_per_pillar, offsets,
                                 static_cast<int32_t *>(b.d_pcells), static_cast<int32_t *>(b.d_pcounts),
                                 static_cast<int32_t *>(b.d_poffs), static_cast<int32_t *>(b.d_overfull), meta, s));

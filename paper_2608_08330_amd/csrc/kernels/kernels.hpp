@@ -25,13 +25,12 @@ hipError_t fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s);
 hipError_t cell_ids(const float *pts, int32_t n, const PillarGeom &g, int32_t *cell, int32_t *slot,
                     int32_t *counts, hipStream_t s);
 
-// K2a: per tile of kScanTile cells: (points, non-empty cells).
-hipError_t scan_reduce(const int32_t *counts, int32_t n_cells, int32_t *tile_sums, hipStream_t s);
-// K2b: exclusive scan of tile sums in place; meta = {valid points, pillars,
-// overfull count (zeroed)}.
-hipError_t scan_tiles(int32_t *tile_sums, int32_t n_tiles, int32_t *meta, hipStream_t s);
+// K2a: per tile of kScanTile cells: (points, non-empty cells); zeroes
+// meta[2] (the overfull count of K2c).
+hipError_t scan_reduce(const int32_t *counts, int32_t n_cells, int32_t *tile_sums, int32_t *meta, hipStream_t s);
 // K2c: offsets[cell] (exclusive prefix of counts), pillar lists in
-// ascending cell order, list of cells holding more than max_pts points.
+// ascending cell order, list of cells holding more than max_pts points;
+// meta = {valid points, pillars, overfull count}.
 hipError_t scan_down(const int32_t *counts, int32_t n_cells, const int32_t *tile_sums,
                      int32_t max_pts, int32_t *offsets, int32_t *pcells, int32_t *pcounts, int32_t *poffs,
                      int32_t *overfull, int32_t *meta, hipStream_t s);

@@ -6,8 +6,9 @@
 //                   per cell; the returned old count is the point's rank of
 //                   arrival in its cell
 //   scan_reduce /   exclusive prefix over all H*W cells -> segment offsets,
-//   scan_tiles /    ascending list of non-empty cells (pillars) and their
-//   scan_down       counts, list of cells over the per-pillar point cap
+//   scan_down       ascending list of non-empty cells (pillars) and their
+//                   counts, list of cells over the per-pillar point cap (each
+//                   block of the second pass adds up the tile sums before it)
 //   scatter         member[offset[cell] + rank] = point index
 //   overfull_select for the few cells above the cap, one wavefront moves the
 //                   cap lowest point indices (found by bisection on the index
@@ -88,7 +89,9 @@ __global__ __launch_bounds__(256) void k_cell_ids(const float4 *__restrict__ pts
 }
 
 __global__ __launch_bounds__(256) void k_scan_reduce(const int32_t *__restrict__ counts,
-                                                     int32_t n_cells, int32_t *__restrict__ tile_sums) {
+                                                     int32_t n_cells, int32_t *__restrict__ tile_sums,
+                                                     int32_t *__restrict__ meta) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) meta[2] = 0;  // overfull count, appended to by the scan
     const int base = blockIdx.x * kScanTile + threadIdx.x * 8;
     int s = 0, f = 0;
 #pragma unroll
@@ -105,28 +108,6 @@ __global__ __launch_bounds__(256) void k_scan_reduce(const int32_t *__restrict__
     if (threadIdx.x == 0) {
         tile_sums[2 * blockIdx.x] = tot.x;
         tile_sums[2 * blockIdx.x + 1] = tot.y;
-    }
-}
-
-__global__ __launch_bounds__(256) void k_scan_tiles(int32_t *__restrict__ ts, int32_t n_tiles,
-                                                    int32_t *__restrict__ meta) {
-    int2 carry = make_int2(0, 0);
-    for (int base = 0; base < n_tiles; base += 256) {
-        const int i = base + threadIdx.x;
-        int2 v = make_int2(0, 0);
-        if (i < n_tiles) v = make_int2(ts[2 * i], ts[2 * i + 1]);
-        int2 tot;
-        const int2 ex = block_excl_scan256(v, &tot);
-        if (i < n_tiles) {
-            ts[2 * i] = carry.x + ex.x;
-            ts[2 * i + 1] = carry.y + ex.y;
-        }
-        carry = add2(carry, tot);
-    }
-    if (threadIdx.x == 0) {
-        meta[0] = carry.x;
-        meta[1] = carry.y;
-        meta[2] = 0;
     }
 }
 
@@ -148,10 +129,19 @@ __global__ __launch_bounds__(256) void k_scan_down(const int32_t *__restrict__ c
         s += v[i];
         f += v[i] > 0;
     }
-    int2 tot;
+    // the sums of the tiles before this one, added up by the block itself
+    // (no separate scan of the tile sums); the last tile writes the totals
+    int2 before = make_int2(0, 0);
+    for (int t = threadIdx.x; t < int(blockIdx.x); t += 256) before = add2(before, make_int2(ts[2 * t], ts[2 * t + 1]));
+    int2 prefix, tot;
+    block_excl_scan256(before, &prefix);
     const int2 ex = block_excl_scan256(make_int2(s, f), &tot);
-    int off = ts[2 * blockIdx.x] + ex.x;
-    int p = ts[2 * blockIdx.x + 1] + ex.y;
+    if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) {
+        meta[0] = prefix.x + tot.x;
+        meta[1] = prefix.y + tot.y;
+    }
+    int off = prefix.x + ex.x;
+    int p = prefix.y + ex.y;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
         const int c = base + i;
@@ -352,13 +342,8 @@ hipError_t cell_ids(const float *pts, int32_t n, const PillarGeom &g, int32_t *c
     return hipGetLastError();
 }
 
-hipError_t scan_reduce(const int32_t *counts, int32_t n_cells, int32_t *tile_sums, hipStream_t s) {
-    k_scan_reduce<<<blocks_for(n_cells, kScanTile), 256, 0, s>>>(counts, n_cells, tile_sums);
-    return hipGetLastError();
-}
-
-hipError_t scan_tiles(int32_t *tile_sums, int32_t n_tiles, int32_t *meta, hipStream_t s) {
-    k_scan_tiles<<<1, 256, 0, s>>>(tile_sums, n_tiles, meta);
+hipError_t scan_reduce(const int32_t *counts, int32_t n_cells, int32_t *tile_sums, int32_t *meta, hipStream_t s) {
+    k_scan_reduce<<<blocks_for(n_cells, kScanTile), 256, 0, s>>>(counts, n_cells, tile_sums, meta);
     return hipGetLastError();
 }
 

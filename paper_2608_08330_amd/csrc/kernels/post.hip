@@ -407,19 +407,6 @@ __global__ __launch_bounds__(256) void k_decode_count(DecodeArgs a) {
     if (threadIdx.x == 0) a.tile_counts[blockIdx.x] = tot;
 }
 
-__global__ __launch_bounds__(256) void k_decode_scan(DecodeArgs a, int32_t n_tiles) {
-    int carry = 0;
-    for (int base = 0; base < n_tiles; base += 256) {
-        const int i = base + threadIdx.x;
-        const int v = i < n_tiles ? a.tile_counts[i] : 0;
-        int tot;
-        const int ex = block_excl_scan256(v, &tot);
-        if (i < n_tiles) a.tile_counts[i] = carry + ex;
-        carry += tot;
-    }
-    if (threadIdx.x == 0) *a.count = carry;
-}
-
 __global__ __launch_bounds__(256) void k_decode_write(DecodeArgs a) {
     const int n_anchor = a.H2 * a.W2 * 2;
     const int base = blockIdx.x * kDecodeTile + threadIdx.x * kPerThread;
@@ -431,8 +418,15 @@ __global__ __launch_bounds__(256) void k_decode_write(DecodeArgs a) {
         keep[q] = ai < n_anchor && a.head[size_t(ai >> 1) * 16 + (ai & 1) * 8] > a.thr;
         c += keep[q];
     }
-    int tot;
-    int pos = a.tile_counts[blockIdx.x] + block_excl_scan256(c, &tot);
+    // this tile's first record: the counts of the tiles before it, summed
+    // by the block itself (no separate scan kernel); the last tile also
+    // writes the total
+    int before = 0;
+    for (int t = threadIdx.x; t < int(blockIdx.x); t += 256) before += a.tile_counts[t];
+    int prefix, tot;
+    block_excl_scan256(before, &prefix);
+    int pos = prefix + block_excl_scan256(c, &tot);
+    if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) *a.count = prefix + tot;
     const float diag = sqrtf(a.aw * a.aw + a.al * a.al);
 #pragma unroll
     for (int q = 0; q < kPerThread; ++q) {
@@ -493,9 +487,6 @@ hipError_t decode(const DecodeArgs &a, hipStream_t s) {
     const int n_tiles = (n_anchor + kDecodeTile - 1) / kDecodeTile;
     k_decode_count<<<n_tiles, 256, 0, s>>>(a);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    k_decode_scan<<<1, 256, 0, s>>>(a, n_tiles);
-    e = hipGetLastError();
     if (e != hipSuccess) return e;
     k_decode_write<<<n_tiles, 256, 0, s>>>(a);
     return hipGetLastError();
