@@ -41,14 +41,14 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 # commands in profiles/traffic_c5_bench.md).  Each figure holds only for the
 # kernel source it was taken on; after a change it reads null until re-taken.
 MEASURED_TRAFFIC = {
-    "conv": dict(src="paper_2608_08330_amd/csrc/kernels/igemm.hip", bytes=26.74e6,
+    "conv": dict(src="paper_2608_08330_amd/csrc/kernels/igemm.hip", bytes=26.73e6,
                  sha256="90a6cec7ffbd0011ebff14ca9359e122b8c5e344f748a4d9bd13a4c0845ad1f9"),
-    "warp_fuse": dict(src="paper_2608_08330_amd/csrc/kernels/post.hip", bytes=485.34e6,
-                      sha256="5b325c8ef097985c7823040a10c6a08e10b12e72443e7a0c624e24c899ee9b94"),
-    "fuse": dict(src="paper_2608_08330_amd/csrc/kernels/post.hip", bytes=453.03e6,
-                 sha256="5b325c8ef097985c7823040a10c6a08e10b12e72443e7a0c624e24c899ee9b94"),
-    "warp_slot": dict(src="paper_2608_08330_amd/csrc/kernels/post.hip", bytes=96.24e6,
-                      sha256="5b325c8ef097985c7823040a10c6a08e10b12e72443e7a0c624e24c899ee9b94"),
+    "warp_fuse": dict(src="paper_2608_08330_amd/csrc/kernels/post.hip", bytes=485.79e6,
+                      sha256="5fe5144baf9f560b5cda7c9a2d05c6af7d77cf266706260c3ba17a9502f3bde9"),
+    "fuse": dict(src="paper_2608_08330_amd/csrc/kernels/post.hip", bytes=453.01e6,
+                 sha256="5fe5144baf9f560b5cda7c9a2d05c6af7d77cf266706260c3ba17a9502f3bde9"),
+    "warp_slot": dict(src="paper_2608_08330_amd/csrc/kernels/post.hip", bytes=96.25e6,
+                      sha256="5fe5144baf9f560b5cda7c9a2d05c6af7d77cf266706260c3ba17a9502f3bde9"),
 }
 
 

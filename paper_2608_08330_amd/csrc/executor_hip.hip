@@ -80,6 +80,7 @@ class HipExecutor : public Executor {
             HIP_TRY(alloc(&b.d_poffs, n_max * 4));
             HIP_TRY(alloc(&b.d_overfull, over_cap * 4));
             HIP_TRY(alloc(&b.d_counts, n_cells * 4));
+            HIP_TRY(hipMemset(b.d_counts, 0, n_cells * 4));  // afterwards the PFN kernel leaves them zero
             HIP_TRY(alloc(&b.d_offsets, n_cells * 4));
             HIP_TRY(alloc(&b.d_tiles, n_tiles * 8));
             HIP_TRY(alloc(&b.d_meta, 64));
@@ -112,8 +113,7 @@ class HipExecutor : public Executor {
                 HIP_TRY(alloc(&d_fused_stage_[u.stage], size_t(u.Hi) * u.Wi * u.Ci * p.elt));
         HIP_TRY(alloc(&d_head, size_t(p.H2) * p.W2 * 16 * 4));
         n_anchor_ = size_t(p.H2) * p.W2 * 2;
-        const size_t dec_tiles = (n_anchor_ + kern::kDecodeTile - 1) / kern::kDecodeTile;
-        HIP_TRY(alloc(&d_dec_tiles, (dec_tiles + 1) * 4));
+        HIP_TRY(alloc(&d_head_counts, (size_t(p.H2) * p.W2 + 15) / 16 * 4));
         HIP_TRY(alloc(&d_rec, n_anchor_ * 9 * 4));
         HIP_TRY(alloc(&d_count, 64));
         nms_max_ = p.d.nms_max_candidates;
@@ -449,6 +449,7 @@ class HipExecutor : public Executor {
         const void *ego_map = nullptr;   // what the fusion reads when the warp is in the branch
         float affine[6] = {1, 0, 0, 0, 1, 0};
         bool warp_ran = false;           // the last frame ran a branch warp kernel
+        bool counts_zero = true;         // every enqueued K1 was followed by the PFN kernel
         hipEvent_t wev[2] = {nullptr, nullptr};  // bracket the branch warp kernel
         Graph graph;                     // the encoder as a HIP graph (use_graphs)
         std::vector<void *> d_act;
@@ -498,7 +499,10 @@ class HipExecutor : public Executor {
         ++ev;
         kern::PillarGeom g{p.d.x_min, p.d.x_max, p.d.y_min, p.d.y_max, p.d.z_min, p.d.z_max,
                            p.d.pillar_size, p.H, p.W};
-        HIP_TRY(kern::fill_i32(counts, n_cells, 0, s));
+        // The cell counts are zero unless an earlier enqueue stopped between
+        // K1 and the PFN kernel, which returns them to zero.
+        if (!b.counts_zero) HIP_TRY(kern::fill_i32(counts, n_cells, 0, s));
+        b.counts_zero = false;
         HIP_TRY(kern::cell_ids(b.src, n, g, static_cast<int32_t *>(b.d_cell), static_cast<int32_t *>(b.d_slot),
                                counts, s));
         HIP_TRY(kern::scan_reduce(counts, n_cells, tiles, meta, s));
@@ -531,6 +535,7 @@ class HipExecutor : public Executor {
         pa.z0 = p.d.z_min;
         pa.inv_dz = float(1.0 / (double(p.d.z_max) - double(p.d.z_min)));
         HIP_TRY(kern::pfn_canvas(p.bf16, pa, n < n_cells ? n : n_cells, s));
+        b.counts_zero = true;
         if (timing) HIP_TRY(hipEventRecord(b.ev[ev], s));
         ++ev;
 
@@ -671,7 +676,8 @@ class HipExecutor : public Executor {
         if (timing && p.d.multiscale) HIP_TRY(hipEventRecord(post_ev_[1], s));
         HIP_TRY(kern::head1x1(p.bf16, d_fused, static_cast<const char *>(d_mat) + p.head_w_off * p.elt,
                               static_cast<const float *>(d_bias) + p.head_b_off, static_cast<float *>(d_head),
-                              p.H2 * p.W2, p.c_slot, s));
+                              p.H2 * p.W2, p.c_slot, p.d.score_logit_threshold,
+                              static_cast<int32_t *>(d_head_counts), s));
         if (timing) HIP_TRY(hipEventRecord(post_ev_[2], s));
         return RTCC_OK;
     }
@@ -693,7 +699,7 @@ class HipExecutor : public Executor {
         da.az = p.d.anchor_z;
         da.ayaw0 = p.d.anchor_yaw[0];
         da.ayaw1 = p.d.anchor_yaw[1];
-        da.tile_counts = static_cast<int32_t *>(d_dec_tiles);
+        da.head_counts = static_cast<const int32_t *>(d_head_counts);
         da.rec = static_cast<float *>(d_rec);
         da.count = static_cast<int32_t *>(d_count);
         HIP_TRY(kern::decode(da, s));
@@ -850,7 +856,7 @@ class HipExecutor : public Executor {
     std::vector<void *> dev_allocs_;
     void *d_mat = nullptr, *d_bias = nullptr, *d_zero = nullptr;
     std::vector<kern::ConvPlan> plans_;
-    void *d_fused = nullptr, *d_head = nullptr, *d_dec_tiles = nullptr, *d_rec = nullptr, *d_count = nullptr;
+    void *d_fused = nullptr, *d_head = nullptr, *d_head_counts = nullptr, *d_rec = nullptr, *d_count = nullptr;
     int nms_max_ = 0;  // 0: no NMS
     void *d_nms_rank = nullptr, *d_nms_flag = nullptr, *d_nms_order = nullptr, *d_nms_foot = nullptr;
     void *d_nms_mask = nullptr, *d_nms_out = nullptr, *d_nms_count = nullptr;

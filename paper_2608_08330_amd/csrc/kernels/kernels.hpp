@@ -45,9 +45,10 @@ hipError_t overfull_select(const int32_t *overfull, const int32_t *meta, const i
 
 // K3: dense canvas [H*W][C]: per cell, channel max over the first
 // min(count, max_pts) members of ReLU(W^T f + b); zero for empty cells.
+// Leaves counts[] all zero, the state K1 expects at the next frame.
 struct PfnArgs {
     const float4 *sorted;  // points in segment order; each segment's first min(count, max_pts) are used
-    const int32_t *counts; // per cell (0: empty)
+    int32_t *counts;       // per cell (0: empty); zeroed by the kernel for the next frame
     const int32_t *pcells, *pcounts, *poffs;  // per pillar: cell, count, segment offset
     const int32_t *meta;   // meta[1] = number of pillars
     const float *w;  // [4][C]
@@ -136,9 +137,11 @@ struct FuseArgs {
 hipError_t fuse(bool bf16, bool attn, const FuseArgs &a, hipStream_t s, hipEvent_t start = nullptr,
                 hipEvent_t stop = nullptr);
 
-// 1x1 head: out[m][16] float32 = bias + Bt[16][C] . in[m][C].
+// 1x1 head: out[m][16] float32 = bias + Bt[16][C] . in[m][C].  counts[w]
+// (w < ceil(M / 16)) = anchors of pixels 16 w .. 16 w + 15 whose class
+// logit (output 0 or 8) is > thr: the decode's compaction offsets.
 hipError_t head1x1(bool bf16, const void *in, const void *wt, const float *bias, float *out,
-                   int32_t M, int32_t C, hipStream_t s);
+                   int32_t M, int32_t C, float thr, int32_t *counts, hipStream_t s);
 
 // Threshold and decode: anchors of [M][16] head outputs (2 anchors x 8).
 struct DecodeArgs {
@@ -147,7 +150,7 @@ struct DecodeArgs {
     float thr;
     float x0, y0, dx, dy;
     float aw, al, ah, az, ayaw0, ayaw1;
-    int32_t *tile_counts;  // [tiles + 1]
+    const int32_t *head_counts;  // [ceil(H2 W2 / 16)] from head1x1 with the same thr
     float *rec;            // [n_anchors][9]: box 7, score, index bits
     int32_t *count;        // total kept
 };

@@ -3,8 +3,8 @@
 // Deterministic counting sort by cell (no float atomics, no order-dependent
 // result):
 //   cell_ids        one thread per point: float32 cell index, atomic count
-//                   per cell; the returned old count is the point's rank of
-//                   arrival in its cell
+//                   per cell (the counts start at zero); the returned old
+//                   count is the point's rank of arrival in its cell
 //   scan_reduce /   exclusive prefix over all H*W cells -> segment offsets,
 //   scan_down       ascending list of non-empty cells (pillars) and their
 //                   counts, list of cells over the per-pillar point cap (each
@@ -15,7 +15,8 @@
 //                   value) to the front of the segment
 //   pfn_canvas      one lane per (cell, 8 channels): linear 4 -> C, ReLU,
 //                   max over the first min(count, cap) members; empty cells
-//                   are written as zeros, so no separate memset
+//                   are written as zeros, so no separate memset, and every
+//                   cell's count is returned to zero for the next frame
 // The only order-dependent intermediate is the order of members inside a
 // segment, and every consumer of it is order-independent (max, set
 // selection), so every output is bitwise reproducible.
@@ -254,7 +255,13 @@ __global__ __launch_bounds__(256) void k_pfn_canvas(PfnArgs a) {
         if (gid >= zero_threads) return;
         const int cell = int(gid / lanes_per_cell);
         const int ch = int(gid - int64_t(cell) * lanes_per_cell) * 8;
-        if (a.counts[cell] != 0) return;
+        // The lanes of a cell are consecutive lanes of one wavefront and read
+        // its count with the same load; the first of them then returns the
+        // count to zero, so the next frame's K1 starts from zeroed counts
+        // (nothing after this kernel reads them).
+        const int cnt = a.counts[cell];
+        if (cnt != 0 && ch == 0) a.counts[cell] = 0;
+        if (cnt != 0) return;
         if (BF16) {
             nt_store16(static_cast<uint16_t *>(a.canvas) + size_t(cell) * a.C + ch, make_uint4(0u, 0u, 0u, 0u));
         } else {

@@ -16,9 +16,10 @@
 //   reads) with the same arithmetic.
 // head1x1: one wavefront per 16 pixels; the 16 outputs of a pixel are one
 //   16 x 16 MFMA tile per 32 (bf16) or 16 (fp32) input channels.
-// decode: tile counts of kept anchors, one-block scan of the tile counts,
-//   then every tile rescans its flags and writes its kept anchors in
-//   ascending anchor order (stable compaction, deterministic).
+// decode: the head counts the kept anchors of each of its wavefronts;
+//   every decode tile adds up the counts before it, rescans its own flags
+//   and writes its kept anchors in ascending anchor order (stable
+//   compaction, deterministic).
 #include <hip/hip_ext.h>
 
 #include <cmath>
@@ -344,7 +345,7 @@ __device__ inline f32x4_t head_mma<float>(uint4 w, uint4 x, f32x4_t c) {
 template <typename T>
 __global__ __launch_bounds__(256) void k_head(const T *__restrict__ in, const T *__restrict__ wt,
                                               const float *__restrict__ bias, float *__restrict__ out,
-                                              int32_t M, int32_t C) {
+                                              int32_t M, int32_t C, float thr, int32_t *__restrict__ counts) {
     constexpr int EPV = 16 / sizeof(T);
     constexpr int BK = 4 * EPV;
     const int lane = threadIdx.x & 63;
@@ -360,11 +361,17 @@ __global__ __launch_bounds__(256) void k_head(const T *__restrict__ in, const T 
         if (ok) x = *reinterpret_cast<const uint4 *>(in + size_t(m) * C + k0 + fk * EPV);
         acc = head_mma<T>(w, x, acc);
     }
+    const int n = fk * 4;
+    const float v0 = acc[0] + bias[n];
     if (ok) {
-        const int n = fk * 4;
         *reinterpret_cast<float4 *>(out + size_t(m) * 16 + n) =
-            make_float4(acc[0] + bias[n], acc[1] + bias[n + 1], acc[2] + bias[n + 2], acc[3] + bias[n + 3]);
+            make_float4(v0, acc[1] + bias[n + 1], acc[2] + bias[n + 2], acc[3] + bias[n + 3]);
     }
+    // anchors of these 16 pixels above the class-logit threshold (output 0
+    // of anchor 0 in the lanes fk = 0, output 8 of anchor 1 in fk = 2), the
+    // same comparison of the same stored value that the decode makes
+    const unsigned long long kept = __ballot(ok && (fk == 0 || fk == 2) && v0 > thr);
+    if (lane == 0) counts[m0 >> 4] = __popcll(kept);
 }
 
 // ------------------------------------------------------------------ decode
@@ -392,20 +399,7 @@ __device__ inline int block_excl_scan256(int v, int *total) {
 }
 
 constexpr int kPerThread = kDecodeTile / 256;
-
-__global__ __launch_bounds__(256) void k_decode_count(DecodeArgs a) {
-    const int n_anchor = a.H2 * a.W2 * 2;
-    const int base = blockIdx.x * kDecodeTile + threadIdx.x * kPerThread;
-    int c = 0;
-#pragma unroll
-    for (int q = 0; q < kPerThread; ++q) {
-        const int ai = base + q;
-        if (ai < n_anchor) c += a.head[size_t(ai >> 1) * 16 + (ai & 1) * 8] > a.thr;
-    }
-    int tot;
-    block_excl_scan256(c, &tot);
-    if (threadIdx.x == 0) a.tile_counts[blockIdx.x] = tot;
-}
+static_assert(kDecodeTile % 256 == 0 && kDecodeTile % 32 == 0, "a decode tile is whole head wavefronts");
 
 __global__ __launch_bounds__(256) void k_decode_write(DecodeArgs a) {
     const int n_anchor = a.H2 * a.W2 * 2;
@@ -418,11 +412,12 @@ __global__ __launch_bounds__(256) void k_decode_write(DecodeArgs a) {
         keep[q] = ai < n_anchor && a.head[size_t(ai >> 1) * 16 + (ai & 1) * 8] > a.thr;
         c += keep[q];
     }
-    // this tile's first record: the counts of the tiles before it, summed
-    // by the block itself (no separate scan kernel); the last tile also
-    // writes the total
+    // this tile's first record: the kept anchors before it, summed by the
+    // block itself from the head's per-wavefront counts (a head wavefront
+    // covers 16 pixels, 32 anchors); the last tile also writes the total
+    constexpr int kHeadWavesPerTile = kDecodeTile / 32;
     int before = 0;
-    for (int t = threadIdx.x; t < int(blockIdx.x); t += 256) before += a.tile_counts[t];
+    for (int t = threadIdx.x; t < int(blockIdx.x) * kHeadWavesPerTile; t += 256) before += a.head_counts[t];
     int prefix, tot;
     block_excl_scan256(before, &prefix);
     int pos = prefix + block_excl_scan256(c, &tot);
@@ -471,23 +466,20 @@ hipError_t fuse(bool bf16, bool attn, const FuseArgs &a, hipStream_t s, hipEvent
 }
 
 hipError_t head1x1(bool bf16, const void *in, const void *wt, const float *bias, float *out,
-                   int32_t M, int32_t C, hipStream_t s) {
+                   int32_t M, int32_t C, float thr, int32_t *counts, hipStream_t s) {
     const unsigned g = unsigned((M + 63) / 64);
     if (bf16)
         k_head<uint16_t><<<g, 256, 0, s>>>(static_cast<const uint16_t *>(in),
-                                           static_cast<const uint16_t *>(wt), bias, out, M, C);
+                                           static_cast<const uint16_t *>(wt), bias, out, M, C, thr, counts);
     else
         k_head<float><<<g, 256, 0, s>>>(static_cast<const float *>(in), static_cast<const float *>(wt),
-                                        bias, out, M, C);
+                                        bias, out, M, C, thr, counts);
     return hipGetLastError();
 }
 
 hipError_t decode(const DecodeArgs &a, hipStream_t s) {
     const int n_anchor = a.H2 * a.W2 * 2;
     const int n_tiles = (n_anchor + kDecodeTile - 1) / kDecodeTile;
-    k_decode_count<<<n_tiles, 256, 0, s>>>(a);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
     k_decode_write<<<n_tiles, 256, 0, s>>>(a);
     return hipGetLastError();
 }

@@ -148,3 +148,17 @@ def test_max_points_exactly_and_ragged_tail():
         run_frame(ctx, fr)
         got = tensors(ctx, cfg)
     _check_frame(cfg, fr, ref, got)
+
+
+def test_consecutive_frames_with_different_points_match_oracle():
+    """No memset of the cell counts per frame (the PFN kernel returns them to
+    zero): frames of different point sets on one context, one of them with a
+    500-point cell and an empty agent, each match the oracle."""
+    cfg, fr_e = _edge_frame()
+    ref_e = N.forward(fr_e, keep=True)
+    fr_n, ref_n = _oracle("t_max")
+    with make_ctx(cfg, fr_e, max_points=cfg["n_points"]) as ctx:
+        for i, (fr, ref) in enumerate(((fr_n, ref_n), (fr_e, ref_e), (fr_n, ref_n), (fr_e, ref_e))):
+            _say("  frame %d" % i)
+            run_frame(ctx, fr)
+            _check_frame(cfg, fr, ref, tensors(ctx, cfg), with_stages=False)
