@@ -150,7 +150,7 @@ struct DecodeArgs {
     float thr;
     float x0, y0, dx, dy;
     float aw, al, ah, az, ayaw0, ayaw1;
-    const int32_t *head_counts;  // [ceil(H2 W2 / 16)] from head1x1 with the same thr
+    const int32_t *head_counts;  // [ceil(H2 W2 / 16)] from head1x1 with the same thr; 16-byte aligned
     float *rec;            // [n_anchors][9]: box 7, score, index bits
     int32_t *count;        // total kept
 };

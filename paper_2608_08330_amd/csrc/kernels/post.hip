@@ -414,10 +414,17 @@ __global__ __launch_bounds__(256) void k_decode_write(DecodeArgs a) {
     }
     // this tile's first record: the kept anchors before it, summed by the
     // block itself from the head's per-wavefront counts (a head wavefront
-    // covers 16 pixels, 32 anchors); the last tile also writes the total
+    // covers 16 pixels, 32 anchors; a tile 32 wavefronts, read as 16-byte
+    // vectors, several in flight per lane); the last tile also writes the total
     constexpr int kHeadWavesPerTile = kDecodeTile / 32;
+    const int4 *hc = reinterpret_cast<const int4 *>(a.head_counts);
+    const int nv = int(blockIdx.x) * (kHeadWavesPerTile / 4);
     int before = 0;
-    for (int t = threadIdx.x; t < int(blockIdx.x) * kHeadWavesPerTile; t += 256) before += a.head_counts[t];
+#pragma unroll 4
+    for (int t = threadIdx.x; t < nv; t += 256) {
+        const int4 v = hc[t];
+        before += (v.x + v.y) + (v.z + v.w);
+    }
     int prefix, tot;
     block_excl_scan256(before, &prefix);
     int pos = prefix + block_excl_scan256(c, &tot);
