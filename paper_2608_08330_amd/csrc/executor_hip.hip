@@ -84,7 +84,9 @@ class HipExecutor : public Executor {
             HIP_TRY(alloc(&b.d_offsets, n_cells * 4));
             HIP_TRY(alloc(&b.d_tiles, n_tiles * 8));
             HIP_TRY(alloc(&b.d_meta, 64));
+            HIP_TRY(hipMemset(b.d_meta, 0, 64));  // no pillars of a previous frame
             HIP_TRY(alloc(&b.d_canvas, n_cells * p.c_pfn * p.elt));
+            HIP_TRY(hipMemset(b.d_canvas, 0, n_cells * p.c_pfn * p.elt));  // then nonzero only at pillars
             b.d_act.resize(p.convs.size());
             for (size_t l = 0; l < p.convs.size(); ++l) {
                 const ConvLayer &c = p.convs[l];
@@ -449,7 +451,7 @@ class HipExecutor : public Executor {
         const void *ego_map = nullptr;   // what the fusion reads when the warp is in the branch
         float affine[6] = {1, 0, 0, 0, 1, 0};
         bool warp_ran = false;           // the last frame ran a branch warp kernel
-        bool counts_zero = true;         // every enqueued K1 was followed by the PFN kernel
+        bool pillars_clean = true;       // every enqueued K1 was followed by the PFN kernel
         hipEvent_t wev[2] = {nullptr, nullptr};  // bracket the branch warp kernel
         Graph graph;                     // the encoder as a HIP graph (use_graphs)
         std::vector<void *> d_act;
@@ -499,12 +501,18 @@ class HipExecutor : public Executor {
         ++ev;
         kern::PillarGeom g{p.d.x_min, p.d.x_max, p.d.y_min, p.d.y_max, p.d.z_min, p.d.z_max,
                            p.d.pillar_size, p.H, p.W};
-        // The cell counts are zero unless an earlier enqueue stopped between
-        // K1 and the PFN kernel, which returns them to zero.
-        if (!b.counts_zero) HIP_TRY(kern::fill_i32(counts, n_cells, 0, s));
-        b.counts_zero = false;
+        // Between frames the cell counts are zero and the canvas is zero
+        // outside the last frame's pillars (K1 clears those, the PFN kernel
+        // writes the new ones and zeroes their counts), unless an earlier
+        // enqueue stopped between the two: then both are reset here.
+        if (!b.pillars_clean) {
+            HIP_TRY(kern::fill_i32(counts, n_cells, 0, s));
+            HIP_TRY(kern::fill_i32(static_cast<int32_t *>(b.d_canvas), int64_t(n_cells) * p.c_pfn * p.elt / 4, 0, s));
+        }
+        b.pillars_clean = false;
+        const kern::CanvasClear cc{b.d_canvas, static_cast<const int32_t *>(b.d_pcells), meta, p.c_pfn};
         HIP_TRY(kern::cell_ids(b.src, n, g, static_cast<int32_t *>(b.d_cell), static_cast<int32_t *>(b.d_slot),
-                               counts, s));
+                               counts, p.bf16, cc, int32_t(std::min<int64_t>(p.n_max, n_cells)), s));
         HIP_TRY(kern::scan_reduce(counts, n_cells, tiles, meta, s));
         HIP_TRY(kern::scan_down(counts, n_cells, tiles, p.d.max_points_per_pillar, offsets,
                                 static_cast<int32_t *>(b.d_pcells), static_cast<int32_t *>(b.d_pcounts),
@@ -527,7 +535,6 @@ class HipExecutor : public Executor {
         pa.w = static_cast<const float *>(d_bias) + p.pfn_w_off;
         pa.b = static_cast<const float *>(d_bias) + p.pfn_b_off;
         pa.canvas = b.d_canvas;
-        pa.n_cells = n_cells;
         pa.C = p.c_pfn;
         pa.max_pts = p.d.max_points_per_pillar;
         pa.inv_hx = float(2.0 / (double(p.d.x_max) - double(p.d.x_min)));
@@ -535,7 +542,7 @@ class HipExecutor : public Executor {
         pa.z0 = p.d.z_min;
         pa.inv_dz = float(1.0 / (double(p.d.z_max) - double(p.d.z_min)));
         HIP_TRY(kern::pfn_canvas(p.bf16, pa, n < n_cells ? n : n_cells, s));
-        b.counts_zero = true;
+        b.pillars_clean = true;
         if (timing) HIP_TRY(hipEventRecord(b.ev[ev], s));
         ++ev;
 

@@ -20,10 +20,19 @@ constexpr int kScanTile = 2048;  // cells per block of the cell scans
 
 hipError_t fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s);
 
-// K1: cell id per point (-1 if dropped); counts[cell] += 1 and the point's
-// rank of arrival in its cell (an arbitrary order) goes to slot[i].
+// The previous frame's pillars, cleared in the canvas by K1.
+struct CanvasClear {
+    void *canvas;           // [H*W][C] in the activation dtype
+    const int32_t *pcells;  // pillar cells of the previous frame
+    const int32_t *meta;    // meta[1] = their number (0 before the first frame)
+    int32_t C;
+};
+// K1: cell id per point (-1 if dropped); counts[cell] += 1 (counts start at
+// zero) and the point's rank of arrival in its cell (an arbitrary order) goes
+// to slot[i].  The same launch zeroes the canvas cells of the previous
+// frame's pillars; max_prev_pillars bounds their number.
 hipError_t cell_ids(const float *pts, int32_t n, const PillarGeom &g, int32_t *cell, int32_t *slot,
-                    int32_t *counts, hipStream_t s);
+                    int32_t *counts, bool bf16, const CanvasClear &cc, int32_t max_prev_pillars, hipStream_t s);
 
 // K2a: per tile of kScanTile cells: (points, non-empty cells); zeroes
 // meta[2] (the overfull count of K2c).
@@ -43,18 +52,18 @@ hipError_t overfull_select(const int32_t *overfull, const int32_t *meta, const i
                            const int32_t *offsets, const float *pts, int32_t *member, float *sorted,
                            int32_t max_pts, int32_t n, hipStream_t s);
 
-// K3: dense canvas [H*W][C]: per cell, channel max over the first
-// min(count, max_pts) members of ReLU(W^T f + b); zero for empty cells.
-// Leaves counts[] all zero, the state K1 expects at the next frame.
+// K3: dense canvas [H*W][C]: per pillar cell, channel max over the first
+// min(count, max_pts) members of ReLU(W^T f + b).  Writes the pillar cells
+// only: every other cell must already be zero (K1 clears the previous
+// frame's pillars).  Leaves counts[] all zero, the state K1 expects next.
 struct PfnArgs {
     const float4 *sorted;  // points in segment order; each segment's first min(count, max_pts) are used
-    int32_t *counts;       // per cell (0: empty); zeroed by the kernel for the next frame
+    int32_t *counts;       // per cell; the pillars' counts are zeroed for the next frame
     const int32_t *pcells, *pcounts, *poffs;  // per pillar: cell, count, segment offset
     const int32_t *meta;   // meta[1] = number of pillars
     const float *w;  // [4][C]
     const float *b;  // [C]
     void *canvas;
-    int32_t n_cells;
     int32_t C;
     int32_t max_pts;
     float inv_hx, inv_hy, z0, inv_dz;

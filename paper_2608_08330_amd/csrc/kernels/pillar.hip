@@ -4,7 +4,9 @@
 // result):
 //   cell_ids        one thread per point: float32 cell index, atomic count
 //                   per cell (the counts start at zero); the returned old
-//                   count is the point's rank of arrival in its cell
+//                   count is the point's rank of arrival in its cell.  Extra
+//                   blocks clear the previous frame's pillars in the canvas
+//                   (the only cells of it that are not zero)
 //   scan_reduce /   exclusive prefix over all H*W cells -> segment offsets,
 //   scan_down       ascending list of non-empty cells (pillars) and their
 //                   counts, list of cells over the per-pillar point cap (each
@@ -13,10 +15,12 @@
 //   overfull_select for the few cells above the cap, one wavefront moves the
 //                   cap lowest point indices (found by bisection on the index
 //                   value) to the front of the segment
-//   pfn_canvas      one lane per (cell, 8 channels): linear 4 -> C, ReLU,
-//                   max over the first min(count, cap) members; empty cells
-//                   are written as zeros, so no separate memset, and every
-//                   cell's count is returned to zero for the next frame
+//   pfn_canvas      one lane per (pillar, 8 channels): linear 4 -> C, ReLU,
+//                   max over the first min(count, cap) members into the
+//                   pillar's cell; the pillar's count is returned to zero for
+//                   the next frame.  Empty cells keep the zeros they hold
+//                   (zeroed once at allocation, and their previous pillars
+//                   cleared by cell_ids)
 // The only order-dependent intermediate is the order of members inside a
 // segment, and every consumer of it is order-independent (max, set
 // selection), so every output is bitwise reproducible.
@@ -69,10 +73,35 @@ __global__ __launch_bounds__(256) void k_fill_i32(int32_t *p, int64_t n, int32_t
         p[i] = v;
 }
 
+// 16 bytes with the non-temporal hint: the canvas is read by the backbone,
+// not by the pillar kernels.
+__device__ inline void nt_store16(void *p, uint4 v) {
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    __builtin_nontemporal_store(u32x4{v.x, v.y, v.z, v.w}, static_cast<u32x4 *>(p));
+}
+
+template <bool BF16>
 __global__ __launch_bounds__(256) void k_cell_ids(const float4 *__restrict__ pts, int32_t n,
                                                   PillarGeom g, int32_t *__restrict__ cell,
                                                   int32_t *__restrict__ slot,
-                                                  int32_t *__restrict__ counts) {
+                                                  int32_t *__restrict__ counts, CanvasClear cc,
+                                                  int32_t point_blocks) {
+    if (int(blockIdx.x) >= point_blocks) {
+        // the previous frame's pillars back to zero, one lane per (pillar, 8
+        // channels); no other canvas cell holds anything but zeros
+        const int lanes = cc.C >> 3;
+        const int gid = (int(blockIdx.x) - point_blocks) * 256 + int(threadIdx.x);
+        const int p = gid / lanes;
+        if (p >= cc.meta[1]) return;
+        const size_t off = size_t(cc.pcells[p]) * cc.C + (gid - p * lanes) * 8;
+        if (BF16) {
+            nt_store16(static_cast<uint16_t *>(cc.canvas) + off, make_uint4(0u, 0u, 0u, 0u));
+        } else {
+            nt_store16(static_cast<float *>(cc.canvas) + off, make_uint4(0u, 0u, 0u, 0u));
+            nt_store16(static_cast<float *>(cc.canvas) + off + 4, make_uint4(0u, 0u, 0u, 0u));
+        }
+        return;
+    }
     const int i = blockIdx.x * 256 + threadIdx.x;
     if (i >= n) return;
     const float4 p = pts[i];
@@ -224,12 +253,6 @@ __global__ __launch_bounds__(256) void k_overfull_select(const int32_t *__restri
     }
 }
 
-// 16 bytes with the non-temporal hint: the canvas is read by the backbone,
-// not by this kernel.
-__device__ inline void nt_store16(void *p, uint4 v) {
-    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-    __builtin_nontemporal_store(u32x4{v.x, v.y, v.z, v.w}, static_cast<u32x4 *>(p));
-}
 
 __device__ inline uint32_t pack_bf16x2(float a, float b) {
     uint32_t ua = __float_as_uint(a), ub = __float_as_uint(b);
@@ -238,50 +261,27 @@ __device__ inline uint32_t pack_bf16x2(float a, float b) {
     return (ua >> 16) | (ub & 0xffff0000u);
 }
 
-// Two kinds of blocks.  The first cover the canvas, a lane per (cell, 8
-// channels), and write zeros into the empty cells; the others take the
-// pillars (the ascending list from the scan), a lane per (pillar, 8
-// channels), and write ReLU(W^T f + b) maxed over the pillar's first
-// min(count, max_pts) points, read in segment order from `sorted`.  Every
-// cell is written exactly once, and the pillar lanes read their cell,
-// count and segment offset together instead of through the cell grid.
+// A lane per (pillar, 8 channels) over the ascending pillar list from the
+// scan: ReLU(W^T f + b) maxed over the pillar's first min(count, max_pts)
+// points, read in segment order from `sorted`, into the pillar's cell.  The
+// lanes read the cell, count and segment offset together; the other cells
+// of the canvas already hold zeros.
 template <bool BF16>
 __global__ __launch_bounds__(256) void k_pfn_canvas(PfnArgs a) {
     const int lanes_per_cell = a.C >> 3;
-    const int64_t zero_threads = int64_t(a.n_cells) * lanes_per_cell;
-    const int zero_blocks = int((zero_threads + 255) / 256);
-    if (int(blockIdx.x) < zero_blocks) {
-        const int64_t gid = int64_t(blockIdx.x) * 256 + threadIdx.x;
-        if (gid >= zero_threads) return;
-        const int cell = int(gid / lanes_per_cell);
-        const int ch = int(gid - int64_t(cell) * lanes_per_cell) * 8;
-        // The lanes of a cell are consecutive lanes of one wavefront and read
-        // its count with the same load; the first of them then returns the
-        // count to zero, so the next frame's K1 starts from zeroed counts
-        // (nothing after this kernel reads them).
-        const int cnt = a.counts[cell];
-        if (cnt != 0 && ch == 0) a.counts[cell] = 0;
-        if (cnt != 0) return;
-        if (BF16) {
-            nt_store16(static_cast<uint16_t *>(a.canvas) + size_t(cell) * a.C + ch, make_uint4(0u, 0u, 0u, 0u));
-        } else {
-            float *dst = static_cast<float *>(a.canvas) + size_t(cell) * a.C + ch;
-            nt_store16(dst, make_uint4(0u, 0u, 0u, 0u));
-            nt_store16(dst + 4, make_uint4(0u, 0u, 0u, 0u));
-        }
-        return;
-    }
     // PFN weights and bias, read once per block into LDS (C <= 512)
     __shared__ float sw[5 * 512];
     for (int q = threadIdx.x; q < 5 * a.C; q += 256) sw[q] = q < 4 * a.C ? a.w[q] : a.b[q - 4 * a.C];
     __syncthreads();
-    const int gid = (int(blockIdx.x) - zero_blocks) * 256 + int(threadIdx.x);
+    const int gid = int(blockIdx.x) * 256 + int(threadIdx.x);
     const int p = gid / lanes_per_cell;
     const int ch = (gid - p * lanes_per_cell) * 8;
     if (p >= a.meta[1]) return;
     const int cell = a.pcells[p];
     const int cnt = a.pcounts[p];
     const int off = a.poffs[p];
+    // the cell's count back to zero, the state the next frame's K1 starts from
+    if (ch == 0) a.counts[cell] = 0;
     const int m = cnt < a.max_pts ? cnt : a.max_pts;
     float w0[8], w1[8], w2[8], w3[8], bb[8], mx[8];
 #pragma unroll
@@ -342,10 +342,16 @@ hipError_t fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s) {
 }
 
 hipError_t cell_ids(const float *pts, int32_t n, const PillarGeom &g, int32_t *cell, int32_t *slot,
-                    int32_t *counts, hipStream_t s) {
-    if (n <= 0) return hipSuccess;
-    k_cell_ids<<<blocks_for(n, 256), 256, 0, s>>>(reinterpret_cast<const float4 *>(pts), n, g, cell,
-                                                   slot, counts);
+                    int32_t *counts, bool bf16, const CanvasClear &cc, int32_t max_prev_pillars, hipStream_t s) {
+    const unsigned point_blocks = n > 0 ? blocks_for(n, 256) : 0u;
+    const unsigned blocks = point_blocks + blocks_for(int64_t(max_prev_pillars) * (cc.C >> 3), 256);
+    if (blocks == 0) return hipSuccess;
+    if (bf16)
+        k_cell_ids<true><<<blocks, 256, 0, s>>>(reinterpret_cast<const float4 *>(pts), n, g, cell, slot, counts, cc,
+                                                int32_t(point_blocks));
+    else
+        k_cell_ids<false><<<blocks, 256, 0, s>>>(reinterpret_cast<const float4 *>(pts), n, g, cell, slot, counts, cc,
+                                                 int32_t(point_blocks));
     return hipGetLastError();
 }
 
@@ -380,8 +386,8 @@ hipError_t overfull_select(const int32_t *overfull, const int32_t *meta, const i
 }
 
 hipError_t pfn_canvas(bool bf16, const PfnArgs &a, int32_t max_pillars, hipStream_t s) {
-    const int lanes = a.C / 8;
-    const unsigned blocks = blocks_for(int64_t(a.n_cells) * lanes, 256) + blocks_for(int64_t(max_pillars) * lanes, 256);
+    const unsigned blocks = blocks_for(int64_t(max_pillars) * (a.C / 8), 256);
+    if (blocks == 0) return hipSuccess;
     if (bf16) k_pfn_canvas<true><<<blocks, 256, 0, s>>>(a);
     else k_pfn_canvas<false><<<blocks, 256, 0, s>>>(a);
     return hipGetLastError();
