@@ -336,7 +336,9 @@ def main(argv=None):
         },
         "secondary_rooflines": {
             "pillar_pfn_canvas": {"bound": "hbm", "achieved": round(pil_bytes / (pillar_ms * 1e-3) / 1e9, 1),
-                                  "peak": PEAK_HBM_GBS, "unit": "GB/s"},
+                                  "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                                  "work": "16 n + 8 P + H*W*C_pfn*elt bytes (the dense canvas as output; the "
+                                          "kernels write the P pillar cells and clear the previous frame's)"},
         },
         "conv_layers": layers,
         "node_ms_mean": {
