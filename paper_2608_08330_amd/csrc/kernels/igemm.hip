@@ -772,7 +772,11 @@ hipError_t launch(const GemmArgs &a, hipStream_t s, hipEvent_t e0 = nullptr, hip
             default: break;
         }
     }
-    if (a.N % 128 == 0) return launch_cfg<T, 128, 128, 4, 2, 4, DECONV>(a, s, e0, e1);
+    // the upsamplings' short K loops (4 or 8 steps) run as fast with a
+    // 3-stage ring, whose 48 KB let more blocks share a CU
+    if (a.N % 128 == 0)
+        return DECONV ? launch_cfg<T, 128, 128, 4, 2, 3, DECONV>(a, s, e0, e1)
+                      : launch_cfg<T, 128, 128, 4, 2, 4, DECONV>(a, s, e0, e1);
     return launch_cfg<T, 128, 64, 4, 1, 4, DECONV>(a, s, e0, e1);
 }
 
