@@ -102,15 +102,17 @@ def _first_difference(ref, got):
     return bad or None
 
 
-def test_c5_per_branch_streams_match_serial_bitwise():
+@pytest.mark.parametrize("graphs", [0, 1], ids=["eager", "graphs"])
+def test_c5_per_branch_streams_match_serial_bitwise(graphs):
     """The per-branch-stream executor (every agent's encoder on its own
-    stream, concurrent with the others) against the single compute stream:
-    every tensor of the frame bitwise equal, with host-staged inputs, for a
-    release of all agents at once (barrier) and for staggered releases.
+    stream, concurrent with the others), launched kernel by kernel or as HIP
+    graphs (the benchmark's configuration), against the single compute
+    stream: every tensor of the frame bitwise equal, with host-staged inputs,
+    for a release of all agents at once (barrier) and for staggered releases.
     Concurrent encoders change the timing inside every kernel; this caught
     LDS buffers refilled while a slow wave still read the previous step."""
     import time
-    print("c5 per-branch streams vs serial", flush=True)
+    print("c5 per-branch streams vs serial, graphs=%d" % graphs, flush=True)
     cfg = synth.config("c5")
     fr = synth.make_frame(cfg)
     K = cfg["K"]
@@ -130,7 +132,7 @@ def test_c5_per_branch_streams_match_serial_bitwise():
     stagger = np.array([0.0, 0.0001, 0.0002, 0.0004, 0.0005, 0.0007, 0.0008, 0.001])
     with make_ctx(cfg, fr, exec=R.RTCC_EXEC_SERIAL) as ctx:
         det_ref, ref = run(ctx, R.RTCC_MODE_RELEASE, zero)
-    with make_ctx(cfg, fr, exec=R.RTCC_EXEC_PER_BRANCH_STREAMS) as ctx:
+    with make_ctx(cfg, fr, exec=R.RTCC_EXEC_PER_BRANCH_STREAMS, use_graphs=graphs) as ctx:
         for rep in range(4):
             for mode, arr in ((R.RTCC_MODE_BARRIER, zero), (R.RTCC_MODE_RELEASE, stagger),
                               (R.RTCC_MODE_RELEASE, zero)):
