@@ -7,8 +7,8 @@ shared encoder instance per agent (Sec. V-A1), whose features are stored in
 agent-indexed slots (Sec. IV-D) and, once all K encoders have finished,
 fused and passed to the detection heads (Sec. III-B).  The paper does not
 print the network's internals; the synthetic network here is the one of the
-workload descriptions in ``synth/configs.py``, and every reading of a point
-the paper leaves open is listed in the design doc.
+workload descriptions in ``synth/configs.py``; where the paper leaves a
+point open, the reading taken is stated at the function that applies it.
 
 Arithmetic is float64 except where a step is defined in lower precision:
   * the pillar cell index is computed in float32 (IEEE round-to-nearest

@@ -4,8 +4,7 @@ TEST INFRASTRUCTURE ONLY (see ``oracle/__init__.py``).
 
 The paper's primary latency endpoint T^det ends when the final detections
 exist: after box decoding, score thresholding and rotated NMS (Sec. V-A3).
-The paper does not spell the NMS out; the readings used here (all listed in
-DESIGN.md):
+The paper does not spell the NMS out; the readings used here:
   * the footprint of a box (x, y, z, w, l, h, yaw) is the rectangle centred
     at (x, y) whose side l lies along (cos yaw, sin yaw) and side w along
     (-sin yaw, cos yaw); overlap is the BEV intersection-over-union;

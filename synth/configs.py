@@ -6,7 +6,7 @@ pillar size, network widths, precision, fusion kind, detection threshold
 and the arrival-trace recipe.  The shapes follow the paper's fork-join
 detector (Sec. V-A1: a PointPillars-based intermediate-fusion detector with
 one shared encoder per agent); the concrete sizes are those of the five
-synthetic workloads this build is measured on.
+synthetic workloads the implementation is measured on.
 
 Grid sizes, layer shapes and every other derived quantity are computed by
 the consumers (oracle and library) on their own.
