@@ -10,6 +10,7 @@ import pytest
 
 from oracle import schedule as S
 from oracle import uplink as U
+from paper_2608_08330_amd import rtcc as L
 
 GOLD = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -173,3 +174,51 @@ def test_event_emitted_once_per_branch():
     # after completion an agent is never served again
     for k in range(3):
         assert res["x"][res["tau"][k]:, k].sum() == 0
+
+
+class _RecordingPolicy:
+    """Delegates to a policy and keeps its averages after every slot."""
+
+    def __init__(self, pol):
+        self.pol = pol
+        self.avgs = []
+
+    def pick(self, t, f, eligible, R, Q):
+        return self.pol.pick(t, f, eligible, R, Q)
+
+    def end_slot(self, x, R):
+        self.pol.end_slot(x, R)
+        self.avgs.append(self.pol.avg.copy())
+
+
+def _pf_golden():
+    with open(os.path.join(os.path.dirname(__file__), "golden", "pf_case.json")) as f:
+        return json.load(f)
+
+
+@pytest.mark.parametrize("case", [0, 1])
+def test_pf_ewma_matches_hand_computed_trace(case):
+    """Proportional fair (c4's scheduler): picks by R / Rbar and the EWMA
+    of every agent's served rate after every slot, against a five-slot
+    trace derived by hand in exact binary fractions."""
+    g = _pf_golden()
+    c = g["cases"][case]
+    R = np.asarray(g["rates"], dtype=np.float64).reshape(len(g["rates"]), g["K"], g["n_rb"])
+    pol = _RecordingPolicy(U.ProportionalFair(g["K"], g["window"], g["init_rate"]))
+    res = U.emulate(R, np.asarray(c["B_bits"]), g["slot_s"], pol)
+    served = [int(np.argmax(x[:, 0])) for x in res["x"]]
+    assert served == c["served"]
+    assert [a.tolist() for a in pol.avgs] == c["avg_after_slot"]
+    assert res["tau"].tolist() == c["completion_slot"]
+
+
+@pytest.mark.parametrize("case", [0, 1])
+def test_native_pf_matches_hand_computed_trace(case):
+    g = _pf_golden()
+    c = g["cases"][case]
+    R = np.asarray(g["rates"], dtype=np.float64).reshape(len(g["rates"]), g["K"], g["n_rb"])
+    done, alloc = L.rtcc_uplink_emulate(R, c["B_bits"], L.RTCC_SCHED_PROPORTIONAL_FAIR, g["slot_s"],
+                                        pf_window=g["window"], pf_init_rate=g["init_rate"], want_alloc=True,
+                                        kind="host")
+    assert alloc[:, 0].tolist() == c["served"]
+    assert done.tolist() == c["completion_slot"]
