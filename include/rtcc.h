@@ -79,8 +79,9 @@ typedef enum rtcc_precision { RTCC_PREC_FP32 = 0, RTCC_PREC_BF16 = 1 } rtcc_prec
 typedef enum rtcc_fusion { RTCC_FUSE_MAX = 0, RTCC_FUSE_ATTN = 1 } rtcc_fusion;
 
 /* Release rule.  RELEASE (RTCC): r_k = a_k, each branch is dispatched by its
- * own completion event.  BARRIER: events are validated and recorded; the
- * K-th valid event dispatches all K encoders in (A, k) = index order. */
+ * own completion event.  BARRIER: events are validated and recorded (the
+ * branch stays WAITING); the K-th valid event releases all K encoders at A
+ * and dispatches them in (A, k) = index order. */
 typedef enum rtcc_mode { RTCC_MODE_RELEASE = 0, RTCC_MODE_BARRIER = 1 } rtcc_mode;
 
 /* Executor.  PER_BRANCH_STREAMS: one HIP stream per agent plus a join
@@ -88,6 +89,11 @@ typedef enum rtcc_mode { RTCC_MODE_RELEASE = 0, RTCC_MODE_BARRIER = 1 } rtcc_mod
  * subgraph (the single-stream model of Sec. III-B), plus a copy stream. */
 typedef enum rtcc_exec { RTCC_EXEC_PER_BRANCH_STREAMS = 0, RTCC_EXEC_SERIAL = 1 } rtcc_exec;
 
+/* Branch state z_k (Sec. IV-C eq. branch_state, Alg. 1).  WAITING: input
+ * not complete, or (BARRIER) recorded but not yet released; RELEASED: input
+ * validated and encoder enqueued on the device; RUNNING: the device has
+ * reached the encoder (its input copy and earlier work of its stream are
+ * done); FINISHED: the encoder completed and its slot is stored. */
 typedef enum rtcc_branch_state {
     RTCC_WAITING = 0,
     RTCC_RELEASED = 1,
@@ -246,7 +252,10 @@ RTCC_API rtcc_status rtcc_begin_frame(rtcc_ctx *ctx, double t0_monotonic_s);
  * E_PREMATURE (now - t0 < arrival_t - tol).  A rejected event leaves the
  * branch WAITING.  RELEASE mode: enqueue the H2D copy and encoder E_k on
  * the branch stream and return without waiting.  BARRIER mode: record;
- * the K-th valid event enqueues all branches. */
+ * the K-th valid event enqueues all branches.  If an enqueue fails
+ * (E_HIP / E_NOMEM), that branch stays WAITING, later branches of a
+ * barrier release are not enqueued, and the frame's join returns
+ * E_STATE. */
 RTCC_API rtcc_status rtcc_release_branch(rtcc_ctx *ctx, int32_t agent, const float *host_points, int64_t n,
                                 const float pose[3], double arrival_t);
 
@@ -258,15 +267,18 @@ RTCC_API rtcc_status rtcc_release_branch(rtcc_ctx *ctx, int32_t agent, const flo
 RTCC_API rtcc_status rtcc_release_branch_device(rtcc_ctx *ctx, int32_t agent, const float *device_points,
                                        int64_t n, const float pose[3], double arrival_t);
 
-/* Join and detect.  If any branch is still WAITING the frame is
+/* Join and detect.  If any branch's input is undelivered the frame is
  * communication-infeasible: RTCC_E_INFEASIBLE, no fusion kernel is
- * launched and the frame is closed.  Otherwise wait (on the GPU) for every
+ * launched and the frame is closed.  If every input arrived but an
+ * encoder's enqueue failed: RTCC_E_STATE, likewise without fusion.
+ * Otherwise wait (on the GPU) for every
  * encoder, run warp, fusion, head, decode and (if enabled) rotated NMS, copy
  * the detections to the host and block until they are there.  out's arrays belong to the
  * context and stay valid until the next rtcc_begin_frame. */
 RTCC_API rtcc_status rtcc_join_and_detect(rtcc_ctx *ctx, rtcc_detections *out);
 
-/* State of one branch in the current or last frame. */
+/* State of one branch in the current or last frame (rtcc_branch_state);
+ * RUNNING and FINISHED are read from the device without blocking. */
 RTCC_API rtcc_status rtcc_get_branch_state(rtcc_ctx *ctx, int32_t agent, int32_t *state);
 
 /* Size in bytes of a tensor of the last completed frame (see

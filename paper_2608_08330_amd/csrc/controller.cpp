@@ -33,6 +33,8 @@ rtcc_status Controller::create(const rtcc_model_desc *d, const void *weights, si
     rtcc_status s = ex_->init(plan_, hw, opts_, err);
     if (s != RTCC_OK) return fail(s, err);
     z_.assign(plan_.K, RTCC_WAITING);
+    recorded_.assign(plan_.K, 0);
+    dispatched_.assign(plan_.K, 0);
     arrival_.assign(plan_.K, 0.0);
     dispatch_.assign(plan_.K, 0.0);
     affine_.assign(plan_.K, std::array<float, 6>{1, 0, 0, 0, 1, 0});
@@ -68,6 +70,9 @@ rtcc_status Controller::begin_frame(double t0) {
     t_begin_ = now_s();
     t0_ = t0;
     std::fill(z_.begin(), z_.end(), int(RTCC_WAITING));
+    std::fill(recorded_.begin(), recorded_.end(), char(0));
+    std::fill(dispatched_.begin(), dispatched_.end(), char(0));
+    dispatch_failed_ = false;
     std::fill(arrival_.begin(), arrival_.end(), 0.0);
     std::fill(dispatch_.begin(), dispatch_.end(), 0.0);
     pending_.clear();
@@ -76,13 +81,28 @@ rtcc_status Controller::begin_frame(double t0) {
     return RTCC_OK;
 }
 
+// Release and enqueue E_agent: z_k becomes RELEASED (input received, encoder
+// enqueued); RUNNING and FINISHED follow the device (refresh_state).  A
+// failed enqueue leaves the branch undispatched and marks the frame, whose
+// join then withholds the post-join subgraph.
 rtcc_status Controller::dispatch_locked(int agent, const float *pts, int64_t n, bool device_src) {
+    z_[agent] = RTCC_RELEASED;
     dispatch_[agent] = now_s() - t0_;
     std::string err;
     rtcc_status s = ex_->dispatch(agent, pts, n, device_src, affine_[agent].data(), err);
-    if (s != RTCC_OK) return fail(s, err);
-    z_[agent] = RTCC_RUNNING;
+    if (s != RTCC_OK) {
+        z_[agent] = RTCC_WAITING;  // not enqueued; its recorded event still makes a repeat a duplicate
+        dispatch_failed_ = true;
+        return fail(s, "dispatch of branch " + std::to_string(agent) + " failed: " + err);
+    }
+    dispatched_[agent] = 1;
     return RTCC_OK;
+}
+
+void Controller::refresh_state(int agent) {
+    if (!dispatched_[agent] || z_[agent] == RTCC_FINISHED) return;
+    const int st = RTCC_RELEASED + std::min(2, std::max(0, ex_->progress(agent)));
+    if (st > z_[agent]) z_[agent] = st;
 }
 
 rtcc_status Controller::release(int agent, const float *pts, int64_t n, const float pose[3],
@@ -90,7 +110,7 @@ rtcc_status Controller::release(int agent, const float *pts, int64_t n, const fl
     std::lock_guard<std::mutex> lk(mu_);
     if (!in_frame_) return fail(RTCC_E_STATE, "release outside a frame");
     if (agent < 0 || agent >= plan_.K) return fail(RTCC_E_ARG, "agent out of range");
-    if (z_[agent] != RTCC_WAITING) return fail(RTCC_E_DUPLICATE, "duplicate completion event");
+    if (z_[agent] != RTCC_WAITING || recorded_[agent]) return fail(RTCC_E_DUPLICATE, "duplicate completion event");
     if (n < 0 || n > plan_.n_max) return fail(RTCC_E_MALFORMED, "point count out of range");
     if (!pts && n > 0) return fail(RTCC_E_MALFORMED, "NULL points with n > 0");
     if (!pose || !std::isfinite(pose[0]) || !std::isfinite(pose[1]) || !std::isfinite(pose[2]))
@@ -109,22 +129,23 @@ rtcc_status Controller::release(int agent, const float *pts, int64_t n, const fl
     }
     pose_affine(plan_, pose, affine_[agent].data());
     pose_[agent] = {pose[0], pose[1], pose[2]};
-    z_[agent] = RTCC_RELEASED;
+    recorded_[agent] = 1;
     arrival_[agent] = arrival;
 
     if (mode_ == RTCC_MODE_RELEASE) return dispatch_locked(agent, pts, n, device_src);
 
+    // Barrier: the branch stays WAITING (its input is recorded, its release
+    // waits for A); the K-th valid event releases every encoder at
+    // A = max_k a_k, and the (r_k, k) order with equal r_k is index order.
     pending_.push_back(Pending{agent, arrival, pts, n, device_src});
     if (int(pending_.size()) < plan_.K) return RTCC_OK;
-    // Barrier: every encoder is released at A = max_k a_k; the (r_k, k)
-    // order with equal r_k is index order.
-    std::sort(pending_.begin(), pending_.end(),
-              [](const Pending &a, const Pending &b) { return a.agent < b.agent; });
-    for (const Pending &pd : pending_) {
+    std::vector<Pending> ready;
+    ready.swap(pending_);
+    std::sort(ready.begin(), ready.end(), [](const Pending &a, const Pending &b) { return a.agent < b.agent; });
+    for (const Pending &pd : ready) {
         rtcc_status s = dispatch_locked(pd.agent, pd.pts, pd.n, pd.device_src);
         if (s != RTCC_OK) return s;
     }
-    pending_.clear();
     return RTCC_OK;
 }
 
@@ -133,11 +154,22 @@ rtcc_status Controller::join(rtcc_detections *out) {
     if (!out) return fail(RTCC_E_ARG, "NULL output");
     if (!in_frame_) return fail(RTCC_E_STATE, "join outside a frame");
     for (int k = 0; k < plan_.K; ++k) {
-        if (z_[k] == RTCC_WAITING) {
+        if (!recorded_[k]) {
             // Communication-infeasible frame: the shared subgraph is withheld.
             in_frame_ = false;
             pending_.clear();
             return fail(RTCC_E_INFEASIBLE, "branch " + std::to_string(k) + " undelivered");
+        }
+    }
+    for (int k = 0; k < plan_.K; ++k) {
+        if (!dispatched_[k]) {
+            // Every input arrived but an encoder was never enqueued (its
+            // dispatch failed): its slot is stale, so no fusion runs.
+            in_frame_ = false;
+            pending_.clear();
+            return fail(RTCC_E_STATE, "branch " + std::to_string(k) +
+                                          (dispatch_failed_ ? " was not dispatched (a dispatch failed)"
+                                                            : " was not dispatched"));
         }
     }
     std::memset(out, 0, sizeof(*out));
@@ -145,6 +177,7 @@ rtcc_status Controller::join(rtcc_detections *out) {
     rtcc_status s = ex_->join(affine_, pose_, t_begin_ - t0_, out, err);
     in_frame_ = false;
     if (s != RTCC_OK) return fail(s, err);
+    // the post-join subgraph ran after every encoder's completion event
     for (int k = 0; k < plan_.K; ++k) z_[k] = RTCC_FINISHED;
     out->t_det_s = now_s() - t0_;
     out->n_agents = plan_.K;
@@ -160,6 +193,7 @@ rtcc_status Controller::branch_state(int agent, int32_t *state) {
     std::lock_guard<std::mutex> lk(mu_);
     if (!state) return fail(RTCC_E_ARG, "NULL output");
     if (agent < 0 || agent >= plan_.K) return fail(RTCC_E_ARG, "agent out of range");
+    refresh_state(agent);
     *state = z_[agent];
     return RTCC_OK;
 }

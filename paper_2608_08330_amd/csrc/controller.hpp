@@ -31,6 +31,10 @@ class Executor {
     // its last node.
     virtual rtcc_status dispatch(int agent, const float *pts, int64_t n, bool device_src, const float affine[6],
                                  std::string &err) = 0;
+    // Progress of a dispatched encoder on the device: 0 enqueued (its input
+    // copy or earlier work of its stream still ahead of it), 1 started, 2
+    // finished (its slot is stored).  Never blocks.
+    virtual int progress(int agent) = 0;
     // Wait for all encoders on the device, run the post-join subgraph with
     // the given per-agent warp affines (feature grid) and poses (for the
     // stage grids of multi-scale fusion), copy detections to the host.  Fills
@@ -89,6 +93,8 @@ class Controller {
         return s;
     }
     rtcc_status dispatch_locked(int agent, const float *pts, int64_t n, bool device_src);
+    // z_k of a dispatched branch follows its encoder on the device.
+    void refresh_state(int agent);
 
     std::mutex mu_;
     Executor *ex_;
@@ -100,6 +106,9 @@ class Controller {
     bool have_output_ = false;
     double t0_ = 0.0, t_begin_ = 0.0;
     std::vector<int> z_;
+    std::vector<char> recorded_;    // event validated in this frame (barrier: before A)
+    std::vector<char> dispatched_;  // encoder enqueued on the device in this frame
+    bool dispatch_failed_ = false;  // an enqueue failed: the frame cannot complete
     std::vector<double> arrival_, dispatch_;
     std::vector<std::array<float, 6>> affine_;
     std::vector<std::array<float, 3>> pose_;

@@ -101,6 +101,7 @@ class HipExecutor : public Executor {
             HIP_TRY(hipStreamCreateWithFlags(&b.stream, hipStreamNonBlocking));
             HIP_TRY(hipEventCreateWithFlags(&b.done, hipEventDisableTiming));
             HIP_TRY(hipEventCreateWithFlags(&b.h2d_done, hipEventDisableTiming));
+            HIP_TRY(hipEventCreateWithFlags(&b.started, hipEventDisableTiming));
             b.ev.resize(5 + p.convs.size() + p.ups.size());
             for (auto &e : b.ev) HIP_TRY(hipEventCreate(&e));
             b.kev.resize(2 * p.convs.size());
@@ -198,6 +199,9 @@ class HipExecutor : public Executor {
         b.src = src;
         b.n = int32_t(n);
         b.host_input = !device_src;
+        // reached once the input copy and everything queued before the
+        // encoder on its stream have completed: the encoder is running
+        HIP_TRY(hipEventRecord(b.started, cs));
         rtcc_status s;
         if (o_.use_graphs && !timing) {
             std::vector<unsigned char> key;
@@ -212,6 +216,13 @@ class HipExecutor : public Executor {
         HIP_TRY(hipEventRecord(b.done, cs));
         b.dispatched = true;
         return RTCC_OK;
+    }
+
+    int progress(int agent) override {
+        const Branch &b = br_[agent];
+        if (!b.dispatched) return 0;
+        if (hipEventQuery(b.done) == hipSuccess) return 2;
+        return hipEventQuery(b.started) == hipSuccess ? 1 : 0;
     }
 
     rtcc_status join(const std::vector<std::array<float, 6>> &affine,
@@ -456,7 +467,7 @@ class HipExecutor : public Executor {
         Graph graph;                     // the encoder as a HIP graph (use_graphs)
         std::vector<void *> d_act;
         hipStream_t stream = nullptr;
-        hipEvent_t done = nullptr, h2d_done = nullptr;
+        hipEvent_t done = nullptr, h2d_done = nullptr, started = nullptr;
         std::vector<hipEvent_t> ev;
         std::vector<hipEvent_t> kev;  // per conv layer: start / stop of its kernels
         const float *src = nullptr;
@@ -834,6 +845,7 @@ class HipExecutor : public Executor {
             if (b.stream) (void)hipStreamDestroy(b.stream);
             if (b.done) (void)hipEventDestroy(b.done);
             if (b.h2d_done) (void)hipEventDestroy(b.h2d_done);
+            if (b.started) (void)hipEventDestroy(b.started);
             for (hipEvent_t e : b.ev)
                 if (e) (void)hipEventDestroy(e);
             for (hipEvent_t e : b.kev)

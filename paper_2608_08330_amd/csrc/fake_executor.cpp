@@ -13,6 +13,10 @@ namespace rtcc {
 namespace {
 std::mutex g_log_mu;
 std::string g_log;
+// What the recording executor reports as device progress of each agent's
+// encoder (set by tests), and agents whose next dispatch fails.
+int g_progress[RTCC_MAX_AGENTS] = {};
+bool g_fail_dispatch[RTCC_MAX_AGENTS] = {};
 void log_line(const std::string &s) {
     std::lock_guard<std::mutex> lk(g_log_mu);
     g_log += s;
@@ -39,13 +43,26 @@ class FakeExecutor : public Executor {
         return RTCC_OK;
     }
     rtcc_status dispatch(int agent, const float *pts, int64_t n, bool device_src, const float affine[6],
-                         std::string &) override {
+                         std::string &err) override {
+        {
+            std::lock_guard<std::mutex> lk(g_log_mu);
+            g_progress[agent] = 0;
+            if (g_fail_dispatch[agent]) {
+                g_fail_dispatch[agent] = false;
+                err = "injected dispatch failure";
+                return RTCC_E_HIP;
+            }
+        }
         std::ostringstream os;
         os << "dispatch " << agent << " n=" << n << " src=" << (device_src ? "device" : "staging")
            << " staged=" << (pts == staging_[agent].data() ? 1 : 0) << " affine=[" << affine[0] << ","
            << affine[1] << "," << affine[2] << "," << affine[3] << "," << affine[4] << "," << affine[5] << "]";
         log_line(os.str());
         return RTCC_OK;
+    }
+    int progress(int agent) override {
+        std::lock_guard<std::mutex> lk(g_log_mu);
+        return g_progress[agent];
     }
     rtcc_status join(const std::vector<std::array<float, 6>> &affine, const std::vector<std::array<float, 3>> &,
                      double, rtcc_detections *out, std::string &) override {
@@ -96,6 +113,19 @@ extern "C" __attribute__((visibility("default"))) size_t rtcc_hosttest_log(char 
     }
     if (clear) rtcc::g_log.clear();
     return n;
+}
+
+// Device progress the recording executor reports for `agent` (0 enqueued,
+// 1 started, 2 finished) until its next dispatch.
+extern "C" __attribute__((visibility("default"))) void rtcc_hosttest_set_progress(int agent, int progress) {
+    std::lock_guard<std::mutex> lk(rtcc::g_log_mu);
+    if (agent >= 0 && agent < RTCC_MAX_AGENTS) rtcc::g_progress[agent] = progress;
+}
+
+// The next dispatch of `agent` fails with RTCC_E_HIP.
+extern "C" __attribute__((visibility("default"))) void rtcc_hosttest_fail_dispatch(int agent) {
+    std::lock_guard<std::mutex> lk(rtcc::g_log_mu);
+    if (agent >= 0 && agent < RTCC_MAX_AGENTS) rtcc::g_fail_dispatch[agent] = true;
 }
 
 namespace rtcc {

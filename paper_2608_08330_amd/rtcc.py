@@ -189,6 +189,10 @@ def load(kind="gpu"):
     if kind == "host":
         lib.rtcc_hosttest_log.restype = ctypes.c_size_t
         lib.rtcc_hosttest_log.argtypes = [ctypes.c_char_p, ctypes.c_size_t, ctypes.c_int]
+        lib.rtcc_hosttest_set_progress.restype = None
+        lib.rtcc_hosttest_set_progress.argtypes = [ctypes.c_int, ctypes.c_int]
+        lib.rtcc_hosttest_fail_dispatch.restype = None
+        lib.rtcc_hosttest_fail_dispatch.argtypes = [ctypes.c_int]
     _LIBS[kind] = lib
     return lib
 

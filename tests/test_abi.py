@@ -72,7 +72,8 @@ def test_release_mode_dispatches_each_branch_at_its_event(host_ctx):
     for i, k in enumerate(order):
         assert R.rtcc_get_branch_state(ctx, k) == R.RTCC_WAITING
         R.rtcc_release_branch(ctx, k, fr["points"][k], fr["poses"][k], 0.1 * i)
-        assert R.rtcc_get_branch_state(ctx, k) == R.RTCC_RUNNING
+        # released = input received and encoder enqueued (eq. branch_state)
+        assert R.rtcc_get_branch_state(ctx, k) == R.RTCC_RELEASED
         assert _host_log()[-1].startswith("dispatch %d " % k)
     det = R.rtcc_join_and_detect(ctx)
     assert all(R.rtcc_get_branch_state(ctx, k) == R.RTCC_FINISHED for k in range(4))
@@ -86,12 +87,71 @@ def test_barrier_mode_dispatches_all_at_last_event_in_index_order(host_ctx):
     R.rtcc_begin_frame(ctx, time.monotonic() - 10)
     for i, k in enumerate([3, 1, 2]):
         R.rtcc_release_branch(ctx, k, fr["points"][k], fr["poses"][k], 0.1 * i)
-        assert R.rtcc_get_branch_state(ctx, k) == R.RTCC_RELEASED
+        # recorded, not released: the barrier releases every encoder at A
+        assert R.rtcc_get_branch_state(ctx, k) == R.RTCC_WAITING
+        assert _status(R.rtcc_release_branch, ctx, k, fr["points"][k], fr["poses"][k], 0.0) == R.RTCC_E_DUPLICATE
     assert not any(l.startswith("dispatch") for l in _host_log(clear=False))
     R.rtcc_release_branch(ctx, 0, fr["points"][0], fr["poses"][0], 0.5)
     disp = [l.split()[1] for l in _host_log() if l.startswith("dispatch")]
     assert disp == ["0", "1", "2", "3"]
+    assert all(R.rtcc_get_branch_state(ctx, k) == R.RTCC_RELEASED for k in range(4))
     R.rtcc_join_and_detect(ctx)
+    assert all(R.rtcc_get_branch_state(ctx, k) == R.RTCC_FINISHED for k in range(4))
+
+
+def test_branch_state_follows_the_device(host_ctx):
+    """RELEASED -> RUNNING -> FINISHED as the executor reports the encoder
+    started and finished (eq. branch_state; Alg. 1): FINISHED at encoder
+    completion, before the join."""
+    cfg, fr, ctx = host_ctx
+    lib = R.load("host")
+    R.rtcc_set_mode(ctx, R.RTCC_MODE_RELEASE)
+    R.rtcc_begin_frame(ctx, time.monotonic() - 1)
+    for k in range(cfg["K"]):
+        R.rtcc_release_branch(ctx, k, fr["points"][k], fr["poses"][k], 0.0)
+    assert R.rtcc_get_branch_state(ctx, 1) == R.RTCC_RELEASED
+    lib.rtcc_hosttest_set_progress(1, 1)
+    assert R.rtcc_get_branch_state(ctx, 1) == R.RTCC_RUNNING
+    lib.rtcc_hosttest_set_progress(1, 2)
+    assert R.rtcc_get_branch_state(ctx, 1) == R.RTCC_FINISHED
+    # states never go back, and the others are untouched
+    lib.rtcc_hosttest_set_progress(1, 0)
+    assert R.rtcc_get_branch_state(ctx, 1) == R.RTCC_FINISHED
+    assert R.rtcc_get_branch_state(ctx, 0) == R.RTCC_RELEASED
+    lib.rtcc_hosttest_set_progress(2, 2)
+    assert R.rtcc_get_branch_state(ctx, 2) == R.RTCC_FINISHED
+    R.rtcc_join_and_detect(ctx)
+    assert all(R.rtcc_get_branch_state(ctx, k) == R.RTCC_FINISHED for k in range(cfg["K"]))
+
+
+@pytest.mark.parametrize("mode", ["release", "barrier"])
+def test_failed_dispatch_withholds_the_join(host_ctx, mode):
+    """An encoder whose enqueue fails never reaches its slot: the join
+    returns an error without running the post-join subgraph, the other
+    branches of a barrier release are not dispatched, and the next frame
+    runs normally."""
+    cfg, fr, ctx = host_ctx
+    lib = R.load("host")
+    R.rtcc_set_mode(ctx, R.RTCC_MODE_BARRIER if mode == "barrier" else R.RTCC_MODE_RELEASE)
+    R.rtcc_begin_frame(ctx, time.monotonic() - 1)
+    lib.rtcc_hosttest_fail_dispatch(1)
+    st = [_status(R.rtcc_release_branch, ctx, k, fr["points"][k], fr["poses"][k], 0.0) for k in range(cfg["K"])]
+    if mode == "release":
+        assert st == [R.RTCC_OK, R.RTCC_E_HIP, R.RTCC_OK, R.RTCC_OK]
+    else:
+        assert st == [R.RTCC_OK, R.RTCC_OK, R.RTCC_OK, R.RTCC_E_HIP]
+    assert R.rtcc_get_branch_state(ctx, 1) == R.RTCC_WAITING
+    disp = [l.split()[1] for l in _host_log() if l.startswith("dispatch")]
+    assert disp == (["0", "2", "3"] if mode == "release" else ["0"])
+    # a repeated event for the failed branch is still a duplicate
+    assert _status(R.rtcc_release_branch, ctx, 1, fr["points"][1], fr["poses"][1], 0.0) == R.RTCC_E_DUPLICATE
+    assert _status(R.rtcc_join_and_detect, ctx) == R.RTCC_E_STATE
+    assert not any(l.startswith("join") for l in _host_log())
+    R.rtcc_begin_frame(ctx, time.monotonic() - 1)
+    for k in range(cfg["K"]):
+        R.rtcc_release_branch(ctx, k, fr["points"][k], fr["poses"][k], 0.0)
+    R.rtcc_join_and_detect(ctx)
+    assert any(l.startswith("join") for l in _host_log())
 
 
 def test_validation_errors_leave_branch_waiting(host_ctx):
