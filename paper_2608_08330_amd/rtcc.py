@@ -170,6 +170,9 @@ _LIBS = {}
 
 
 def lib_path(kind="gpu"):
+    if kind == "host" and os.environ.get("RTCC_HOSTTEST_LIB"):
+        # a sanitizer build of the host test library (build_sanitize.py)
+        return os.environ["RTCC_HOSTTEST_LIB"]
     return os.path.join(LIB_DIR, "librtcc.so" if kind == "gpu" else "librtcc_hosttest.so")
 
 
