@@ -327,13 +327,17 @@ RTCC_API rtcc_status rtcc_graph_stats(rtcc_ctx *ctx, int64_t *counts);
  * NMS end T^det).  On the current HIP device, synchronous.
  *   device_records: [n][9] float32 x, y, z, w, l, h, yaw, score, anchor
  *     index (int32 bit pattern), in ascending anchor index (ties in score
- *     rank by it);
+ *     rank by it); any non-NaN score ranks by its value (negative scores,
+ *     raw logits for instance, included; -0 equals +0).  Every write to the
+ *     records must be complete before the call (synchronise the stream that
+ *     produced them): the call runs on a stream of its own;
  *   max_candidates, iou_threshold: as nms_max_candidates / nms_iou_threshold
  *     of rtcc_model_desc (1 .. 16384, [0, 1]);
  *   device_out: [min(n, max_candidates)][9] float32, receives the kept
  *     records in ascending anchor index; *kept their number.
  * n = 0 keeps nothing.  E_ARG for NULL pointers with n > 0, n < 0,
- * n > 2^31 - 1 or parameters out of range; E_NOMEM / E_HIP for device
+ * n > 2^31 - 1, parameters out of range, or a NaN score (found on the
+ * device; device_out is then undefined); E_NOMEM / E_HIP for device
  * errors.  Scratch memory is allocated and freed inside the call.  The
  * message of a failure is rtcc_last_error(NULL). */
 RTCC_API rtcc_status rtcc_rotated_nms(const float *device_records, int64_t n, int32_t max_candidates,

@@ -186,6 +186,7 @@ struct NmsArgs {
     int32_t *out_count;           // kept, on the device
     double iou_threshold;         // suppress iff IoU > threshold
     int32_t max_candidates;       // 1 .. kNmsMaxCandidates
+    int32_t *bad_score = nullptr; // optional: set to 1 if a score is NaN (the caller clears it)
 };
 // max_records bounds n (the grid of the per-record kernels).
 hipError_t rotated_nms(const NmsArgs &a, int64_t max_records, hipStream_t s);

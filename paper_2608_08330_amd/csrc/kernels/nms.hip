@@ -47,13 +47,18 @@ namespace {
 constexpr int kRecFloats = 9;
 constexpr int kFoot = kNmsFootDoubles;  // x, y, w, l, cos, sin, valid, circumradius
 
-// Ranking key of record i: the score's bit pattern above the complement of
-// i.  Scores are sigmoids (>= +0), whose bit patterns order like the
-// values, so key_j > key_i iff record j precedes record i (higher score, or
-// equal score and lower index).
+// Ranking key of record i: an order-preserving image of the score above the
+// complement of i, so key_j > key_i iff record j precedes record i (higher
+// score, or equal score and lower index).  The image flips the sign bit of
+// a non-negative float and every bit of a negative one, which orders all
+// finite and infinite values like the numbers (-0 is taken as +0); a NaN
+// maps to 0 and ranks after every number (callers reject NaN scores).
 __device__ inline unsigned long long rank_key(const NmsArgs &a, int i) {
-    const uint32_t bits = __float_as_uint(a.rec[size_t(i) * kRecFloats + 7]);
-    return (static_cast<unsigned long long>(bits) << 32) | (0xffffffffu - uint32_t(i));
+    const float sc = a.rec[size_t(i) * kRecFloats + 7];
+    uint32_t bits = sc == 0.f ? 0u : __float_as_uint(sc);
+    uint32_t ord = (bits >> 31) ? ~bits : (bits | 0x80000000u);
+    if (sc != sc) ord = 0u;
+    return (static_cast<unsigned long long>(ord) << 32) | (0xffffffffu - uint32_t(i));
 }
 
 // Blocks (tile I of 256 records, split v of the key tiles): each thread
@@ -69,6 +74,10 @@ __global__ __launch_bounds__(256) void k_nms_rank(NmsArgs a) {
         const int I = item / S, v = item - (item / S) * S;
         const int i = I * 256 + int(threadIdx.x);
         const unsigned long long ki = i < n ? rank_key(a, i) : ~0ull;
+        if (a.bad_score && v == 0 && i < n) {
+            const float sc = a.rec[size_t(i) * kRecFloats + 7];
+            if (sc != sc) *a.bad_score = 1;
+        }
         int r = 0;
         for (int J = v; J < T; J += S) {
             const int j0 = J * 256;

@@ -58,9 +58,10 @@ extern "C" RTCC_API rtcc_status rtcc_rotated_nms(const float *device_records, in
     hipStream_t s = nullptr;
     hipError_t e = hipStreamCreateWithFlags(&s, hipStreamNonBlocking);
     if (e != hipSuccess) return hip_fail(e, "hipStreamCreateWithFlags");
-    const int32_t n32 = int32_t(n);
+    // count[0] = n, count[1] = kept, count[2] = NaN-score flag
+    const int32_t init[3] = {int32_t(n), 0, 0};
     int32_t *count = static_cast<int32_t *>(sc.p[5]);
-    int32_t host_kept = 0;
+    int32_t host_out[2] = {0, 0};
     rtcc::kern::NmsArgs a{};
     a.rec = device_records;
     a.count = count;
@@ -75,14 +76,16 @@ extern "C" RTCC_API rtcc_status rtcc_rotated_nms(const float *device_records, in
     a.colcount = static_cast<int32_t *>(sc.p[9]);
     a.out = device_out;
     a.out_count = count + 1;
+    a.bad_score = count + 2;
     a.iou_threshold = double(iou_threshold);
     a.max_candidates = max_candidates;
-    e = hipMemcpyAsync(count, &n32, 4, hipMemcpyHostToDevice, s);
+    e = hipMemcpyAsync(count, init, sizeof(init), hipMemcpyHostToDevice, s);
     if (e == hipSuccess) e = rtcc::kern::rotated_nms(a, n, s);
-    if (e == hipSuccess) e = hipMemcpyAsync(&host_kept, count + 1, 4, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(host_out, count + 1, sizeof(host_out), hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     (void)hipStreamDestroy(s);
     if (e != hipSuccess) return hip_fail(e, "rotated NMS");
-    *kept = host_kept;
+    if (host_out[1]) return fail(RTCC_E_ARG, "a record's score is NaN (no defined ranking)");
+    *kept = host_out[0];
     return RTCC_OK;
 }

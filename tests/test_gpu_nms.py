@@ -136,3 +136,30 @@ def test_shared_edges_and_nearly_parallel_edges():
     anchors = np.arange(n, dtype=np.int32) * 3
     for thr in (0.15, 0.5):
         _check(boxes, scores, anchors, 4096, thr, "grid thr %g" % thr)
+
+
+def test_negative_and_signed_zero_scores():
+    """Scores of either sign (raw logits, say) rank by value: negative scores
+    rank below positive ones and among themselves by magnitude, -0 ties +0
+    (broken by anchor index), infinities at the ends."""
+    rng = np.random.default_rng(31)
+    boxes, _, anchors = _scene(rng, 800, 12.0, 6)
+    scores = rng.normal(0.0, 3.0, 800).astype(np.float32)
+    scores[:40] = -scores[40:80]           # mirrored pairs
+    scores[100:110] = 0.0
+    scores[110:120] = -0.0
+    scores[200] = np.inf
+    scores[201] = -np.inf
+    for cap, thr in ((4096, 0.15), (300, 0.15), (4096, 0.0)):
+        kept = _check(boxes, scores, anchors, cap, thr, "signed cap %d thr %g" % (cap, thr))
+        assert kept > 0
+
+
+def test_nan_score_rejected():
+    rng = np.random.default_rng(32)
+    boxes, scores, anchors = _scene(rng, 50, 5.0)
+    scores[17] = np.nan
+    rec = _records(boxes, scores, anchors)
+    with pytest.raises(R.RtccError) as e:
+        _gpu_nms(rec, 64, 0.15)
+    assert e.value.status == R.RTCC_E_ARG
