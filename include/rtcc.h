@@ -58,7 +58,7 @@ extern "C" {
 #define RTCC_API
 #endif
 
-#define RTCC_ABI_VERSION 5
+#define RTCC_ABI_VERSION 6
 #define RTCC_MAX_AGENTS 16
 #define RTCC_MAX_STAGES 4
 
@@ -159,6 +159,15 @@ typedef struct rtcc_model_desc {
     int32_t multiscale;
 } rtcc_model_desc;
 
+/* Optional device-memory hook: every device buffer of a context (weights,
+ * activations, slots, scratch) comes from dev_alloc and goes back through
+ * dev_free at rtcc_destroy, e.g. PyTorch's caching allocator.  dev_alloc
+ * returns NULL on failure (rtcc_create then fails with RTCC_E_NOMEM); the
+ * memory must stay valid until dev_free.  Pinned host staging is always
+ * hipHostMalloc. */
+typedef void *(*rtcc_dev_alloc_fn)(size_t bytes, void *user);
+typedef void (*rtcc_dev_free_fn)(void *ptr, void *user);
+
 typedef struct rtcc_runtime_opts {
     int32_t exec;          /* rtcc_exec                                              */
     int32_t use_graphs;    /* 1: each branch's encoder (after the input copy) and the
@@ -169,6 +178,24 @@ typedef struct rtcc_runtime_opts {
     int32_t node_timing;   /* 1: record HIP events around every node of every frame  */
     int32_t device;        /* HIP device ordinal                                     */
     double premature_tol_s;/* an event with arrival_t > now - t0 + tol is premature  */
+    /* Tiling override of the 3x3 convolutions (tests and tuning; results are
+     * the same function of the inputs, within rounding of the summation
+     * order): 0 = the per-layer plan; 1..6 = that halo tiling (1: 8 x 16
+     * pixels x 128 channels, 2: 4 x 16 x 128, 3 / 4: the stride-2 forms of 1
+     * / 2, 5: 4 x 16 x 64 in two wave groups, 6: its stride-2 form) on every
+     * layer whose stride and channels it supports, the plan elsewhere; 7 =
+     * the implicit GEMM on every layer.  conv_splits (0 or 1: none) splits
+     * the K loop of the forced layers where it divides evenly. */
+    int32_t conv_variant;
+    int32_t conv_splits;
+    rtcc_dev_alloc_fn dev_alloc;  /* NULL: hipMalloc / hipFree                     */
+    rtcc_dev_free_fn dev_free;    /* required with dev_alloc                       */
+    void *alloc_user;             /* passed to dev_alloc / dev_free                */
+    /* Optional hipStream_t of the context's device on which the post-join
+     * subgraph (and, with the SERIAL executor, every encoder) runs, e.g. the
+     * caller's PyTorch stream; NULL: a stream of the context's own.  Not
+     * destroyed by the library. */
+    void *join_stream;
 } rtcc_runtime_opts;
 
 typedef struct rtcc_detections {
@@ -198,8 +225,16 @@ typedef enum rtcc_tensor_id {
                                  yaw, score, anchor index (int32 bits); ascending anchor    */
     RTCC_T_WARPED = 8,        /* [H2, W2, C] stored dtype, the agent's ego-frame map when
                                  warp_in_branch = 1 (E_ARG otherwise)               (agent) */
-    RTCC_T_FUSED_STAGE = 9    /* [Hs, Ws, Cs] stored dtype, fused map of stage `agent` when
+    RTCC_T_FUSED_STAGE = 9,   /* [Hs, Ws, Cs] stored dtype, fused map of stage `agent` when
                                  multiscale = 1 (E_ARG otherwise)                           */
+    RTCC_T_PILLAR_MEMBERS = 10,/* int32 [sum_p min(count_p, max_points_per_pillar)]: the
+                                 points each pillar fed to the PFN, as original indices,
+                                 pillar by pillar in ascending cell order, ascending
+                                 within a pillar (the order inside a pillar's segment on
+                                 the device is arbitrary; this readback sorts it)   (agent) */
+    RTCC_T_CONV_OUT = 11      /* [Ho, Wo, Co] stored dtype, output of 3x3 conv layer
+                                 `agent >> 8` (0-based over all stages), agent
+                                 `agent & 255`                                              */
 } rtcc_tensor_id;
 
 typedef struct rtcc_ctx rtcc_ctx;
@@ -313,6 +348,13 @@ RTCC_API rtcc_status rtcc_profile_nodes(rtcc_ctx *ctx, int32_t warmup, int32_t r
  * at least rtcc_node_count() floats. */
 RTCC_API rtcc_status rtcc_node_times(rtcc_ctx *ctx, float *ms, int32_t *n);
 RTCC_API rtcc_status rtcc_node_count(rtcc_ctx *ctx, int32_t *n);
+
+/* Kernel tiling of 3x3 conv layer `layer` (0-based over all stages):
+ * plan[0] = 0 implicit GEMM, 1..6 the halo tilings of
+ * rtcc_runtime_opts.conv_variant; plan[1] = K slices (1 = unsplit).  plan:
+ * caller-owned int32_t[2].  Errors: RTCC_E_ARG (NULL or layer out of
+ * range), RTCC_E_STATE (the host test library has no kernels). */
+RTCC_API rtcc_status rtcc_conv_plan(rtcc_ctx *ctx, int32_t layer, int32_t *plan);
 
 /* With opts.use_graphs = 1: counts[0] = HIP graphs instantiated, counts[1] =
  * in-place updates attempted (a branch or the join whose arguments changed

@@ -116,6 +116,11 @@ rtcc_status rtcc_node_count(rtcc_ctx *ctx, int32_t *n) {
     return guarded([&] { return ctx->ctl.node_count(n); });
 }
 
+rtcc_status rtcc_conv_plan(rtcc_ctx *ctx, int32_t layer, int32_t *plan) {
+    if (!ctx) return RTCC_E_ARG;
+    return guarded([&] { return ctx->ctl.conv_plan(layer, plan); });
+}
+
 rtcc_status rtcc_graph_stats(rtcc_ctx *ctx, int64_t *counts) {
     if (!ctx) return RTCC_E_ARG;
     return guarded([&] { return ctx->ctl.graph_stats(counts); });

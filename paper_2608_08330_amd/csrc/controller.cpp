@@ -26,6 +26,10 @@ rtcc_status Controller::create(const rtcc_model_desc *d, const void *weights, si
         return fail(RTCC_E_ARG, "premature_tol_s must be finite and >= 0");
     if ((o.use_graphs != 0 && o.use_graphs != 1) || (o.node_timing != 0 && o.node_timing != 1))
         return fail(RTCC_E_ARG, "use_graphs and node_timing must be 0 or 1");
+    if (o.conv_variant < 0 || o.conv_variant > 7 || o.conv_splits < 0 || o.conv_splits > 64)
+        return fail(RTCC_E_ARG, "conv_variant must be in [0, 7] and conv_splits in [0, 64]");
+    if ((o.dev_alloc == nullptr) != (o.dev_free == nullptr))
+        return fail(RTCC_E_ARG, "dev_alloc and dev_free must be given together");
     opts_ = o;
     HostWeights hw;
     if (!prepare_weights(plan_, static_cast<const float *>(weights), bytes / 4, hw, err))
@@ -244,6 +248,14 @@ rtcc_status Controller::node_count(int32_t *n) {
     std::lock_guard<std::mutex> lk(mu_);
     if (!n) return fail(RTCC_E_ARG, "NULL output");
     *n = ex_->node_count();
+    return RTCC_OK;
+}
+
+rtcc_status Controller::conv_plan(int layer, int32_t out[2]) {
+    std::lock_guard<std::mutex> lk(mu_);
+    if (!out) return fail(RTCC_E_ARG, "NULL output");
+    if (layer < 0 || layer >= int(plan_.convs.size())) return fail(RTCC_E_ARG, "layer out of range");
+    if (!ex_->conv_plan(layer, out)) return fail(RTCC_E_STATE, "no kernel plan in this executor");
     return RTCC_OK;
 }
 

@@ -51,6 +51,13 @@ class Executor {
     virtual rtcc_status node_times(float *ms, int *n, std::string &err) = 0;
     // HIP graph instantiations, in-place update attempts and launches so far.
     virtual void graph_stats(int64_t out[3]) const { out[0] = out[1] = out[2] = 0; }
+    // Kernel tiling and K split of 3x3 conv layer `layer` (false if out of
+    // range).
+    virtual bool conv_plan(int layer, int32_t out[2]) const {
+        (void)layer;
+        out[0] = out[1] = 0;
+        return false;
+    }
 };
 
 // Defined by exactly one executor translation unit of a build.
@@ -84,6 +91,7 @@ class Controller {
     rtcc_status node_times(float *ms, int32_t *n);
     rtcc_status node_count(int32_t *n);
     rtcc_status graph_stats(int64_t out[3]);
+    rtcc_status conv_plan(int layer, int32_t out[2]);
 
     const char *last_error() const { return err_.c_str(); }
 

@@ -61,7 +61,10 @@ class HipExecutor : public Executor {
         plans_.clear();
         size_t ws_bytes = 0;
         for (const ConvLayer &c : p.convs) {
-            plans_.push_back(kern::conv_plan(p.bf16, c.Hi, c.Wi, c.Ci, c.Ho, c.Wo, c.Co, c.stride, n_cu));
+            kern::ConvPlan cp = kern::conv_plan(p.bf16, c.Hi, c.Wi, c.Ci, c.Ho, c.Wo, c.Co, c.stride, n_cu);
+            if (o.conv_variant > 0)
+                cp = kern::conv_plan_forced(p.bf16, cp, o.conv_variant, o.conv_splits, c.Ci, c.Ho, c.Wo, c.Co, c.stride);
+            plans_.push_back(cp);
             ws_bytes = std::max(ws_bytes, plans_.back().ws_bytes);
         }
         HIP_TRY(alloc(&d_zero, 256));
@@ -139,7 +142,12 @@ class HipExecutor : public Executor {
         boxes_.resize(n_anchor_ * 7);
         scores_.resize(n_anchor_);
         aidx_.resize(n_anchor_);
-        HIP_TRY(hipStreamCreateWithFlags(&join_stream_, hipStreamNonBlocking));
+        if (o.join_stream) {
+            join_stream_ = static_cast<hipStream_t>(o.join_stream);
+            own_join_stream_ = false;
+        } else {
+            HIP_TRY(hipStreamCreateWithFlags(&join_stream_, hipStreamNonBlocking));
+        }
         HIP_TRY(hipStreamCreateWithFlags(&copy_stream_, hipStreamNonBlocking));
         HIP_TRY(hipStreamCreateWithFlags(&aux_stream_, hipStreamNonBlocking));
         HIP_TRY(hipStreamCreateWithFlags(&cap_stream_, hipStreamNonBlocking));
@@ -288,11 +296,28 @@ class HipExecutor : public Executor {
     }
 
     rtcc_status tensor_bytes(int id, int agent, size_t *bytes, std::string &err) override {
+        if (id == RTCC_T_PILLAR_MEMBERS) {
+            std::vector<int32_t> m;
+            rtcc_status s = used_members(agent, m, err);
+            if (s == RTCC_OK) *bytes = m.size() * 4;
+            return s;
+        }
         void *ptr = nullptr;
         return locate(id, agent, &ptr, bytes, err);
     }
 
     rtcc_status get_tensor(int id, int agent, void *dst, size_t bytes, std::string &err) override {
+        if (id == RTCC_T_PILLAR_MEMBERS) {
+            std::vector<int32_t> m;
+            rtcc_status s = used_members(agent, m, err);
+            if (s != RTCC_OK) return s;
+            if (bytes != m.size() * 4) {
+                err = "destination size " + std::to_string(bytes) + " != tensor size " + std::to_string(m.size() * 4);
+                return RTCC_E_ARG;
+            }
+            if (!m.empty()) std::memcpy(dst, m.data(), bytes);
+            return RTCC_OK;
+        }
         void *ptr = nullptr;
         size_t need = 0;
         rtcc_status s = locate(id, agent, &ptr, &need, err);
@@ -382,6 +407,13 @@ class HipExecutor : public Executor {
         }
         *n = q;
         return RTCC_OK;
+    }
+
+    bool conv_plan(int layer, int32_t out[2]) const override {
+        if (layer < 0 || layer >= int(plans_.size())) return false;
+        out[0] = plans_[layer].variant;
+        out[1] = plans_[layer].splits;
+        return true;
     }
 
     void graph_stats(int64_t out[3]) const override {
@@ -488,7 +520,15 @@ class HipExecutor : public Executor {
     }
 
     hipError_t alloc(void **p, size_t bytes) {
-        hipError_t e = hipMalloc(p, align256(bytes ? bytes : 1));
+        const size_t b = align256(bytes ? bytes : 1);
+        if (o_.dev_alloc) {
+            // the caller's allocator (e.g. PyTorch's caching allocator)
+            *p = o_.dev_alloc(b, o_.alloc_user);
+            if (!*p) return hipErrorOutOfMemory;
+            dev_allocs_.push_back(*p);
+            return hipSuccess;
+        }
+        hipError_t e = hipMalloc(p, b);
         if (e == hipSuccess) dev_allocs_.push_back(*p);
         return e;
     }
@@ -745,11 +785,64 @@ class HipExecutor : public Executor {
         return RTCC_OK;
     }
 
+    // The points each pillar of the agent's last frame fed to the PFN: the
+    // first min(count, cap) entries of its member segment (the overfull
+    // selection moved the lowest indices there), sorted per pillar, pillars
+    // in ascending cell order.
+    rtcc_status used_members(int agent, std::vector<int32_t> &out, std::string &err) {
+        if (agent < 0 || agent >= p_.K) {
+            err = "agent out of range";
+            return RTCC_E_ARG;
+        }
+        HIP_TRY(hipSetDevice(dev_));
+        const Branch &b = br_[agent];
+        int32_t meta[3] = {0, 0, 0};
+        HIP_TRY(hipMemcpyAsync(meta, b.d_meta, 12, hipMemcpyDeviceToHost, aux_stream_));
+        HIP_TRY(hipStreamSynchronize(aux_stream_));
+        const int32_t valid = meta[0], P = meta[1];
+        if (valid < 0 || valid > b.n || P < 0 || P > valid) {
+            err = "pillar metadata out of range";
+            return RTCC_E_INTERNAL;
+        }
+        std::vector<int32_t> cnt(P), off(P), mem(valid);
+        if (P > 0) {
+            HIP_TRY(hipMemcpyAsync(cnt.data(), b.d_pcounts, size_t(P) * 4, hipMemcpyDeviceToHost, aux_stream_));
+            HIP_TRY(hipMemcpyAsync(off.data(), b.d_poffs, size_t(P) * 4, hipMemcpyDeviceToHost, aux_stream_));
+            HIP_TRY(hipMemcpyAsync(mem.data(), b.d_member, size_t(valid) * 4, hipMemcpyDeviceToHost, aux_stream_));
+            HIP_TRY(hipStreamSynchronize(aux_stream_));
+        }
+        const int cap = p_.d.max_points_per_pillar;
+        out.clear();
+        for (int32_t q = 0; q < P; ++q) {
+            const int32_t m = std::min(cnt[q], cap);
+            if (m < 1 || off[q] < 0 || int64_t(off[q]) + cnt[q] > valid) {
+                err = "pillar segment out of range";
+                return RTCC_E_INTERNAL;
+            }
+            const size_t at = out.size();
+            out.insert(out.end(), mem.begin() + off[q], mem.begin() + off[q] + m);
+            std::sort(out.begin() + at, out.end());
+        }
+        return RTCC_OK;
+    }
+
     rtcc_status locate(int id, int agent, void **ptr, size_t *bytes, std::string &err) {
         const Plan &p = p_;
         const bool per_agent = id == RTCC_T_PILLAR_CELLS || id == RTCC_T_PILLAR_COUNTS ||
                                id == RTCC_T_CANVAS || id == RTCC_T_SLOT || id == RTCC_T_WARPED;
         int stage = 0;
+        if (id == RTCC_T_CONV_OUT) {
+            const int layer = agent >> 8;
+            agent &= 255;
+            if (layer < 0 || layer >= int(p.convs.size()) || agent < 0 || agent >= p.K) {
+                err = "conv layer or agent out of range";
+                return RTCC_E_ARG;
+            }
+            const ConvLayer &c = p.convs[layer];
+            *ptr = br_[agent].d_act[layer];
+            *bytes = size_t(c.Ho) * c.Wo * c.Co * p.elt;
+            return RTCC_OK;
+        }
         if (id == RTCC_T_STAGE_OUT) {
             stage = agent >> 8;
             agent &= 255;
@@ -854,10 +947,13 @@ class HipExecutor : public Executor {
                 if (e) (void)hipEventDestroy(e);
             drop(b.graph);
         }
-        for (void *ptr : dev_allocs_) (void)hipFree(ptr);
+        for (void *ptr : dev_allocs_) {
+            if (o_.dev_alloc) o_.dev_free(ptr, o_.alloc_user);
+            else (void)hipFree(ptr);
+        }
         if (h_rec) (void)hipHostFree(h_rec);
         if (h_small) (void)hipHostFree(h_small);
-        if (join_stream_) (void)hipStreamDestroy(join_stream_);
+        if (join_stream_ && own_join_stream_) (void)hipStreamDestroy(join_stream_);
         if (copy_stream_) (void)hipStreamDestroy(copy_stream_);
         if (aux_stream_) (void)hipStreamDestroy(aux_stream_);
         for (Graph &g : post_graph_) drop(g);
@@ -886,6 +982,7 @@ class HipExecutor : public Executor {
     std::vector<float> boxes_, scores_;
     std::vector<int32_t> aidx_;
     hipStream_t join_stream_ = nullptr, copy_stream_ = nullptr, aux_stream_ = nullptr;
+    bool own_join_stream_ = true;  // false: the caller's stream (opts.join_stream)
     hipEvent_t ev_frame0_ = nullptr, ev_head_ = nullptr;
     hipEvent_t post_ev_[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
     std::vector<std::array<float, 6>> last_affine_;

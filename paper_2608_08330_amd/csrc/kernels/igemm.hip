@@ -840,6 +840,54 @@ ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, in
     return p;
 }
 
+ConvPlan conv_plan_forced(bool bf16, const ConvPlan &planned, int variant, int splits, int Ci, int Ho, int Wo,
+                          int Co, int stride) {
+    (void)Ho;
+    (void)Wo;
+    const int elt = bf16 ? 2 : 4;
+    const int row_bytes = Ci * elt;
+    const bool rb128 = row_bytes % 128 == 0 && row_bytes >= 512;
+    // K steps of the kernel the forced tiling launches: input-channel chunks
+    // (halo tilings, split further over the wave groups) or 64-byte K steps
+    int steps = 0, groups = 1;
+    bool fits = false;
+    switch (variant) {
+        case 7:  // the implicit GEMM everywhere
+            variant = kConvImplicit;
+            steps = 9 * Ci / (bf16 ? 32 : 16);
+            fits = true;
+            break;
+        case kConvHalo8:
+        case kConvHalo4:
+            fits = stride == 1 && Co % 128 == 0;
+            steps = row_bytes / (rb128 ? 128 : 64);
+            break;
+        case kConvHalo8S2:
+        case kConvHalo4S2:
+            fits = stride == 2 && Co % 128 == 0 && row_bytes % 64 == 0;
+            steps = row_bytes / 64;
+            break;
+        case kConvHalo4N64K2:
+            fits = stride == 1 && Co % 64 == 0;
+            steps = row_bytes / (rb128 ? 128 : 64);
+            groups = 2;
+            break;
+        case kConvHalo4S2N64K2:
+            fits = stride == 2 && Co % 64 == 0 && row_bytes % 64 == 0;
+            steps = row_bytes / 64;
+            groups = 2;
+            break;
+        default: break;
+    }
+    if (!fits || steps % groups != 0 || steps / groups < 1) return planned;
+    ConvPlan p{variant, 1, 0};
+    // a split-K slice holds whole chunks of one wave group's share; the
+    // two-group tilings run unsplit
+    if (splits > 1 && groups == 1 && steps % splits == 0) p.splits = splits;
+    if (p.splits > 1) p.ws_bytes = size_t(p.splits) * Ho * Wo * Co * 4;
+    return p;
+}
+
 int gemm_tiles(int M, int N) { return ((M + 127) / 128) * (N % 128 == 0 ? N / 128 : (N + 63) / 64); }
 
 }  // namespace kern

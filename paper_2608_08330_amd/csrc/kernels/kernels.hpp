@@ -105,6 +105,11 @@ struct ConvPlan {
 };
 // Kernel variant and K split of one 3x3 conv layer on a GPU with n_cu CUs.
 ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, int stride, int n_cu);
+// The plan with tiling `variant` (1..6, or 7 = the implicit GEMM) and K split
+// `splits` forced where the layer's stride and channels allow it; `planned`
+// elsewhere.
+ConvPlan conv_plan_forced(bool bf16, const ConvPlan &planned, int variant, int splits, int Ci, int Ho, int Wo,
+                          int Co, int stride);
 // With start / stop events, the first kernel of the convolution records
 // `start` when it begins executing and the last one `stop` when it ends
 // (kernel execution time, without the dispatch gap before it).

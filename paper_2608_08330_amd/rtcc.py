@@ -20,7 +20,7 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_DIR = os.path.join(HERE, "lib")
 
-RTCC_ABI_VERSION = 5
+RTCC_ABI_VERSION = 6
 RTCC_MAX_AGENTS = 16
 RTCC_MAX_STAGES = 4
 
@@ -37,7 +37,8 @@ RTCC_MODE_RELEASE, RTCC_MODE_BARRIER = 0, 1
 RTCC_EXEC_PER_BRANCH_STREAMS, RTCC_EXEC_SERIAL = 0, 1
 RTCC_WAITING, RTCC_RELEASED, RTCC_RUNNING, RTCC_FINISHED = 0, 1, 2, 3
 (RTCC_T_PILLAR_CELLS, RTCC_T_PILLAR_COUNTS, RTCC_T_CANVAS, RTCC_T_SLOT, RTCC_T_FUSED,
- RTCC_T_HEAD, RTCC_T_STAGE_OUT, RTCC_T_DECODED, RTCC_T_WARPED, RTCC_T_FUSED_STAGE) = range(10)
+ RTCC_T_HEAD, RTCC_T_STAGE_OUT, RTCC_T_DECODED, RTCC_T_WARPED, RTCC_T_FUSED_STAGE,
+ RTCC_T_PILLAR_MEMBERS, RTCC_T_CONV_OUT) = range(12)
 (RTCC_SCHED_MAXRATE, RTCC_SCHED_MAXWEIGHT, RTCC_SCHED_EARLIEST_RELEASE, RTCC_SCHED_WEIGHTED_RATE,
  RTCC_SCHED_ROUND_ROBIN, RTCC_SCHED_PROPORTIONAL_FAIR) = range(6)
 
@@ -74,6 +75,10 @@ class rtcc_model_desc(ctypes.Structure):
     ]
 
 
+DEV_ALLOC_FN = ctypes.CFUNCTYPE(ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p)
+DEV_FREE_FN = ctypes.CFUNCTYPE(None, ctypes.c_void_p, ctypes.c_void_p)
+
+
 class rtcc_runtime_opts(ctypes.Structure):
     _fields_ = [
         ("exec", ctypes.c_int32),
@@ -81,7 +86,37 @@ class rtcc_runtime_opts(ctypes.Structure):
         ("node_timing", ctypes.c_int32),
         ("device", ctypes.c_int32),
         ("premature_tol_s", ctypes.c_double),
+        ("conv_variant", ctypes.c_int32),
+        ("conv_splits", ctypes.c_int32),
+        ("dev_alloc", DEV_ALLOC_FN),
+        ("dev_free", DEV_FREE_FN),
+        ("alloc_user", ctypes.c_void_p),
+        ("join_stream", ctypes.c_void_p),
     ]
+
+
+def use_torch_memory(opts, device=0, stream=None):
+    """Route the context's device buffers through PyTorch's caching
+    allocator (and, with ``stream``, run the post-join subgraph on that
+    torch stream).  The callbacks are kept on ``opts``, which rtcc_create
+    keeps alive with the context."""
+    import torch
+
+    def _alloc(nbytes, _user):
+        try:
+            return torch.cuda.caching_allocator_alloc(int(nbytes), device)
+        except RuntimeError:
+            return None
+
+    def _free(ptr, _user):
+        torch.cuda.caching_allocator_delete(ptr)
+
+    opts._callbacks = (DEV_ALLOC_FN(_alloc), DEV_FREE_FN(_free))
+    opts.dev_alloc, opts.dev_free = opts._callbacks
+    if stream is not None:
+        opts.join_stream = stream.cuda_stream
+        opts._stream = stream
+    return opts
 
 
 class rtcc_uplink_desc(ctypes.Structure):
@@ -116,7 +151,7 @@ EXPORTS = (
     "rtcc_create", "rtcc_destroy", "rtcc_set_mode", "rtcc_staging_buffer", "rtcc_begin_frame",
     "rtcc_release_branch", "rtcc_release_branch_device", "rtcc_join_and_detect",
     "rtcc_get_branch_state", "rtcc_tensor_bytes", "rtcc_get_tensor", "rtcc_profile_nodes",
-    "rtcc_node_times", "rtcc_node_count", "rtcc_graph_stats", "rtcc_rotated_nms", "rtcc_uplink_emulate", "rtcc_schedule_model",
+    "rtcc_node_times", "rtcc_node_count", "rtcc_graph_stats", "rtcc_conv_plan", "rtcc_rotated_nms", "rtcc_uplink_emulate", "rtcc_schedule_model",
     "rtcc_upward_rank", "rtcc_status_str", "rtcc_last_error",
 )
 
@@ -151,6 +186,7 @@ def _declare(lib):
         "rtcc_node_times": (S, [_P, _F, ctypes.POINTER(ctypes.c_int32)]),
         "rtcc_node_count": (S, [_P, ctypes.POINTER(ctypes.c_int32)]),
         "rtcc_graph_stats": (S, [_P, ctypes.POINTER(ctypes.c_int64)]),
+        "rtcc_conv_plan": (S, [_P, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32)]),
         "rtcc_rotated_nms": (S, [_P, ctypes.c_int64, ctypes.c_int32, ctypes.c_float, _P,
                                  ctypes.POINTER(ctypes.c_int64)]),
         "rtcc_uplink_emulate": (S, [ctypes.POINTER(rtcc_uplink_desc), _P, _P, _P, _P, _P]),
@@ -297,7 +333,9 @@ def rtcc_create(desc, blob, opts=None, kind="gpu"):
     if st != RTCC_OK:
         msg = lib.rtcc_last_error(None)
         raise RtccError(st, msg.decode() if msg else "")
-    return Context(lib, h)
+    ctx = Context(lib, h)
+    ctx._opts = opts  # keeps allocator callbacks alive with the context
+    return ctx
 
 
 def rtcc_destroy(ctx):
@@ -473,6 +511,13 @@ def rtcc_node_count(ctx):
     n = ctypes.c_int32()
     ctx.check(ctx.lib.rtcc_node_count(ctx.handle, ctypes.byref(n)))
     return n.value
+
+
+def rtcc_conv_plan(ctx, layer):
+    """(tiling, K slices) of 3x3 conv layer ``layer``."""
+    out = (ctypes.c_int32 * 2)()
+    ctx.check(ctx.lib.rtcc_conv_plan(ctx.handle, int(layer), out))
+    return int(out[0]), int(out[1])
 
 
 def rtcc_graph_stats(ctx):

@@ -234,6 +234,29 @@ _CONFIGS = {
         reps=2,
         seed_index=6,
     ),
+    # Conv-tiling instance: c5's channels (128 / 256 / 256) on an 88 x 120
+    # grid, so every halo tiling and the implicit GEMM run on several tiles
+    # with ragged edges (stage grids 44 x 60, 22 x 30, 11 x 15).
+    "t_var": dict(
+        K=2,
+        n_points=12000,
+        dist="mixture",
+        x_range=(-17.6, 17.6),
+        y_range=(-24.0, 24.0),
+        z_range=(-3.0, 1.0),
+        pillar=0.4,
+        max_pts=32,
+        c_pfn=64,
+        precision="bf16",
+        stages=((2, 128, 2), (2, 256, 2), (2, 256, 2)),
+        up_channels=128,
+        fusion="attn",
+        logit_threshold=1.5,
+        arrivals=dict(kind="lognormal", median_ms=3.0, sigma=0.8),
+        traces=4,
+        reps=2,
+        seed_index=8,
+    ),
 }
 
 # Six-agent measured-DAG instance: the config-3 network (bf16, attention
@@ -251,7 +274,7 @@ _CONFIGS["s6"] = dict(
     seed_index=7,
 )
 
-CONFIG_NAMES = ("c1", "c2", "c3", "c4", "c5", "t_max", "t_attn", "s6")
+CONFIG_NAMES = ("c1", "c2", "c3", "c4", "c5", "t_max", "t_attn", "t_var", "s6")
 
 ROOT_SEED = 20260830
 

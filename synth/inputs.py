@@ -1,7 +1,7 @@
 """Seeded random draws: point clouds, agent poses, network weights, arrival
 vectors and per-slot fading gains.
 
-Seeding: ``SeedSequence(ROOT_SEED).spawn(8)[cfg['seed_index']]`` is the
+Seeding: ``SeedSequence(ROOT_SEED).spawn(9)[cfg['seed_index']]`` is the
 config's sequence; it spawns four children, in this order, for points,
 poses, weights and arrival traces.  A config whose data comes from another
 config (the load sweep reuses the config-3 network and frames) takes the
@@ -15,7 +15,7 @@ import numpy as np
 
 from .configs import ROOT_SEED, config, network_layers
 
-_N_CONFIG_SEEDS = 8
+_N_CONFIG_SEEDS = 9
 _CHILD = {"points": 0, "poses": 1, "weights": 2, "traces": 3}
 
 # Standard deviation of the bias vectors.  The weight matrices are He-normal

@@ -36,6 +36,10 @@ def make_ctx(cfg, frame, max_points=None, **opt):
     o.node_timing = opt.get("node_timing", 0)
     o.device = 0
     o.premature_tol_s = opt.get("tol", 1e-6)
+    o.conv_variant = opt.get("conv_variant", 0)
+    o.conv_splits = opt.get("conv_splits", 0)
+    if opt.get("torch_memory"):
+        R.use_torch_memory(o, 0, opt.get("join_stream"))
     n_max = max_points if max_points is not None else max(len(p) for p in frame["points"])
     return R.rtcc_create(R.model_desc(cfg, max(n_max, 1)), R.weights_blob(cfg, frame["weights"]), o,
                          kind=opt.get("kind", "gpu"))
@@ -164,3 +168,133 @@ def check_frame_nms(ctx, det, cfg):
     assert np.array_equal(det["boxes"].view(np.uint32), dec["boxes"][kept].view(np.uint32))
     assert np.array_equal(det["scores"].view(np.uint32), dec["scores"][kept].view(np.uint32))
     return dec
+
+
+# --------------------------------------------------------------- tight checks
+# Checks of one kernel at a time: the oracle op applied to the GPU's own
+# input of that op, so the only differences left are the summation order of
+# float32 accumulation against float64 and, at a bf16 storage point, the
+# rounding those differences can flip (one bf16 step, 2^-7 relative).  A
+# tile-edge, halo or indexing error is far outside these bounds.
+
+BF16_STEP = 2.0 ** -7
+
+
+def tight(cfg):
+    """(relative, floor) bounds of the one-kernel checks: one bf16 step at a
+    bf16 storage point; float32 accumulation against float64 otherwise."""
+    return (BF16_STEP, 1e-4) if cfg["precision"] == "bf16" else (1e-5, 1e-5)
+
+
+def assert_close_elementwise(got, ref, rel, floor, what):
+    """|got - ref| <= rel * |ref| + floor * max|ref| for every element."""
+    g = np.asarray(got, dtype=np.float64).ravel()
+    r = np.asarray(ref, dtype=np.float64).ravel()
+    assert g.shape == r.shape, (what, g.shape, r.shape)
+    scale = float(np.max(np.abs(r))) if r.size else 0.0
+    bound = rel * np.abs(r) + floor * scale
+    bad = np.nonzero(np.abs(g - r) > bound)[0]
+    assert bad.size == 0, (what, "elements outside the bound", int(bad.size), "of", int(r.size), "first",
+                           int(bad[0]), float(g[bad[0]]), float(r[bad[0]]))
+    return float(np.max(np.abs(g - r)) / scale) if scale else 0.0
+
+
+def check_decode_exact(ctx, cfg):
+    """The GPU's decoded records against the oracle's decode of the GPU's
+    own head output: the same anchors (the logit > threshold decision on the
+    same float32 value and the float32 threshold), boxes to float32
+    rounding of the residual decode, scores likewise.  A row / column mix-up
+    or a half-cell shift of the anchor centres moves a box by a cell."""
+    from oracle import network as ON
+    H2, W2 = ON.feature_grid(cfg)
+    head = R.rtcc_get_tensor(ctx, R.RTCC_T_HEAD, 0, np.float32).reshape(H2, W2, 16).astype(np.float64)
+    thr = float(np.float32(cfg["logit_threshold"]))
+    ref = ON.decode(head, cfg, threshold=thr)
+    dec = R.decoded_records(ctx)
+    assert np.array_equal(dec["anchor_idx"].astype(np.int64), ref["anchor_idx"]), "decoded anchor set"
+    n = len(ref["anchor_idx"])
+    if n:
+        for col in range(7):
+            scale = max(1.0, float(np.max(np.abs(ref["boxes"][:, col]))))
+            err = np.max(np.abs(dec["boxes"][:, col].astype(np.float64) - ref["boxes"][:, col]))
+            assert err <= 1e-6 * scale, ("box column", col, err, scale)
+        assert np.max(np.abs(dec["scores"].astype(np.float64) - ref["scores"])) <= 1e-6
+    return n
+
+
+def check_members(ctx, cfg, points, agent):
+    """The points each pillar fed to the point-feature net, bit-exact: the
+    lowest max_pts original indices of every pillar, pillars in cell order."""
+    from oracle import network as ON
+    pil = ON.pillars(ON.cell_ids(points, cfg), cfg["max_pts"])
+    want = np.concatenate(pil["used"]).astype(np.int32) if pil["used"] else np.zeros(0, np.int32)
+    got = R.rtcc_get_tensor(ctx, R.RTCC_T_PILLAR_MEMBERS, agent, np.int32)
+    assert np.array_equal(got, want), ("pillar members, agent", agent, got.size, want.size)
+    return got.size
+
+
+def conv_layer_shapes(cfg):
+    """(stage, layer in stage, stride, C_in, C_out) of every 3x3 conv."""
+    out = []
+    c_in = cfg["c_pfn"]
+    for s, (stride, c_out, n) in enumerate(cfg["stages"]):
+        for l in range(n):
+            out.append((s, l, stride if l == 0 else 1, c_in if l == 0 else c_out, c_out))
+        c_in = c_out
+    return out
+
+
+def check_conv_layers(ctx, cfg, pw, agent, rel=None, floor=None):
+    """Every 3x3 conv layer of one agent against the oracle conv of the
+    GPU's own input to it (the canvas, then the previous layer's output),
+    elementwise; then every upsampling into the slot from the GPU's stage
+    outputs.  Returns the largest relative deviation per layer."""
+    from oracle import network as ON
+    if rel is None:
+        rel, floor = tight(cfg)
+    H, W = ON.grid(cfg)
+    x = as_f32(R.rtcc_get_tensor(ctx, R.RTCC_T_CANVAS, agent), cfg).reshape(H, W, -1)
+    errs = []
+    stage_out = []
+    shapes = conv_layer_shapes(cfg)
+    for li, (s, l, stride, _ci, co) in enumerate(shapes):
+        ref = ON._store(cfg, ON.conv3x3(x.astype(np.float64), pw["s%dc%d_w" % (s, l)], pw["s%dc%d_b" % (s, l)],
+                                        stride))
+        got = as_f32(R.rtcc_get_tensor(ctx, R.RTCC_T_CONV_OUT, (li << 8) | agent), cfg).reshape(ref.shape)
+        errs.append(assert_close_elementwise(got, ref, rel, floor, ("conv layer", li, "agent", agent)))
+        x = got
+        if li + 1 == len(shapes) or shapes[li + 1][0] != s:
+            stage_out.append(got)
+    if cfg["up_channels"] and not cfg.get("multiscale"):
+        H2, W2 = ON.feature_grid(cfg)
+        slot = as_f32(R.rtcc_get_tensor(ctx, R.RTCC_T_SLOT, agent), cfg).reshape(H2, W2, -1)
+        up = cfg["up_channels"]
+        rel_u = 1
+        for s, (stride, _c, _n) in enumerate(cfg["stages"]):
+            if s > 0:
+                rel_u *= stride
+            ref = ON._store(cfg, ON.deconv(stage_out[s].astype(np.float64), pw["up%d_w" % s], pw["up%d_b" % s],
+                                           rel_u, H2, W2))
+            errs.append(assert_close_elementwise(slot[:, :, s * up:(s + 1) * up], ref, rel, floor,
+                                                 ("upsample", s, "agent", agent)))
+    return errs
+
+
+def check_fusion_and_head(ctx, cfg, poses, pw, rel=None, floor=None):
+    """The fused map against the oracle warp + fusion of the GPU's own slots,
+    and the head against the oracle head of the GPU's own fused map, both
+    elementwise."""
+    from oracle import network as ON
+    if rel is None:
+        rel, floor = (BF16_STEP, 1e-3) if cfg["precision"] == "bf16" else (1e-5, 1e-5)
+    H2, W2 = ON.feature_grid(cfg)
+    slots = [as_f32(R.rtcc_get_tensor(ctx, R.RTCC_T_SLOT, k), cfg).reshape(H2, W2, -1).astype(np.float64)
+             for k in range(cfg["K"])]
+    warped = [ON.warp(slots[k], poses[k], cfg) for k in range(cfg["K"])]
+    fused_ref = ON._store(cfg, ON.fuse_attn(warped) if cfg["fusion"] == "attn" else ON.fuse_max(warped))
+    fused = as_f32(R.rtcc_get_tensor(ctx, R.RTCC_T_FUSED), cfg).reshape(H2, W2, -1)
+    e_f = assert_close_elementwise(fused, fused_ref, rel, floor, "fusion")
+    head_ref = ON.head(fused.astype(np.float64), pw["head_w"], pw["head_b"])
+    head = R.rtcc_get_tensor(ctx, R.RTCC_T_HEAD, 0, np.float32).reshape(H2, W2, 16)
+    e_h = assert_close_elementwise(head, head_ref, 1e-5, 1e-5, "head")
+    return e_f, e_h

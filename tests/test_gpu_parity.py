@@ -14,7 +14,8 @@ import pytest
 import synth
 from oracle import network as N
 from paper_2608_08330_amd import rtcc as R
-from tests.helpers import TOL, check_frame_nms, compare_detections, make_ctx, rel_err, run_frame, tensors
+from tests.helpers import (TOL, check_conv_layers, check_decode_exact, check_frame_nms, check_fusion_and_head,
+                           check_members, compare_detections, make_ctx, rel_err, run_frame, tensors)
 
 pytestmark = pytest.mark.gpu
 
@@ -67,6 +68,13 @@ def test_frame_parity_and_mode_identity(name):
         dec_r = check_frame_nms(ctx, det_r, cfg)
         compare_detections(dec_r, ref["det"], cfg, ref["head"])
         _say("  %s: %d decoded, %d after NMS" % (name, det_r["count_decoded"], det_r["count"]))
+        # one kernel at a time, on the GPU's own inputs
+        for k in range(cfg["K"]):
+            check_members(ctx, cfg, fr["points"][k], k)
+        pw = N.prepared_weights(cfg, fr["weights"])
+        check_conv_layers(ctx, cfg, pw, 0)
+        check_fusion_and_head(ctx, cfg, fr["poses"], pw)
+        assert check_decode_exact(ctx, cfg) == det_r["count_decoded"]
         det_b = run_frame(ctx, fr, R.RTCC_MODE_BARRIER, a)
         got_b = tensors(ctx, cfg)
         dec_b = R.decoded_records(ctx)
@@ -134,6 +142,10 @@ def test_edge_cases_empty_agent_overfull_cell_and_invalid_points():
     with make_ctx(cfg, fr, max_points=cfg["n_points"]) as ctx:
         run_frame(ctx, fr)
         got = tensors(ctx, cfg)
+        # which 32 of the 500 points fed the PFN, bit-exact
+        assert check_members(ctx, cfg, fr["points"][0], 0) == 0
+        check_members(ctx, cfg, fr["points"][1], 1)
+        check_members(ctx, cfg, fr["points"][2], 2)
     assert got["cells"][0].size == 0 and got["counts"][0].size == 0
     _check_frame(cfg, fr, ref, got)
 
@@ -162,3 +174,74 @@ def test_consecutive_frames_with_different_points_match_oracle():
             _say("  frame %d" % i)
             run_frame(ctx, fr)
             _check_frame(cfg, fr, ref, tensors(ctx, cfg), with_stages=False)
+            for k in range(cfg["K"]):
+                check_members(ctx, cfg, fr["points"][k], k)
+
+
+def test_branch_states_follow_the_device():
+    """RELEASED at release, FINISHED once the device has run the encoder, read
+    without a join (eq. branch_state)."""
+    import time
+    import torch
+    cfg = synth.config("t_attn")
+    fr, _ref = _oracle("t_attn")
+    with make_ctx(cfg, fr) as ctx:
+        R.rtcc_set_mode(ctx, R.RTCC_MODE_BARRIER)
+        R.rtcc_begin_frame(ctx, time.monotonic() - 1.0)
+        for k in range(cfg["K"] - 1):
+            R.rtcc_release_branch(ctx, k, fr["points"][k], fr["poses"][k], 0.0)
+            assert R.rtcc_get_branch_state(ctx, k) == R.RTCC_WAITING
+        k = cfg["K"] - 1
+        R.rtcc_release_branch(ctx, k, fr["points"][k], fr["poses"][k], 0.0)
+        assert all(R.rtcc_get_branch_state(ctx, j) >= R.RTCC_RELEASED for j in range(cfg["K"]))
+        torch.cuda.synchronize()
+        assert all(R.rtcc_get_branch_state(ctx, j) == R.RTCC_FINISHED for j in range(cfg["K"]))
+        R.rtcc_join_and_detect(ctx)
+        assert all(R.rtcc_get_branch_state(ctx, j) == R.RTCC_FINISHED for j in range(cfg["K"]))
+
+
+@pytest.mark.parametrize("variant", [1, 2, 3, 4, 5, 6, 7])
+@pytest.mark.parametrize("splits", [0, 2])
+def test_forced_conv_tilings(variant, splits):
+    """Each 3x3-conv tiling (and split-K) forced on every layer it supports,
+    on a grid with several ragged tiles per layer at c5's channel counts:
+    every layer elementwise against the oracle conv of its GPU input, and
+    the head against the oracle end to end."""
+    _say("forced conv tiling %d splits %d" % (variant, splits))
+    cfg = synth.config("t_var")
+    fr, ref = _oracle("t_var")
+    with make_ctx(cfg, fr, conv_variant=variant, conv_splits=splits) as ctx:
+        run_frame(ctx, fr)
+        plans = [R.rtcc_conv_plan(ctx, l) for l in range(sum(n for _s, _c, n in cfg["stages"]))]
+        _say("  plans %s" % plans)
+        want = 0 if variant == 7 else variant
+        assert sum(v == want for v, _sp in plans) >= 1
+        if splits:
+            assert any(sp == splits for _v, sp in plans) or variant in (5, 6)
+        pw = N.prepared_weights(cfg, fr["weights"])
+        for k in range(cfg["K"]):
+            check_conv_layers(ctx, cfg, pw, k)
+        got = tensors(ctx, cfg)
+    _check_frame(cfg, fr, ref, got)
+
+
+def test_torch_allocator_and_stream_hook():
+    """Device buffers from PyTorch's caching allocator and the post-join
+    subgraph on a torch stream give the same frame, bit for bit."""
+    import torch
+    cfg = synth.config("t_attn")
+    fr, _ref = _oracle("t_attn")
+    with make_ctx(cfg, fr) as ctx:
+        run_frame(ctx, fr)
+        want = tensors(ctx, cfg, with_stages=False)
+    before = torch.cuda.memory_allocated()
+    st = torch.cuda.Stream()
+    with make_ctx(cfg, fr, torch_memory=True, join_stream=st) as ctx:
+        assert torch.cuda.memory_allocated() > before
+        for _ in range(2):
+            run_frame(ctx, fr)
+            got = tensors(ctx, cfg, with_stages=False)
+            assert np.array_equal(got["head"].view(np.uint32), want["head"].view(np.uint32))
+            assert np.array_equal(got["fused"].view(np.uint32), want["fused"].view(np.uint32))
+    torch.cuda.synchronize()
+    assert torch.cuda.memory_allocated() == before
