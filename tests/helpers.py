@@ -14,8 +14,9 @@ TOL = {"fp32": 1e-4, "bf16": 2e-2}
 
 
 def rel_err(x, r):
-    x = np.asarray(x, dtype=np.float64)
-    r = np.asarray(r, dtype=np.float64)
+    x = np.asarray(x, dtype=np.float64).ravel()
+    r = np.asarray(r, dtype=np.float64).ravel()
+    assert x.shape == r.shape, (x.shape, r.shape)
     den = np.max(np.abs(r)) if r.size else 0.0
     if den == 0.0:
         return float(np.max(np.abs(x))) if x.size else 0.0
