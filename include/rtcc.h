@@ -385,6 +385,26 @@ RTCC_API rtcc_status rtcc_graph_stats(rtcc_ctx *ctx, int64_t *counts);
 RTCC_API rtcc_status rtcc_rotated_nms(const float *device_records, int64_t n, int32_t max_candidates,
                                       float iou_threshold, float *device_out, int64_t *kept);
 
+/* rtcc_rotated_nms for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same kernels and results, with the scratch in one
+ * library-owned device array of fixed size (11.9 MB per GPU, held from the
+ * first call on that GPU until the process ends).  Allocates nothing and
+ * creates no stream.
+ *   device_records, n, max_candidates, iou_threshold, device_out, kept: as
+ *     for rtcc_rotated_nms, with n <= 131072 and max_candidates <= 4096
+ *     (E_ARG beyond these limits);
+ *   hip_stream: a hipStream_t of the current device (NULL = the null
+ *     stream); the kernels run on it, after the work already queued there,
+ *     and the call returns once it has finished them.
+ * Calls on one GPU share its scratch array: the library serialises them (a
+ * per-device lock held until the stream is done), so a call waits for any
+ * other in the process on that GPU.  The array keeps the last call's
+ * contents; every part a call reads is written by that call first. */
+RTCC_API rtcc_status rtcc_rotated_nms_noalloc(const float *device_records, int64_t n, int32_t max_candidates,
+                                              float iou_threshold, float *device_out, int64_t *kept,
+                                              void *hip_stream);
+
 /* ------------------------------------------------------------------------
  * Host-side models of the communication and of the profiled DAG.  They run
  * on the host only (no GPU work, no context), are deterministic, and report

@@ -33,6 +33,7 @@ HIP_SOURCES = [
     "kernels/post.hip",
     "kernels/nms.hip",
     "nms_api.hip",
+    "nms_noalloc.hip",
 ]
 
 # Packed fp32 instructions are disabled for every device compile.

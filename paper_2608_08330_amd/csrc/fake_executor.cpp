@@ -140,3 +140,11 @@ extern "C" __attribute__((visibility("default"))) rtcc_status rtcc_rotated_nms(c
     rtcc::set_thread_error("rtcc_rotated_nms needs the GPU library");
     return RTCC_E_STATE;
 }
+
+extern "C" __attribute__((visibility("default"))) rtcc_status rtcc_rotated_nms_noalloc(const float *, int64_t, int32_t,
+                                                                                      float, float *, int64_t *kept,
+                                                                                      void *) {
+    if (kept) *kept = 0;
+    rtcc::set_thread_error("rtcc_rotated_nms_noalloc needs the GPU library");
+    return RTCC_E_STATE;
+}

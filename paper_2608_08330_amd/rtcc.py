@@ -151,7 +151,7 @@ EXPORTS = (
     "rtcc_create", "rtcc_destroy", "rtcc_set_mode", "rtcc_staging_buffer", "rtcc_begin_frame",
     "rtcc_release_branch", "rtcc_release_branch_device", "rtcc_join_and_detect",
     "rtcc_get_branch_state", "rtcc_tensor_bytes", "rtcc_get_tensor", "rtcc_profile_nodes",
-    "rtcc_node_times", "rtcc_node_count", "rtcc_graph_stats", "rtcc_conv_plan", "rtcc_rotated_nms", "rtcc_uplink_emulate", "rtcc_schedule_model",
+    "rtcc_node_times", "rtcc_node_count", "rtcc_graph_stats", "rtcc_conv_plan", "rtcc_rotated_nms", "rtcc_rotated_nms_noalloc", "rtcc_uplink_emulate", "rtcc_schedule_model",
     "rtcc_upward_rank", "rtcc_status_str", "rtcc_last_error",
 )
 
@@ -189,6 +189,8 @@ def _declare(lib):
         "rtcc_conv_plan": (S, [_P, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32)]),
         "rtcc_rotated_nms": (S, [_P, ctypes.c_int64, ctypes.c_int32, ctypes.c_float, _P,
                                  ctypes.POINTER(ctypes.c_int64)]),
+        "rtcc_rotated_nms_noalloc": (S, [_P, ctypes.c_int64, ctypes.c_int32, ctypes.c_float, _P,
+                                         ctypes.POINTER(ctypes.c_int64), _P]),
         "rtcc_uplink_emulate": (S, [ctypes.POINTER(rtcc_uplink_desc), _P, _P, _P, _P, _P]),
         "rtcc_schedule_model": (S, [ctypes.c_int32, _P, _P, ctypes.c_int64, ctypes.c_int32, _I64P, _I64P, _P]),
         "rtcc_upward_rank": (S, [ctypes.c_int32, _P, ctypes.c_int32, _P, _P]),
@@ -412,6 +414,19 @@ def rtcc_rotated_nms(device_records, n, max_candidates, iou_threshold, device_ou
     kept = ctypes.c_int64()
     st = lib.rtcc_rotated_nms(_P(device_records), n, max_candidates, iou_threshold, _P(device_out),
                               ctypes.byref(kept))
+    if st != 0:
+        raise RtccError(st, (lib.rtcc_last_error(None) or b"").decode())
+    return kept.value
+
+
+def rtcc_rotated_nms_noalloc(device_records, n, max_candidates, iou_threshold, device_out, stream=0,
+                             kind="gpu"):
+    """rtcc_rotated_nms without device allocation, on a HIP stream handle
+    (integer, 0 = the null stream); returns the number kept."""
+    lib = load(kind)
+    kept = ctypes.c_int64()
+    st = lib.rtcc_rotated_nms_noalloc(_P(device_records), n, max_candidates, iou_threshold, _P(device_out),
+                                      ctypes.byref(kept), _P(stream))
     if st != 0:
         raise RtccError(st, (lib.rtcc_last_error(None) or b"").decode())
     return kept.value
