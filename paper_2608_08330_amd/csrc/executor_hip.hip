@@ -177,7 +177,14 @@ class HipExecutor : public Executor {
         HIP_TRY(hipStreamSynchronize(copy_stream_));
         HIP_TRY(hipStreamSynchronize(join_stream_));
         HIP_TRY(hipEventRecord(ev_frame0_, compute_stream_for_join()));
-        for (Branch &b : br_) b.dispatched = false;
+        // The last frame's canvas pillars (readable until now) go back to
+        // zero at the start of the frame, ahead of the branch's next encoder
+        // on its stream (or the one compute stream), normally long before its
+        // completion event.
+        for (Branch &b : br_) {
+            b.dispatched = false;
+            if (b.canvas_dirty) HIP_TRY(clear_canvas(b, o_.exec == RTCC_EXEC_SERIAL ? join_stream_ : b.stream));
+        }
         return RTCC_OK;
     }
 
@@ -207,6 +214,7 @@ class HipExecutor : public Executor {
         b.src = src;
         b.n = int32_t(n);
         b.host_input = !device_src;
+        HIP_TRY(prepare_branch(b, cs));
         // reached once the input copy and everything queued before the
         // encoder on its stream have completed: the encoder is running
         HIP_TRY(hipEventRecord(b.started, cs));
@@ -221,6 +229,7 @@ class HipExecutor : public Executor {
             s = enqueue_encoder(b, cs, timing, 1, err);
         }
         if (s != RTCC_OK) return s;
+        b.canvas_dirty = true;  // the encoder writes this frame's pillars
         HIP_TRY(hipEventRecord(b.done, cs));
         b.dispatched = true;
         return RTCC_OK;
@@ -347,11 +356,16 @@ class HipExecutor : public Executor {
         std::vector<std::vector<float>> t(p_.K + 1);
         for (int r = 0; r < warmup + reps; ++r) {
             for (int k = 0; k <= p_.K; ++k) {
+                if (k < p_.K) HIP_TRY(prepare_branch(br_[k], s));
                 HIP_TRY(hipEventRecord(e0, s));
                 rtcc_status st = k < p_.K ? enqueue_encoder(br_[k], s, false, 0, err)
                                           : enqueue_post(last_affine_, last_poses_, s, false, err);
                 if (st != RTCC_OK) return st;
                 HIP_TRY(hipEventRecord(e1, s));
+                if (k < p_.K) {
+                    br_[k].canvas_dirty = true;
+                    HIP_TRY(clear_canvas(br_[k], s));  // untimed, as after a frame
+                }
                 HIP_TRY(hipEventSynchronize(e1));
                 float ms = 0.f;
                 HIP_TRY(hipEventElapsedTime(&ms, e0, e1));
@@ -495,6 +509,7 @@ class HipExecutor : public Executor {
         float affine[6] = {1, 0, 0, 0, 1, 0};
         bool warp_ran = false;           // the last frame ran a branch warp kernel
         bool pillars_clean = true;       // every enqueued K1 was followed by the PFN kernel
+        bool canvas_dirty = false;       // the canvas holds pillars not yet cleared (canvas_clear)
         hipEvent_t wev[2] = {nullptr, nullptr};  // bracket the branch warp kernel
         Graph graph;                     // the encoder as a HIP graph (use_graphs)
         std::vector<void *> d_act;
@@ -552,32 +567,23 @@ class HipExecutor : public Executor {
         ++ev;
         kern::PillarGeom g{p.d.x_min, p.d.x_max, p.d.y_min, p.d.y_max, p.d.z_min, p.d.z_max,
                            p.d.pillar_size, p.H, p.W};
-        // Between frames the cell counts are zero and the canvas is zero
-        // outside the last frame's pillars (K1 clears those, the PFN kernel
-        // writes the new ones and zeroes their counts), unless an earlier
-        // enqueue stopped between the two: then both are reset here.
-        if (!b.pillars_clean) {
-            HIP_TRY(kern::fill_i32(counts, n_cells, 0, s));
-            HIP_TRY(kern::fill_i32(static_cast<int32_t *>(b.d_canvas), int64_t(n_cells) * p.c_pfn * p.elt / 4, 0, s));
-        }
+        // Between frames the cell counts are zero (the PFN kernel returns
+        // them to zero) and the canvas is zero outside the last frame's
+        // pillars (prepare_branch).
         b.pillars_clean = false;
-        const kern::CanvasClear cc{b.d_canvas, static_cast<const int32_t *>(b.d_pcells), meta, p.c_pfn};
         HIP_TRY(kern::cell_ids(b.src, n, g, static_cast<int32_t *>(b.d_cell), static_cast<int32_t *>(b.d_slot),
-                               counts, p.bf16, cc, int32_t(std::min<int64_t>(p.n_max, n_cells)), s));
+                               counts, s));
         HIP_TRY(kern::scan_reduce(counts, n_cells, tiles, meta, s));
         HIP_TRY(kern::scan_down(counts, n_cells, tiles, p.d.max_points_per_pillar, offsets,
                                 static_cast<int32_t *>(b.d_pcells), static_cast<int32_t *>(b.d_pcounts),
                                 static_cast<int32_t *>(b.d_poffs), static_cast<int32_t *>(b.d_overfull), meta, s));
         HIP_TRY(kern::scatter(static_cast<int32_t *>(b.d_cell), static_cast<int32_t *>(b.d_slot), offsets, n,
                               b.src, static_cast<int32_t *>(b.d_member), static_cast<float *>(b.d_sorted), s));
-        HIP_TRY(kern::overfull_select(static_cast<int32_t *>(b.d_overfull), meta, counts, offsets, b.src,
-                                      static_cast<int32_t *>(b.d_member), static_cast<float *>(b.d_sorted),
-                                      p.d.max_points_per_pillar, n, s));
         if (timing) HIP_TRY(hipEventRecord(b.ev[ev], s));
         ++ev;
 
         kern::PfnArgs pa{};
-        pa.sorted = static_cast<const float4 *>(b.d_sorted);
+        pa.sorted = static_cast<float4 *>(b.d_sorted);
         pa.counts = counts;
         pa.pcells = static_cast<const int32_t *>(b.d_pcells);
         pa.pcounts = static_cast<const int32_t *>(b.d_pcounts);
@@ -592,6 +598,11 @@ class HipExecutor : public Executor {
         pa.inv_hy = float(2.0 / (double(p.d.y_max) - double(p.d.y_min)));
         pa.z0 = p.d.z_min;
         pa.inv_dz = float(1.0 / (double(p.d.z_max) - double(p.d.z_min)));
+        pa.overfull = static_cast<const int32_t *>(b.d_overfull);
+        pa.offsets = offsets;
+        pa.member = static_cast<int32_t *>(b.d_member);
+        pa.pts = reinterpret_cast<const float4 *>(b.src);
+        pa.n = n;
         HIP_TRY(kern::pfn_canvas(p.bf16, pa, n < n_cells ? n : n_cells, s));
         b.pillars_clean = true;
         if (timing) HIP_TRY(hipEventRecord(b.ev[ev], s));
@@ -653,6 +664,37 @@ class HipExecutor : public Executor {
             ++ev;
         }
         return RTCC_OK;
+    }
+
+    // Before an encoder: the canvas must be zero outside the pillars the
+    // encoder writes.  begin_frame clears the last frame's (clear_canvas);
+    // should they still be there, they are cleared here.  If an earlier
+    // enqueue stopped between K1 and the PFN kernel, counts and the whole
+    // canvas are reset.  Runs outside any graph: what it enqueues depends on
+    // the branch's state, not on the frame's arguments.
+    hipError_t prepare_branch(Branch &b, hipStream_t s) {
+        const int n_cells = p_.H * p_.W;
+        hipError_t e = hipSuccess;
+        if (!b.pillars_clean) {
+            e = kern::fill_i32(static_cast<int32_t *>(b.d_counts), n_cells, 0, s);
+            if (e == hipSuccess)
+                e = kern::fill_i32(static_cast<int32_t *>(b.d_canvas), int64_t(n_cells) * p_.c_pfn * p_.elt / 4, 0, s);
+            if (e != hipSuccess) return e;
+            b.pillars_clean = true;
+            b.canvas_dirty = false;
+        }
+        return b.canvas_dirty ? clear_canvas(b, s) : hipSuccess;
+    }
+
+    // Zero the canvas cells of the agent's last pillars (their list is the
+    // scan's output of the last enqueued encoder) on stream s.
+    hipError_t clear_canvas(Branch &b, hipStream_t s) {
+        const int n_cells = p_.H * p_.W;
+        const int max_p = int(std::min<int64_t>(p_.n_max, n_cells));
+        hipError_t e = kern::canvas_clear(p_.bf16, b.d_canvas, static_cast<const int32_t *>(b.d_pcells),
+                                          static_cast<const int32_t *>(b.d_meta), p_.c_pfn, max_p, s);
+        if (e == hipSuccess) b.canvas_dirty = false;
+        return e;
     }
 
     // Upsampling u of the map `in` into channels [c_off, c_off + Co) of `out`

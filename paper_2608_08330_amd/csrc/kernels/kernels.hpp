@@ -20,19 +20,11 @@ constexpr int kScanTile = 2048;  // cells per block of the cell scans
 
 hipError_t fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s);
 
-// The previous frame's pillars, cleared in the canvas by K1.
-struct CanvasClear {
-    void *canvas;           // [H*W][C] in the activation dtype
-    const int32_t *pcells;  // pillar cells of the previous frame
-    const int32_t *meta;    // meta[1] = their number (0 before the first frame)
-    int32_t C;
-};
 // K1: cell id per point (-1 if dropped); counts[cell] += 1 (counts start at
 // zero) and the point's rank of arrival in its cell (an arbitrary order) goes
-// to slot[i].  The same launch zeroes the canvas cells of the previous
-// frame's pillars; max_prev_pillars bounds their number.
+// to slot[i].
 hipError_t cell_ids(const float *pts, int32_t n, const PillarGeom &g, int32_t *cell, int32_t *slot,
-                    int32_t *counts, bool bf16, const CanvasClear &cc, int32_t max_prev_pillars, hipStream_t s);
+                    int32_t *counts, hipStream_t s);
 
 // K2a: per tile of kScanTile cells: (points, non-empty cells); zeroes
 // meta[2] (the overfull count of K2c).
@@ -46,18 +38,14 @@ hipError_t scan_down(const int32_t *counts, int32_t n_cells, const int32_t *tile
 // K2d: member[offsets[cell] + slot] = point index.
 hipError_t scatter(const int32_t *cell, const int32_t *slot, const int32_t *offsets, int32_t n,
                    const float *pts, int32_t *member, float *sorted, hipStream_t s);
-// K2e: for every overfull cell, move its max_pts lowest point indices to
-// the front of its member segment.
-hipError_t overfull_select(const int32_t *overfull, const int32_t *meta, const int32_t *counts,
-                           const int32_t *offsets, const float *pts, int32_t *member, float *sorted,
-                           int32_t max_pts, int32_t n, hipStream_t s);
-
 // K3: dense canvas [H*W][C]: per pillar cell, channel max over the first
-// min(count, max_pts) members of ReLU(W^T f + b).  Writes the pillar cells
-// only: every other cell must already be zero (K1 clears the previous
-// frame's pillars).  Leaves counts[] all zero, the state K1 expects next.
+// min(count, max_pts) members of ReLU(W^T f + b) (for cells over the cap,
+// after moving the max_pts lowest point indices to the front of the
+// segment).  Writes the pillar cells only: every other cell must already be
+// zero (canvas_clear zeroes the previous frame's pillars).  Leaves counts[]
+// all zero, the state K1 expects next.
 struct PfnArgs {
-    const float4 *sorted;  // points in segment order; each segment's first min(count, max_pts) are used
+    float4 *sorted;        // points in segment order; each segment's first min(count, max_pts) are used
     int32_t *counts;       // per cell; the pillars' counts are zeroed for the next frame
     const int32_t *pcells, *pcounts, *poffs;  // per pillar: cell, count, segment offset
     const int32_t *meta;   // meta[1] = number of pillars
@@ -67,9 +55,21 @@ struct PfnArgs {
     int32_t C;
     int32_t max_pts;
     float inv_hx, inv_hy, z0, inv_dz;
+    // cells over the cap: their list and number (meta[2]), segment offsets,
+    // member indices, the input points and their count
+    const int32_t *overfull;
+    const int32_t *offsets;
+    int32_t *member;
+    const float4 *pts;
+    int32_t n;
+    int32_t pillar_blocks;  // set by pfn_canvas
 };
 // max_pillars bounds meta[1] (at most min(cells, points)).
-hipError_t pfn_canvas(bool bf16, const PfnArgs &a, int32_t max_pillars, hipStream_t s);
+hipError_t pfn_canvas(bool bf16, PfnArgs a, int32_t max_pillars, hipStream_t s);
+// The canvas cells of the pillars listed in pcells (meta[1] of them) back to
+// zero; max_pillars bounds meta[1].
+hipError_t canvas_clear(bool bf16, void *canvas, const int32_t *pcells, const int32_t *meta, int32_t C,
+                        int32_t max_pillars, hipStream_t s);
 
 // ------------------------------------------------------------ implicit GEMM
 // conv:   out[m][c_off + n] for m = output pixel, 3x3 taps, pad 1, stride.

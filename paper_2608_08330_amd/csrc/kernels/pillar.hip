@@ -1,26 +1,25 @@
 // Pillarization and point-feature canvas for gfx950.
 //
 // Deterministic counting sort by cell (no float atomics, no order-dependent
-// result):
+// result), five dependent launches:
 //   cell_ids        one thread per point: float32 cell index, atomic count
 //                   per cell (the counts start at zero); the returned old
-//                   count is the point's rank of arrival in its cell.  Extra
-//                   blocks clear the previous frame's pillars in the canvas
-//                   (the only cells of it that are not zero)
+//                   count is the point's rank of arrival in its cell
 //   scan_reduce /   exclusive prefix over all H*W cells -> segment offsets,
 //   scan_down       ascending list of non-empty cells (pillars) and their
 //                   counts, list of cells over the per-pillar point cap (each
 //                   block of the second pass adds up the tile sums before it)
 //   scatter         member[offset[cell] + rank] = point index
-//   overfull_select for the few cells above the cap, one wavefront moves the
-//                   cap lowest point indices (found by bisection on the index
-//                   value) to the front of the segment
 //   pfn_canvas      one lane per (pillar, 8 channels): linear 4 -> C, ReLU,
-//                   max over the first min(count, cap) members into the
-//                   pillar's cell; the pillar's count is returned to zero for
-//                   the next frame.  Empty cells keep the zeros they hold
-//                   (zeroed once at allocation, and their previous pillars
-//                   cleared by cell_ids)
+//                   max over the pillar's points into its cell; the pillar's
+//                   count is returned to zero for the next frame.  Extra
+//                   blocks take the few cells over the cap: one wavefront
+//                   moves the cap lowest point indices (found by bisection on
+//                   the index value) to the front of the segment and writes
+//                   that pillar's features
+// The canvas is zero outside the pillars: canvas_clear zeroes the last
+// frame's pillar cells again (off the encoder's path: the executor runs it
+// when the next frame begins, before any branch input has arrived).
 // The only order-dependent intermediate is the order of members inside a
 // segment, and every consumer of it is order-independent (max, set
 // selection), so every output is bitwise reproducible.
@@ -80,28 +79,9 @@ __device__ inline void nt_store16(void *p, uint4 v) {
     __builtin_nontemporal_store(u32x4{v.x, v.y, v.z, v.w}, static_cast<u32x4 *>(p));
 }
 
-template <bool BF16>
-__global__ __launch_bounds__(256) void k_cell_ids(const float4 *__restrict__ pts, int32_t n,
-                                                  PillarGeom g, int32_t *__restrict__ cell,
-                                                  int32_t *__restrict__ slot,
-                                                  int32_t *__restrict__ counts, CanvasClear cc,
-                                                  int32_t point_blocks) {
-    if (int(blockIdx.x) >= point_blocks) {
-        // the previous frame's pillars back to zero, one lane per (pillar, 8
-        // channels); no other canvas cell holds anything but zeros
-        const int lanes = cc.C >> 3;
-        const int gid = (int(blockIdx.x) - point_blocks) * 256 + int(threadIdx.x);
-        const int p = gid / lanes;
-        if (p >= cc.meta[1]) return;
-        const size_t off = size_t(cc.pcells[p]) * cc.C + (gid - p * lanes) * 8;
-        if (BF16) {
-            nt_store16(static_cast<uint16_t *>(cc.canvas) + off, make_uint4(0u, 0u, 0u, 0u));
-        } else {
-            nt_store16(static_cast<float *>(cc.canvas) + off, make_uint4(0u, 0u, 0u, 0u));
-            nt_store16(static_cast<float *>(cc.canvas) + off + 4, make_uint4(0u, 0u, 0u, 0u));
-        }
-        return;
-    }
+__global__ __launch_bounds__(256) void k_cell_ids(const float4 *__restrict__ pts, int32_t n, PillarGeom g,
+                                                  int32_t *__restrict__ cell, int32_t *__restrict__ slot,
+                                                  int32_t *__restrict__ counts) {
     const int i = blockIdx.x * 256 + threadIdx.x;
     if (i >= n) return;
     const float4 p = pts[i];
@@ -204,56 +184,6 @@ __global__ __launch_bounds__(256) void k_scatter(const int32_t *__restrict__ cel
     }
 }
 
-__global__ __launch_bounds__(256) void k_overfull_select(const int32_t *__restrict__ overfull,
-                                                         const int32_t *__restrict__ meta,
-                                                         const int32_t *__restrict__ counts,
-                                                         const int32_t *__restrict__ offsets,
-                                                         const float4 *__restrict__ pts,
-                                                         int32_t *__restrict__ member,
-                                                         float4 *__restrict__ sorted,
-                                                         int32_t max_pts, int32_t n) {
-    const int lane = threadIdx.x & 63;
-    const int wave = (blockIdx.x * 256 + threadIdx.x) >> 6;
-    const int n_waves = (gridDim.x * 256) >> 6;
-    const int n_over = meta[2];
-    for (int w = wave; w < n_over; w += n_waves) {
-        const int c = overfull[w];
-        const int cnt = counts[c];
-        int32_t *seg = member + offsets[c];
-        float4 *sseg = sorted + offsets[c];
-        // Smallest T with #{members < T} >= max_pts.  Members are distinct
-        // point indices in [0, n), so exactly max_pts members lie below T.
-        int lo = 1, hi = n;
-        while (lo < hi) {
-            const int mid = lo + (hi - lo) / 2;
-            int below = 0;
-            for (int j = lane; j < cnt; j += 64) below += seg[j] < mid;
-#pragma unroll
-            for (int d = 32; d >= 1; d >>= 1) below += __shfl_xor(below, d, 64);
-            if (below >= max_pts) hi = mid;
-            else lo = mid + 1;
-        }
-        const int T = lo;
-        // Stable in-place compaction of the selected members to the front:
-        // a chunk is read completely before any of it is overwritten, and
-        // writes never pass the chunk being read.
-        int pos = 0;
-        for (int base = 0; base < cnt && pos < max_pts; base += 64) {
-            const int j = base + lane;
-            const int e = j < cnt ? seg[j] : INT_MAX;
-            const bool sel = j < cnt && e < T;
-            const unsigned long long m = __ballot(sel);
-            const int my = pos + __popcll(m & ((1ull << lane) - 1ull));
-            if (sel) {
-                seg[my] = e;
-                sseg[my] = pts[e];
-            }
-            pos += __popcll(m);
-        }
-    }
-}
-
-
 __device__ inline uint32_t pack_bf16x2(float a, float b) {
     uint32_t ua = __float_as_uint(a), ub = __float_as_uint(b);
     ua += 0x7fffu + ((ua >> 16) & 1u);
@@ -261,58 +191,25 @@ __device__ inline uint32_t pack_bf16x2(float a, float b) {
     return (ua >> 16) | (ub & 0xffff0000u);
 }
 
-// A lane per (pillar, 8 channels) over the ascending pillar list from the
-// scan: ReLU(W^T f + b) maxed over the pillar's first min(count, max_pts)
-// points, read in segment order from `sorted`, into the pillar's cell.  The
-// lanes read the cell, count and segment offset together; the other cells
-// of the canvas already hold zeros.
-template <bool BF16>
-__global__ __launch_bounds__(256) void k_pfn_canvas(PfnArgs a) {
-    const int lanes_per_cell = a.C >> 3;
-    // PFN weights and bias, read once per block into LDS (C <= 512)
-    __shared__ float sw[5 * 512];
-    for (int q = threadIdx.x; q < 5 * a.C; q += 256) sw[q] = q < 4 * a.C ? a.w[q] : a.b[q - 4 * a.C];
-    __syncthreads();
-    const int gid = int(blockIdx.x) * 256 + int(threadIdx.x);
-    const int p = gid / lanes_per_cell;
-    const int ch = (gid - p * lanes_per_cell) * 8;
-    if (p >= a.meta[1]) return;
-    const int cell = a.pcells[p];
-    const int cnt = a.pcounts[p];
-    const int off = a.poffs[p];
-    // the cell's count back to zero, the state the next frame's K1 starts from
-    if (ch == 0) a.counts[cell] = 0;
-    const int m = cnt < a.max_pts ? cnt : a.max_pts;
-    float w0[8], w1[8], w2[8], w3[8], bb[8], mx[8];
+// One point's contribution to 8 channels of its pillar: ReLU(b + W^T f),
+// f = (x / hx, y / hy, (z - z0) / dz, r), maxed into mx.  The same code for
+// pillars under and over the cap.
+__device__ inline void pfn_point(const PfnArgs &a, const float4 pt, const float (&w0)[8], const float (&w1)[8],
+                                 const float (&w2)[8], const float (&w3)[8], const float (&bb)[8], float (&mx)[8]) {
+    const float f0 = pt.x * a.inv_hx;
+    const float f1 = pt.y * a.inv_hy;
+    const float f2 = (pt.z - a.z0) * a.inv_dz;
+    const float f3 = pt.w;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-        w0[i] = sw[0 * a.C + ch + i];
-        w1[i] = sw[1 * a.C + ch + i];
-        w2[i] = sw[2 * a.C + ch + i];
-        w3[i] = sw[3 * a.C + ch + i];
-        bb[i] = sw[4 * a.C + ch + i];
-        mx[i] = 0.f;
+        float h = bb[i] + w0[i] * f0 + w1[i] * f1 + w2[i] * f2 + w3[i] * f3;
+        h = h > 0.f ? h : 0.f;  // +0 for every non-positive value
+        mx[i] = fmaxf(mx[i], h);
     }
-    auto add = [&](const float4 pt) {
-        const float f0 = pt.x * a.inv_hx;
-        const float f1 = pt.y * a.inv_hy;
-        const float f2 = (pt.z - a.z0) * a.inv_dz;
-        const float f3 = pt.w;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            float h = bb[i] + w0[i] * f0 + w1[i] * f1 + w2[i] * f2 + w3[i] * f3;
-            h = h > 0.f ? h : 0.f;  // +0 for every non-positive value
-            mx[i] = fmaxf(mx[i], h);
-        }
-    };
-    // two points per step, both loads in flight (max is order-free)
-    for (int t = 0; t < m; t += 2) {
-        const float4 p0 = a.sorted[off + t];
-        const bool two = t + 1 < m;
-        const float4 p1 = a.sorted[off + (two ? t + 1 : t)];
-        add(p0);
-        if (two) add(p1);
-    }
+}
+
+template <bool BF16>
+__device__ inline void store_canvas8(const PfnArgs &a, int cell, int ch, const float (&mx)[8]) {
     if (BF16) {
         uint4 o;
         o.x = pack_bf16x2(mx[0], mx[1]);
@@ -329,6 +226,134 @@ __global__ __launch_bounds__(256) void k_pfn_canvas(PfnArgs a) {
     }
 }
 
+// Blocks [0, a.pillar_blocks): a lane per (pillar, 8 channels) over the
+// ascending pillar list from the scan: ReLU(W^T f + b) maxed over the
+// pillar's points, read in segment order from `sorted`, into the pillar's
+// cell; pillars over the cap are left to the other blocks.  Blocks from
+// a.pillar_blocks on: one wavefront per cell over the cap moves the cap
+// lowest point indices to the front of its segment (member indices and
+// points) and writes the features of those points.  The lanes read the
+// cell, count and segment offset together; the other cells of the canvas
+// already hold zeros.  Counts go back to zero for the next frame.
+template <bool BF16>
+__global__ __launch_bounds__(256) void k_pfn_canvas(PfnArgs a) {
+    // PFN weights and bias, read once per block into LDS (C <= 512)
+    __shared__ float sw[5 * 512];
+    for (int q = threadIdx.x; q < 5 * a.C; q += 256) sw[q] = q < 4 * a.C ? a.w[q] : a.b[q - 4 * a.C];
+    __syncthreads();
+    if (int(blockIdx.x) >= a.pillar_blocks) {
+        // cells over the cap, one wavefront each
+        const int lane = threadIdx.x & 63;
+        const int wave = ((int(blockIdx.x) - a.pillar_blocks) * 256 + int(threadIdx.x)) >> 6;
+        const int n_waves = ((int(gridDim.x) - a.pillar_blocks) * 256) >> 6;
+        const int n_over = a.meta[2];
+        for (int w = wave; w < n_over; w += n_waves) {
+            const int c = a.overfull[w];
+            const int cnt = a.counts[c];
+            int32_t *seg = a.member + a.offsets[c];
+            float4 *sseg = a.sorted + a.offsets[c];
+            // Smallest T with #{members < T} >= max_pts.  Members are
+            // distinct point indices in [0, n), so exactly max_pts members
+            // lie below T.
+            int lo = 1, hi = a.n;
+            while (lo < hi) {
+                const int mid = lo + (hi - lo) / 2;
+                int below = 0;
+                for (int j = lane; j < cnt; j += 64) below += seg[j] < mid;
+#pragma unroll
+                for (int d = 32; d >= 1; d >>= 1) below += __shfl_xor(below, d, 64);
+                if (below >= a.max_pts) hi = mid;
+                else lo = mid + 1;
+            }
+            const int T = lo;
+            // Stable in-place compaction of the selected members to the
+            // front: a chunk is read completely before any of it is
+            // overwritten, and writes never pass the chunk being read.
+            int pos = 0;
+            for (int base = 0; base < cnt && pos < a.max_pts; base += 64) {
+                const int j = base + lane;
+                const int e = j < cnt ? seg[j] : INT_MAX;
+                const bool sel = j < cnt && e < T;
+                const unsigned long long m = __ballot(sel);
+                const int my = pos + __popcll(m & ((1ull << lane) - 1ull));
+                if (sel) {
+                    seg[my] = e;
+                    sseg[my] = a.pts[e];
+                }
+                pos += __popcll(m);
+            }
+            // the wave's own writes above are read back by other lanes
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            for (int ch = lane * 8; ch < a.C; ch += 64 * 8) {
+                float w0[8], w1[8], w2[8], w3[8], bb[8], mx[8];
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    w0[i] = sw[0 * a.C + ch + i];
+                    w1[i] = sw[1 * a.C + ch + i];
+                    w2[i] = sw[2 * a.C + ch + i];
+                    w3[i] = sw[3 * a.C + ch + i];
+                    bb[i] = sw[4 * a.C + ch + i];
+                    mx[i] = 0.f;
+                }
+                for (int t = 0; t < a.max_pts; ++t) pfn_point(a, sseg[t], w0, w1, w2, w3, bb, mx);
+                store_canvas8<BF16>(a, c, ch, mx);
+            }
+            if (lane == 0) a.counts[c] = 0;
+        }
+        return;
+    }
+    const int lanes_per_cell = a.C >> 3;
+    const int gid = int(blockIdx.x) * 256 + int(threadIdx.x);
+    const int p = gid / lanes_per_cell;
+    const int ch = (gid - p * lanes_per_cell) * 8;
+    if (p >= a.meta[1]) return;
+    const int cell = a.pcells[p];
+    const int cnt = a.pcounts[p];
+    const int off = a.poffs[p];
+    if (cnt > a.max_pts) return;  // over the cap: the blocks above
+    // the cell's count back to zero, the state the next frame's K1 starts from
+    if (ch == 0) a.counts[cell] = 0;
+    float w0[8], w1[8], w2[8], w3[8], bb[8], mx[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        w0[i] = sw[0 * a.C + ch + i];
+        w1[i] = sw[1 * a.C + ch + i];
+        w2[i] = sw[2 * a.C + ch + i];
+        w3[i] = sw[3 * a.C + ch + i];
+        bb[i] = sw[4 * a.C + ch + i];
+        mx[i] = 0.f;
+    }
+    // two points per step, both loads in flight (max is order-free)
+    for (int t = 0; t < cnt; t += 2) {
+        const float4 p0 = a.sorted[off + t];
+        const bool two = t + 1 < cnt;
+        const float4 p1 = a.sorted[off + (two ? t + 1 : t)];
+        pfn_point(a, p0, w0, w1, w2, w3, bb, mx);
+        if (two) pfn_point(a, p1, w0, w1, w2, w3, bb, mx);
+    }
+    store_canvas8<BF16>(a, cell, ch, mx);
+}
+
+// The canvas cells of the last frame's pillars back to zero, one lane per
+// (pillar, 8 channels); the rest of the canvas holds zeros already.
+template <bool BF16>
+__global__ __launch_bounds__(256) void k_canvas_clear(void *canvas, const int32_t *__restrict__ pcells,
+                                                      const int32_t *__restrict__ meta, int32_t C) {
+    const int lanes = C >> 3;
+    const int gid = int(blockIdx.x) * 256 + int(threadIdx.x);
+    const int p = gid / lanes;
+    if (p >= meta[1]) return;
+    const size_t off = size_t(pcells[p]) * C + (gid - p * lanes) * 8;
+    if (BF16) {
+        nt_store16(static_cast<uint16_t *>(canvas) + off, make_uint4(0u, 0u, 0u, 0u));
+    } else {
+        nt_store16(static_cast<float *>(canvas) + off, make_uint4(0u, 0u, 0u, 0u));
+        nt_store16(static_cast<float *>(canvas) + off + 4, make_uint4(0u, 0u, 0u, 0u));
+    }
+}
+
 inline unsigned blocks_for(int64_t n, int per) { return unsigned((n + per - 1) / per); }
 
 }  // namespace
@@ -342,16 +367,9 @@ hipError_t fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s) {
 }
 
 hipError_t cell_ids(const float *pts, int32_t n, const PillarGeom &g, int32_t *cell, int32_t *slot,
-                    int32_t *counts, bool bf16, const CanvasClear &cc, int32_t max_prev_pillars, hipStream_t s) {
-    const unsigned point_blocks = n > 0 ? blocks_for(n, 256) : 0u;
-    const unsigned blocks = point_blocks + blocks_for(int64_t(max_prev_pillars) * (cc.C >> 3), 256);
-    if (blocks == 0) return hipSuccess;
-    if (bf16)
-        k_cell_ids<true><<<blocks, 256, 0, s>>>(reinterpret_cast<const float4 *>(pts), n, g, cell, slot, counts, cc,
-                                                int32_t(point_blocks));
-    else
-        k_cell_ids<false><<<blocks, 256, 0, s>>>(reinterpret_cast<const float4 *>(pts), n, g, cell, slot, counts, cc,
-                                                 int32_t(point_blocks));
+                    int32_t *counts, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    k_cell_ids<<<blocks_for(n, 256), 256, 0, s>>>(reinterpret_cast<const float4 *>(pts), n, g, cell, slot, counts);
     return hipGetLastError();
 }
 
@@ -376,20 +394,23 @@ hipError_t scatter(const int32_t *cell, const int32_t *slot, const int32_t *offs
     return hipGetLastError();
 }
 
-hipError_t overfull_select(const int32_t *overfull, const int32_t *meta, const int32_t *counts,
-                           const int32_t *offsets, const float *pts, int32_t *member, float *sorted,
-                           int32_t max_pts, int32_t n, hipStream_t s) {
-    if (n <= max_pts) return hipSuccess;  // no cell can exceed the cap
-    k_overfull_select<<<64, 256, 0, s>>>(overfull, meta, counts, offsets, reinterpret_cast<const float4 *>(pts),
-                                         member, reinterpret_cast<float4 *>(sorted), max_pts, n);
-    return hipGetLastError();
-}
-
-hipError_t pfn_canvas(bool bf16, const PfnArgs &a, int32_t max_pillars, hipStream_t s) {
-    const unsigned blocks = blocks_for(int64_t(max_pillars) * (a.C / 8), 256);
+hipError_t pfn_canvas(bool bf16, PfnArgs a, int32_t max_pillars, hipStream_t s) {
+    // pillar blocks, then 64 blocks for the cells over the cap when any
+    // cell can exceed it
+    a.pillar_blocks = int32_t(blocks_for(int64_t(max_pillars) * (a.C / 8), 256));
+    const unsigned blocks = unsigned(a.pillar_blocks) + (a.n > a.max_pts ? 64u : 0u);
     if (blocks == 0) return hipSuccess;
     if (bf16) k_pfn_canvas<true><<<blocks, 256, 0, s>>>(a);
     else k_pfn_canvas<false><<<blocks, 256, 0, s>>>(a);
+    return hipGetLastError();
+}
+
+hipError_t canvas_clear(bool bf16, void *canvas, const int32_t *pcells, const int32_t *meta, int32_t C,
+                        int32_t max_pillars, hipStream_t s) {
+    const unsigned blocks = blocks_for(int64_t(max_pillars) * (C / 8), 256);
+    if (blocks == 0) return hipSuccess;
+    if (bf16) k_canvas_clear<true><<<blocks, 256, 0, s>>>(canvas, pcells, meta, C);
+    else k_canvas_clear<false><<<blocks, 256, 0, s>>>(canvas, pcells, meta, C);
     return hipGetLastError();
 }
 

@@ -245,3 +245,24 @@ def test_torch_allocator_and_stream_hook():
             assert np.array_equal(got["fused"].view(np.uint32), want["fused"].view(np.uint32))
     torch.cuda.synchronize()
     assert torch.cuda.memory_allocated() == before
+
+
+def test_frame_after_an_infeasible_frame_matches_oracle():
+    """An infeasible frame runs some encoders but no join, so their canvas
+    pillars are not cleared after it: the next encoder of each branch clears
+    them first, and the next frame (other points) matches the oracle."""
+    import time
+    cfg, fr_e = _edge_frame()
+    fr_n, ref_n = _oracle("t_max")
+    with make_ctx(cfg, fr_e, max_points=cfg["n_points"]) as ctx:
+        run_frame(ctx, fr_e)
+        R.rtcc_begin_frame(ctx, time.monotonic() - 1.0)
+        for k in range(cfg["K"] - 1):
+            R.rtcc_release_branch(ctx, k, fr_n["points"][k], fr_n["poses"][k], 0.0)
+        with pytest.raises(R.RtccError) as e:
+            R.rtcc_join_and_detect(ctx)
+        assert e.value.status == R.RTCC_E_INFEASIBLE
+        run_frame(ctx, fr_n)
+        _check_frame(cfg, fr_n, ref_n, tensors(ctx, cfg), with_stages=False)
+        for k in range(cfg["K"]):
+            check_members(ctx, cfg, fr_n["points"][k], k)
