@@ -744,6 +744,7 @@ class HipExecutor : public Executor {
                 }
                 wa.fused = d_fused_stage_[u.stage];
                 wa.K = p.K;
+                wa.ident = kern::identity_mask(wa.affine, p.K);
                 wa.H2 = u.Hi;
                 wa.W2 = u.Wi;
                 wa.C = u.Ci;
@@ -767,6 +768,7 @@ class HipExecutor : public Executor {
             }
             wa.fused = d_fused;
             wa.K = p.K;
+            wa.ident = kern::identity_mask(wa.affine, p.K);
             wa.H2 = p.H2;
             wa.W2 = p.W2;
             wa.C = p.c_slot;

@@ -125,7 +125,17 @@ struct WarpArgs {
     float affine[16][6];    // per agent {M00, M01, t0, M10, M11, t1}
     void *fused;            // [H2*W2][C]
     int32_t K, H2, W2, C;
+    uint32_t ident;         // bit k: agent k's affine is exactly the identity
 };
+// Bit k set iff affine[k] is {1, 0, 0, 0, 1, 0} (by value).
+inline uint32_t identity_mask(const float (*affine)[6], int K) {
+    uint32_t m = 0;
+    for (int k = 0; k < K; ++k)
+        if (affine[k][0] == 1.f && affine[k][1] == 0.f && affine[k][2] == 0.f && affine[k][3] == 0.f &&
+            affine[k][4] == 1.f && affine[k][5] == 0.f)
+            m |= 1u << k;
+    return m;
+}
 // With start / stop events the launch records them around the kernel's own
 // execution (hipExtLaunchKernelGGL).
 hipError_t warp_fuse(bool bf16, bool attn, const WarpArgs &a, hipStream_t s, hipEvent_t start = nullptr,

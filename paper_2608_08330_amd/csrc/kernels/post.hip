@@ -238,10 +238,16 @@ __global__ __launch_bounds__(256) void k_warp_fuse(WarpArgs a) {
     const float fj = float(j), fi = float(i);
     Fold<VEC, ATTN> f(a.C);
     // with branch-free sampling one agent at a time already keeps 8 loads
-    // per lane in flight; that measured fastest at the 8-agent size
+    // per lane in flight; that measured fastest at the 8-agent size.  An
+    // agent whose affine is the identity (the ego) samples every cell at
+    // itself with weight 1: one load of the cell's slice gives the same value
+    // as the four corners.
     for (int k = 0; k < a.K; ++k) {
         float x[VEC];
-        warp_sample<T, VEC, false>(static_cast<const T *>(a.slots[k]), a.affine[k], a.H2, a.W2, a.C, fi, fj, l, x);
+        if ((a.ident >> k) & 1u)
+            load_slice<T, VEC, false>(static_cast<const T *>(a.slots[k]) + size_t(cell) * a.C, l, x);
+        else
+            warp_sample<T, VEC, false>(static_cast<const T *>(a.slots[k]), a.affine[k], a.H2, a.W2, a.C, fi, fj, l, x);
         f.add(k, x);
     }
     f.finish();
