@@ -82,7 +82,8 @@ def layer_work(cfg):
             s = stride if l == 0 else 1
             ho, wo = -(-h // s), -(-w // s)
             convs.append(dict(flops=2.0 * ho * wo * co * 9 * c, M=ho * wo, N=co, K=9 * c,
-                              bytes=(h * w * c + ho * wo * co + 9 * c * co) * elt))
+                              bytes=(h * w * c + ho * wo * co + 9 * c * co) * elt,
+                              Hi=h, Wi=w, Ci=c, stride=s, stage=len(stage), layer=l))
             h, w, c = ho, wo, co
         stage.append((h, w, c))
     H2, W2 = stage[0][0], stage[0][1]
@@ -104,30 +105,52 @@ def encoder_flops(cfg, lw, n_used):
     return pfn + sum(c["flops"] for c in lw["convs"]) + ups
 
 
-def timed_steps(ctx, cfg, frame, dev_pts, steps, warmup, R, torch, record_nodes=True):
+def timed_steps(ctx, cfg, frames, dev_pts, steps, warmup, R, torch, record_nodes=True, release_us=None):
     """Warm-up, then exactly `steps` timed frames bracketed by device syncs.
-    Returns wall seconds and (with record_nodes) the per-node HIP-event times
-    of every step."""
+    Step s runs stream frame s mod len(frames) (its own points and poses), as
+    a live stream does.  Returns wall seconds and (with record_nodes) the
+    per-node HIP-event times of every step; with release_us (a list), the
+    host time of every release call of the timed steps is appended to it."""
     K = cfg["K"]
-    n = [len(p) for p in frame["points"]]
+    F = len(frames)
 
-    def one():
+    def one(f, times=None):
+        fr, dev = frames[f], dev_pts[f]
         R.rtcc_begin_frame(ctx, time.monotonic() - 1.0)
         for k in range(K):
-            R.rtcc_release_branch_device(ctx, k, dev_pts[k].data_ptr(), n[k], frame["poses"][k], 0.0)
+            t0 = time.perf_counter()
+            R.rtcc_release_branch_device(ctx, k, dev[k].data_ptr(), len(fr["points"][k]), fr["poses"][k], 0.0)
+            if times is not None:
+                times.append((time.perf_counter() - t0) * 1e6)
         return R.rtcc_join_and_detect(ctx)
 
-    for _ in range(warmup):
-        one()
+    for w in range(warmup):
+        one(w % F)
     torch.cuda.synchronize()
     node = []
     t = time.perf_counter()
-    for _ in range(steps):
-        one()
+    for i in range(steps):
+        one((warmup + i) % F, release_us)
         if record_nodes:
             node.append(R.rtcc_node_times(ctx))
     torch.cuda.synchronize()
     return time.perf_counter() - t, node
+
+
+def used_points(ctx, cfg, frames, dev_pts, R):
+    """Points fed to the point-feature net per frame of the stream (sum over
+    agents of min(count, cap) of every pillar), from the library's pillar
+    counts after running each frame once."""
+    import numpy as np
+    out = []
+    for f, fr in enumerate(frames):
+        R.rtcc_begin_frame(ctx, time.monotonic() - 1.0)
+        for k in range(cfg["K"]):
+            R.rtcc_release_branch_device(ctx, k, dev_pts[f][k].data_ptr(), len(fr["points"][k]), fr["poses"][k], 0.0)
+        R.rtcc_join_and_detect(ctx)
+        out.append([int(np.minimum(R.rtcc_get_tensor(ctx, R.RTCC_T_PILLAR_COUNTS, k, np.int32), cfg["max_pts"]).sum())
+                    for k in range(cfg["K"])])
+    return out
 
 
 def gemm_reference(layers, torch, iters=50):
@@ -155,31 +178,162 @@ def gemm_reference(layers, torch, iters=50):
     return rows
 
 
-def cpu_baseline(cfg, frame, budget_s):
-    """The fp64 oracle (untuned) on one agent's encoder, repeated while the
-    budget lasts.  Reports encoder GFLOP/s on the host cores."""
-    import numpy as np
-    from oracle import network as N
+def _blas_threads():
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        return max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
-        threads = os.cpu_count() or 1
+        return os.cpu_count() or 1
+
+
+def oracle_stage_times(cfg, frame, agents=(0,), post=True):
+    """Wall seconds of every stage of the fp64 oracle (untuned): O1 cell ids,
+    O2 pillars, O3 point-feature canvas, O4 each conv stage, O5 upsampling,
+    for the listed agents' encoders; then O7 warp and O8 fusion of all K
+    agents, O9 head, O10 decode (the post-join stages reuse the listed
+    agents' slots for the others).  Returns (seconds by stage, FLOPs of the
+    encoders run)."""
+    import numpy as np
+    from oracle import network as N
+    pw = N.prepared_weights(cfg, frame["weights"])
+    lw = layer_work(cfg)
+    st = {}
+
+    def tick(name, t0):
+        st[name] = st.get(name, 0.0) + time.perf_counter() - t0
+
+    flops = 0.0
+    slots = []
+    for k in agents:
+        pts = frame["points"][k]
+        t0 = time.perf_counter(); cell = N.cell_ids(pts, cfg); tick("O1_cell_ids", t0)
+        t0 = time.perf_counter(); pil = N.pillars(cell, cfg["max_pts"]); tick("O2_pillars", t0)
+        t0 = time.perf_counter(); x = N.pfn_canvas(pts, pil, pw["pfn_w"], pw["pfn_b"], cfg); tick("O3_pfn_canvas", t0)
+        x = N._store(cfg, x)
+        stage_out = []
+        for s, (stride, _c, n) in enumerate(cfg["stages"]):
+            t0 = time.perf_counter()
+            for l in range(n):
+                x = N._store(cfg, N.conv3x3(x, pw["s%dc%d_w" % (s, l)], pw["s%dc%d_b" % (s, l)], stride if l == 0 else 1))
+            tick("O4_conv_stage%d" % s, t0)
+            stage_out.append(x)
+        if cfg["up_channels"]:
+            t0 = time.perf_counter()
+            H2, W2 = stage_out[0].shape[:2]
+            parts, rel = [], 1
+            for s, (stride, _c, _n) in enumerate(cfg["stages"]):
+                if s > 0:
+                    rel *= stride
+                parts.append(N._store(cfg, N.deconv(stage_out[s], pw["up%d_w" % s], pw["up%d_b" % s], rel, H2, W2)))
+            slot = np.concatenate(parts, axis=2)
+            tick("O5_upsample", t0)
+        else:
+            slot = stage_out[-1]
+        slots.append(slot)
+        flops += encoder_flops(cfg, lw, int(np.minimum(pil["counts"], cfg["max_pts"]).sum()))
+    if post:
+        full = [slots[k % len(slots)] for k in range(cfg["K"])]
+        t0 = time.perf_counter(); warped = [N.warp(full[k], frame["poses"][k], cfg) for k in range(cfg["K"])]
+        tick("O7_warp", t0)
+        t0 = time.perf_counter()
+        fused = N._store(cfg, N.fuse_attn(warped) if cfg["fusion"] == "attn" else N.fuse_max(warped))
+        tick("O8_fusion", t0)
+        t0 = time.perf_counter(); Z = N.head(fused, pw["head_w"], pw["head_b"]); tick("O9_head", t0)
+        t0 = time.perf_counter(); N.decode(Z, cfg); tick("O10_decode", t0)
+    return st, flops
+
+
+def schedule_decision_us(cfg, reps=2000):
+    """Host cost of one release decision of the schedule oracle (the
+    single-stream RTCC execution of K arrivals: validation-free ordering by
+    (a_k, k) and the start / finish recursion), microseconds per frame."""
+    import numpy as np
+    from oracle import schedule as S
+    rng = np.random.default_rng(0)
+    a = rng.uniform(0.0, 0.1, (reps, cfg["K"]))
+    c = np.full(cfg["K"], 2e-4)
+    t = time.perf_counter()
+    for r in range(reps):
+        S.rtcc(a[r], c, [5e-5])
+    return (time.perf_counter() - t) / reps * 1e6
+
+
+def cpu_baseline(cfg, frame, budget_s):
+    """The fp64 oracle (untuned) on the host cores: agent encoders repeated
+    while the budget lasts with the BLAS library's threads (the value), the
+    same single-threaded on a bounded sample, the stage split of one agent
+    encoder, and the schedule oracle's cost per decision."""
+    import numpy as np
+    from oracle import network as N
+    threads = _blas_threads()
     pw = N.prepared_weights(cfg, frame["weights"])
     lw = layer_work(cfg)
     done, flops = 0, 0.0
     t = time.perf_counter()
+    stages = None
     while True:
         k = done % cfg["K"]
-        enc = N.encoder(frame["points"][k], cfg, pw)
-        used = int(np.minimum(enc["counts"], cfg["max_pts"]).sum())
-        flops += encoder_flops(cfg, lw, used)
+        if done == 0:
+            stages, f = oracle_stage_times(cfg, frame, agents=(k,), post=False)
+            flops += f
+        else:
+            enc = N.encoder(frame["points"][k], cfg, pw)
+            flops += encoder_flops(cfg, lw, int(np.minimum(enc["counts"], cfg["max_pts"]).sum()))
         done += 1
         if time.perf_counter() - t >= budget_s:
             break
     dt = time.perf_counter() - t
-    return dict(value=flops / dt / 1e12, unit="TFLOP/s", cores=int(threads), kind="oracle",
-                sample="%d agent encoder(s) of the %s frame (fp64 numpy oracle), %.1f s" % (done, cfg["name"], dt))
+    out = dict(value=flops / dt / 1e12, unit="TFLOP/s", cores=int(threads), kind="oracle",
+               sample="%d agent encoder(s) of the %s frame (fp64 numpy oracle), %.1f s, %d BLAS threads"
+                      % (done, cfg["name"], dt, threads),
+               stages_ms_one_agent={k: round(v * 1e3, 1) for k, v in stages.items()})
+    # single-threaded: the last conv stage of one agent (the smallest grid),
+    # repeated for a few seconds
+    try:
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1):
+            cl = lw["convs"][-1]
+            x = np.random.default_rng(0).random((cl["Hi"], cl["Wi"], cl["Ci"]))
+            w = pw["s%dc%d_w" % (cl["stage"], cl["layer"])]
+            b = pw["s%dc%d_b" % (cl["stage"], cl["layer"])]
+            n1, t1 = 0, time.perf_counter()
+            while time.perf_counter() - t1 < min(budget_s, 5.0) or n1 == 0:
+                N.conv3x3(x, w, b, cl["stride"])
+                n1 += 1
+            dt1 = time.perf_counter() - t1
+        out["single_thread"] = dict(value=n1 * lw["convs"][-1]["flops"] / dt1 / 1e12, unit="TFLOP/s", cores=1,
+                                    sample="%d x the last 3x3 conv layer (%d x %d x %d -> %d), %.1f s" % (
+                                        n1, x.shape[0], x.shape[1], x.shape[2], w.shape[3], dt1))
+    except Exception as e:  # pragma: no cover
+        out["single_thread"] = dict(error=str(e))
+    out["schedule_decision_us"] = round(schedule_decision_us(cfg), 2)
+    return out
+
+
+def cpu_stage_table(names=("c1", "c2", "c3", "c5")):
+    """Stage-by-stage wall time of the fp64 oracle for one agent encoder and
+    the post-join subgraph of each config, with all BLAS threads and with one
+    (JSON on stdout)."""
+    import synth
+    from threadpoolctl import threadpool_limits
+    rows = []
+    for name in names:
+        cfg = synth.config(name)
+        frame = synth.make_frame(cfg)
+        for threads in (None, 1):
+            with threadpool_limits(limits=threads):
+                n_thr = _blas_threads()
+                t = time.perf_counter()
+                st, flops = oracle_stage_times(cfg, frame, agents=(0,), post=True)
+                total = time.perf_counter() - t
+            enc = sum(v for k, v in st.items() if k[:2] in ("O1", "O2", "O3", "O4", "O5"))
+            rows.append(dict(config=name, threads=n_thr, stages_ms={k: round(v * 1e3, 2) for k, v in st.items()},
+                             encoder_ms=round(enc * 1e3, 2), encoder_gflops=round(flops / enc / 1e9, 2),
+                             total_ms=round(total * 1e3, 2)))
+            print("# %s threads=%d encoder %.1f ms" % (name, n_thr, enc * 1e3), file=sys.stderr, flush=True)
+    print(json.dumps(dict(cpu=os.cpu_count(), rows=rows, schedule_decision_us=round(
+        schedule_decision_us(synth.config("c5")), 2))))
+    return 0
 
 
 def main(argv=None):
@@ -207,10 +361,19 @@ def main(argv=None):
     ap.add_argument("--gemm-reference", action="store_true",
                     help="also time the vendor GEMM (torch.matmul, hipBLASLt) on every conv layer's GEMM shape "
                          "(M x K times K x N, bf16) next to the conv kernel")
+    ap.add_argument("--stream-frames", type=int, default=3,
+                    help="distinct seeded frames (points and poses) the throughput pass cycles through, so that "
+                         "HIP graphs are updated every step as on a live stream")
+    ap.add_argument("--cpu-stages", action="store_true",
+                    help="only time the CPU oracle stage by stage for c1, c2, c3 and c5, with all BLAS threads and "
+                         "single-threaded, and print the table as JSON")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB, 5 times "
                          "(reference for the FETCH_SIZE / WRITE_SIZE counters)")
     a = ap.parse_args(argv)
+
+    if a.cpu_stages:
+        return cpu_stage_table()
 
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the detector path runs on a single MI355X and has no "
@@ -252,27 +415,40 @@ def main(argv=None):
         o.premature_tol_s = 1e-6
         return R.rtcc_create(R.model_desc(cfg), R.weights_blob(cfg, frame["weights"]), o)
 
-    dev_pts = [torch.from_numpy(p).to("cuda") for p in frame["points"]]
+    # a stream of frames: frame 0 is the config's, the others new seeded
+    # points and poses (the network is the same)
+    F = max(1, a.stream_frames)
+    frames = [frame] + [synth.make_frame(cfg, f) for f in range(1, F)]
+    dev_frames = [[torch.from_numpy(p).to("cuda") for p in fr["points"]] for fr in frames]
+    dev_pts = dev_frames[0]
     torch.cuda.synchronize()
 
-    # throughput: the library's executor, no node events
+    # throughput: the library's executor, no node events, cycling the stream
     ctx_t = make_ctx(a.exec, False)
-    wall, _ = timed_steps(ctx_t, cfg, frame, dev_pts, a.steps, a.warmup, R, torch, record_nodes=False)
+    used_f = used_points(ctx_t, cfg, frames, dev_frames, R)
+    release_us = []
+    wall, _ = timed_steps(ctx_t, cfg, frames, dev_frames, a.steps, a.warmup, R, torch, record_nodes=False,
+                          release_us=release_us)
     ms_per_step = wall / a.steps * 1e3
+    step_flops = [sum(encoder_flops(cfg, lw, u) for u in used_f[(a.warmup + i) % F]) for i in range(a.steps)]
+    value = sum(step_flops) / wall / 1e12
+    eager = None
+    if a.exec == "streams" and not a.no_graphs:
+        # the same stream launched kernel by kernel
+        o = R.rtcc_runtime_opts()
+        o.exec = R.RTCC_EXEC_PER_BRANCH_STREAMS
+        o.premature_tol_s = 1e-6
+        ctx_e = R.rtcc_create(R.model_desc(cfg), R.weights_blob(cfg, frame["weights"]), o)
+        wall_e, _ = timed_steps(ctx_e, cfg, frames, dev_frames, a.steps, a.warmup, R, torch, record_nodes=False)
+        ctx_e.close()
+        eager = dict(ms_per_step=round(wall_e / a.steps * 1e3, 4), value=round(sum(step_flops) / wall_e / 1e12, 3),
+                     unit="TFLOP/s")
     # roofline and per-node tables: one compute stream (the paper's execution
     # model), so that node durations do not overlap; conv nodes are timed by
     # events that bracket their kernels
     ctx = make_ctx("serial", True)
-    wall_s, node = timed_steps(ctx, cfg, frame, dev_pts, a.roofline_steps, a.warmup, R, torch)
+    wall_s, node = timed_steps(ctx, cfg, [frame], [dev_pts], a.roofline_steps, a.warmup, R, torch)
     rsteps = a.roofline_steps
-
-    # used points per agent (PFN FLOPs), from the library's pillar counts
-    used = []
-    for k in range(K):
-        cnt = R.rtcc_get_tensor(ctx, R.RTCC_T_PILLAR_COUNTS, k, np.int32)
-        used.append(int(np.minimum(cnt, cfg["max_pts"]).sum()))
-    enc_flops = sum(encoder_flops(cfg, lw, u) for u in used)
-    value = enc_flops * a.steps / wall / 1e12
 
     # node layout per agent: h2d, pillar, pfn, conv[L], up[S or 1], warp (0 unless in the branch);
     # post: warp_fuse (or fuse), head, decode, nms
@@ -326,8 +502,11 @@ def main(argv=None):
             "agents": K, "inputs": "device-resident",
             "executor": "per-branch streams" if a.exec == "streams" else "serial",
             "hip_graphs": bool(a.exec == "streams" and not a.no_graphs),
+            "stream_frames": F,
         },
         "serial_ms_per_step": round(wall_s / rsteps * 1e3, 4),
+        "eager_streams": eager,
+        "release_call_us_p50": round(float(np.median(release_us)), 2) if release_us else None,
         "roofline": {
             "bound": "mfma", "kernel": "3x3 conv: halo-tiled k_conv3s1 + implicit-GEMM k_igemm",
             "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",

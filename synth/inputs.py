@@ -84,11 +84,13 @@ def points_per_agent(cfg):
     return [int(v) for v in n] if n is not None else [int(cfg["n_points"])] * cfg["K"]
 
 
-def make_points(cfg):
-    """List of K float32 arrays [n_k, 4] = (x, y, z, intensity), agent frame."""
+def make_points(cfg, frame=0):
+    """List of K float32 arrays [n_k, 4] = (x, y, z, intensity), agent frame.
+    Frame f > 0 of a stream draws from its own child sequences (frame 0 is
+    the config's frame)."""
     out = []
     for k, n in enumerate(points_per_agent(cfg)):
-        rng = _rng(cfg, "points", k)
+        rng = _rng(cfg, "points", k) if frame == 0 else _rng(cfg, "points", k, frame)
         if cfg["dist"] == "uniform":
             pts = _uniform_cloud(rng, n, cfg)
         elif cfg["dist"] == "mixture":
@@ -99,13 +101,14 @@ def make_points(cfg):
     return out
 
 
-def make_poses(cfg):
+def make_poses(cfg, frame=0):
     """[K, 3] float64 agent-to-ego poses (yaw rad, tx m, ty m).
 
     Agent 0 is the ego vehicle (identity).  Other agents draw yaw uniform in
-    [-pi, pi) and a translation uniform in [-5, 5) m per axis.
+    [-pi, pi) and a translation uniform in [-5, 5) m per axis.  Frame f > 0
+    of a stream draws from its own child sequence.
     """
-    rng = _rng(cfg, "poses")
+    rng = _rng(cfg, "poses") if frame == 0 else _rng(cfg, "poses", frame)
     K = cfg["K"]
     poses = np.zeros((K, 3), dtype=np.float64)
     if K > 1:
@@ -127,12 +130,15 @@ def make_weights(cfg):
     return w
 
 
-def make_frame(name_or_cfg):
+def make_frame(name_or_cfg, frame=0):
+    """Inputs of one frame: points, poses and the (frame-independent)
+    weights.  ``frame`` > 0 gives further frames of a stream: new points and
+    poses, the same network."""
     cfg = config(name_or_cfg) if isinstance(name_or_cfg, str) else name_or_cfg
     return dict(
         cfg=cfg,
-        points=make_points(cfg),
-        poses=make_poses(cfg),
+        points=make_points(cfg, frame),
+        poses=make_poses(cfg, frame),
         weights=make_weights(cfg),
     )
 

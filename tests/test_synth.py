@@ -55,3 +55,18 @@ def test_ofdma_draws_are_deterministic_and_independent_per_trace():
     # branch inputs of 60.6 to 65.2 KiB of 16-byte points
     kib = np.array(synth.points_per_agent(cfg)) * arr["bytes_per_point"] / 1024
     assert abs(kib.min() - 60.6) < 0.01 and abs(kib.max() - 65.2) < 0.01
+
+
+def test_stream_frames_differ_and_frame_zero_is_the_config_frame():
+    a = synth.make_frame("t_attn")
+    b = synth.make_frame("t_attn", 0)
+    c = synth.make_frame("t_attn", 1)
+    d = synth.make_frame("t_attn", 1)
+    for k in range(len(a["points"])):
+        assert np.array_equal(a["points"][k], b["points"][k])
+        assert not np.array_equal(a["points"][k], c["points"][k])
+        assert np.array_equal(c["points"][k], d["points"][k])
+    assert np.array_equal(a["poses"], b["poses"]) and not np.array_equal(a["poses"][1:], c["poses"][1:])
+    assert np.all(c["poses"][0] == 0.0)
+    for name in a["weights"]:
+        assert np.array_equal(a["weights"][name], c["weights"][name])
