@@ -259,6 +259,55 @@ typedef struct rtcc_ctx rtcc_ctx;
 RTCC_API rtcc_status rtcc_create(const rtcc_model_desc *model, const void *weights, size_t weights_bytes,
                         const rtcc_runtime_opts *opts, rtcc_ctx **out);
 
+/* Weights checkpoint: the blob of rtcc_create with a manifest that names it
+ * (the paper's detector loads trained parameters, Sec. IV-A; here the
+ * parameters are a seeded draw, and the manifest says which).  Little
+ * endian, in this order:
+ *   header, 128 bytes:
+ *     [0, 8)     magic "RTCCWGT" and a NUL byte
+ *     [8, 12)    uint32 version = 1
+ *     [12, 16)   uint32 n_tensors, in [1, 4096]
+ *     [16, 48)   config id: text, NUL-terminated, zero-padded
+ *     [48, 56)   uint64 seed of the draw the weights come from (0 if none)
+ *     [56, 64)   uint64 data_offset: start of the data section, a multiple
+ *                of 64, after the tensor table (the gap is zero)
+ *     [64, 72)   uint64 data_bytes: the data section runs to the end of the
+ *                file (data_offset + data_bytes = file size)
+ *     [72, 104)  SHA-256 (FIPS 180-4) of the data section
+ *     [104, 128) zero
+ *   tensor table, n_tensors entries of 128 bytes, in data order:
+ *     [0, 64)    name, NUL-terminated, zero-padded
+ *     [64, 68)   uint32 dtype = 0 (float32)
+ *     [68, 72)   uint32 ndim in [1, 4]
+ *     [72, 104)  int64 shape[4] (entries past ndim are 0)
+ *     [104, 112) uint64 offset of the tensor in the data section
+ *     [112, 120) uint64 nbytes = 4 x the product of the shape
+ *     [120, 128) zero
+ *   data section: the tensors back to back with no gaps, which is exactly
+ *     the weights blob of rtcc_create (names and shapes as listed there:
+ *     pfn_w, pfn_b, s{s}c{l}_w / _b, up{s}_w / _b, head_w, head_b). */
+typedef struct rtcc_checkpoint_info {
+    char config_id[32];
+    uint64_t seed;
+    int32_t version;
+    int32_t n_tensors;
+    uint64_t data_bytes;
+    uint8_t sha256[32];      /* of the data section, as verified                */
+} rtcc_checkpoint_info;
+
+/* Parse and verify a checkpoint held in host memory (borrowed for the
+ * call): header, table, exact size and the data section's SHA-256.
+ * Errors: RTCC_E_ARG (NULL pointer), RTCC_E_MALFORMED (any check fails;
+ * rtcc_last_error(NULL) names it).  On error *info is zeroed. */
+RTCC_API rtcc_status rtcc_read_checkpoint(const void *file, size_t file_bytes, rtcc_checkpoint_info *info);
+
+/* rtcc_create from a checkpoint: verified as by rtcc_read_checkpoint, and
+ * its tensor table must list the descriptor's tensors in blob order with
+ * their names and shapes (RTCC_E_ARG otherwise).  The file is borrowed for
+ * the call only.  Other errors as rtcc_create. */
+RTCC_API rtcc_status rtcc_create_from_checkpoint(const rtcc_model_desc *model, const void *file, size_t file_bytes,
+                                                 const rtcc_runtime_opts *opts, rtcc_ctx **out);
+
 /* Release everything the context owns.  NULL is a no-op. */
 RTCC_API void rtcc_destroy(rtcc_ctx *ctx);
 

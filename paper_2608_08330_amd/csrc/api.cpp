@@ -1,8 +1,11 @@
 // extern "C" entry points of include/rtcc.h.  Argument marshalling onto the
 // controller; no computation happens here.
+#include <cstring>
 #include <new>
 #include <string>
+#include <vector>
 
+#include "checkpoint.hpp"
 #include "controller.hpp"
 
 struct rtcc_ctx {
@@ -49,6 +52,74 @@ rtcc_status rtcc_create(const rtcc_model_desc *model, const void *weights, size_
     }
     *out = ctx;
     return RTCC_OK;
+}
+
+rtcc_status rtcc_read_checkpoint(const void *file, size_t file_bytes, rtcc_checkpoint_info *info) {
+    if (!info) {
+        t_create_error = "info is NULL";
+        return RTCC_E_ARG;
+    }
+    std::memset(info, 0, sizeof(*info));
+    return guarded([&] {
+        rtcc::CkptView v;
+        std::string err;
+        const rtcc_status s = rtcc::parse_checkpoint(file, file_bytes, v, err);
+        if (s != RTCC_OK) {
+            t_create_error = err;
+            return s;
+        }
+        *info = v.info;
+        return RTCC_OK;
+    });
+}
+
+rtcc_status rtcc_create_from_checkpoint(const rtcc_model_desc *model, const void *file, size_t file_bytes,
+                                        const rtcc_runtime_opts *opts, rtcc_ctx **out) {
+    if (!out) return RTCC_E_ARG;
+    *out = nullptr;
+    std::vector<float> blob;
+    const rtcc_status s = guarded([&] {
+        if (!model) {
+            t_create_error = "model descriptor is NULL";
+            return RTCC_E_ARG;
+        }
+        rtcc::CkptView v;
+        std::string err;
+        rtcc_status st = rtcc::parse_checkpoint(file, file_bytes, v, err);
+        if (st != RTCC_OK) {
+            t_create_error = err;
+            return st;
+        }
+        rtcc::Plan plan;
+        if (!rtcc::make_plan(*model, plan, err)) {
+            t_create_error = err;
+            return RTCC_E_ARG;
+        }
+        // the tensor table must list exactly the descriptor's tensors, in
+        // blob order, with their shapes
+        const std::vector<rtcc::CkptTensor> want = rtcc::expected_tensors(plan);
+        if (want.size() != v.tensors.size()) {
+            t_create_error = "checkpoint has " + std::to_string(v.tensors.size()) + " tensors, descriptor needs " +
+                             std::to_string(want.size());
+            return RTCC_E_ARG;
+        }
+        for (size_t i = 0; i < want.size(); ++i) {
+            const rtcc::CkptTensor &a = v.tensors[i], &b = want[i];
+            bool same = a.name == b.name && a.ndim == b.ndim;
+            for (int d = 0; same && d < 4; ++d) same = a.shape[d] == b.shape[d];
+            if (!same) {
+                t_create_error = "checkpoint tensor " + std::to_string(i) + " is " + a.name +
+                                 " with another shape or name than the descriptor's " + b.name;
+                return RTCC_E_ARG;
+            }
+        }
+        // the data section may sit at any alignment in the caller's buffer
+        blob.resize(size_t(v.info.data_bytes / 4));
+        std::memcpy(blob.data(), v.data, size_t(v.info.data_bytes));
+        return RTCC_OK;
+    });
+    if (s != RTCC_OK) return s;
+    return rtcc_create(model, blob.data(), blob.size() * 4, opts, out);
 }
 
 void rtcc_destroy(rtcc_ctx *ctx) { delete ctx; }

@@ -26,18 +26,31 @@ void log_line(const std::string &s) {
 
 class FakeExecutor : public Executor {
   public:
-    rtcc_status init(const Plan &p, const HostWeights &, const rtcc_runtime_opts &o,
+    rtcc_status init(const Plan &p, const HostWeights &hw, const rtcc_runtime_opts &o,
                      std::string &) override {
         plan_ = p;
         staging_.assign(p.K, std::vector<float>(size_t(p.n_max) * 4, 0.f));
         std::ostringstream os;
         os << "init K=" << p.K << " H=" << p.H << " W=" << p.W << " H2=" << p.H2 << " W2=" << p.W2
            << " C=" << p.c_slot << " convs=" << p.convs.size() << " ups=" << p.ups.size()
-           << " exec=" << o.exec;
+           << " exec=" << o.exec << " weights_fnv=" << std::hex << weights_digest(hw) << std::dec;
         log_line(os.str());
         return RTCC_OK;
     }
     float *staging(int agent) override { return staging_[agent].data(); }
+    // FNV-1a (64-bit) over the prepared weight bytes: equal prepared weights
+    // give equal digests, so tests can tell which weights a context got
+    static uint64_t weights_digest(const HostWeights &hw) {
+        uint64_t h = 1469598103934665603ull;
+        auto eat = [&](const void *p, size_t n) {
+            const unsigned char *b = static_cast<const unsigned char *>(p);
+            for (size_t i = 0; i < n; ++i) h = (h ^ b[i]) * 1099511628211ull;
+        };
+        eat(hw.bias.data(), hw.bias.size() * sizeof(float));
+        eat(hw.mat_bf16.data(), hw.mat_bf16.size() * sizeof(uint16_t));
+        eat(hw.mat_f32.data(), hw.mat_f32.size() * sizeof(float));
+        return h;
+    }
     rtcc_status begin_frame(std::string &) override {
         log_line("begin_frame");
         return RTCC_OK;

@@ -132,6 +132,17 @@ class rtcc_uplink_desc(ctypes.Structure):
     ]
 
 
+class rtcc_checkpoint_info(ctypes.Structure):
+    _fields_ = [
+        ("config_id", ctypes.c_char * 32),
+        ("seed", ctypes.c_uint64),
+        ("version", ctypes.c_int32),
+        ("n_tensors", ctypes.c_int32),
+        ("data_bytes", ctypes.c_uint64),
+        ("sha256", ctypes.c_uint8 * 32),
+    ]
+
+
 class rtcc_detections(ctypes.Structure):
     _fields_ = [
         ("count", ctypes.c_int64),
@@ -148,7 +159,7 @@ class rtcc_detections(ctypes.Structure):
 
 
 EXPORTS = (
-    "rtcc_create", "rtcc_destroy", "rtcc_set_mode", "rtcc_staging_buffer", "rtcc_begin_frame",
+    "rtcc_create", "rtcc_read_checkpoint", "rtcc_create_from_checkpoint", "rtcc_destroy", "rtcc_set_mode", "rtcc_staging_buffer", "rtcc_begin_frame",
     "rtcc_release_branch", "rtcc_release_branch_device", "rtcc_join_and_detect",
     "rtcc_get_branch_state", "rtcc_tensor_bytes", "rtcc_get_tensor", "rtcc_profile_nodes",
     "rtcc_node_times", "rtcc_node_count", "rtcc_graph_stats", "rtcc_conv_plan", "rtcc_rotated_nms", "rtcc_rotated_nms_noalloc", "rtcc_uplink_emulate", "rtcc_schedule_model",
@@ -172,6 +183,9 @@ def _declare(lib):
     sig = {
         "rtcc_create": (S, [ctypes.POINTER(rtcc_model_desc), _P, ctypes.c_size_t,
                             ctypes.POINTER(rtcc_runtime_opts), ctypes.POINTER(_P)]),
+        "rtcc_read_checkpoint": (S, [_P, ctypes.c_size_t, ctypes.POINTER(rtcc_checkpoint_info)]),
+        "rtcc_create_from_checkpoint": (S, [ctypes.POINTER(rtcc_model_desc), _P, ctypes.c_size_t,
+                                            ctypes.POINTER(rtcc_runtime_opts), ctypes.POINTER(_P)]),
         "rtcc_destroy": (None, [_P]),
         "rtcc_set_mode": (S, [_P, ctypes.c_int]),
         "rtcc_staging_buffer": (S, [_P, ctypes.c_int32, ctypes.POINTER(_F), ctypes.POINTER(ctypes.c_int64)]),
@@ -337,6 +351,33 @@ def rtcc_create(desc, blob, opts=None, kind="gpu"):
         raise RtccError(st, msg.decode() if msg else "")
     ctx = Context(lib, h)
     ctx._opts = opts  # keeps allocator callbacks alive with the context
+    return ctx
+
+
+def rtcc_read_checkpoint(data, kind="gpu"):
+    """Verify a checkpoint (bytes); returns a dict of its manifest."""
+    lib = load(kind)
+    buf = ctypes.create_string_buffer(bytes(data), len(data))
+    info = rtcc_checkpoint_info()
+    st = lib.rtcc_read_checkpoint(buf, len(data), ctypes.byref(info))
+    if st != RTCC_OK:
+        msg = lib.rtcc_last_error(None)
+        raise RtccError(st, msg.decode() if msg else "")
+    return dict(config_id=info.config_id.decode(), seed=int(info.seed), version=int(info.version),
+                n_tensors=int(info.n_tensors), data_bytes=int(info.data_bytes), sha256=bytes(info.sha256).hex())
+
+
+def rtcc_create_from_checkpoint(desc, data, opts=None, kind="gpu"):
+    lib = load(kind)
+    buf = ctypes.create_string_buffer(bytes(data), len(data))
+    h = _P()
+    st = lib.rtcc_create_from_checkpoint(ctypes.byref(desc), buf, len(data),
+                                         ctypes.byref(opts) if opts is not None else None, ctypes.byref(h))
+    if st != RTCC_OK:
+        msg = lib.rtcc_last_error(None)
+        raise RtccError(st, msg.decode() if msg else "")
+    ctx = Context(lib, h)
+    ctx._opts = opts
     return ctx
 
 

@@ -8,7 +8,8 @@ C ABI and host models are built with -fsanitize=thread and with
     agent released from their own threads, racing duplicates, a thread
     polling branch states, infeasible frames and injected dispatch failures,
     in both release rules;
-  * tests/test_abi.py, with the sanitized host library and its runtime
+  * tests/test_abi.py and tests/test_checkpoint.py (the checkpoint parser
+    on malformed files), with the sanitized host library and its runtime
     preloaded into the interpreter.
 A sanitizer report, or a failed check, fails the test."""
 
@@ -62,7 +63,8 @@ def test_stress_driver_is_clean(san, model_files):
 def test_abi_tests_pass_under_sanitizer(san):
     so, _ = BS.build(san)
     r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-s", "-p", "no:cacheprovider", "-m", "not gpu",
-                        "-k", "not library_loads", os.path.join(ROOT, "tests", "test_abi.py")],
+                        "-k", "not library_loads", os.path.join(ROOT, "tests", "test_abi.py"),
+                        os.path.join(ROOT, "tests", "test_checkpoint.py")],
                        stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True, timeout=600, cwd=ROOT,
                        env=_env(san, so))
     assert REPORT[san] not in r.stdout, r.stdout[-4000:]
