@@ -3,8 +3,10 @@
 
 One step = one complete frame through the C ABI: K branch encoders
 (pillarize, point-feature net, 3x3 conv backbone, upsample) released on
-device-resident inputs, then the join (warp, fusion, head, decode, NMS,
-D2H).  --warp-in-branch moves the pose warp into the branches.
+device-resident inputs that all arrive at once (one batch of K completion
+events: one pillar-stage launch chain over the K agents, then every backbone
+on its own stream), then the join (warp, fusion, head, decode, NMS, D2H).
+--warp-in-branch moves the pose warp into the branches.
 
 Output: one JSON line with
   value       encoder throughput, TFLOP/s = algorithmic encoder FLOPs of the
@@ -105,23 +107,30 @@ def encoder_flops(cfg, lw, n_used):
     return pfn + sum(c["flops"] for c in lw["convs"]) + ups
 
 
-def timed_steps(ctx, cfg, frames, dev_pts, steps, warmup, R, torch, record_nodes=True, release_us=None):
+def timed_steps(ctx, cfg, frames, dev_pts, steps, warmup, R, torch, record_nodes=True, release_us=None, batch=True):
     """Warm-up, then exactly `steps` timed frames bracketed by device syncs.
     Step s runs stream frame s mod len(frames) (its own points and poses), as
-    a live stream does.  Returns wall seconds and (with record_nodes) the
-    per-node HIP-event times of every step; with release_us (a list), the
-    host time of every release call of the timed steps is appended to it."""
+    a live stream does.  Every agent's input arrives at once, so with
+    `batch` the K completion events are released in one call (one group);
+    otherwise one call per event.  Returns wall seconds and (with
+    record_nodes) the per-node HIP-event times of every step; with
+    release_us (a list), the host time of each frame's release calls is
+    appended to it."""
     K = cfg["K"]
     F = len(frames)
 
     def one(f, times=None):
         fr, dev = frames[f], dev_pts[f]
         R.rtcc_begin_frame(ctx, time.monotonic() - 1.0)
-        for k in range(K):
-            t0 = time.perf_counter()
-            R.rtcc_release_branch_device(ctx, k, dev[k].data_ptr(), len(fr["points"][k]), fr["poses"][k], 0.0)
-            if times is not None:
-                times.append((time.perf_counter() - t0) * 1e6)
+        t0 = time.perf_counter()
+        if batch:
+            R.rtcc_release_branches(ctx, [dict(agent=k, device=1, points=dev[k].data_ptr(), n=len(fr["points"][k]),
+                                               pose=fr["poses"][k], arrival_t=0.0) for k in range(K)])
+        else:
+            for k in range(K):
+                R.rtcc_release_branch_device(ctx, k, dev[k].data_ptr(), len(fr["points"][k]), fr["poses"][k], 0.0)
+        if times is not None:
+            times.append((time.perf_counter() - t0) * 1e6)
         return R.rtcc_join_and_detect(ctx)
 
     for w in range(warmup):
@@ -449,6 +458,11 @@ def main(argv=None):
     ctx = make_ctx("serial", True)
     wall_s, node = timed_steps(ctx, cfg, [frame], [dev_pts], a.roofline_steps, a.warmup, R, torch)
     rsteps = a.roofline_steps
+    # the same frames released one event at a time: every agent's pillar
+    # stage alone (a group of one)
+    ctx_1 = make_ctx("serial", True)
+    _, node_1 = timed_steps(ctx_1, cfg, [frame], [dev_pts], a.roofline_steps, a.warmup, R, torch, batch=False)
+    ctx_1.close()
 
     # node layout per agent: h2d, pillar, pfn, conv[L], up[S or 1], warp (0 unless in the branch);
     # post: warp_fuse (or fuse), head, decode, nms
@@ -463,7 +477,11 @@ def main(argv=None):
     conv_launches = L * K * rsteps
     achieved = conv_flops / (conv_ms * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if cfg["precision"] == "bf16" else PEAK_FP32_TFLOPS
-    pillar_ms = sum(node[:, k * per_agent + 1].sum() + node[:, k * per_agent + 2].sum() for k in range(K))
+    # pillar stage: the K agents released together run it as one launch
+    # chain, so every member's pillar + PFN nodes are the group's span
+    node_1 = np.array(node_1)
+    group_ms = float((node[:, 1] + node[:, 2]).sum())
+    single_ms = sum(float(node_1[:, k * per_agent + 1].sum() + node_1[:, k * per_agent + 2].sum()) for k in range(K))
     P = [int(R.rtcc_tensor_bytes(ctx, R.RTCC_T_PILLAR_CELLS, k)) // 4 for k in range(K)]
     pil_bytes = sum(16 * len(frame["points"][k]) + 8 * P[k] + lw["H"] * lw["W"] * cfg["c_pfn"] * lw["elt"]
                     for k in range(K)) * rsteps
@@ -506,7 +524,7 @@ def main(argv=None):
         },
         "serial_ms_per_step": round(wall_s / rsteps * 1e3, 4),
         "eager_streams": eager,
-        "release_call_us_p50": round(float(np.median(release_us)), 2) if release_us else None,
+        "release_us_per_frame_p50": round(float(np.median(release_us)), 2) if release_us else None,
         "roofline": {
             "bound": "mfma", "kernel": "3x3 conv: halo-tiled k_conv3s1 + implicit-GEMM k_igemm",
             "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
@@ -514,15 +532,23 @@ def main(argv=None):
             "launches": conv_launches, "avg_launch_us": round(conv_ms * 1e3 / conv_launches, 3),
         },
         "secondary_rooflines": {
-            "pillar_pfn_canvas": {"bound": "hbm", "achieved": round(pil_bytes / (pillar_ms * 1e-3) / 1e9, 1),
+            "pillar_pfn_canvas": {"bound": "hbm", "achieved": round(pil_bytes / (group_ms * 1e-3) / 1e9, 1),
                                   "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                                  "work": "16 n + 8 P + H*W*C_pfn*elt bytes (the dense canvas as output; the "
-                                          "kernels write the P pillar cells and clear the previous frame's)"},
+                                  "frac": round(pil_bytes / (group_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+                                  "agents": K, "span_us": round(group_ms / rsteps * 1e3, 2),
+                                  "per_agent_alone": {
+                                      "achieved": round(pil_bytes / (single_ms * 1e-3) / 1e9, 1),
+                                      "us_per_agent": round(single_ms / (K * rsteps) * 1e3, 2)},
+                                  "work": "16 n + 8 P + H*W*C_pfn*elt bytes per agent (the dense canvas as "
+                                          "output; the kernels write the P pillar cells and clear the previous "
+                                          "frame's), all K agents over the span of their one launch chain"},
         },
         "conv_layers": layers,
         "node_ms_mean": {
-            "pillar": round(float(np.mean([node[:, k * per_agent + 1] for k in range(K)])), 4),
-            "pfn_canvas": round(float(np.mean([node[:, k * per_agent + 2] for k in range(K)])), 4),
+            "pillar_group_of_%d" % K: round(float(node[:, 1].mean()), 4),
+            "pfn_canvas_group_of_%d" % K: round(float(node[:, 2].mean()), 4),
+            "pillar_alone": round(float(np.mean([node_1[:, k * per_agent + 1] for k in range(K)])), 4),
+            "pfn_canvas_alone": round(float(np.mean([node_1[:, k * per_agent + 2] for k in range(K)])), 4),
             "conv_total_per_agent": round(conv_ms / (K * rsteps), 4),
             "up_total_per_agent": round(float(np.sum([node[:, k * per_agent + 3 + L:k * per_agent + per_agent]
                                                       for k in range(K)]) / (K * rsteps)), 4),

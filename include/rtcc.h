@@ -80,8 +80,8 @@ typedef enum rtcc_fusion { RTCC_FUSE_MAX = 0, RTCC_FUSE_ATTN = 1 } rtcc_fusion;
 
 /* Release rule.  RELEASE (RTCC): r_k = a_k, each branch is dispatched by its
  * own completion event.  BARRIER: events are validated and recorded (the
- * branch stays WAITING); the K-th valid event releases all K encoders at A
- * and dispatches them in (A, k) = index order. */
+ * branch stays WAITING); the K-th valid event releases all K encoders at A,
+ * dispatched together in (A, k) = index order. */
 typedef enum rtcc_mode { RTCC_MODE_RELEASE = 0, RTCC_MODE_BARRIER = 1 } rtcc_mode;
 
 /* Executor.  PER_BRANCH_STREAMS: one HIP stream per agent plus a join
@@ -336,9 +336,9 @@ RTCC_API rtcc_status rtcc_begin_frame(rtcc_ctx *ctx, double t0_monotonic_s);
  * E_PREMATURE (now - t0 < arrival_t - tol).  A rejected event leaves the
  * branch WAITING.  RELEASE mode: enqueue the H2D copy and encoder E_k on
  * the branch stream and return without waiting.  BARRIER mode: record;
- * the K-th valid event enqueues all branches.  If an enqueue fails
- * (E_HIP / E_NOMEM), that branch stays WAITING, later branches of a
- * barrier release are not enqueued, and the frame's join returns
+ * the K-th valid event enqueues all branches, as one group (see
+ * rtcc_release_branches).  If an enqueue fails (E_HIP / E_NOMEM), the
+ * branches of that enqueue stay WAITING and the frame's join returns
  * E_STATE. */
 RTCC_API rtcc_status rtcc_release_branch(rtcc_ctx *ctx, int32_t agent, const float *host_points, int64_t n,
                                 const float pose[3], double arrival_t);
@@ -350,6 +350,38 @@ RTCC_API rtcc_status rtcc_release_branch(rtcc_ctx *ctx, int32_t agent, const flo
  * the call. */
 RTCC_API rtcc_status rtcc_release_branch_device(rtcc_ctx *ctx, int32_t agent, const float *device_points,
                                        int64_t n, const float pose[3], double arrival_t);
+
+/* One completion event of a batch (rtcc_release_branches). */
+typedef struct rtcc_event {
+    int32_t agent;
+    int32_t device;        /* 0: points in host memory (as rtcc_release_branch),
+                              1: resident in device memory (as
+                              rtcc_release_branch_device)                       */
+    const float *points;   /* [n][4] float32, agent frame                       */
+    int64_t n;
+    float pose[3];         /* agent-to-ego SE(2): yaw rad, tx m, ty m           */
+    double arrival_t;      /* a_k, seconds since t0                             */
+} rtcc_event;
+
+/* Completion events that arrived together (Sec. IV-B/IV-C: every e_k that
+ * has arrived releases its branch; several may arrive at once).  The events
+ * are checked and recorded in array order exactly as count calls of
+ * rtcc_release_branch / rtcc_release_branch_device would be (a second event
+ * for one agent within the batch is E_DUPLICATE); status, if not NULL,
+ * receives each event's result [count].  RELEASE mode: the branches of all
+ * accepted events are released as one group: their encoders' pillar stage
+ * runs as one launch chain over the group (one grid row per agent) and each
+ * backbone then continues on its own branch stream; the outputs are those
+ * of separate releases, bit for bit.  BARRIER mode: the events are
+ * recorded, and when the K-th valid event is among them all K branches are
+ * released as one group.  Returns RTCC_OK if every event was accepted and
+ * enqueued; otherwise an enqueue failure (E_HIP / E_NOMEM: the whole group
+ * stays WAITING and the frame's join returns E_STATE), else the first
+ * rejected event's status; rtcc_last_error names it.  E_ARG if count is not
+ * in [0, RTCC_MAX_AGENTS] or events is NULL with count > 0 (nothing
+ * recorded). */
+RTCC_API rtcc_status rtcc_release_branches(rtcc_ctx *ctx, int32_t count, const rtcc_event *events,
+                                           rtcc_status *status);
 
 /* Join and detect.  If any branch's input is undelivered the frame is
  * communication-infeasible: RTCC_E_INFEASIBLE, no fusion kernel is

@@ -151,6 +151,11 @@ rtcc_status rtcc_release_branch_device(rtcc_ctx *ctx, int32_t agent, const float
     return guarded([&] { return ctx->ctl.release(agent, device_points, n, pose, arrival_t, true); });
 }
 
+rtcc_status rtcc_release_branches(rtcc_ctx *ctx, int32_t count, const rtcc_event *events, rtcc_status *status) {
+    if (!ctx) return RTCC_E_ARG;
+    return guarded([&] { return ctx->ctl.release_group(count, events, status); });
+}
+
 rtcc_status rtcc_join_and_detect(rtcc_ctx *ctx, rtcc_detections *out) {
     if (!ctx) return RTCC_E_ARG;
     return guarded([&] { return ctx->ctl.join(out); });

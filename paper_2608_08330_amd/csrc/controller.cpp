@@ -85,21 +85,32 @@ rtcc_status Controller::begin_frame(double t0) {
     return RTCC_OK;
 }
 
-// Release and enqueue E_agent: z_k becomes RELEASED (input received, encoder
-// enqueued); RUNNING and FINISHED follow the device (refresh_state).  A
-// failed enqueue leaves the branch undispatched and marks the frame, whose
-// join then withholds the post-join subgraph.
-rtcc_status Controller::dispatch_locked(int agent, const float *pts, int64_t n, bool device_src) {
-    z_[agent] = RTCC_RELEASED;
-    dispatch_[agent] = now_s() - t0_;
-    std::string err;
-    rtcc_status s = ex_->dispatch(agent, pts, n, device_src, affine_[agent].data(), err);
-    if (s != RTCC_OK) {
-        z_[agent] = RTCC_WAITING;  // not enqueued; its recorded event still makes a repeat a duplicate
-        dispatch_failed_ = true;
-        return fail(s, "dispatch of branch " + std::to_string(agent) + " failed: " + err);
+// Release and enqueue the encoders of a group: every z_k becomes RELEASED
+// (input received, encoder enqueued); RUNNING and FINISHED follow the device
+// (refresh_state).  A failed enqueue leaves the group's branches
+// undispatched and marks the frame, whose join then withholds the post-join
+// subgraph.
+rtcc_status Controller::dispatch_locked(std::vector<Pending> &group) {
+    if (group.empty()) return RTCC_OK;
+    std::sort(group.begin(), group.end(), [](const Pending &a, const Pending &b) { return a.agent < b.agent; });
+    const double now = now_s() - t0_;
+    std::vector<DispatchItem> items;
+    for (const Pending &pd : group) {
+        z_[pd.agent] = RTCC_RELEASED;
+        dispatch_[pd.agent] = now;
+        items.push_back(DispatchItem{pd.agent, pd.pts, pd.n, pd.device_src, affine_[pd.agent].data()});
     }
-    dispatched_[agent] = 1;
+    std::string err;
+    rtcc_status s = ex_->dispatch(items.data(), int(items.size()), err);
+    if (s != RTCC_OK) {
+        // not enqueued; the recorded events still make repeats duplicates
+        for (const Pending &pd : group) z_[pd.agent] = RTCC_WAITING;
+        dispatch_failed_ = true;
+        std::string who;
+        for (const Pending &pd : group) who += (who.empty() ? "" : ", ") + std::to_string(pd.agent);
+        return fail(s, "dispatch of branch " + who + " failed: " + err);
+    }
+    for (const Pending &pd : group) dispatched_[pd.agent] = 1;
     return RTCC_OK;
 }
 
@@ -109,9 +120,8 @@ void Controller::refresh_state(int agent) {
     if (st > z_[agent]) z_[agent] = st;
 }
 
-rtcc_status Controller::release(int agent, const float *pts, int64_t n, const float pose[3],
-                                double arrival, bool device_src) {
-    std::lock_guard<std::mutex> lk(mu_);
+rtcc_status Controller::record_locked(int agent, const float *pts, int64_t n, const float pose[3],
+                                      double arrival, bool device_src, Pending *pd) {
     if (!in_frame_) return fail(RTCC_E_STATE, "release outside a frame");
     if (agent < 0 || agent >= plan_.K) return fail(RTCC_E_ARG, "agent out of range");
     if (z_[agent] != RTCC_WAITING || recorded_[agent]) return fail(RTCC_E_DUPLICATE, "duplicate completion event");
@@ -135,21 +145,57 @@ rtcc_status Controller::release(int agent, const float *pts, int64_t n, const fl
     pose_[agent] = {pose[0], pose[1], pose[2]};
     recorded_[agent] = 1;
     arrival_[agent] = arrival;
+    *pd = Pending{agent, arrival, pts, n, device_src};
+    return RTCC_OK;
+}
 
-    if (mode_ == RTCC_MODE_RELEASE) return dispatch_locked(agent, pts, n, device_src);
-
-    // Barrier: the branch stays WAITING (its input is recorded, its release
-    // waits for A); the K-th valid event releases every encoder at
-    // A = max_k a_k, and the (r_k, k) order with equal r_k is index order.
-    pending_.push_back(Pending{agent, arrival, pts, n, device_src});
+rtcc_status Controller::release_locked(std::vector<Pending> &accepted) {
+    if (accepted.empty()) return RTCC_OK;
+    if (mode_ == RTCC_MODE_RELEASE) return dispatch_locked(accepted);
+    // Barrier: the branches stay WAITING (their inputs are recorded, their
+    // release waits for A); the K-th valid event releases every encoder at
+    // A = max_k a_k, as one group in index order.
+    pending_.insert(pending_.end(), accepted.begin(), accepted.end());
     if (int(pending_.size()) < plan_.K) return RTCC_OK;
     std::vector<Pending> ready;
     ready.swap(pending_);
-    std::sort(ready.begin(), ready.end(), [](const Pending &a, const Pending &b) { return a.agent < b.agent; });
-    for (const Pending &pd : ready) {
-        rtcc_status s = dispatch_locked(pd.agent, pd.pts, pd.n, pd.device_src);
-        if (s != RTCC_OK) return s;
+    return dispatch_locked(ready);
+}
+
+rtcc_status Controller::release(int agent, const float *pts, int64_t n, const float pose[3],
+                                double arrival, bool device_src) {
+    std::lock_guard<std::mutex> lk(mu_);
+    Pending pd{};
+    rtcc_status s = record_locked(agent, pts, n, pose, arrival, device_src, &pd);
+    if (s != RTCC_OK) return s;
+    std::vector<Pending> one{pd};
+    return release_locked(one);
+}
+
+rtcc_status Controller::release_group(int32_t count, const rtcc_event *events, rtcc_status *status) {
+    std::lock_guard<std::mutex> lk(mu_);
+    if (count < 0 || count > RTCC_MAX_AGENTS) return fail(RTCC_E_ARG, "event count out of [0, RTCC_MAX_AGENTS]");
+    if (count > 0 && !events) return fail(RTCC_E_ARG, "NULL events");
+    std::vector<Pending> accepted;
+    rtcc_status first = RTCC_OK;
+    std::string first_err;
+    for (int32_t i = 0; i < count; ++i) {
+        const rtcc_event &e = events[i];
+        Pending pd{};
+        rtcc_status s = e.device != 0 && e.device != 1
+                            ? fail(RTCC_E_MALFORMED, "event.device must be 0 or 1")
+                            : record_locked(e.agent, e.points, e.n, e.pose, e.arrival_t, e.device == 1, &pd);
+        if (status) status[i] = s;
+        if (s == RTCC_OK) {
+            accepted.push_back(pd);
+        } else if (first == RTCC_OK) {
+            first = s;
+            first_err = "event " + std::to_string(i) + ": " + err_;
+        }
     }
+    const rtcc_status d = release_locked(accepted);
+    if (d != RTCC_OK) return d;  // the frame cannot complete: reported first
+    if (first != RTCC_OK) return fail(first, first_err);
     return RTCC_OK;
 }
 

@@ -19,6 +19,14 @@ namespace rtcc {
 
 // What the controller asks of an executor.  All calls come with the
 // controller's mutex held.
+struct DispatchItem {
+    int agent;
+    const float *pts;
+    int64_t n;
+    bool device_src;
+    const float *affine;  // [6]
+};
+
 class Executor {
   public:
     virtual ~Executor() = default;
@@ -26,11 +34,11 @@ class Executor {
                              std::string &err) = 0;
     virtual float *staging(int agent) = 0;
     virtual rtcc_status begin_frame(std::string &err) = 0;
-    // Enqueue H2D (unless device_src) and encoder E_agent; `affine` is the
-    // agent's pose warp (index space), used by the branch when the warp is
-    // its last node.
-    virtual rtcc_status dispatch(int agent, const float *pts, int64_t n, bool device_src, const float affine[6],
-                                 std::string &err) = 0;
+    // Enqueue H2D (unless device_src) and encoder E_k of every item, as one
+    // group released together (m >= 1, distinct agents in ascending order).
+    // `affine` is the agent's pose warp (index space), used by the branch
+    // when the warp is its last node.
+    virtual rtcc_status dispatch(const DispatchItem *items, int m, std::string &err) = 0;
     // Progress of a dispatched encoder on the device: 0 enqueued (its input
     // copy or earlier work of its stream still ahead of it), 1 started, 2
     // finished (its slot is stored).  Never blocks.
@@ -83,6 +91,9 @@ class Controller {
     rtcc_status begin_frame(double t0);
     rtcc_status release(int agent, const float *pts, int64_t n, const float pose[3], double arrival,
                         bool device_src);
+    // Events that arrived together: each validated and recorded in order as
+    // release() would; the accepted ones are released as one group.
+    rtcc_status release_group(int32_t count, const rtcc_event *events, rtcc_status *status);
     rtcc_status join(rtcc_detections *out);
     rtcc_status branch_state(int agent, int32_t *state);
     rtcc_status tensor_bytes(int id, int agent, size_t *bytes);
@@ -100,7 +111,15 @@ class Controller {
         err_ = msg;
         return s;
     }
-    rtcc_status dispatch_locked(int agent, const float *pts, int64_t n, bool device_src);
+    // Validate and record one completion event (Sec. IV-C); on success *pd
+    // is the branch's pending release.
+    rtcc_status record_locked(int agent, const float *pts, int64_t n, const float pose[3], double arrival,
+                              bool device_src, Pending *pd);
+    // Release the recorded branches of `group` (ascending agents) together.
+    rtcc_status dispatch_locked(std::vector<Pending> &group);
+    // RELEASE: dispatch `accepted` now; BARRIER: add it to the pending set
+    // and dispatch all K once the K-th event is in.
+    rtcc_status release_locked(std::vector<Pending> &accepted);
     // z_k of a dispatched branch follows its encoder on the device.
     void refresh_state(int agent);
 

@@ -9,6 +9,12 @@
 // and slot (Sec. IV-D), so branches never share memory and may overlap.  The
 // join waits on every branch's completion event on the GPU (no host wait)
 // before the post-join kernels run.
+//
+// Branches released together (one batch of events, or every branch at the
+// barrier's A) share one launch chain of the pillar stage: its kernels run
+// the group's agents side by side (one grid row per agent) on the first
+// member's stream, after which every member's backbone continues on its own
+// stream.  A single release is a group of one.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -83,7 +89,7 @@ class HipExecutor : public Executor {
             HIP_TRY(alloc(&b.d_poffs, n_max * 4));
             HIP_TRY(alloc(&b.d_overfull, over_cap * 4));
             HIP_TRY(alloc(&b.d_counts, n_cells * 4));
-            HIP_TRY(hipMemset(b.d_counts, 0, n_cells * 4));  // afterwards the PFN kernel leaves them zero
+            HIP_TRY(hipMemset(b.d_counts, 0, n_cells * 4));  // afterwards the cell scan leaves them zero
             HIP_TRY(alloc(&b.d_offsets, n_cells * 4));
             HIP_TRY(alloc(&b.d_tiles, n_tiles * 8));
             HIP_TRY(alloc(&b.d_meta, 64));
@@ -112,6 +118,27 @@ class HipExecutor : public Executor {
             if (p.d.warp_in_branch)
                 for (auto &e : b.wev) HIP_TRY(hipEventCreate(&e));
         }
+        // every agent's pillar buffers, as the pillar kernels index them
+        std::vector<kern::PillarBufs> pb(p.K);
+        for (int k = 0; k < p.K; ++k) {
+            const Branch &b = br_[k];
+            pb[k].cell = static_cast<int32_t *>(b.d_cell);
+            pb[k].slot = static_cast<int32_t *>(b.d_slot);
+            pb[k].counts = static_cast<int32_t *>(b.d_counts);
+            pb[k].tiles = static_cast<int32_t *>(b.d_tiles);
+            pb[k].meta = static_cast<int32_t *>(b.d_meta);
+            pb[k].offsets = static_cast<int32_t *>(b.d_offsets);
+            pb[k].pcells = static_cast<int32_t *>(b.d_pcells);
+            pb[k].pcounts = static_cast<int32_t *>(b.d_pcounts);
+            pb[k].poffs = static_cast<int32_t *>(b.d_poffs);
+            pb[k].overfull = static_cast<int32_t *>(b.d_overfull);
+            pb[k].member = static_cast<int32_t *>(b.d_member);
+            pb[k].sorted = static_cast<float4 *>(b.d_sorted);
+            pb[k].canvas = b.d_canvas;
+        }
+        HIP_TRY(alloc(&d_pbufs_, sizeof(kern::PillarBufs) * p.K));
+        HIP_TRY(hipMemcpy(d_pbufs_, pb.data(), sizeof(kern::PillarBufs) * p.K, hipMemcpyHostToDevice));
+        HIP_TRY(hipEventCreateWithFlags(&ev_group_, hipEventDisableTiming));
         HIP_TRY(alloc(&d_fused, size_t(p.H2) * p.W2 * p.c_slot * p.elt));
         d_fused_stage_.assign(p.ups.size(), nullptr);
         if (p.d.multiscale)
@@ -188,50 +215,116 @@ class HipExecutor : public Executor {
         return RTCC_OK;
     }
 
-    rtcc_status dispatch(int agent, const float *pts, int64_t n, bool device_src, const float affine[6],
-                         std::string &err) override {
+    rtcc_status dispatch(const DispatchItem *items, int m, std::string &err) override {
         HIP_TRY(hipSetDevice(dev_));
-        Branch &b = br_[agent];
-        for (int e = 0; e < 6; ++e) b.affine[e] = affine[e];
+        if (m < 1 || m > kern::kMaxGroup) {
+            err = "dispatch group of " + std::to_string(m) + " agents";
+            return RTCC_E_INTERNAL;
+        }
         const bool serial = o_.exec == RTCC_EXEC_SERIAL;
-        hipStream_t cs = serial ? join_stream_ : b.stream;
         const bool timing = o_.node_timing != 0;
-        if (timing) HIP_TRY(hipEventRecord(b.ev[0], cs));
-        const float *src = pts;
-        if (!device_src) {
-            src = static_cast<const float *>(b.d_pts);
-            if (n > 0) {
-                if (serial) {
-                    // dedicated transfer stream, event, compute stream waits
-                    HIP_TRY(hipMemcpyAsync(b.d_pts, b.staging, size_t(n) * 16, hipMemcpyHostToDevice, copy_stream_));
-                    HIP_TRY(hipEventRecord(b.h2d_done, copy_stream_));
-                    HIP_TRY(hipStreamWaitEvent(cs, b.h2d_done, 0));
-                } else {
-                    HIP_TRY(hipMemcpyAsync(b.d_pts, b.staging, size_t(n) * 16, hipMemcpyHostToDevice, cs));
+        Branch &lead = br_[items[0].agent];
+        // the group's pillar stage runs on the first member's stream
+        hipStream_t ls = serial ? join_stream_ : lead.stream;
+        int agents[kern::kMaxGroup];
+        for (int j = 0; j < m; ++j) {
+            const DispatchItem &it = items[j];
+            agents[j] = it.agent;
+            Branch &b = br_[it.agent];
+            for (int e = 0; e < 6; ++e) b.affine[e] = it.affine[e];
+            hipStream_t bs = serial ? join_stream_ : b.stream;
+            if (timing) HIP_TRY(hipEventRecord(b.ev[0], bs));
+            const float *src = it.pts;
+            if (!it.device_src) {
+                src = static_cast<const float *>(b.d_pts);
+                if (it.n > 0) {
+                    // the member's own stream (the lead's is ls), or in
+                    // SERIAL mode the transfer stream
+                    HIP_TRY(hipMemcpyAsync(b.d_pts, b.staging, size_t(it.n) * 16, hipMemcpyHostToDevice,
+                                           serial ? copy_stream_ : bs));
+                    if (serial) {
+                        HIP_TRY(hipEventRecord(b.h2d_done, copy_stream_));
+                        HIP_TRY(hipStreamWaitEvent(ls, b.h2d_done, 0));
+                    }
                 }
             }
+            // ls runs after the member's input copy and after the work of the
+            // last frame queued on the member's stream (its canvas clear)
+            if (bs != ls) {
+                HIP_TRY(hipEventRecord(b.h2d_done, bs));
+                HIP_TRY(hipStreamWaitEvent(ls, b.h2d_done, 0));
+            }
+            b.src = src;
+            b.n = int32_t(it.n);
+            b.host_input = !it.device_src;
+            HIP_TRY(prepare_branch(b, ls));
         }
-        b.src = src;
-        b.n = int32_t(n);
-        b.host_input = !device_src;
-        HIP_TRY(prepare_branch(b, cs));
-        // reached once the input copy and everything queued before the
-        // encoder on its stream have completed: the encoder is running
-        HIP_TRY(hipEventRecord(b.started, cs));
-        rtcc_status s;
-        if (o_.use_graphs && !timing) {
+        // reached once every member's input copy and everything queued
+        // before the group's encoders have completed: the encoders run
+        for (int j = 0; j < m; ++j) HIP_TRY(hipEventRecord(br_[agents[j]].started, ls));
+        rtcc_status st;
+        const bool graphs = o_.use_graphs && !timing;
+        if (m == 1) {
+            // a branch released alone: its whole encoder, as one graph whose
+            // arguments are its input, point count and (branch warp) pose
+            Branch &b = lead;
+            if (graphs) {
+                std::vector<unsigned char> key;
+                put(key, b.src);
+                put(key, b.n);
+                if (p_.d.warp_in_branch)
+                    for (int e = 0; e < 6; ++e) put(key, b.affine[e]);
+                st = run_graph(b.graph, key, ls, [&](hipStream_t c) {
+                    rtcc_status r = enqueue_pillars(agents, 1, c, false, err);
+                    return r == RTCC_OK ? enqueue_backbone(b, c, false, err) : r;
+                }, err);
+            } else {
+                st = enqueue_pillars(agents, 1, ls, timing, err);
+                if (st == RTCC_OK) st = enqueue_backbone(b, ls, timing, err);
+            }
+            if (st != RTCC_OK) return st;
+            b.canvas_dirty = true;  // the encoder writes this frame's pillars
+            HIP_TRY(hipEventRecord(b.done, ls));
+            b.dispatched = true;
+            return RTCC_OK;
+        }
+        // a group: one pillar-stage chain over the members (a graph whose
+        // arguments are the members, their inputs and point counts), then
+        // every member's backbone on its own stream
+        if (graphs) {
             std::vector<unsigned char> key;
-            put(key, b.src);
-            put(key, b.n);
-            for (int e = 0; e < 6; ++e) put(key, b.affine[e]);
-            s = run_graph(b.graph, key, cs, [&](hipStream_t c) { return enqueue_encoder(b, c, false, 1, err); }, err);
+            for (int j = 0; j < m; ++j) {
+                put(key, agents[j]);
+                put(key, br_[agents[j]].src);
+                put(key, br_[agents[j]].n);
+            }
+            st = run_graph(group_graph_, key, ls,
+                           [&](hipStream_t c) { return enqueue_pillars(agents, m, c, false, err); }, err);
         } else {
-            s = enqueue_encoder(b, cs, timing, 1, err);
+            st = enqueue_pillars(agents, m, ls, timing, err);
         }
-        if (s != RTCC_OK) return s;
-        b.canvas_dirty = true;  // the encoder writes this frame's pillars
-        HIP_TRY(hipEventRecord(b.done, cs));
-        b.dispatched = true;
+        if (st != RTCC_OK) return st;
+        if (!serial) HIP_TRY(hipEventRecord(ev_group_, ls));
+        for (int j = 0; j < m; ++j) {
+            Branch &b = br_[agents[j]];
+            hipStream_t bs = serial ? join_stream_ : b.stream;
+            if (bs != ls) HIP_TRY(hipStreamWaitEvent(bs, ev_group_, 0));
+            if (graphs) {
+                // the backbone's arguments are fixed buffers; only a branch
+                // warp depends on the frame (its pose)
+                std::vector<unsigned char> key;
+                if (p_.d.warp_in_branch)
+                    for (int e = 0; e < 6; ++e) put(key, b.affine[e]);
+                st = run_graph(b.backbone_graph, key, bs,
+                               [&](hipStream_t c) { return enqueue_backbone(b, c, false, err); }, err);
+            } else {
+                st = enqueue_backbone(b, bs, timing, err);
+            }
+            if (st != RTCC_OK) return st;
+            b.canvas_dirty = true;
+            HIP_TRY(hipEventRecord(b.done, bs));
+            b.dispatched = true;
+        }
         return RTCC_OK;
     }
 
@@ -358,8 +451,13 @@ class HipExecutor : public Executor {
             for (int k = 0; k <= p_.K; ++k) {
                 if (k < p_.K) HIP_TRY(prepare_branch(br_[k], s));
                 HIP_TRY(hipEventRecord(e0, s));
-                rtcc_status st = k < p_.K ? enqueue_encoder(br_[k], s, false, 0, err)
-                                          : enqueue_post(last_affine_, last_poses_, s, false, err);
+                rtcc_status st;
+                if (k < p_.K) {
+                    st = enqueue_pillars(&k, 1, s, false, err);
+                    if (st == RTCC_OK) st = enqueue_backbone(br_[k], s, false, err);
+                } else {
+                    st = enqueue_post(last_affine_, last_poses_, s, false, err);
+                }
                 if (st != RTCC_OK) return st;
                 HIP_TRY(hipEventRecord(e1, s));
                 if (k < p_.K) {
@@ -396,8 +494,11 @@ class HipExecutor : public Executor {
         const int L = int(p_.convs.size()), S = int(p_.ups.size());
         for (const Branch &b : br_) {
             float v = 0.f;
+            // input copy, then the pillar stage (shared by a group: timed by
+            // the events of its first member)
+            const Branch &g = br_[b.ev_src];
             for (int e = 0; e < 3; ++e) {
-                HIP_TRY(hipEventElapsedTime(&v, b.ev[e], b.ev[e + 1]));
+                HIP_TRY(hipEventElapsedTime(&v, e == 0 ? b.ev[0] : g.ev[e], g.ev[e + 1]));
                 ms[q++] = v;
             }
             for (int l = 0; l < L; ++l) {
@@ -511,7 +612,8 @@ class HipExecutor : public Executor {
         bool pillars_clean = true;       // every enqueued K1 was followed by the PFN kernel
         bool canvas_dirty = false;       // the canvas holds pillars not yet cleared (canvas_clear)
         hipEvent_t wev[2] = {nullptr, nullptr};  // bracket the branch warp kernel
-        Graph graph;                     // the encoder as a HIP graph (use_graphs)
+        Graph graph;                     // the encoder as a HIP graph (use_graphs, released alone)
+        Graph backbone_graph;            // its backbone (use_graphs, released in a group)
         std::vector<void *> d_act;
         hipStream_t stream = nullptr;
         hipEvent_t done = nullptr, h2d_done = nullptr, started = nullptr;
@@ -521,6 +623,7 @@ class HipExecutor : public Executor {
         int32_t n = 0;
         bool host_input = true;
         bool dispatched = false;
+        int ev_src = 0;  // the branch whose ev[1..3] timed this one's pillar stage
     };
 
     hipStream_t compute_stream_for_join() const { return join_stream_; }
@@ -552,62 +655,62 @@ class HipExecutor : public Executor {
         return alloc(reinterpret_cast<void **>(p), bytes);
     }
 
-    // Encoder E_k: pillarize, PFN canvas, backbone, upsample into slot k.
-    // `ev_base` is the index of the event recorded after the input copy.
-    rtcc_status enqueue_encoder(Branch &b, hipStream_t s, bool timing, int ev_base, std::string &err) {
+    // Pillar stage of the encoders of `agents` (m of them, side by side in
+    // every launch): cell ids, scans, scatter, PFN canvas.  With timing, each
+    // member's node times for them are those of the first member's ev[1] /
+    // ev[2] / ev[3].
+    rtcc_status enqueue_pillars(const int *agents, int m, hipStream_t s, bool timing, std::string &err) {
         const Plan &p = p_;
         const int n_cells = p.H * p.W;
-        const int n = b.n;
-        int32_t *counts = static_cast<int32_t *>(b.d_counts);
-        int32_t *offsets = static_cast<int32_t *>(b.d_offsets);
-        int32_t *tiles = static_cast<int32_t *>(b.d_tiles);
-        int32_t *meta = static_cast<int32_t *>(b.d_meta);
-        int ev = ev_base;
-        if (timing) HIP_TRY(hipEventRecord(b.ev[ev], s));
-        ++ev;
+        kern::PillarGroup grp{};
+        grp.bufs = static_cast<const kern::PillarBufs *>(d_pbufs_);
+        grp.m = m;
+        grp.n_max = 0;
+        for (int j = 0; j < m; ++j) {
+            const Branch &b = br_[agents[j]];
+            grp.agent[j] = agents[j];
+            grp.pts[j] = reinterpret_cast<const float4 *>(b.src);
+            grp.n[j] = b.n;
+            grp.n_max = std::max(grp.n_max, b.n);
+        }
+        // the shared stages are timed once, by the first member's events
+        for (int j = 0; j < m; ++j) br_[agents[j]].ev_src = agents[0];
+        auto mark = [&](int e) -> hipError_t {
+            return timing ? hipEventRecord(br_[agents[0]].ev[e], s) : hipSuccess;
+        };
+        HIP_TRY(mark(1));
         kern::PillarGeom g{p.d.x_min, p.d.x_max, p.d.y_min, p.d.y_max, p.d.z_min, p.d.z_max,
                            p.d.pillar_size, p.H, p.W};
-        // Between frames the cell counts are zero (the PFN kernel returns
-        // them to zero) and the canvas is zero outside the last frame's
-        // pillars (prepare_branch).
-        b.pillars_clean = false;
-        HIP_TRY(kern::cell_ids(b.src, n, g, static_cast<int32_t *>(b.d_cell), static_cast<int32_t *>(b.d_slot),
-                               counts, s));
-        HIP_TRY(kern::scan_reduce(counts, n_cells, tiles, meta, s));
-        HIP_TRY(kern::scan_down(counts, n_cells, tiles, p.d.max_points_per_pillar, offsets,
-                                static_cast<int32_t *>(b.d_pcells), static_cast<int32_t *>(b.d_pcounts),
-                                static_cast<int32_t *>(b.d_poffs), static_cast<int32_t *>(b.d_overfull), meta, s));
-        HIP_TRY(kern::scatter(static_cast<int32_t *>(b.d_cell), static_cast<int32_t *>(b.d_slot), offsets, n,
-                              b.src, static_cast<int32_t *>(b.d_member), static_cast<float *>(b.d_sorted), s));
-        if (timing) HIP_TRY(hipEventRecord(b.ev[ev], s));
-        ++ev;
+        // Between frames the cell counts are zero (the second scan pass
+        // returns them to zero) and the canvas is zero outside the last
+        // frame's pillars (prepare_branch).
+        for (int j = 0; j < m; ++j) br_[agents[j]].pillars_clean = false;
+        HIP_TRY(kern::cell_ids(grp, g, s));
+        HIP_TRY(kern::scan_reduce(grp, n_cells, s));
+        HIP_TRY(kern::scan_down(grp, n_cells, p.d.max_points_per_pillar, s));
+        HIP_TRY(kern::scatter(grp, s));
+        HIP_TRY(mark(2));
 
         kern::PfnArgs pa{};
-        pa.sorted = static_cast<float4 *>(b.d_sorted);
-        pa.counts = counts;
-        pa.pcells = static_cast<const int32_t *>(b.d_pcells);
-        pa.pcounts = static_cast<const int32_t *>(b.d_pcounts);
-        pa.poffs = static_cast<const int32_t *>(b.d_poffs);
-        pa.meta = meta;
         pa.w = static_cast<const float *>(d_bias) + p.pfn_w_off;
         pa.b = static_cast<const float *>(d_bias) + p.pfn_b_off;
-        pa.canvas = b.d_canvas;
         pa.C = p.c_pfn;
         pa.max_pts = p.d.max_points_per_pillar;
         pa.inv_hx = float(2.0 / (double(p.d.x_max) - double(p.d.x_min)));
         pa.inv_hy = float(2.0 / (double(p.d.y_max) - double(p.d.y_min)));
         pa.z0 = p.d.z_min;
         pa.inv_dz = float(1.0 / (double(p.d.z_max) - double(p.d.z_min)));
-        pa.overfull = static_cast<const int32_t *>(b.d_overfull);
-        pa.offsets = offsets;
-        pa.member = static_cast<int32_t *>(b.d_member);
-        pa.pts = reinterpret_cast<const float4 *>(b.src);
-        pa.n = n;
-        HIP_TRY(kern::pfn_canvas(p.bf16, pa, n < n_cells ? n : n_cells, s));
-        b.pillars_clean = true;
-        if (timing) HIP_TRY(hipEventRecord(b.ev[ev], s));
-        ++ev;
+        HIP_TRY(kern::pfn_canvas(p.bf16, pa, grp, grp.n_max < n_cells ? grp.n_max : n_cells, s));
+        for (int j = 0; j < m; ++j) br_[agents[j]].pillars_clean = true;
+        HIP_TRY(mark(3));
+        return RTCC_OK;
+    }
 
+    // Backbone of encoder E_k after its pillar stage: convs, upsampling into
+    // slot k, and the branch warp when it is the branch's last node.
+    rtcc_status enqueue_backbone(Branch &b, hipStream_t s, bool timing, std::string &err) {
+        const Plan &p = p_;
+        int ev = 4;
         const void *x = b.d_canvas;
         for (size_t l = 0; l < p.convs.size(); ++l) {
             const ConvLayer &c = p.convs[l];
@@ -990,7 +1093,10 @@ class HipExecutor : public Executor {
             for (hipEvent_t e : b.wev)
                 if (e) (void)hipEventDestroy(e);
             drop(b.graph);
+            drop(b.backbone_graph);
         }
+        drop(group_graph_);
+        if (ev_group_) (void)hipEventDestroy(ev_group_);
         for (void *ptr : dev_allocs_) {
             if (o_.dev_alloc) o_.dev_free(ptr, o_.alloc_user);
             else (void)hipFree(ptr);
@@ -1034,6 +1140,9 @@ class HipExecutor : public Executor {
     std::vector<void *> d_fused_stage_;  // multi-scale: fused map of every stage
     hipStream_t cap_stream_ = nullptr;   // where graphs are captured (use_graphs)
     Graph post_graph_[2];                // post-join: up to T^head, then decode and NMS
+    Graph group_graph_;                  // pillar stage of a group of branches
+    void *d_pbufs_ = nullptr;            // kern::PillarBufs of every agent
+    hipEvent_t ev_group_ = nullptr;      // a group's pillar stage is done
     int64_t graph_stats_[3] = {0, 0, 0}; // instantiations, update attempts, launches
 };
 

@@ -55,22 +55,32 @@ class FakeExecutor : public Executor {
         log_line("begin_frame");
         return RTCC_OK;
     }
-    rtcc_status dispatch(int agent, const float *pts, int64_t n, bool device_src, const float affine[6],
-                         std::string &err) override {
+    rtcc_status dispatch(const DispatchItem *items, int m, std::string &err) override {
         {
             std::lock_guard<std::mutex> lk(g_log_mu);
-            g_progress[agent] = 0;
-            if (g_fail_dispatch[agent]) {
-                g_fail_dispatch[agent] = false;
-                err = "injected dispatch failure";
-                return RTCC_E_HIP;
-            }
+            for (int j = 0; j < m; ++j) g_progress[items[j].agent] = 0;
+            for (int j = 0; j < m; ++j)
+                if (g_fail_dispatch[items[j].agent]) {
+                    g_fail_dispatch[items[j].agent] = false;
+                    err = "injected dispatch failure";
+                    return RTCC_E_HIP;
+                }
         }
-        std::ostringstream os;
-        os << "dispatch " << agent << " n=" << n << " src=" << (device_src ? "device" : "staging")
-           << " staged=" << (pts == staging_[agent].data() ? 1 : 0) << " affine=[" << affine[0] << ","
-           << affine[1] << "," << affine[2] << "," << affine[3] << "," << affine[4] << "," << affine[5] << "]";
-        log_line(os.str());
+        if (m > 1) {
+            std::ostringstream os;
+            os << "group";
+            for (int j = 0; j < m; ++j) os << " " << items[j].agent;
+            log_line(os.str());
+        }
+        for (int j = 0; j < m; ++j) {
+            const DispatchItem &it = items[j];
+            const float *affine = it.affine;
+            std::ostringstream os;
+            os << "dispatch " << it.agent << " n=" << it.n << " src=" << (it.device_src ? "device" : "staging")
+               << " staged=" << (it.pts == staging_[it.agent].data() ? 1 : 0) << " affine=[" << affine[0] << ","
+               << affine[1] << "," << affine[2] << "," << affine[3] << "," << affine[4] << "," << affine[5] << "]";
+            log_line(os.str());
+        }
         return RTCC_OK;
     }
     int progress(int agent) override {

@@ -20,52 +20,61 @@ constexpr int kScanTile = 2048;  // cells per block of the cell scans
 
 hipError_t fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s);
 
+// One agent's pillar-stage buffers (device pointers, fixed for a context).
+// Sizes: cell, slot, member [n_max]; sorted [n_max] points; counts,
+// offsets [H*W]; tiles [2 * tiles of kScanTile cells]; pcells, pcounts,
+// poffs [min(n_max, H*W)]; overfull [n_max / (max_pts + 1) + 1]; meta [3];
+// canvas [H*W][C].
+struct PillarBufs {
+    int32_t *cell, *slot, *counts, *tiles, *meta, *offsets;
+    int32_t *pcells, *pcounts, *poffs, *overfull, *member;
+    float4 *sorted;
+    void *canvas;
+};
+
+// The agents whose pillar stage one launch chain runs: blockIdx.y = j
+// takes agent agent[j] (its buffers bufs[agent[j]], its n[j] points at
+// pts[j]).  One agent is a group of one.
+constexpr int kMaxGroup = 16;
+struct PillarGroup {
+    const PillarBufs *bufs;  // device array, indexed by agent
+    const float4 *pts[kMaxGroup];
+    int32_t n[kMaxGroup];
+    int32_t agent[kMaxGroup];
+    int32_t m;      // agents in the group, 1..kMaxGroup
+    int32_t n_max;  // max over the group of n[j]
+};
+
 // K1: cell id per point (-1 if dropped); counts[cell] += 1 (counts start at
 // zero) and the point's rank of arrival in its cell (an arbitrary order) goes
 // to slot[i].
-hipError_t cell_ids(const float *pts, int32_t n, const PillarGeom &g, int32_t *cell, int32_t *slot,
-                    int32_t *counts, hipStream_t s);
+hipError_t cell_ids(const PillarGroup &grp, const PillarGeom &g, hipStream_t s);
 
 // K2a: per tile of kScanTile cells: (points, non-empty cells); zeroes
 // meta[2] (the overfull count of K2c).
-hipError_t scan_reduce(const int32_t *counts, int32_t n_cells, int32_t *tile_sums, int32_t *meta, hipStream_t s);
+hipError_t scan_reduce(const PillarGroup &grp, int32_t n_cells, hipStream_t s);
 // K2c: offsets[cell] (exclusive prefix of counts), pillar lists in
-// ascending cell order, list of cells holding more than max_pts points;
-// meta = {valid points, pillars, overfull count}.
-hipError_t scan_down(const int32_t *counts, int32_t n_cells, const int32_t *tile_sums,
-                     int32_t max_pts, int32_t *offsets, int32_t *pcells, int32_t *pcounts, int32_t *poffs,
-                     int32_t *overfull, int32_t *meta, hipStream_t s);
-// K2d: member[offsets[cell] + slot] = point index.
-hipError_t scatter(const int32_t *cell, const int32_t *slot, const int32_t *offsets, int32_t n,
-                   const float *pts, int32_t *member, float *sorted, hipStream_t s);
+// ascending cell order, list of the pillars (indices into them) holding
+// more than max_pts points; meta = {valid points, pillars, overfull count}.
+// Leaves counts[] all zero, the state K1 expects next.
+hipError_t scan_down(const PillarGroup &grp, int32_t n_cells, int32_t max_pts, hipStream_t s);
+// K2d: member[offsets[cell] + slot] = point index, sorted[...] = the point.
+hipError_t scatter(const PillarGroup &grp, hipStream_t s);
 // K3: dense canvas [H*W][C]: per pillar cell, channel max over the first
 // min(count, max_pts) members of ReLU(W^T f + b) (for cells over the cap,
 // after moving the max_pts lowest point indices to the front of the
 // segment).  Writes the pillar cells only: every other cell must already be
-// zero (canvas_clear zeroes the previous frame's pillars).  Leaves counts[]
-// all zero, the state K1 expects next.
+// zero (canvas_clear zeroes the previous frame's pillars).
 struct PfnArgs {
-    float4 *sorted;        // points in segment order; each segment's first min(count, max_pts) are used
-    int32_t *counts;       // per cell; the pillars' counts are zeroed for the next frame
-    const int32_t *pcells, *pcounts, *poffs;  // per pillar: cell, count, segment offset
-    const int32_t *meta;   // meta[1] = number of pillars
     const float *w;  // [4][C]
     const float *b;  // [C]
-    void *canvas;
     int32_t C;
     int32_t max_pts;
     float inv_hx, inv_hy, z0, inv_dz;
-    // cells over the cap: their list and number (meta[2]), segment offsets,
-    // member indices, the input points and their count
-    const int32_t *overfull;
-    const int32_t *offsets;
-    int32_t *member;
-    const float4 *pts;
-    int32_t n;
     int32_t pillar_blocks;  // set by pfn_canvas
 };
-// max_pillars bounds meta[1] (at most min(cells, points)).
-hipError_t pfn_canvas(bool bf16, PfnArgs a, int32_t max_pillars, hipStream_t s);
+// max_pillars bounds every agent's meta[1] (at most min(cells, points)).
+hipError_t pfn_canvas(bool bf16, PfnArgs a, const PillarGroup &grp, int32_t max_pillars, hipStream_t s);
 // The canvas cells of the pillars listed in pcells (meta[1] of them) back to
 // zero; max_pillars bounds meta[1].
 hipError_t canvas_clear(bool bf16, void *canvas, const int32_t *pcells, const int32_t *meta, int32_t C,

@@ -1,19 +1,22 @@
 // Pillarization and point-feature canvas for gfx950.
 //
 // Deterministic counting sort by cell (no float atomics, no order-dependent
-// result), five dependent launches:
-//   cell_ids        one thread per point: float32 cell index, atomic count
+// result), five dependent launches, each over a group of agents released
+// together (the blocks of the group's agents are interleaved, see
+// group_block; a single release is a group of one):
+//   cell_ids        two points per thread: float32 cell index, atomic count
 //                   per cell (the counts start at zero); the returned old
 //                   count is the point's rank of arrival in its cell
 //   scan_reduce /   exclusive prefix over all H*W cells -> segment offsets,
 //   scan_down       ascending list of non-empty cells (pillars) and their
-//                   counts, list of cells over the per-pillar point cap (each
-//                   block of the second pass adds up the tile sums before it)
+//                   counts (staged in LDS, stored coalesced), list of the
+//                   pillars over the per-pillar point cap (each block of the
+//                   second pass adds up the tile sums before it); the counts
+//                   go back to zero for the next frame
 //   scatter         member[offset[cell] + rank] = point index
-//   pfn_canvas      one lane per (pillar, 8 channels): linear 4 -> C, ReLU,
-//                   max over the pillar's points into its cell; the pillar's
-//                   count is returned to zero for the next frame.  Extra
-//                   blocks take the few cells over the cap: one wavefront
+//   pfn_canvas      one lane per (two pillars, 8 channels): linear 4 -> C,
+//                   ReLU, max over the pillar's points into its cell.  Extra
+//                   blocks take the few pillars over the cap: one wavefront
 //                   moves the cap lowest point indices (found by bisection on
 //                   the index value) to the front of the segment and writes
 //                   that pillar's features
@@ -79,12 +82,21 @@ __device__ inline void nt_store16(void *p, uint4 v) {
     __builtin_nontemporal_store(u32x4{v.x, v.y, v.z, v.w}, static_cast<u32x4 *>(p));
 }
 
-__global__ __launch_bounds__(256) void k_cell_ids(const float4 *__restrict__ pts, int32_t n, PillarGeom g,
-                                                  int32_t *__restrict__ cell, int32_t *__restrict__ slot,
-                                                  int32_t *__restrict__ counts) {
-    const int i = blockIdx.x * 256 + threadIdx.x;
-    if (i >= n) return;
-    const float4 p = pts[i];
+// Block -> (agent row j of the group, block index b within that agent's
+// grid): the agents' blocks are interleaved.  The dispatcher hands
+// consecutive blocks to the XCDs in turn, so in a group of 8 every agent's
+// blocks run on one XCD, and the random accesses of its pillar stage (cell
+// counts, offsets, member lists) stay in that XCD's L2.
+struct GroupBlock {
+    int j, b, nb;  // agent row, block within the agent, blocks per agent
+};
+__device__ inline GroupBlock group_block(const PillarGroup &grp) {
+    const int m = grp.m;
+    return GroupBlock{int(blockIdx.x) % m, int(blockIdx.x) / m, int(gridDim.x) / m};
+}
+__device__ inline PillarBufs group_bufs(const PillarGroup &grp, int j) { return grp.bufs[grp.agent[j]]; }
+
+__device__ inline int cell_of(const float4 p, const PillarGeom &g) {
     int c = -1;
     if (__builtin_isfinite(p.x) && __builtin_isfinite(p.y) && __builtin_isfinite(p.z) &&
         __builtin_isfinite(p.w) && p.x >= g.x0 && p.x < g.x1 && p.y >= g.y0 && p.y < g.y1 &&
@@ -94,21 +106,48 @@ __global__ __launch_bounds__(256) void k_cell_ids(const float4 *__restrict__ pts
         const float fy = floorf(__fdiv_rn(__fsub_rn(p.y, g.y0), g.v));
         if (fx >= 0.f && fx < float(g.W) && fy >= 0.f && fy < float(g.H)) c = int(fy) * g.W + int(fx);
     }
-    cell[i] = c;
-    if (c >= 0) slot[i] = atomicAdd(&counts[c], 1);
+    return c;
 }
 
-__global__ __launch_bounds__(256) void k_scan_reduce(const int32_t *__restrict__ counts,
-                                                     int32_t n_cells, int32_t *__restrict__ tile_sums,
-                                                     int32_t *__restrict__ meta) {
-    if (blockIdx.x == 0 && threadIdx.x == 0) meta[2] = 0;  // overfull count, appended to by the scan
-    const int base = blockIdx.x * kScanTile + threadIdx.x * 8;
+// Points per thread of the per-point kernels (cell ids, scatter): both
+// loads and both atomics of a thread are in flight together.
+constexpr int kPtsPerThread = 2;
+constexpr int kPtsPerBlock = 256 * kPtsPerThread;
+
+__global__ __launch_bounds__(256) void k_cell_ids(const PillarGroup grp, const PillarGeom g) {
+    const GroupBlock gb = group_block(grp);
+    const int j = gb.j;
+    const int n = grp.n[j];
+    const int i0 = gb.b * kPtsPerBlock + threadIdx.x;
+    if (i0 >= n) return;
+    const PillarBufs B = group_bufs(grp, j);
+    const float4 *pts = grp.pts[j];
+    int c[kPtsPerThread];
+#pragma unroll
+    for (int u = 0; u < kPtsPerThread; ++u) {
+        const int i = i0 + u * 256;
+        c[u] = i < n ? cell_of(pts[i], g) : -2;
+    }
+#pragma unroll
+    for (int u = 0; u < kPtsPerThread; ++u) {
+        const int i = i0 + u * 256;
+        if (c[u] == -2) continue;
+        B.cell[i] = c[u];
+        if (c[u] >= 0) B.slot[i] = atomicAdd(&B.counts[c[u]], 1);
+    }
+}
+
+__global__ __launch_bounds__(256) void k_scan_reduce(const PillarGroup grp, int32_t n_cells) {
+    const GroupBlock gb = group_block(grp);
+    const PillarBufs B = group_bufs(grp, gb.j);
+    if (gb.b == 0 && threadIdx.x == 0) B.meta[2] = 0;  // overfull count, appended to by the scan
+    const int base = gb.b * kScanTile + threadIdx.x * 8;
     int s = 0, f = 0;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
         const int c = base + i;
         if (c < n_cells) {
-            const int v = counts[c];
+            const int v = B.counts[c];
             s += v;
             f += v > 0;
         }
@@ -116,71 +155,89 @@ __global__ __launch_bounds__(256) void k_scan_reduce(const int32_t *__restrict__
     int2 tot;
     block_excl_scan256(make_int2(s, f), &tot);
     if (threadIdx.x == 0) {
-        tile_sums[2 * blockIdx.x] = tot.x;
-        tile_sums[2 * blockIdx.x + 1] = tot.y;
+        B.tiles[2 * gb.b] = tot.x;
+        B.tiles[2 * gb.b + 1] = tot.y;
     }
 }
 
-__global__ __launch_bounds__(256) void k_scan_down(const int32_t *__restrict__ counts, int32_t n_cells,
-                                                   const int32_t *__restrict__ ts, int32_t max_pts,
-                                                   int32_t *__restrict__ offsets,
-                                                   int32_t *__restrict__ pcells,
-                                                   int32_t *__restrict__ pcounts,
-                                                   int32_t *__restrict__ poffs,
-                                                   int32_t *__restrict__ overfull,
-                                                   int32_t *__restrict__ meta) {
-    const int base = blockIdx.x * kScanTile + threadIdx.x * 8;
+__global__ __launch_bounds__(256) void k_scan_down(const PillarGroup grp, int32_t n_cells, int32_t max_pts) {
+    // the tile's pillars (cell, count, offset), staged for coalesced stores
+    __shared__ int3 stage[kScanTile];
+    const GroupBlock gb = group_block(grp);
+    const PillarBufs B = group_bufs(grp, gb.j);
+    const int base = gb.b * kScanTile + threadIdx.x * 8;
     int v[8];
     int s = 0, f = 0;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
         const int c = base + i;
-        v[i] = c < n_cells ? counts[c] : 0;
+        v[i] = c < n_cells ? B.counts[c] : 0;
         s += v[i];
         f += v[i] > 0;
     }
     // the sums of the tiles before this one, added up by the block itself
     // (no separate scan of the tile sums); the last tile writes the totals
     int2 before = make_int2(0, 0);
-    for (int t = threadIdx.x; t < int(blockIdx.x); t += 256) before = add2(before, make_int2(ts[2 * t], ts[2 * t + 1]));
+    for (int t = threadIdx.x; t < gb.b; t += 256)
+        before = add2(before, make_int2(B.tiles[2 * t], B.tiles[2 * t + 1]));
     int2 prefix, tot;
     block_excl_scan256(before, &prefix);
     const int2 ex = block_excl_scan256(make_int2(s, f), &tot);
-    if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) {
-        meta[0] = prefix.x + tot.x;
-        meta[1] = prefix.y + tot.y;
+    if (gb.b == gb.nb - 1 && threadIdx.x == 0) {
+        B.meta[0] = prefix.x + tot.x;
+        B.meta[1] = prefix.y + tot.y;
     }
     int off = prefix.x + ex.x;
-    int p = prefix.y + ex.y;
+    int q = ex.y;  // the thread's first pillar within the tile
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
         const int c = base + i;
         if (c < n_cells) {
-            offsets[c] = off;
+            B.offsets[c] = off;
+            // counts go back to zero: the state the next frame's K1 starts from
+            if (v[i] > 0) B.counts[c] = 0;
             if (v[i] > 0) {
-                pcells[p] = c;
-                pcounts[p] = v[i];
-                poffs[p] = off;
-                ++p;
-                if (v[i] > max_pts) overfull[atomicAdd(&meta[2], 1)] = c;
+                stage[q] = make_int3(c, v[i], off);
+                if (v[i] > max_pts) B.overfull[atomicAdd(&B.meta[2], 1)] = prefix.y + q;
+                ++q;
             }
             off += v[i];
         }
     }
+    __syncthreads();
+    for (int t = threadIdx.x; t < tot.y; t += 256) {
+        const int3 e = stage[t];
+        B.pcells[prefix.y + t] = e.x;
+        B.pcounts[prefix.y + t] = e.y;
+        B.poffs[prefix.y + t] = e.z;
+    }
 }
 
-__global__ __launch_bounds__(256) void k_scatter(const int32_t *__restrict__ cell,
-                                                 const int32_t *__restrict__ slot,
-                                                 const int32_t *__restrict__ offsets, int32_t n,
-                                                 const float4 *__restrict__ pts,
-                                                 int32_t *__restrict__ member, float4 *__restrict__ sorted) {
-    const int i = blockIdx.x * 256 + threadIdx.x;
-    if (i >= n) return;
-    const int c = cell[i];
-    if (c >= 0) {
-        const int d = offsets[c] + slot[i];
-        member[d] = i;
-        sorted[d] = pts[i];
+__global__ __launch_bounds__(256) void k_scatter(const PillarGroup grp) {
+    const GroupBlock gb = group_block(grp);
+    const int j = gb.j;
+    const int n = grp.n[j];
+    const int i0 = gb.b * kPtsPerBlock + threadIdx.x;
+    if (i0 >= n) return;
+    const PillarBufs B = group_bufs(grp, j);
+    const float4 *pts = grp.pts[j];
+    int c[kPtsPerThread], d[kPtsPerThread];
+#pragma unroll
+    for (int u = 0; u < kPtsPerThread; ++u) {
+        const int i = i0 + u * 256;
+        c[u] = i < n ? B.cell[i] : -1;
+        d[u] = c[u] >= 0 ? B.slot[i] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < kPtsPerThread; ++u)
+        if (c[u] >= 0) d[u] += B.offsets[c[u]];
+#pragma unroll
+    for (int u = 0; u < kPtsPerThread; ++u) {
+        const int i = i0 + u * 256;
+        if (c[u] >= 0) {
+            B.member[d[u]] = i;
+            B.sorted[d[u]] = pts[i];
+        }
     }
 }
 
@@ -209,16 +266,16 @@ __device__ inline void pfn_point(const PfnArgs &a, const float4 pt, const float 
 }
 
 template <bool BF16>
-__device__ inline void store_canvas8(const PfnArgs &a, int cell, int ch, const float (&mx)[8]) {
+__device__ inline void store_canvas8(const PfnArgs &a, void *canvas, int cell, int ch, const float (&mx)[8]) {
     if (BF16) {
         uint4 o;
         o.x = pack_bf16x2(mx[0], mx[1]);
         o.y = pack_bf16x2(mx[2], mx[3]);
         o.z = pack_bf16x2(mx[4], mx[5]);
         o.w = pack_bf16x2(mx[6], mx[7]);
-        nt_store16(static_cast<uint16_t *>(a.canvas) + size_t(cell) * a.C + ch, o);
+        nt_store16(static_cast<uint16_t *>(canvas) + size_t(cell) * a.C + ch, o);
     } else {
-        float *dst = static_cast<float *>(a.canvas) + size_t(cell) * a.C + ch;
+        float *dst = static_cast<float *>(canvas) + size_t(cell) * a.C + ch;
         nt_store16(dst, make_uint4(__float_as_uint(mx[0]), __float_as_uint(mx[1]), __float_as_uint(mx[2]),
                                    __float_as_uint(mx[3])));
         nt_store16(dst + 4, make_uint4(__float_as_uint(mx[4]), __float_as_uint(mx[5]), __float_as_uint(mx[6]),
@@ -236,30 +293,35 @@ __device__ inline void store_canvas8(const PfnArgs &a, int cell, int ch, const f
 // cell, count and segment offset together; the other cells of the canvas
 // already hold zeros.  Counts go back to zero for the next frame.
 template <bool BF16>
-__global__ __launch_bounds__(256) void k_pfn_canvas(PfnArgs a) {
+__global__ __launch_bounds__(256) void k_pfn_canvas(const PfnArgs a, const PillarGroup grp) {
     // PFN weights and bias, read once per block into LDS (C <= 512)
     __shared__ float sw[5 * 512];
     for (int q = threadIdx.x; q < 5 * a.C; q += 256) sw[q] = q < 4 * a.C ? a.w[q] : a.b[q - 4 * a.C];
     __syncthreads();
-    if (int(blockIdx.x) >= a.pillar_blocks) {
-        // cells over the cap, one wavefront each
+    const GroupBlock gb = group_block(grp);
+    const int j = gb.j;
+    const PillarBufs B = group_bufs(grp, j);
+    if (gb.b >= a.pillar_blocks) {
+        // pillars over the cap, one wavefront each
         const int lane = threadIdx.x & 63;
-        const int wave = ((int(blockIdx.x) - a.pillar_blocks) * 256 + int(threadIdx.x)) >> 6;
-        const int n_waves = ((int(gridDim.x) - a.pillar_blocks) * 256) >> 6;
-        const int n_over = a.meta[2];
+        const int wave = ((gb.b - a.pillar_blocks) * 256 + int(threadIdx.x)) >> 6;
+        const int n_waves = ((gb.nb - a.pillar_blocks) * 256) >> 6;
+        const int n_over = B.meta[2];
+        const float4 *pts = grp.pts[j];
         for (int w = wave; w < n_over; w += n_waves) {
-            const int c = a.overfull[w];
-            const int cnt = a.counts[c];
-            int32_t *seg = a.member + a.offsets[c];
-            float4 *sseg = a.sorted + a.offsets[c];
+            const int pil = B.overfull[w];
+            const int c = B.pcells[pil];
+            const int cnt = B.pcounts[pil];
+            int32_t *seg = B.member + B.poffs[pil];
+            float4 *sseg = B.sorted + B.poffs[pil];
             // Smallest T with #{members < T} >= max_pts.  Members are
             // distinct point indices in [0, n), so exactly max_pts members
             // lie below T.
-            int lo = 1, hi = a.n;
+            int lo = 1, hi = grp.n[j];
             while (lo < hi) {
                 const int mid = lo + (hi - lo) / 2;
                 int below = 0;
-                for (int j = lane; j < cnt; j += 64) below += seg[j] < mid;
+                for (int q = lane; q < cnt; q += 64) below += seg[q] < mid;
 #pragma unroll
                 for (int d = 32; d >= 1; d >>= 1) below += __shfl_xor(below, d, 64);
                 if (below >= a.max_pts) hi = mid;
@@ -271,14 +333,14 @@ __global__ __launch_bounds__(256) void k_pfn_canvas(PfnArgs a) {
             // overwritten, and writes never pass the chunk being read.
             int pos = 0;
             for (int base = 0; base < cnt && pos < a.max_pts; base += 64) {
-                const int j = base + lane;
-                const int e = j < cnt ? seg[j] : INT_MAX;
-                const bool sel = j < cnt && e < T;
+                const int q = base + lane;
+                const int e = q < cnt ? seg[q] : INT_MAX;
+                const bool sel = q < cnt && e < T;
                 const unsigned long long m = __ballot(sel);
                 const int my = pos + __popcll(m & ((1ull << lane) - 1ull));
                 if (sel) {
                     seg[my] = e;
-                    sseg[my] = a.pts[e];
+                    sseg[my] = pts[e];
                 }
                 pos += __popcll(m);
             }
@@ -298,24 +360,29 @@ __global__ __launch_bounds__(256) void k_pfn_canvas(PfnArgs a) {
                     mx[i] = 0.f;
                 }
                 for (int t = 0; t < a.max_pts; ++t) pfn_point(a, sseg[t], w0, w1, w2, w3, bb, mx);
-                store_canvas8<BF16>(a, c, ch, mx);
+                store_canvas8<BF16>(a, B.canvas, c, ch, mx);
             }
-            if (lane == 0) a.counts[c] = 0;
         }
         return;
     }
+    // two pillars per lane (8 channels of each): their loads are in flight
+    // together
     const int lanes_per_cell = a.C >> 3;
-    const int gid = int(blockIdx.x) * 256 + int(threadIdx.x);
-    const int p = gid / lanes_per_cell;
-    const int ch = (gid - p * lanes_per_cell) * 8;
-    if (p >= a.meta[1]) return;
-    const int cell = a.pcells[p];
-    const int cnt = a.pcounts[p];
-    const int off = a.poffs[p];
-    if (cnt > a.max_pts) return;  // over the cap: the blocks above
-    // the cell's count back to zero, the state the next frame's K1 starts from
-    if (ch == 0) a.counts[cell] = 0;
-    float w0[8], w1[8], w2[8], w3[8], bb[8], mx[8];
+    const int gid = gb.b * 256 + int(threadIdx.x);
+    const int pp = gid / lanes_per_cell;
+    const int ch = (gid - pp * lanes_per_cell) * 8;
+    const int P = B.meta[1];
+    const int p0 = 2 * pp;
+    if (p0 >= P) return;
+    const bool has1 = p0 + 1 < P;
+    const int cell0 = B.pcells[p0], cnt0 = B.pcounts[p0], off0 = B.poffs[p0];
+    const int cell1 = has1 ? B.pcells[p0 + 1] : 0;
+    const int cnt1 = has1 ? B.pcounts[p0 + 1] : 0;
+    const int off1 = has1 ? B.poffs[p0 + 1] : off0;
+    // pillars over the cap are left to the blocks above
+    const int n0 = cnt0 <= a.max_pts ? cnt0 : 0;
+    const int n1 = cnt1 <= a.max_pts ? cnt1 : 0;
+    float w0[8], w1[8], w2[8], w3[8], bb[8], m0[8], m1[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
         w0[i] = sw[0 * a.C + ch + i];
@@ -323,17 +390,21 @@ __global__ __launch_bounds__(256) void k_pfn_canvas(PfnArgs a) {
         w2[i] = sw[2 * a.C + ch + i];
         w3[i] = sw[3 * a.C + ch + i];
         bb[i] = sw[4 * a.C + ch + i];
-        mx[i] = 0.f;
+        m0[i] = 0.f;
+        m1[i] = 0.f;
     }
-    // two points per step, both loads in flight (max is order-free)
-    for (int t = 0; t < cnt; t += 2) {
-        const float4 p0 = a.sorted[off + t];
-        const bool two = t + 1 < cnt;
-        const float4 p1 = a.sorted[off + (two ? t + 1 : t)];
-        pfn_point(a, p0, w0, w1, w2, w3, bb, mx);
-        if (two) pfn_point(a, p1, w0, w1, w2, w3, bb, mx);
+    // the last point of a pillar stands in for the points past its end (the
+    // max is unchanged by a repeat); every index stays inside its segment
+    const int l0 = n0 > 0 ? n0 - 1 : 0, l1 = n1 > 0 ? n1 - 1 : 0;
+    const int tmax = n0 > n1 ? n0 : n1;
+    for (int t = 0; t < tmax; ++t) {
+        const float4 q0 = B.sorted[off0 + (t < l0 ? t : l0)];
+        const float4 q1 = B.sorted[off1 + (t < l1 ? t : l1)];
+        if (n0 > 0) pfn_point(a, q0, w0, w1, w2, w3, bb, m0);
+        if (n1 > 0) pfn_point(a, q1, w0, w1, w2, w3, bb, m1);
     }
-    store_canvas8<BF16>(a, cell, ch, mx);
+    if (n0 > 0) store_canvas8<BF16>(a, B.canvas, cell0, ch, m0);
+    if (n1 > 0) store_canvas8<BF16>(a, B.canvas, cell1, ch, m1);
 }
 
 // The canvas cells of the last frame's pillars back to zero, one lane per
@@ -366,42 +437,37 @@ hipError_t fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t cell_ids(const float *pts, int32_t n, const PillarGeom &g, int32_t *cell, int32_t *slot,
-                    int32_t *counts, hipStream_t s) {
-    if (n <= 0) return hipSuccess;
-    k_cell_ids<<<blocks_for(n, 256), 256, 0, s>>>(reinterpret_cast<const float4 *>(pts), n, g, cell, slot, counts);
+hipError_t cell_ids(const PillarGroup &grp, const PillarGeom &g, hipStream_t s) {
+    if (grp.n_max <= 0) return hipSuccess;
+    k_cell_ids<<<blocks_for(grp.n_max, kPtsPerBlock) * unsigned(grp.m), 256, 0, s>>>(grp, g);
     return hipGetLastError();
 }
 
-hipError_t scan_reduce(const int32_t *counts, int32_t n_cells, int32_t *tile_sums, int32_t *meta, hipStream_t s) {
-    k_scan_reduce<<<blocks_for(n_cells, kScanTile), 256, 0, s>>>(counts, n_cells, tile_sums, meta);
+hipError_t scan_reduce(const PillarGroup &grp, int32_t n_cells, hipStream_t s) {
+    k_scan_reduce<<<blocks_for(n_cells, kScanTile) * unsigned(grp.m), 256, 0, s>>>(grp, n_cells);
     return hipGetLastError();
 }
 
-hipError_t scan_down(const int32_t *counts, int32_t n_cells, const int32_t *tile_sums,
-                     int32_t max_pts, int32_t *offsets, int32_t *pcells, int32_t *pcounts, int32_t *poffs,
-                     int32_t *overfull, int32_t *meta, hipStream_t s) {
-    k_scan_down<<<blocks_for(n_cells, kScanTile), 256, 0, s>>>(counts, n_cells, tile_sums, max_pts,
-                                                                offsets, pcells, pcounts, poffs, overfull, meta);
+hipError_t scan_down(const PillarGroup &grp, int32_t n_cells, int32_t max_pts, hipStream_t s) {
+    k_scan_down<<<blocks_for(n_cells, kScanTile) * unsigned(grp.m), 256, 0, s>>>(grp, n_cells, max_pts);
     return hipGetLastError();
 }
 
-hipError_t scatter(const int32_t *cell, const int32_t *slot, const int32_t *offsets, int32_t n,
-                   const float *pts, int32_t *member, float *sorted, hipStream_t s) {
-    if (n <= 0) return hipSuccess;
-    k_scatter<<<blocks_for(n, 256), 256, 0, s>>>(cell, slot, offsets, n, reinterpret_cast<const float4 *>(pts),
-                                                 member, reinterpret_cast<float4 *>(sorted));
+hipError_t scatter(const PillarGroup &grp, hipStream_t s) {
+    if (grp.n_max <= 0) return hipSuccess;
+    k_scatter<<<blocks_for(grp.n_max, kPtsPerBlock) * unsigned(grp.m), 256, 0, s>>>(grp);
     return hipGetLastError();
 }
 
-hipError_t pfn_canvas(bool bf16, PfnArgs a, int32_t max_pillars, hipStream_t s) {
+hipError_t pfn_canvas(bool bf16, PfnArgs a, const PillarGroup &grp, int32_t max_pillars, hipStream_t s) {
     // pillar blocks, then 64 blocks for the cells over the cap when any
-    // cell can exceed it
-    a.pillar_blocks = int32_t(blocks_for(int64_t(max_pillars) * (a.C / 8), 256));
-    const unsigned blocks = unsigned(a.pillar_blocks) + (a.n > a.max_pts ? 64u : 0u);
+    // agent's cell can exceed it
+    a.pillar_blocks = int32_t(blocks_for(int64_t((max_pillars + 1) / 2) * (a.C / 8), 256));
+    const unsigned blocks = unsigned(a.pillar_blocks) + (grp.n_max > a.max_pts ? 64u : 0u);
     if (blocks == 0) return hipSuccess;
-    if (bf16) k_pfn_canvas<true><<<blocks, 256, 0, s>>>(a);
-    else k_pfn_canvas<false><<<blocks, 256, 0, s>>>(a);
+    const unsigned grid = blocks * unsigned(grp.m);
+    if (bf16) k_pfn_canvas<true><<<grid, 256, 0, s>>>(a, grp);
+    else k_pfn_canvas<false><<<grid, 256, 0, s>>>(a, grp);
     return hipGetLastError();
 }
 

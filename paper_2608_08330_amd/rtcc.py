@@ -132,6 +132,17 @@ class rtcc_uplink_desc(ctypes.Structure):
     ]
 
 
+class rtcc_event(ctypes.Structure):
+    _fields_ = [
+        ("agent", ctypes.c_int32),
+        ("device", ctypes.c_int32),
+        ("points", ctypes.c_void_p),
+        ("n", ctypes.c_int64),
+        ("pose", ctypes.c_float * 3),
+        ("arrival_t", ctypes.c_double),
+    ]
+
+
 class rtcc_checkpoint_info(ctypes.Structure):
     _fields_ = [
         ("config_id", ctypes.c_char * 32),
@@ -160,7 +171,7 @@ class rtcc_detections(ctypes.Structure):
 
 EXPORTS = (
     "rtcc_create", "rtcc_read_checkpoint", "rtcc_create_from_checkpoint", "rtcc_destroy", "rtcc_set_mode", "rtcc_staging_buffer", "rtcc_begin_frame",
-    "rtcc_release_branch", "rtcc_release_branch_device", "rtcc_join_and_detect",
+    "rtcc_release_branch", "rtcc_release_branch_device", "rtcc_release_branches", "rtcc_join_and_detect",
     "rtcc_get_branch_state", "rtcc_tensor_bytes", "rtcc_get_tensor", "rtcc_profile_nodes",
     "rtcc_node_times", "rtcc_node_count", "rtcc_graph_stats", "rtcc_conv_plan", "rtcc_rotated_nms", "rtcc_rotated_nms_noalloc", "rtcc_uplink_emulate", "rtcc_schedule_model",
     "rtcc_upward_rank", "rtcc_status_str", "rtcc_last_error",
@@ -192,6 +203,7 @@ def _declare(lib):
         "rtcc_begin_frame": (S, [_P, ctypes.c_double]),
         "rtcc_release_branch": (S, [_P, ctypes.c_int32, _P, ctypes.c_int64, _F, ctypes.c_double]),
         "rtcc_release_branch_device": (S, [_P, ctypes.c_int32, _P, ctypes.c_int64, _F, ctypes.c_double]),
+        "rtcc_release_branches": (S, [_P, ctypes.c_int32, ctypes.POINTER(rtcc_event), ctypes.POINTER(ctypes.c_int)]),
         "rtcc_join_and_detect": (S, [_P, ctypes.POINTER(rtcc_detections)]),
         "rtcc_get_branch_state": (S, [_P, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32)]),
         "rtcc_tensor_bytes": (S, [_P, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_size_t)]),
@@ -424,6 +436,35 @@ def rtcc_release_branch_device(ctx, agent, device_ptr, n, pose, arrival_t):
     pp, keep = _pose(pose)
     return ctx.check(ctx.lib.rtcc_release_branch_device(ctx.handle, agent, _P(device_ptr), int(n), pp,
                                                         float(arrival_t)))
+
+
+def rtcc_release_branches(ctx, events, statuses=None):
+    """Events that arrived together.  ``events``: list of dicts with agent,
+    points (a float32 [n, 4] host array, or with device=1 a device pointer
+    int), n (device events), pose, arrival_t.  Raises on a non-OK status; with
+    ``statuses`` (a list) each event's status is appended to it."""
+    m = len(events)
+    arr = (rtcc_event * max(m, 1))()
+    keep = []
+    for i, e in enumerate(events):
+        ev = arr[i]
+        ev.agent = int(e["agent"])
+        ev.device = int(e.get("device", 0))
+        if ev.device == 1:
+            ev.points = int(e["points"])
+            ev.n = int(e["n"])
+        else:
+            p = np.ascontiguousarray(e["points"], dtype=np.float32).reshape(-1, 4)
+            keep.append(p)
+            ev.points = p.ctypes.data if len(p) else None
+            ev.n = int(e.get("n", len(p)))
+        ev.pose[:] = [float(v) for v in e["pose"]]
+        ev.arrival_t = float(e["arrival_t"])
+    st = (ctypes.c_int * max(m, 1))()
+    r = ctx.lib.rtcc_release_branches(ctx.handle, m, arr, st)
+    if statuses is not None:
+        statuses.extend(int(st[i]) for i in range(m))
+    return ctx.check(r)
 
 
 def rtcc_join_and_detect(ctx):

@@ -127,9 +127,9 @@ def test_branch_state_follows_the_device(host_ctx):
 @pytest.mark.parametrize("mode", ["release", "barrier"])
 def test_failed_dispatch_withholds_the_join(host_ctx, mode):
     """An encoder whose enqueue fails never reaches its slot: the join
-    returns an error without running the post-join subgraph, the other
-    branches of a barrier release are not dispatched, and the next frame
-    runs normally."""
+    returns an error without running the post-join subgraph, a barrier
+    release (one group of all K) leaves every branch undispatched, and the
+    next frame runs normally."""
     cfg, fr, ctx = host_ctx
     lib = R.load("host")
     R.rtcc_set_mode(ctx, R.RTCC_MODE_BARRIER if mode == "barrier" else R.RTCC_MODE_RELEASE)
@@ -142,7 +142,9 @@ def test_failed_dispatch_withholds_the_join(host_ctx, mode):
         assert st == [R.RTCC_OK, R.RTCC_OK, R.RTCC_OK, R.RTCC_E_HIP]
     assert R.rtcc_get_branch_state(ctx, 1) == R.RTCC_WAITING
     disp = [l.split()[1] for l in _host_log() if l.startswith("dispatch")]
-    assert disp == (["0", "2", "3"] if mode == "release" else ["0"])
+    assert disp == (["0", "2", "3"] if mode == "release" else [])
+    if mode == "barrier":
+        assert all(R.rtcc_get_branch_state(ctx, k) == R.RTCC_WAITING for k in range(cfg["K"]))
     # a repeated event for the failed branch is still a duplicate
     assert _status(R.rtcc_release_branch, ctx, 1, fr["points"][1], fr["poses"][1], 0.0) == R.RTCC_E_DUPLICATE
     assert _status(R.rtcc_join_and_detect, ctx) == R.RTCC_E_STATE
@@ -343,3 +345,106 @@ def test_bad_runtime_opts_rejected(field, value):
     ctx = R.rtcc_create(R.model_desc(cfg), w, o, kind="host")
     assert R.rtcc_graph_stats(ctx) == (0, 0, 0)   # the recording executor runs no graphs
     ctx.close()
+
+
+# --------------------------------------------------------- batched events
+
+def _events(cfg, fr, agents, arrival=0.0):
+    return [dict(agent=k, points=fr["points"][k], pose=fr["poses"][k], arrival_t=arrival) for k in agents]
+
+
+def test_batch_release_is_one_group_in_index_order(host_ctx):
+    cfg, fr, ctx = host_ctx
+    R.rtcc_set_mode(ctx, R.RTCC_MODE_RELEASE)
+    R.rtcc_begin_frame(ctx, time.monotonic() - 1)
+    _host_log()
+    st = []
+    R.rtcc_release_branches(ctx, _events(cfg, fr, [2, 0, 3, 1]), st)
+    assert st == [R.RTCC_OK] * 4
+    log = _host_log()
+    assert log[0] == "group 0 1 2 3"
+    assert [l.split()[1] for l in log[1:] if l.startswith("dispatch")] == ["0", "1", "2", "3"]
+    assert all(R.rtcc_get_branch_state(ctx, k) == R.RTCC_RELEASED for k in range(cfg["K"]))
+    det = R.rtcc_join_and_detect(ctx)
+    # released together: one dispatch time for the whole group
+    assert len(set(det["dispatch_s"])) == 1
+
+
+def test_batch_release_events_are_checked_one_by_one(host_ctx):
+    cfg, fr, ctx = host_ctx
+    R.rtcc_set_mode(ctx, R.RTCC_MODE_RELEASE)
+    R.rtcc_begin_frame(ctx, time.monotonic() - 1)
+    R.rtcc_release_branch(ctx, 3, fr["points"][3], fr["poses"][3], 0.0)
+    _host_log()
+    ev = _events(cfg, fr, [0, 1, 0, 3, 2])
+    ev[1]["pose"] = (math.nan, 0.0, 0.0)       # malformed
+    ev[4]["arrival_t"] = 100.0                 # premature
+    st = []
+    with pytest.raises(R.RtccError) as e:
+        R.rtcc_release_branches(ctx, ev, st)
+    # the first rejected event names the call's status
+    assert e.value.status == R.RTCC_E_MALFORMED and "event 1" in str(e.value)
+    assert st == [R.RTCC_OK, R.RTCC_E_MALFORMED, R.RTCC_E_DUPLICATE, R.RTCC_E_DUPLICATE, R.RTCC_E_PREMATURE]
+    # the one accepted event was released (a group of one: no group line)
+    log = _host_log()
+    assert [l.split()[1] for l in log if l.startswith("dispatch")] == ["0"]
+    assert not any(l.startswith("group") for l in log)
+    assert [R.rtcc_get_branch_state(ctx, k) for k in range(4)] == [
+        R.RTCC_RELEASED, R.RTCC_WAITING, R.RTCC_WAITING, R.RTCC_RELEASED]
+    # the rejected branches can still be released
+    R.rtcc_release_branches(ctx, _events(cfg, fr, [1, 2]))
+    R.rtcc_join_and_detect(ctx)
+
+
+def test_batch_release_under_barrier(host_ctx):
+    cfg, fr, ctx = host_ctx
+    R.rtcc_set_mode(ctx, R.RTCC_MODE_BARRIER)
+    R.rtcc_begin_frame(ctx, time.monotonic() - 1)
+    _host_log()
+    R.rtcc_release_branches(ctx, _events(cfg, fr, [3, 1]))
+    assert not any(l.startswith("dispatch") for l in _host_log())
+    assert all(R.rtcc_get_branch_state(ctx, k) == R.RTCC_WAITING for k in range(4))
+    R.rtcc_release_branch(ctx, 0, fr["points"][0], fr["poses"][0], 0.0)
+    assert not _host_log()
+    R.rtcc_release_branches(ctx, _events(cfg, fr, [2]))
+    log = _host_log()
+    assert log[0] == "group 0 1 2 3"
+    assert [l.split()[1] for l in log if l.startswith("dispatch")] == ["0", "1", "2", "3"]
+    R.rtcc_join_and_detect(ctx)
+
+
+def test_batch_release_argument_errors(host_ctx):
+    cfg, fr, ctx = host_ctx
+    lib = R.load("host")
+    R.rtcc_set_mode(ctx, R.RTCC_MODE_RELEASE)
+    R.rtcc_begin_frame(ctx, time.monotonic() - 1)
+    _host_log()
+    st = (ctypes.c_int * 1)()
+    assert lib.rtcc_release_branches(ctx.handle, 1, None, st) == R.RTCC_E_ARG
+    assert lib.rtcc_release_branches(ctx.handle, -1, None, None) == R.RTCC_E_ARG
+    assert lib.rtcc_release_branches(ctx.handle, R.RTCC_MAX_AGENTS + 1, None, None) == R.RTCC_E_ARG
+    assert lib.rtcc_release_branches(None, 0, None, None) == R.RTCC_E_ARG
+    assert lib.rtcc_release_branches(ctx.handle, 0, None, None) == R.RTCC_OK
+    ev = _events(cfg, fr, [0])
+    ev[0]["device"] = 2
+    st = []
+    assert _status(R.rtcc_release_branches, ctx, ev, st) == R.RTCC_E_MALFORMED
+    assert st == [R.RTCC_E_MALFORMED]
+    assert not any(l.startswith("dispatch") for l in _host_log())
+    assert R.rtcc_get_branch_state(ctx, 0) == R.RTCC_WAITING
+
+
+def test_batch_release_dispatch_failure_leaves_the_group_waiting(host_ctx):
+    cfg, fr, ctx = host_ctx
+    lib = R.load("host")
+    R.rtcc_set_mode(ctx, R.RTCC_MODE_RELEASE)
+    R.rtcc_begin_frame(ctx, time.monotonic() - 1)
+    lib.rtcc_hosttest_fail_dispatch(2)
+    st = []
+    assert _status(R.rtcc_release_branches, ctx, _events(cfg, fr, [0, 1, 2, 3]), st) == R.RTCC_E_HIP
+    assert st == [R.RTCC_OK] * 4  # every event valid; the enqueue failed
+    assert all(R.rtcc_get_branch_state(ctx, k) == R.RTCC_WAITING for k in range(4))
+    assert _status(R.rtcc_join_and_detect, ctx) == R.RTCC_E_STATE
+    R.rtcc_begin_frame(ctx, time.monotonic() - 1)
+    R.rtcc_release_branches(ctx, _events(cfg, fr, [0, 1, 2, 3]))
+    R.rtcc_join_and_detect(ctx)

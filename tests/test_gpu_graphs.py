@@ -85,10 +85,14 @@ def test_graph_replays_equal_eager(name, exec_kind, extra):
             assert want["decoded"] > 0 or name.startswith("t_"), i
         inst, upd, launches = R.rtcc_graph_stats(graph)
         assert R.rtcc_graph_stats(eager) == (0, 0, 0)
-    assert launches == len(seq) * (K + 2)
-    # first frame: K branch graphs and the join's two; changed point counts or
-    # poses update them in place rather than instantiating new ones
-    assert K + 2 <= inst <= K + 2 + upd
+    # a branch released alone is one graph; a barrier frame releases the K
+    # branches as one group: its pillar-stage graph and K backbone graphs
+    n_bar = sum(1 for _p, _q, m in seq if m == R.RTCC_MODE_BARRIER)
+    assert launches == (len(seq) - n_bar) * (K + 2) + n_bar * (K + 3)
+    # first frames: K branch graphs, the join's two, the group's and K
+    # backbones; changed point counts or poses update them in place rather
+    # than instantiating new ones
+    assert 2 * K + 3 <= inst <= 2 * K + 3 + upd
     assert upd >= K
     _say("  instantiated %d, updates %d, launches %d" % (inst, upd, launches))
 
