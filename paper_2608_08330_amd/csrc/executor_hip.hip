@@ -60,6 +60,7 @@ class HipExecutor : public Executor {
         const size_t n_cells = size_t(p.H) * p.W;
         const size_t n_tiles = (n_cells + kern::kScanTile - 1) / kern::kScanTile;
         const size_t over_cap = n_max / size_t(p.d.max_points_per_pillar + 1) + 1;
+        tiles_ = int(n_tiles);
         // Kernel variant and split-K of every conv layer.
         int n_cu = 0;
         HIP_TRY(hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev_));
@@ -88,10 +89,16 @@ class HipExecutor : public Executor {
             HIP_TRY(alloc(&b.d_pcounts, n_max * 4));
             HIP_TRY(alloc(&b.d_poffs, n_max * 4));
             HIP_TRY(alloc(&b.d_overfull, over_cap * 4));
-            HIP_TRY(alloc(&b.d_counts, n_cells * 4));
-            HIP_TRY(hipMemset(b.d_counts, 0, n_cells * 4));  // afterwards the cell scan leaves them zero
-            HIP_TRY(alloc(&b.d_offsets, n_cells * 4));
-            HIP_TRY(alloc(&b.d_tiles, n_tiles * 8));
+            HIP_TRY(alloc(&b.d_ttotal, n_tiles * 4));
+            HIP_TRY(hipMemset(b.d_ttotal, 0, n_tiles * 4));  // the pillar kernels leave it zero
+            HIP_TRY(alloc(&b.d_tstart, (n_tiles + 1) * 4));
+            HIP_TRY(alloc(&b.d_npil, n_tiles * 4));
+            HIP_TRY(alloc(&b.d_binned, n_max * 4));
+            HIP_TRY(alloc(&b.d_cellb, n_max * 4));
+            HIP_TRY(alloc(&b.d_rank, n_max * 4));
+            HIP_TRY(alloc(&b.d_tcell, n_cells * 4));
+            HIP_TRY(alloc(&b.d_tcount, n_cells * 4));
+            HIP_TRY(alloc(&b.d_toff, n_cells * 4));
             HIP_TRY(alloc(&b.d_meta, 64));
             HIP_TRY(hipMemset(b.d_meta, 0, 64));  // no pillars of a previous frame
             HIP_TRY(alloc(&b.d_canvas, n_cells * p.c_pfn * p.elt));
@@ -124,10 +131,16 @@ class HipExecutor : public Executor {
             const Branch &b = br_[k];
             pb[k].cell = static_cast<int32_t *>(b.d_cell);
             pb[k].slot = static_cast<int32_t *>(b.d_slot);
-            pb[k].counts = static_cast<int32_t *>(b.d_counts);
-            pb[k].tiles = static_cast<int32_t *>(b.d_tiles);
+            pb[k].ttotal = static_cast<int32_t *>(b.d_ttotal);
+            pb[k].tstart = static_cast<int32_t *>(b.d_tstart);
+            pb[k].binned = static_cast<int32_t *>(b.d_binned);
+            pb[k].cellb = static_cast<int32_t *>(b.d_cellb);
+            pb[k].rank = static_cast<int32_t *>(b.d_rank);
+            pb[k].tcell = static_cast<int32_t *>(b.d_tcell);
+            pb[k].tcount = static_cast<int32_t *>(b.d_tcount);
+            pb[k].toff = static_cast<int32_t *>(b.d_toff);
+            pb[k].npil = static_cast<int32_t *>(b.d_npil);
             pb[k].meta = static_cast<int32_t *>(b.d_meta);
-            pb[k].offsets = static_cast<int32_t *>(b.d_offsets);
             pb[k].pcells = static_cast<int32_t *>(b.d_pcells);
             pb[k].pcounts = static_cast<int32_t *>(b.d_pcounts);
             pb[k].poffs = static_cast<int32_t *>(b.d_poffs);
@@ -603,7 +616,9 @@ class HipExecutor : public Executor {
         void *d_pts = nullptr, *d_cell = nullptr, *d_slot = nullptr, *d_member = nullptr;
         void *d_sorted = nullptr;  // points in segment (pillar) order
         void *d_pcells = nullptr, *d_pcounts = nullptr, *d_poffs = nullptr, *d_overfull = nullptr;
-        void *d_counts = nullptr, *d_offsets = nullptr, *d_tiles = nullptr, *d_meta = nullptr;
+        void *d_ttotal = nullptr, *d_tstart = nullptr, *d_npil = nullptr, *d_meta = nullptr;
+        void *d_binned = nullptr, *d_cellb = nullptr, *d_rank = nullptr;
+        void *d_tcell = nullptr, *d_tcount = nullptr, *d_toff = nullptr;  // the tiles' pillar lists
         void *d_canvas = nullptr, *d_slotbuf = nullptr, *d_ws = nullptr;
         void *d_warped = nullptr;        // ego-frame map (warp in the branch)
         const void *ego_map = nullptr;   // what the fusion reads when the warp is in the branch
@@ -666,6 +681,8 @@ class HipExecutor : public Executor {
         grp.bufs = static_cast<const kern::PillarBufs *>(d_pbufs_);
         grp.m = m;
         grp.n_max = 0;
+        grp.n_cells = n_cells;
+        grp.tiles = tiles_;
         for (int j = 0; j < m; ++j) {
             const Branch &b = br_[agents[j]];
             grp.agent[j] = agents[j];
@@ -681,14 +698,13 @@ class HipExecutor : public Executor {
         HIP_TRY(mark(1));
         kern::PillarGeom g{p.d.x_min, p.d.x_max, p.d.y_min, p.d.y_max, p.d.z_min, p.d.z_max,
                            p.d.pillar_size, p.H, p.W};
-        // Between frames the cell counts are zero (the second scan pass
-        // returns them to zero) and the canvas is zero outside the last
-        // frame's pillars (prepare_branch).
+        // Between frames the canvas is zero outside the last frame's pillars
+        // (prepare_branch).
         for (int j = 0; j < m; ++j) br_[agents[j]].pillars_clean = false;
-        HIP_TRY(kern::cell_ids(grp, g, s));
-        HIP_TRY(kern::scan_reduce(grp, n_cells, s));
-        HIP_TRY(kern::scan_down(grp, n_cells, p.d.max_points_per_pillar, s));
-        HIP_TRY(kern::scatter(grp, s));
+        HIP_TRY(kern::bin_count(grp, g, s));
+        HIP_TRY(kern::bin_scatter(grp, s));
+        HIP_TRY(kern::tile_sort(grp, p.d.max_points_per_pillar, s));
+        HIP_TRY(kern::pillar_lists(grp, s));
         HIP_TRY(mark(2));
 
         kern::PfnArgs pa{};
@@ -772,14 +788,14 @@ class HipExecutor : public Executor {
     // Before an encoder: the canvas must be zero outside the pillars the
     // encoder writes.  begin_frame clears the last frame's (clear_canvas);
     // should they still be there, they are cleared here.  If an earlier
-    // enqueue stopped between K1 and the PFN kernel, counts and the whole
-    // canvas are reset.  Runs outside any graph: what it enqueues depends on
-    // the branch's state, not on the frame's arguments.
+    // enqueue stopped before the PFN kernel, the tiles' point totals and the
+    // whole canvas are reset.  Runs outside any graph: what it enqueues
+    // depends on the branch's state, not on the frame's arguments.
     hipError_t prepare_branch(Branch &b, hipStream_t s) {
         const int n_cells = p_.H * p_.W;
         hipError_t e = hipSuccess;
         if (!b.pillars_clean) {
-            e = kern::fill_i32(static_cast<int32_t *>(b.d_counts), n_cells, 0, s);
+            e = kern::fill_i32(static_cast<int32_t *>(b.d_ttotal), tiles_, 0, s);
             if (e == hipSuccess)
                 e = kern::fill_i32(static_cast<int32_t *>(b.d_canvas), int64_t(n_cells) * p_.c_pfn * p_.elt / 4, 0, s);
             if (e != hipSuccess) return e;
@@ -1142,6 +1158,7 @@ class HipExecutor : public Executor {
     Graph post_graph_[2];                // post-join: up to T^head, then decode and NMS
     Graph group_graph_;                  // pillar stage of a group of branches
     void *d_pbufs_ = nullptr;            // kern::PillarBufs of every agent
+    int tiles_ = 0;                      // tiles of cells of the pillar sort
     hipEvent_t ev_group_ = nullptr;      // a group's pillar stage is done
     int64_t graph_stats_[3] = {0, 0, 0}; // instantiations, update attempts, launches
 };

@@ -21,46 +21,58 @@ constexpr int kScanTile = 2048;  // cells per block of the cell scans
 hipError_t fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s);
 
 // One agent's pillar-stage buffers (device pointers, fixed for a context).
-// Sizes: cell, slot, member [n_max]; sorted [n_max] points; counts,
-// offsets [H*W]; tiles [2 * tiles of kScanTile cells]; pcells, pcounts,
-// poffs [min(n_max, H*W)]; overfull [n_max / (max_pts + 1) + 1]; meta [3];
-// canvas [H*W][C].
+// With tiles = ceil(H*W / kScanTile) tiles of cells, the sizes are: cell,
+// slot, binned, cellb, rank, member [n_max]; sorted [n_max] points; ttotal
+// [tiles] (zero between frames); tstart [tiles + 1]; npil [tiles]; tcell, tcount, toff
+// [H*W]; pcells, pcounts, poffs [min(n_max, H*W)]; overfull
+// [n_max / (max_pts + 1) + 1]; meta [3]; canvas [H*W][C].
 struct PillarBufs {
-    int32_t *cell, *slot, *counts, *tiles, *meta, *offsets;
-    int32_t *pcells, *pcounts, *poffs, *overfull, *member;
+    int32_t *cell, *slot, *ttotal, *tstart, *binned, *cellb, *rank;
+    int32_t *tcell, *tcount, *toff, *npil;
+    int32_t *pcells, *pcounts, *poffs, *overfull, *member, *meta;
     float4 *sorted;
     void *canvas;
 };
 
-// The agents whose pillar stage one launch chain runs: blockIdx.y = j
-// takes agent agent[j] (its buffers bufs[agent[j]], its n[j] points at
-// pts[j]).  One agent is a group of one.
+constexpr int kPtsPerBlock = 512;  // points per block of the per-point kernels
+
+// The agents whose pillar stage one launch chain runs: agent row j is agent
+// agent[j] (its buffers bufs[agent[j]], its n[j] points at pts[j]).  One
+// agent is a group of one.
 constexpr int kMaxGroup = 16;
 struct PillarGroup {
     const PillarBufs *bufs;  // device array, indexed by agent
     const float4 *pts[kMaxGroup];
     int32_t n[kMaxGroup];
     int32_t agent[kMaxGroup];
-    int32_t m;      // agents in the group, 1..kMaxGroup
-    int32_t n_max;  // max over the group of n[j]
+    int32_t m;       // agents in the group, 1..kMaxGroup
+    int32_t n_max;   // max over the group of n[j]
+    int32_t n_cells; // H * W
+    int32_t tiles;   // ceil(n_cells / kScanTile)
 };
 
-// K1: cell id per point (-1 if dropped); counts[cell] += 1 (counts start at
-// zero) and the point's rank of arrival in its cell (an arbitrary order) goes
-// to slot[i].
-hipError_t cell_ids(const PillarGroup &grp, const PillarGeom &g, hipStream_t s);
-
-// K2a: per tile of kScanTile cells: (points, non-empty cells); zeroes
-// meta[2] (the overfull count of K2c).
-hipError_t scan_reduce(const PillarGroup &grp, int32_t n_cells, hipStream_t s);
-// K2c: offsets[cell] (exclusive prefix of counts), pillar lists in
-// ascending cell order, list of the pillars (indices into them) holding
-// more than max_pts points; meta = {valid points, pillars, overfull count}.
-// Leaves counts[] all zero, the state K1 expects next.
-hipError_t scan_down(const PillarGroup &grp, int32_t n_cells, int32_t max_pts, hipStream_t s);
-// K2d: member[offsets[cell] + slot] = point index, sorted[...] = the point.
-hipError_t scatter(const PillarGroup &grp, hipStream_t s);
-// K3: dense canvas [H*W][C]: per pillar cell, channel max over the first
+// The sort of points by cell (counting in LDS):
+// K1 bin_count: cell id per point (-1 if dropped); per block of
+//    kPtsPerBlock points, its points' count in every tile of cells, one
+//    atomic ttotal[tile] += count per non-empty tile (ttotal starts at
+//    zero) reserving the block's run in the tile, and each point's
+//    position within its tile (slot).
+// K2 bin_scatter: tstart[t] = first point of tile t in tile order,
+//    tstart[tiles] = meta[0] = valid points, meta[2] (overfull count) = 0;
+//    binned / cellb = point index / cell in tile order.
+// K3 tile_sort: per tile, LDS counts of its cells: the tile's pillars in
+//    ascending cell order at tcell / tcount / toff [tile * kScanTile + q]
+//    (npil[tile] of them), the pillars over max_pts listed in overfull
+//    (by that index, meta[2] of them), and member / sorted = the points in
+//    cell order (rank within a cell: an arbitrary order).
+hipError_t bin_count(const PillarGroup &grp, const PillarGeom &g, hipStream_t s);
+hipError_t bin_scatter(const PillarGroup &grp, hipStream_t s);
+hipError_t tile_sort(const PillarGroup &grp, int32_t max_pts, hipStream_t s);
+// K4 pillar_lists: the global pillar lists pcells / pcounts / poffs in
+// ascending cell order, meta[1] = P pillars, from the tiles' lists;
+// ttotal back to zero.
+hipError_t pillar_lists(const PillarGroup &grp, hipStream_t s);
+// K5 pfn_canvas: the dense canvas [H*W][C]: per pillar cell, channel max over the first
 // min(count, max_pts) members of ReLU(W^T f + b) (for cells over the cap,
 // after moving the max_pts lowest point indices to the front of the
 // segment).  Writes the pillar cells only: every other cell must already be

@@ -1,25 +1,30 @@
 // Pillarization and point-feature canvas for gfx950.
 //
-// Deterministic counting sort by cell (no float atomics, no order-dependent
-// result), five dependent launches, each over a group of agents released
-// together (the blocks of the group's agents are interleaved, see
-// group_block; a single release is a group of one):
-//   cell_ids        two points per thread: float32 cell index, atomic count
-//                   per cell (the counts start at zero); the returned old
-//                   count is the point's rank of arrival in its cell
-//   scan_reduce /   exclusive prefix over all H*W cells -> segment offsets,
-//   scan_down       ascending list of non-empty cells (pillars) and their
-//                   counts (staged in LDS, stored coalesced), list of the
-//                   pillars over the per-pillar point cap (each block of the
-//                   second pass adds up the tile sums before it); the counts
-//                   go back to zero for the next frame
-//   scatter         member[offset[cell] + rank] = point index
-//   pfn_canvas      one lane per (two pillars, 8 channels): linear 4 -> C,
-//                   ReLU, max over the pillar's points into its cell.  Extra
-//                   blocks take the few pillars over the cap: one wavefront
-//                   moves the cap lowest point indices (found by bisection on
-//                   the index value) to the front of the segment and writes
-//                   that pillar's features
+// Deterministic sort of points by cell (LDS, one global atomic per non-empty (point block, tile) bin, no
+// order-dependent result), five dependent launches, each
+// over a group of agents released together (the blocks of the group's
+// agents are interleaved, see group_block; a single release is a group of
+// one).  Cells are cut into tiles of kScanTile cells, points into blocks of
+// kPtsPerBlock:
+//   bin_count    cell id per point; per point block, an LDS histogram of its
+//                points over the tiles, the point's rank in its (block,
+//                tile) bin from the LDS atomic; every non-empty bin
+//                reserves its run in its tile (the only global atomics: one
+//                per non-empty bin, not one per point)
+//   bin_scatter  the tiles' first points (each block scans the tiles'
+//                totals itself), point indices and cells in tile order
+//   tile_sort    one block per tile: LDS counts of the tile's cells, their
+//                scan -> the tile's pillars in ascending cell order and
+//                each point's place in cell order (member, sorted)
+//   pillar_lists one block per tile: its pillar list moved to its place in
+//                the global lists (the block adds up the earlier tiles'
+//                pillar counts itself)
+//   pfn_canvas   one lane per (two pillars, 8 channels): linear 4 -> C,
+//                ReLU, max over the pillar's points into its cell.  Extra
+//                blocks take the few pillars over the cap: one wavefront
+//                moves the cap lowest point indices (found by bisection on
+//                the index value) to the front of the segment and writes
+//                that pillar's features
 // The canvas is zero outside the pillars: canvas_clear zeroes the last
 // frame's pillar cells again (off the encoder's path: the executor runs it
 // when the next frame begins, before any branch input has arrived).
@@ -109,136 +114,197 @@ __device__ inline int cell_of(const float4 p, const PillarGeom &g) {
     return c;
 }
 
-// Points per thread of the per-point kernels (cell ids, scatter): both
-// loads and both atomics of a thread are in flight together.
-constexpr int kPtsPerThread = 2;
-constexpr int kPtsPerBlock = 256 * kPtsPerThread;
+inline __device__ int blocks_of(int n) { return (n + kPtsPerBlock - 1) / kPtsPerBlock; }
 
-__global__ __launch_bounds__(256) void k_cell_ids(const PillarGroup grp, const PillarGeom g) {
+// K1: cell ids, per-(block, tile) counts and the block's run in every
+// tile; two points per thread.
+__global__ __launch_bounds__(256) void k_bin_count(const PillarGroup grp, const PillarGeom g) {
+    extern __shared__ int lds[];  // [grp.tiles] counts, then [grp.tiles] bases
+    int *hist = lds, *base = lds + grp.tiles;
     const GroupBlock gb = group_block(grp);
     const int j = gb.j;
     const int n = grp.n[j];
-    const int i0 = gb.b * kPtsPerBlock + threadIdx.x;
-    if (i0 >= n) return;
+    if (gb.b >= blocks_of(n)) return;  // the whole block: past this agent's points
     const PillarBufs B = group_bufs(grp, j);
     const float4 *pts = grp.pts[j];
-    int c[kPtsPerThread];
+    for (int t = threadIdx.x; t < grp.tiles; t += 256) hist[t] = 0;
+    __syncthreads();
+    int tile[2], rank[2];
 #pragma unroll
-    for (int u = 0; u < kPtsPerThread; ++u) {
-        const int i = i0 + u * 256;
-        c[u] = i < n ? cell_of(pts[i], g) : -2;
-    }
-#pragma unroll
-    for (int u = 0; u < kPtsPerThread; ++u) {
-        const int i = i0 + u * 256;
-        if (c[u] == -2) continue;
-        B.cell[i] = c[u];
-        if (c[u] >= 0) B.slot[i] = atomicAdd(&B.counts[c[u]], 1);
-    }
-}
-
-__global__ __launch_bounds__(256) void k_scan_reduce(const PillarGroup grp, int32_t n_cells) {
-    const GroupBlock gb = group_block(grp);
-    const PillarBufs B = group_bufs(grp, gb.j);
-    if (gb.b == 0 && threadIdx.x == 0) B.meta[2] = 0;  // overfull count, appended to by the scan
-    const int base = gb.b * kScanTile + threadIdx.x * 8;
-    int s = 0, f = 0;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        const int c = base + i;
-        if (c < n_cells) {
-            const int v = B.counts[c];
-            s += v;
-            f += v > 0;
+    for (int u = 0; u < 2; ++u) {
+        const int i = gb.b * kPtsPerBlock + u * 256 + int(threadIdx.x);
+        tile[u] = -1;
+        if (i < n) {
+            const int c = cell_of(pts[i], g);
+            B.cell[i] = c;
+            if (c >= 0) {
+                tile[u] = c / kScanTile;
+                rank[u] = atomicAdd(&hist[tile[u]], 1);
+            }
         }
     }
+    __syncthreads();
+    // the block's run in every tile it touches: one global atomic per
+    // non-empty (block, tile) bin
+    for (int t = threadIdx.x; t < grp.tiles; t += 256) {
+        const int h = hist[t];
+        if (h > 0) base[t] = atomicAdd(&B.ttotal[t], h);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+        if (tile[u] >= 0) B.slot[gb.b * kPtsPerBlock + u * 256 + int(threadIdx.x)] = base[tile[u]] + rank[u];
+}
+
+// K2: every point to its place in tile order.  Each block scans the tiles'
+// totals in LDS into the tiles' first points; the agent's first block also
+// stores them (tstart) and the point count.
+__global__ __launch_bounds__(256) void k_bin_scatter(const PillarGroup grp) {
+    extern __shared__ int ts[];  // [grp.tiles + 1]
+    const GroupBlock gb = group_block(grp);
+    const int j = gb.j;
+    const int n = grp.n[j];
+    const PillarBufs B = group_bufs(grp, j);
+    const int T = grp.tiles;
+    const int per = (T + 255) / 256;
+    int s = 0;
+    for (int r = 0; r < per; ++r) {
+        const int t = int(threadIdx.x) * per + r;
+        if (t < T) s += B.ttotal[t];
+    }
     int2 tot;
-    block_excl_scan256(make_int2(s, f), &tot);
-    if (threadIdx.x == 0) {
-        B.tiles[2 * gb.b] = tot.x;
-        B.tiles[2 * gb.b + 1] = tot.y;
+    int acc = block_excl_scan256(make_int2(s, 0), &tot).x;
+    for (int r = 0; r < per; ++r) {
+        const int t = int(threadIdx.x) * per + r;
+        if (t < T) {
+            ts[t] = acc;
+            acc += B.ttotal[t];
+        }
+    }
+    if (threadIdx.x == 0) ts[T] = tot.x;
+    __syncthreads();
+    if (gb.b == 0) {
+        for (int t = threadIdx.x; t <= T; t += 256) B.tstart[t] = ts[t];
+        if (threadIdx.x == 0) {
+            B.meta[0] = tot.x;
+            B.meta[1] = 0;  // the pillar lists' kernel writes the pillar count
+            B.meta[2] = 0;  // pillars over the cap, appended to by the tile sort
+        }
+    }
+    if (gb.b >= blocks_of(n)) return;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        const int i = gb.b * kPtsPerBlock + u * 256 + int(threadIdx.x);
+        if (i < n) {
+            const int c = B.cell[i];
+            if (c >= 0) {
+                const int d = ts[c / kScanTile] + B.slot[i];
+                B.binned[d] = i;
+                B.cellb[d] = c;
+            }
+        }
     }
 }
 
-__global__ __launch_bounds__(256) void k_scan_down(const PillarGroup grp, int32_t n_cells, int32_t max_pts) {
-    // the tile's pillars (cell, count, offset), staged for coalesced stores
-    __shared__ int3 stage[kScanTile];
+// K4: one block per tile of cells.
+constexpr int kSortCache = 8;
+__global__ __launch_bounds__(256) void k_tile_sort(const PillarGroup grp, int32_t max_pts) {
+    __shared__ int cnt[kScanTile];
+    __shared__ int loff[kScanTile];
     const GroupBlock gb = group_block(grp);
-    const PillarBufs B = group_bufs(grp, gb.j);
-    const int base = gb.b * kScanTile + threadIdx.x * 8;
+    const int j = gb.j, t = gb.b;
+    const PillarBufs B = group_bufs(grp, j);
+    const float4 *pts = grp.pts[j];
+    const int lo = B.tstart[t], hi = B.tstart[t + 1];
+    const int c0 = t * kScanTile;
+    for (int q = threadIdx.x; q < kScanTile; q += 256) cnt[q] = 0;
+    __syncthreads();
+    // the tile's first kSortCache * 256 points keep their cell and rank in
+    // registers between the passes; any further ones go through `rank`
+    int lcell[kSortCache], rk[kSortCache];
+#pragma unroll
+    for (int u = 0; u < kSortCache; ++u) {
+        const int e = lo + int(threadIdx.x) + u * 256;
+        lcell[u] = e < hi ? B.cellb[e] - c0 : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < kSortCache; ++u)
+        if (lo + int(threadIdx.x) + u * 256 < hi) rk[u] = atomicAdd(&cnt[lcell[u]], 1);
+    for (int e = lo + int(threadIdx.x) + kSortCache * 256; e < hi; e += 256)
+        B.rank[e] = atomicAdd(&cnt[B.cellb[e] - c0], 1);
+    __syncthreads();
     int v[8];
     int s = 0, f = 0;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-        const int c = base + i;
-        v[i] = c < n_cells ? B.counts[c] : 0;
+        v[i] = cnt[threadIdx.x * 8 + i];
         s += v[i];
         f += v[i] > 0;
     }
-    // the sums of the tiles before this one, added up by the block itself
-    // (no separate scan of the tile sums); the last tile writes the totals
-    int2 before = make_int2(0, 0);
-    for (int t = threadIdx.x; t < gb.b; t += 256)
-        before = add2(before, make_int2(B.tiles[2 * t], B.tiles[2 * t + 1]));
-    int2 prefix, tot;
-    block_excl_scan256(before, &prefix);
+    int2 tot;
     const int2 ex = block_excl_scan256(make_int2(s, f), &tot);
-    if (gb.b == gb.nb - 1 && threadIdx.x == 0) {
-        B.meta[0] = prefix.x + tot.x;
-        B.meta[1] = prefix.y + tot.y;
-    }
-    int off = prefix.x + ex.x;
-    int q = ex.y;  // the thread's first pillar within the tile
+    int off = ex.x, q = ex.y;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-        const int c = base + i;
-        if (c < n_cells) {
-            B.offsets[c] = off;
-            // counts go back to zero: the state the next frame's K1 starts from
-            if (v[i] > 0) B.counts[c] = 0;
-            if (v[i] > 0) {
-                stage[q] = make_int3(c, v[i], off);
-                if (v[i] > max_pts) B.overfull[atomicAdd(&B.meta[2], 1)] = prefix.y + q;
-                ++q;
-            }
-            off += v[i];
+        const int lc = int(threadIdx.x) * 8 + i;
+        loff[lc] = off;
+        if (v[i] > 0) {
+            const int sidx = c0 + q;
+            B.tcell[sidx] = c0 + lc;
+            B.tcount[sidx] = v[i];
+            B.toff[sidx] = lo + off;
+            if (v[i] > max_pts) B.overfull[atomicAdd(&B.meta[2], 1)] = sidx;
+            ++q;
+        }
+        off += v[i];
+    }
+    if (threadIdx.x == 0) B.npil[t] = tot.y;
+    __syncthreads();
+    int idx[kSortCache];
+#pragma unroll
+    for (int u = 0; u < kSortCache; ++u) {
+        const int e = lo + int(threadIdx.x) + u * 256;
+        idx[u] = e < hi ? B.binned[e] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < kSortCache; ++u) {
+        const int e = lo + int(threadIdx.x) + u * 256;
+        if (e < hi) {
+            const int d = lo + loff[lcell[u]] + rk[u];
+            B.member[d] = idx[u];
+            B.sorted[d] = pts[idx[u]];
         }
     }
-    __syncthreads();
-    for (int t = threadIdx.x; t < tot.y; t += 256) {
-        const int3 e = stage[t];
-        B.pcells[prefix.y + t] = e.x;
-        B.pcounts[prefix.y + t] = e.y;
-        B.poffs[prefix.y + t] = e.z;
+    for (int e = lo + int(threadIdx.x) + kSortCache * 256; e < hi; e += 256) {
+        const int d = lo + loff[B.cellb[e] - c0] + B.rank[e];
+        const int i = B.binned[e];
+        B.member[d] = i;
+        B.sorted[d] = pts[i];
     }
 }
 
-__global__ __launch_bounds__(256) void k_scatter(const PillarGroup grp) {
+// K5: the tiles' pillar lists concatenated into the global ones, one block
+// per tile: its first global pillar is the sum of the earlier tiles'
+// pillar counts.  The last tile's block writes the pillar count.
+__global__ __launch_bounds__(256) void k_pillar_lists(const PillarGroup grp) {
     const GroupBlock gb = group_block(grp);
-    const int j = gb.j;
-    const int n = grp.n[j];
-    const int i0 = gb.b * kPtsPerBlock + threadIdx.x;
-    if (i0 >= n) return;
-    const PillarBufs B = group_bufs(grp, j);
-    const float4 *pts = grp.pts[j];
-    int c[kPtsPerThread], d[kPtsPerThread];
-#pragma unroll
-    for (int u = 0; u < kPtsPerThread; ++u) {
-        const int i = i0 + u * 256;
-        c[u] = i < n ? B.cell[i] : -1;
-        d[u] = c[u] >= 0 ? B.slot[i] : 0;
+    const int t = gb.b;
+    const PillarBufs B = group_bufs(grp, gb.j);
+    int s = 0;
+    for (int q = threadIdx.x; q < t; q += 256) s += B.npil[q];
+    int2 tot;
+    block_excl_scan256(make_int2(s, 0), &tot);
+    const int first = tot.x, np = B.npil[t];
+    const int c0 = t * kScanTile;
+    for (int q = threadIdx.x; q < np; q += 256) {
+        B.pcells[first + q] = B.tcell[c0 + q];
+        B.pcounts[first + q] = B.tcount[c0 + q];
+        B.poffs[first + q] = B.toff[c0 + q];
     }
-#pragma unroll
-    for (int u = 0; u < kPtsPerThread; ++u)
-        if (c[u] >= 0) d[u] += B.offsets[c[u]];
-#pragma unroll
-    for (int u = 0; u < kPtsPerThread; ++u) {
-        const int i = i0 + u * 256;
-        if (c[u] >= 0) {
-            B.member[d[u]] = i;
-            B.sorted[d[u]] = pts[i];
-        }
-    }
+    if (t == grp.tiles - 1 && threadIdx.x == 0) B.meta[1] = first + np;
+    // the tile's point total back to zero, the state the next frame's bin
+    // count starts from (every reader of it has finished)
+    if (threadIdx.x == 0) B.ttotal[t] = 0;
 }
 
 __device__ inline uint32_t pack_bf16x2(float a, float b) {
@@ -283,15 +349,14 @@ __device__ inline void store_canvas8(const PfnArgs &a, void *canvas, int cell, i
     }
 }
 
-// Blocks [0, a.pillar_blocks): a lane per (pillar, 8 channels) over the
-// ascending pillar list from the scan: ReLU(W^T f + b) maxed over the
-// pillar's points, read in segment order from `sorted`, into the pillar's
-// cell; pillars over the cap are left to the other blocks.  Blocks from
-// a.pillar_blocks on: one wavefront per cell over the cap moves the cap
+// Blocks [0, a.pillar_blocks): a lane per (two pillars, 8 channels) of the
+// global pillar list takes ReLU(W^T f + b) maxed over the pillar's points,
+// read in segment order from `sorted`, into the pillar's cell.  Pillars
+// over the cap are left to the other blocks.  Blocks from
+// a.pillar_blocks on: one wavefront per pillar over the cap moves the cap
 // lowest point indices to the front of its segment (member indices and
-// points) and writes the features of those points.  The lanes read the
-// cell, count and segment offset together; the other cells of the canvas
-// already hold zeros.  Counts go back to zero for the next frame.
+// points) and writes the features of those points.  The other cells of the
+// canvas already hold zeros.
 template <bool BF16>
 __global__ __launch_bounds__(256) void k_pfn_canvas(const PfnArgs a, const PillarGroup grp) {
     // PFN weights and bias, read once per block into LDS (C <= 512)
@@ -309,11 +374,11 @@ __global__ __launch_bounds__(256) void k_pfn_canvas(const PfnArgs a, const Pilla
         const int n_over = B.meta[2];
         const float4 *pts = grp.pts[j];
         for (int w = wave; w < n_over; w += n_waves) {
-            const int pil = B.overfull[w];
-            const int c = B.pcells[pil];
-            const int cnt = B.pcounts[pil];
-            int32_t *seg = B.member + B.poffs[pil];
-            float4 *sseg = B.sorted + B.poffs[pil];
+            const int sidx = B.overfull[w];  // in the tiles' pillar lists
+            const int c = B.tcell[sidx];
+            const int cnt = B.tcount[sidx];
+            int32_t *seg = B.member + B.toff[sidx];
+            float4 *sseg = B.sorted + B.toff[sidx];
             // Smallest T with #{members < T} >= max_pts.  Members are
             // distinct point indices in [0, n), so exactly max_pts members
             // lie below T.
@@ -437,25 +502,26 @@ hipError_t fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t cell_ids(const PillarGroup &grp, const PillarGeom &g, hipStream_t s) {
+hipError_t bin_count(const PillarGroup &grp, const PillarGeom &g, hipStream_t s) {
     if (grp.n_max <= 0) return hipSuccess;
-    k_cell_ids<<<blocks_for(grp.n_max, kPtsPerBlock) * unsigned(grp.m), 256, 0, s>>>(grp, g);
+    k_bin_count<<<blocks_for(grp.n_max, kPtsPerBlock) * unsigned(grp.m), 256, size_t(grp.tiles) * 8, s>>>(grp, g);
     return hipGetLastError();
 }
 
-hipError_t scan_reduce(const PillarGroup &grp, int32_t n_cells, hipStream_t s) {
-    k_scan_reduce<<<blocks_for(n_cells, kScanTile) * unsigned(grp.m), 256, 0, s>>>(grp, n_cells);
+hipError_t bin_scatter(const PillarGroup &grp, hipStream_t s) {
+    // at least one block per agent: the first one stores the tile starts
+    const unsigned nb = grp.n_max > 0 ? blocks_for(grp.n_max, kPtsPerBlock) : 1u;
+    k_bin_scatter<<<nb * unsigned(grp.m), 256, size_t(grp.tiles + 1) * 4, s>>>(grp);
     return hipGetLastError();
 }
 
-hipError_t scan_down(const PillarGroup &grp, int32_t n_cells, int32_t max_pts, hipStream_t s) {
-    k_scan_down<<<blocks_for(n_cells, kScanTile) * unsigned(grp.m), 256, 0, s>>>(grp, n_cells, max_pts);
+hipError_t tile_sort(const PillarGroup &grp, int32_t max_pts, hipStream_t s) {
+    k_tile_sort<<<unsigned(grp.tiles) * unsigned(grp.m), 256, 0, s>>>(grp, max_pts);
     return hipGetLastError();
 }
 
-hipError_t scatter(const PillarGroup &grp, hipStream_t s) {
-    if (grp.n_max <= 0) return hipSuccess;
-    k_scatter<<<blocks_for(grp.n_max, kPtsPerBlock) * unsigned(grp.m), 256, 0, s>>>(grp);
+hipError_t pillar_lists(const PillarGroup &grp, hipStream_t s) {
+    k_pillar_lists<<<unsigned(grp.tiles) * unsigned(grp.m), 256, 0, s>>>(grp);
     return hipGetLastError();
 }
 
