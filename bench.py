@@ -182,7 +182,7 @@ def gemm_reference(layers, torch, iters=50):
         torch.cuda.synchronize()
         us = e0.elapsed_time(e1) / iters * 1e3
         rows.append({"M": M, "N": N, "K": K, "hipblaslt_us": round(us, 2),
-                     "hipblaslt_tflops": round(2.0 * M * N * K / (us * 1e-6) / 1e12, 1), "conv_us": l["us"]})
+                     "hipblaslt_tflops": round(2.0 * M * N * K / (us * 1e-6) / 1e12, 1), "conv_us_per_agent": l["us_per_agent"]})
         del x, w
     return rows
 
@@ -474,13 +474,15 @@ def main(argv=None):
         base = k * per_agent + 3
         conv_ms += node[:, base:base + L].sum()
     conv_flops = sum(c["flops"] for c in lw["convs"]) * K * rsteps
-    conv_launches = L * K * rsteps
+    # the K agents released together: one launch per conv layer serves all
+    conv_launches = L * rsteps
     achieved = conv_flops / (conv_ms * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if cfg["precision"] == "bf16" else PEAK_FP32_TFLOPS
     # pillar stage: the K agents released together run it as one launch
     # chain, so every member's pillar + PFN nodes are the group's span
     node_1 = np.array(node_1)
-    group_ms = float((node[:, 1] + node[:, 2]).sum())
+    # (each member's node is its share of the shared launches)
+    group_ms = sum(float(node[:, k * per_agent + 1].sum() + node[:, k * per_agent + 2].sum()) for k in range(K))
     single_ms = sum(float(node_1[:, k * per_agent + 1].sum() + node_1[:, k * per_agent + 2].sum()) for k in range(K))
     P = [int(R.rtcc_tensor_bytes(ctx, R.RTCC_T_PILLAR_CELLS, k)) // 4 for k in range(K)]
     pil_bytes = sum(16 * len(frame["points"][k]) + 8 * P[k] + lw["H"] * lw["W"] * cfg["c_pfn"] * lw["elt"]
@@ -497,7 +499,7 @@ def main(argv=None):
     layers = []
     for l, c in enumerate(lw["convs"]):
         us = float(np.mean([node[:, k * per_agent + 3 + l] for k in range(K)])) * 1e3
-        layers.append({"M": c["M"], "N": c["N"], "K": c["K"], "us": round(us, 2),
+        layers.append({"M": c["M"], "N": c["N"], "K": c["K"], "us_per_agent": round(us, 2),
                        "tflops": round(c["flops"] / (us * 1e-6) / 1e12, 1)})
     out = {
         "metric": METRIC,
@@ -545,8 +547,8 @@ def main(argv=None):
         },
         "conv_layers": layers,
         "node_ms_mean": {
-            "pillar_group_of_%d" % K: round(float(node[:, 1].mean()), 4),
-            "pfn_canvas_group_of_%d" % K: round(float(node[:, 2].mean()), 4),
+            "pillar_group_of_%d" % K: round(float(sum(node[:, k * per_agent + 1].mean() for k in range(K))), 4),
+            "pfn_canvas_group_of_%d" % K: round(float(sum(node[:, k * per_agent + 2].mean() for k in range(K))), 4),
             "pillar_alone": round(float(np.mean([node_1[:, k * per_agent + 1] for k in range(K)])), 4),
             "pfn_canvas_alone": round(float(np.mean([node_1[:, k * per_agent + 2] for k in range(K)])), 4),
             "conv_total_per_agent": round(conv_ms / (K * rsteps), 4),

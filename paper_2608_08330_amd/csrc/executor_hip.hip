@@ -11,10 +11,10 @@
 // before the post-join kernels run.
 //
 // Branches released together (one batch of events, or every branch at the
-// barrier's A) share one launch chain of the pillar stage: its kernels run
-// the group's agents side by side (one grid row per agent) on the first
-// member's stream, after which every member's backbone continues on its own
-// stream.  A single release is a group of one.
+// barrier's A) share one sequence of launches on the first member's stream:
+// every pillar kernel, conv layer and upsampling runs the group's agents side
+// by side in one grid, each agent's output bit for bit that of a launch of
+// its own.  A single release is a group of one.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -149,9 +149,9 @@ class HipExecutor : public Executor {
             pb[k].sorted = static_cast<float4 *>(b.d_sorted);
             pb[k].canvas = b.d_canvas;
         }
+        HIP_TRY(hipEventCreateWithFlags(&ev_clear_, hipEventDisableTiming));
         HIP_TRY(alloc(&d_pbufs_, sizeof(kern::PillarBufs) * p.K));
         HIP_TRY(hipMemcpy(d_pbufs_, pb.data(), sizeof(kern::PillarBufs) * p.K, hipMemcpyHostToDevice));
-        HIP_TRY(hipEventCreateWithFlags(&ev_group_, hipEventDisableTiming));
         HIP_TRY(alloc(&d_fused, size_t(p.H2) * p.W2 * p.c_slot * p.elt));
         d_fused_stage_.assign(p.ups.size(), nullptr);
         if (p.d.multiscale)
@@ -213,17 +213,32 @@ class HipExecutor : public Executor {
         HIP_TRY(hipSetDevice(dev_));
         // Work of an abandoned (infeasible) frame may still be running and
         // reading the staging buffers that the caller is about to refill.
-        for (Branch &b : br_) HIP_TRY(hipStreamSynchronize(b.stream));
-        HIP_TRY(hipStreamSynchronize(copy_stream_));
-        HIP_TRY(hipStreamSynchronize(join_stream_));
+        // (After a completed join every stream is idle already.)
+        if (!idle_) {
+            for (Branch &b : br_) HIP_TRY(hipStreamSynchronize(b.stream));
+            HIP_TRY(hipStreamSynchronize(copy_stream_));
+            HIP_TRY(hipStreamSynchronize(join_stream_));
+            idle_ = true;
+        }
+        clear_pending_ = false;
         HIP_TRY(hipEventRecord(ev_frame0_, compute_stream_for_join()));
         // The last frame's canvas pillars (readable until now) go back to
-        // zero at the start of the frame, ahead of the branch's next encoder
-        // on its stream (or the one compute stream), normally long before its
-        // completion event.
-        for (Branch &b : br_) {
-            b.dispatched = false;
-            if (b.canvas_dirty) HIP_TRY(clear_canvas(b, o_.exec == RTCC_EXEC_SERIAL ? join_stream_ : b.stream));
+        // zero at the start of the frame, in one launch for every branch on
+        // the join stream, which the stream of every encoder launch of the
+        // frame then waits for: ahead of the branch's next encoder, normally
+        // long before its completion event.
+        int dirty[kern::kMaxGroup];
+        int nd = 0;
+        for (int k = 0; k < p_.K; ++k) {
+            br_[k].dispatched = false;
+            if (br_[k].canvas_dirty) dirty[nd++] = k;
+        }
+        if (nd > 0) {
+            HIP_TRY(clear_canvases(dirty, nd, join_stream_));
+            if (o_.exec != RTCC_EXEC_SERIAL) {
+                HIP_TRY(hipEventRecord(ev_clear_, join_stream_));
+                clear_pending_ = true;
+            }
         }
         return RTCC_OK;
     }
@@ -237,7 +252,7 @@ class HipExecutor : public Executor {
         const bool serial = o_.exec == RTCC_EXEC_SERIAL;
         const bool timing = o_.node_timing != 0;
         Branch &lead = br_[items[0].agent];
-        // the group's pillar stage runs on the first member's stream
+        // the group's encoders run on the first member's stream
         hipStream_t ls = serial ? join_stream_ : lead.stream;
         int agents[kern::kMaxGroup];
         for (int j = 0; j < m; ++j) {
@@ -261,9 +276,9 @@ class HipExecutor : public Executor {
                     }
                 }
             }
-            // ls runs after the member's input copy and after the work of the
-            // last frame queued on the member's stream (its canvas clear)
-            if (bs != ls) {
+            // ls runs after the member's input copy on the member's stream
+            // (the stream holds no other work of the frame)
+            if (bs != ls && !it.device_src && it.n > 0) {
                 HIP_TRY(hipEventRecord(b.h2d_done, bs));
                 HIP_TRY(hipStreamWaitEvent(ls, b.h2d_done, 0));
             }
@@ -272,70 +287,56 @@ class HipExecutor : public Executor {
             b.host_input = !it.device_src;
             HIP_TRY(prepare_branch(b, ls));
         }
+        // ... and after the frame's canvas clear
+        if (clear_pending_) HIP_TRY(hipStreamWaitEvent(ls, ev_clear_, 0));
+        idle_ = false;
+        // The group's launches serve every member: the first member's events
+        // time them, mark their start and their end for all.
+        for (int j = 0; j < m; ++j) {
+            br_[agents[j]].ev_src = agents[0];
+            br_[agents[j]].group_m = m;
+        }
         // reached once every member's input copy and everything queued
         // before the group's encoders have completed: the encoders run
-        for (int j = 0; j < m; ++j) HIP_TRY(hipEventRecord(br_[agents[j]].started, ls));
+        HIP_TRY(hipEventRecord(lead.started, ls));
         rtcc_status st;
         const bool graphs = o_.use_graphs && !timing;
-        if (m == 1) {
-            // a branch released alone: its whole encoder, as one graph whose
-            // arguments are its input, point count and (branch warp) pose
-            Branch &b = lead;
-            if (graphs) {
-                std::vector<unsigned char> key;
-                put(key, b.src);
-                put(key, b.n);
-                if (p_.d.warp_in_branch)
-                    for (int e = 0; e < 6; ++e) put(key, b.affine[e]);
-                st = run_graph(b.graph, key, ls, [&](hipStream_t c) {
-                    rtcc_status r = enqueue_pillars(agents, 1, c, false, err);
-                    return r == RTCC_OK ? enqueue_backbone(b, c, false, err) : r;
-                }, err);
-            } else {
-                st = enqueue_pillars(agents, 1, ls, timing, err);
-                if (st == RTCC_OK) st = enqueue_backbone(b, ls, timing, err);
-            }
-            if (st != RTCC_OK) return st;
-            b.canvas_dirty = true;  // the encoder writes this frame's pillars
-            HIP_TRY(hipEventRecord(b.done, ls));
-            b.dispatched = true;
-            return RTCC_OK;
-        }
-        // a group: one pillar-stage chain over the members (a graph whose
-        // arguments are the members, their inputs and point counts), then
-        // every member's backbone on its own stream
+        // the encoders as one sequence of launches on ls: the pillar stage
+        // and then every backbone layer over the whole group
+        auto encoders = [&](hipStream_t c, bool t) {
+            rtcc_status r = enqueue_pillars(agents, m, c, t, err);
+            return r == RTCC_OK ? enqueue_backbone(agents, m, c, t, err) : r;
+        };
         if (graphs) {
-            std::vector<unsigned char> key;
+            // two graphs per branch released alone and for a group: the
+            // pillar stage, whose arguments (the members, their inputs and
+            // point counts) change from frame to frame, and the backbones,
+            // whose buffers are fixed (their graph is updated only for other
+            // members or, with branch warps, other poses)
+            std::vector<unsigned char> kp, kb;
             for (int j = 0; j < m; ++j) {
-                put(key, agents[j]);
-                put(key, br_[agents[j]].src);
-                put(key, br_[agents[j]].n);
+                const Branch &b = br_[agents[j]];
+                put(kp, agents[j]);
+                put(kp, b.src);
+                put(kp, b.n);
+                put(kb, agents[j]);
+                if (p_.d.warp_in_branch)
+                    for (int e = 0; e < 6; ++e) put(kb, b.affine[e]);
             }
-            st = run_graph(group_graph_, key, ls,
-                           [&](hipStream_t c) { return enqueue_pillars(agents, m, c, false, err); }, err);
+            st = run_graph_or_eager(m == 1 ? lead.pillar_graph : group_pillar_graph_, kp, ls,
+                                    [&](hipStream_t c) { return enqueue_pillars(agents, m, c, false, err); },
+                                    err);
+            if (st == RTCC_OK)
+                st = run_graph(m == 1 ? lead.graph : group_graph_, kb, ls,
+                               [&](hipStream_t c) { return enqueue_backbone(agents, m, c, false, err); }, err);
         } else {
-            st = enqueue_pillars(agents, m, ls, timing, err);
+            st = encoders(ls, timing);
         }
         if (st != RTCC_OK) return st;
-        if (!serial) HIP_TRY(hipEventRecord(ev_group_, ls));
+        HIP_TRY(hipEventRecord(lead.done, ls));
         for (int j = 0; j < m; ++j) {
             Branch &b = br_[agents[j]];
-            hipStream_t bs = serial ? join_stream_ : b.stream;
-            if (bs != ls) HIP_TRY(hipStreamWaitEvent(bs, ev_group_, 0));
-            if (graphs) {
-                // the backbone's arguments are fixed buffers; only a branch
-                // warp depends on the frame (its pose)
-                std::vector<unsigned char> key;
-                if (p_.d.warp_in_branch)
-                    for (int e = 0; e < 6; ++e) put(key, b.affine[e]);
-                st = run_graph(b.backbone_graph, key, bs,
-                               [&](hipStream_t c) { return enqueue_backbone(b, c, false, err); }, err);
-            } else {
-                st = enqueue_backbone(b, bs, timing, err);
-            }
-            if (st != RTCC_OK) return st;
-            b.canvas_dirty = true;
-            HIP_TRY(hipEventRecord(b.done, bs));
+            b.canvas_dirty = true;  // the encoder writes this frame's pillars
             b.dispatched = true;
         }
         return RTCC_OK;
@@ -344,8 +345,9 @@ class HipExecutor : public Executor {
     int progress(int agent) override {
         const Branch &b = br_[agent];
         if (!b.dispatched) return 0;
-        if (hipEventQuery(b.done) == hipSuccess) return 2;
-        return hipEventQuery(b.started) == hipSuccess ? 1 : 0;
+        const Branch &g = br_[b.ev_src];  // the launches that serve it
+        if (hipEventQuery(g.done) == hipSuccess) return 2;
+        return hipEventQuery(g.started) == hipSuccess ? 1 : 0;
     }
 
     rtcc_status join(const std::vector<std::array<float, 6>> &affine,
@@ -353,7 +355,10 @@ class HipExecutor : public Executor {
                      std::string &err) override {
         HIP_TRY(hipSetDevice(dev_));
         hipStream_t js = compute_stream_for_join();
-        for (Branch &b : br_) HIP_TRY(hipStreamWaitEvent(js, b.done, 0));
+        // every distinct completion event (a group has one)
+        for (int k = 0; k < p_.K; ++k)
+            if (br_[k].ev_src == k || br_[br_[k].ev_src].ev_src != br_[k].ev_src)
+                HIP_TRY(hipStreamWaitEvent(js, br_[br_[k].ev_src].done, 0));
         const bool timing = o_.node_timing != 0;
         // one-kernel fusion nodes are timed by events bracketing the kernel
         if (timing && p_.d.multiscale) HIP_TRY(hipEventRecord(post_ev_[0], js));
@@ -365,8 +370,9 @@ class HipExecutor : public Executor {
                 for (int e = 0; e < 6; ++e) put(key, affine[k][e]);
                 for (int e = 0; e < 3; ++e) put(key, poses[k][e]);
             }
-            s = run_graph(post_graph_[0], key, js,
-                          [&](hipStream_t c) { return enqueue_post_head(affine, poses, c, false, err); }, err);
+            s = run_graph_or_eager(post_graph_[0], key, js,
+                                   [&](hipStream_t c) { return enqueue_post_head(affine, poses, c, false, err); },
+                                   err);
             if (s != RTCC_OK) return s;
             HIP_TRY(hipEventRecord(ev_head_, js));
             s = run_graph(post_graph_[1], {}, js, [&](hipStream_t c) { return enqueue_post_detect(c, false, err); },
@@ -378,6 +384,12 @@ class HipExecutor : public Executor {
         int32_t *hs = reinterpret_cast<int32_t *>(h_small);
         HIP_TRY(hipMemcpyAsync(hs, d_count, 4, hipMemcpyDeviceToHost, js));
         if (nms_max_ > 0) HIP_TRY(hipMemcpyAsync(hs + 1, d_nms_count, 4, hipMemcpyDeviceToHost, js));
+        // the first records come back with the counts (one round trip in
+        // the common case), the rest, if any, after them
+        const void *recs = nms_max_ > 0 ? d_nms_out : d_rec;
+        const size_t cap = nms_max_ > 0 ? size_t(nms_max_) : n_anchor_;
+        const size_t first = std::min(cap, kFirstRecords);
+        HIP_TRY(hipMemcpyAsync(h_rec, recs, first * 36, hipMemcpyDeviceToHost, js));
         HIP_TRY(spin_sync(js));
         const int64_t decoded = hs[0];
         const int64_t count = nms_max_ > 0 ? hs[1] : decoded;
@@ -386,11 +398,12 @@ class HipExecutor : public Executor {
             err = "decode or NMS produced an out-of-range count";
             return RTCC_E_INTERNAL;
         }
-        if (count > 0) {
-            HIP_TRY(hipMemcpyAsync(h_rec, nms_max_ > 0 ? d_nms_out : d_rec, size_t(count) * 36,
-                                   hipMemcpyDeviceToHost, js));
+        if (size_t(count) > first) {
+            HIP_TRY(hipMemcpyAsync(h_rec + first * 9, static_cast<const char *>(recs) + first * 36,
+                                   (size_t(count) - first) * 36, hipMemcpyDeviceToHost, js));
             HIP_TRY(spin_sync(js));
         }
+        idle_ = true;  // every stream's work of the frame has completed
         for (int64_t i = 0; i < count; ++i) {
             const float *r = h_rec + i * 9;
             std::memcpy(&boxes_[i * 7], r, 7 * sizeof(float));
@@ -467,7 +480,7 @@ class HipExecutor : public Executor {
                 rtcc_status st;
                 if (k < p_.K) {
                     st = enqueue_pillars(&k, 1, s, false, err);
-                    if (st == RTCC_OK) st = enqueue_backbone(br_[k], s, false, err);
+                    if (st == RTCC_OK) st = enqueue_backbone(&k, 1, s, false, err);
                 } else {
                     st = enqueue_post(last_affine_, last_poses_, s, false, err);
                 }
@@ -475,7 +488,7 @@ class HipExecutor : public Executor {
                 HIP_TRY(hipEventRecord(e1, s));
                 if (k < p_.K) {
                     br_[k].canvas_dirty = true;
-                    HIP_TRY(clear_canvas(br_[k], s));  // untimed, as after a frame
+                    HIP_TRY(clear_canvases(&k, 1, s));  // untimed, as after a frame
                 }
                 HIP_TRY(hipEventSynchronize(e1));
                 float ms = 0.f;
@@ -507,21 +520,25 @@ class HipExecutor : public Executor {
         const int L = int(p_.convs.size()), S = int(p_.ups.size());
         for (const Branch &b : br_) {
             float v = 0.f;
-            // input copy, then the pillar stage (shared by a group: timed by
-            // the events of its first member)
+            // input copy, then the encoder's launches: shared by a group and
+            // timed by the events of its first member, each member takes an
+            // equal share (the members' shares add up to the launch)
             const Branch &g = br_[b.ev_src];
-            for (int e = 0; e < 3; ++e) {
-                HIP_TRY(hipEventElapsedTime(&v, e == 0 ? b.ev[0] : g.ev[e], g.ev[e + 1]));
-                ms[q++] = v;
+            const float share = 1.0f / float(b.group_m);
+            HIP_TRY(hipEventElapsedTime(&v, b.ev[0], g.ev[1]));
+            ms[q++] = v;
+            for (int e = 1; e < 3; ++e) {
+                HIP_TRY(hipEventElapsedTime(&v, g.ev[e], g.ev[e + 1]));
+                ms[q++] = v * share;
             }
             for (int l = 0; l < L; ++l) {
-                HIP_TRY(hipEventElapsedTime(&v, b.kev[2 * l], b.kev[2 * l + 1]));
-                ms[q++] = v;
+                HIP_TRY(hipEventElapsedTime(&v, g.kev[2 * l], g.kev[2 * l + 1]));
+                ms[q++] = v * share;
             }
             for (int u = 0; u < S; ++u) {
                 v = 0.f;
-                if (!p_.d.multiscale) HIP_TRY(hipEventElapsedTime(&v, b.ev[3 + L + u], b.ev[4 + L + u]));
-                ms[q++] = v;
+                if (!p_.d.multiscale) HIP_TRY(hipEventElapsedTime(&v, g.ev[3 + L + u], g.ev[4 + L + u]));
+                ms[q++] = v * share;
             }
             if (S == 0) ms[q++] = 0.f;
             v = 0.f;
@@ -555,6 +572,7 @@ class HipExecutor : public Executor {
         hipGraph_t g = nullptr;
         hipGraphExec_t x = nullptr;
         std::vector<unsigned char> key;
+        std::vector<unsigned char> seen;  // the last key launched without the graph
     };
     static void drop(Graph &gr) {
         if (gr.x) (void)hipGraphExecDestroy(gr.x);
@@ -562,6 +580,7 @@ class HipExecutor : public Executor {
         gr.x = nullptr;
         gr.g = nullptr;
         gr.key.clear();
+        gr.seen.clear();
     }
     template <class T>
     static void put(std::vector<unsigned char> &key, const T &v) {
@@ -611,6 +630,19 @@ class HipExecutor : public Executor {
         return RTCC_OK;
     }
 
+    // For launches whose arguments may change every frame: replay the graph
+    // when the key is the one it holds; capture (or update) it when the same
+    // new key comes twice in a row; otherwise launch eagerly, which costs
+    // less than a capture and an update that a stream of changing frames
+    // would pay every frame.
+    template <class F>
+    rtcc_status run_graph_or_eager(Graph &gr, const std::vector<unsigned char> &key, hipStream_t s, F &&enqueue,
+                                   std::string &err) {
+        if ((gr.x && gr.key == key) || gr.seen == key) return run_graph(gr, key, s, enqueue, err);
+        gr.seen = key;
+        return enqueue(s);
+    }
+
     struct Branch {
         float *staging = nullptr;
         void *d_pts = nullptr, *d_cell = nullptr, *d_slot = nullptr, *d_member = nullptr;
@@ -627,8 +659,8 @@ class HipExecutor : public Executor {
         bool pillars_clean = true;       // every enqueued K1 was followed by the PFN kernel
         bool canvas_dirty = false;       // the canvas holds pillars not yet cleared (canvas_clear)
         hipEvent_t wev[2] = {nullptr, nullptr};  // bracket the branch warp kernel
-        Graph graph;                     // the encoder as a HIP graph (use_graphs, released alone)
-        Graph backbone_graph;            // its backbone (use_graphs, released in a group)
+        Graph pillar_graph;              // its pillar stage as a HIP graph (use_graphs, released alone)
+        Graph graph;                     // its backbone as a HIP graph (use_graphs, released alone)
         std::vector<void *> d_act;
         hipStream_t stream = nullptr;
         hipEvent_t done = nullptr, h2d_done = nullptr, started = nullptr;
@@ -638,7 +670,8 @@ class HipExecutor : public Executor {
         int32_t n = 0;
         bool host_input = true;
         bool dispatched = false;
-        int ev_src = 0;  // the branch whose ev[1..3] timed this one's pillar stage
+        int ev_src = 0;   // the branch whose events timed this one's encoder launches
+        int group_m = 1;  // branches those launches served
     };
 
     hipStream_t compute_stream_for_join() const { return join_stream_; }
@@ -690,8 +723,6 @@ class HipExecutor : public Executor {
             grp.n[j] = b.n;
             grp.n_max = std::max(grp.n_max, b.n);
         }
-        // the shared stages are timed once, by the first member's events
-        for (int j = 0; j < m; ++j) br_[agents[j]].ev_src = agents[0];
         auto mark = [&](int e) -> hipError_t {
             return timing ? hipEventRecord(br_[agents[0]].ev[e], s) : hipSuccess;
         };
@@ -722,19 +753,21 @@ class HipExecutor : public Executor {
         return RTCC_OK;
     }
 
-    // Backbone of encoder E_k after its pillar stage: convs, upsampling into
-    // slot k, and the branch warp when it is the branch's last node.
-    rtcc_status enqueue_backbone(Branch &b, hipStream_t s, bool timing, std::string &err) {
+    // Backbones of the encoders of `agents` (m of them) after their pillar
+    // stage: every conv layer and every upsampling as one launch over the m
+    // maps (GemmArgs::batch), which gives each map the bits of a launch of
+    // its own; then the branch warps when the warp is the branches' last
+    // node.  With timing, the first member's events bracket the shared
+    // launches.
+    rtcc_status enqueue_backbone(const int *agents, int m, hipStream_t s, bool timing, std::string &err) {
         const Plan &p = p_;
+        Branch &lead = br_[agents[0]];
         int ev = 4;
-        const void *x = b.d_canvas;
         for (size_t l = 0; l < p.convs.size(); ++l) {
             const ConvLayer &c = p.convs[l];
             kern::GemmArgs ga{};
-            ga.in = x;
             ga.wt = static_cast<const char *>(d_mat) + c.w_off * p.elt;
             ga.bias = static_cast<const float *>(d_bias) + c.b_off;
-            ga.out = b.d_act[l];
             ga.Hi = c.Hi; ga.Wi = c.Wi; ga.Ci = c.Ci;
             ga.Ho = c.Ho; ga.Wo = c.Wo; ga.N = c.Co;
             ga.stride = c.stride;
@@ -742,45 +775,62 @@ class HipExecutor : public Executor {
             ga.ldo = c.Co;
             ga.c_off = 0;
             ga.splits = plans_[l].splits;
-            ga.variant = plans_[l].variant;
+            ga.variant = kern::conv_variant_for(plans_[l], m);
             ga.zero = d_zero;
-            ga.ws = static_cast<float *>(b.d_ws);
+            ga.batch = m;
+            for (int j = 0; j < m; ++j) {
+                const Branch &b = br_[agents[j]];
+                ga.in_b[j] = l == 0 ? b.d_canvas : b.d_act[l - 1];
+                ga.out_b[j] = b.d_act[l];
+                ga.ws_b[j] = static_cast<float *>(b.d_ws);
+            }
+            ga.in = ga.in_b[0];
+            ga.out = ga.out_b[0];
+            ga.ws = ga.ws_b[0];
             // with timing, conv nodes are timed by events bracketing their
             // kernels' execution (no dispatch gap)
-            HIP_TRY(kern::conv3x3(p.bf16, ga, s, timing ? b.kev[2 * l] : nullptr,
-                                  timing ? b.kev[2 * l + 1] : nullptr));
-            if (timing) HIP_TRY(hipEventRecord(b.ev[ev], s));
+            HIP_TRY(kern::conv3x3(p.bf16, ga, s, timing ? lead.kev[2 * l] : nullptr,
+                                  timing ? lead.kev[2 * l + 1] : nullptr));
+            if (timing) HIP_TRY(hipEventRecord(lead.ev[ev], s));
             ++ev;
-            x = b.d_act[l];
         }
         for (const UpLayer &u : p.ups) {
             if (p.d.multiscale) break;  // upsampling runs once, on the fused maps
-            HIP_TRY(upsample(u, b.d_act[p.stage_last_conv[u.stage]], b.d_slotbuf, s));
-            if (timing) HIP_TRY(hipEventRecord(b.ev[ev], s));
+            const void *in[kern::kMaxGroup];
+            void *out[kern::kMaxGroup];
+            for (int j = 0; j < m; ++j) {
+                in[j] = br_[agents[j]].d_act[p.stage_last_conv[u.stage]];
+                out[j] = br_[agents[j]].d_slotbuf;
+            }
+            HIP_TRY(upsample(u, in, out, m, s));
+            if (timing) HIP_TRY(hipEventRecord(lead.ev[ev], s));
             ++ev;
         }
         if (p.d.warp_in_branch) {
-            // The identity pose (the ego agent) samples every cell exactly at
-            // itself with weight 1, a copy: the fusion then reads the slot.
-            // (Compared by value: the identity's off-diagonal terms may be -0.)
-            static const float kIdentity[6] = {1, 0, 0, 0, 1, 0};
-            b.warp_ran = false;
-            for (int e = 0; e < 6; ++e) b.warp_ran |= b.affine[e] != kIdentity[e];
-            if (!b.warp_ran) {
-                b.ego_map = b.d_slotbuf;
-            } else {
-                kern::WarpSlotArgs wa{};
-                wa.slot = b.d_slotbuf;
-                for (int e = 0; e < 6; ++e) wa.affine[e] = b.affine[e];
-                wa.out = b.d_warped;
-                wa.H2 = p.H2;
-                wa.W2 = p.W2;
-                wa.C = p.c_slot;
-                HIP_TRY(kern::warp_slot(p.bf16, wa, s, timing ? b.wev[0] : nullptr, timing ? b.wev[1] : nullptr));
-                b.ego_map = b.d_warped;
+            for (int j = 0; j < m; ++j) {
+                Branch &b = br_[agents[j]];
+                // The identity pose (the ego agent) samples every cell exactly
+                // at itself with weight 1, a copy: the fusion then reads the
+                // slot.  (Compared by value: the identity's off-diagonal terms
+                // may be -0.)
+                static const float kIdentity[6] = {1, 0, 0, 0, 1, 0};
+                b.warp_ran = false;
+                for (int e = 0; e < 6; ++e) b.warp_ran |= b.affine[e] != kIdentity[e];
+                if (!b.warp_ran) {
+                    b.ego_map = b.d_slotbuf;
+                } else {
+                    kern::WarpSlotArgs wa{};
+                    wa.slot = b.d_slotbuf;
+                    for (int e = 0; e < 6; ++e) wa.affine[e] = b.affine[e];
+                    wa.out = b.d_warped;
+                    wa.H2 = p.H2;
+                    wa.W2 = p.W2;
+                    wa.C = p.c_slot;
+                    HIP_TRY(kern::warp_slot(p.bf16, wa, s, timing ? b.wev[0] : nullptr,
+                                            timing ? b.wev[1] : nullptr));
+                    b.ego_map = b.d_warped;
+                }
             }
-            if (timing) HIP_TRY(hipEventRecord(b.ev[ev], s));
-            ++ev;
         }
         return RTCC_OK;
     }
@@ -802,29 +852,34 @@ class HipExecutor : public Executor {
             b.pillars_clean = true;
             b.canvas_dirty = false;
         }
-        return b.canvas_dirty ? clear_canvas(b, s) : hipSuccess;
+        if (!b.canvas_dirty) return hipSuccess;
+        const int agent = int(&b - br_.data());
+        return clear_canvases(&agent, 1, s);
     }
 
-    // Zero the canvas cells of the agent's last pillars (their list is the
-    // scan's output of the last enqueued encoder) on stream s.
-    hipError_t clear_canvas(Branch &b, hipStream_t s) {
+    // Zero the canvas cells of the last pillars of the given branches (their
+    // lists are the pillar stage's output of their last encoders) on stream
+    // s, in one launch.
+    hipError_t clear_canvases(const int *agents, int m, hipStream_t s) {
         const int n_cells = p_.H * p_.W;
         const int max_p = int(std::min<int64_t>(p_.n_max, n_cells));
-        hipError_t e = kern::canvas_clear(p_.bf16, b.d_canvas, static_cast<const int32_t *>(b.d_pcells),
-                                          static_cast<const int32_t *>(b.d_meta), p_.c_pfn, max_p, s);
-        if (e == hipSuccess) b.canvas_dirty = false;
+        kern::PillarGroup grp{};
+        grp.bufs = static_cast<const kern::PillarBufs *>(d_pbufs_);
+        grp.m = m;
+        for (int j = 0; j < m; ++j) grp.agent[j] = agents[j];
+        hipError_t e = kern::canvas_clear(p_.bf16, grp, p_.c_pfn, max_p, s);
+        if (e == hipSuccess)
+            for (int j = 0; j < m; ++j) br_[agents[j]].canvas_dirty = false;
         return e;
     }
 
     // Upsampling u of the map `in` into channels [c_off, c_off + Co) of `out`
     // ([H2][W2][c_slot]).
-    hipError_t upsample(const UpLayer &u, const void *in, void *out, hipStream_t s) {
+    hipError_t upsample(const UpLayer &u, const void *const *in, void *const *out, int m, hipStream_t s) {
         const Plan &p = p_;
         kern::GemmArgs ga{};
-        ga.in = in;
         ga.wt = static_cast<const char *>(d_mat) + u.w_off * p.elt;
         ga.bias = static_cast<const float *>(d_bias) + u.b_off;
-        ga.out = out;
         ga.Hi = u.Hi; ga.Wi = u.Wi; ga.Ci = u.Ci;
         ga.Ho = p.H2; ga.Wo = p.W2; ga.N = u.Co;
         ga.stride = 1;
@@ -835,6 +890,14 @@ class HipExecutor : public Executor {
         ga.variant = kern::kConvImplicit;
         ga.zero = d_zero;
         ga.ws = nullptr;
+        ga.batch = m;
+        for (int j = 0; j < m; ++j) {
+            ga.in_b[j] = in[j];
+            ga.out_b[j] = out[j];
+            ga.ws_b[j] = nullptr;
+        }
+        ga.in = in[0];
+        ga.out = out[0];
         return kern::deconv(p.bf16, ga, s);
     }
 
@@ -868,7 +931,9 @@ class HipExecutor : public Executor {
                 wa.W2 = u.Wi;
                 wa.C = u.Ci;
                 HIP_TRY(kern::warp_fuse(p.bf16, p.d.fusion == RTCC_FUSE_ATTN, wa, s));
-                HIP_TRY(upsample(u, d_fused_stage_[u.stage], d_fused, s));
+                const void *fin = d_fused_stage_[u.stage];
+                void *fout = d_fused;
+                HIP_TRY(upsample(u, &fin, &fout, 1, s));
             }
         } else if (p.d.warp_in_branch) {
             kern::FuseArgs fa{};
@@ -1109,10 +1174,11 @@ class HipExecutor : public Executor {
             for (hipEvent_t e : b.wev)
                 if (e) (void)hipEventDestroy(e);
             drop(b.graph);
-            drop(b.backbone_graph);
+            drop(b.pillar_graph);
         }
         drop(group_graph_);
-        if (ev_group_) (void)hipEventDestroy(ev_group_);
+        drop(group_pillar_graph_);
+        if (ev_clear_) (void)hipEventDestroy(ev_clear_);
         for (void *ptr : dev_allocs_) {
             if (o_.dev_alloc) o_.dev_free(ptr, o_.alloc_user);
             else (void)hipFree(ptr);
@@ -1156,10 +1222,14 @@ class HipExecutor : public Executor {
     std::vector<void *> d_fused_stage_;  // multi-scale: fused map of every stage
     hipStream_t cap_stream_ = nullptr;   // where graphs are captured (use_graphs)
     Graph post_graph_[2];                // post-join: up to T^head, then decode and NMS
-    Graph group_graph_;                  // pillar stage of a group of branches
+    Graph group_graph_;                  // the backbones of a group of branches
+    Graph group_pillar_graph_;           // the pillar stage of a group of branches
+    hipEvent_t ev_clear_ = nullptr;      // the frame's canvas clear is done
+    bool clear_pending_ = false;         // encoder launches must wait for ev_clear_
+    bool idle_ = true;                   // no work queued since the last completed join
+    static constexpr size_t kFirstRecords = 1024;  // records read back with the counts
     void *d_pbufs_ = nullptr;            // kern::PillarBufs of every agent
     int tiles_ = 0;                      // tiles of cells of the pillar sort
-    hipEvent_t ev_group_ = nullptr;      // a group's pillar stage is done
     int64_t graph_stats_[3] = {0, 0, 0}; // instantiations, update attempts, launches
 };
 

@@ -183,8 +183,20 @@ __device__ inline void staged_store(unsigned char *stage, const f32x4_t (&acc)[F
     }
 }
 
+// The arguments of map bt of a batched launch (see GemmArgs::batch).
+__device__ inline GemmArgs batch_args(const GemmArgs &a0, int bt) {
+    GemmArgs a = a0;
+    if (a0.batch > 1) {
+        a.in = a0.in_b[bt];
+        a.out = a0.out_b[bt];
+        a.ws = a0.ws_b[bt];
+    }
+    return a;
+}
+__device__ inline int batch_of(const GemmArgs &a0) { return a0.batch > 1 ? a0.batch : 1; }
+
 template <typename T, int BM, int BN, int WGM, int WGN, int STAGES, bool DECONV>
-__global__ __launch_bounds__(64 * WGM * WGN) void k_igemm(GemmArgs a) {
+__global__ __launch_bounds__(64 * WGM * WGN) void k_igemm(GemmArgs a0) {
     constexpr int NW = WGM * WGN;                    // wavefronts per block
     constexpr int EPV = Traits<T>::EPV;
     constexpr int BK = kRowBytes / int(sizeof(T));  // elements per row per K step
@@ -206,6 +218,17 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_igemm(GemmArgs a) {
     const int wave = tid >> 6;
     const int wm = wave % WGM, wn = wave / WGM;
 
+    // XCD-aware tile order: block ids are dealt to the 8 XCDs round-robin;
+    // give each XCD a contiguous run of tiles.  Batched, map bt's blocks are
+    // one contiguous run (with 8 maps, one XCD's).
+    int bid = blockIdx.x;
+    const int nbx = gridDim.x;
+    if ((nbx & 7) == 0) bid = (bid & 7) * (nbx >> 3) + (bid >> 3);
+    const int per_map = nbx / batch_of(a0);
+    const int bt = bid / per_map;
+    bid -= bt * per_map;
+    const GemmArgs a = batch_args(a0, bt);
+
     const int Ci = a.Ci;
     const int M = DECONV ? a.Hi * a.Wi : a.Ho * a.Wo;
     const int N = a.N;
@@ -213,13 +236,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_igemm(GemmArgs a) {
     const int KT_all = K / BK;
     const int KT = KT_all / a.splits;
 
-    // XCD-aware tile order: block ids are dealt to the 8 XCDs round-robin;
-    // give each XCD a contiguous run of tiles.
     const int mt = (M + BM - 1) / BM;
     const int nt = (N + BN - 1) / BN;
-    int bid = blockIdx.x;
-    const int nbx = gridDim.x;
-    if ((nbx & 7) == 0) bid = (bid & 7) * (nbx >> 3) + (bid >> 3);
     const int m_tile = bid % mt;
     const int rest = bid / mt;  // n tile, then split
     const int n_tile = rest % nt;
@@ -418,7 +436,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_igemm(GemmArgs a) {
 // the weights of the next R - 2 steps plus, at taps 1 .. R - 1, the next
 // chunk's patch (issued at tap 0 after the weights of step s + R - 1).
 template <typename T, int TH, int BN, int WGM, int WGN, int RB, int STRIDE, int KG, int R, bool ILV>
-__global__ __launch_bounds__(64 * WGM * WGN * KG) void k_conv3s1(GemmArgs a) {
+__global__ __launch_bounds__(64 * WGM * WGN * KG) void k_conv3s1(GemmArgs a0) {
     constexpr int NW = WGM * WGN;  // wavefronts per group
     constexpr int EPV = Traits<T>::EPV;
     constexpr int VPR = RB / 16;                 // 16-byte vectors per row and step
@@ -461,15 +479,21 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void k_conv3s1(GemmArgs a) {
         uint32_t(reinterpret_cast<uintptr_t>((lds_void *)gsmem)));
     const uint32_t lds_b = lds_base + 2 * A_BYTES;
 
+    int bid = blockIdx.x;
+    const int nbx = gridDim.x;
+    if ((nbx & 7) == 0) bid = (bid & 7) * (nbx >> 3) + (bid >> 3);
+    // batched: map bt's blocks are one contiguous run (with 8 maps, one XCD's)
+    const int per_map = nbx / batch_of(a0);
+    const int bt = bid / per_map;
+    bid -= bt * per_map;
+    const GemmArgs a = batch_args(a0, bt);
+
     const int Ci = a.Ci, N = a.N, Ho = a.Ho, Wo = a.Wo;
     const int K = 9 * Ci;
     const int CH = (Ci / BK) / a.splits / KG;  // chunks of this split and group
 
     const int tx = (Wo + TW - 1) / TW, ty = (Ho + TH - 1) / TH;
     const int nt = N / BN;
-    int bid = blockIdx.x;
-    const int nbx = gridDim.x;
-    if ((nbx & 7) == 0) bid = (bid & 7) * (nbx >> 3) + (bid >> 3);
     // channel tile fastest: the nt blocks that read the same input patch
     // are neighbours in the remapped order and so run on the same XCD,
     // where the patch is fetched from HBM once and then hits in L2
@@ -694,7 +718,8 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void k_conv3s1(GemmArgs a) {
 // out[m][n] = ReLU(bias[n] + sum over slices s = 0 .. S-1 of ws[s][m][n]),
 // summed in slice order.  Four channels per thread.
 template <typename T>
-__global__ __launch_bounds__(256) void k_splitk_reduce(GemmArgs a) {
+__global__ __launch_bounds__(256) void k_splitk_reduce(GemmArgs a0) {
+    const GemmArgs a = batch_args(a0, blockIdx.y);
     const int M = a.Ho * a.Wo;
     const int N = a.N;
     const int64_t q = int64_t(blockIdx.x) * 256 + threadIdx.x;
@@ -729,23 +754,25 @@ template <typename T, int BM, int BN, int WGM, int WGN, int STAGES, bool DECONV>
 hipError_t launch_cfg(const GemmArgs &a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr) {
     const int M = DECONV ? a.Hi * a.Wi : a.Ho * a.Wo;
     const unsigned gz = DECONV ? unsigned(a.u * a.u) : 1u;
-    const unsigned nx = unsigned((M + BM - 1) / BM) * unsigned((a.N + BN - 1) / BN) * unsigned(a.splits);
+    const unsigned nb = unsigned(a.batch > 1 ? a.batch : 1);
+    const unsigned nx = unsigned((M + BM - 1) / BM) * unsigned((a.N + BN - 1) / BN) * unsigned(a.splits) * nb;
     hipError_t e = launch_kernel(k_igemm<T, BM, BN, WGM, WGN, STAGES, DECONV>, dim3(nx, 1, gz),
                                  dim3(64 * WGM * WGN), s, e0, a.splits == 1 ? e1 : nullptr, a);
     if (e != hipSuccess || a.splits == 1) return e;
     const int64_t total = int64_t(M) * (a.N / 4);
-    return launch_kernel(k_splitk_reduce<T>, dim3(unsigned((total + 255) / 256)), dim3(256), s, nullptr, e1, a);
+    return launch_kernel(k_splitk_reduce<T>, dim3(unsigned((total + 255) / 256), nb), dim3(256), s, nullptr, e1, a);
 }
 
 template <typename T, int TH, int BN, int WGM, int WGN, int RB, int STRIDE, int KG, int R, bool ILV>
 hipError_t launch_halo(const GemmArgs &a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr) {
+    const unsigned nb = unsigned(a.batch > 1 ? a.batch : 1);
     const unsigned tiles = unsigned((a.Wo + 15) / 16) * unsigned((a.Ho + TH - 1) / TH);
-    const unsigned nx = tiles * unsigned(a.N / BN) * unsigned(a.splits);
+    const unsigned nx = tiles * unsigned(a.N / BN) * unsigned(a.splits) * nb;
     hipError_t e = launch_kernel(k_conv3s1<T, TH, BN, WGM, WGN, RB, STRIDE, KG, R, ILV>, dim3(nx),
                                  dim3(64 * WGM * WGN * KG), s, e0, a.splits == 1 ? e1 : nullptr, a);
     if (e != hipSuccess || a.splits == 1) return e;
     const int64_t total = int64_t(a.Ho) * a.Wo * (a.N / 4);
-    return launch_kernel(k_splitk_reduce<T>, dim3(unsigned((total + 255) / 256)), dim3(256), s, nullptr, e1, a);
+    return launch_kernel(k_splitk_reduce<T>, dim3(unsigned((total + 255) / 256), nb), dim3(256), s, nullptr, e1, a);
 }
 
 template <typename T, bool DECONV>
@@ -794,27 +821,25 @@ ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, in
     (void)Hi;
     (void)Wi;
     const int bk = bf16 ? 32 : 16;  // implicit GEMM K step (64 bytes)
-    ConvPlan p{kConvImplicit, 1, 0};
+    ConvPlan p{kConvImplicit, 1, 0, kConvImplicit, 1};
     const int elt = bf16 ? 2 : 4;
     if (stride == 1 && Co % 128 == 0) {
         // 8 x 16-pixel tiles with 8 wavefronts where the grid fills the
         // chip; otherwise 4 x 16-pixel tiles with 4 wavefronts, split over
         // channel chunks until half the CUs hold a tile (an f32 partial
         // round trip costs more than idle CUs beyond that, measured on
-        // 64 x 64 grids)
+        // 64 x 64 grids).  Batched maps take the 8 x 16 tiles once their
+        // tiles fill the chip.
         const int tx = (Wo + 15) / 16, nt = Co / 128;
         const int t8 = tx * ((Ho + 7) / 8) * nt, t4 = tx * ((Ho + 3) / 4) * nt;
         const int chunk_bytes = ((Ci * elt) % 128 == 0 && Ci * elt >= 512) ? 128 : 64;
         const int chunks = Ci * elt / chunk_bytes;
-        const int t64 = tx * ((Ho + 3) / 4) * (Co / 64);
+        p.variant_wide = kConvHalo8;
         if (t8 >= n_cu) {
             p.variant = kConvHalo8;
-        } else if (t64 >= n_cu && chunks % 2 == 0) {
-            // 64-channel tiles fill the chip; two wave groups split the
-            // channel chunks so every CU runs 8 wavefronts
-            p.variant = kConvHalo4N64K2;
         } else {
             p.variant = kConvHalo4;
+            p.wide_maps = (n_cu + t8 - 1) / t8;
             if (t4 < n_cu / 2)
                 for (int sp = 2; sp <= chunks && t4 * p.splits < n_cu / 2; ++sp)
                     if (chunks % sp == 0) p.splits = sp;
@@ -824,11 +849,13 @@ ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, in
         // 64 input channels the implicit GEMM is faster
         const int tx = (Wo + 15) / 16, nt = Co / 128;
         const int t8 = tx * ((Ho + 7) / 8) * nt;
-        const int t64 = tx * ((Ho + 3) / 4) * (Co / 64);
-        const int chunks = Ci * elt / 64;
-        if (t8 >= n_cu) p.variant = kConvHalo8S2;
-        else if (t64 >= n_cu && chunks % 2 == 0) p.variant = kConvHalo4S2N64K2;
-        else p.variant = kConvHalo4S2;
+        p.variant_wide = kConvHalo8S2;
+        if (t8 >= n_cu) {
+            p.variant = kConvHalo8S2;
+        } else {
+            p.variant = kConvHalo4S2;
+            p.wide_maps = (n_cu + t8 - 1) / t8;
+        }
     } else {
         const int tiles = gemm_tiles(Ho * Wo, Co);
         const int kt = 9 * Ci / bk;
@@ -880,7 +907,7 @@ ConvPlan conv_plan_forced(bool bf16, const ConvPlan &planned, int variant, int s
         default: break;
     }
     if (!fits || steps % groups != 0 || steps / groups < 1) return planned;
-    ConvPlan p{variant, 1, 0};
+    ConvPlan p{variant, 1, 0, variant, 1};
     // a split-K slice holds whole chunks of one wave group's share; the
     // two-group tilings run unsplit
     if (splits > 1 && groups == 1 && steps % splits == 0) p.splits = splits;

@@ -87,10 +87,10 @@ struct PfnArgs {
 };
 // max_pillars bounds every agent's meta[1] (at most min(cells, points)).
 hipError_t pfn_canvas(bool bf16, PfnArgs a, const PillarGroup &grp, int32_t max_pillars, hipStream_t s);
-// The canvas cells of the pillars listed in pcells (meta[1] of them) back to
-// zero; max_pillars bounds meta[1].
-hipError_t canvas_clear(bool bf16, void *canvas, const int32_t *pcells, const int32_t *meta, int32_t C,
-                        int32_t max_pillars, hipStream_t s);
+// For every agent of the group, the canvas cells of the pillars listed in its
+// pcells (meta[1] of them) back to zero; max_pillars bounds meta[1].  Only
+// grp.bufs, grp.agent and grp.m are read.
+hipError_t canvas_clear(bool bf16, const PillarGroup &grp, int32_t C, int32_t max_pillars, hipStream_t s);
 
 // ------------------------------------------------------------ implicit GEMM
 // conv:   out[m][c_off + n] for m = output pixel, 3x3 taps, pad 1, stride.
@@ -111,6 +111,14 @@ struct GemmArgs {
     int32_t variant;   // conv kernel: kConvImplicit or one of the halo tilings
     const void *zero;  // >= 16 zero bytes in device memory (padding reads)
     float *ws;         // split-K partials [splits][M][N] float32
+    // Several agents' maps side by side in one launch (the same layer and
+    // weights): batch > 1 takes agent b's input, output and split-K partials
+    // from in_b / out_b / ws_b [b] instead of in / out / ws.  Every output
+    // element is computed exactly as in a launch of its own.
+    int32_t batch;     // 0 or 1: one map
+    const void *in_b[16];
+    void *out_b[16];
+    float *ws_b[16];
 };
 constexpr int kConvImplicit = 0;  // implicit GEMM (any stride)
 constexpr int kConvHalo8 = 1;     // stride-1 halo tiles of 8 x 16 pixels, 8 waves
@@ -120,17 +128,28 @@ constexpr int kConvHalo4S2 = 4;   // stride-2 halo tiles of 4 x 16 output pixels
 constexpr int kConvHalo4N64K2 = 5;    // stride-1 4 x 16 pixels x 64 channels, 2 groups of 4 waves
 constexpr int kConvHalo4S2N64K2 = 6;  // stride-2 4 x 16 pixels x 64 channels, 2 groups of 4 waves
 struct ConvPlan {
-    int variant;
+    int variant;      // tiling of a launch over one map
     int splits;
-    size_t ws_bytes;  // split-K workspace needed (0 without split)
+    size_t ws_bytes;  // split-K workspace needed per map (0 without split)
+    // From wide_maps maps per launch on (a batched launch, GemmArgs::batch),
+    // tiling variant_wide, whose every output element is accumulated in the
+    // same order as with `variant` (the same K chunks, taps and MFMA
+    // sequence; only the output tile differs), so batching never changes a
+    // bit of the result.
+    int variant_wide;
+    int wide_maps;
 };
 // Kernel variant and K split of one 3x3 conv layer on a GPU with n_cu CUs.
+// Only tilings with one wave group per tile are planned (a second group
+// would sum half of the K chunks apart, another accumulation order).
 ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, int stride, int n_cu);
 // The plan with tiling `variant` (1..6, or 7 = the implicit GEMM) and K split
 // `splits` forced where the layer's stride and channels allow it; `planned`
-// elsewhere.
+// elsewhere.  A forced tiling is used for batched launches too.
 ConvPlan conv_plan_forced(bool bf16, const ConvPlan &planned, int variant, int splits, int Ci, int Ho, int Wo,
                           int Co, int stride);
+// The tiling of a launch over `maps` maps.
+inline int conv_variant_for(const ConvPlan &p, int maps) { return maps >= p.wide_maps ? p.variant_wide : p.variant; }
 // With start / stop events, the first kernel of the convolution records
 // `start` when it begins executing and the last one `stop` when it ends
 // (kernel execution time, without the dispatch gap before it).

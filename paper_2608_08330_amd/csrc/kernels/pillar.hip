@@ -473,20 +473,23 @@ __global__ __launch_bounds__(256) void k_pfn_canvas(const PfnArgs a, const Pilla
 }
 
 // The canvas cells of the last frame's pillars back to zero, one lane per
-// (pillar, 8 channels); the rest of the canvas holds zeros already.
+// (pillar, 8 channels), for every agent of the group (its pillar list and
+// count are those of its last encoder); the rest of each canvas holds zeros
+// already.
 template <bool BF16>
-__global__ __launch_bounds__(256) void k_canvas_clear(void *canvas, const int32_t *__restrict__ pcells,
-                                                      const int32_t *__restrict__ meta, int32_t C) {
+__global__ __launch_bounds__(256) void k_canvas_clear(const PillarGroup grp, int32_t C) {
+    const GroupBlock gb = group_block(grp);
+    const PillarBufs B = group_bufs(grp, gb.j);
     const int lanes = C >> 3;
-    const int gid = int(blockIdx.x) * 256 + int(threadIdx.x);
+    const int gid = gb.b * 256 + int(threadIdx.x);
     const int p = gid / lanes;
-    if (p >= meta[1]) return;
-    const size_t off = size_t(pcells[p]) * C + (gid - p * lanes) * 8;
+    if (p >= B.meta[1]) return;
+    const size_t off = size_t(B.pcells[p]) * C + (gid - p * lanes) * 8;
     if (BF16) {
-        nt_store16(static_cast<uint16_t *>(canvas) + off, make_uint4(0u, 0u, 0u, 0u));
+        nt_store16(static_cast<uint16_t *>(B.canvas) + off, make_uint4(0u, 0u, 0u, 0u));
     } else {
-        nt_store16(static_cast<float *>(canvas) + off, make_uint4(0u, 0u, 0u, 0u));
-        nt_store16(static_cast<float *>(canvas) + off + 4, make_uint4(0u, 0u, 0u, 0u));
+        nt_store16(static_cast<float *>(B.canvas) + off, make_uint4(0u, 0u, 0u, 0u));
+        nt_store16(static_cast<float *>(B.canvas) + off + 4, make_uint4(0u, 0u, 0u, 0u));
     }
 }
 
@@ -537,12 +540,12 @@ hipError_t pfn_canvas(bool bf16, PfnArgs a, const PillarGroup &grp, int32_t max_
     return hipGetLastError();
 }
 
-hipError_t canvas_clear(bool bf16, void *canvas, const int32_t *pcells, const int32_t *meta, int32_t C,
-                        int32_t max_pillars, hipStream_t s) {
+hipError_t canvas_clear(bool bf16, const PillarGroup &grp, int32_t C, int32_t max_pillars, hipStream_t s) {
     const unsigned blocks = blocks_for(int64_t(max_pillars) * (C / 8), 256);
     if (blocks == 0) return hipSuccess;
-    if (bf16) k_canvas_clear<true><<<blocks, 256, 0, s>>>(canvas, pcells, meta, C);
-    else k_canvas_clear<false><<<blocks, 256, 0, s>>>(canvas, pcells, meta, C);
+    const unsigned grid = blocks * unsigned(grp.m);
+    if (bf16) k_canvas_clear<true><<<grid, 256, 0, s>>>(grp, C);
+    else k_canvas_clear<false><<<grid, 256, 0, s>>>(grp, C);
     return hipGetLastError();
 }
 
