@@ -43,20 +43,22 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 # commands in profiles/traffic_c5_bench.md).  Each figure holds only for the
 # kernel source it was taken on; after a change it reads null until re-taken.
 MEASURED_TRAFFIC = {
-    "conv": dict(src="paper_2608_08330_amd/csrc/kernels/igemm.hip", bytes=26.74e6,
-                 sha256="85a26081a63ce6d021aeea6520fb964af6ec453dd3094369184e1d99af239008"),
-    "warp_fuse": dict(src="paper_2608_08330_amd/csrc/kernels/post.hip", bytes=486.76e6,
-                      sha256="6d2341b8b2231406389bf9b8fe995ec1c3ce72cd83f6dbbdf794ff549e2fd6d5"),
-    "fuse": dict(src="paper_2608_08330_amd/csrc/kernels/post.hip", bytes=453.03e6,
-                 sha256="6d2341b8b2231406389bf9b8fe995ec1c3ce72cd83f6dbbdf794ff549e2fd6d5"),
-    "warp_slot": dict(src="paper_2608_08330_amd/csrc/kernels/post.hip", bytes=96.25e6,
-                      sha256="6d2341b8b2231406389bf9b8fe995ec1c3ce72cd83f6dbbdf794ff549e2fd6d5"),
+    # per 8-agent launch of a conv layer (averaged over the 13 layers)
+    "conv": dict(src="paper_2608_08330_amd/csrc/kernels/igemm.hip", bytes=154.5e6,
+                 sha256="f5545b4225c4f5eda113274dea7dc1c4aa1dde46f11aae94b4de9414aa466bd5"),
+    "warp_fuse": dict(src="paper_2608_08330_amd/csrc/kernels/post.hip", bytes=471.4e6,
+                      sha256="3dd695761a7ddeb2490129b0aded0e14dffcbbacb69f9ef0ac79eb63c8d0a814"),
+    # per 8-agent launch chain of the pillar stage (five kernels)
+    "pillar": dict(src="paper_2608_08330_amd/csrc/kernels/pillar.hip", bytes=195e6,
+                   sha256="75547fe4e96df6793946122f770939c49c0334a4250e7b36b154152a2ca40586"),
 }
 
 
 def measured_traffic(kernel):
     import hashlib
-    t = MEASURED_TRAFFIC[kernel]
+    t = MEASURED_TRAFFIC.get(kernel)
+    if t is None:
+        return None
     try:
         with open(os.path.join(ROOT, t["src"]), "rb") as f:
             same = hashlib.sha256(f.read()).hexdigest() == t["sha256"]
@@ -538,6 +540,7 @@ def main(argv=None):
                                   "peak": PEAK_HBM_GBS, "unit": "GB/s",
                                   "frac": round(pil_bytes / (group_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
                                   "agents": K, "span_us": round(group_ms / rsteps * 1e3, 2),
+                                  "traffic": measured_traffic("pillar"),
                                   "per_agent_alone": {
                                       "achieved": round(pil_bytes / (single_ms * 1e-3) / 1e9, 1),
                                       "us_per_agent": round(single_ms / (K * rsteps) * 1e3, 2)},
