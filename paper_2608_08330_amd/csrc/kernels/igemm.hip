@@ -778,7 +778,8 @@ hipError_t launch_halo(const GemmArgs &a, hipStream_t s, hipEvent_t e0 = nullptr
 template <typename T, bool DECONV>
 hipError_t launch(const GemmArgs &a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr) {
     if (!DECONV) {
-        // 128-byte K steps pay off from 256 input channels (bf16) on
+        // 128-byte K steps pay off from 256 input channels (bf16) on, where
+        // one block holds a CU (kConvHalo8C64 keeps 64-byte steps)
         const bool rb128 = (a.Ci * int(sizeof(T))) % 128 == 0 && a.Ci * int(sizeof(T)) >= 512;
         // template arguments: TH, BN, WGM, WGN, RB, STRIDE, KG, weight ring
         // depth R, interleaved LDS reads; R and the interleaving as they
@@ -787,11 +788,12 @@ hipError_t launch(const GemmArgs &a, hipStream_t s, hipEvent_t e0 = nullptr, hip
             case kConvHalo8:
                 return rb128 ? launch_halo<T, 8, 128, 4, 2, 128, 1, 1, 4, true>(a, s, e0, e1)
                              : launch_halo<T, 8, 128, 4, 2, 64, 1, 1, 4, false>(a, s, e0, e1);
+            case kConvHalo8C64: return launch_halo<T, 8, 128, 4, 2, 64, 1, 1, 4, false>(a, s, e0, e1);
             case kConvHalo4:
                 return rb128 ? launch_halo<T, 4, 128, 2, 2, 128, 1, 1, 3, true>(a, s, e0, e1)
                              : launch_halo<T, 4, 128, 2, 2, 64, 1, 1, 3, true>(a, s, e0, e1);
             case kConvHalo8S2: return launch_halo<T, 8, 128, 4, 2, 64, 2, 1, 4, true>(a, s, e0, e1);
-            case kConvHalo4S2: return launch_halo<T, 4, 128, 4, 2, 64, 2, 1, 3, true>(a, s, e0, e1);
+            case kConvHalo4S2: return launch_halo<T, 4, 128, 4, 2, 64, 2, 1, 4, true>(a, s, e0, e1);
             case kConvHalo4N64K2:
                 return rb128 ? launch_halo<T, 4, 64, 2, 2, 128, 1, 2, 4, true>(a, s, e0, e1)
                              : launch_halo<T, 4, 64, 2, 2, 64, 1, 2, 3, true>(a, s, e0, e1);
@@ -835,7 +837,14 @@ ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, in
         const int chunk_bytes = ((Ci * elt) % 128 == 0 && Ci * elt >= 512) ? 128 : 64;
         const int chunks = Ci * elt / chunk_bytes;
         p.variant_wide = kConvHalo8;
-        if (t8 >= n_cu) {
+        if (t8 >= n_cu && chunk_bytes == 128) {
+            // a map whose 8 x 16 tiles fill the chip by themselves: 64-byte
+            // chunks, two blocks per CU (at 128 x 128 x 256 -> 256, 8 maps
+            // per launch: 7% faster per map than 128-byte chunks, one map
+            // alone 10% slower; both forms accumulate alike, so the one
+            // tiling serves every launch)
+            p.variant = p.variant_wide = kConvHalo8C64;
+        } else if (t8 >= n_cu) {
             p.variant = kConvHalo8;
         } else {
             p.variant = kConvHalo4;
@@ -846,7 +855,9 @@ ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, in
         }
     } else if (stride == 2 && Co % 128 == 0 && Ci * elt >= 256) {
         // stride-2 patches (2 TH + 1 rows of 33 pixels, column-split); at
-        // 64 input channels the implicit GEMM is faster
+        // 64 input channels (two chunks) the implicit GEMM is faster, alone
+        // and in the 8-agent launch of the c5 frame (19.4-19.8 us per agent
+        // against 20.2-20.6 with 4-row and 22.3 with 8-row stride-2 tiles)
         const int tx = (Wo + 15) / 16, nt = Co / 128;
         const int t8 = tx * ((Ho + 7) / 8) * nt;
         p.variant_wide = kConvHalo8S2;
@@ -888,6 +899,10 @@ ConvPlan conv_plan_forced(bool bf16, const ConvPlan &planned, int variant, int s
         case kConvHalo4:
             fits = stride == 1 && Co % 128 == 0;
             steps = row_bytes / (rb128 ? 128 : 64);
+            break;
+        case kConvHalo8C64:
+            fits = stride == 1 && Co % 128 == 0 && row_bytes % 64 == 0;
+            steps = row_bytes / 64;
             break;
         case kConvHalo8S2:
         case kConvHalo4S2:

@@ -127,6 +127,11 @@ constexpr int kConvHalo8S2 = 3;   // stride-2 halo tiles of 8 x 16 output pixels
 constexpr int kConvHalo4S2 = 4;   // stride-2 halo tiles of 4 x 16 output pixels, 8 waves
 constexpr int kConvHalo4N64K2 = 5;    // stride-1 4 x 16 pixels x 64 channels, 2 groups of 4 waves
 constexpr int kConvHalo4S2N64K2 = 6;  // stride-2 4 x 16 pixels x 64 channels, 2 groups of 4 waves
+// kConvHalo8 with 64-byte channel chunks also where 128-byte chunks apply
+// (C_in * elt >= 512): 64 KB of LDS instead of 112 KB, so two blocks share
+// a CU and one's prologue and epilogue overlap the other's K loop.  (Id 7 is
+// the runtime option that forces the implicit GEMM.)
+constexpr int kConvHalo8C64 = 8;
 struct ConvPlan {
     int variant;      // tiling of a launch over one map
     int splits;
