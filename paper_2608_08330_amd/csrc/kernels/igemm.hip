@@ -228,6 +228,15 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_igemm(GemmArgs a0) {
     const int bt = bid / per_map;
     bid -= bt * per_map;
     const GemmArgs a = batch_args(a0, bt);
+    // upsampling: the u x u output phases of one input tile are neighbours
+    // (same XCD: the input tile is read from its L2, and the phases' writes
+    // fill whole output rows together)
+    int phase = 0;
+    if (DECONV) {
+        const int uu = a.u * a.u;
+        phase = bid % uu;
+        bid /= uu;
+    }
 
     const int Ci = a.Ci;
     const int M = DECONV ? a.Hi * a.Wi : a.Ho * a.Wo;
@@ -242,7 +251,6 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_igemm(GemmArgs a0) {
     const int rest = bid / mt;  // n tile, then split
     const int n_tile = rest % nt;
     const int split = rest / nt;
-    const int phase = DECONV ? int(blockIdx.z) : 0;
     const int m0 = m_tile * BM;
     const int n0 = n_tile * BN;
     const int kt0 = split * KT;
@@ -753,10 +761,11 @@ hipError_t launch_kernel(F kernel, dim3 grid, dim3 block, hipStream_t s, hipEven
 template <typename T, int BM, int BN, int WGM, int WGN, int STAGES, bool DECONV>
 hipError_t launch_cfg(const GemmArgs &a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr) {
     const int M = DECONV ? a.Hi * a.Wi : a.Ho * a.Wo;
-    const unsigned gz = DECONV ? unsigned(a.u * a.u) : 1u;
+    const unsigned phases = DECONV ? unsigned(a.u * a.u) : 1u;
     const unsigned nb = unsigned(a.batch > 1 ? a.batch : 1);
-    const unsigned nx = unsigned((M + BM - 1) / BM) * unsigned((a.N + BN - 1) / BN) * unsigned(a.splits) * nb;
-    hipError_t e = launch_kernel(k_igemm<T, BM, BN, WGM, WGN, STAGES, DECONV>, dim3(nx, 1, gz),
+    const unsigned nx =
+        unsigned((M + BM - 1) / BM) * unsigned((a.N + BN - 1) / BN) * unsigned(a.splits) * phases * nb;
+    hipError_t e = launch_kernel(k_igemm<T, BM, BN, WGM, WGN, STAGES, DECONV>, dim3(nx),
                                  dim3(64 * WGM * WGN), s, e0, a.splits == 1 ? e1 : nullptr, a);
     if (e != hipSuccess || a.splits == 1) return e;
     const int64_t total = int64_t(M) * (a.N / 4);
@@ -789,6 +798,10 @@ hipError_t launch(const GemmArgs &a, hipStream_t s, hipEvent_t e0 = nullptr, hip
                 return rb128 ? launch_halo<T, 8, 128, 4, 2, 128, 1, 1, 4, true>(a, s, e0, e1)
                              : launch_halo<T, 8, 128, 4, 2, 64, 1, 1, 4, false>(a, s, e0, e1);
             case kConvHalo8C64: return launch_halo<T, 8, 128, 4, 2, 64, 1, 1, 4, false>(a, s, e0, e1);
+            case kConvHalo16:
+                return rb128 ? launch_halo<T, 16, 128, 4, 2, 128, 1, 1, 4, true>(a, s, e0, e1)
+                             : launch_halo<T, 16, 128, 4, 2, 64, 1, 1, 4, true>(a, s, e0, e1);
+            case kConvHalo16C64: return launch_halo<T, 16, 128, 4, 2, 64, 1, 1, 4, true>(a, s, e0, e1);
             case kConvHalo4:
                 return rb128 ? launch_halo<T, 4, 128, 2, 2, 128, 1, 1, 3, true>(a, s, e0, e1)
                              : launch_halo<T, 4, 128, 2, 2, 64, 1, 1, 3, true>(a, s, e0, e1);
@@ -823,7 +836,7 @@ ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, in
     (void)Hi;
     (void)Wi;
     const int bk = bf16 ? 32 : 16;  // implicit GEMM K step (64 bytes)
-    ConvPlan p{kConvImplicit, 1, 0, kConvImplicit, 1};
+    ConvPlan p{kConvImplicit, 1, 0, kConvImplicit, 1, kConvImplicit, 1 << 30};
     const int elt = bf16 ? 2 : 4;
     if (stride == 1 && Co % 128 == 0) {
         // 8 x 16-pixel tiles with 8 wavefronts where the grid fills the
@@ -836,7 +849,15 @@ ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, in
         const int t8 = tx * ((Ho + 7) / 8) * nt, t4 = tx * ((Ho + 3) / 4) * nt;
         const int chunk_bytes = ((Ci * elt) % 128 == 0 && Ci * elt >= 512) ? 128 : 64;
         const int chunks = Ci * elt / chunk_bytes;
+        // 16 x 16 tiles for batches whose 16-row tiles cover the CUs, on maps
+        // whose 8-row tiles give at most one block per CU (c5, 8 agents per
+        // launch: 128 x 128 x 256 -> 256 4-7%, 64 x 64 x 256 -> 256 8% faster
+        // than 8-row tiles; 256 x 256 x 128 -> 128, two 8-row blocks per CU
+        // per map, 2-4% slower)
+        const int t16 = ((Wo + 15) / 16) * ((Ho + 15) / 16) * nt;
+        if (t8 <= n_cu) p.wide16_maps = (n_cu + t16 - 1) / t16;
         p.variant_wide = kConvHalo8;
+        p.variant_wide16 = kConvHalo16;
         if (t8 >= n_cu && chunk_bytes == 128) {
             // a map whose 8 x 16 tiles fill the chip by themselves: 64-byte
             // chunks, two blocks per CU (at 128 x 128 x 256 -> 256, 8 maps
@@ -844,6 +865,7 @@ ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, in
             // alone 10% slower; both forms accumulate alike, so the one
             // tiling serves every launch)
             p.variant = p.variant_wide = kConvHalo8C64;
+            p.variant_wide16 = kConvHalo16C64;
         } else if (t8 >= n_cu) {
             p.variant = kConvHalo8;
         } else {
@@ -901,8 +923,13 @@ ConvPlan conv_plan_forced(bool bf16, const ConvPlan &planned, int variant, int s
             steps = row_bytes / (rb128 ? 128 : 64);
             break;
         case kConvHalo8C64:
+        case kConvHalo16C64:
             fits = stride == 1 && Co % 128 == 0 && row_bytes % 64 == 0;
             steps = row_bytes / 64;
+            break;
+        case kConvHalo16:
+            fits = stride == 1 && Co % 128 == 0;
+            steps = row_bytes / (rb128 ? 128 : 64);
             break;
         case kConvHalo8S2:
         case kConvHalo4S2:
@@ -922,7 +949,7 @@ ConvPlan conv_plan_forced(bool bf16, const ConvPlan &planned, int variant, int s
         default: break;
     }
     if (!fits || steps % groups != 0 || steps / groups < 1) return planned;
-    ConvPlan p{variant, 1, 0, variant, 1};
+    ConvPlan p{variant, 1, 0, variant, 1, variant, 1 << 30};
     // a split-K slice holds whole chunks of one wave group's share; the
     // two-group tilings run unsplit
     if (splits > 1 && groups == 1 && steps % splits == 0) p.splits = splits;

@@ -132,6 +132,13 @@ constexpr int kConvHalo4S2N64K2 = 6;  // stride-2 4 x 16 pixels x 64 channels, 2
 // a CU and one's prologue and epilogue overlap the other's K loop.  (Id 7 is
 // the runtime option that forces the implicit GEMM.)
 constexpr int kConvHalo8C64 = 8;
+// Stride-1 halo tiles of 16 x 16 pixels (8 waves of 64 pixels x 64
+// channels): per channel chunk one weight tile serves twice the pixels of
+// the 8-row tiles, for batched launches whose 16-row tiles cover the chip.
+// kConvHalo16 takes 128-byte chunks where kConvHalo8 does; kConvHalo16C64
+// always 64-byte chunks (the accumulation order of kConvHalo8C64).
+constexpr int kConvHalo16 = 9;
+constexpr int kConvHalo16C64 = 10;
 struct ConvPlan {
     int variant;      // tiling of a launch over one map
     int splits;
@@ -143,18 +150,23 @@ struct ConvPlan {
     // bit of the result.
     int variant_wide;
     int wide_maps;
+    // From wide16_maps maps on, tiling variant_wide16 (the same order again).
+    int variant_wide16;
+    int wide16_maps;
 };
 // Kernel variant and K split of one 3x3 conv layer on a GPU with n_cu CUs.
 // Only tilings with one wave group per tile are planned (a second group
 // would sum half of the K chunks apart, another accumulation order).
 ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, int stride, int n_cu);
-// The plan with tiling `variant` (1..6, or 7 = the implicit GEMM) and K split
+// The plan with tiling `variant` (1..6, 8..10, or 7 = the implicit GEMM) and K split
 // `splits` forced where the layer's stride and channels allow it; `planned`
 // elsewhere.  A forced tiling is used for batched launches too.
 ConvPlan conv_plan_forced(bool bf16, const ConvPlan &planned, int variant, int splits, int Ci, int Ho, int Wo,
                           int Co, int stride);
 // The tiling of a launch over `maps` maps.
-inline int conv_variant_for(const ConvPlan &p, int maps) { return maps >= p.wide_maps ? p.variant_wide : p.variant; }
+inline int conv_variant_for(const ConvPlan &p, int maps) {
+    return maps >= p.wide16_maps ? p.variant_wide16 : maps >= p.wide_maps ? p.variant_wide : p.variant;
+}
 // With start / stop events, the first kernel of the convolution records
 // `start` when it begins executing and the last one `stop` when it ends
 // (kernel execution time, without the dispatch gap before it).
