@@ -443,8 +443,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_igemm(GemmArgs a0) {
 // once step s's weights have landed, the loads still allowed in flight are
 // the weights of the next R - 2 steps plus, at taps 1 .. R - 1, the next
 // chunk's patch (issued at tap 0 after the weights of step s + R - 1).
-template <typename T, int TH, int BN, int WGM, int WGN, int RB, int STRIDE, int KG, int R, bool ILV>
-__global__ __launch_bounds__(64 * WGM * WGN * KG) void k_conv3s1(GemmArgs a0) {
+template <typename T, int TH, int BN, int WGM, int WGN, int RB, int STRIDE, int KG, int R, bool ILV, int PB = 2,
+          int WPE = 1>
+__global__ __launch_bounds__(64 * WGM * WGN * KG, WPE) void k_conv3s1(GemmArgs a0) {
     constexpr int NW = WGM * WGN;  // wavefronts per group
     constexpr int EPV = Traits<T>::EPV;
     constexpr int VPR = RB / 16;                 // 16-byte vectors per row and step
@@ -469,7 +470,8 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void k_conv3s1(GemmArgs a0) {
     static_assert(FM * WGM == TH && FN >= 1, "wave layout must tile the block");
 
     static_assert(R >= 3 && R <= 9, "weight ring depth");
-    constexpr int G_BYTES = 2 * A_BYTES + R * B_BYTES;  // LDS of one group
+    static_assert(PB == 1 || PB == 2, "patch buffers");
+    constexpr int G_BYTES = PB * A_BYTES + R * B_BYTES;  // LDS of one group
     static_assert((KG - 1) * NW * 64 * FM * FN * 16 <= KG * G_BYTES, "group reduction must fit in LDS");
     __shared__ __attribute__((aligned(1024))) unsigned char smem[KG * G_BYTES];
 
@@ -485,7 +487,7 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void k_conv3s1(GemmArgs a0) {
     unsigned char *gsmem = smem + grp * G_BYTES;
     const uint32_t lds_base = __builtin_amdgcn_readfirstlane(
         uint32_t(reinterpret_cast<uintptr_t>((lds_void *)gsmem)));
-    const uint32_t lds_b = lds_base + 2 * A_BYTES;
+    const uint32_t lds_b = lds_base + PB * A_BYTES;
 
     int bid = blockIdx.x;
     const int nbx = gridDim.x;
@@ -540,7 +542,7 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void k_conv3s1(GemmArgs a0) {
     // local chunk i of this group is chunk c_begin + grp + KG i of the layer
     auto issue_patch = [&](int chunk) {
         const int c0 = (c_begin + grp + KG * chunk) * BK;
-        const uint32_t dst = lds_base + (chunk & 1) * A_BYTES;
+        const uint32_t dst = lds_base + (PB == 2 ? (chunk & 1) : 0) * A_BYTES;
 #pragma unroll
         for (int j = 0; j < LA; ++j) {
             const void *g = zero;
@@ -573,10 +575,11 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void k_conv3s1(GemmArgs a0) {
     struct Frag {
         uint4 a[KS][FM], b[KS][FN];
     };
-    // step (chunk c, tap t): patch buffer c & 1, weight buffer s % R
+    // step (chunk c, tap t): patch buffer c & 1 (the one buffer with PB =
+    // 1), weight buffer s % R
     auto read_frags = [&](Frag &f, int c, int t, int s) {
-        const unsigned char *pa = gsmem + (c & 1) * A_BYTES;
-        const unsigned char *pb = gsmem + 2 * A_BYTES + (s % R) * B_BYTES;
+        const unsigned char *pa = gsmem + (PB == 2 ? (c & 1) : 0) * A_BYTES;
+        const unsigned char *pb = gsmem + PB * A_BYTES + (s % R) * B_BYTES;
         const int dy = t / 3, dx = t % 3;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
@@ -616,18 +619,43 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void k_conv3s1(GemmArgs a0) {
         constexpr bool last = decltype(lastc)::value;
         constexpr bool more = !(last && t == 8);
         const int s = c * 9 + t;
+        if constexpr (PB == 1 && t == 8 && !last) {
+            // One patch buffer: the next chunk's patch replaces this one
+            // once every wave has read its tap-8 operands (the barrier
+            // below); this step's MFMAs run while it lands.  In flight after
+            // step s + 1's weights: those of steps s + 2 .. s + R - 1.
+            vm_wait<(R - 2) * LB>((R - 2) * LB);
+            lds_reads_done();
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+            issue_patch(c + 1);
+            issue_w(s + R);
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+                for (int i = 0; i < FM; ++i)
+#pragma unroll
+                    for (int j = 0; j < FN; ++j) acc[i][j] = Traits<T>::mma(cur.b[ks][j], cur.a[ks][i], acc[i][j]);
+            // the patch has landed once only step s + R's weights remain
+            vm_wait<LB>(LB);
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+            read_frags(cur, c + 1, 0, s + 1);
+            return;
+        }
         if constexpr (more) {
             // still in flight once step s + 1's weights (and at tap 8 the
             // next patch, issued before them) have landed: the weights of
             // steps s + 2 .. s + R - 1 (fewer near the end) and, at taps
             // 1 .. R - 2, the next chunk's patch
-            if constexpr (!last) vm_wait<(R - 2) * LB + LA>((R - 2) * LB + (t >= 1 && t <= R - 2 ? LA : 0));
+            if constexpr (!last)
+                vm_wait<(R - 2) * LB + LA>((R - 2) * LB + (PB == 2 && t >= 1 && t <= R - 2 ? LA : 0));
             else vm_wait<(R - 2) * LB>((7 - t < R - 2 ? 7 - t : R - 2) * LB);
             lds_reads_done();
             __builtin_amdgcn_s_barrier();
             asm volatile("" ::: "memory");
             if constexpr (!last || t + R < 9) issue_w(s + R);
-            if constexpr (t == 0 && !last) issue_patch(c + 1);
+            if constexpr (PB == 2 && t == 0 && !last) issue_patch(c + 1);
             if constexpr (t < 8) read_frags(nxt, c, t + 1, s + 1);
             else read_frags(nxt, c + 1, 0, s + 1);
         }
@@ -772,12 +800,13 @@ hipError_t launch_cfg(const GemmArgs &a, hipStream_t s, hipEvent_t e0 = nullptr,
     return launch_kernel(k_splitk_reduce<T>, dim3(unsigned((total + 255) / 256), nb), dim3(256), s, nullptr, e1, a);
 }
 
-template <typename T, int TH, int BN, int WGM, int WGN, int RB, int STRIDE, int KG, int R, bool ILV>
+template <typename T, int TH, int BN, int WGM, int WGN, int RB, int STRIDE, int KG, int R, bool ILV, int PB = 2,
+          int WPE = 1>
 hipError_t launch_halo(const GemmArgs &a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr) {
     const unsigned nb = unsigned(a.batch > 1 ? a.batch : 1);
     const unsigned tiles = unsigned((a.Wo + 15) / 16) * unsigned((a.Ho + TH - 1) / TH);
     const unsigned nx = tiles * unsigned(a.N / BN) * unsigned(a.splits) * nb;
-    hipError_t e = launch_kernel(k_conv3s1<T, TH, BN, WGM, WGN, RB, STRIDE, KG, R, ILV>, dim3(nx),
+    hipError_t e = launch_kernel(k_conv3s1<T, TH, BN, WGM, WGN, RB, STRIDE, KG, R, ILV, PB, WPE>, dim3(nx),
                                  dim3(64 * WGM * WGN * KG), s, e0, a.splits == 1 ? e1 : nullptr, a);
     if (e != hipSuccess || a.splits == 1) return e;
     const int64_t total = int64_t(a.Ho) * a.Wo * (a.N / 4);
@@ -807,6 +836,7 @@ hipError_t launch(const GemmArgs &a, hipStream_t s, hipEvent_t e0 = nullptr, hip
                              : launch_halo<T, 4, 128, 2, 2, 64, 1, 1, 3, true>(a, s, e0, e1);
             case kConvHalo8S2: return launch_halo<T, 8, 128, 4, 2, 64, 2, 1, 4, true>(a, s, e0, e1);
             case kConvHalo4S2: return launch_halo<T, 4, 128, 4, 2, 64, 2, 1, 4, true>(a, s, e0, e1);
+            case kConvHalo8S2N256: return launch_halo<T, 8, 256, 4, 2, 64, 2, 1, 4, true>(a, s, e0, e1);
             case kConvHalo4N64K2:
                 return rb128 ? launch_halo<T, 4, 64, 2, 2, 128, 1, 2, 4, true>(a, s, e0, e1)
                              : launch_halo<T, 4, 64, 2, 2, 64, 1, 2, 3, true>(a, s, e0, e1);
@@ -855,9 +885,9 @@ ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, in
         // than 8-row tiles; 256 x 256 x 128 -> 128, two 8-row blocks per CU
         // per map, 2-4% slower)
         const int t16 = ((Wo + 15) / 16) * ((Ho + 15) / 16) * nt;
-        if (t8 <= n_cu) p.wide16_maps = (n_cu + t16 - 1) / t16;
+        if (t8 <= n_cu) p.wider_maps = (n_cu + t16 - 1) / t16;
         p.variant_wide = kConvHalo8;
-        p.variant_wide16 = kConvHalo16;
+        p.variant_wider = kConvHalo16;
         if (t8 >= n_cu && chunk_bytes == 128) {
             // a map whose 8 x 16 tiles fill the chip by themselves: 64-byte
             // chunks, two blocks per CU (at 128 x 128 x 256 -> 256, 8 maps
@@ -865,7 +895,7 @@ ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, in
             // alone 10% slower; both forms accumulate alike, so the one
             // tiling serves every launch)
             p.variant = p.variant_wide = kConvHalo8C64;
-            p.variant_wide16 = kConvHalo16C64;
+            p.variant_wider = kConvHalo16C64;
         } else if (t8 >= n_cu) {
             p.variant = kConvHalo8;
         } else {
@@ -883,6 +913,14 @@ ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, in
         const int tx = (Wo + 15) / 16, nt = Co / 128;
         const int t8 = tx * ((Ho + 7) / 8) * nt;
         p.variant_wide = kConvHalo8S2;
+        if (Co % 256 == 0) {
+            // 256-channel tiles once a batch's tiles cover the CUs (c5, 8
+            // agents per launch: 256 x 256 x 128 -> 128 x 128 x 256 17% and
+            // 128 x 128 x 256 -> 64 x 64 x 256 14% faster than 128-channel
+            // tiles)
+            p.variant_wider = kConvHalo8S2N256;
+            p.wider_maps = (n_cu + t8 / 2 - 1) / (t8 / 2);
+        }
         if (t8 >= n_cu) {
             p.variant = kConvHalo8S2;
         } else {
@@ -930,6 +968,10 @@ ConvPlan conv_plan_forced(bool bf16, const ConvPlan &planned, int variant, int s
         case kConvHalo16:
             fits = stride == 1 && Co % 128 == 0;
             steps = row_bytes / (rb128 ? 128 : 64);
+            break;
+        case kConvHalo8S2N256:
+            fits = stride == 2 && Co % 256 == 0 && row_bytes % 64 == 0;
+            steps = row_bytes / 64;
             break;
         case kConvHalo8S2:
         case kConvHalo4S2:

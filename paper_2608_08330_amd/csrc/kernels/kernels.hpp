@@ -139,6 +139,10 @@ constexpr int kConvHalo8C64 = 8;
 // always 64-byte chunks (the accumulation order of kConvHalo8C64).
 constexpr int kConvHalo16 = 9;
 constexpr int kConvHalo16C64 = 10;
+// Stride-2 halo tiles of 8 x 16 output pixels x 256 channels (8 waves of
+// 32 pixels x 128 channels): the input patch of a tile is staged once for
+// all 256 output channels instead of once per 128.
+constexpr int kConvHalo8S2N256 = 11;
 struct ConvPlan {
     int variant;      // tiling of a launch over one map
     int splits;
@@ -150,22 +154,23 @@ struct ConvPlan {
     // bit of the result.
     int variant_wide;
     int wide_maps;
-    // From wide16_maps maps on, tiling variant_wide16 (the same order again).
-    int variant_wide16;
-    int wide16_maps;
+    // From wider_maps maps on, tiling variant_wider (the same order again).
+    // wider_maps >= wide_maps.
+    int variant_wider;
+    int wider_maps;
 };
 // Kernel variant and K split of one 3x3 conv layer on a GPU with n_cu CUs.
 // Only tilings with one wave group per tile are planned (a second group
 // would sum half of the K chunks apart, another accumulation order).
 ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, int stride, int n_cu);
-// The plan with tiling `variant` (1..6, 8..10, or 7 = the implicit GEMM) and K split
+// The plan with tiling `variant` (1..6, 8..11, or 7 = the implicit GEMM) and K split
 // `splits` forced where the layer's stride and channels allow it; `planned`
 // elsewhere.  A forced tiling is used for batched launches too.
 ConvPlan conv_plan_forced(bool bf16, const ConvPlan &planned, int variant, int splits, int Ci, int Ho, int Wo,
                           int Co, int stride);
 // The tiling of a launch over `maps` maps.
 inline int conv_variant_for(const ConvPlan &p, int maps) {
-    return maps >= p.wide16_maps ? p.variant_wide16 : maps >= p.wide_maps ? p.variant_wide : p.variant;
+    return maps >= p.wider_maps ? p.variant_wider : maps >= p.wide_maps ? p.variant_wide : p.variant;
 }
 // With start / stop events, the first kernel of the convolution records
 // `start` when it begins executing and the last one `stop` when it ends
