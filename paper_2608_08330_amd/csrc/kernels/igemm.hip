@@ -443,9 +443,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_igemm(GemmArgs a0) {
 // once step s's weights have landed, the loads still allowed in flight are
 // the weights of the next R - 2 steps plus, at taps 1 .. R - 1, the next
 // chunk's patch (issued at tap 0 after the weights of step s + R - 1).
-template <typename T, int TH, int BN, int WGM, int WGN, int RB, int STRIDE, int KG, int R, bool ILV, int PB = 2,
-          int WPE = 1>
-__global__ __launch_bounds__(64 * WGM * WGN * KG, WPE) void k_conv3s1(GemmArgs a0) {
+template <typename T, int TH, int BN, int WGM, int WGN, int RB, int STRIDE, int KG, int R, bool ILV>
+__global__ __launch_bounds__(64 * WGM * WGN * KG) void k_conv3s1(GemmArgs a0) {
     constexpr int NW = WGM * WGN;  // wavefronts per group
     constexpr int EPV = Traits<T>::EPV;
     constexpr int VPR = RB / 16;                 // 16-byte vectors per row and step
@@ -470,8 +469,7 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG, WPE) void k_conv3s1(GemmArgs a
     static_assert(FM * WGM == TH && FN >= 1, "wave layout must tile the block");
 
     static_assert(R >= 3 && R <= 9, "weight ring depth");
-    static_assert(PB == 1 || PB == 2, "patch buffers");
-    constexpr int G_BYTES = PB * A_BYTES + R * B_BYTES;  // LDS of one group
+    constexpr int G_BYTES = 2 * A_BYTES + R * B_BYTES;  // LDS of one group
     static_assert((KG - 1) * NW * 64 * FM * FN * 16 <= KG * G_BYTES, "group reduction must fit in LDS");
     __shared__ __attribute__((aligned(1024))) unsigned char smem[KG * G_BYTES];
 
@@ -487,7 +485,7 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG, WPE) void k_conv3s1(GemmArgs a
     unsigned char *gsmem = smem + grp * G_BYTES;
     const uint32_t lds_base = __builtin_amdgcn_readfirstlane(
         uint32_t(reinterpret_cast<uintptr_t>((lds_void *)gsmem)));
-    const uint32_t lds_b = lds_base + PB * A_BYTES;
+    const uint32_t lds_b = lds_base + 2 * A_BYTES;
 
     int bid = blockIdx.x;
     const int nbx = gridDim.x;
@@ -542,7 +540,7 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG, WPE) void k_conv3s1(GemmArgs a
     // local chunk i of this group is chunk c_begin + grp + KG i of the layer
     auto issue_patch = [&](int chunk) {
         const int c0 = (c_begin + grp + KG * chunk) * BK;
-        const uint32_t dst = lds_base + (PB == 2 ? (chunk & 1) : 0) * A_BYTES;
+        const uint32_t dst = lds_base + (chunk & 1) * A_BYTES;
 #pragma unroll
         for (int j = 0; j < LA; ++j) {
             const void *g = zero;
@@ -575,11 +573,10 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG, WPE) void k_conv3s1(GemmArgs a
     struct Frag {
         uint4 a[KS][FM], b[KS][FN];
     };
-    // step (chunk c, tap t): patch buffer c & 1 (the one buffer with PB =
-    // 1), weight buffer s % R
+    // step (chunk c, tap t): patch buffer c & 1, weight buffer s % R
     auto read_frags = [&](Frag &f, int c, int t, int s) {
-        const unsigned char *pa = gsmem + (PB == 2 ? (c & 1) : 0) * A_BYTES;
-        const unsigned char *pb = gsmem + PB * A_BYTES + (s % R) * B_BYTES;
+        const unsigned char *pa = gsmem + (c & 1) * A_BYTES;
+        const unsigned char *pb = gsmem + 2 * A_BYTES + (s % R) * B_BYTES;
         const int dy = t / 3, dx = t % 3;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
@@ -619,43 +616,18 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG, WPE) void k_conv3s1(GemmArgs a
         constexpr bool last = decltype(lastc)::value;
         constexpr bool more = !(last && t == 8);
         const int s = c * 9 + t;
-        if constexpr (PB == 1 && t == 8 && !last) {
-            // One patch buffer: the next chunk's patch replaces this one
-            // once every wave has read its tap-8 operands (the barrier
-            // below); this step's MFMAs run while it lands.  In flight after
-            // step s + 1's weights: those of steps s + 2 .. s + R - 1.
-            vm_wait<(R - 2) * LB>((R - 2) * LB);
-            lds_reads_done();
-            __builtin_amdgcn_s_barrier();
-            asm volatile("" ::: "memory");
-            issue_patch(c + 1);
-            issue_w(s + R);
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-                for (int i = 0; i < FM; ++i)
-#pragma unroll
-                    for (int j = 0; j < FN; ++j) acc[i][j] = Traits<T>::mma(cur.b[ks][j], cur.a[ks][i], acc[i][j]);
-            // the patch has landed once only step s + R's weights remain
-            vm_wait<LB>(LB);
-            __builtin_amdgcn_s_barrier();
-            asm volatile("" ::: "memory");
-            read_frags(cur, c + 1, 0, s + 1);
-            return;
-        }
         if constexpr (more) {
             // still in flight once step s + 1's weights (and at tap 8 the
             // next patch, issued before them) have landed: the weights of
             // steps s + 2 .. s + R - 1 (fewer near the end) and, at taps
             // 1 .. R - 2, the next chunk's patch
-            if constexpr (!last)
-                vm_wait<(R - 2) * LB + LA>((R - 2) * LB + (PB == 2 && t >= 1 && t <= R - 2 ? LA : 0));
+            if constexpr (!last) vm_wait<(R - 2) * LB + LA>((R - 2) * LB + (t >= 1 && t <= R - 2 ? LA : 0));
             else vm_wait<(R - 2) * LB>((7 - t < R - 2 ? 7 - t : R - 2) * LB);
             lds_reads_done();
             __builtin_amdgcn_s_barrier();
             asm volatile("" ::: "memory");
             if constexpr (!last || t + R < 9) issue_w(s + R);
-            if constexpr (PB == 2 && t == 0 && !last) issue_patch(c + 1);
+            if constexpr (t == 0 && !last) issue_patch(c + 1);
             if constexpr (t < 8) read_frags(nxt, c, t + 1, s + 1);
             else read_frags(nxt, c + 1, 0, s + 1);
         }
@@ -800,13 +772,12 @@ hipError_t launch_cfg(const GemmArgs &a, hipStream_t s, hipEvent_t e0 = nullptr,
     return launch_kernel(k_splitk_reduce<T>, dim3(unsigned((total + 255) / 256), nb), dim3(256), s, nullptr, e1, a);
 }
 
-template <typename T, int TH, int BN, int WGM, int WGN, int RB, int STRIDE, int KG, int R, bool ILV, int PB = 2,
-          int WPE = 1>
+template <typename T, int TH, int BN, int WGM, int WGN, int RB, int STRIDE, int KG, int R, bool ILV>
 hipError_t launch_halo(const GemmArgs &a, hipStream_t s, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr) {
     const unsigned nb = unsigned(a.batch > 1 ? a.batch : 1);
     const unsigned tiles = unsigned((a.Wo + 15) / 16) * unsigned((a.Ho + TH - 1) / TH);
     const unsigned nx = tiles * unsigned(a.N / BN) * unsigned(a.splits) * nb;
-    hipError_t e = launch_kernel(k_conv3s1<T, TH, BN, WGM, WGN, RB, STRIDE, KG, R, ILV, PB, WPE>, dim3(nx),
+    hipError_t e = launch_kernel(k_conv3s1<T, TH, BN, WGM, WGN, RB, STRIDE, KG, R, ILV>, dim3(nx),
                                  dim3(64 * WGM * WGN * KG), s, e0, a.splits == 1 ? e1 : nullptr, a);
     if (e != hipSuccess || a.splits == 1) return e;
     const int64_t total = int64_t(a.Ho) * a.Wo * (a.N / 4);
@@ -890,10 +861,10 @@ ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, in
         p.variant_wider = kConvHalo16;
         if (t8 >= n_cu && chunk_bytes == 128) {
             // a map whose 8 x 16 tiles fill the chip by themselves: 64-byte
-            // chunks, two blocks per CU (at 128 x 128 x 256 -> 256, 8 maps
-            // per launch: 7% faster per map than 128-byte chunks, one map
-            // alone 10% slower; both forms accumulate alike, so the one
-            // tiling serves every launch)
+            // chunks (at 128 x 128 x 256 -> 256, 8 maps per launch: 7%
+            // faster per map than 128-byte chunks, one map alone 10%
+            // slower; the batched frame decides, and all launches of a
+            // layer must accumulate alike)
             p.variant = p.variant_wide = kConvHalo8C64;
             p.variant_wider = kConvHalo16C64;
         } else if (t8 >= n_cu) {

@@ -128,8 +128,8 @@ constexpr int kConvHalo4S2 = 4;   // stride-2 halo tiles of 4 x 16 output pixels
 constexpr int kConvHalo4N64K2 = 5;    // stride-1 4 x 16 pixels x 64 channels, 2 groups of 4 waves
 constexpr int kConvHalo4S2N64K2 = 6;  // stride-2 4 x 16 pixels x 64 channels, 2 groups of 4 waves
 // kConvHalo8 with 64-byte channel chunks also where 128-byte chunks apply
-// (C_in * elt >= 512): 64 KB of LDS instead of 112 KB, so two blocks share
-// a CU and one's prologue and epilogue overlap the other's K loop.  (Id 7 is
+// (C_in * elt >= 512): twice the steps with half the operand bytes each,
+// which measured faster in launches over several agents' maps.  (Id 7 is
 // the runtime option that forces the implicit GEMM.)
 constexpr int kConvHalo8C64 = 8;
 // Stride-1 halo tiles of 16 x 16 pixels (8 waves of 64 pixels x 64
