@@ -186,9 +186,10 @@ typedef struct rtcc_runtime_opts {
      * with 64-byte channel chunks at any channel count, 9: 16 x 16 x 128,
      * 10: 9 with 64-byte chunks, 11: the stride-2 8 x 16 x 256) on every
      * layer whose stride and channels it supports, the plan elsewhere; 7 =
-     * the implicit GEMM on every layer.  conv_splits (0 or 1: none) splits
-     * the K loop of the forced layers where it divides evenly.  Values
-     * outside [0, 11]: RTCC_E_ARG. */
+     * the implicit GEMM on every layer, 12 = the implicit GEMM with 256 x
+     * 128 tiles on every layer with 128k output channels.  conv_splits (0
+     * or 1: none) splits the K loop of the forced layers where it divides
+     * evenly.  Values outside [0, 12]: RTCC_E_ARG. */
     int32_t conv_variant;
     int32_t conv_splits;
     rtcc_dev_alloc_fn dev_alloc;  /* NULL: hipMalloc / hipFree                     */
@@ -434,11 +435,11 @@ RTCC_API rtcc_status rtcc_node_times(rtcc_ctx *ctx, float *ms, int32_t *n);
 RTCC_API rtcc_status rtcc_node_count(rtcc_ctx *ctx, int32_t *n);
 
 /* Kernel tiling of 3x3 conv layer `layer` (0-based over all stages):
- * plan[0] = 0 implicit GEMM, 1..6 and 8..11 the halo tilings of
- * rtcc_runtime_opts.conv_variant for a launch over one agent's map (a
- * batched launch over several agents may use a wider tiling of the same
- * accumulation order: 1 or 9 for 2, 3 or 11 for 3 and 4, 10 for 8);
- * plan[1] = K slices (1 = unsplit).  plan:
+ * plan[0] = 0 implicit GEMM, 12 its 256 x 128 tiles, 1..6 and 8..11 the
+ * halo tilings of rtcc_runtime_opts.conv_variant for a launch over one
+ * agent's map (a batched launch over several agents may use a wider tiling
+ * of the same accumulation order: 1 or 9 for 2, 3 or 11 for 3 and 4, 10
+ * for 8); plan[1] = K slices (1 = unsplit).  plan:
  * caller-owned int32_t[2].  Errors: RTCC_E_ARG (NULL or layer out of
  * range), RTCC_E_STATE (the host test library has no kernels). */
 RTCC_API rtcc_status rtcc_conv_plan(rtcc_ctx *ctx, int32_t layer, int32_t *plan);

@@ -26,8 +26,8 @@ rtcc_status Controller::create(const rtcc_model_desc *d, const void *weights, si
         return fail(RTCC_E_ARG, "premature_tol_s must be finite and >= 0");
     if ((o.use_graphs != 0 && o.use_graphs != 1) || (o.node_timing != 0 && o.node_timing != 1))
         return fail(RTCC_E_ARG, "use_graphs and node_timing must be 0 or 1");
-    if (o.conv_variant < 0 || o.conv_variant > 11 || o.conv_splits < 0 || o.conv_splits > 64)
-        return fail(RTCC_E_ARG, "conv_variant must be in [0, 11] and conv_splits in [0, 64]");
+    if (o.conv_variant < 0 || o.conv_variant > 12 || o.conv_splits < 0 || o.conv_splits > 64)
+        return fail(RTCC_E_ARG, "conv_variant must be in [0, 12] and conv_splits in [0, 64]");
     if ((o.dev_alloc == nullptr) != (o.dev_free == nullptr))
         return fail(RTCC_E_ARG, "dev_alloc and dev_free must be given together");
     opts_ = o;

@@ -143,6 +143,9 @@ constexpr int kConvHalo16C64 = 10;
 // 32 pixels x 128 channels): the input patch of a tile is staged once for
 // all 256 output channels instead of once per 128.
 constexpr int kConvHalo8S2N256 = 11;
+// The implicit GEMM with tiles of 256 pixels x 128 channels and a 3-stage
+// ring (72 KB of LDS, two blocks per CU).
+constexpr int kConvImplicit256 = 12;
 struct ConvPlan {
     int variant;      // tiling of a launch over one map
     int splits;
@@ -163,7 +166,7 @@ struct ConvPlan {
 // Only tilings with one wave group per tile are planned (a second group
 // would sum half of the K chunks apart, another accumulation order).
 ConvPlan conv_plan(bool bf16, int Hi, int Wi, int Ci, int Ho, int Wo, int Co, int stride, int n_cu);
-// The plan with tiling `variant` (1..6, 8..11, or 7 = the implicit GEMM) and K split
+// The plan with tiling `variant` (1..6, 8..12, or 7 = the implicit GEMM) and K split
 // `splits` forced where the layer's stride and channels allow it; `planned`
 // elsewhere.  A forced tiling is used for batched launches too.
 ConvPlan conv_plan_forced(bool bf16, const ConvPlan &planned, int variant, int splits, int Ci, int Ho, int Wo,

@@ -200,7 +200,7 @@ def test_branch_states_follow_the_device():
         assert all(R.rtcc_get_branch_state(ctx, j) == R.RTCC_FINISHED for j in range(cfg["K"]))
 
 
-@pytest.mark.parametrize("variant", [1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11])
+@pytest.mark.parametrize("variant", [1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12])
 @pytest.mark.parametrize("splits", [0, 2])
 def test_forced_conv_tilings(variant, splits):
     """Each 3x3-conv tiling (and split-K) forced on every layer it supports,

@@ -91,14 +91,15 @@ def test_c5_every_conv_layer_and_upsampling(c5, agent):
 
 def test_c5_conv_plan(c5):
     """The tilings the planner gives the 13 c5 layers (256 CUs): the
-    64-channel stride-2 entry as the implicit GEMM, stage 0 as 8-row
+    64-channel stride-2 entry as the implicit GEMM with 256-pixel tiles,
+    stage 0 as 8-row
     tiles, the stage-1 entry as 8-row stride-2 tiles, stage 1 as 8-row tiles
     with 64-byte channel chunks, the stage-2 entry and stage 2 as 4-row
     tiles (their batched launches take the 8-row forms of the same
     accumulation order); no layer split over its K loop."""
     plans = [R.rtcc_conv_plan(c5["ctx"], l) for l in range(13)]
     _say("  plans %s" % plans)
-    assert plans == [(v, 1) for v in (0, 1, 1, 3, 8, 8, 8, 8, 4, 2, 2, 2, 2)]
+    assert plans == [(v, 1) for v in (12, 1, 1, 3, 8, 8, 8, 8, 4, 2, 2, 2, 2)]
 
 
 def test_c5_fusion_head_and_decode(c5):
