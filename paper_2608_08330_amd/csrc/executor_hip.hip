@@ -179,6 +179,11 @@ class HipExecutor : public Executor {
         }
         HIP_TRY(hipHostMalloc(reinterpret_cast<void **>(&h_rec), n_anchor_ * 9 * 4, hipHostMallocDefault));
         HIP_TRY(hipHostMalloc(reinterpret_cast<void **>(&h_small), 64, hipHostMallocDefault));
+        // the frame's counts and first records, written by the last kernel
+        // of the post-join work (coherent: read by the host once the join
+        // stream has passed that kernel)
+        export_first_ = int(std::min(nms_max_ > 0 ? size_t(nms_max_) : n_anchor_, kFirstRecords));
+        HIP_TRY(hipHostMalloc(&h_export, 64 + size_t(export_first_) * 36, hipHostMallocCoherent));
         boxes_.resize(n_anchor_ * 7);
         scores_.resize(n_anchor_);
         aidx_.resize(n_anchor_);
@@ -287,8 +292,8 @@ class HipExecutor : public Executor {
             b.host_input = !it.device_src;
             HIP_TRY(prepare_branch(b, ls));
         }
-        // ... and after the frame's canvas clear
-        if (clear_pending_) HIP_TRY(hipStreamWaitEvent(ls, ev_clear_, 0));
+        // ... and (from its second launch on) after the frame's canvas clear
+        hipEvent_t clear_ev = clear_pending_ ? ev_clear_ : nullptr;
         idle_ = false;
         // The group's launches serve every member: the first member's events
         // time them, mark their start and their end for all.
@@ -304,7 +309,7 @@ class HipExecutor : public Executor {
         // the encoders as one sequence of launches on ls: the pillar stage
         // and then every backbone layer over the whole group
         auto encoders = [&](hipStream_t c, bool t) {
-            rtcc_status r = enqueue_pillars(agents, m, c, t, err);
+            rtcc_status r = enqueue_pillars(agents, m, c, t, clear_ev, err);
             return r == RTCC_OK ? enqueue_backbone(agents, m, c, t, err) : r;
         };
         if (graphs) {
@@ -323,9 +328,17 @@ class HipExecutor : public Executor {
                 if (p_.d.warp_in_branch)
                     for (int e = 0; e < 6; ++e) put(kb, b.affine[e]);
             }
-            st = run_graph_or_eager(m == 1 ? lead.pillar_graph : group_pillar_graph_, kp, ls,
-                                    [&](hipStream_t c) { return enqueue_pillars(agents, m, c, false, err); },
-                                    err);
+            // a captured graph cannot wait on the clear inside: it waits
+            // before the graph launch
+            Graph &pg = m == 1 ? lead.pillar_graph : group_pillar_graph_;
+            if (graph_runs(pg, kp)) {
+                if (clear_ev) HIP_TRY(hipStreamWaitEvent(ls, clear_ev, 0));
+                st = run_graph(pg, kp, ls,
+                               [&](hipStream_t c) { return enqueue_pillars(agents, m, c, false, nullptr, err); }, err);
+            } else {
+                pg.seen = kp;
+                st = enqueue_pillars(agents, m, ls, false, clear_ev, err);
+            }
             if (st == RTCC_OK)
                 st = run_graph(m == 1 ? lead.graph : group_graph_, kb, ls,
                                [&](hipStream_t c) { return enqueue_backbone(agents, m, c, false, err); }, err);
@@ -381,16 +394,11 @@ class HipExecutor : public Executor {
             s = enqueue_post(affine, poses, js, timing, err);
         }
         if (s != RTCC_OK) return s;
-        int32_t *hs = reinterpret_cast<int32_t *>(h_small);
-        HIP_TRY(hipMemcpyAsync(hs, d_count, 4, hipMemcpyDeviceToHost, js));
-        if (nms_max_ > 0) HIP_TRY(hipMemcpyAsync(hs + 1, d_nms_count, 4, hipMemcpyDeviceToHost, js));
-        // the first records come back with the counts (one round trip in
-        // the common case), the rest, if any, after them
-        const void *recs = nms_max_ > 0 ? d_nms_out : d_rec;
-        const size_t cap = nms_max_ > 0 ? size_t(nms_max_) : n_anchor_;
-        const size_t first = std::min(cap, kFirstRecords);
-        HIP_TRY(hipMemcpyAsync(h_rec, recs, first * 36, hipMemcpyDeviceToHost, js));
+        // the counts and the first records are in h_export once the stream
+        // has passed the post-join work (no copy call in the common case);
+        // the rest, if any, are copied after them
         HIP_TRY(spin_sync(js));
+        const int32_t *hs = static_cast<const int32_t *>(h_export);
         const int64_t decoded = hs[0];
         const int64_t count = nms_max_ > 0 ? hs[1] : decoded;
         if (decoded < 0 || size_t(decoded) > n_anchor_ || count < 0 || count > decoded ||
@@ -398,14 +406,17 @@ class HipExecutor : public Executor {
             err = "decode or NMS produced an out-of-range count";
             return RTCC_E_INTERNAL;
         }
+        const size_t first = size_t(export_first_);
+        const float *head_recs = reinterpret_cast<const float *>(static_cast<const char *>(h_export) + 64);
         if (size_t(count) > first) {
+            const void *recs = nms_max_ > 0 ? d_nms_out : d_rec;
             HIP_TRY(hipMemcpyAsync(h_rec + first * 9, static_cast<const char *>(recs) + first * 36,
                                    (size_t(count) - first) * 36, hipMemcpyDeviceToHost, js));
             HIP_TRY(spin_sync(js));
         }
         idle_ = true;  // every stream's work of the frame has completed
         for (int64_t i = 0; i < count; ++i) {
-            const float *r = h_rec + i * 9;
+            const float *r = size_t(i) < first ? head_recs + i * 9 : h_rec + i * 9;
             std::memcpy(&boxes_[i * 7], r, 7 * sizeof(float));
             scores_[i] = r[7];
             std::memcpy(&aidx_[i], &r[8], 4);
@@ -479,7 +490,7 @@ class HipExecutor : public Executor {
                 HIP_TRY(hipEventRecord(e0, s));
                 rtcc_status st;
                 if (k < p_.K) {
-                    st = enqueue_pillars(&k, 1, s, false, err);
+                    st = enqueue_pillars(&k, 1, s, false, nullptr, err);
                     if (st == RTCC_OK) st = enqueue_backbone(&k, 1, s, false, err);
                 } else {
                     st = enqueue_post(last_affine_, last_poses_, s, false, err);
@@ -638,9 +649,13 @@ class HipExecutor : public Executor {
     template <class F>
     rtcc_status run_graph_or_eager(Graph &gr, const std::vector<unsigned char> &key, hipStream_t s, F &&enqueue,
                                    std::string &err) {
-        if ((gr.x && gr.key == key) || gr.seen == key) return run_graph(gr, key, s, enqueue, err);
+        if (graph_runs(gr, key)) return run_graph(gr, key, s, enqueue, err);
         gr.seen = key;
         return enqueue(s);
+    }
+    // whether run_graph_or_eager runs the graph for this key
+    static bool graph_runs(const Graph &gr, const std::vector<unsigned char> &key) {
+        return (gr.x && gr.key == key) || gr.seen == key;
     }
 
     struct Branch {
@@ -707,7 +722,11 @@ class HipExecutor : public Executor {
     // every launch): cell ids, scans, scatter, PFN canvas.  With timing, each
     // member's node times for them are those of the first member's ev[1] /
     // ev[2] / ev[3].
-    rtcc_status enqueue_pillars(const int *agents, int m, hipStream_t s, bool timing, std::string &err) {
+    // With clear_ev, the launches after the first wait for it (the frame's
+    // canvas clear reads the members' last pillar lists, which bin_scatter
+    // and pillar_lists rewrite; bin_count runs beside it).
+    rtcc_status enqueue_pillars(const int *agents, int m, hipStream_t s, bool timing, hipEvent_t clear_ev,
+                                std::string &err) {
         const Plan &p = p_;
         const int n_cells = p.H * p.W;
         kern::PillarGroup grp{};
@@ -733,6 +752,7 @@ class HipExecutor : public Executor {
         // (prepare_branch).
         for (int j = 0; j < m; ++j) br_[agents[j]].pillars_clean = false;
         HIP_TRY(kern::bin_count(grp, g, s));
+        if (clear_ev) HIP_TRY(hipStreamWaitEvent(s, clear_ev, 0));
         HIP_TRY(kern::bin_scatter(grp, s));
         HIP_TRY(kern::tile_sort(grp, p.d.max_points_per_pillar, s));
         HIP_TRY(kern::pillar_lists(grp, s));
@@ -1010,6 +1030,10 @@ class HipExecutor : public Executor {
             HIP_TRY(kern::rotated_nms(na, int64_t(n_anchor_), s));
         }
         if (timing) HIP_TRY(hipEventRecord(post_ev_[4], s));
+        HIP_TRY(kern::export_results(static_cast<const int32_t *>(d_count),
+                                     nms_max_ > 0 ? static_cast<const int32_t *>(d_nms_count) : nullptr,
+                                     static_cast<const float *>(nms_max_ > 0 ? d_nms_out : d_rec), export_first_,
+                                     h_export, s));
         return RTCC_OK;
     }
 
@@ -1185,6 +1209,7 @@ class HipExecutor : public Executor {
         }
         if (h_rec) (void)hipHostFree(h_rec);
         if (h_small) (void)hipHostFree(h_small);
+        if (h_export) (void)hipHostFree(h_export);
         if (join_stream_ && own_join_stream_) (void)hipStreamDestroy(join_stream_);
         if (copy_stream_) (void)hipStreamDestroy(copy_stream_);
         if (aux_stream_) (void)hipStreamDestroy(aux_stream_);
@@ -1210,6 +1235,8 @@ class HipExecutor : public Executor {
     void *d_nms_mask_t = nullptr, *d_nms_partial = nullptr, *d_nms_colrows = nullptr, *d_nms_colcount = nullptr;
     float *h_rec = nullptr;
     void *h_small = nullptr;
+    void *h_export = nullptr;  // counts + first records of the frame (export_results)
+    int export_first_ = 0;
     size_t n_anchor_ = 0;
     std::vector<float> boxes_, scores_;
     std::vector<int32_t> aidx_;

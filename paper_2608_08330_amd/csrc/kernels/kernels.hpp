@@ -245,6 +245,13 @@ struct DecodeArgs {
 };
 constexpr int kDecodeTile = 1024;
 hipError_t decode(const DecodeArgs &a, hipStream_t s);
+// The frame's result into pinned host memory: words 0 and 1 of `host` the
+// counts *count0 and *count1 (0 without count1), and from byte 64 the first
+// min(*count1 or *count0, first) 36-byte records of `recs`; written with
+// vector stores and fenced at system scope, so the host reads them once
+// the stream has passed the kernel.
+hipError_t export_results(const int32_t *count0, const int32_t *count1, const float *recs, int first, void *host,
+                          hipStream_t s);
 
 // Rotated NMS of the decoded records (see nms.hip).
 constexpr int kNmsMaxCandidates = 16384;

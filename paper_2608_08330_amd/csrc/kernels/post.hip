@@ -497,5 +497,26 @@ hipError_t decode(const DecodeArgs &a, hipStream_t s) {
     return hipGetLastError();
 }
 
+// One block: the counts, then the records as 4-byte words.
+__global__ __launch_bounds__(256) void k_export(const int32_t *count0, const int32_t *count1, const uint32_t *recs,
+                                                int first, uint32_t *host) {
+    const int32_t c0 = *count0, c1 = count1 ? *count1 : 0;
+    const int32_t n = count1 ? c1 : c0;
+    const int words = (n < 0 ? 0 : n < first ? n : first) * 9;
+    for (int i = int(threadIdx.x); i < words; i += 256) host[16 + i] = recs[i];
+    if (threadIdx.x == 0) {
+        host[0] = uint32_t(c0);
+        host[1] = uint32_t(c1);
+    }
+    __threadfence_system();
+}
+
+hipError_t export_results(const int32_t *count0, const int32_t *count1, const float *recs, int first, void *host,
+                          hipStream_t s) {
+    k_export<<<1, 256, 0, s>>>(count0, count1, reinterpret_cast<const uint32_t *>(recs), first,
+                               static_cast<uint32_t *>(host));
+    return hipGetLastError();
+}
+
 }  // namespace kern
 }  // namespace rtcc
