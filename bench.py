@@ -44,10 +44,10 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 # kernel source it was taken on; after a change it reads null until re-taken.
 MEASURED_TRAFFIC = {
     # per 8-agent launch of a conv layer (averaged over the 13 layers)
-    "conv": dict(src="paper_2608_08330_amd/csrc/kernels/igemm.hip", bytes=154.5e6,
-                 sha256="f5545b4225c4f5eda113274dea7dc1c4aa1dde46f11aae94b4de9414aa466bd5"),
-    "warp_fuse": dict(src="paper_2608_08330_amd/csrc/kernels/post.hip", bytes=471.4e6,
-                      sha256="3dd695761a7ddeb2490129b0aded0e14dffcbbacb69f9ef0ac79eb63c8d0a814"),
+    "conv": dict(src="paper_2608_08330_amd/csrc/kernels/igemm.hip", bytes=171.2e6,
+                 sha256="2983a7cfa99752fb651dd83c81099c82f17027d4e3059ede9743b71d0fca2ef0"),
+    "warp_fuse": dict(src="paper_2608_08330_amd/csrc/kernels/post.hip", bytes=471.0e6,
+                      sha256="b870ed95289aecf1a7bc1ce8e7f7670f9b28115f3b8183885f4f303359713141"),
     # per 8-agent launch chain of the pillar stage (five kernels)
     "pillar": dict(src="paper_2608_08330_amd/csrc/kernels/pillar.hip", bytes=195e6,
                    sha256="75547fe4e96df6793946122f770939c49c0334a4250e7b36b154152a2ca40586"),
