@@ -225,27 +225,32 @@ class HipExecutor : public Executor {
             HIP_TRY(hipStreamSynchronize(join_stream_));
             idle_ = true;
         }
-        clear_pending_ = false;
         HIP_TRY(hipEventRecord(ev_frame0_, compute_stream_for_join()));
-        // The last frame's canvas pillars (readable until now) go back to
-        // zero at the start of the frame, in one launch for every branch on
-        // the join stream, which the stream of every encoder launch of the
-        // frame then waits for: ahead of the branch's next encoder, normally
-        // long before its completion event.
+        for (Branch &b : br_) b.dispatched = false;
+        // canvases the last join did not clear (an abandoned frame)
+        HIP_TRY(clear_dirty_canvases(false));
+        return RTCC_OK;
+    }
+
+    // The last frame's canvas pillars back to zero, in one launch for every
+    // branch on the join stream, which the stream of every encoder launch of
+    // the next frame then waits for (from its pillar stage's second launch
+    // on).  after_join: the branches' canvases stay readable as tensors
+    // (rebuilt from their pillar lists).
+    hipError_t clear_dirty_canvases(bool after_join) {
         int dirty[kern::kMaxGroup];
         int nd = 0;
-        for (int k = 0; k < p_.K; ++k) {
-            br_[k].dispatched = false;
+        for (int k = 0; k < p_.K; ++k)
             if (br_[k].canvas_dirty) dirty[nd++] = k;
+        if (nd == 0) return hipSuccess;
+        hipError_t e = clear_canvases(dirty, nd, join_stream_);
+        if (e != hipSuccess) return e;
+        for (int j = 0; j < nd; ++j) br_[dirty[j]].canvas_consumed = after_join;
+        if (o_.exec != RTCC_EXEC_SERIAL) {
+            e = hipEventRecord(ev_clear_, join_stream_);
+            if (e == hipSuccess) clear_pending_ = true;
         }
-        if (nd > 0) {
-            HIP_TRY(clear_canvases(dirty, nd, join_stream_));
-            if (o_.exec != RTCC_EXEC_SERIAL) {
-                HIP_TRY(hipEventRecord(ev_clear_, join_stream_));
-                clear_pending_ = true;
-            }
-        }
-        return RTCC_OK;
+        return e;
     }
 
     rtcc_status dispatch(const DispatchItem *items, int m, std::string &err) override {
@@ -350,6 +355,7 @@ class HipExecutor : public Executor {
         for (int j = 0; j < m; ++j) {
             Branch &b = br_[agents[j]];
             b.canvas_dirty = true;  // the encoder writes this frame's pillars
+            b.canvas_consumed = false;
             b.dispatched = true;
         }
         return RTCC_OK;
@@ -421,6 +427,10 @@ class HipExecutor : public Executor {
             scores_[i] = r[7];
             std::memcpy(&aidx_[i], &r[8], 4);
         }
+        // The GPU is idle until the caller's next frame: its canvas pillars go
+        // back to zero now, not at the next frame's start (the canvas tensor
+        // is rebuilt when read).
+        HIP_TRY(clear_dirty_canvases(true));
         float ms = 0.f;
         HIP_TRY(hipEventElapsedTime(&ms, ev_frame0_, ev_head_));
         out->count = count;
@@ -442,7 +452,7 @@ class HipExecutor : public Executor {
             return s;
         }
         void *ptr = nullptr;
-        return locate(id, agent, &ptr, bytes, err);
+        return locate(id, agent, &ptr, bytes, err, false);
     }
 
     rtcc_status get_tensor(int id, int agent, void *dst, size_t bytes, std::string &err) override {
@@ -500,6 +510,7 @@ class HipExecutor : public Executor {
                 if (k < p_.K) {
                     br_[k].canvas_dirty = true;
                     HIP_TRY(clear_canvases(&k, 1, s));  // untimed, as after a frame
+                    br_[k].canvas_consumed = true;
                 }
                 HIP_TRY(hipEventSynchronize(e1));
                 float ms = 0.f;
@@ -673,6 +684,9 @@ class HipExecutor : public Executor {
         bool warp_ran = false;           // the last frame ran a branch warp kernel
         bool pillars_clean = true;       // every enqueued K1 was followed by the PFN kernel
         bool canvas_dirty = false;       // the canvas holds pillars not yet cleared (canvas_clear)
+        // the last frame's pillars were cleared at the end of its join: the
+        // canvas tensor is rebuilt from the pillar lists when read
+        bool canvas_consumed = false;
         hipEvent_t wev[2] = {nullptr, nullptr};  // bracket the branch warp kernel
         Graph pillar_graph;              // its pillar stage as a HIP graph (use_graphs, released alone)
         Graph graph;                     // its backbone as a HIP graph (use_graphs, released alone)
@@ -758,16 +772,7 @@ class HipExecutor : public Executor {
         HIP_TRY(kern::pillar_lists(grp, s));
         HIP_TRY(mark(2));
 
-        kern::PfnArgs pa{};
-        pa.w = static_cast<const float *>(d_bias) + p.pfn_w_off;
-        pa.b = static_cast<const float *>(d_bias) + p.pfn_b_off;
-        pa.C = p.c_pfn;
-        pa.max_pts = p.d.max_points_per_pillar;
-        pa.inv_hx = float(2.0 / (double(p.d.x_max) - double(p.d.x_min)));
-        pa.inv_hy = float(2.0 / (double(p.d.y_max) - double(p.d.y_min)));
-        pa.z0 = p.d.z_min;
-        pa.inv_dz = float(1.0 / (double(p.d.z_max) - double(p.d.z_min)));
-        HIP_TRY(kern::pfn_canvas(p.bf16, pa, grp, grp.n_max < n_cells ? grp.n_max : n_cells, s));
+        HIP_TRY(kern::pfn_canvas(p.bf16, pfn_args(), grp, grp.n_max < n_cells ? grp.n_max : n_cells, s));
         for (int j = 0; j < m; ++j) br_[agents[j]].pillars_clean = true;
         HIP_TRY(mark(3));
         return RTCC_OK;
@@ -1078,7 +1083,56 @@ class HipExecutor : public Executor {
         return RTCC_OK;
     }
 
-    rtcc_status locate(int id, int agent, void **ptr, size_t *bytes, std::string &err) {
+    // The canvas of the agent's last frame, whose pillars were cleared after
+    // its join, rebuilt into a buffer of its own: the PFN kernel again over
+    // the last pillar lists, the points over the cap as that frame selected
+    // them (replay), into a zeroed canvas.  Bit for bit the canvas the first
+    // conv layer read.
+    rtcc_status rebuild_canvas(int agent, void **ptr, std::string &err) {
+        const Plan &p = p_;
+        const int n_cells = p.H * p.W;
+        const size_t bytes = size_t(n_cells) * p.c_pfn * p.elt;
+        HIP_TRY(hipSetDevice(dev_));
+        if (!d_canvas_view_) HIP_TRY(alloc(&d_canvas_view_, bytes));
+        // after the clear (join stream), which reads the same pillar lists
+        HIP_TRY(hipStreamSynchronize(join_stream_));
+        HIP_TRY(kern::fill_i32(static_cast<int32_t *>(d_canvas_view_), int64_t(bytes / 4), 0, aux_stream_));
+        const Branch &b = br_[agent];
+        kern::PillarGroup grp{};
+        grp.bufs = static_cast<const kern::PillarBufs *>(d_pbufs_);
+        grp.m = 1;
+        grp.agent[0] = agent;
+        grp.pts[0] = nullptr;  // not read in replay
+        grp.n[0] = b.n;
+        grp.n_max = b.n;
+        grp.n_cells = n_cells;
+        grp.tiles = tiles_;
+        kern::PfnArgs pa = pfn_args();
+        pa.replay = 1;
+        pa.canvas = d_canvas_view_;
+        HIP_TRY(kern::pfn_canvas(p.bf16, pa, grp, grp.n_max < n_cells ? grp.n_max : n_cells, aux_stream_));
+        HIP_TRY(hipStreamSynchronize(aux_stream_));
+        *ptr = d_canvas_view_;
+        return RTCC_OK;
+    }
+
+    kern::PfnArgs pfn_args() const {
+        const Plan &p = p_;
+        kern::PfnArgs pa{};
+        pa.w = static_cast<const float *>(d_bias) + p.pfn_w_off;
+        pa.b = static_cast<const float *>(d_bias) + p.pfn_b_off;
+        pa.C = p.c_pfn;
+        pa.max_pts = p.d.max_points_per_pillar;
+        pa.inv_hx = float(2.0 / (double(p.d.x_max) - double(p.d.x_min)));
+        pa.inv_hy = float(2.0 / (double(p.d.y_max) - double(p.d.y_min)));
+        pa.z0 = p.d.z_min;
+        pa.inv_dz = float(1.0 / (double(p.d.z_max) - double(p.d.z_min)));
+        return pa;
+    }
+
+    // *ptr, *bytes: where tensor id of the agent is on the device and its size
+    // (with data false only the size is needed)
+    rtcc_status locate(int id, int agent, void **ptr, size_t *bytes, std::string &err, bool data = true) {
         const Plan &p = p_;
         const bool per_agent = id == RTCC_T_PILLAR_CELLS || id == RTCC_T_PILLAR_COUNTS ||
                                id == RTCC_T_CANVAS || id == RTCC_T_SLOT || id == RTCC_T_WARPED;
@@ -1119,9 +1173,12 @@ class HipExecutor : public Executor {
                 return RTCC_OK;
             }
             case RTCC_T_CANVAS:
-                *ptr = br_[agent].d_canvas;
                 *bytes = size_t(p.H) * p.W * p.c_pfn * p.elt;
-                return RTCC_OK;
+                if (!br_[agent].canvas_consumed || !data) {
+                    *ptr = br_[agent].d_canvas;
+                    return RTCC_OK;
+                }
+                return rebuild_canvas(agent, ptr, err);
             case RTCC_T_SLOT:
                 if (p.d.multiscale) {
                     err = "multi-scale fusion: the branch ends at its stage outputs (no slot)";
@@ -1248,6 +1305,7 @@ class HipExecutor : public Executor {
     std::vector<std::array<float, 3>> last_poses_;
     std::vector<void *> d_fused_stage_;  // multi-scale: fused map of every stage
     hipStream_t cap_stream_ = nullptr;   // where graphs are captured (use_graphs)
+    void *d_canvas_view_ = nullptr;      // a rebuilt canvas (tensor reads)
     Graph post_graph_[2];                // post-join: up to T^head, then decode and NMS
     Graph group_graph_;                  // the backbones of a group of branches
     Graph group_pillar_graph_;           // the pillar stage of a group of branches

@@ -84,6 +84,12 @@ struct PfnArgs {
     int32_t max_pts;
     float inv_hx, inv_hy, z0, inv_dz;
     int32_t pillar_blocks;  // set by pfn_canvas
+    // replay = 1: the pillars over the cap already hold their selected points
+    // first (a previous launch on the same lists chose them), so they are
+    // not chosen again; the canvas cells come out bit for bit as in that
+    // launch.  canvas: where the cells go (nullptr: the agent's canvas).
+    int32_t replay;
+    void *canvas;
 };
 // max_pillars bounds every agent's meta[1] (at most min(cells, points)).
 hipError_t pfn_canvas(bool bf16, PfnArgs a, const PillarGroup &grp, int32_t max_pillars, hipStream_t s);

@@ -366,6 +366,7 @@ __global__ __launch_bounds__(256) void k_pfn_canvas(const PfnArgs a, const Pilla
     const GroupBlock gb = group_block(grp);
     const int j = gb.j;
     const PillarBufs B = group_bufs(grp, j);
+    void *const canvas = a.canvas ? a.canvas : B.canvas;
     if (gb.b >= a.pillar_blocks) {
         // pillars over the cap, one wavefront each
         const int lane = threadIdx.x & 63;
@@ -379,40 +380,42 @@ __global__ __launch_bounds__(256) void k_pfn_canvas(const PfnArgs a, const Pilla
             const int cnt = B.tcount[sidx];
             int32_t *seg = B.member + B.toff[sidx];
             float4 *sseg = B.sorted + B.toff[sidx];
-            // Smallest T with #{members < T} >= max_pts.  Members are
-            // distinct point indices in [0, n), so exactly max_pts members
-            // lie below T.
-            int lo = 1, hi = grp.n[j];
-            while (lo < hi) {
-                const int mid = lo + (hi - lo) / 2;
-                int below = 0;
-                for (int q = lane; q < cnt; q += 64) below += seg[q] < mid;
+            if (!a.replay) {
+                // Smallest T with #{members < T} >= max_pts.  Members are
+                // distinct point indices in [0, n), so exactly max_pts members
+                // lie below T.
+                int lo = 1, hi = grp.n[j];
+                while (lo < hi) {
+                    const int mid = lo + (hi - lo) / 2;
+                    int below = 0;
+                    for (int q = lane; q < cnt; q += 64) below += seg[q] < mid;
 #pragma unroll
-                for (int d = 32; d >= 1; d >>= 1) below += __shfl_xor(below, d, 64);
-                if (below >= a.max_pts) hi = mid;
-                else lo = mid + 1;
-            }
-            const int T = lo;
-            // Stable in-place compaction of the selected members to the
-            // front: a chunk is read completely before any of it is
-            // overwritten, and writes never pass the chunk being read.
-            int pos = 0;
-            for (int base = 0; base < cnt && pos < a.max_pts; base += 64) {
-                const int q = base + lane;
-                const int e = q < cnt ? seg[q] : INT_MAX;
-                const bool sel = q < cnt && e < T;
-                const unsigned long long m = __ballot(sel);
-                const int my = pos + __popcll(m & ((1ull << lane) - 1ull));
-                if (sel) {
-                    seg[my] = e;
-                    sseg[my] = pts[e];
+                    for (int d = 32; d >= 1; d >>= 1) below += __shfl_xor(below, d, 64);
+                    if (below >= a.max_pts) hi = mid;
+                    else lo = mid + 1;
                 }
-                pos += __popcll(m);
+                const int T = lo;
+                // Stable in-place compaction of the selected members to the
+                // front: a chunk is read completely before any of it is
+                // overwritten, and writes never pass the chunk being read.
+                int pos = 0;
+                for (int base = 0; base < cnt && pos < a.max_pts; base += 64) {
+                    const int q = base + lane;
+                    const int e = q < cnt ? seg[q] : INT_MAX;
+                    const bool sel = q < cnt && e < T;
+                    const unsigned long long m = __ballot(sel);
+                    const int my = pos + __popcll(m & ((1ull << lane) - 1ull));
+                    if (sel) {
+                        seg[my] = e;
+                        sseg[my] = pts[e];
+                    }
+                    pos += __popcll(m);
+                }
+                // the wave's own writes above are read back by other lanes
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+                __builtin_amdgcn_wave_barrier();
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
             }
-            // the wave's own writes above are read back by other lanes
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
             for (int ch = lane * 8; ch < a.C; ch += 64 * 8) {
                 float w0[8], w1[8], w2[8], w3[8], bb[8], mx[8];
 #pragma unroll
@@ -425,7 +428,7 @@ __global__ __launch_bounds__(256) void k_pfn_canvas(const PfnArgs a, const Pilla
                     mx[i] = 0.f;
                 }
                 for (int t = 0; t < a.max_pts; ++t) pfn_point(a, sseg[t], w0, w1, w2, w3, bb, mx);
-                store_canvas8<BF16>(a, B.canvas, c, ch, mx);
+                store_canvas8<BF16>(a, canvas, c, ch, mx);
             }
         }
         return;
@@ -468,8 +471,8 @@ __global__ __launch_bounds__(256) void k_pfn_canvas(const PfnArgs a, const Pilla
         if (n0 > 0) pfn_point(a, q0, w0, w1, w2, w3, bb, m0);
         if (n1 > 0) pfn_point(a, q1, w0, w1, w2, w3, bb, m1);
     }
-    if (n0 > 0) store_canvas8<BF16>(a, B.canvas, cell0, ch, m0);
-    if (n1 > 0) store_canvas8<BF16>(a, B.canvas, cell1, ch, m1);
+    if (n0 > 0) store_canvas8<BF16>(a, canvas, cell0, ch, m0);
+    if (n1 > 0) store_canvas8<BF16>(a, canvas, cell1, ch, m1);
 }
 
 // The canvas cells of the last frame's pillars back to zero, one lane per
