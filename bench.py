@@ -50,7 +50,7 @@ MEASURED_TRAFFIC = {
                       sha256="b870ed95289aecf1a7bc1ce8e7f7670f9b28115f3b8183885f4f303359713141"),
     # per 8-agent launch chain of the pillar stage (five kernels)
     "pillar": dict(src="paper_2608_08330_amd/csrc/kernels/pillar.hip", bytes=195e6,
-                   sha256="75547fe4e96df6793946122f770939c49c0334a4250e7b36b154152a2ca40586"),
+                   sha256="624b87e26ad92d9196d0e1e206e92b8349c8c32de965453523b85f3ee2223d4b"),
 }
 
 
