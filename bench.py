@@ -545,8 +545,9 @@ def main(argv=None):
                                       "achieved": round(pil_bytes / (single_ms * 1e-3) / 1e9, 1),
                                       "us_per_agent": round(single_ms / (K * rsteps) * 1e3, 2)},
                                   "work": "16 n + 8 P + H*W*C_pfn*elt bytes per agent (the dense canvas as "
-                                          "output; the kernels write the P pillar cells and clear the previous "
-                                          "frame's), all K agents over the span of their one launch chain"},
+                                          "output; the kernels write the P pillar cells, the previous frame's "
+                                          "were cleared after its join), all K agents over the span of their one "
+                                          "launch chain"},
         },
         "conv_layers": layers,
         "node_ms_mean": {
