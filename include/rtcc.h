@@ -444,6 +444,18 @@ RTCC_API rtcc_status rtcc_node_count(rtcc_ctx *ctx, int32_t *n);
  * range), RTCC_E_STATE (the host test library has no kernels). */
 RTCC_API rtcc_status rtcc_conv_plan(rtcc_ctx *ctx, int32_t layer, int32_t *plan);
 
+/* The tiling the library plans for a 3x3 conv layer, without a context or a
+ * device: shape = {Hi, Wi, C_in, Ho, Wo, C_out, stride, n_cu} (int32_t[8],
+ * n_cu = the GPU's compute units; a context plans with its device's count),
+ * bf16 != 0 for bf16 operands (else fp32), maps = the agents' maps one
+ * launch covers (1: one agent; a group release launches every layer over
+ * its members).  out[0] = tiling id as in rtcc_conv_plan (a launch over
+ * several maps may take a wider tiling of the same accumulation order),
+ * out[1] = K slices.  out: caller-owned int32_t[2].  Errors: RTCC_E_ARG
+ * (NULL pointer, a size or n_cu below 1, stride not 1 or 2, maps outside
+ * [1, 16]). */
+RTCC_API rtcc_status rtcc_conv_tiling(int32_t bf16, const int32_t *shape, int32_t maps, int32_t *out);
+
 /* With opts.use_graphs = 1: counts[0] = HIP graphs instantiated, counts[1] =
  * in-place updates attempted (a branch or the join whose arguments changed
  * since its graph was captured is captured again and the executable graph

@@ -25,7 +25,7 @@ ARCH = "gfx950"
 HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
 CXX = shutil.which("g++") or "g++"
 
-HOST_SOURCES = ["api.cpp", "checkpoint.cpp", "controller.cpp", "model.cpp", "uplink.cpp"]
+HOST_SOURCES = ["api.cpp", "checkpoint.cpp", "controller.cpp", "model.cpp", "uplink.cpp", "kernels/conv_plan.cpp"]
 HIP_SOURCES = [
     "executor_hip.hip",
     "kernels/pillar.hip",

@@ -1,5 +1,5 @@
 // extern "C" entry points of include/rtcc.h.  Argument marshalling onto the
-// controller; no computation happens here.
+// controller (and, for rtcc_conv_tiling, the conv planner).
 #include <cstring>
 #include <new>
 #include <string>
@@ -7,6 +7,7 @@
 
 #include "checkpoint.hpp"
 #include "controller.hpp"
+#include "kernels/conv_plan.hpp"
 
 struct rtcc_ctx {
     rtcc::Controller ctl;
@@ -195,6 +196,18 @@ rtcc_status rtcc_node_count(rtcc_ctx *ctx, int32_t *n) {
 rtcc_status rtcc_conv_plan(rtcc_ctx *ctx, int32_t layer, int32_t *plan) {
     if (!ctx) return RTCC_E_ARG;
     return guarded([&] { return ctx->ctl.conv_plan(layer, plan); });
+}
+
+rtcc_status rtcc_conv_tiling(int32_t bf16, const int32_t *shape, int32_t maps, int32_t *out) {
+    if (!shape || !out || maps < 1 || maps > 16) return RTCC_E_ARG;
+    for (int i = 0; i < 8; ++i)
+        if (i != 6 && shape[i] < 1) return RTCC_E_ARG;
+    if (shape[6] != 1 && shape[6] != 2) return RTCC_E_ARG;
+    const rtcc::kern::ConvPlan p = rtcc::kern::conv_plan(bf16 != 0, shape[0], shape[1], shape[2], shape[3], shape[4],
+                                                         shape[5], shape[6], shape[7]);
+    out[0] = rtcc::kern::conv_variant_for(p, maps);
+    out[1] = p.splits;
+    return RTCC_OK;
 }
 
 rtcc_status rtcc_graph_stats(rtcc_ctx *ctx, int64_t *counts) {

@@ -173,7 +173,7 @@ EXPORTS = (
     "rtcc_create", "rtcc_read_checkpoint", "rtcc_create_from_checkpoint", "rtcc_destroy", "rtcc_set_mode", "rtcc_staging_buffer", "rtcc_begin_frame",
     "rtcc_release_branch", "rtcc_release_branch_device", "rtcc_release_branches", "rtcc_join_and_detect",
     "rtcc_get_branch_state", "rtcc_tensor_bytes", "rtcc_get_tensor", "rtcc_profile_nodes",
-    "rtcc_node_times", "rtcc_node_count", "rtcc_graph_stats", "rtcc_conv_plan", "rtcc_rotated_nms", "rtcc_rotated_nms_noalloc", "rtcc_uplink_emulate", "rtcc_schedule_model",
+    "rtcc_node_times", "rtcc_node_count", "rtcc_graph_stats", "rtcc_conv_plan", "rtcc_conv_tiling", "rtcc_rotated_nms", "rtcc_rotated_nms_noalloc", "rtcc_uplink_emulate", "rtcc_schedule_model",
     "rtcc_upward_rank", "rtcc_status_str", "rtcc_last_error",
 )
 
@@ -213,6 +213,8 @@ def _declare(lib):
         "rtcc_node_count": (S, [_P, ctypes.POINTER(ctypes.c_int32)]),
         "rtcc_graph_stats": (S, [_P, ctypes.POINTER(ctypes.c_int64)]),
         "rtcc_conv_plan": (S, [_P, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32)]),
+        "rtcc_conv_tiling": (S, [ctypes.c_int32, ctypes.POINTER(ctypes.c_int32), ctypes.c_int32,
+                                 ctypes.POINTER(ctypes.c_int32)]),
         "rtcc_rotated_nms": (S, [_P, ctypes.c_int64, ctypes.c_int32, ctypes.c_float, _P,
                                  ctypes.POINTER(ctypes.c_int64)]),
         "rtcc_rotated_nms_noalloc": (S, [_P, ctypes.c_int64, ctypes.c_int32, ctypes.c_float, _P,
@@ -614,6 +616,19 @@ def rtcc_conv_plan(ctx, layer):
     """(tiling, K slices) of 3x3 conv layer ``layer``."""
     out = (ctypes.c_int32 * 2)()
     ctx.check(ctx.lib.rtcc_conv_plan(ctx.handle, int(layer), out))
+    return int(out[0]), int(out[1])
+
+
+def rtcc_conv_tiling(Hi, Wi, Ci, Ho, Wo, Co, stride, n_cu, maps=1, bf16=True, lib=None):
+    """(tiling, K slices) the library plans for a 3x3 conv layer of this shape
+    on a GPU with n_cu compute units, in a launch over `maps` maps (host
+    computation; `lib`: a loaded library, default the GPU library)."""
+    lib = lib if lib is not None else load()
+    shape = (ctypes.c_int32 * 8)(Hi, Wi, Ci, Ho, Wo, Co, stride, n_cu)
+    out = (ctypes.c_int32 * 2)()
+    st = lib.rtcc_conv_tiling(1 if bf16 else 0, shape, int(maps), out)
+    if st != RTCC_OK:
+        raise RtccError(st, "rtcc_conv_tiling")
     return int(out[0]), int(out[1])
 
 
