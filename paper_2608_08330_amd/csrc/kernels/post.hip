@@ -173,10 +173,32 @@ __device__ inline void warp_sample(const T *slot, const float *m, int H2, int W2
     }
 }
 
+// Sum over the 32 lanes of a half wavefront, bitwise the same in every lane:
+// within each 16-lane row, DPP quad permutes (lane ^ 1, lane ^ 2) and the
+// row's half mirror and mirror (every lane of an 8- or 16-lane group meets a
+// lane of the other half, which holds the other half's sum), then a swizzle
+// that swaps the two rows (lane ^ 16).  Each step adds a pair of partial
+// sums that are the same in both lanes, so the tree, and the rounding, is
+// the same everywhere.  DPP moves are register-to-register; only the last
+// step goes through the LDS crossbar.
+template <int CTRL>
+__device__ inline float dpp_move(float x) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xf, 0xf, false));
+}
+__device__ inline float half_wave_sum(float d) {
+    d += dpp_move<0xb1>(d);   // quad_perm [1, 0, 3, 2]
+    d += dpp_move<0x4e>(d);   // quad_perm [2, 3, 0, 1]
+    d += dpp_move<0x141>(d);  // row_half_mirror
+    d += dpp_move<0x140>(d);  // row_mirror
+    // bit-mask swizzle within 32 lanes: and 0x1f, or 0, xor 0x10
+    d += __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, d), 0x401f));
+    return d;
+}
+
 // Cross-agent fusion of one cell's VEC-channel slice, agents folded in index
 // order: a running channel max, or an online softmax whose scores
-// <X_0, X_k> / sqrt(C) are reduced over the 32 lanes of the cell with
-// butterfly shuffles (fixed order, so deterministic).
+// <X_0, X_k> / sqrt(C) are reduced over the 32 lanes of the cell
+// (half_wave_sum: a fixed tree, so deterministic).
 template <int VEC, bool ATTN>
 struct Fold {
     float q[VEC], acc[VEC];
@@ -197,8 +219,7 @@ struct Fold {
             float d = 0.f;
 #pragma unroll
             for (int e = 0; e < VEC; ++e) d += q[e] * x[e];
-#pragma unroll
-            for (int off = 16; off >= 1; off >>= 1) d += __shfl_xor(d, off, 32);
+            d = half_wave_sum(d);
             const float sc = d * inv_sqrt_c;
             const float nm = fmaxf(run_max, sc);
             const float scale = expf(run_max - nm);
