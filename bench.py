@@ -44,8 +44,8 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 # kernel source it was taken on; after a change it reads null until re-taken.
 MEASURED_TRAFFIC = {
     # per 8-agent launch of a conv layer (averaged over the 13 layers)
-    "conv": dict(src="paper_2608_08330_amd/csrc/kernels/igemm.hip", bytes=165.8e6,
-                 sha256="962ca22cab5141bebfb8759635903aa8283f1bda78733d3812b7fc0edfcc9d4e"),
+    "conv": dict(src="paper_2608_08330_amd/csrc/kernels/igemm.hip", bytes=154.8e6,
+                 sha256="1ea11a11e3bed1bdddb119fe33f47298bae88df767b509db8774190339f217c4"),
     "warp_fuse": dict(src="paper_2608_08330_amd/csrc/kernels/post.hip", bytes=470.7e6,
                       sha256="562dd140afe28bc3966284f101d72795578cd0121b43b5c34804a2cd10cba84f"),
     # per 8-agent launch chain of the pillar stage (five kernels)

@@ -187,7 +187,8 @@ typedef struct rtcc_runtime_opts {
      * 10: 9 with 64-byte chunks, 11: the stride-2 8 x 16 x 256) on every
      * layer whose stride and channels it supports, the plan elsewhere; 7 =
      * the implicit GEMM on every layer, 12 = the implicit GEMM with 256 x
-     * 128 tiles on every layer with 128k output channels.  conv_splits (0
+     * 128 tiles (every other tile summing its K steps in reverse order) on
+     * every layer with 128k output channels.  conv_splits (0
      * or 1: none) splits the K loop of the forced layers where it divides
      * evenly.  Values outside [0, 12]: RTCC_E_ARG. */
     int32_t conv_variant;

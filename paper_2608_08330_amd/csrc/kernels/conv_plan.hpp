@@ -33,7 +33,9 @@ constexpr int kConvHalo16C64 = 10;
 // all 256 output channels instead of once per 128.
 constexpr int kConvHalo8S2N256 = 11;
 // The implicit GEMM with tiles of 256 pixels x 128 channels and a 3-stage
-// ring (72 KB of LDS, two blocks per CU).
+// ring (72 KB of LDS, two blocks per CU).  Odd M tiles run their K steps in
+// reverse, another accumulation order than kConvImplicit: a layer's plan
+// takes one of the two for every batch size.
 constexpr int kConvImplicit256 = 12;
 struct ConvPlan {
     int variant;      // tiling of a launch over one map

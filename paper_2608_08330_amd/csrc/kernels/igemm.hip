@@ -290,8 +290,13 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_igemm(GemmArgs a0) {
         }
     }
 
+    // 256-pixel conv tiles (one output row of a stride-2 layer each): every
+    // other tile runs its K steps backwards, so that the input row two
+    // neighbouring tiles share (the last tap row of one, the first of the
+    // other) is read by both in the same steps, while it is in the L2
+    const bool rev = !DECONV && BM == 256 && (m_tile & 1);
     auto issue = [&](int kt, int buf) {
-        const int k0 = (kt0 + kt) * BK;
+        const int k0 = (kt0 + (rev ? KT - 1 - kt : kt)) * BK;
         int tap = 0, c0 = k0;
         if (!DECONV) {
             tap = k0 / Ci;

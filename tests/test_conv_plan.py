@@ -11,7 +11,8 @@ import pytest
 import synth
 from paper_2608_08330_amd import rtcc as R
 
-IMPLICIT = (0, 12)      # implicit GEMM, 128 x 128 or 256 x 128 tiles
+IMPLICIT = (0,)         # implicit GEMM, 128 x 128 tiles
+IMPLICIT256 = (12,)     # 256 x 128 tiles, every other tile's K steps backwards
 HALO_RULE = (1, 2, 9)   # halo tilings whose chunk width follows the channel rule
 HALO_C64 = (8, 10)      # halo tilings with 64-byte chunks
 HALO_S2 = (3, 4, 11)    # stride-2 halo tilings (64-byte chunks)
@@ -40,6 +41,8 @@ def _layers(name):
 def _family(variant, ci, elt):
     if variant in IMPLICIT:
         return "implicit"
+    if variant in IMPLICIT256:
+        return "implicit256"
     if variant in HALO_RULE:
         return ("halo", 128 if (ci * elt) % 128 == 0 and ci * elt >= 512 else 64)
     if variant in HALO_C64 or variant in HALO_S2:
@@ -75,7 +78,7 @@ def test_every_batch_size_accumulates_alike(name, n_cu):
             assert v not in TWO_GROUPS
             if shape[6] == 1:
                 assert v not in HALO_S2
-            elif v not in IMPLICIT:
+            elif v not in IMPLICIT + IMPLICIT256:
                 assert v in HALO_S2
 
 
