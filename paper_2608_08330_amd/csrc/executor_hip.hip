@@ -180,10 +180,11 @@ class HipExecutor : public Executor {
         HIP_TRY(hipHostMalloc(reinterpret_cast<void **>(&h_rec), n_anchor_ * 9 * 4, hipHostMallocDefault));
         HIP_TRY(hipHostMalloc(reinterpret_cast<void **>(&h_small), 64, hipHostMallocDefault));
         // the frame's counts and first records, written by the last kernel
-        // of the post-join work (coherent: read by the host once the join
-        // stream has passed that kernel)
+        // of the post-join work (coherent: read by the host once that kernel
+        // has set its flag, word 2)
         export_first_ = int(std::min(nms_max_ > 0 ? size_t(nms_max_) : n_anchor_, kFirstRecords));
         HIP_TRY(hipHostMalloc(&h_export, 64 + size_t(export_first_) * 36, hipHostMallocCoherent));
+        std::memset(h_export, 0, 64);
         boxes_.resize(n_anchor_ * 7);
         scores_.resize(n_anchor_);
         aidx_.resize(n_anchor_);
@@ -382,6 +383,10 @@ class HipExecutor : public Executor {
         // one-kernel fusion nodes are timed by events bracketing the kernel
         if (timing && p_.d.multiscale) HIP_TRY(hipEventRecord(post_ev_[0], js));
         rtcc_status s;
+        // the export kernel at the end of the post-join work sets this flag;
+        // every export enqueued before has completed (joins wait for theirs,
+        // node profiling synchronises)
+        __atomic_store_n(static_cast<uint32_t *>(h_export) + 2, 0u, __ATOMIC_RELAXED);
         if (o_.use_graphs && !timing) {
             std::vector<unsigned char> key;
             for (int k = 0; k < p_.K; ++k) {
@@ -400,10 +405,16 @@ class HipExecutor : public Executor {
             s = enqueue_post(affine, poses, js, timing, err);
         }
         if (s != RTCC_OK) return s;
-        // the counts and the first records are in h_export once the stream
-        // has passed the post-join work (no copy call in the common case);
-        // the rest, if any, are copied after them
-        HIP_TRY(spin_sync(js));
+        // The GPU is idle until the caller's next frame: its canvas pillars go
+        // back to zero now, behind the export on the join stream, not at the
+        // next frame's start (the canvas tensor is rebuilt when read).
+        HIP_TRY(clear_dirty_canvases(true));
+        // the counts and the first records are in h_export once the export
+        // kernel has set the flag (no copy call in the common case; the clear
+        // behind it is not waited for); the rest, if any, are copied after
+        // them
+        s = wait_export(js, err);
+        if (s != RTCC_OK) return s;
         const int32_t *hs = static_cast<const int32_t *>(h_export);
         const int64_t decoded = hs[0];
         const int64_t count = nms_max_ > 0 ? hs[1] : decoded;
@@ -420,17 +431,13 @@ class HipExecutor : public Executor {
                                    (size_t(count) - first) * 36, hipMemcpyDeviceToHost, js));
             HIP_TRY(spin_sync(js));
         }
-        idle_ = true;  // every stream's work of the frame has completed
+        idle_ = true;  // the frame's work has completed (the canvas clear may still run)
         for (int64_t i = 0; i < count; ++i) {
             const float *r = size_t(i) < first ? head_recs + i * 9 : h_rec + i * 9;
             std::memcpy(&boxes_[i * 7], r, 7 * sizeof(float));
             scores_[i] = r[7];
             std::memcpy(&aidx_[i], &r[8], 4);
         }
-        // The GPU is idle until the caller's next frame: its canvas pillars go
-        // back to zero now, not at the next frame's start (the canvas tensor
-        // is rebuilt when read).
-        HIP_TRY(clear_dirty_canvases(true));
         float ms = 0.f;
         HIP_TRY(hipEventElapsedTime(&ms, ev_frame0_, ev_head_));
         out->count = count;
@@ -704,6 +711,23 @@ class HipExecutor : public Executor {
     };
 
     hipStream_t compute_stream_for_join() const { return join_stream_; }
+
+    // Until the export kernel of this join has set word 2 of h_export to 1
+    // (acquire).  A stream error ends the wait with that error; a stream
+    // that completes without the store (no export kernel ran) is an
+    // internal error.
+    rtcc_status wait_export(hipStream_t s, std::string &err) {
+        const uint32_t *w = static_cast<const uint32_t *>(h_export) + 2;
+        for (;;) {
+            if (__atomic_load_n(w, __ATOMIC_ACQUIRE) == 1u) return RTCC_OK;
+            const hipError_t e = hipStreamQuery(s);
+            if (e == hipErrorNotReady) continue;
+            HIP_TRY(e);
+            if (__atomic_load_n(w, __ATOMIC_ACQUIRE) == 1u) return RTCC_OK;
+            err = "the join stream completed without exporting the frame";
+            return RTCC_E_INTERNAL;
+        }
+    }
 
     // Wait for a stream by polling: T^det is a latency measurement, and a
     // blocking wait adds the host's wake-up time to it.

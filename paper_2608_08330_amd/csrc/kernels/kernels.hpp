@@ -199,8 +199,10 @@ hipError_t decode(const DecodeArgs &a, hipStream_t s);
 // The frame's result into pinned host memory: words 0 and 1 of `host` the
 // counts *count0 and *count1 (0 without count1), and from byte 64 the first
 // min(*count1 or *count0, first) 36-byte records of `recs`; written with
-// vector stores and fenced at system scope, so the host reads them once
-// the stream has passed the kernel.
+// vector stores and fenced at system scope; then 1 is stored to word 2 with
+// release semantics at system scope, so a host that cleared word 2 before
+// enqueuing the kernel and then reads 1 there (acquire) also sees the counts
+// and records, without waiting for the stream.
 hipError_t export_results(const int32_t *count0, const int32_t *count1, const float *recs, int first, void *host,
                           hipStream_t s);
 

@@ -530,6 +530,8 @@ __global__ __launch_bounds__(256) void k_export(const int32_t *count0, const int
         host[1] = uint32_t(c1);
     }
     __threadfence_system();
+    __syncthreads();  // every thread's stores are fenced before the flag
+    if (threadIdx.x == 0) __hip_atomic_store(&host[2], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
 hipError_t export_results(const int32_t *count0, const int32_t *count1, const float *recs, int first, void *host,
