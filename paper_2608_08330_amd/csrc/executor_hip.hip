@@ -238,17 +238,20 @@ class HipExecutor : public Executor {
     // the next frame then waits for (from its pillar stage's second launch
     // on).  after_join: the branches' canvases stay readable as tensors
     // (rebuilt from their pillar lists).
-    hipError_t clear_dirty_canvases(bool after_join) {
+    // s: the stream of the join's post-join work (default: the join stream).
+    hipError_t clear_dirty_canvases(bool after_join, hipStream_t s = nullptr) {
+        if (!s) s = join_stream_;
         int dirty[kern::kMaxGroup];
         int nd = 0;
         for (int k = 0; k < p_.K; ++k)
             if (br_[k].canvas_dirty) dirty[nd++] = k;
         if (nd == 0) return hipSuccess;
-        hipError_t e = clear_canvases(dirty, nd, join_stream_);
+        hipError_t e = clear_canvases(dirty, nd, s);
         if (e != hipSuccess) return e;
+        clear_stream_ = s;
         for (int j = 0; j < nd; ++j) br_[dirty[j]].canvas_consumed = after_join;
         if (o_.exec != RTCC_EXEC_SERIAL) {
-            e = hipEventRecord(ev_clear_, join_stream_);
+            e = hipEventRecord(ev_clear_, s);
             if (e == hipSuccess) clear_pending_ = true;
         }
         return e;
@@ -375,11 +378,19 @@ class HipExecutor : public Executor {
                      std::string &err) override {
         HIP_TRY(hipSetDevice(dev_));
         hipStream_t js = compute_stream_for_join();
+        const bool timing = o_.node_timing != 0;
+        // A frame whose K encoders ran as one group launch: the post-join work
+        // follows that launch on its stream (stream order instead of a wait
+        // on its completion event from another queue).  Not with the
+        // caller's join stream, node timing or the serial executor.
+        const int src0 = br_[0].ev_src;
+        bool one_launch = own_join_stream_ && !timing && o_.exec != RTCC_EXEC_SERIAL;
+        for (int k = 0; k < p_.K && one_launch; ++k) one_launch = br_[k].ev_src == src0;
+        if (one_launch) js = br_[src0].stream;
         // every distinct completion event (a group has one)
-        for (int k = 0; k < p_.K; ++k)
+        for (int k = 0; k < p_.K && !one_launch; ++k)
             if (br_[k].ev_src == k || br_[br_[k].ev_src].ev_src != br_[k].ev_src)
                 HIP_TRY(hipStreamWaitEvent(js, br_[br_[k].ev_src].done, 0));
-        const bool timing = o_.node_timing != 0;
         // one-kernel fusion nodes are timed by events bracketing the kernel
         if (timing && p_.d.multiscale) HIP_TRY(hipEventRecord(post_ev_[0], js));
         rtcc_status s;
@@ -408,7 +419,7 @@ class HipExecutor : public Executor {
         // The GPU is idle until the caller's next frame: its canvas pillars go
         // back to zero now, behind the export on the join stream, not at the
         // next frame's start (the canvas tensor is rebuilt when read).
-        HIP_TRY(clear_dirty_canvases(true));
+        HIP_TRY(clear_dirty_canvases(true, js));
         // the counts and the first records are in h_export once the export
         // kernel has set the flag (no copy call in the common case; the clear
         // behind it is not waited for); the rest, if any, are copied after
@@ -1118,8 +1129,8 @@ class HipExecutor : public Executor {
         const size_t bytes = size_t(n_cells) * p.c_pfn * p.elt;
         HIP_TRY(hipSetDevice(dev_));
         if (!d_canvas_view_) HIP_TRY(alloc(&d_canvas_view_, bytes));
-        // after the clear (join stream), which reads the same pillar lists
-        HIP_TRY(hipStreamSynchronize(join_stream_));
+        // after the clear, which reads the same pillar lists
+        HIP_TRY(hipStreamSynchronize(clear_stream_ ? clear_stream_ : join_stream_));
         HIP_TRY(kern::fill_i32(static_cast<int32_t *>(d_canvas_view_), int64_t(bytes / 4), 0, aux_stream_));
         const Branch &b = br_[agent];
         kern::PillarGroup grp{};
@@ -1323,6 +1334,7 @@ class HipExecutor : public Executor {
     std::vector<int32_t> aidx_;
     hipStream_t join_stream_ = nullptr, copy_stream_ = nullptr, aux_stream_ = nullptr;
     bool own_join_stream_ = true;  // false: the caller's stream (opts.join_stream)
+    hipStream_t clear_stream_ = nullptr;  // the stream of the last canvas clear
     hipEvent_t ev_frame0_ = nullptr, ev_head_ = nullptr;
     hipEvent_t post_ev_[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
     std::vector<std::array<float, 6>> last_affine_;
