@@ -302,7 +302,8 @@ class HipExecutor : public Executor {
             HIP_TRY(prepare_branch(b, ls));
         }
         // ... and (from its second launch on) after the frame's canvas clear
-        hipEvent_t clear_ev = clear_pending_ ? ev_clear_ : nullptr;
+        // (in stream order when the clear was enqueued on this stream)
+        hipEvent_t clear_ev = clear_pending_ && clear_stream_ != ls ? ev_clear_ : nullptr;
         idle_ = false;
         // The group's launches serve every member: the first member's events
         // time them, mark their start and their end for all.
