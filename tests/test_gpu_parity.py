@@ -266,3 +266,27 @@ def test_frame_after_an_infeasible_frame_matches_oracle():
         _check_frame(cfg, fr_n, ref_n, tensors(ctx, cfg), with_stages=False)
         for k in range(cfg["K"]):
             check_members(ctx, cfg, fr_n["points"][k], k)
+
+
+@pytest.mark.parametrize("graphs", [0, 1])
+def test_join_reads_back_more_records_than_the_first_block(graphs):
+    """With NMS off and a threshold below every logit, the join returns every
+    anchor of c1 (8,192, more than the 1,024 records the last kernel of the
+    join writes to host memory; the rest come by copy).  Three frames in a
+    row (the join clears the export flag and waits for it again each time),
+    each bit for bit the GPU's own decoded records, which match the oracle's
+    decode of the GPU's head output."""
+    _say("join read-back beyond the first records, graphs %d" % graphs)
+    cfg = synth.config("c1")
+    cfg["nms_max_candidates"] = 0
+    cfg["logit_threshold"] = -1e30
+    fr, _ref = _oracle("c1")
+    with make_ctx(cfg, fr, use_graphs=graphs) as ctx:
+        for _ in range(3):
+            det = run_frame(ctx, fr)
+            n = check_decode_exact(ctx, cfg)
+            dec = R.decoded_records(ctx)
+            assert det["count"] == det["count_decoded"] == n > 1024
+            assert np.array_equal(det["anchor_idx"], dec["anchor_idx"])
+            assert np.array_equal(det["boxes"].view(np.uint32), dec["boxes"].view(np.uint32))
+            assert np.array_equal(det["scores"].view(np.uint32), dec["scores"].view(np.uint32))
