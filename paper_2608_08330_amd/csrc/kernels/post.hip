@@ -524,7 +524,12 @@ __global__ __launch_bounds__(256) void k_export(const int32_t *count0, const int
     const int32_t c0 = *count0, c1 = count1 ? *count1 : 0;
     const int32_t n = count1 ? c1 : c0;
     const int words = (n < 0 ? 0 : n < first ? n : first) * 9;
-    for (int i = int(threadIdx.x); i < words; i += 256) host[16 + i] = recs[i];
+    // 16-byte stores across the bus (host + 64 and recs are 16-byte aligned),
+    // then the last words
+    const int quads = words >> 2;
+    for (int i = int(threadIdx.x); i < quads; i += 256)
+        reinterpret_cast<uint4 *>(host + 16)[i] = reinterpret_cast<const uint4 *>(recs)[i];
+    for (int i = 4 * quads + int(threadIdx.x); i < words; i += 256) host[16 + i] = recs[i];
     if (threadIdx.x == 0) {
         host[0] = uint32_t(c0);
         host[1] = uint32_t(c1);
