@@ -222,8 +222,8 @@ struct Fold {
             d = half_wave_sum(d);
             const float sc = d * inv_sqrt_c;
             const float nm = fmaxf(run_max, sc);
-            const float scale = expf(run_max - nm);
-            const float p = expf(sc - nm);
+            const float scale = __expf(run_max - nm);
+            const float p = __expf(sc - nm);
             run_sum = run_sum * scale + p;
 #pragma unroll
             for (int e = 0; e < VEC; ++e) acc[e] = acc[e] * scale + p * x[e];
